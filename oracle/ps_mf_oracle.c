@@ -1,0 +1,417 @@
+/*
+ * ORACLE — test infrastructure only.  A plain, slow, single-threaded CPU implementation
+ * of the clocked SSP/ESSP matrix-factorization SGD that the HIP library computes.  Only
+ * the tests, the package smoke check and the benchmark's CPU-baseline leg may load it;
+ * the product path never does.  It shares no code with the HIP library.
+ *
+ * What it computes (Dai et al., arXiv 1410.8043):
+ *   - objective: sum over observed (i,j) of (D_ij - L_i . R_j)^2 + lambda(|L|_F^2 + |R|_F^2)
+ *     (Section 3.1); the factor 2 of the gradient is absorbed into the step (Section 3.1);
+ *   - per-rating update (Section 3.1):  e_ij = D_ij - L_i . R_j,
+ *       L_i += eta (e_ij R_j - lambda L_i),   R_j += eta (e_ij L_i - lambda R_j);
+ *   - P workers own disjoint rating shards (Section 3.1: data partitioned over workers);
+ *     a clock is one minibatch of each worker's shard (Section 5, Clock() per minibatch);
+ *   - SSP bounded staleness (Section 3.2, formal SSP condition): the view of worker p at
+ *     clock c contains every update of clocks <= c-s-1 plus any subset of the window;
+ *     ESSP (Section 2.2, Section 4) is an implementation that pushes fresh rows eagerly;
+ *   - the reference sequence x_{c+1} = x_c + sum_p u_{p,c} (Section 3.2, the "true"
+ *     sequence); updates are coalesced and applied at the clock boundary (Section 4).
+ *
+ * Readings of points the paper leaves open (each is listed in the design notes):
+ *   - one fixed view per (worker, clock); a worker's contributions within a clock are
+ *     summed (no read-my-writes inside a clock);
+ *   - the view is a whole committed version v = max(0, c - d(p,c)), d chosen by a
+ *     deterministic policy: SSP_LAZY d = (c + p mod (s+1)) mod (s+1); SSP_WORST d = s;
+ *     ESSP d = min(s, 1);
+ *   - step normalisation: SUM uses the summed per-rating steps; ROWMEAN divides each
+ *     row's summed contribution by that row's rating count in the clock's minibatch;
+ *   - the lambda term enters once per rating, at the view (Section 3.1 update rule);
+ *   - minibatch block of a rating: splitmix64(seed ^ (i<<32 | j)) mod B, block c mod B
+ *     at clock c; rows with no rating in the block are left unchanged;
+ *   - ratings are visited in canonical (i, j, load index) order inside a block, so the
+ *     result does not depend on which worker owns which shard;
+ *   - versions are stored in fp32; all arithmetic is fp64; a new version is rounded once:
+ *     V_{c+1} = fp32(fp64(V_c) + Delta);
+ *   - loss (Section 5: squared loss, not the penalised objective) is
+ *     sum over all ratings (D_ij - L_i . R_j)^2 at the latest version, in fp64.
+ *
+ * Build: gcc -O2 -fPIC -shared -std=c11 ps_mf_oracle.c -o libps_mf_oracle.so
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define OR_OK 0
+#define OR_EINVAL -1
+#define OR_ENOMEM -2
+#define OR_ESTATE -4
+
+enum { OR_LAZY = 0, OR_WORST = 1, OR_ESSP = 2 };
+enum { OR_ROWMEAN = 0, OR_SUM = 1 };
+enum { OR_X_OWNER = 0, OR_X_ROW_PTR = 1, OR_X_COL = 2, OR_X_PERM = 3, OR_X_USER_COUNT = 4, OR_X_ITEM_COUNT = 5,
+       OR_X_VERSION_LOG = 6 };
+
+typedef struct {
+  int64_t N, M;
+  int32_t K, P, s, policy, step, B;
+  double eta, lambda;
+  uint64_t seed;
+  int32_t *owner; /* N */
+  /* ratings as loaded */
+  int64_t nnz;
+  int32_t *user, *item;
+  float *val;
+  /* canonical layout: ratings of block b are order[bstart[b] .. bstart[b+1]) */
+  int64_t *bstart;  /* B+1 */
+  int64_t *order;   /* nnz: load indices */
+  int32_t *ucount;  /* B*N */
+  int32_t *icount;  /* B*M */
+  int loaded, has_factors;
+  /* ring of s+1 committed versions; version v lives in slot v mod (s+1) */
+  float *Lring, *Rring;
+  int64_t clock;
+  /* version log, clock-major: entry c*P + p = v(p,c) */
+  int64_t *vlog;
+  int64_t vlog_len, vlog_cap;
+  double *dL, *dR;
+} oracle_t;
+
+/* SplitMix64 (Steele, Lea & Flood 2014): one step of the sequential generator from `state`. */
+static uint64_t splitmix64_next(uint64_t state) {
+  uint64_t z = state + 0x9E3779B97F4A7C15ULL;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+int oracle_splitmix64(uint64_t state, uint64_t *out) {
+  *out = splitmix64_next(state);
+  return OR_OK;
+}
+
+/* minibatch block of rating (i, j) */
+static int32_t block_of(const oracle_t *o, int64_t i, int64_t j) {
+  if (o->B == 1) return 0;
+  uint64_t key = o->seed ^ (((uint64_t)i << 32) | (uint64_t)(uint32_t)j);
+  return (int32_t)(splitmix64_next(key) % (uint64_t)o->B);
+}
+
+/* staleness d(p, c) chosen by the policy; always in [0, s] */
+static int64_t delay_of(const oracle_t *o, int64_t p, int64_t c) {
+  int64_t s = o->s;
+  switch (o->policy) {
+    case OR_LAZY: return (c + p % (s + 1)) % (s + 1);
+    case OR_WORST: return s;
+    default: return s < 1 ? s : 1; /* ESSP */
+  }
+}
+
+/* the committed version worker p reads at clock c */
+static int64_t view_version(const oracle_t *o, int64_t p, int64_t c) {
+  int64_t v = c - delay_of(o, p, c);
+  return v < 0 ? 0 : v;
+}
+
+int oracle_view_version(const oracle_t *o, int64_t p, int64_t c, int64_t *v) {
+  if (!o || p < 0 || p >= o->P || c < 0) return OR_EINVAL;
+  *v = view_version(o, p, c);
+  return OR_OK;
+}
+
+void oracle_destroy(oracle_t *o) {
+  if (!o) return;
+  free(o->owner); free(o->user); free(o->item); free(o->val);
+  free(o->bstart); free(o->order); free(o->ucount); free(o->icount);
+  free(o->Lring); free(o->Rring); free(o->vlog); free(o->dL); free(o->dR);
+  free(o);
+}
+
+int oracle_create(int64_t N, int64_t M, int32_t K, int32_t P, int32_t s, double eta, double lambda, int32_t policy,
+                  int32_t step, int32_t B, uint64_t seed, const int32_t *owner, oracle_t **out) {
+  if (!out) return OR_EINVAL;
+  *out = NULL;
+  if (N <= 0 || M <= 0 || K <= 0 || P <= 0 || s < 0 || B < 1 || N > 0x7fffffff || M > 0x7fffffff) return OR_EINVAL;
+  if (policy < OR_LAZY || policy > OR_ESSP || (step != OR_ROWMEAN && step != OR_SUM)) return OR_EINVAL;
+  if (!isfinite(eta) || !isfinite(lambda)) return OR_EINVAL;
+  oracle_t *o = (oracle_t *)calloc(1, sizeof(oracle_t));
+  if (!o) return OR_ENOMEM;
+  o->N = N; o->M = M; o->K = K; o->P = P; o->s = s; o->eta = eta; o->lambda = lambda;
+  o->policy = policy; o->step = step; o->B = B; o->seed = seed;
+  o->owner = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
+  if (!o->owner) { oracle_destroy(o); return OR_ENOMEM; }
+  for (int64_t i = 0; i < N; ++i) {
+    int32_t p = owner ? owner[i] : (int32_t)(i % P);
+    if (p < 0 || p >= P) { oracle_destroy(o); return OR_EINVAL; }
+    o->owner[i] = p;
+  }
+  *out = o;
+  return OR_OK;
+}
+
+/* canonical order inside a block: (user, item, load index) */
+static const oracle_t *g_sort_ctx;
+static int cmp_canonical(const void *a, const void *b) {
+  int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+  const oracle_t *o = g_sort_ctx;
+  if (o->user[x] != o->user[y]) return o->user[x] < o->user[y] ? -1 : 1;
+  if (o->item[x] != o->item[y]) return o->item[x] < o->item[y] ? -1 : 1;
+  return x < y ? -1 : (x > y);
+}
+
+int oracle_load(oracle_t *o, const int32_t *user, const int32_t *item, const float *val, int64_t nnz) {
+  if (!o || nnz < 0 || (nnz > 0 && (!user || !item || !val))) return OR_EINVAL;
+  if (o->loaded) return OR_ESTATE;
+  for (int64_t t = 0; t < nnz; ++t)
+    if (user[t] < 0 || user[t] >= o->N || item[t] < 0 || item[t] >= o->M || !isfinite(val[t])) return OR_EINVAL;
+  size_t n = (size_t)(nnz > 0 ? nnz : 1);
+  o->user = (int32_t *)malloc(sizeof(int32_t) * n);
+  o->item = (int32_t *)malloc(sizeof(int32_t) * n);
+  o->val = (float *)malloc(sizeof(float) * n);
+  o->order = (int64_t *)malloc(sizeof(int64_t) * n);
+  o->bstart = (int64_t *)calloc((size_t)o->B + 1, sizeof(int64_t));
+  o->ucount = (int32_t *)calloc((size_t)(o->B * o->N), sizeof(int32_t));
+  o->icount = (int32_t *)calloc((size_t)(o->B * o->M), sizeof(int32_t));
+  int32_t *blk = (int32_t *)malloc(sizeof(int32_t) * n);
+  int64_t *fill = (int64_t *)calloc((size_t)o->B, sizeof(int64_t));
+  if (!o->user || !o->item || !o->val || !o->order || !o->bstart || !o->ucount || !o->icount || !blk || !fill) {
+    free(blk); free(fill);
+    return OR_ENOMEM;
+  }
+  o->nnz = nnz;
+  if (nnz > 0) {
+    memcpy(o->user, user, sizeof(int32_t) * (size_t)nnz);
+    memcpy(o->item, item, sizeof(int32_t) * (size_t)nnz);
+    memcpy(o->val, val, sizeof(float) * (size_t)nnz);
+  }
+  /* bucket by block, then sort each bucket canonically */
+  for (int64_t t = 0; t < nnz; ++t) {
+    blk[t] = block_of(o, user[t], item[t]);
+    o->bstart[blk[t] + 1] += 1;
+    o->ucount[(int64_t)blk[t] * o->N + user[t]] += 1;
+    o->icount[(int64_t)blk[t] * o->M + item[t]] += 1;
+  }
+  for (int32_t b = 0; b < o->B; ++b) o->bstart[b + 1] += o->bstart[b];
+  for (int64_t t = 0; t < nnz; ++t) o->order[o->bstart[blk[t]] + fill[blk[t]]++] = t;
+  g_sort_ctx = o;
+  for (int32_t b = 0; b < o->B; ++b)
+    qsort(o->order + o->bstart[b], (size_t)(o->bstart[b + 1] - o->bstart[b]), sizeof(int64_t), cmp_canonical);
+  free(blk); free(fill);
+  o->loaded = 1;
+  return OR_OK;
+}
+
+int oracle_set_factors(oracle_t *o, const float *L0, const float *R0) {
+  if (!o || !L0 || !R0) return OR_EINVAL;
+  size_t nl = (size_t)(o->N * o->K), nr = (size_t)(o->M * o->K);
+  for (size_t x = 0; x < nl; ++x) if (!isfinite(L0[x])) return OR_EINVAL;
+  for (size_t x = 0; x < nr; ++x) if (!isfinite(R0[x])) return OR_EINVAL;
+  if (!o->Lring) {
+    o->Lring = (float *)malloc(sizeof(float) * nl * (size_t)(o->s + 1));
+    o->Rring = (float *)malloc(sizeof(float) * nr * (size_t)(o->s + 1));
+    o->dL = (double *)malloc(sizeof(double) * nl);
+    o->dR = (double *)malloc(sizeof(double) * nr);
+    if (!o->Lring || !o->Rring || !o->dL || !o->dR) return OR_ENOMEM;
+  }
+  /* version 0 in slot 0 */
+  memcpy(o->Lring, L0, sizeof(float) * nl);
+  memcpy(o->Rring, R0, sizeof(float) * nr);
+  o->clock = 0;
+  o->vlog_len = 0;
+  o->has_factors = 1;
+  return OR_OK;
+}
+
+static float *L_of(const oracle_t *o, int64_t v) { return o->Lring + (size_t)(v % (o->s + 1)) * (size_t)(o->N * o->K); }
+static float *R_of(const oracle_t *o, int64_t v) { return o->Rring + (size_t)(v % (o->s + 1)) * (size_t)(o->M * o->K); }
+
+/* one clock: every worker computes its update from its view; the sum is committed */
+static int one_clock(oracle_t *o) {
+  const int64_t c = o->clock, K = o->K;
+  const int32_t b = (int32_t)(c % o->B);
+  memset(o->dL, 0, sizeof(double) * (size_t)(o->N * K));
+  memset(o->dR, 0, sizeof(double) * (size_t)(o->M * K));
+  for (int64_t q = o->bstart[b]; q < o->bstart[b + 1]; ++q) {
+    const int64_t t = o->order[q];
+    const int64_t i = o->user[t], j = o->item[t];
+    const int64_t v = view_version(o, o->owner[i], c);
+    const float *Li = L_of(o, v) + i * K;
+    const float *Rj = R_of(o, v) + j * K;
+    double dot = 0.0;
+    for (int64_t k = 0; k < K; ++k) dot += (double)Li[k] * (double)Rj[k];
+    const double e = (double)o->val[t] - dot;
+    const double su = (o->step == OR_ROWMEAN) ? 1.0 / (double)o->ucount[(int64_t)b * o->N + i] : 1.0;
+    const double si = (o->step == OR_ROWMEAN) ? 1.0 / (double)o->icount[(int64_t)b * o->M + j] : 1.0;
+    double *dLi = o->dL + i * K, *dRj = o->dR + j * K;
+    for (int64_t k = 0; k < K; ++k) {
+      dLi[k] += o->eta * su * (e * (double)Rj[k] - o->lambda * (double)Li[k]);
+      dRj[k] += o->eta * si * (e * (double)Li[k] - o->lambda * (double)Rj[k]);
+    }
+  }
+  /* log the versions read at this clock */
+  if (o->vlog_len + o->P > o->vlog_cap) {
+    int64_t cap = o->vlog_cap ? o->vlog_cap * 2 : 64 * (int64_t)o->P;
+    while (cap < o->vlog_len + o->P) cap *= 2;
+    int64_t *nv = (int64_t *)realloc(o->vlog, sizeof(int64_t) * (size_t)cap);
+    if (!nv) return OR_ENOMEM;
+    o->vlog = nv; o->vlog_cap = cap;
+  }
+  for (int64_t p = 0; p < o->P; ++p) o->vlog[o->vlog_len++] = view_version(o, p, c);
+  /* commit: V_{c+1} = fp32(V_c + Delta); the Deltas are complete, so the slot that held
+     version c-s may now be overwritten */
+  const float *Lc = L_of(o, c), *Rc = R_of(o, c);
+  float *Ln = L_of(o, c + 1), *Rn = R_of(o, c + 1);
+  for (int64_t x = 0; x < o->N * K; ++x) Ln[x] = (float)((double)Lc[x] + o->dL[x]);
+  for (int64_t x = 0; x < o->M * K; ++x) Rn[x] = (float)((double)Rc[x] + o->dR[x]);
+  o->clock = c + 1;
+  return OR_OK;
+}
+
+int oracle_clock(oracle_t *o, int32_t n) {
+  if (!o || n < 0) return OR_EINVAL;
+  if (!o->loaded || !o->has_factors) return OR_ESTATE;
+  for (int32_t q = 0; q < n; ++q) {
+    int rc = one_clock(o);
+    if (rc) return rc;
+  }
+  return OR_OK;
+}
+
+int oracle_get_clock(const oracle_t *o, int64_t *c) {
+  if (!o || !c) return OR_EINVAL;
+  *c = o->clock;
+  return OR_OK;
+}
+
+/* copy committed version v (must still be in the ring: clock-s <= v <= clock) */
+int oracle_get_version(const oracle_t *o, int64_t v, float *L, float *R) {
+  if (!o || !L || !R) return OR_EINVAL;
+  if (!o->has_factors) return OR_ESTATE;
+  if (v > o->clock || v < o->clock - o->s || v < 0) return OR_EINVAL;
+  memcpy(L, L_of(o, v), sizeof(float) * (size_t)(o->N * o->K));
+  memcpy(R, R_of(o, v), sizeof(float) * (size_t)(o->M * o->K));
+  return OR_OK;
+}
+
+/* squared loss at the latest version */
+int oracle_loss(const oracle_t *o, double *out) {
+  if (!o || !out) return OR_EINVAL;
+  if (!o->loaded || !o->has_factors) return OR_ESTATE;
+  const float *L = L_of(o, o->clock), *R = R_of(o, o->clock);
+  double acc = 0.0;
+  for (int64_t t = 0; t < o->nnz; ++t) {
+    const float *Li = L + (int64_t)o->user[t] * o->K, *Rj = R + (int64_t)o->item[t] * o->K;
+    double dot = 0.0;
+    for (int64_t k = 0; k < o->K; ++k) dot += (double)Li[k] * (double)Rj[k];
+    const double e = (double)o->val[t] - dot;
+    acc += e * e;
+  }
+  *out = acc;
+  return OR_OK;
+}
+
+/*
+ * Rows of version (clock + nclocks) for selected users and items, advancing only those
+ * rows.  Valid only while every view read in those clocks is version 0 (so the needed
+ * views are the initial factors): e.g. the first clock under any policy, or clocks
+ * 0..s under SSP_WORST.  The oracle's own clock does not move.
+ */
+int oracle_rows_from_v0(const oracle_t *o, int32_t nclocks, int64_t nu, const int64_t *users, int64_t ni,
+                        const int64_t *items, float *L_out, float *R_out) {
+  if (!o || nclocks < 0 || nu < 0 || ni < 0) return OR_EINVAL;
+  if (!o->loaded || !o->has_factors || o->clock != 0) return OR_ESTATE;
+  const int64_t K = o->K;
+  for (int64_t c = 0; c < nclocks; ++c)
+    for (int64_t p = 0; p < o->P; ++p)
+      if (view_version(o, p, c) != 0) return OR_EINVAL;
+  const float *L0 = L_of(o, 0), *R0 = R_of(o, 0);
+  int64_t *upos = (int64_t *)malloc(sizeof(int64_t) * (size_t)o->N);
+  int64_t *ipos = (int64_t *)malloc(sizeof(int64_t) * (size_t)o->M);
+  double *dl = (double *)calloc((size_t)(nu * K + 1), sizeof(double));
+  double *dr = (double *)calloc((size_t)(ni * K + 1), sizeof(double));
+  if (!upos || !ipos || !dl || !dr) { free(upos); free(ipos); free(dl); free(dr); return OR_ENOMEM; }
+  for (int64_t i = 0; i < o->N; ++i) upos[i] = -1;
+  for (int64_t j = 0; j < o->M; ++j) ipos[j] = -1;
+  for (int64_t a = 0; a < nu; ++a) { if (users[a] < 0 || users[a] >= o->N) goto bad; upos[users[a]] = a; }
+  for (int64_t a = 0; a < ni; ++a) { if (items[a] < 0 || items[a] >= o->M) goto bad; ipos[items[a]] = a; }
+  for (int64_t a = 0; a < nu; ++a) memcpy(L_out + a * K, L0 + users[a] * K, sizeof(float) * (size_t)K);
+  for (int64_t a = 0; a < ni; ++a) memcpy(R_out + a * K, R0 + items[a] * K, sizeof(float) * (size_t)K);
+  for (int64_t c = 0; c < nclocks; ++c) {
+    const int32_t b = (int32_t)(c % o->B);
+    memset(dl, 0, sizeof(double) * (size_t)(nu * K));
+    memset(dr, 0, sizeof(double) * (size_t)(ni * K));
+    for (int64_t q = o->bstart[b]; q < o->bstart[b + 1]; ++q) {
+      const int64_t t = o->order[q];
+      const int64_t i = o->user[t], j = o->item[t];
+      if (upos[i] < 0 && ipos[j] < 0) continue;
+      const float *Li = L0 + i * K, *Rj = R0 + j * K;
+      double dot = 0.0;
+      for (int64_t k = 0; k < K; ++k) dot += (double)Li[k] * (double)Rj[k];
+      const double e = (double)o->val[t] - dot;
+      if (upos[i] >= 0) {
+        const double su = (o->step == OR_ROWMEAN) ? 1.0 / (double)o->ucount[(int64_t)b * o->N + i] : 1.0;
+        double *d = dl + upos[i] * K;
+        for (int64_t k = 0; k < K; ++k) d[k] += o->eta * su * (e * (double)Rj[k] - o->lambda * (double)Li[k]);
+      }
+      if (ipos[j] >= 0) {
+        const double si = (o->step == OR_ROWMEAN) ? 1.0 / (double)o->icount[(int64_t)b * o->M + j] : 1.0;
+        double *d = dr + ipos[j] * K;
+        for (int64_t k = 0; k < K; ++k) d[k] += o->eta * si * (e * (double)Li[k] - o->lambda * (double)Rj[k]);
+      }
+    }
+    for (int64_t x = 0; x < nu * K; ++x) L_out[x] = (float)((double)L_out[x] + dl[x]);
+    for (int64_t x = 0; x < ni * K; ++x) R_out[x] = (float)((double)R_out[x] + dr[x]);
+  }
+  free(upos); free(ipos); free(dl); free(dr);
+  return OR_OK;
+bad:
+  free(upos); free(ipos); free(dl); free(dr);
+  return OR_EINVAL;
+}
+
+/*
+ * Canonical integer layout, the same form the library exports:
+ *   OWNER        int32 [N]
+ *   ROW_PTR(b)   int64 [N+1]  prefix sums of per-user counts in block b (users in id order)
+ *   COL(b)       int32 [nnz_b] items in canonical (user, item, load index) order
+ *   PERM(b)      int64 [nnz_b] load indices in the same order
+ *   USER_COUNT(b) int32 [N], ITEM_COUNT(b) int32 [M]
+ *   VERSION_LOG  int64 [clocks * P], entry c*P + p = v(p, c)
+ */
+int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t cap, int64_t *len) {
+  if (!o || !len) return OR_EINVAL;
+  if (kind != OR_X_OWNER && kind != OR_X_VERSION_LOG) {
+    if (!o->loaded) return OR_ESTATE;
+    if (b < 0 || b >= o->B) return OR_EINVAL;
+  }
+  int64_t n = 0;
+  switch (kind) {
+    case OR_X_OWNER: n = o->N; break;
+    case OR_X_ROW_PTR: n = o->N + 1; break;
+    case OR_X_COL: case OR_X_PERM: n = o->bstart[b + 1] - o->bstart[b]; break;
+    case OR_X_USER_COUNT: n = o->N; break;
+    case OR_X_ITEM_COUNT: n = o->M; break;
+    case OR_X_VERSION_LOG: n = o->vlog_len; break;
+    default: return OR_EINVAL;
+  }
+  *len = n;
+  if (!buf) return OR_OK;
+  if (cap < n) return OR_EINVAL;
+  switch (kind) {
+    case OR_X_OWNER: memcpy(buf, o->owner, sizeof(int32_t) * (size_t)n); break;
+    case OR_X_ROW_PTR: {
+      int64_t *rp = (int64_t *)buf;
+      rp[0] = 0;
+      for (int64_t i = 0; i < o->N; ++i) rp[i + 1] = rp[i] + o->ucount[(int64_t)b * o->N + i];
+      break;
+    }
+    case OR_X_COL:
+      for (int64_t q = 0; q < n; ++q) ((int32_t *)buf)[q] = o->item[o->order[o->bstart[b] + q]];
+      break;
+    case OR_X_PERM: memcpy(buf, o->order + o->bstart[b], sizeof(int64_t) * (size_t)n); break;
+    case OR_X_USER_COUNT: memcpy(buf, o->ucount + (int64_t)b * o->N, sizeof(int32_t) * (size_t)n); break;
+    case OR_X_ITEM_COUNT: memcpy(buf, o->icount + (int64_t)b * o->M, sizeof(int32_t) * (size_t)n); break;
+    case OR_X_VERSION_LOG: if (n) memcpy(buf, o->vlog, sizeof(int64_t) * (size_t)n); break;
+  }
+  return OR_OK;
+}
