@@ -1,0 +1,159 @@
+"""Throughput of the clocked SSP/ESSP matrix-factorization SGD sweep on one MI355X.
+
+One step = one clock of all P logical workers over one minibatch (sweep: residuals, dL
+segment sums, dR accumulation; commit: the new version), i.e. every per-clock step of the
+method.  The default workload is the Netflix-shaped 100M-rating matrix (480,189 users x
+17,770 items, Zipf(1.1) user degrees capped at the item count, Zipf(0.9) item
+popularity), rank K=128, P=64 workers, s=3, eta=0.002, lambda=0.05, one full shard per
+clock; inputs are seeded synthetic data resident in HBM before timing starts.
+
+Prints one JSON line: rating-updates/s, the dominant kernel's roofline position (HIP
+events on the library's stream) and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_FP32_VECTOR_TFLOPS = 157.3   # MI355X published fp32 vector peak (packed FMA)
+PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
+POLICIES = {"lazy": 0, "worst": 1, "essp": 2}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30, help="timed clocks")
+    ap.add_argument("--warmup", type=int, default=3, help="untimed clocks before timing")
+    ap.add_argument("--config", default="full")
+    ap.add_argument("--s", type=int, default=None, help="staleness (default: 3 for the full config)")
+    ap.add_argument("--policy", default="lazy", choices=sorted(POLICIES))
+    ap.add_argument("--cpu-sample", type=int, default=50_000_000,
+                    help="ratings in the oracle's timed sample (0 disables the CPU baseline)")
+    ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, spec, K, s, policy, nsample):
+    """The oracle, single-threaded, on the ratings of a prefix of users (one clock)."""
+    import oracle
+
+    order = np.argsort(w.user, kind="stable")
+    take = order[:nsample]
+    u, i, v = w.user[take], w.item[take], w.val[take]
+    o = oracle.Oracle(spec.N, spec.M, K, spec.P, s, spec.eta, spec.lam, policy, oracle.ROWMEAN, spec.B, spec.seed)
+    o.load(u, i, v)
+    o.set_factors(w.L0, w.R0)
+    t0 = time.perf_counter()
+    o.clock(1)
+    dt = time.perf_counter() - t0
+    o.close()
+    return {"value": len(take) / dt, "unit": "rating-updates/s", "cores": 1, "kind": "oracle",
+            "sample": f"one clock over the {len(take)} ratings of users {int(u.min())}..{int(u.max())} "
+                      f"(users in id order) of the same workload, {dt:.1f} s on "
+                      f"{platform.processor() or platform.machine()}, 1 thread"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU path is a design, not part of this build)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_1410_8043_amd import ps_mf, synth
+
+    spec = synth.CONFIGS[args.config]
+    s = args.s if args.s is not None else (3 if 3 in spec.s_values else spec.s_values[0])
+    policy = POLICIES[args.policy]
+    torch.cuda.set_device(0)
+    t_gen = time.perf_counter()
+    w = synth.generate(spec)
+    t_gen = time.perf_counter() - t_gen
+    print(f"[bench] generated {args.config}: {w.nnz} ratings in {t_gen:.1f} s", file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream()
+    g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, B=spec.B,
+                   mb_seed=spec.seed, timing=not args.no_timing, stream=stream)
+    t_load = time.perf_counter()
+    g.load_ratings(w.user, w.item, w.val)
+    g.set_factors(w.L0, w.R0)
+    t_load = time.perf_counter() - t_load
+    print(f"[bench] layout + upload {t_load:.1f} s", file=sys.stderr, flush=True)
+    nnz_clock = w.nnz / spec.B  # mean ratings per clock (exact for B=1)
+
+    g.clock(args.warmup)
+    torch.cuda.synchronize()
+    if not args.no_timing:
+        base_sweep = g.kernel_time(ps_mf.KERNEL_SWEEP)
+        base_commit = g.kernel_time(ps_mf.KERNEL_COMMIT)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    g.clock(args.steps)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    print(f"[bench] {args.steps} clocks in {dt * 1e3:.2f} ms", file=sys.stderr, flush=True)
+    loss = g.loss()
+
+    value = nnz_clock * args.steps / dt
+    K = spec.K
+    roof = None
+    extra = {}
+    if not args.no_timing:
+        ms_s, n_s = g.kernel_time(ps_mf.KERNEL_SWEEP)
+        ms_c, n_c = g.kernel_time(ps_mf.KERNEL_COMMIT)
+        sweep_ms = (ms_s - base_sweep[0]) / (n_s - base_sweep[1])
+        commit_ms = (ms_c - base_commit[0]) / (n_c - base_commit[1])
+        flops = 6.0 * K * nnz_clock                  # 3K fp32 FMA per rating update
+        achieved = flops / (sweep_ms * 1e-3) / 1e12  # TFLOP/s
+        roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), "traffic": None}
+        # compulsory HBM bytes of one clock: each rating once (int32 item + fp32 value),
+        # the view version read, the base version read when s > 0, the new version written
+        table = (spec.N + spec.M) * K * 4
+        hbm_bytes = 8 * nnz_clock + table * (2 if s == 0 else 3)
+        extra = {"sweep_ms": round(sweep_ms, 4), "commit_ms": round(commit_ms, 4),
+                 "hbm_algorithmic_frac": round(hbm_bytes / (dt / args.steps) / (PEAK_HBM_GBS * 1e9), 4)}
+    g.close()
+
+    cpu = None
+    if args.cpu_sample > 0:
+        print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, spec, K, s, policy, min(args.cpu_sample, w.nnz))
+
+    line = {
+        "metric": "rating-updates/sec at K=128, 100M ratings (1 GPU); % of HBM roofline",
+        "value": round(value, 1),
+        "unit": "rating-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dt / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded, Netflix-shaped)",
+        "config": {"workload": f"{args.config}: {spec.N} users x {spec.M} items, {w.nnz} ratings, K={K}, "
+                               f"P={spec.P}, s={s}, policy={args.policy}, B={spec.B}, eta={spec.eta}, "
+                               f"lambda={spec.lam}",
+                   "global_batch": int(nnz_clock), "parallelism": "1 GPU, P logical workers",
+                   "loss_after": loss, **extra},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

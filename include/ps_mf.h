@@ -1,0 +1,159 @@
+/*
+ * ps_mf — clocked SSP / ESSP matrix-factorization SGD on one MI355X (gfx950), P logical
+ * workers emulated on one GPU.  C ABI: plain host or device pointers and sizes only.
+ *
+ * The method (Dai et al., "High-Performance Distributed ML at Scale through Parameter
+ * Server Consistency Models", arXiv 1410.8043):
+ *   - Section 3.1: factor an N x M ratings matrix D into L (N x K) and R (K x M) by SGD;
+ *     per observed rating e_ij = D_ij - L_i . R_j and
+ *         L_i += eta (e_ij R_j - lambda L_i),   R_j += eta (e_ij L_i - lambda R_j)
+ *     (the factor 2 absorbed into eta); L and R live in the parameter server, the
+ *     ratings are partitioned over workers.
+ *   - Section 3.2 (formal SSP condition): worker p at clock c reads a view that holds
+ *     every update of clocks <= c-s-1 plus any subset of the in-window updates.
+ *   - Section 2.2 / Section 4: ESSP pushes fresh rows eagerly; GET / INC / CLOCK, with
+ *     the updates of a clock coalesced and applied at the clock boundary.
+ *   - Section 5: one Clock() processes one minibatch; the squared loss is reported.
+ *
+ * Semantics implemented (readings of points the paper leaves open):
+ *   - each (worker p, clock c) reads ONE committed version v(p,c) = max(0, c - d(p,c)),
+ *     with d from the policy: SSP_LAZY d = (c + p mod (s+1)) mod (s+1) (staleness spread
+ *     uniformly over 0..s, as a lazily refreshed cache does); SSP_WORST d = s (exactly the
+ *     guaranteed pre-window); ESSP d = min(s, 1) (the eager push lands one clock later);
+ *   - version c+1 = version c + the sum over workers of their clock-c updates, each
+ *     computed at the worker's view (no read-my-writes inside a clock);
+ *   - STEP ROWMEAN (default) divides a row's summed contribution by its number of ratings
+ *     in the clock's minibatch (items: across all workers); STEP SUM does not;
+ *   - minibatch block of rating (i, j) = splitmix64(seed ^ (i << 32 | j)) mod B, where
+ *     splitmix64(x) is one step of the SplitMix64 generator from state x; clock c
+ *     processes block c mod B; rows with no rating in the block are unchanged;
+ *   - duplicate (i, j) ratings are separate terms.
+ *
+ * Storage: factors are fp32.  R is stored items x K row-major (the transpose of the
+ * paper's K x M layout).  The handle keeps a ring of s+1 committed versions in HBM;
+ * version v lives in slot v mod (s+1).
+ *
+ * Conventions for every call:
+ *   - returns PS_MF_OK (0) or a negative code; ps_mf_last_error() gives the message;
+ *   - host input arrays are copied before the call returns; output buffers belong to
+ *     the caller; the handle owns all device memory it allocates;
+ *   - a handle is not thread-safe; calls on one handle must not overlap;
+ *   - kernels run on the handle's stream (ps_mf_set_stream), asynchronously unless the
+ *     call says it synchronizes.
+ */
+#ifndef PS_MF_H
+#define PS_MF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ps_mf ps_mf_t;
+
+/* return codes */
+#define PS_MF_OK 0
+#define PS_MF_EINVAL (-1) /* bad argument: sizes, ranges, non-finite values, unknown keys */
+#define PS_MF_ENOMEM (-2) /* host or device allocation failed; the handle stays destroyable */
+#define PS_MF_EDEVICE (-3) /* a HIP call failed (no device, launch error, fault) */
+#define PS_MF_ESTATE (-4) /* call out of order (e.g. clock before load and set_factors) */
+
+/* option keys (ps_mf_set_option); all must be set before ps_mf_load_ratings */
+#define PS_MF_OPT_POLICY 1    /* PS_MF_SSP_LAZY (default), PS_MF_SSP_WORST, PS_MF_ESSP */
+#define PS_MF_OPT_STEP 2      /* PS_MF_STEP_ROWMEAN (default), PS_MF_STEP_SUM */
+#define PS_MF_OPT_MB_BLOCKS 3 /* B >= 1 minibatch blocks (default 1: full shard per clock) */
+#define PS_MF_OPT_MB_SEED 4   /* 64-bit seed of the block hash (default 0) */
+#define PS_MF_OPT_HOST_ONLY 5 /* 1: build and export the integer layout only; never touch a device */
+#define PS_MF_OPT_TIMING 6    /* 1: record HIP events around every kernel (ps_mf_kernel_time) */
+
+#define PS_MF_SSP_LAZY 0
+#define PS_MF_SSP_WORST 1
+#define PS_MF_ESSP 2
+
+#define PS_MF_STEP_ROWMEAN 0
+#define PS_MF_STEP_SUM 1
+
+/* index kinds (ps_mf_export_index) */
+#define PS_MF_IDX_OWNER 0       /* int32 [users]: worker of each user */
+#define PS_MF_IDX_ROW_PTR 1     /* int64 [users+1]: prefix sums of USER_COUNT(b), users in id order */
+#define PS_MF_IDX_COL 2         /* int32 [nnz_b]: items of block b in (user, item, load index) order */
+#define PS_MF_IDX_PERM 3        /* int64 [nnz_b]: load indices in the same order */
+#define PS_MF_IDX_USER_COUNT 4  /* int32 [users]: ratings of each user in block b */
+#define PS_MF_IDX_ITEM_COUNT 5  /* int32 [items]: ratings of each item in block b (all workers) */
+#define PS_MF_IDX_VERSION_LOG 6 /* int64 [clocks*P]: v(p,c) at entry c*P + p (clock-major, Section 3.2) */
+
+/* kernel ids (ps_mf_kernel_time) */
+#define PS_MF_KERNEL_SWEEP 0  /* residual, dL segment-sum and dR accumulation of one clock */
+#define PS_MF_KERNEL_COMMIT 1 /* clock commit: R (and untouched L rows) of the new version */
+
+/*
+ * Create a handle for an N x M problem of rank K with P workers and staleness s
+ * (Section 3.1 problem statement; Section 3.2 staleness).  No device memory is touched.
+ * Limits: 1 <= users, items <= 2^31-1; 1 <= K <= 512; 1 <= P <= 65536; 0 <= s <= 1024;
+ * eta and lambda finite.  EINVAL otherwise; *out is NULL on failure.
+ */
+int ps_mf_create(int64_t users, int64_t items, int32_t K, int32_t P, int32_t s, float eta, float lambda,
+                 ps_mf_t **out);
+
+/* Set an option (keys above) before ps_mf_load_ratings; ESTATE after it, EINVAL for an
+   unknown key or value. */
+int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value);
+
+/* Optional explicit data partition (Section 3.1: ratings partitioned over workers):
+   owner[users] with values in [0, P); default owner(i) = i mod P.  Before load. */
+int ps_mf_set_owner_map(ps_mf_t *h, const int32_t *owner);
+
+/* Launch everything on this HIP stream (a hipStream_t, e.g. torch's current stream);
+   NULL selects the handle's own stream.  The caller keeps the stream alive. */
+int ps_mf_set_stream(ps_mf_t *h, void *hip_stream);
+
+/* Load the observed ratings D_obs as host COO arrays of length n (Section 3.1): user in
+   [0, users), item in [0, items), finite value.  Builds the per-block layout (integer
+   work, on the host) and uploads it.  Once per handle (ESTATE on a second call).
+   Synchronizes. */
+int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const float *value, int64_t n);
+
+/* Set version 0 from host arrays L (users x K) and R (items x K), row-major fp32,
+   finite.  Resets the clock to 0 and the version log.  Synchronizes. */
+int ps_mf_set_factors(ps_mf_t *h, const float *L, const float *R);
+
+/* All P workers advance n >= 0 clocks in lockstep (Section 3.2): for each clock c the
+   worker views are chosen, the sweep runs over block c mod B and version c+1 is
+   committed.  Asynchronous on the handle's stream.  ESTATE before load and set_factors. */
+int ps_mf_clock(ps_mf_t *h, int32_t n);
+
+/* Squared loss (Section 5): sum over every loaded rating of (D_ij - L_i . R_j)^2 at the
+   latest version, accumulated in fp64.  Synchronizes. */
+int ps_mf_loss(ps_mf_t *h, double *out);
+
+/* Copy the latest committed version into host arrays L (users x K), R (items x K).
+   Synchronizes. */
+int ps_mf_get_factors(ps_mf_t *h, float *L, float *R);
+
+/* Copy committed version v (clock-s <= v <= clock: still in the ring).  Synchronizes. */
+int ps_mf_get_version(ps_mf_t *h, int64_t v, float *L, float *R);
+
+/* Number of clocks committed since set_factors. */
+int ps_mf_get_clock(ps_mf_t *h, int64_t *clock);
+
+/* Copy an integer index (kinds above) of block `block` into buf (capacity `cap`
+   elements); *len receives the element count.  buf = NULL only queries *len.  EINVAL
+   if cap is too small.  Works in host-only mode. */
+int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64_t cap, int64_t *len);
+
+/* With PS_MF_OPT_TIMING on: total milliseconds and launch count of a kernel id over all
+   clocks run so far (HIP events on the handle's stream).  Synchronizes. */
+int ps_mf_kernel_time(ps_mf_t *h, int32_t kernel, double *ms, int64_t *count);
+
+/* Message of the last failed call on this handle (never NULL). */
+const char *ps_mf_last_error(const ps_mf_t *h);
+
+/* Free everything the handle owns; NULL-safe; valid after any failure. */
+void ps_mf_destroy(ps_mf_t *h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PS_MF_H */

@@ -1,0 +1,132 @@
+"""The C-ABI library: symbols, argument checks and the host-side integer layout (no GPU).
+
+Host-only handles (PS_MF_OPT_HOST_ONLY) build and export the integer layout without
+touching a device; their exports must equal the oracle's, bit for bit.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+ps_mf = pytest.importorskip("paper_1410_8043_amd.ps_mf", reason="libps_mf.so not built")
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "ps_mf.h")).read()
+    return sorted(set(re.findall(r"\b(ps_mf_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(ps_mf.LIB_PATH)
+    names = declared_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(ps_mf.SYMBOLS)
+
+
+@pytest.mark.parametrize("args", [
+    (0, 1, 1, 1, 0, 0.1, 0.1), (1, 0, 1, 1, 0, 0.1, 0.1), (1, 1, 0, 1, 0, 0.1, 0.1), (1, 1, 513, 1, 0, 0.1, 0.1),
+    (1, 1, 1, 0, 0, 0.1, 0.1), (1, 1, 1, 1, -1, 0.1, 0.1), (1, 1, 1, 1, 0, float("nan"), 0.1),
+    (1, 1, 1, 1, 0, 0.1, float("inf")), (2**31, 1, 1, 1, 0, 0.1, 0.1)])
+def test_create_rejects_bad_arguments(args):
+    with pytest.raises(ps_mf.PsMfError) as e:
+        ps_mf.ps_mf_create(*args)
+    assert e.value.code == ps_mf.EINVAL
+
+
+def test_option_and_state_errors():
+    h = ps_mf.ps_mf_create(4, 3, 2, 2, 1, 0.1, 0.1)
+    try:
+        for key, val in [(99, 0), (ps_mf.OPT_POLICY, 7), (ps_mf.OPT_STEP, 5), (ps_mf.OPT_MB_BLOCKS, 0)]:
+            with pytest.raises(ps_mf.PsMfError) as e:
+                ps_mf.ps_mf_set_option(h, key, val)
+            assert e.value.code == ps_mf.EINVAL
+        with pytest.raises(ps_mf.PsMfError) as e:
+            ps_mf.ps_mf_set_owner_map(h, np.array([0, 1, 2, 0]))
+        assert e.value.code == ps_mf.EINVAL
+        for f in (lambda: ps_mf.ps_mf_clock(h, 1), lambda: ps_mf.ps_mf_loss(h),
+                  lambda: ps_mf.ps_mf_set_factors(h, np.zeros((4, 2)), np.zeros((3, 2)))):
+            with pytest.raises(ps_mf.PsMfError) as e:
+                f()
+            assert e.value.code == ps_mf.ESTATE
+        ps_mf.ps_mf_set_option(h, ps_mf.OPT_HOST_ONLY, 1)
+        ps_mf.ps_mf_load_ratings(h, np.array([0, 3]), np.array([2, 0]), np.array([1.0, 5.0]))
+        with pytest.raises(ps_mf.PsMfError) as e:
+            ps_mf.ps_mf_load_ratings(h, np.array([0]), np.array([0]), np.array([1.0]))
+        assert e.value.code == ps_mf.ESTATE
+        with pytest.raises(ps_mf.PsMfError) as e:
+            ps_mf.ps_mf_set_option(h, ps_mf.OPT_POLICY, ps_mf.ESSP)
+        assert e.value.code == ps_mf.ESTATE
+        with pytest.raises(ps_mf.PsMfError) as e:
+            ps_mf.ps_mf_export_index(h, ps_mf.IDX_COL, 1)
+        assert e.value.code == ps_mf.EINVAL
+        assert "block" in ps_mf.ps_mf_last_error(h)
+    finally:
+        ps_mf.ps_mf_destroy(h)
+    ps_mf.ps_mf_destroy(None)  # NULL-safe
+
+
+@pytest.mark.parametrize("bad", [dict(user=[0, 4]), dict(user=[-1, 0]), dict(item=[0, 3]),
+                                 dict(value=[1.0, float("nan")]), dict(value=[float("inf"), 1.0])])
+def test_load_rejects_bad_ratings(bad):
+    coo = dict(user=[0, 1], item=[0, 2], value=[1.0, 2.0])
+    coo.update(bad)
+    with ps_mf.PsMf(4, 3, 2, 1, 0, 0.1, 0.1, host_only=True) as g:
+        with pytest.raises(ps_mf.PsMfError) as e:
+            g.load_ratings(np.array(coo["user"]), np.array(coo["item"]), np.array(coo["value"]))
+        assert e.value.code == ps_mf.EINVAL
+
+
+def compare_layout(g, o, B, N, M):
+    assert np.array_equal(g.export_index(ps_mf.IDX_OWNER), o.export(oracle.X_OWNER))
+    for b in range(B):
+        for kind_g, kind_o in [(ps_mf.IDX_ROW_PTR, oracle.X_ROW_PTR), (ps_mf.IDX_COL, oracle.X_COL),
+                               (ps_mf.IDX_PERM, oracle.X_PERM), (ps_mf.IDX_USER_COUNT, oracle.X_USER_COUNT),
+                               (ps_mf.IDX_ITEM_COUNT, oracle.X_ITEM_COUNT)]:
+            a, e = g.export_index(kind_g, b), o.export(kind_o, b)
+            assert a.dtype == e.dtype and np.array_equal(a, e), (b, kind_g)
+
+
+@pytest.mark.parametrize("B", [1, 3, 8])
+@pytest.mark.parametrize("custom_owner", [False, True])
+def test_host_layout_is_bit_exact_with_oracle(B, custom_owner):
+    rng = np.random.default_rng(B)
+    N, M, P, n = 300, 120, 7, 5000
+    user = rng.integers(0, N, n).astype(np.int32)
+    item = rng.integers(0, M, n).astype(np.int32)  # duplicates included on purpose
+    val = rng.integers(1, 6, n).astype(np.float32)
+    owner = rng.integers(0, P, N).astype(np.int32) if custom_owner else None
+    seed = 0x14108043 + B
+    with ps_mf.PsMf(N, M, 4, P, 2, 0.01, 0.05, B=B, mb_seed=seed, owner=owner, host_only=True) as g:
+        g.load_ratings(user, item, val)
+        o = oracle.Oracle(N, M, 4, P, 2, 0.01, 0.05, oracle.SSP_LAZY, oracle.ROWMEAN, B, seed, owner)
+        o.load(user, item, val)
+        compare_layout(g, o, B, N, M)
+
+
+def test_host_layout_on_generated_workload():
+    from paper_1410_8043_amd import synth
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.05)
+    w = synth.generate(spec, K=8)
+    with ps_mf.PsMf(spec.N, spec.M, 8, spec.P, 3, 0.01, 0.05, B=spec.B, mb_seed=spec.seed, host_only=True) as g:
+        g.load_ratings(w.user, w.item, w.val)
+        o = oracle.Oracle(spec.N, spec.M, 8, spec.P, 3, 0.01, 0.05, oracle.SSP_LAZY, oracle.ROWMEAN, spec.B, spec.seed)
+        o.load(w.user, w.item, w.val)
+        compare_layout(g, o, spec.B, spec.N, spec.M)
+
+
+def test_empty_and_single_rating_layouts():
+    with ps_mf.PsMf(5, 4, 3, 2, 0, 0.1, 0.1, host_only=True) as g:
+        g.load_ratings(np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+        assert g.export_index(ps_mf.IDX_COL).size == 0
+        assert np.array_equal(g.export_index(ps_mf.IDX_ROW_PTR), np.zeros(6, np.int64))
+    with ps_mf.PsMf(5, 4, 3, 2, 0, 0.1, 0.1, host_only=True) as g:
+        g.load_ratings(np.array([4]), np.array([3]), np.array([2.0]))
+        assert np.array_equal(g.export_index(ps_mf.IDX_ROW_PTR), [0, 0, 0, 0, 0, 1])
+        assert np.array_equal(g.export_index(ps_mf.IDX_ITEM_COUNT), [0, 0, 0, 1])

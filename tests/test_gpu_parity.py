@@ -1,0 +1,237 @@
+"""HIP path vs the CPU oracle, through the C ABI, on the same seeded inputs (MI355X).
+
+Tolerances (stated for the method): factors max |GPU - oracle| <= 1e-4 and loss relative
+error <= 1e-5 after the config's clocks; integer work (layout, version log) bit-exact.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from golden_cases import load_cases
+from paper_1410_8043_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+FACTOR_TOL = 1e-4
+LOSS_RTOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_1410_8043_amd import ps_mf
+
+    return ps_mf
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, policy=0, step=0, B=1,
+             seed=0, owner=None, check_versions=False):
+    say(f"case N={N} M={M} K={K} P={P} s={s} policy={policy} step={step} B={B} nnz={len(w_user)} clocks={clocks}")
+    o = oracle.Oracle(N, M, K, P, s, eta, lam, policy, step, B, seed, owner)
+    o.load(w_user, w_item, w_val)
+    o.set_factors(L0, R0)
+    with ps_mf.PsMf(N, M, K, P, s, eta, lam, policy=policy, step=step, B=B, mb_seed=seed, owner=owner) as g:
+        g.load_ratings(w_user, w_item, w_val)
+        g.set_factors(L0, R0)
+        g.clock(clocks)
+        o.clock(clocks)
+        L, R = g.get_factors()
+        Lo, Ro = o.get_factors()
+        err = max(np.abs(L - Lo).max(initial=0), np.abs(R - Ro).max(initial=0))
+        loss, loss_o = g.loss(), o.loss()
+        assert err <= FACTOR_TOL, err
+        assert abs(loss - loss_o) <= LOSS_RTOL * max(loss_o, 1e-30), (loss, loss_o)
+        assert np.array_equal(g.export_index(gpu_mod().IDX_VERSION_LOG), o.export(oracle.X_VERSION_LOG))
+        if check_versions:
+            for v in range(max(0, clocks - s), clocks + 1):
+                Lv, Rv = g.get_version(v)
+                Lov, Rov = o.get_version(v)
+                assert max(np.abs(Lv - Lov).max(), np.abs(Rv - Rov).max()) <= FACTOR_TOL
+    return err
+
+
+def gpu_mod():
+    from paper_1410_8043_amd import ps_mf
+    return ps_mf
+
+
+# ---------------------------------------------------------------- hand-worked values
+@pytest.mark.parametrize("case", load_cases(), ids=lambda c: c["name"])
+def test_hand_examples_through_abi(gpu, case):
+    u = np.array([r[0] for r in case["ratings"]], np.int32)
+    i = np.array([r[1] for r in case["ratings"]], np.int32)
+    v = np.array([r[2] for r in case["ratings"]], np.float32)
+    say(f"hand example {case['name']}")
+    with gpu.PsMf(case["N"], case["M"], case["K"], case["P"], case["s"], case["eta"], case["lam"],
+                  policy=case["policy"], step=case["step"], owner=case["owner"]) as g:
+        g.load_ratings(u, i, v)
+        g.set_factors(case["L0"], case["R0"])
+        for ex in sorted(case["expect"], key=lambda e: e["clock"]):
+            g.clock(ex["clock"] - g.clock_value)
+            L, R = g.get_factors()
+            np.testing.assert_allclose(L.ravel(), ex["L"], atol=1e-6, rtol=0)
+            np.testing.assert_allclose(R.ravel(), ex["R"], atol=1e-6, rtol=0)
+            if ex["loss"] is not None:
+                assert abs(g.loss() - ex["loss"]) <= 1e-5 * ex["loss"]
+
+
+# ---------------------------------------------------------------- configured workloads
+@pytest.mark.parametrize("s", [0, 2])
+@pytest.mark.parametrize("policy", [oracle.SSP_LAZY, oracle.SSP_WORST, oracle.ESSP])
+def test_tiny_config(gpu, s, policy):
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta,
+             lam=spec.lam, clocks=spec.clocks, policy=policy, check_versions=True)
+
+
+@pytest.mark.parametrize("step", [oracle.ROWMEAN, oracle.SUM])
+def test_tiny_config_step_modes(gpu, step):
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=2, eta=spec.eta,
+             lam=spec.lam, clocks=spec.clocks, step=step)
+
+
+@pytest.mark.parametrize("s", [0, 1, 3, 7])
+def test_full_shape_scaled(gpu, s):
+    """The 100M-rating K=128 workload's degree laws at 2% of its size (several tiles, ragged tails)."""
+    spec = synth.scaled(synth.CONFIGS["full"], 0.02)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta,
+             lam=spec.lam, clocks=10, check_versions=True)
+
+
+@pytest.mark.parametrize("policy", [oracle.SSP_WORST, oracle.ESSP])
+def test_full_shape_scaled_policies(gpu, policy):
+    spec = synth.scaled(synth.CONFIGS["full"], 0.02)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=7, eta=spec.eta,
+             lam=spec.lam, clocks=10, policy=policy)
+
+
+def test_medium_shape_scaled_minibatch_blocks(gpu):
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.05)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=spec.clocks, B=spec.B, seed=spec.seed, check_versions=True)
+
+
+def test_contention_shape_scaled(gpu):
+    spec = synth.scaled(synth.CONFIGS["contention"], 0.03)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=15, eta=spec.eta,
+             lam=spec.lam, clocks=20)
+
+
+def test_large_shape_scaled(gpu):
+    spec = synth.scaled(synth.CONFIGS["large"], 0.005)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=10)
+
+
+@pytest.mark.parametrize("s", [0, 3])
+def test_long_rows_take_the_workgroup_path(gpu, s):
+    """Users with thousands of ratings (the capped Zipf head) exercise the long-row kernel."""
+    spec = synth.ConfigSpec("heavy", 9, 40, 9000, 60_000, 1.1, 0.9, 8, 0.5, 64, 4, (s,), 0.01, 0.05, 5, 1)
+    w = synth.generate(spec)
+    assert np.bincount(w.user).max() >= 4096
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=0.01,
+             lam=0.05, clocks=5)
+
+
+# ---------------------------------------------------------------- ragged rank and edge cases
+def small_problem(seed, N, M, nnz, K, dup=0):
+    rng = np.random.default_rng(seed)
+    cells = rng.choice(N * M, size=nnz, replace=False)
+    user = (cells // M).astype(np.int32)
+    item = (cells % M).astype(np.int32)
+    if dup:
+        extra = rng.integers(0, nnz, size=dup)
+        user = np.concatenate([user, user[extra]])
+        item = np.concatenate([item, item[extra]])
+    val = rng.integers(1, 6, size=user.shape[0]).astype(np.float32)
+    L0 = (0.1 * rng.standard_normal((N, K))).astype(np.float32)
+    R0 = (0.1 * rng.standard_normal((M, K))).astype(np.float32)
+    return user, item, val, L0, R0
+
+
+@pytest.mark.parametrize("K", [1, 7, 16, 33, 100, 128, 200, 256, 512])
+def test_ragged_rank(gpu, K):
+    N, M = 300, 90
+    user, item, val, L0, R0 = small_problem(K, N, M, 3000, K, dup=20)
+    run_both(gpu, user, item, val, L0, R0, N=N, M=M, K=K, P=5, s=2, eta=0.05, lam=0.05, clocks=6)
+
+
+def test_zero_degree_rows_and_custom_owner(gpu):
+    N, M, K = 200, 80, 16
+    user, item, val, L0, R0 = small_problem(3, N, M, 1500, K)
+    keep = (user % 3 != 0) & (item % 4 != 0)  # many users and items with no rating
+    owner = np.random.default_rng(4).integers(0, 6, N).astype(np.int32)
+    run_both(gpu, user[keep], item[keep], val[keep], L0, R0, N=N, M=M, K=K, P=6, s=3, eta=0.05, lam=0.05,
+             clocks=8, owner=owner, check_versions=True)
+
+
+def test_single_rating_and_empty(gpu):
+    L0 = np.full((3, 4), 0.5, np.float32)
+    R0 = np.full((2, 4), 0.25, np.float32)
+    run_both(gpu, np.array([2], np.int32), np.array([1], np.int32), np.array([3.0], np.float32), L0, R0,
+             N=3, M=2, K=4, P=2, s=1, eta=0.1, lam=0.1, clocks=4)
+    run_both(gpu, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32), L0, R0,
+             N=3, M=2, K=4, P=2, s=1, eta=0.1, lam=0.1, clocks=3)
+
+
+def test_device_handle_exports_match_oracle_layout(gpu):
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.02)
+    w = synth.generate(spec, K=8)
+    with gpu.PsMf(spec.N, spec.M, 8, spec.P, 3, 0.01, 0.05, B=spec.B, mb_seed=spec.seed) as g:
+        g.load_ratings(w.user, w.item, w.val)
+        o = oracle.Oracle(spec.N, spec.M, 8, spec.P, 3, 0.01, 0.05, oracle.SSP_LAZY, oracle.ROWMEAN, spec.B,
+                          spec.seed)
+        o.load(w.user, w.item, w.val)
+        for b in range(spec.B):
+            assert np.array_equal(g.export_index(gpu.IDX_PERM, b), o.export(oracle.X_PERM, b))
+            assert np.array_equal(g.export_index(gpu.IDX_ROW_PTR, b), o.export(oracle.X_ROW_PTR, b))
+
+
+def test_checkpoint_resume_at_s0(gpu):
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    args = (spec.N, spec.M, spec.K, spec.P, 0, spec.eta, spec.lam)
+    with gpu.PsMf(*args) as a:
+        a.load_ratings(w.user, w.item, w.val)
+        a.set_factors(w.L0, w.R0)
+        a.clock(10)
+        L10, R10 = a.get_factors()
+    with gpu.PsMf(*args) as b:
+        b.load_ratings(w.user, w.item, w.val)
+        b.set_factors(w.L0, w.R0)
+        b.clock(5)
+        L5, R5 = b.get_factors()
+        b.set_factors(L5, R5)
+        b.clock(5)
+        Lr, Rr = b.get_factors()
+    assert max(np.abs(L10 - Lr).max(), np.abs(R10 - Rr).max()) <= FACTOR_TOL
+
+
+def test_timing_option_counts_launches(gpu):
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    with gpu.PsMf(spec.N, spec.M, spec.K, spec.P, 2, spec.eta, spec.lam, timing=True) as g:
+        g.load_ratings(w.user, w.item, w.val)
+        g.set_factors(w.L0, w.R0)
+        g.clock(7)
+        ms, n = g.kernel_time(gpu.KERNEL_SWEEP)
+        assert n == 7 and ms > 0
+        ms, n = g.kernel_time(gpu.KERNEL_COMMIT)
+        assert n == 7 and ms > 0
