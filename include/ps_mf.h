@@ -66,6 +66,9 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_OPT_MB_SEED 4   /* 64-bit seed of the block hash (default 0) */
 #define PS_MF_OPT_HOST_ONLY 5 /* 1: build and export the integer layout only; never touch a device */
 #define PS_MF_OPT_TIMING 6    /* 1: record HIP events around every kernel (ps_mf_kernel_time) */
+#define PS_MF_OPT_TILE_BYTES 7 /* bytes of user rows per tile of the item-major sweep (default 3 MiB,
+                                  sized to one XCD's 4 MiB L2); >= 1 */
+#define PS_MF_OPT_UNIT_MAX 8   /* ratings per item-major work unit (default 1024); >= 1 */
 
 #define PS_MF_SSP_LAZY 0
 #define PS_MF_SSP_WORST 1

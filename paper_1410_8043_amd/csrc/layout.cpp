@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cmath>
+#include <functional>
 #include <new>
 #include <numeric>
 #include <thread>
@@ -33,6 +34,100 @@ void counting_pass(const std::vector<int64_t> &src, std::vector<int64_t> &dst, i
   for (int64_t x : src) cnt[static_cast<size_t>(key(x)) + 1] += 1;
   for (int64_t r = 0; r < range; ++r) cnt[r + 1] += cnt[r];
   for (int64_t x : src) dst[static_cast<size_t>(cnt[static_cast<size_t>(key(x))]++)] = x;
+}
+
+// Work units of one sweep direction over the nb canonical entries of a block.
+//   xrow(e), yrow(e): stationary and gathered row of entry e;
+//   tile(e) in [0, ntiles), cls_of_tile(t): the worker class whose view the tile reads.
+// The canonical order must already be sorted by y within equal x (true for both
+// directions: canonical is (user, item)), so two stable passes give (tile, x, y).
+void build_units(int64_t nb, int64_t nx, int64_t ntiles, const std::function<int32_t(int64_t)> &xrow,
+                 const std::function<int32_t(int64_t)> &yrow, const std::function<int32_t(int64_t)> &tile,
+                 const std::function<int32_t(int64_t)> &cls_of_tile, const std::vector<float> &val,
+                 int32_t unit_max, UnitSet &U) {
+  U.ntiles = ntiles;
+  std::vector<int64_t> a(static_cast<size_t>(nb)), b(static_cast<size_t>(nb));
+  std::iota(a.begin(), a.end(), int64_t(0));
+  counting_pass(a, b, nx, xrow);
+  counting_pass(b, a, ntiles, tile);
+  std::vector<int64_t>().swap(b);
+  struct Unit { int32_t tile, x; int64_t beg; int32_t len; };
+  std::vector<Unit> units;
+  std::vector<int64_t> tile_units(static_cast<size_t>(ntiles) + 1, 0);
+  for (int64_t e = 0; e < nb;) {
+    const int32_t t = tile(a[e]), x = xrow(a[e]);
+    int64_t f = e;
+    while (f < nb && xrow(a[f]) == x && tile(a[f]) == t) ++f;
+    for (int64_t c = e; c < f; c += unit_max) {
+      units.push_back({t, x, c, static_cast<int32_t>(std::min<int64_t>(unit_max, f - c))});
+      tile_units[t + 1] += 1;
+    }
+    e = f;
+  }
+  for (int64_t t = 0; t < ntiles; ++t) tile_units[t + 1] += tile_units[t];
+  const int64_t nu = static_cast<int64_t>(units.size());
+  // partial rows in (x, tile, chunk) order: units are generated in (tile, x) order, so a
+  // stable pass by x gives it
+  U.x_pp.assign(static_cast<size_t>(nx) + 1, 0);
+  for (const Unit &u : units) U.x_pp[u.x + 1] += 1;
+  for (int64_t x = 0; x < nx; ++x) U.x_pp[x + 1] += U.x_pp[x];
+  std::vector<int32_t> out_of(static_cast<size_t>(nu));
+  {
+    std::vector<int64_t> fill(U.x_pp.begin(), U.x_pp.end() - 1);
+    for (int64_t k = 0; k < nu; ++k) out_of[k] = static_cast<int32_t>(fill[units[k].x]++);
+  }
+  // execution order: tile by tile, longest unit first; kXcds contiguous chunks of about
+  // equal rating count
+  U.y.resize(static_cast<size_t>(nb));
+  U.val.resize(static_cast<size_t>(nb));
+  U.unit_x.resize(static_cast<size_t>(nu));
+  U.unit_cls.resize(static_cast<size_t>(nu));
+  U.unit_len.resize(static_cast<size_t>(nu));
+  U.unit_out.resize(static_cast<size_t>(nu));
+  U.unit_beg.resize(static_cast<size_t>(nu));
+  U.xcd_off.assign(kXcds + 1, nu);
+  int64_t k = 0, pos = 0;
+  int next_xcd = 0;
+  std::vector<int64_t> ids;
+  for (int64_t t = 0; t < ntiles; ++t) {
+    ids.resize(static_cast<size_t>(tile_units[t + 1] - tile_units[t]));
+    std::iota(ids.begin(), ids.end(), tile_units[t]);
+    std::stable_sort(ids.begin(), ids.end(), [&](int64_t q, int64_t r) { return units[q].len > units[r].len; });
+    for (int64_t q : ids) {
+      while (next_xcd < kXcds && pos * kXcds >= next_xcd * nb) U.xcd_off[next_xcd++] = k;
+      const Unit &u = units[q];
+      U.unit_x[k] = u.x;
+      U.unit_cls[k] = cls_of_tile(u.tile);
+      U.unit_len[k] = u.len;
+      U.unit_out[k] = out_of[q];
+      U.unit_beg[k] = pos;
+      for (int64_t c = 0; c < u.len; ++c) {
+        const int64_t e = a[u.beg + c];
+        U.y[pos] = yrow(e);
+        U.val[pos] = val[e];
+        ++pos;
+      }
+      ++k;
+    }
+  }
+  while (next_xcd < kXcds) U.xcd_off[next_xcd++] = k;
+  U.xcd_off[kXcds] = k;
+}
+
+// number of distinct (x, tile) runs for a tile function (entries sorted by x already)
+int64_t count_runs(int64_t nb, const std::vector<int64_t> &by_x, const std::function<int32_t(int64_t)> &xrow,
+                   const std::function<int32_t(int64_t)> &tile, int64_t ntiles, std::vector<int64_t> &last) {
+  last.assign(static_cast<size_t>(ntiles), -1);
+  int64_t runs = 0;
+  for (int64_t e = 0; e < nb; ++e) {
+    const int64_t x = xrow(by_x[e]);
+    const int32_t t = tile(by_x[e]);
+    if (last[t] != x) {
+      last[t] = x;
+      ++runs;
+    }
+  }
+  return runs;
 }
 
 }  // namespace
@@ -76,6 +171,11 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
       a.swap(b);
     }
     std::vector<int64_t>().swap(b);
+    // ---- worker class of each user; class-pure user tiles for the item-major sweep
+    std::vector<int32_t> ucls(static_cast<size_t>(N));
+    for (int64_t i = 0; i < N; ++i) ucls[i] = p.cls_of_worker[p.owner[i]];
+    std::vector<int64_t> rank_in_cls(static_cast<size_t>(N)), in_cls(static_cast<size_t>(p.nclass), 0);
+    for (int64_t i = 0; i < N; ++i) rank_in_cls[i] = in_cls[ucls[i]]++;
     // ---- per block arrays
     out.assign(static_cast<size_t>(p.B), BlockLayout());
     std::vector<int64_t> bstart(static_cast<size_t>(p.B) + 1, 0);
@@ -98,33 +198,76 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
       L.ucount.assign(static_cast<size_t>(N), 0);
       L.icount.assign(static_cast<size_t>(M), 0);
       L.icount_cls.assign(static_cast<size_t>(M * p.nclass), 0);
+      std::vector<int32_t> ent_user(static_cast<size_t>(nb));
       for (int64_t x = 0; x < nb; ++x) {
         const int64_t t = L.perm[x];
+        ent_user[x] = user[t];
         L.ucount[user[t]] += 1;
         L.icount[item[t]] += 1;
-        L.icount_cls[static_cast<size_t>(item[t]) * p.nclass + p.cls_of_worker[p.owner[user[t]]]] += 1;
+        L.icount_cls[static_cast<size_t>(item[t]) * p.nclass + ucls[user[t]]] += 1;
       }
       L.row_ptr.assign(static_cast<size_t>(N) + 1, 0);
       for (int64_t i = 0; i < N; ++i) L.row_ptr[i + 1] = L.row_ptr[i] + L.ucount[i];
-      // segment schedule: longest first so that long rows start early
-      std::vector<int32_t> users;
-      for (int64_t i = 0; i < N; ++i) {
-        if (L.ucount[i] > 0) users.push_back(static_cast<int32_t>(i));
-        else L.untouched.push_back(static_cast<int32_t>(i));
+
+      // ---- units.  Tiles start at the L2-sized row count and grow (x2) while the units
+      // would average fewer than 16 ratings (each unit costs one partial row).
+      const int64_t min_avg = 16;
+      // user-major: x = user, y = item, tile = (class, item range)
+      {
+        const std::function<int32_t(int64_t)> xr = [&](int64_t e) { return ent_user[e]; };
+        const std::function<int32_t(int64_t)> yr = [&](int64_t e) { return L.col[e]; };
+        int64_t rows = std::max<int64_t>(1, std::min<int64_t>(p.tile_rows_item, M));
+        std::vector<int64_t> by_x(static_cast<size_t>(nb)), last;
+        std::iota(by_x.begin(), by_x.end(), int64_t(0));  // canonical is sorted by user
+        for (;;) {
+          const int64_t nt = (M + rows - 1) / rows;
+          const std::function<int32_t(int64_t)> tl = [&, rows, nt](int64_t e) {
+            return static_cast<int32_t>(ucls[ent_user[e]] * nt + L.col[e] / rows);
+          };
+          if (rows >= M || count_runs(nb, by_x, xr, tl, nt * p.nclass, last) * min_avg <= nb) break;
+          rows *= 2;
+        }
+        const int64_t nt = (M + rows - 1) / rows;
+        const std::function<int32_t(int64_t)> tl = [&, rows, nt](int64_t e) {
+          return static_cast<int32_t>(ucls[ent_user[e]] * nt + L.col[e] / rows);
+        };
+        const std::function<int32_t(int64_t)> ct = [nt](int64_t t) { return static_cast<int32_t>(t / nt); };
+        build_units(nb, N, nt * p.nclass, xr, yr, tl, ct, L.val, p.unit_max, L.by_user);
       }
-      std::stable_sort(users.begin(), users.end(),
-                       [&](int32_t x, int32_t y) { return L.ucount[x] > L.ucount[y]; });
-      L.seg_user = users;
-      L.seg_beg.resize(users.size());
-      L.seg_len.resize(users.size());
-      L.seg_cls.resize(users.size());
-      L.nheavy = 0;
-      for (size_t s = 0; s < users.size(); ++s) {
-        const int32_t u = users[s];
-        L.seg_beg[s] = L.row_ptr[u];
-        L.seg_len[s] = L.ucount[u];
-        L.seg_cls[s] = p.cls_of_worker[p.owner[u]];
-        if (L.ucount[u] >= p.heavy_min) L.nheavy = static_cast<int32_t>(s + 1);
+      // item-major: x = item, y = user, tile = class-pure user range
+      {
+        const std::function<int32_t(int64_t)> xr = [&](int64_t e) { return L.col[e]; };
+        const std::function<int32_t(int64_t)> yr = [&](int64_t e) { return ent_user[e]; };
+        std::vector<int64_t> by_x(static_cast<size_t>(nb)), tmp(static_cast<size_t>(nb)), last;
+        std::iota(tmp.begin(), tmp.end(), int64_t(0));
+        counting_pass(tmp, by_x, M, xr);
+        std::vector<int64_t>().swap(tmp);
+        int64_t rows = std::max<int64_t>(1, std::min<int64_t>(p.tile_rows_user, N));
+        std::vector<int64_t> cls_base;
+        auto tiles_for = [&](int64_t r) {
+          cls_base.assign(static_cast<size_t>(p.nclass) + 1, 0);
+          for (int32_t c = 0; c < p.nclass; ++c) cls_base[c + 1] = cls_base[c] + (in_cls[c] + r - 1) / r;
+          return cls_base[p.nclass];
+        };
+        for (;;) {
+          const int64_t nt = tiles_for(rows);
+          const std::function<int32_t(int64_t)> tl = [&, rows](int64_t e) {
+            const int32_t u = ent_user[e];
+            return static_cast<int32_t>(cls_base[ucls[u]] + rank_in_cls[u] / rows);
+          };
+          if (rows >= N || count_runs(nb, by_x, xr, tl, std::max<int64_t>(nt, 1), last) * min_avg <= nb) break;
+          rows *= 2;
+        }
+        const int64_t nt = std::max<int64_t>(tiles_for(rows), 1);
+        const std::function<int32_t(int64_t)> tl = [&, rows](int64_t e) {
+          const int32_t u = ent_user[e];
+          return static_cast<int32_t>(cls_base[ucls[u]] + rank_in_cls[u] / rows);
+        };
+        std::vector<int32_t> tile_cls(static_cast<size_t>(nt), 0);
+        for (int32_t c = 0; c < p.nclass; ++c)
+          for (int64_t t = cls_base[c]; t < cls_base[c + 1]; ++t) tile_cls[t] = c;
+        const std::function<int32_t(int64_t)> ct = [&](int64_t t) { return tile_cls[t]; };
+        build_units(nb, M, nt, xr, yr, tl, ct, L.val, p.unit_max, L.by_item);
       }
     }
     return 0;

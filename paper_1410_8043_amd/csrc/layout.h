@@ -1,6 +1,6 @@
 // Host-side integer layout of the observed ratings: minibatch blocks, per-block CSR by
-// user in canonical (user, item, load index) order, and the segment schedule the sweep
-// kernels walk.  Integer work only; bit-exact by construction.
+// user in canonical (user, item, load index) order, and the work units the sweep kernels
+// walk.  Integer work only; bit-exact by construction.
 #pragma once
 
 #include <cstdint>
@@ -8,6 +8,8 @@
 #include <vector>
 
 namespace psmf {
+
+constexpr int kXcds = 8;  // MI355X: 8 accelerator complex dies, each with its own L2
 
 // SplitMix64 (Steele, Lea & Flood 2014): one step of the sequential generator from
 // `state`.  Used for the minibatch block of a rating.
@@ -24,6 +26,25 @@ inline int32_t block_of(uint64_t seed, int32_t B, int64_t i, int64_t j) {
   return static_cast<int32_t>(splitmix64_next(key) % static_cast<uint64_t>(B));
 }
 
+// The ratings of one block cut into work units for one sweep direction.  The sweep keeps
+// one "stationary" row x in registers and gathers the rows y of the other factor from a
+// tile of y rows small enough to stay in one XCD's L2:
+//   user-major (dL): x = user, y = item, tiles = (worker class, item id range);
+//   item-major (dR): x = item, y = user, tiles = class-pure ranges of users.
+// A unit is a run of one x's ratings inside one tile, split at unit_max ratings.  Units
+// are stored in execution order (tile, longest first) and cut into kXcds contiguous
+// chunks of about equal rating count; chunk x runs on XCD x.  Each unit writes one
+// partial row; the partial rows of x are [x_pp[x], x_pp[x+1]).
+struct UnitSet {
+  std::vector<int32_t> y;         // gathered row of each rating, in unit order
+  std::vector<float> val;         // rating value, in unit order
+  std::vector<int32_t> unit_x, unit_cls, unit_len, unit_out;
+  std::vector<int64_t> unit_beg;
+  std::vector<int64_t> xcd_off;   // [kXcds + 1]
+  std::vector<int64_t> x_pp;      // [rows of x + 1]
+  int64_t ntiles = 0;
+};
+
 struct BlockLayout {
   int64_t nnz = 0;
   // ratings of the block in canonical (user, item, load index) order
@@ -34,13 +55,7 @@ struct BlockLayout {
   std::vector<int32_t> ucount;   // [users]
   std::vector<int32_t> icount;   // [items]
   std::vector<int32_t> icount_cls;  // [items * nclass]: raters of the item per worker class
-  // segment schedule: users with >= 1 rating, longest first (ties: lower id first)
-  std::vector<int32_t> seg_user;
-  std::vector<int64_t> seg_beg;
-  std::vector<int32_t> seg_len;
-  std::vector<int32_t> seg_cls;
-  int32_t nheavy = 0;  // the first nheavy segments are long enough for a whole workgroup
-  std::vector<int32_t> untouched;  // users with no rating in the block
+  UnitSet by_user, by_item;
 };
 
 struct LayoutParams {
@@ -50,8 +65,10 @@ struct LayoutParams {
   int32_t nclass = 1;               // worker classes that share one view schedule
   const int32_t *owner = nullptr;   // [users]
   const int32_t *cls_of_worker = nullptr;  // [P]
-  int32_t heavy_min = 1 << 30;      // segments with at least this many ratings are "heavy"
   int32_t threads = 1;
+  int64_t tile_rows_item = 1 << 30; // items per tile of the user-major sweep
+  int64_t tile_rows_user = 1 << 30; // users per tile of the item-major sweep
+  int32_t unit_max = 1024;          // ratings per work unit
 };
 
 // Validates the COO input (EINVAL message in err) and fills one BlockLayout per block.

@@ -3,21 +3,27 @@
 // and the host orchestration around them.
 //
 // Device state (HBM):
-//   ring    : (s+1) slots, each [L: users x Kp | R: items x Kp] fp32 row-major; version v
-//             lives in slot v mod (s+1); Kp = K rounded up to the kernels' row width,
-//             padding columns are kept at zero in every slot.
-//   dR      : items x Kp fp32 accumulator of the clock's item updates (zero between clocks).
-//   per block: col/val in canonical (user, item, load index) order, the segment schedule
-//             (user, first entry, length, worker class), item counts (total and per worker
-//             class), the list of users without a rating in the block.
+//   ring      : (s+1) slots, each [L: users x Kp | R: items x Kp] fp32 row-major; version v
+//               lives in slot v mod (s+1); Kp = K rounded up to a power of two >= 8, the
+//               padding columns are kept at zero in every slot.
+//   per block : the ratings twice, as work units of the user-major and of the item-major
+//               sweep (see layout.h), user and item rating counts (items also per worker
+//               class).
+//   partial_u : [units, Kp] one row of sum_j e_ij R^v_j per user-major unit;
+//   partial_i : [units, Kp] one row of sum_i e_ij L^v_i per item-major unit.
 //   slot table: for clock c, the ring slot each worker class reads (Section 3.2 view).
 //
-// One clock c (Section 3.1 update, Section 3.2 SSP view, Section 4 coalesced commit):
-//   sweep  : for every user segment of block c mod B: e = D_ij - L^v_i . R^v_j for each
-//            rating, dL_i summed in registers, L^{c+1}_i written once (one writer per
-//            user), e * L^v_i added into dR_j with hardware fp32 atomics;
-//   commit : R^{c+1}_j = R^c_j + scale_j (dR_j - lambda sum_v n_j^(v) R^v_j); dR_j = 0;
-//            users without a rating in the block copy L^c_i into the new slot (s > 0).
+// One clock c (Section 3.1 update, Section 3.2 SSP view, Section 4 coalesced commit).
+// Neither sweep uses atomics: a unit keeps one row (the stationary side) in registers,
+// gathers the other side's rows from a tile that stays in one XCD's L2, recomputes the
+// residual e = D_ij - L^v_i . R^v_j and writes one partial row.
+//   sweep (item-major units, then user-major units);
+//   finalize : L^{c+1}_i = L^c_i + scale_i (sum of i's partial rows - n_i lambda L^v_i),
+//              users without a rating in the block keep L^c_i;
+//   commit   : R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class
+//              n_j^(class) R^{v(class)}_j).
+// Both sweeps read versions <= c only; finalize and commit write version c+1 into the
+// slot that held version c-s, after both sweeps are done with it.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -35,262 +41,149 @@
 
 namespace {
 
-constexpr int kBlock = 256;   // threads per workgroup (4 wavefronts of 64)
+constexpr int kBlock = 256;  // threads per workgroup (4 wavefronts of 64)
 constexpr int kMaxKp = 512;
-constexpr int kHeavyMin = 4096;  // ratings per user from which a whole workgroup takes the row
+constexpr int kXcds = psmf::kXcds;
 
 // ------------------------------------------------------------------ device helpers
-template <int E>
-__device__ __forceinline__ void load_row(float (&d)[E], const float *__restrict__ p) {
-  if constexpr (E == 1) {
-    d[0] = p[0];
-  } else if constexpr (E == 2) {
-    const float2 t = *reinterpret_cast<const float2 *>(p);
-    d[0] = t.x; d[1] = t.y;
-  } else {
+// A factor row of Kp = G*E floats is spread over a lane group of G lanes: lane g holds the
+// float4 chunks q*G + g (q = 0 .. E/4-1), so each float4 load of the group reads 16*G
+// contiguous bytes.
+template <int G, int E>
+__device__ __forceinline__ void load_row(float (&d)[E], const float *__restrict__ row, int g) {
 #pragma unroll
-    for (int q = 0; q < E / 4; ++q) {
-      const float4 t = *reinterpret_cast<const float4 *>(p + 4 * q);
-      d[4 * q] = t.x; d[4 * q + 1] = t.y; d[4 * q + 2] = t.z; d[4 * q + 3] = t.w;
-    }
+  for (int q = 0; q < E / 4; ++q) {
+    const float4 t = *reinterpret_cast<const float4 *>(row + 4 * (q * G + g));
+    d[4 * q] = t.x; d[4 * q + 1] = t.y; d[4 * q + 2] = t.z; d[4 * q + 3] = t.w;
   }
 }
 
-template <int E>
-__device__ __forceinline__ void store_row(float *__restrict__ p, const float (&d)[E]) {
-  if constexpr (E == 1) {
-    p[0] = d[0];
-  } else if constexpr (E == 2) {
-    *reinterpret_cast<float2 *>(p) = make_float2(d[0], d[1]);
-  } else {
+template <int G, int E>
+__device__ __forceinline__ void store_row(float *__restrict__ row, const float (&d)[E], int g) {
 #pragma unroll
-    for (int q = 0; q < E / 4; ++q)
-      *reinterpret_cast<float4 *>(p + 4 * q) = make_float4(d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]);
-  }
+  for (int q = 0; q < E / 4; ++q)
+    *reinterpret_cast<float4 *>(row + 4 * (q * G + g)) = make_float4(d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]);
 }
 
-// sum over the G lanes of a lane group (G a power of two dividing 64)
+// Sum over the G lanes of an aligned lane group with DPP moves inside a 16-lane row:
+// quad_perm [1,0,3,2] (xor 1), quad_perm [2,3,0,1] (xor 2), row_half_mirror (the other
+// quad of the 8), row_mirror (the other 8 of the 16).  Every lane gets the total.
 template <int G>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int m = G / 2; m > 0; m >>= 1) v += __shfl_xor(v, m, G);
+  static_assert(G == 2 || G == 4 || G == 8 || G == 16, "lane groups live inside one DPP row");
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
+  if constexpr (G >= 4) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));
+  if constexpr (G >= 8) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, false));
+  if constexpr (G >= 16) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, false));
   return v;
 }
 
-struct SweepArgs {
-  const int32_t *seg_user;
-  const int64_t *seg_beg;
-  const int32_t *seg_len;
-  const int32_t *seg_cls;
-  int32_t seg_first, nseg;
-  const int32_t *col;
+// residual e = r - x . y of one rating (x stationary, y gathered)
+template <int G, int E>
+__device__ __forceinline__ float residual(const float (&x)[E], const float (&y)[E], float r) {
+  float p = 0.f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) p = fmaf(x[e], y[e], p);
+  return r - group_sum<G>(p);
+}
+
+struct UnitArgs {
+  const int32_t *unit_x, *unit_cls, *unit_len, *unit_out;
+  const int64_t *unit_beg;
+  const int64_t *xcd_off;   // [kXcds + 1]
+  const int32_t *y;         // gathered row of each rating
   const float *val;
   const int32_t *cls_slot;  // ring slot read by each worker class at this clock
-  float *ring;
+  const float *ring;
   int64_t slot_stride;      // floats per slot
-  int64_t r_off;            // offset of R inside a slot
-  int32_t slot_c, slot_n;   // slots of versions c and c+1
-  float *dR;
-  float eta, lambda;
-  int32_t rowmean;
+  int64_t x_off, y_off;     // offsets of the stationary and the gathered table in a slot
+  float *partial;           // [units, Kp]
 };
 
-// L^{c+1}_i = L^c_i + scale (dL_i - n lambda L^v_i): the lambda term of each of the n
-// ratings is hoisted, scale = eta (SUM) or eta / n (ROWMEAN).
-template <int E>
-__device__ __forceinline__ void finish_user(const SweepArgs &a, int64_t rowoff, int sv, int n, const float (&lv)[E],
-                                            const float (&dl)[E]) {
-  float lc[E];
-  if (a.slot_c == sv) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) lc[e] = lv[e];
-  } else {
-    load_row<E>(lc, a.ring + a.slot_c * a.slot_stride + rowoff);
-  }
-  const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
-  const float nl = static_cast<float>(n) * a.lambda;
-  float o[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) o[e] = lc[e] + sc * (dl[e] - nl * lv[e]);
-  store_row<E>(a.ring + a.slot_n * a.slot_stride + rowoff, o);
+// The unit processed by lane group `grp` of this workgroup: workgroup b runs on XCD
+// b mod 8 and takes the units of that XCD's chunk; -1 if there is none.
+__device__ __forceinline__ int64_t unit_of(const UnitArgs &a, int grp, int groups_per_wg) {
+  const int xcd = blockIdx.x % kXcds;
+  const int64_t local = static_cast<int64_t>(blockIdx.x / kXcds) * groups_per_wg + grp;
+  const int64_t first = a.xcd_off[xcd];
+  return local < a.xcd_off[xcd + 1] - first ? first + local : -1;
 }
 
-// one lane group of G lanes per user segment; lane g owns columns [g*E, g*E+E)
+// One lane group per work unit: acc = sum_t (val_t - x . Y_{y_t}) Y_{y_t} over the unit's
+// ratings, x the unit's stationary row, two gathered rows in flight; acc -> partial row.
 template <int G, int E>
-__global__ __launch_bounds__(kBlock) void k_sweep_light(SweepArgs a) {
+__global__ __launch_bounds__(kBlock) void k_units(UnitArgs a) {
   constexpr int Kp = G * E;
-  const int lane = threadIdx.x & (G - 1);
-  const int64_t gid = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / G;
-  if (gid >= a.nseg) return;  // whole groups leave together
-  const int64_t seg = a.seg_first + gid;
-  const int64_t u = a.seg_user[seg];
-  const int64_t beg = a.seg_beg[seg];
-  const int n = a.seg_len[seg];
-  const int sv = a.cls_slot[a.seg_cls[seg]];
-  const float *__restrict__ Rv = a.ring + sv * a.slot_stride + a.r_off + lane * E;
-  const int64_t rowoff = u * Kp + lane * E;
-  float lv[E], dl[E];
-  load_row<E>(lv, a.ring + sv * a.slot_stride + rowoff);
+  const int g = threadIdx.x & (G - 1);
+  const int64_t unit = unit_of(a, threadIdx.x / G, kBlock / G);
+  if (unit < 0) return;  // whole groups leave together
+  const int sv = a.cls_slot[a.unit_cls[unit]];
+  const float *__restrict__ V = a.ring + sv * a.slot_stride;
+  const float *__restrict__ Y = V + a.y_off;
+  const int64_t beg = a.unit_beg[unit];
+  const int n = a.unit_len[unit];
+  const int32_t *__restrict__ yi = a.y + beg;
+  const float *__restrict__ vr = a.val + beg;
+  float x[E], acc[E];
+  load_row<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
 #pragma unroll
-  for (int e = 0; e < E; ++e) dl[e] = 0.f;
-  for (int t = 0; t < n; ++t) {
-    const int64_t j = a.col[beg + t];
-    const float r = a.val[beg + t];
-    float rj[E];
-    load_row<E>(rj, Rv + j * Kp);
-    float p = 0.f;
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  int t = 0;
+  for (; t + 1 < n; t += 2) {
+    const int64_t j0 = yi[t], j1 = yi[t + 1];
+    const float r0 = vr[t], r1 = vr[t + 1];
+    float y0[E], y1[E];
+    load_row<G, E>(y0, Y + j0 * Kp, g);
+    load_row<G, E>(y1, Y + j1 * Kp, g);
+    const float e0 = residual<G, E>(x, y0, r0);
+    const float e1 = residual<G, E>(x, y1, r1);
 #pragma unroll
-    for (int e = 0; e < E; ++e) p = fmaf(lv[e], rj[e], p);
-    const float err = r - group_sum<G>(p);
-    float *dst = a.dR + j * Kp + lane * E;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      dl[e] = fmaf(err, rj[e], dl[e]);
-      atomicAdd(dst + e, err * lv[e]);
-    }
+    for (int e = 0; e < E; ++e) acc[e] = fmaf(e1, y1[e], fmaf(e0, y0[e], acc[e]));
   }
-  finish_user<E>(a, rowoff, sv, n, lv, dl);
+  if (t < n) {
+    float y0[E];
+    load_row<G, E>(y0, Y + static_cast<int64_t>(yi[t]) * Kp, g);
+    const float e0 = residual<G, E>(x, y0, vr[t]);
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = fmaf(e0, y0[e], acc[e]);
+  }
+  store_row<G, E>(a.partial + static_cast<int64_t>(a.unit_out[unit]) * Kp, acc, g);
 }
 
-// one workgroup per long user segment: its kBlock/G lane groups split the ratings and
-// combine their partial dL in LDS before the single write of L^{c+1}_i
+// Squared loss over the user-major units of a block at one ring slot: e in fp32, e^2
+// accumulated in fp64, one partial per workgroup (fixed order: deterministic).
 template <int G, int E>
-__global__ __launch_bounds__(kBlock) void k_sweep_heavy(SweepArgs a) {
-  constexpr int Kp = G * E;
-  constexpr int NG = kBlock / G;
-  __shared__ float part[NG * Kp];
-  const int lane = threadIdx.x & (G - 1);
-  const int grp = threadIdx.x / G;
-  const int64_t seg = a.seg_first + blockIdx.x;
-  const int64_t u = a.seg_user[seg];
-  const int64_t beg = a.seg_beg[seg];
-  const int n = a.seg_len[seg];
-  const int sv = a.cls_slot[a.seg_cls[seg]];
-  const float *__restrict__ Rv = a.ring + sv * a.slot_stride + a.r_off + lane * E;
-  const int64_t rowoff = u * Kp + lane * E;
-  float lv[E], dl[E];
-  load_row<E>(lv, a.ring + sv * a.slot_stride + rowoff);
-#pragma unroll
-  for (int e = 0; e < E; ++e) dl[e] = 0.f;
-  for (int t = grp; t < n; t += NG) {
-    const int64_t j = a.col[beg + t];
-    const float r = a.val[beg + t];
-    float rj[E];
-    load_row<E>(rj, Rv + j * Kp);
-    float p = 0.f;
-#pragma unroll
-    for (int e = 0; e < E; ++e) p = fmaf(lv[e], rj[e], p);
-    const float err = r - group_sum<G>(p);
-    float *dst = a.dR + j * Kp + lane * E;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      dl[e] = fmaf(err, rj[e], dl[e]);
-      atomicAdd(dst + e, err * lv[e]);
-    }
-  }
-#pragma unroll
-  for (int e = 0; e < E; ++e) part[grp * Kp + lane * E + e] = dl[e];
-  __syncthreads();
-  if (grp == 0) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      float s = 0.f;
-      for (int g = 0; g < NG; ++g) s += part[g * Kp + lane * E + e];
-      dl[e] = s;
-    }
-    finish_user<E>(a, rowoff, sv, n, lv, dl);
-  }
-}
-
-struct CommitArgs {
-  float *ring;
-  int64_t slot_stride, r_off;
-  int64_t items;
-  int32_t Kp;
-  int32_t slot_c, slot_n;
-  const int32_t *icount;      // [items]
-  const int32_t *icount_cls;  // [items * nclass]
-  int32_t nclass;
-  const int32_t *cls_slot;    // [nclass]
-  float *dR;
-  float eta, lambda;
-  int32_t rowmean;
-};
-
-// R^{c+1}_j = R^c_j + scale_j (dR_j - lambda sum_classes n_j^(class) R^{v(class)}_j), dR_j = 0
-__global__ __launch_bounds__(kBlock) void k_commit(CommitArgs a) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (idx >= a.items * a.Kp) return;
-  const int64_t j = idx / a.Kp;
-  const int n = a.icount[j];
-  float *R = a.ring + a.r_off;
-  const float rc = R[a.slot_c * a.slot_stride + idx];
-  float out = rc;
-  if (n > 0) {
-    float lam = 0.f;
-    for (int q = 0; q < a.nclass; ++q) {
-      const int cnt = a.icount_cls[j * a.nclass + q];
-      if (cnt) lam = fmaf(static_cast<float>(cnt), R[a.cls_slot[q] * a.slot_stride + idx], lam);
-    }
-    const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
-    out = rc + sc * (a.dR[idx] - a.lambda * lam);
-    a.dR[idx] = 0.f;
-  }
-  R[a.slot_n * a.slot_stride + idx] = out;
-}
-
-// users without a rating in the block: L^{c+1}_i = L^c_i
-__global__ __launch_bounds__(kBlock) void k_copy_rows(const int32_t *__restrict__ users, int64_t n, int32_t Kp,
-                                                      float *ring, int64_t slot_stride, int32_t slot_c,
-                                                      int32_t slot_n) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (idx >= n * Kp) return;
-  const int64_t off = static_cast<int64_t>(users[idx / Kp]) * Kp + idx % Kp;
-  ring[slot_n * slot_stride + off] = ring[slot_c * slot_stride + off];
-}
-
-// squared loss partial sums: each lane group takes one segment, e computed in fp32,
-// e^2 accumulated in fp64; one partial per workgroup
-template <int G, int E>
-__global__ __launch_bounds__(kBlock) void k_loss(const int32_t *__restrict__ seg_user,
-                                                 const int64_t *__restrict__ seg_beg,
-                                                 const int32_t *__restrict__ seg_len, int64_t nseg,
-                                                 const int32_t *__restrict__ col, const float *__restrict__ val,
-                                                 const float *__restrict__ L, const float *__restrict__ R,
-                                                 double *__restrict__ partial) {
+__global__ __launch_bounds__(kBlock) void k_loss(UnitArgs a, int32_t slot, double *__restrict__ out) {
   constexpr int Kp = G * E;
   constexpr int NG = kBlock / G;
   __shared__ double acc_sh[NG];
-  const int lane = threadIdx.x & (G - 1);
+  const int g = threadIdx.x & (G - 1);
   const int grp = threadIdx.x / G;
-  const int64_t gid = static_cast<int64_t>(blockIdx.x) * NG + grp;
+  const int64_t unit = unit_of(a, grp, NG);
   double acc = 0.0;
-  if (gid < nseg) {
-    const int64_t u = seg_user[gid];
-    const int64_t beg = seg_beg[gid];
-    const int n = seg_len[gid];
-    float lv[E];
-    load_row<E>(lv, L + u * Kp + lane * E);
+  if (unit >= 0) {
+    const float *__restrict__ V = a.ring + slot * a.slot_stride;
+    const int64_t beg = a.unit_beg[unit];
+    const int n = a.unit_len[unit];
+    float x[E];
+    load_row<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
     for (int t = 0; t < n; ++t) {
-      float rj[E];
-      load_row<E>(rj, R + static_cast<int64_t>(col[beg + t]) * Kp + lane * E);
-      float p = 0.f;
-#pragma unroll
-      for (int e = 0; e < E; ++e) p = fmaf(lv[e], rj[e], p);
-      const float err = val[beg + t] - group_sum<G>(p);
-      acc += static_cast<double>(err) * static_cast<double>(err);
+      float y[E];
+      load_row<G, E>(y, V + a.y_off + static_cast<int64_t>(a.y[beg + t]) * Kp, g);
+      const float e = residual<G, E>(x, y, a.val[beg + t]);
+      acc += static_cast<double>(e) * static_cast<double>(e);
     }
   }
-  if (lane == 0) acc_sh[grp] = acc;
+  if (g == 0) acc_sh[grp] = acc;
   __syncthreads();
   if (threadIdx.x == 0) {
     double s = 0.0;
-    for (int g = 0; g < NG; ++g) s += acc_sh[g];
-    partial[blockIdx.x] = s;
+    for (int h = 0; h < NG; ++h) s += acc_sh[h];
+    out[blockIdx.x] = s;
   }
 }
 
-// fixed-order final sum of the partials (deterministic for a given layout)
+// fixed-order final sum of the loss partials (deterministic for a given layout)
 __global__ __launch_bounds__(kBlock) void k_sum_partials(const double *__restrict__ partial, int64_t n,
                                                           double *__restrict__ out) {
   __shared__ double sh[kBlock];
@@ -305,19 +198,95 @@ __global__ __launch_bounds__(kBlock) void k_sum_partials(const double *__restric
   }
 }
 
+struct FinalArgs {
+  float *ring;
+  int64_t slot_stride;
+  int64_t users;
+  int32_t Kp;
+  int32_t slot_c, slot_n;
+  const int32_t *ucount;   // [users]
+  const int32_t *ucls;     // [users]
+  const int32_t *cls_slot; // [nclass]
+  const float *partial;    // user-major partial rows
+  const int64_t *user_pp;  // [users + 1]
+  float eta, lambda;
+  int32_t rowmean;
+};
+
+// L^{c+1}_i = L^c_i + scale_i (sum of i's partial rows - n_i lambda L^v_i): the lambda term
+// of each of the n_i ratings is hoisted; scale = eta (SUM) or eta / n_i (ROWMEAN).  Users
+// without a rating in the block keep L^c_i (copied when the new slot differs).
+__global__ __launch_bounds__(kBlock) void k_finalize_users(FinalArgs a) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (idx >= a.users * a.Kp) return;
+  const int64_t i = idx / a.Kp, k = idx - i * a.Kp;
+  const int n = a.ucount[i];
+  if (n == 0) {
+    if (a.slot_n != a.slot_c) a.ring[a.slot_n * a.slot_stride + idx] = a.ring[a.slot_c * a.slot_stride + idx];
+    return;
+  }
+  float d = 0.f;
+  for (int64_t p = a.user_pp[i]; p < a.user_pp[i + 1]; ++p) d += a.partial[p * a.Kp + k];
+  const float lc = a.ring[a.slot_c * a.slot_stride + idx];
+  const float lv = a.ring[a.cls_slot[a.ucls[i]] * a.slot_stride + idx];
+  const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
+  a.ring[a.slot_n * a.slot_stride + idx] = lc + sc * (d - static_cast<float>(n) * a.lambda * lv);
+}
+
+struct CommitArgs {
+  float *ring;
+  int64_t slot_stride, r_off;
+  int64_t items;
+  int32_t Kp;
+  int32_t slot_c, slot_n;
+  const int32_t *icount;      // [items]
+  const int32_t *icount_cls;  // [items * nclass]
+  int32_t nclass;
+  const int32_t *cls_slot;    // [nclass]
+  const float *partial;       // item-major partial rows
+  const int64_t *item_pp;     // [items + 1]
+  float eta, lambda;
+  int32_t rowmean;
+};
+
+// R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class n_j^(class) R^{v(class)}_j)
+__global__ __launch_bounds__(kBlock) void k_commit(CommitArgs a) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (idx >= a.items * a.Kp) return;
+  const int64_t j = idx / a.Kp, k = idx - j * a.Kp;
+  const int n = a.icount[j];
+  float *R = a.ring + a.r_off;
+  const float rc = R[a.slot_c * a.slot_stride + idx];
+  float out = rc;
+  if (n > 0) {
+    float d = 0.f;
+    for (int64_t p = a.item_pp[j]; p < a.item_pp[j + 1]; ++p) d += a.partial[p * a.Kp + k];
+    float lam = 0.f;
+    for (int q = 0; q < a.nclass; ++q) {
+      const int cnt = a.icount_cls[j * a.nclass + q];
+      if (cnt) lam = fmaf(static_cast<float>(cnt), R[a.cls_slot[q] * a.slot_stride + idx], lam);
+    }
+    const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
+    out = rc + sc * (d - a.lambda * lam);
+  }
+  R[a.slot_n * a.slot_stride + idx] = out;
+}
+
 // ------------------------------------------------------------------ kernel dispatch on Kp
+// lane-group shape per padded rank: G lanes x E floats, G <= 16 so that a group sits in
+// one DPP row, E a multiple of 4 for float4 access
 struct Shape {
   int G, E;
 };
 Shape shape_for(int Kp) {
   switch (Kp) {
-    case 8: return {8, 1};
-    case 16: return {8, 2};
+    case 8: return {2, 4};
+    case 16: return {4, 4};
     case 32: return {8, 4};
-    case 64: return {16, 4};
-    case 128: return {32, 4};
-    case 256: return {64, 4};
-    default: return {64, 8};  // 512
+    case 64: return {8, 8};
+    case 128: return {8, 16};
+    case 256: return {16, 16};
+    default: return {16, 32};  // 512
   }
 }
 int padded_k(int K) {
@@ -329,39 +298,27 @@ int padded_k(int K) {
 template <template <int, int> class F, class... Args>
 hipError_t dispatch(int Kp, Args &&...args) {
   switch (Kp) {
-    case 8: return F<8, 1>::run(args...);
-    case 16: return F<8, 2>::run(args...);
+    case 8: return F<2, 4>::run(args...);
+    case 16: return F<4, 4>::run(args...);
     case 32: return F<8, 4>::run(args...);
-    case 64: return F<16, 4>::run(args...);
-    case 128: return F<32, 4>::run(args...);
-    case 256: return F<64, 4>::run(args...);
-    default: return F<64, 8>::run(args...);
+    case 64: return F<8, 8>::run(args...);
+    case 128: return F<8, 16>::run(args...);
+    case 256: return F<16, 16>::run(args...);
+    default: return F<16, 32>::run(args...);
   }
 }
 
 template <int G, int E>
-struct LaunchLight {
-  static hipError_t run(const SweepArgs &a, hipStream_t st) {
-    const int64_t threads = static_cast<int64_t>(a.nseg) * G;
-    const unsigned grid = static_cast<unsigned>((threads + kBlock - 1) / kBlock);
-    hipLaunchKernelGGL((k_sweep_light<G, E>), dim3(grid), dim3(kBlock), 0, st, a);
-    return hipGetLastError();
-  }
-};
-template <int G, int E>
-struct LaunchHeavy {
-  static hipError_t run(const SweepArgs &a, hipStream_t st) {
-    hipLaunchKernelGGL((k_sweep_heavy<G, E>), dim3(static_cast<unsigned>(a.nseg)), dim3(kBlock), 0, st, a);
+struct LaunchUnits {
+  static hipError_t run(const UnitArgs &a, int64_t grid, hipStream_t st) {
+    hipLaunchKernelGGL((k_units<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a);
     return hipGetLastError();
   }
 };
 template <int G, int E>
 struct LaunchLoss {
-  static hipError_t run(const int32_t *su, const int64_t *sb, const int32_t *sl, int64_t nseg, const int32_t *col,
-                        const float *val, const float *L, const float *R, double *partial, hipStream_t st) {
-    constexpr int NG = kBlock / G;
-    const unsigned grid = static_cast<unsigned>((nseg + NG - 1) / NG);
-    hipLaunchKernelGGL((k_loss<G, E>), dim3(grid), dim3(kBlock), 0, st, su, sb, sl, nseg, col, val, L, R, partial);
+  static hipError_t run(const UnitArgs &a, int32_t slot, int64_t grid, double *out, hipStream_t st) {
+    hipLaunchKernelGGL((k_loss<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a, slot, out);
     return hipGetLastError();
   }
 };
@@ -369,14 +326,18 @@ struct LaunchLoss {
 }  // namespace
 
 // ------------------------------------------------------------------ handle
-struct DeviceBlock {
-  int64_t nnz = 0, nseg = 0, nheavy = 0, nuntouched = 0;
-  int32_t *col = nullptr;
+struct DeviceUnits {
+  int64_t nunits = 0, grid = 0;  // grid: workgroups of a launch (kXcds x the largest chunk)
+  int32_t *y = nullptr;
   float *val = nullptr;
-  int32_t *seg_user = nullptr, *seg_len = nullptr, *seg_cls = nullptr;
-  int64_t *seg_beg = nullptr;
-  int32_t *icount = nullptr, *icount_cls = nullptr;
-  int32_t *untouched = nullptr;
+  int32_t *unit_x = nullptr, *unit_cls = nullptr, *unit_len = nullptr, *unit_out = nullptr;
+  int64_t *unit_beg = nullptr, *xcd_off = nullptr, *x_pp = nullptr;
+};
+
+struct DeviceBlock {
+  int64_t nnz = 0;
+  int32_t *ucount = nullptr, *icount = nullptr, *icount_cls = nullptr;
+  DeviceUnits by_user, by_item;
 };
 
 struct ps_mf {
@@ -388,6 +349,8 @@ struct ps_mf {
   int32_t policy = PS_MF_SSP_LAZY, step = PS_MF_STEP_ROWMEAN, B = 1;
   uint64_t seed = 0;
   bool host_only = false, timing = false;
+  int64_t tile_bytes = 3 << 20;  // rows per L2 tile of the sweeps, in bytes
+  int32_t unit_max = 1024;
   std::vector<int32_t> owner;
   // host state
   bool loaded = false, has_factors = false;
@@ -403,7 +366,8 @@ struct ps_mf {
   bool own_stream = false;
   hipStream_t user_stream = nullptr;
   float *ring = nullptr;
-  float *dR = nullptr;
+  float *partial_u = nullptr, *partial_i = nullptr;
+  int32_t *ucls = nullptr;
   int32_t *slot_table = nullptr;  // [(2s+1) * nclass]
   double *loss_partial = nullptr;
   int64_t loss_partial_len = 0;
@@ -434,13 +398,13 @@ int fail(ps_mf_t *h, int code, const char *fmt, ...) {
   return code;
 }
 
-#define HIP_TRY(h, expr)                                                                          \
-  do {                                                                                           \
-    hipError_t e_ = (expr);                                                                      \
-    if (e_ != hipSuccess) {                                                                      \
+#define HIP_TRY(h, expr)                                                                                  \
+  do {                                                                                                   \
+    hipError_t e_ = (expr);                                                                              \
+    if (e_ != hipSuccess) {                                                                              \
       if (e_ == hipErrorOutOfMemory) return fail(h, PS_MF_ENOMEM, "%s: %s", #expr, hipGetErrorString(e_)); \
-      return fail(h, PS_MF_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_));                     \
-    }                                                                                            \
+      return fail(h, PS_MF_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_));                             \
+    }                                                                                                    \
   } while (0)
 
 int dev_alloc(ps_mf_t *h, void **p, size_t bytes) {
@@ -463,6 +427,39 @@ int upload(ps_mf_t *h, T **dst, const std::vector<T> &src) {
   if (rc) return rc;
   if (!src.empty()) HIP_TRY(h, hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice));
   return PS_MF_OK;
+}
+
+int upload_units(ps_mf_t *h, DeviceUnits &d, const psmf::UnitSet &u) {
+  int r;
+  if ((r = upload(h, &d.y, u.y)) || (r = upload(h, &d.val, u.val)) || (r = upload(h, &d.unit_x, u.unit_x)) ||
+      (r = upload(h, &d.unit_cls, u.unit_cls)) || (r = upload(h, &d.unit_len, u.unit_len)) ||
+      (r = upload(h, &d.unit_out, u.unit_out)) || (r = upload(h, &d.unit_beg, u.unit_beg)) ||
+      (r = upload(h, &d.xcd_off, u.xcd_off)) || (r = upload(h, &d.x_pp, u.x_pp)))
+    return r;
+  d.nunits = static_cast<int64_t>(u.unit_x.size());
+  int64_t most = 0;
+  for (int x = 0; x < kXcds; ++x) most = std::max<int64_t>(most, u.xcd_off[x + 1] - u.xcd_off[x]);
+  const int groups = kBlock / shape_for(h->Kp).G;
+  d.grid = kXcds * ((most + groups - 1) / groups);
+  return PS_MF_OK;
+}
+
+UnitArgs unit_args(const ps_mf_t *h, const DeviceUnits &d, float *partial, int64_t x_off, int64_t y_off) {
+  UnitArgs a{};
+  a.unit_x = d.unit_x;
+  a.unit_cls = d.unit_cls;
+  a.unit_len = d.unit_len;
+  a.unit_out = d.unit_out;
+  a.unit_beg = d.unit_beg;
+  a.xcd_off = d.xcd_off;
+  a.y = d.y;
+  a.val = d.val;
+  a.ring = h->ring;
+  a.slot_stride = (h->N + h->M) * h->Kp;
+  a.x_off = x_off;
+  a.y_off = y_off;
+  a.partial = partial;
+  return a;
 }
 
 int64_t delay_of(const ps_mf_t *h, int64_t p, int64_t c) {
@@ -505,11 +502,11 @@ int host_threads() {
   return static_cast<int>(std::min(16u, n));
 }
 
-int record(ps_mf_t *h, int kernel, hipEvent_t *a) {
+int record(ps_mf_t *h, hipEvent_t *a) {
+  *a = nullptr;
   if (!h->timing) return PS_MF_OK;
   HIP_TRY(h, hipEventCreate(a));
   HIP_TRY(h, hipEventRecord(*a, h->stream));
-  (void)kernel;
   return PS_MF_OK;
 }
 int record_end(ps_mf_t *h, int kernel, hipEvent_t a) {
@@ -529,51 +526,48 @@ int one_clock(ps_mf_t *h) {
   const DeviceBlock &db = h->dblocks[b];
   const int32_t *cls_slot = h->slot_table + table_row(h, c) * h->nclass;
   const int64_t slot_stride = (h->N + h->M) * h->Kp;
-
-  SweepArgs a{};
-  a.seg_user = db.seg_user;
-  a.seg_beg = db.seg_beg;
-  a.seg_len = db.seg_len;
-  a.seg_cls = db.seg_cls;
-  a.col = db.col;
-  a.val = db.val;
-  a.cls_slot = cls_slot;
-  a.ring = h->ring;
-  a.slot_stride = slot_stride;
-  a.r_off = h->N * h->Kp;
-  a.slot_c = slot_c;
-  a.slot_n = slot_n;
-  a.dR = h->dR;
-  a.eta = h->eta;
-  a.lambda = h->lambda;
-  a.rowmean = h->step == PS_MF_STEP_ROWMEAN;
+  const int64_t r_off = h->N * h->Kp;
+  const int rowmean = h->step == PS_MF_STEP_ROWMEAN;
 
   hipEvent_t ev = nullptr;
-  int rc = record(h, PS_MF_KERNEL_SWEEP, &ev);
+  int rc = record(h, &ev);
   if (rc) return rc;
-  if (db.nheavy > 0) {
-    a.seg_first = 0;
-    a.nseg = static_cast<int32_t>(db.nheavy);
-    HIP_TRY(h, dispatch<LaunchHeavy>(h->Kp, a, h->stream));
+  if (db.by_item.nunits > 0) {  // x = item (R), y = user (L)
+    UnitArgs a = unit_args(h, db.by_item, h->partial_i, r_off, 0);
+    a.cls_slot = cls_slot;
+    HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, a, db.by_item.grid, h->stream));
   }
-  if (db.nseg > db.nheavy) {
-    a.seg_first = static_cast<int32_t>(db.nheavy);
-    a.nseg = static_cast<int32_t>(db.nseg - db.nheavy);
-    HIP_TRY(h, dispatch<LaunchLight>(h->Kp, a, h->stream));
+  if (db.by_user.nunits > 0) {  // x = user (L), y = item (R)
+    UnitArgs a = unit_args(h, db.by_user, h->partial_u, 0, r_off);
+    a.cls_slot = cls_slot;
+    HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, a, db.by_user.grid, h->stream));
   }
   if ((rc = record_end(h, PS_MF_KERNEL_SWEEP, ev))) return rc;
 
-  if ((rc = record(h, PS_MF_KERNEL_COMMIT, &ev))) return rc;
-  if (slot_n != slot_c && db.nuntouched > 0) {
-    const int64_t n = db.nuntouched * h->Kp;
-    hipLaunchKernelGGL(k_copy_rows, dim3(static_cast<unsigned>((n + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                       h->stream, db.untouched, db.nuntouched, h->Kp, h->ring, slot_stride, slot_c, slot_n);
-    HIP_TRY(h, hipGetLastError());
-  }
+  if ((rc = record(h, &ev))) return rc;
+  FinalArgs fa{};
+  fa.ring = h->ring;
+  fa.slot_stride = slot_stride;
+  fa.users = h->N;
+  fa.Kp = h->Kp;
+  fa.slot_c = slot_c;
+  fa.slot_n = slot_n;
+  fa.ucount = db.ucount;
+  fa.ucls = h->ucls;
+  fa.cls_slot = cls_slot;
+  fa.partial = h->partial_u;
+  fa.user_pp = db.by_user.x_pp;
+  fa.eta = h->eta;
+  fa.lambda = h->lambda;
+  fa.rowmean = rowmean;
+  const int64_t nfin = h->N * h->Kp;
+  hipLaunchKernelGGL(k_finalize_users, dim3(static_cast<unsigned>((nfin + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                     h->stream, fa);
+  HIP_TRY(h, hipGetLastError());
   CommitArgs ca{};
   ca.ring = h->ring;
   ca.slot_stride = slot_stride;
-  ca.r_off = h->N * h->Kp;
+  ca.r_off = r_off;
   ca.items = h->M;
   ca.Kp = h->Kp;
   ca.slot_c = slot_c;
@@ -582,10 +576,11 @@ int one_clock(ps_mf_t *h) {
   ca.icount_cls = db.icount_cls;
   ca.nclass = h->nclass;
   ca.cls_slot = cls_slot;
-  ca.dR = h->dR;
+  ca.partial = h->partial_i;
+  ca.item_pp = db.by_item.x_pp;
   ca.eta = h->eta;
   ca.lambda = h->lambda;
-  ca.rowmean = a.rowmean;
+  ca.rowmean = rowmean;
   const int64_t ncommit = h->M * h->Kp;
   hipLaunchKernelGGL(k_commit, dim3(static_cast<unsigned>((ncommit + kBlock - 1) / kBlock)), dim3(kBlock), 0,
                      h->stream, ca);
@@ -648,6 +643,14 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
     case PS_MF_OPT_TIMING:
       h->timing = value != 0;
       return PS_MF_OK;
+    case PS_MF_OPT_TILE_BYTES:
+      if (value < 1) return fail(h, PS_MF_EINVAL, "tile bytes must be >= 1");
+      h->tile_bytes = value;
+      return PS_MF_OK;
+    case PS_MF_OPT_UNIT_MAX:
+      if (value < 1 || value > (1 << 30)) return fail(h, PS_MF_EINVAL, "unit size must be in [1, 2^30]");
+      h->unit_max = static_cast<int32_t>(value);
+      return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
   }
@@ -699,8 +702,10 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   lp.nclass = h->nclass;
   lp.owner = h->owner.data();
   lp.cls_of_worker = h->cls_of_worker.data();
-  lp.heavy_min = kHeavyMin;
   lp.threads = host_threads();
+  lp.tile_rows_item = std::max<int64_t>(64, h->tile_bytes / (static_cast<int64_t>(h->Kp) * 4));
+  lp.tile_rows_user = lp.tile_rows_item;
+  lp.unit_max = h->unit_max;
   std::string err;
   const int rc = psmf::build_layout(lp, user, item, value, n, h->layout, err);
   if (rc == -1) return fail(h, PS_MF_EINVAL, "%s", err.c_str());
@@ -713,28 +718,28 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   const size_t slot = static_cast<size_t>((h->N + h->M) * h->Kp);
   auto undo = [h](int code) { h->loaded = false; return code; };
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->ring), slot * (h->s + 1) * sizeof(float)))) return undo(r);
-  if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->dR), static_cast<size_t>(h->M * h->Kp) * sizeof(float)))) return undo(r);
-  hipError_t e = hipMemset(h->dR, 0, static_cast<size_t>(h->M * h->Kp) * sizeof(float));
-  if (e != hipSuccess) return undo(fail(h, PS_MF_EDEVICE, "hipMemset: %s", hipGetErrorString(e)));
   h->dblocks.assign(static_cast<size_t>(h->B), DeviceBlock());
-  int64_t max_groups = 1;
+  int64_t max_units_u = 1, max_units_i = 1, loss_len = 0;
   for (int b = 0; b < h->B; ++b) {
     const psmf::BlockLayout &L = h->layout[b];
     DeviceBlock &d = h->dblocks[b];
     d.nnz = L.nnz;
-    d.nseg = static_cast<int64_t>(L.seg_user.size());
-    d.nheavy = L.nheavy;
-    d.nuntouched = static_cast<int64_t>(L.untouched.size());
-    if ((r = upload(h, &d.col, L.col)) || (r = upload(h, &d.val, L.val)) || (r = upload(h, &d.seg_user, L.seg_user)) ||
-        (r = upload(h, &d.seg_beg, L.seg_beg)) || (r = upload(h, &d.seg_len, L.seg_len)) ||
-        (r = upload(h, &d.seg_cls, L.seg_cls)) || (r = upload(h, &d.icount, L.icount)) ||
-        (r = upload(h, &d.icount_cls, L.icount_cls)) || (r = upload(h, &d.untouched, L.untouched)))
+    if ((r = upload(h, &d.ucount, L.ucount)) || (r = upload(h, &d.icount, L.icount)) ||
+        (r = upload(h, &d.icount_cls, L.icount_cls)) || (r = upload_units(h, d.by_user, L.by_user)) ||
+        (r = upload_units(h, d.by_item, L.by_item)))
       return undo(r);
-    const int G = shape_for(h->Kp).G;
-    max_groups = std::max<int64_t>(max_groups, (d.nseg + kBlock / G - 1) / (kBlock / G));
+    max_units_u = std::max<int64_t>(max_units_u, d.by_user.nunits);
+    max_units_i = std::max<int64_t>(max_units_i, d.by_item.nunits);
+    loss_len += d.by_user.grid;
   }
-  // loss partials: one per workgroup of each block, laid end to end
-  h->loss_partial_len = max_groups * h->B;
+  if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->partial_u), static_cast<size_t>(max_units_u * h->Kp) * sizeof(float))) ||
+      (r = dev_alloc(h, reinterpret_cast<void **>(&h->partial_i), static_cast<size_t>(max_units_i * h->Kp) * sizeof(float))))
+    return undo(r);
+  // user class (for the finalize of L), loss partials (one per workgroup of each block)
+  std::vector<int32_t> ucls(static_cast<size_t>(h->N));
+  for (int64_t i = 0; i < h->N; ++i) ucls[i] = h->cls_of_worker[h->owner[i]];
+  if ((r = upload(h, &h->ucls, ucls))) return undo(r);
+  h->loss_partial_len = std::max<int64_t>(1, loss_len);
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->loss_partial), static_cast<size_t>(h->loss_partial_len) * sizeof(double))))
     return undo(r);
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->loss_out), sizeof(double)))) return undo(r);
@@ -766,7 +771,6 @@ int ps_mf_set_factors(ps_mf_t *h, const float *L, const float *R) {
   const size_t slot = static_cast<size_t>((h->N + h->M) * h->Kp);
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   HIP_TRY(h, hipMemset(h->ring, 0, slot * (h->s + 1) * sizeof(float)));
-  HIP_TRY(h, hipMemset(h->dR, 0, static_cast<size_t>(h->M * h->Kp) * sizeof(float)));
   HIP_TRY(h, hipMemcpy2D(h->ring, h->Kp * sizeof(float), L, h->K * sizeof(float), h->K * sizeof(float),
                          static_cast<size_t>(h->N), hipMemcpyHostToDevice));
   HIP_TRY(h, hipMemcpy2D(h->ring + h->N * h->Kp, h->Kp * sizeof(float), R, h->K * sizeof(float),
@@ -797,14 +801,13 @@ int ps_mf_loss(ps_mf_t *h, double *out) {
   const int32_t sl = static_cast<int32_t>(h->clock % (h->s + 1));
   const float *L = h->ring + sl * slot_stride;
   const float *R = L + h->N * h->Kp;
-  const int G = shape_for(h->Kp).G;
   int64_t off = 0;
   for (int b = 0; b < h->B; ++b) {
     const DeviceBlock &d = h->dblocks[b];
-    if (d.nseg == 0) continue;
-    HIP_TRY(h, dispatch<LaunchLoss>(h->Kp, d.seg_user, d.seg_beg, d.seg_len, d.nseg, d.col, d.val, L, R,
-                                     h->loss_partial + off, h->stream));
-    off += (d.nseg + kBlock / G - 1) / (kBlock / G);
+    if (d.by_user.nunits == 0) continue;
+    UnitArgs ua = unit_args(h, d.by_user, nullptr, 0, h->N * h->Kp);
+    HIP_TRY(h, dispatch<LaunchLoss>(h->Kp, ua, sl, d.by_user.grid, h->loss_partial + off, h->stream));
+    off += d.by_user.grid;
   }
   if (off == 0) {
     *out = 0.0;
