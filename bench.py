@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--cpu-sample", type=int, default=50_000_000,
                     help="ratings in the oracle's timed sample (0 disables the CPU baseline)")
     ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
+    ap.add_argument("--tile-bytes", type=int, default=None, help="bytes of rows per L2 tile of the sweeps")
+    ap.add_argument("--unit-max", type=int, default=None, help="ratings per sweep work unit")
     return ap.parse_args()
 
 
@@ -84,7 +86,8 @@ def main():
     print(f"[bench] generated {args.config}: {w.nnz} ratings in {t_gen:.1f} s", file=sys.stderr, flush=True)
     stream = torch.cuda.current_stream()
     g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, B=spec.B,
-                   mb_seed=spec.seed, timing=not args.no_timing, stream=stream)
+                   mb_seed=spec.seed, timing=not args.no_timing, stream=stream, tile_bytes=args.tile_bytes,
+                   unit_max=args.unit_max)
     t_load = time.perf_counter()
     g.load_ratings(w.user, w.item, w.val)
     g.set_factors(w.L0, w.R0)

@@ -94,7 +94,8 @@ typedef struct ps_mf ps_mf_t;
  * Create a handle for an N x M problem of rank K with P workers and staleness s
  * (Section 3.1 problem statement; Section 3.2 staleness).  No device memory is touched.
  * Limits: 1 <= users, items <= 2^31-1; 1 <= K <= 512; 1 <= P <= 65536; 0 <= s <= 1024;
- * eta and lambda finite.  EINVAL otherwise; *out is NULL on failure.
+ * users * Kp * 4 and items * Kp * 4 below 2^32 bytes (Kp = K rounded up to a power of two,
+ * at least 8); eta and lambda finite.  EINVAL otherwise; *out is NULL on failure.
  */
 int ps_mf_create(int64_t users, int64_t items, int32_t K, int32_t P, int32_t s, float eta, float lambda,
                  ps_mf_t **out);

@@ -77,41 +77,70 @@ void build_units(int64_t nb, int64_t nx, int64_t ntiles, const std::function<int
     for (int64_t k = 0; k < nu; ++k) out_of[k] = static_cast<int32_t>(fill[units[k].x]++);
   }
   // execution order: tile by tile, longest unit first; kXcds contiguous chunks of about
-  // equal rating count
-  U.y.resize(static_cast<size_t>(nb));
-  U.val.resize(static_cast<size_t>(nb));
-  U.unit_x.resize(static_cast<size_t>(nu));
-  U.unit_cls.resize(static_cast<size_t>(nu));
-  U.unit_len.resize(static_cast<size_t>(nu));
-  U.unit_out.resize(static_cast<size_t>(nu));
-  U.unit_beg.resize(static_cast<size_t>(nu));
-  U.xcd_off.assign(kXcds + 1, nu);
-  int64_t k = 0, pos = 0;
-  int next_xcd = 0;
+  // equal rating count.  Each unit's ratings start at a multiple of kUnitAlign entries and
+  // are padded with (row 0, value 0) entries to a multiple of kUnitAlign.  Empty units
+  // (length 0, writing the spare partial row nu) pad every chunk start and every change
+  // of worker class to a multiple of kWaveUnits, so the units of one wavefront always
+  // read the same ring slot.
+  std::vector<int64_t> order;
+  order.reserve(static_cast<size_t>(nu));
   std::vector<int64_t> ids;
   for (int64_t t = 0; t < ntiles; ++t) {
     ids.resize(static_cast<size_t>(tile_units[t + 1] - tile_units[t]));
     std::iota(ids.begin(), ids.end(), tile_units[t]);
     std::stable_sort(ids.begin(), ids.end(), [&](int64_t q, int64_t r) { return units[q].len > units[r].len; });
-    for (int64_t q : ids) {
-      while (next_xcd < kXcds && pos * kXcds >= next_xcd * nb) U.xcd_off[next_xcd++] = k;
-      const Unit &u = units[q];
-      U.unit_x[k] = u.x;
-      U.unit_cls[k] = cls_of_tile(u.tile);
-      U.unit_len[k] = u.len;
-      U.unit_out[k] = out_of[q];
-      U.unit_beg[k] = pos;
-      for (int64_t c = 0; c < u.len; ++c) {
-        const int64_t e = a[u.beg + c];
-        U.y[pos] = yrow(e);
-        U.val[pos] = val[e];
-        ++pos;
-      }
-      ++k;
-    }
+    order.insert(order.end(), ids.begin(), ids.end());
   }
-  while (next_xcd < kXcds) U.xcd_off[next_xcd++] = k;
-  U.xcd_off[kXcds] = k;
+  int64_t padded = 0;
+  for (const Unit &u : units) padded += (u.len + kUnitAlign - 1) / kUnitAlign * kUnitAlign;
+  U.y.assign(static_cast<size_t>(padded), 0);
+  U.val.assign(static_cast<size_t>(padded), 0.f);
+  U.unit_x.clear();
+  U.unit_cls.clear();
+  U.unit_len.clear();
+  U.unit_out.clear();
+  U.unit_beg.clear();
+  U.xcd_off.assign(kXcds + 1, 0);
+  int64_t pos = 0, rated = 0;
+  int next_xcd = 0;
+  int32_t prev_cls = -1;
+  auto pad_to_wave = [&](int32_t cls) {
+    while (U.unit_x.size() % kWaveUnits != 0) {
+      U.unit_x.push_back(0);
+      U.unit_cls.push_back(cls);
+      U.unit_len.push_back(0);
+      U.unit_out.push_back(static_cast<int32_t>(nu));
+      U.unit_beg.push_back(0);
+    }
+  };
+  for (int64_t q : order) {
+    const Unit &u = units[q];
+    const int32_t cls = cls_of_tile(u.tile);
+    bool chunk_start = false;
+    while (next_xcd < kXcds && rated * kXcds >= next_xcd * nb) {
+      if (!chunk_start) pad_to_wave(prev_cls < 0 ? cls : prev_cls);
+      chunk_start = true;
+      U.xcd_off[next_xcd++] = static_cast<int64_t>(U.unit_x.size());
+    }
+    if (!chunk_start && cls != prev_cls && prev_cls >= 0) pad_to_wave(prev_cls);
+    prev_cls = cls;
+    U.unit_x.push_back(u.x);
+    U.unit_cls.push_back(cls);
+    U.unit_len.push_back(u.len);
+    U.unit_out.push_back(out_of[q]);
+    U.unit_beg.push_back(pos);
+    for (int64_t c = 0; c < u.len; ++c) {
+      const int64_t e = a[u.beg + c];
+      U.y[pos + c] = yrow(e);
+      U.val[pos + c] = val[e];
+    }
+    rated += u.len;
+    pos += (u.len + kUnitAlign - 1) / kUnitAlign * kUnitAlign;
+  }
+  pad_to_wave(prev_cls < 0 ? 0 : prev_cls);
+  while (next_xcd < kXcds) U.xcd_off[next_xcd++] = static_cast<int64_t>(U.unit_x.size());
+  U.xcd_off[kXcds] = static_cast<int64_t>(U.unit_x.size());
+  U.nreal = nu;
 }
 
 // number of distinct (x, tile) runs for a tile function (entries sorted by x already)

@@ -9,7 +9,9 @@
 
 namespace psmf {
 
-constexpr int kXcds = 8;  // MI355X: 8 accelerator complex dies, each with its own L2
+constexpr int kXcds = 8;       // MI355X: 8 accelerator complex dies, each with its own L2
+constexpr int kUnitAlign = 8;  // a unit's ratings start at, and are padded to, a multiple of this
+constexpr int kWaveUnits = 32; // units of one wavefront (at most 32 lane groups) share a worker class
 
 // SplitMix64 (Steele, Lea & Flood 2014): one step of the sequential generator from
 // `state`.  Used for the minibatch block of a rating.
@@ -36,13 +38,14 @@ inline int32_t block_of(uint64_t seed, int32_t B, int64_t i, int64_t j) {
 // chunks of about equal rating count; chunk x runs on XCD x.  Each unit writes one
 // partial row; the partial rows of x are [x_pp[x], x_pp[x+1]).
 struct UnitSet {
-  std::vector<int32_t> y;         // gathered row of each rating, in unit order
-  std::vector<float> val;         // rating value, in unit order
+  std::vector<int32_t> y;         // gathered row of each rating, in unit order (padded)
+  std::vector<float> val;         // rating value, in unit order (padding: 0)
   std::vector<int32_t> unit_x, unit_cls, unit_len, unit_out;
   std::vector<int64_t> unit_beg;
   std::vector<int64_t> xcd_off;   // [kXcds + 1]
   std::vector<int64_t> x_pp;      // [rows of x + 1]
   int64_t ntiles = 0;
+  int64_t nreal = 0;              // units with ratings; empty padding units write partial row nreal
 };
 
 struct BlockLayout {

@@ -44,6 +44,10 @@ namespace {
 constexpr int kBlock = 256;  // threads per workgroup (4 wavefronts of 64)
 constexpr int kMaxKp = 512;
 constexpr int kXcds = psmf::kXcds;
+#ifndef PS_MF_ROWS_IN_FLIGHT
+#define PS_MF_ROWS_IN_FLIGHT 4
+#endif
+constexpr int kRowsInFlight = PS_MF_ROWS_IN_FLIGHT;  // gathered rows loaded before their use (divides 8)
 
 // ------------------------------------------------------------------ device helpers
 // A factor row of Kp = G*E floats is spread over a lane group of G lanes: lane g holds the
@@ -97,6 +101,7 @@ struct UnitArgs {
   const float *ring;
   int64_t slot_stride;      // floats per slot
   int64_t x_off, y_off;     // offsets of the stationary and the gathered table in a slot
+  int64_t y_bytes;          // bytes of the gathered table (< 2^32)
   float *partial;           // [units, Kp]
 };
 
@@ -109,43 +114,69 @@ __device__ __forceinline__ int64_t unit_of(const UnitArgs &a, int grp, int group
   return local < a.xcd_off[xcd + 1] - first ? first + local : -1;
 }
 
+// 32-bit-offset loads from one factor table through a buffer resource (CDNA word 3
+// 0x00020000: raw, untyped dword access); offsets past num_bytes read as zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t table_rsrc(const float *base, int64_t num_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), static_cast<short>(0),
+                                           static_cast<int>(static_cast<uint32_t>(num_bytes)), 0x00020000);
+}
+
+template <int G, int E>
+__device__ __forceinline__ void load_row_rsrc(float (&d)[E], __amdgpu_buffer_rsrc_t rs, uint32_t row_bytes, int g) {
+#pragma unroll
+  for (int q = 0; q < E / 4; ++q) {
+    const auto t = __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(row_bytes + 16u * (q * G + g)), 0, 0);
+    d[4 * q] = __uint_as_float(t[0]);
+    d[4 * q + 1] = __uint_as_float(t[1]);
+    d[4 * q + 2] = __uint_as_float(t[2]);
+    d[4 * q + 3] = __uint_as_float(t[3]);
+  }
+}
+
 // One lane group per work unit: acc = sum_t (val_t - x . Y_{y_t}) Y_{y_t} over the unit's
-// ratings, x the unit's stationary row, two gathered rows in flight; acc -> partial row.
+// ratings, x the unit's stationary row; acc -> the unit's partial row.  The unit's
+// (row, value) pairs are read 8 at a time with one 32-byte load per lane group (a unit
+// starts at a multiple of 8 entries and is padded to one); kRowsInFlight gathered rows
+// are loaded before they are used.
 template <int G, int E>
 __global__ __launch_bounds__(kBlock) void k_units(UnitArgs a) {
   constexpr int Kp = G * E;
   const int g = threadIdx.x & (G - 1);
   const int64_t unit = unit_of(a, threadIdx.x / G, kBlock / G);
   if (unit < 0) return;  // whole groups leave together
-  const int sv = a.cls_slot[a.unit_cls[unit]];
+  // every unit of a wavefront reads the same ring slot (the layout pads class changes to
+  // whole wavefronts), so the slot and the buffer resource are wave-uniform
+  const int sv = __builtin_amdgcn_readfirstlane(a.cls_slot[a.unit_cls[unit]]);
   const float *__restrict__ V = a.ring + sv * a.slot_stride;
-  const float *__restrict__ Y = V + a.y_off;
+  const __amdgpu_buffer_rsrc_t ys = table_rsrc(V + a.y_off, a.y_bytes);
   const int64_t beg = a.unit_beg[unit];
   const int n = a.unit_len[unit];
-  const int32_t *__restrict__ yi = a.y + beg;
-  const float *__restrict__ vr = a.val + beg;
+  const int4 *__restrict__ yi = reinterpret_cast<const int4 *>(a.y + beg);
+  const float4 *__restrict__ vr = reinterpret_cast<const float4 *>(a.val + beg);
   float x[E], acc[E];
   load_row<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
-  int t = 0;
-  for (; t + 1 < n; t += 2) {
-    const int64_t j0 = yi[t], j1 = yi[t + 1];
-    const float r0 = vr[t], r1 = vr[t + 1];
-    float y0[E], y1[E];
-    load_row<G, E>(y0, Y + j0 * Kp, g);
-    load_row<G, E>(y1, Y + j1 * Kp, g);
-    const float e0 = residual<G, E>(x, y0, r0);
-    const float e1 = residual<G, E>(x, y1, r1);
+  for (int t0 = 0; t0 < n; t0 += 8) {
+    const int4 i0 = yi[t0 / 4], i1 = yi[t0 / 4 + 1];
+    const float4 v0 = vr[t0 / 4], v1 = vr[t0 / 4 + 1];
+    const int idx[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+    const float val[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = fmaf(e1, y1[e], fmaf(e0, y0[e], acc[e]));
-  }
-  if (t < n) {
-    float y0[E];
-    load_row<G, E>(y0, Y + static_cast<int64_t>(yi[t]) * Kp, g);
-    const float e0 = residual<G, E>(x, y0, vr[t]);
+    for (int q = 0; q < 8; q += kRowsInFlight) {
+      if (t0 + q >= n) break;  // only padding left
+      float y[kRowsInFlight][E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = fmaf(e0, y0[e], acc[e]);
+      for (int w = 0; w < kRowsInFlight; ++w)
+        load_row_rsrc<G, E>(y[w], ys, static_cast<uint32_t>(idx[q + w]) * (Kp * 4u), g);
+#pragma unroll
+      for (int w = 0; w < kRowsInFlight; ++w) {
+        // padding entries (past the unit's n ratings) contribute nothing
+        const float err = (t0 + q + w < n) ? residual<G, E>(x, y[w], val[q + w]) : 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(err, y[w][e], acc[e]);
+      }
+    }
   }
   store_row<G, E>(a.partial + static_cast<int64_t>(a.unit_out[unit]) * Kp, acc, g);
 }
@@ -215,22 +246,34 @@ struct FinalArgs {
 
 // L^{c+1}_i = L^c_i + scale_i (sum of i's partial rows - n_i lambda L^v_i): the lambda term
 // of each of the n_i ratings is hoisted; scale = eta (SUM) or eta / n_i (ROWMEAN).  Users
-// without a rating in the block keep L^c_i (copied when the new slot differs).
+// without a rating in the block keep L^c_i (copied when the new slot differs).  One
+// thread per 4 columns.
 __global__ __launch_bounds__(kBlock) void k_finalize_users(FinalArgs a) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (idx >= a.users * a.Kp) return;
-  const int64_t i = idx / a.Kp, k = idx - i * a.Kp;
+  const int64_t q4 = a.Kp / 4;
+  if (idx >= a.users * q4) return;
+  const int64_t i = idx / q4;
   const int n = a.ucount[i];
+  float4 *ring4 = reinterpret_cast<float4 *>(a.ring);
+  const int64_t ss4 = a.slot_stride / 4;
   if (n == 0) {
-    if (a.slot_n != a.slot_c) a.ring[a.slot_n * a.slot_stride + idx] = a.ring[a.slot_c * a.slot_stride + idx];
+    if (a.slot_n != a.slot_c) ring4[a.slot_n * ss4 + idx] = ring4[a.slot_c * ss4 + idx];
     return;
   }
-  float d = 0.f;
-  for (int64_t p = a.user_pp[i]; p < a.user_pp[i + 1]; ++p) d += a.partial[p * a.Kp + k];
-  const float lc = a.ring[a.slot_c * a.slot_stride + idx];
-  const float lv = a.ring[a.cls_slot[a.ucls[i]] * a.slot_stride + idx];
+  const float4 *part4 = reinterpret_cast<const float4 *>(a.partial);
+  const int64_t k4 = idx - i * q4;
+  float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+  for (int64_t p = a.user_pp[i]; p < a.user_pp[i + 1]; ++p) {
+    const float4 t = part4[p * q4 + k4];
+    d.x += t.x; d.y += t.y; d.z += t.z; d.w += t.w;
+  }
+  const float4 lc = ring4[a.slot_c * ss4 + idx];
+  const float4 lv = ring4[a.cls_slot[a.ucls[i]] * ss4 + idx];
   const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
-  a.ring[a.slot_n * a.slot_stride + idx] = lc + sc * (d - static_cast<float>(n) * a.lambda * lv);
+  const float nl = static_cast<float>(n) * a.lambda;
+  ring4[a.slot_n * ss4 + idx] = make_float4(lc.x + sc * (d.x - nl * lv.x), lc.y + sc * (d.y - nl * lv.y),
+                                            lc.z + sc * (d.z - nl * lv.z), lc.w + sc * (d.w - nl * lv.w));
 }
 
 struct CommitArgs {
@@ -249,27 +292,41 @@ struct CommitArgs {
   int32_t rowmean;
 };
 
-// R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class n_j^(class) R^{v(class)}_j)
+// R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class n_j^(class) R^{v(class)}_j).
+// One thread per 4 columns.
 __global__ __launch_bounds__(kBlock) void k_commit(CommitArgs a) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (idx >= a.items * a.Kp) return;
-  const int64_t j = idx / a.Kp, k = idx - j * a.Kp;
+  const int64_t q4 = a.Kp / 4;
+  if (idx >= a.items * q4) return;
+  const int64_t j = idx / q4;
   const int n = a.icount[j];
-  float *R = a.ring + a.r_off;
-  const float rc = R[a.slot_c * a.slot_stride + idx];
-  float out = rc;
+  float4 *R4 = reinterpret_cast<float4 *>(a.ring + a.r_off);
+  const int64_t ss4 = a.slot_stride / 4;
+  const float4 rc = R4[a.slot_c * ss4 + idx];
+  float4 out = rc;
   if (n > 0) {
-    float d = 0.f;
-    for (int64_t p = a.item_pp[j]; p < a.item_pp[j + 1]; ++p) d += a.partial[p * a.Kp + k];
-    float lam = 0.f;
+    const float4 *part4 = reinterpret_cast<const float4 *>(a.partial);
+    const int64_t k4 = idx - j * q4;
+    float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+    for (int64_t p = a.item_pp[j]; p < a.item_pp[j + 1]; ++p) {
+      const float4 t = part4[p * q4 + k4];
+      d.x += t.x; d.y += t.y; d.z += t.z; d.w += t.w;
+    }
+    float4 lam = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int q = 0; q < a.nclass; ++q) {
       const int cnt = a.icount_cls[j * a.nclass + q];
-      if (cnt) lam = fmaf(static_cast<float>(cnt), R[a.cls_slot[q] * a.slot_stride + idx], lam);
+      if (cnt) {
+        const float c = static_cast<float>(cnt);
+        const float4 r = R4[a.cls_slot[q] * ss4 + idx];
+        lam = make_float4(fmaf(c, r.x, lam.x), fmaf(c, r.y, lam.y), fmaf(c, r.z, lam.z), fmaf(c, r.w, lam.w));
+      }
     }
     const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
-    out = rc + sc * (d - a.lambda * lam);
+    out = make_float4(rc.x + sc * (d.x - a.lambda * lam.x), rc.y + sc * (d.y - a.lambda * lam.y),
+                      rc.z + sc * (d.z - a.lambda * lam.z), rc.w + sc * (d.w - a.lambda * lam.w));
   }
-  R[a.slot_n * a.slot_stride + idx] = out;
+  R4[a.slot_n * ss4 + idx] = out;
 }
 
 // ------------------------------------------------------------------ kernel dispatch on Kp
@@ -327,7 +384,8 @@ struct LaunchLoss {
 
 // ------------------------------------------------------------------ handle
 struct DeviceUnits {
-  int64_t nunits = 0, grid = 0;  // grid: workgroups of a launch (kXcds x the largest chunk)
+  int64_t nunits = 0;  // units with ratings (the padding units come after them in the chunks)
+  int64_t grid = 0;    // workgroups of a launch: kXcds x the largest chunk
   int32_t *y = nullptr;
   float *val = nullptr;
   int32_t *unit_x = nullptr, *unit_cls = nullptr, *unit_len = nullptr, *unit_out = nullptr;
@@ -436,7 +494,7 @@ int upload_units(ps_mf_t *h, DeviceUnits &d, const psmf::UnitSet &u) {
       (r = upload(h, &d.unit_out, u.unit_out)) || (r = upload(h, &d.unit_beg, u.unit_beg)) ||
       (r = upload(h, &d.xcd_off, u.xcd_off)) || (r = upload(h, &d.x_pp, u.x_pp)))
     return r;
-  d.nunits = static_cast<int64_t>(u.unit_x.size());
+  d.nunits = u.nreal;
   int64_t most = 0;
   for (int x = 0; x < kXcds; ++x) most = std::max<int64_t>(most, u.xcd_off[x + 1] - u.xcd_off[x]);
   const int groups = kBlock / shape_for(h->Kp).G;
@@ -444,7 +502,8 @@ int upload_units(ps_mf_t *h, DeviceUnits &d, const psmf::UnitSet &u) {
   return PS_MF_OK;
 }
 
-UnitArgs unit_args(const ps_mf_t *h, const DeviceUnits &d, float *partial, int64_t x_off, int64_t y_off) {
+UnitArgs unit_args(const ps_mf_t *h, const DeviceUnits &d, float *partial, int64_t x_off, int64_t y_off,
+                   int64_t y_rows) {
   UnitArgs a{};
   a.unit_x = d.unit_x;
   a.unit_cls = d.unit_cls;
@@ -458,6 +517,7 @@ UnitArgs unit_args(const ps_mf_t *h, const DeviceUnits &d, float *partial, int64
   a.slot_stride = (h->N + h->M) * h->Kp;
   a.x_off = x_off;
   a.y_off = y_off;
+  a.y_bytes = y_rows * h->Kp * 4;
   a.partial = partial;
   return a;
 }
@@ -533,12 +593,12 @@ int one_clock(ps_mf_t *h) {
   int rc = record(h, &ev);
   if (rc) return rc;
   if (db.by_item.nunits > 0) {  // x = item (R), y = user (L)
-    UnitArgs a = unit_args(h, db.by_item, h->partial_i, r_off, 0);
+    UnitArgs a = unit_args(h, db.by_item, h->partial_i, r_off, 0, h->N);
     a.cls_slot = cls_slot;
     HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, a, db.by_item.grid, h->stream));
   }
   if (db.by_user.nunits > 0) {  // x = user (L), y = item (R)
-    UnitArgs a = unit_args(h, db.by_user, h->partial_u, 0, r_off);
+    UnitArgs a = unit_args(h, db.by_user, h->partial_u, 0, r_off, h->M);
     a.cls_slot = cls_slot;
     HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, a, db.by_user.grid, h->stream));
   }
@@ -560,7 +620,7 @@ int one_clock(ps_mf_t *h) {
   fa.eta = h->eta;
   fa.lambda = h->lambda;
   fa.rowmean = rowmean;
-  const int64_t nfin = h->N * h->Kp;
+  const int64_t nfin = h->N * h->Kp / 4;
   hipLaunchKernelGGL(k_finalize_users, dim3(static_cast<unsigned>((nfin + kBlock - 1) / kBlock)), dim3(kBlock), 0,
                      h->stream, fa);
   HIP_TRY(h, hipGetLastError());
@@ -581,7 +641,7 @@ int one_clock(ps_mf_t *h) {
   ca.eta = h->eta;
   ca.lambda = h->lambda;
   ca.rowmean = rowmean;
-  const int64_t ncommit = h->M * h->Kp;
+  const int64_t ncommit = h->M * h->Kp / 4;
   hipLaunchKernelGGL(k_commit, dim3(static_cast<unsigned>((ncommit + kBlock - 1) / kBlock)), dim3(kBlock), 0,
                      h->stream, ca);
   HIP_TRY(h, hipGetLastError());
@@ -603,6 +663,9 @@ int ps_mf_create(int64_t users, int64_t items, int32_t K, int32_t P, int32_t s, 
   *out = nullptr;
   if (users < 1 || items < 1 || users > 0x7fffffff || items > 0x7fffffff) return PS_MF_EINVAL;
   if (K < 1 || K > kMaxKp || P < 1 || P > 65536 || s < 0 || s > 1024) return PS_MF_EINVAL;
+  // the sweeps address one factor table with 32-bit byte offsets
+  if (users * padded_k(K) * 4 >= (int64_t(1) << 32) || items * padded_k(K) * 4 >= (int64_t(1) << 32))
+    return PS_MF_EINVAL;
   if (!std::isfinite(eta) || !std::isfinite(lambda)) return PS_MF_EINVAL;
   ps_mf_t *h = new (std::nothrow) ps_mf_t();
   if (!h) return PS_MF_ENOMEM;
@@ -728,8 +791,8 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
         (r = upload(h, &d.icount_cls, L.icount_cls)) || (r = upload_units(h, d.by_user, L.by_user)) ||
         (r = upload_units(h, d.by_item, L.by_item)))
       return undo(r);
-    max_units_u = std::max<int64_t>(max_units_u, d.by_user.nunits);
-    max_units_i = std::max<int64_t>(max_units_i, d.by_item.nunits);
+    max_units_u = std::max<int64_t>(max_units_u, d.by_user.nunits + 1);  // + the padding units' row
+    max_units_i = std::max<int64_t>(max_units_i, d.by_item.nunits + 1);
     loss_len += d.by_user.grid;
   }
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->partial_u), static_cast<size_t>(max_units_u * h->Kp) * sizeof(float))) ||
@@ -805,7 +868,7 @@ int ps_mf_loss(ps_mf_t *h, double *out) {
   for (int b = 0; b < h->B; ++b) {
     const DeviceBlock &d = h->dblocks[b];
     if (d.by_user.nunits == 0) continue;
-    UnitArgs ua = unit_args(h, d.by_user, nullptr, 0, h->N * h->Kp);
+    UnitArgs ua = unit_args(h, d.by_user, nullptr, 0, h->N * h->Kp, h->M);
     HIP_TRY(h, dispatch<LaunchLoss>(h->Kp, ua, sl, d.by_user.grid, h->loss_partial + off, h->stream));
     off += d.by_user.grid;
   }
