@@ -43,6 +43,11 @@ def parse():
     ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
     ap.add_argument("--tile-bytes", type=int, default=None, help="bytes of rows per L2 tile of the sweeps")
     ap.add_argument("--unit-max", type=int, default=None, help="ratings per sweep work unit")
+    ap.add_argument("--copy-calibration-bytes", type=int, default=0,
+                    help="run one plain copy kernel (y = x * 2) of this many bytes before timing, for "
+                         "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE")
+    ap.add_argument("--traffic-file", default=os.path.join(ROOT, "profiles", "k_units_full_traffic.json"),
+                    help="measured HBM traffic of the sweep (used while the kernel source is unchanged)")
     return ap.parse_args()
 
 
@@ -64,6 +69,23 @@ def cpu_baseline(w, spec, K, s, policy, nsample):
             "sample": f"one clock over the {len(take)} ratings of users {int(u.min())}..{int(u.max())} "
                       f"(users in id order) of the same workload, {dt:.1f} s on "
                       f"{platform.processor() or platform.machine()}, 1 thread"}
+
+
+def measured_traffic(path, config, s, policy):
+    """HBM bytes per clock of the sweep from committed rocprofv3 counter runs, or None when
+    they are missing, were taken on another workload, or the kernel source has changed."""
+    from paper_1410_8043_amd import rocprof_summary
+
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != rocprof_summary.kernel_source_sha256():
+        return None
+    if t.get("workload") != {"config": config, "s": s, "policy": policy}:
+        return None
+    return round(t["traffic_bytes_per_clock"])
 
 
 def main():
@@ -95,6 +117,12 @@ def main():
     print(f"[bench] layout + upload {t_load:.1f} s", file=sys.stderr, flush=True)
     nnz_clock = w.nnz / spec.B  # mean ratings per clock (exact for B=1)
 
+    if args.copy_calibration_bytes > 0:
+        src = torch.ones(args.copy_calibration_bytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.mul(src, 2.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     g.clock(args.warmup)
     torch.cuda.synchronize()
     if not args.no_timing:
@@ -120,7 +148,8 @@ def main():
         flops = 6.0 * K * nnz_clock                  # 3K fp32 FMA per rating update
         achieved = flops / (sweep_ms * 1e-3) / 1e12  # TFLOP/s
         roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4),
+                "traffic": measured_traffic(args.traffic_file, args.config, s, args.policy)}
         # compulsory HBM bytes of one clock: each rating once (int32 item + fp32 value),
         # the view version read, the base version read when s > 0, the new version written
         table = (spec.N + spec.M) * K * 4

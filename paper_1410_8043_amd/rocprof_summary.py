@@ -1,0 +1,147 @@
+"""Summaries of rocprofv3 result databases for the ps_mf kernels.
+
+    python -m paper_1410_8043_amd.rocprof_summary stats <dir>
+        per-kernel calls, total and average duration from a --kernel-trace --stats run;
+    python -m paper_1410_8043_amd.rocprof_summary counters <dir> [<dir> ...]
+        per-kernel counter values (sum over a dispatch's dimensions) of --pmc runs;
+    python -m paper_1410_8043_amd.rocprof_summary traffic --fetch <dir> --write <dir> \
+            --copy-bytes N --out profiles/<name>.json
+        HBM bytes per clock of the sweep kernel from one FETCH_SIZE and one WRITE_SIZE run,
+        scaled by what the same counters read for a plain copy kernel (torch's elementwise
+        y = x * 2 over N bytes), written as JSON next to the sha256 of the kernel
+        source, so that bench.py reports it only while the kernel is unchanged.
+
+Each input directory is the -d directory of one rocprofv3 run (the *_results.db file
+is found below it).
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import glob
+import hashlib
+import json
+import os
+import sqlite3
+import sys
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCE = os.path.join(_HERE, "csrc", "ps_mf.hip")
+SWEEP_KERNEL = "k_units"
+
+
+def kernel_source_sha256() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def _db(d: str) -> sqlite3.Connection:
+    found = sorted(glob.glob(os.path.join(d, "**", "*results.db"), recursive=True))
+    if not found:
+        raise FileNotFoundError(f"no rocprofv3 results database under {d}")
+    return sqlite3.connect(found[-1])
+
+
+def short_name(kernel_name: str) -> str:
+    name = kernel_name.replace("(anonymous namespace)::", "")
+    if name.startswith("void "):
+        name = name[5:]
+    return name.split("(")[0].strip()
+
+
+def stats(d: str):
+    con = _db(d)
+    rows = con.execute("select name, total_calls, total_duration, average, percentage from top_kernels").fetchall()
+    # the top_kernels view reports microseconds
+    return [(short_name(n), int(c), tot / 1e3, avg / 1e3, pct) for n, c, tot, avg, pct in rows]
+
+
+def counters(d: str):
+    """{(kernel, counter): [value per dispatch, in dispatch order]}"""
+    con = _db(d)
+    rows = con.execute("select dispatch_id, kernel_name, counter_name, sum(value) from counters_collection "
+                       "group by dispatch_id, counter_name order by dispatch_id").fetchall()
+    out = collections.defaultdict(list)
+    for _, kname, cname, val in rows:
+        out[(kname, cname)].append(val)
+    return out
+
+
+def _find(cnt, kernel_prefix: str, counter: str):
+    for (k, c), v in cnt.items():
+        if c == counter and short_name(k).startswith(kernel_prefix):
+            return v
+    raise KeyError(f"{counter} of {kernel_prefix} not found")
+
+
+COPY_KERNEL = "MulFunctor"  # torch's elementwise y = x * 2 (reads and writes copy_bytes)
+
+
+def _copy_value(cnt, counter: str) -> float:
+    for (k, c), v in cnt.items():
+        if c == counter and COPY_KERNEL in k:
+            return max(v)
+    raise KeyError(f"{counter} of the calibration copy kernel not found")
+
+
+def traffic(fetch_dir: str, write_dir: str, copy_bytes: int, launches_per_clock: int = 2):
+    """HBM bytes per clock of the sweep (its launches of one clock summed), calibrated."""
+    f, w = counters(fetch_dir), counters(write_dir)
+    copy_f = _copy_value(f, "FETCH_SIZE")
+    copy_w = _copy_value(w, "WRITE_SIZE")
+    fetch_scale = copy_bytes / (copy_f * 1024.0)
+    write_scale = copy_bytes / (copy_w * 1024.0)
+    sf = _find(f, SWEEP_KERNEL, "FETCH_SIZE")
+    sw = _find(w, SWEEP_KERNEL, "WRITE_SIZE")
+    clocks = len(sf) // launches_per_clock
+    fetch = sum(sf[: clocks * launches_per_clock]) * 1024.0 * fetch_scale / clocks
+    write = sum(sw[: clocks * launches_per_clock]) * 1024.0 * write_scale / clocks
+    return {
+        "kernel": SWEEP_KERNEL,
+        "launches_per_clock": launches_per_clock,
+        "fetch_bytes_per_clock": fetch,
+        "write_bytes_per_clock": write,
+        "traffic_bytes_per_clock": fetch + write,
+        "copy_calibration": {"bytes": copy_bytes, "fetch_kib": copy_f, "write_kib": copy_w,
+                             "fetch_scale": fetch_scale, "write_scale": write_scale},
+        "per_launch_fetch_kib": sf,
+        "per_launch_write_kib": sw,
+        "kernel_source_sha256": kernel_source_sha256(),
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    a = sub.add_parser("stats")
+    a.add_argument("dir")
+    b = sub.add_parser("counters")
+    b.add_argument("dirs", nargs="+")
+    c = sub.add_parser("traffic")
+    c.add_argument("--fetch", required=True)
+    c.add_argument("--write", required=True)
+    c.add_argument("--copy-bytes", type=int, required=True)
+    c.add_argument("--out", required=True)
+    c.add_argument("--command", default="")
+    c.add_argument("--config", default="full")
+    c.add_argument("--s", type=int, default=3)
+    c.add_argument("--policy", default="lazy")
+    args = ap.parse_args(argv)
+    if args.cmd == "stats":
+        for name, calls, tot, avg, pct in stats(args.dir):
+            print(f"{calls:6d} calls  total {tot:10.3f} ms  avg {avg:9.4f} ms  {pct:5.1f}%  {name}")
+    elif args.cmd == "counters":
+        for d in args.dirs:
+            for (k, cname), vals in sorted(counters(d).items()):
+                print(f"{short_name(k)[:48]:48s} {cname:18s} " + " ".join(f"{v:.5g}" for v in vals[:8]))
+    else:
+        t = traffic(args.fetch, args.write, args.copy_bytes)
+        t["command"] = args.command
+        t["workload"] = {"config": args.config, "s": args.s, "policy": args.policy}
+        with open(args.out, "w") as f:
+            json.dump(t, f, indent=1)
+        print(json.dumps({k: v for k, v in t.items() if not k.startswith("per_launch")}, indent=1))
+
+
+if __name__ == "__main__":
+    sys.exit(main())
