@@ -43,10 +43,13 @@ def parse():
     ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
     ap.add_argument("--tile-bytes", type=int, default=None, help="bytes of rows per L2 tile of the sweeps")
     ap.add_argument("--unit-max", type=int, default=None, help="ratings per sweep work unit")
+    ap.add_argument("--cells", type=int, default=None, help="1/0: LDS-staged cells for the dense part")
+    ap.add_argument("--heavy-min", type=int, default=None, help="ratings from which a user goes to the cells")
+    ap.add_argument("--two-streams", type=int, default=None, help="1/0: units on a second stream beside the cells")
     ap.add_argument("--copy-calibration-bytes", type=int, default=0,
                     help="run one plain copy kernel (y = x * 2) of this many bytes before timing, for "
                          "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE")
-    ap.add_argument("--traffic-file", default=os.path.join(ROOT, "profiles", "k_units_full_traffic.json"),
+    ap.add_argument("--traffic-file", default=os.path.join(ROOT, "profiles", "k_sweep_full_traffic.json"),
                     help="measured HBM traffic of the sweep (used while the kernel source is unchanged)")
     return ap.parse_args()
 
@@ -109,7 +112,8 @@ def main():
     stream = torch.cuda.current_stream()
     g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, B=spec.B,
                    mb_seed=spec.seed, timing=not args.no_timing, stream=stream, tile_bytes=args.tile_bytes,
-                   unit_max=args.unit_max)
+                   unit_max=args.unit_max, cells=args.cells, heavy_min=args.heavy_min,
+                   two_streams=args.two_streams)
     t_load = time.perf_counter()
     g.load_ratings(w.user, w.item, w.val)
     g.set_factors(w.L0, w.R0)

@@ -68,7 +68,13 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_OPT_TIMING 6    /* 1: record HIP events around every kernel (ps_mf_kernel_time) */
 #define PS_MF_OPT_TILE_BYTES 7 /* bytes of user rows per tile of the item-major sweep (default 3 MiB,
                                   sized to one XCD's 4 MiB L2); >= 1 */
-#define PS_MF_OPT_UNIT_MAX 8   /* ratings per item-major work unit (default 1024); >= 1 */
+#define PS_MF_OPT_UNIT_MAX 8   /* ratings per sweep work unit (default 1024); >= 1 */
+#define PS_MF_OPT_CELLS 9      /* 1 (default): sweep the dense part (users with many ratings) through
+                                  LDS-staged cells; 0: every rating through the L2 work units */
+#define PS_MF_OPT_HEAVY_MIN 10 /* ratings in a block from which a user's ratings go to the cells;
+                                  -1 (default): 16 x items / LDS sub-tile rows, at least 256 */
+#define PS_MF_OPT_TWO_STREAMS 11 /* 1 (default): run the L2 work units on a second, internal stream
+                                    (default priority) beside the cells; 0: one stream */
 
 #define PS_MF_SSP_LAZY 0
 #define PS_MF_SSP_WORST 1

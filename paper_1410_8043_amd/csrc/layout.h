@@ -48,6 +48,30 @@ struct UnitSet {
   int64_t nreal = 0;              // units with ratings; empty padding units write partial row nreal
 };
 
+// The dense part of one sweep direction, staged through LDS.  A cell is one workgroup:
+// ng stationary rows x (one per lane group, -1 = unused) of one worker class, and a
+// sequence of steps; a step is a sub-tile of ts gathered rows that the workgroup copies
+// into LDS before every lane group sweeps its row's ratings inside the sub-tile:
+//   user-major: x = heavy users of one class (similar degree), steps = item ranges;
+//   item-major: x = items (similar heavy-rater count), steps = ranges of the class's
+//               heavy users.
+// The ratings of (cell, k-th step, group) are ly/lv[run_beg .. run_beg + run_len): ly the
+// row's position inside the sub-tile.  Runs start at multiples of kUnitAlign and are
+// padded to one.  Each used (cell, group) writes one partial row cell_out.
+struct CellSet {
+  int32_t ts = 0, ng = 0;
+  std::vector<int32_t> step_rows;      // [nsteps * ts], -1 = no row
+  std::vector<int32_t> cell_x;         // [ncells * ng]
+  std::vector<int32_t> cell_cls;       // [ncells]
+  std::vector<int32_t> cell_step_ptr;  // [ncells + 1] into cell_steps
+  std::vector<int32_t> cell_steps;     // step ids
+  std::vector<int32_t> run_beg, run_len;  // [cell_steps.size() * ng]
+  std::vector<int32_t> cell_out;       // [ncells * ng], -1 for unused groups
+  std::vector<uint16_t> ly;
+  std::vector<float> lv;
+  int64_t nnz = 0;                     // ratings covered by the cells
+};
+
 struct BlockLayout {
   int64_t nnz = 0;
   // ratings of the block in canonical (user, item, load index) order
@@ -59,6 +83,8 @@ struct BlockLayout {
   std::vector<int32_t> icount;   // [items]
   std::vector<int32_t> icount_cls;  // [items * nclass]: raters of the item per worker class
   UnitSet by_user, by_item;
+  CellSet cells_user, cells_item;
+  int64_t partial_rows_user = 0, partial_rows_item = 0;  // rows of x_pp (units and cells)
 };
 
 struct LayoutParams {
@@ -72,6 +98,10 @@ struct LayoutParams {
   int64_t tile_rows_item = 1 << 30; // items per tile of the user-major sweep
   int64_t tile_rows_user = 1 << 30; // users per tile of the item-major sweep
   int32_t unit_max = 1024;          // ratings per work unit
+  int32_t cell_rows = 0;            // ts: gathered rows per LDS sub-tile (0: no cells)
+  int32_t cell_groups = 0;          // ng: lane groups per cell workgroup
+  int64_t heavy_min = 1 << 30;      // users with at least this many ratings in the block go to cells
+  int32_t cell_target = 1024;       // about this many user-major cells in total
 };
 
 // Validates the COO input (EINVAL message in err) and fills one BlockLayout per block.

@@ -17,10 +17,10 @@
 // Neither sweep uses atomics: a unit keeps one row (the stationary side) in registers,
 // gathers the other side's rows from a tile that stays in one XCD's L2, recomputes the
 // residual e = D_ij - L^v_i . R^v_j and writes one partial row.
-//   sweep (item-major units, then user-major units);
-//   finalize : L^{c+1}_i = L^c_i + scale_i (sum of i's partial rows - n_i lambda L^v_i),
-//              users without a rating in the block keep L^c_i;
-//   commit   : R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class
+//   sweep    : the item-major and the user-major units in one launch;
+//   commit   : in one launch, L^{c+1}_i = L^c_i + scale_i (sum of i's partial rows -
+//              n_i lambda L^v_i) (users without a rating in the block keep L^c_i) and
+//              R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class
 //              n_j^(class) R^{v(class)}_j).
 // Both sweeps read versions <= c only; finalize and commit write version c+1 into the
 // slot that held version c-s, after both sweeps are done with it.
@@ -41,13 +41,20 @@
 
 namespace {
 
-constexpr int kBlock = 256;  // threads per workgroup (4 wavefronts of 64)
+constexpr int kBlock = 256;       // threads per workgroup of the small kernels (4 wavefronts)
+constexpr int kSweepBlock = 1024; // threads per workgroup of the sweep (16 wavefronts: one per CU)
+constexpr int kTileFloats = 32768; // LDS sub-tile of a cell: 128 KiB = ts rows of Kp floats
+constexpr int kLossSegment = 512;  // ratings per lane group of the loss
 constexpr int kMaxKp = 512;
 constexpr int kXcds = psmf::kXcds;
 #ifndef PS_MF_ROWS_IN_FLIGHT
 #define PS_MF_ROWS_IN_FLIGHT 4
 #endif
 constexpr int kRowsInFlight = PS_MF_ROWS_IN_FLIGHT;  // gathered rows loaded before their use (divides 8)
+// rows in flight for E floats per lane: the 512-wide rows keep one (registers are capped
+// at 128 per lane with 16 wavefronts per CU)
+template <int E>
+constexpr int rows_in_flight() { return E >= 32 ? 1 : kRowsInFlight; }
 
 // ------------------------------------------------------------------ device helpers
 // A factor row of Kp = G*E floats is spread over a lane group of G lanes: lane g holds the
@@ -68,6 +75,9 @@ __device__ __forceinline__ void store_row(float *__restrict__ row, const float (
   for (int q = 0; q < E / 4; ++q)
     *reinterpret_cast<float4 *>(row + 4 * (q * G + g)) = make_float4(d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]);
 }
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 // Sum over the G lanes of an aligned lane group with DPP moves inside a 16-lane row:
 // quad_perm [1,0,3,2] (xor 1), quad_perm [2,3,0,1] (xor 2), row_half_mirror (the other
@@ -105,11 +115,12 @@ struct UnitArgs {
   float *partial;           // [units, Kp]
 };
 
-// The unit processed by lane group `grp` of this workgroup: workgroup b runs on XCD
-// b mod 8 and takes the units of that XCD's chunk; -1 if there is none.
-__device__ __forceinline__ int64_t unit_of(const UnitArgs &a, int grp, int groups_per_wg) {
-  const int xcd = blockIdx.x % kXcds;
-  const int64_t local = static_cast<int64_t>(blockIdx.x / kXcds) * groups_per_wg + grp;
+// The unit processed by lane group `grp` of workgroup `block` (counted within its sweep;
+// the first sweep's grid is a multiple of 8, so workgroup b of either sweep runs on XCD
+// b mod 8) takes the units of that XCD's chunk; -1 if there is none.
+__device__ __forceinline__ int64_t unit_of(const UnitArgs &a, int block, int grp, int groups_per_wg) {
+  const int xcd = block % kXcds;
+  const int64_t local = static_cast<int64_t>(block / kXcds) * groups_per_wg + grp;
   const int64_t first = a.xcd_off[xcd];
   return local < a.xcd_off[xcd + 1] - first ? first + local : -1;
 }
@@ -139,11 +150,9 @@ __device__ __forceinline__ void load_row_rsrc(float (&d)[E], __amdgpu_buffer_rsr
 // starts at a multiple of 8 entries and is padded to one); kRowsInFlight gathered rows
 // are loaded before they are used.
 template <int G, int E>
-__global__ __launch_bounds__(kBlock) void k_units(UnitArgs a) {
+__device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g) {
   constexpr int Kp = G * E;
-  const int g = threadIdx.x & (G - 1);
-  const int64_t unit = unit_of(a, threadIdx.x / G, kBlock / G);
-  if (unit < 0) return;  // whole groups leave together
+  constexpr int RF = rows_in_flight<E>();
   // every unit of a wavefront reads the same ring slot (the layout pads class changes to
   // whole wavefronts), so the slot and the buffer resource are wave-uniform
   const int sv = __builtin_amdgcn_readfirstlane(a.cls_slot[a.unit_cls[unit]]);
@@ -151,26 +160,26 @@ __global__ __launch_bounds__(kBlock) void k_units(UnitArgs a) {
   const __amdgpu_buffer_rsrc_t ys = table_rsrc(V + a.y_off, a.y_bytes);
   const int64_t beg = a.unit_beg[unit];
   const int n = a.unit_len[unit];
-  const int4 *__restrict__ yi = reinterpret_cast<const int4 *>(a.y + beg);
-  const float4 *__restrict__ vr = reinterpret_cast<const float4 *>(a.val + beg);
+  const i32x4 *__restrict__ yi = reinterpret_cast<const i32x4 *>(a.y + beg);
+  const f32x4 *__restrict__ vr = reinterpret_cast<const f32x4 *>(a.val + beg);
   float x[E], acc[E];
   load_row<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
   for (int t0 = 0; t0 < n; t0 += 8) {
-    const int4 i0 = yi[t0 / 4], i1 = yi[t0 / 4 + 1];
-    const float4 v0 = vr[t0 / 4], v1 = vr[t0 / 4 + 1];
-    const int idx[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
-    const float val[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    const i32x4 i0 = yi[t0 / 4], i1 = yi[t0 / 4 + 1];
+    const f32x4 v0 = vr[t0 / 4], v1 = vr[t0 / 4 + 1];
+    const int idx[8] = {i0[0], i0[1], i0[2], i0[3], i1[0], i1[1], i1[2], i1[3]};
+    const float val[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
 #pragma unroll
-    for (int q = 0; q < 8; q += kRowsInFlight) {
+    for (int q = 0; q < 8; q += RF) {
       if (t0 + q >= n) break;  // only padding left
-      float y[kRowsInFlight][E];
+      float y[RF][E];
 #pragma unroll
-      for (int w = 0; w < kRowsInFlight; ++w)
+      for (int w = 0; w < RF; ++w)
         load_row_rsrc<G, E>(y[w], ys, static_cast<uint32_t>(idx[q + w]) * (Kp * 4u), g);
 #pragma unroll
-      for (int w = 0; w < kRowsInFlight; ++w) {
+      for (int w = 0; w < RF; ++w) {
         // padding entries (past the unit's n ratings) contribute nothing
         const float err = (t0 + q + w < n) ? residual<G, E>(x, y[w], val[q + w]) : 0.f;
 #pragma unroll
@@ -181,27 +190,141 @@ __global__ __launch_bounds__(kBlock) void k_units(UnitArgs a) {
   store_row<G, E>(a.partial + static_cast<int64_t>(a.unit_out[unit]) * Kp, acc, g);
 }
 
-// Squared loss over the user-major units of a block at one ring slot: e in fp32, e^2
-// accumulated in fp64, one partial per workgroup (fixed order: deterministic).
+struct CellArgs {
+  const int32_t *step_rows;      // [nsteps * ts]
+  const int32_t *cell_x, *cell_cls, *cell_step_ptr, *cell_steps, *run_beg, *run_len, *cell_out;
+  const uint16_t *ly;
+  const float *lv;
+  const int32_t *cls_slot;
+  const float *ring;
+  int64_t slot_stride, x_off, y_off;
+  int32_t ts;
+  float *partial;
+};
+
+// One cell per workgroup: lane group q keeps the stationary row x_q in registers; for each
+// step the workgroup copies the step's ts gathered rows into LDS, then every lane group
+// sweeps its row's ratings inside the sub-tile (rows read from LDS).  The partial row of
+// each used group is written at the end.
 template <int G, int E>
-__global__ __launch_bounds__(kBlock) void k_loss(UnitArgs a, int32_t slot, double *__restrict__ out) {
+__device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4 *tile) {
+  constexpr int Kp = G * E;
+  constexpr int RF = rows_in_flight<E>();
+  constexpr int NG = kSweepBlock / G;
+  constexpr int Q4 = Kp / 4;  // float4 per row
+  const int g = threadIdx.x & (G - 1);
+  const int grp = threadIdx.x / G;
+  const int sv = c.cls_slot[c.cell_cls[cell]];  // one class per cell: uniform
+  const float *__restrict__ V = c.ring + sv * c.slot_stride;
+  const float4 *__restrict__ Y4 = reinterpret_cast<const float4 *>(V + c.y_off);
+  const int32_t xr = c.cell_x[cell * NG + grp];
+  float x[E], acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) { x[e] = 0.f; acc[e] = 0.f; }
+  if (xr >= 0) load_row<G, E>(x, V + c.x_off + static_cast<int64_t>(xr) * Kp, g);
+  const int32_t k0 = c.cell_step_ptr[cell], k1 = c.cell_step_ptr[cell + 1];
+  for (int32_t k = k0; k < k1; ++k) {
+    const int32_t *rows = c.step_rows + static_cast<int64_t>(c.cell_steps[k]) * c.ts;
+    __syncthreads();  // the previous sub-tile is no longer read
+    for (int idx = threadIdx.x; idx < c.ts * Q4; idx += kSweepBlock) {
+      const int32_t r = rows[idx / Q4];
+      tile[idx] = r >= 0 ? Y4[static_cast<int64_t>(r) * Q4 + idx % Q4] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    __syncthreads();
+    const int32_t beg = c.run_beg[static_cast<int64_t>(k) * NG + grp];
+    const int n = c.run_len[static_cast<int64_t>(k) * NG + grp];
+    const uint16_t *__restrict__ li = c.ly + beg;
+    const float *__restrict__ lv = c.lv + beg;
+    for (int t0 = 0; t0 < n; t0 += 8) {
+      const uint4 i8 = *reinterpret_cast<const uint4 *>(li + t0);  // 8 x uint16
+      const f32x4 v0 = *reinterpret_cast<const f32x4 *>(lv + t0), v1 = *reinterpret_cast<const f32x4 *>(lv + t0 + 4);
+      const int idx[8] = {static_cast<int>(i8.x & 0xffff), static_cast<int>(i8.x >> 16),
+                          static_cast<int>(i8.y & 0xffff), static_cast<int>(i8.y >> 16),
+                          static_cast<int>(i8.z & 0xffff), static_cast<int>(i8.z >> 16),
+                          static_cast<int>(i8.w & 0xffff), static_cast<int>(i8.w >> 16)};
+      const float val[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+#pragma unroll
+      for (int q = 0; q < 8; q += RF) {
+        if (t0 + q >= n) break;
+        float y[RF][E];
+#pragma unroll
+        for (int w = 0; w < RF; ++w) {
+#pragma unroll
+          for (int h = 0; h < E / 4; ++h) {
+            const float4 tt = tile[idx[q + w] * Q4 + h * G + g];
+            y[w][4 * h] = tt.x; y[w][4 * h + 1] = tt.y; y[w][4 * h + 2] = tt.z; y[w][4 * h + 3] = tt.w;
+          }
+        }
+#pragma unroll
+        for (int w = 0; w < RF; ++w) {
+          const float err = (t0 + q + w < n) ? residual<G, E>(x, y[w], val[q + w]) : 0.f;
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[e] = fmaf(err, y[w][e], acc[e]);
+        }
+      }
+    }
+  }
+  const int32_t out = c.cell_out[cell * NG + grp];
+  if (out >= 0) store_row<G, E>(c.partial + static_cast<int64_t>(out) * Kp, acc, g);
+}
+
+// The LDS-staged cells of both sweep directions in one launch (one 1024-thread workgroup
+// per cell): workgroups [0, ncell_a) take set A, the rest set B.
+struct CellSweepArgs {
+  CellArgs ca, cb;
+  int32_t ncell_a;
+};
+
+template <int G, int E>
+__global__ __launch_bounds__(kSweepBlock) void k_cells(CellSweepArgs s) {
+  __shared__ float4 tile[kTileFloats / 4];
+  const int b = static_cast<int>(blockIdx.x);
+  if (b < s.ncell_a) run_cell<G, E>(s.ca, b, tile);
+  else run_cell<G, E>(s.cb, b - s.ncell_a, tile);
+}
+
+// The work units of both sweep directions in one launch: workgroups [0, grid_a) take set
+// A, the rest set B (grid_a is a multiple of 8, so workgroup b of either set runs on XCD
+// b mod 8).  The two directions only read the ring and write their own partial rows, so
+// they may run concurrently, also with the cells.
+struct UnitSweepArgs {
+  UnitArgs ua, ub;
+  int32_t grid_a;
+};
+
+template <int G, int E>
+__global__ __launch_bounds__(kBlock) void k_units(UnitSweepArgs s) {
+  const int b = static_cast<int>(blockIdx.x);
+  const bool first = b < s.grid_a;
+  const UnitArgs &a = first ? s.ua : s.ub;
+  const int64_t unit = unit_of(a, first ? b : b - s.grid_a, threadIdx.x / G, kBlock / G);
+  if (unit < 0) return;  // whole groups leave together
+  run_unit<G, E>(a, unit, threadIdx.x & (G - 1));
+}
+
+// Squared loss over the canonical CSR of a block at one ring slot: one lane group per
+// segment (a user's ratings, cut at kLossSegment), e in fp32, e^2 accumulated in fp64,
+// one partial per workgroup (fixed order, so the result is deterministic).
+template <int G, int E>
+__global__ __launch_bounds__(kBlock) void k_loss(const int32_t *__restrict__ seg_user,
+                                                 const int64_t *__restrict__ seg_beg, int64_t nseg,
+                                                 const int32_t *__restrict__ col, const float *__restrict__ val,
+                                                 const float *__restrict__ L, const float *__restrict__ R,
+                                                 double *__restrict__ out) {
   constexpr int Kp = G * E;
   constexpr int NG = kBlock / G;
   __shared__ double acc_sh[NG];
   const int g = threadIdx.x & (G - 1);
   const int grp = threadIdx.x / G;
-  const int64_t unit = unit_of(a, grp, NG);
+  const int64_t sg = static_cast<int64_t>(blockIdx.x) * NG + grp;
   double acc = 0.0;
-  if (unit >= 0) {
-    const float *__restrict__ V = a.ring + slot * a.slot_stride;
-    const int64_t beg = a.unit_beg[unit];
-    const int n = a.unit_len[unit];
+  if (sg < nseg) {
     float x[E];
-    load_row<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
-    for (int t = 0; t < n; ++t) {
+    load_row<G, E>(x, L + static_cast<int64_t>(seg_user[sg]) * Kp, g);
+    for (int64_t t = seg_beg[sg]; t < seg_beg[sg + 1]; ++t) {
       float y[E];
-      load_row<G, E>(y, V + a.y_off + static_cast<int64_t>(a.y[beg + t]) * Kp, g);
-      const float e = residual<G, E>(x, y, a.val[beg + t]);
+      load_row<G, E>(y, R + static_cast<int64_t>(col[t]) * Kp, g);
+      const float e = residual<G, E>(x, y, val[t]);
       acc += static_cast<double>(e) * static_cast<double>(e);
     }
   }
@@ -248,8 +371,7 @@ struct FinalArgs {
 // of each of the n_i ratings is hoisted; scale = eta (SUM) or eta / n_i (ROWMEAN).  Users
 // without a rating in the block keep L^c_i (copied when the new slot differs).  One
 // thread per 4 columns.
-__global__ __launch_bounds__(kBlock) void k_finalize_users(FinalArgs a) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+__device__ __forceinline__ void finalize_users(const FinalArgs &a, int64_t idx) {
   const int64_t q4 = a.Kp / 4;
   if (idx >= a.users * q4) return;
   const int64_t i = idx / q4;
@@ -294,8 +416,7 @@ struct CommitArgs {
 
 // R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class n_j^(class) R^{v(class)}_j).
 // One thread per 4 columns.
-__global__ __launch_bounds__(kBlock) void k_commit(CommitArgs a) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+__device__ __forceinline__ void commit_items(const CommitArgs &a, int64_t idx) {
   const int64_t q4 = a.Kp / 4;
   if (idx >= a.items * q4) return;
   const int64_t j = idx / q4;
@@ -327,6 +448,16 @@ __global__ __launch_bounds__(kBlock) void k_commit(CommitArgs a) {
                       rc.z + sc * (d.z - a.lambda * lam.z), rc.w + sc * (d.w - a.lambda * lam.w));
   }
   R4[a.slot_n * ss4 + idx] = out;
+}
+
+// Version c+1 of both factors in one launch: workgroups [0, grid_users) finalize L, the
+// rest commit R (they write different rows of the new slot and read only partial rows and
+// versions <= c).
+__global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, int32_t grid_users) {
+  if (static_cast<int32_t>(blockIdx.x) < grid_users)
+    finalize_users(fa, static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x);
+  else
+    commit_items(ca, static_cast<int64_t>(blockIdx.x - grid_users) * kBlock + threadIdx.x);
 }
 
 // ------------------------------------------------------------------ kernel dispatch on Kp
@@ -366,16 +497,25 @@ hipError_t dispatch(int Kp, Args &&...args) {
 }
 
 template <int G, int E>
+struct LaunchCells {
+  static hipError_t run(const CellSweepArgs &a, int64_t grid, hipStream_t st) {
+    hipLaunchKernelGGL((k_cells<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kSweepBlock), 0, st, a);
+    return hipGetLastError();
+  }
+};
+template <int G, int E>
 struct LaunchUnits {
-  static hipError_t run(const UnitArgs &a, int64_t grid, hipStream_t st) {
+  static hipError_t run(const UnitSweepArgs &a, int64_t grid, hipStream_t st) {
     hipLaunchKernelGGL((k_units<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a);
     return hipGetLastError();
   }
 };
 template <int G, int E>
 struct LaunchLoss {
-  static hipError_t run(const UnitArgs &a, int32_t slot, int64_t grid, double *out, hipStream_t st) {
-    hipLaunchKernelGGL((k_loss<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a, slot, out);
+  static hipError_t run(const int32_t *seg_user, const int64_t *seg_beg, int64_t nseg, const int32_t *col,
+                        const float *val, const float *L, const float *R, int64_t grid, double *out, hipStream_t st) {
+    hipLaunchKernelGGL((k_loss<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, seg_user, seg_beg,
+                       nseg, col, val, L, R, out);
     return hipGetLastError();
   }
 };
@@ -392,10 +532,25 @@ struct DeviceUnits {
   int64_t *unit_beg = nullptr, *xcd_off = nullptr, *x_pp = nullptr;
 };
 
+struct DeviceCells {
+  int64_t ncells = 0, padded = 0;  // cells with work; launch slots (a multiple of 8)
+  int32_t ts = 0;
+  int32_t *step_rows = nullptr, *cell_x = nullptr, *cell_cls = nullptr, *cell_step_ptr = nullptr,
+          *cell_steps = nullptr, *run_beg = nullptr, *run_len = nullptr, *cell_out = nullptr;
+  uint16_t *ly = nullptr;
+  float *lv = nullptr;
+};
+
 struct DeviceBlock {
-  int64_t nnz = 0;
+  int64_t nnz = 0, loss_grid = 0;
   int32_t *ucount = nullptr, *icount = nullptr, *icount_cls = nullptr;
+  int64_t nseg = 0;            // the canonical CSR cut into loss segments
+  int32_t *seg_user = nullptr;
+  int64_t *seg_beg = nullptr;  // [nseg + 1]
+  int32_t *col = nullptr;
+  float *val = nullptr;
   DeviceUnits by_user, by_item;
+  DeviceCells cells_user, cells_item;
 };
 
 struct ps_mf {
@@ -409,6 +564,8 @@ struct ps_mf {
   bool host_only = false, timing = false;
   int64_t tile_bytes = 3 << 20;  // rows per L2 tile of the sweeps, in bytes
   int32_t unit_max = 1024;
+  bool cells = true;             // stage the dense part (heavy users) through LDS
+  int64_t heavy_min = -1;        // ratings from which a user goes to the cells (-1: automatic)
   std::vector<int32_t> owner;
   // host state
   bool loaded = false, has_factors = false;
@@ -423,6 +580,9 @@ struct ps_mf {
   hipStream_t stream = nullptr;
   bool own_stream = false;
   hipStream_t user_stream = nullptr;
+  hipStream_t side_stream = nullptr;  // runs the work units beside the cells (default priority)
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool two_streams = true;
   float *ring = nullptr;
   float *partial_u = nullptr, *partial_i = nullptr;
   int32_t *ucls = nullptr;
@@ -502,6 +662,43 @@ int upload_units(ps_mf_t *h, DeviceUnits &d, const psmf::UnitSet &u) {
   return PS_MF_OK;
 }
 
+int upload_cells(ps_mf_t *h, DeviceCells &d, const psmf::CellSet &c) {
+  int r;
+  if ((r = upload(h, &d.step_rows, c.step_rows)) || (r = upload(h, &d.cell_x, c.cell_x)) ||
+      (r = upload(h, &d.cell_cls, c.cell_cls)) || (r = upload(h, &d.cell_step_ptr, c.cell_step_ptr)) ||
+      (r = upload(h, &d.cell_steps, c.cell_steps)) || (r = upload(h, &d.run_beg, c.run_beg)) ||
+      (r = upload(h, &d.run_len, c.run_len)) || (r = upload(h, &d.cell_out, c.cell_out)) ||
+      (r = upload(h, &d.ly, c.ly)) || (r = upload(h, &d.lv, c.lv)))
+    return r;
+  d.ncells = static_cast<int64_t>(c.cell_cls.size());
+  d.padded = (d.ncells + kXcds - 1) / kXcds * kXcds;
+  d.ts = c.ts;
+  return PS_MF_OK;
+}
+
+CellArgs cell_args(const ps_mf_t *h, const DeviceCells &d, float *partial, int64_t x_off, int64_t y_off,
+                   const int32_t *cls_slot) {
+  CellArgs a{};
+  a.step_rows = d.step_rows;
+  a.cell_x = d.cell_x;
+  a.cell_cls = d.cell_cls;
+  a.cell_step_ptr = d.cell_step_ptr;
+  a.cell_steps = d.cell_steps;
+  a.run_beg = d.run_beg;
+  a.run_len = d.run_len;
+  a.cell_out = d.cell_out;
+  a.ly = d.ly;
+  a.lv = d.lv;
+  a.cls_slot = cls_slot;
+  a.ring = h->ring;
+  a.slot_stride = (h->N + h->M) * h->Kp;
+  a.x_off = x_off;
+  a.y_off = y_off;
+  a.ts = d.ts;
+  a.partial = partial;
+  return a;
+}
+
 UnitArgs unit_args(const ps_mf_t *h, const DeviceUnits &d, float *partial, int64_t x_off, int64_t y_off,
                    int64_t y_rows) {
   UnitArgs a{};
@@ -553,6 +750,11 @@ int ensure_device(ps_mf_t *h) {
       h->own_stream = true;
     }
   }
+  if (h->two_streams && !h->side_stream) {
+    HIP_TRY(h, hipStreamCreateWithFlags(&h->side_stream, hipStreamNonBlocking));
+    HIP_TRY(h, hipEventCreateWithFlags(&h->fork, hipEventDisableTiming));
+    HIP_TRY(h, hipEventCreateWithFlags(&h->join, hipEventDisableTiming));
+  }
   return PS_MF_OK;
 }
 
@@ -592,15 +794,33 @@ int one_clock(ps_mf_t *h) {
   hipEvent_t ev = nullptr;
   int rc = record(h, &ev);
   if (rc) return rc;
-  if (db.by_item.nunits > 0) {  // x = item (R), y = user (L)
-    UnitArgs a = unit_args(h, db.by_item, h->partial_i, r_off, 0, h->N);
-    a.cls_slot = cls_slot;
-    HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, a, db.by_item.grid, h->stream));
-  }
-  if (db.by_user.nunits > 0) {  // x = user (L), y = item (R)
-    UnitArgs a = unit_args(h, db.by_user, h->partial_u, 0, r_off, h->M);
-    a.cls_slot = cls_slot;
-    HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, a, db.by_user.grid, h->stream));
+  {
+    // set A = user-major (x = user / L, y = item / R); set B = item-major (x = item, y = user)
+    CellSweepArgs cs{};
+    cs.ca = cell_args(h, db.cells_user, h->partial_u, 0, r_off, cls_slot);
+    cs.cb = cell_args(h, db.cells_item, h->partial_i, r_off, 0, cls_slot);
+    cs.ncell_a = static_cast<int32_t>(db.cells_user.ncells);
+    const int64_t ncells = db.cells_user.ncells + db.cells_item.ncells;
+    UnitSweepArgs us{};
+    us.ua = unit_args(h, db.by_user, h->partial_u, 0, r_off, h->M);
+    us.ub = unit_args(h, db.by_item, h->partial_i, r_off, 0, h->N);
+    us.ua.cls_slot = cls_slot;
+    us.ub.cls_slot = cls_slot;
+    const int64_t gu = db.by_user.nunits > 0 ? db.by_user.grid : 0;
+    const int64_t gi = db.by_item.nunits > 0 ? db.by_item.grid : 0;
+    us.grid_a = static_cast<int32_t>(gu);
+    if (ncells > 0 && gu + gi > 0 && h->side_stream) {
+      // cells on the handle's stream, units on the side stream, both after what precedes
+      HIP_TRY(h, hipEventRecord(h->fork, h->stream));
+      HIP_TRY(h, hipStreamWaitEvent(h->side_stream, h->fork, 0));
+      HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, us, gu + gi, h->side_stream));
+      HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
+      HIP_TRY(h, hipEventRecord(h->join, h->side_stream));
+      HIP_TRY(h, hipStreamWaitEvent(h->stream, h->join, 0));
+    } else {
+      if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
+      if (gu + gi > 0) HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, us, gu + gi, h->stream));
+    }
   }
   if ((rc = record_end(h, PS_MF_KERNEL_SWEEP, ev))) return rc;
 
@@ -621,9 +841,6 @@ int one_clock(ps_mf_t *h) {
   fa.lambda = h->lambda;
   fa.rowmean = rowmean;
   const int64_t nfin = h->N * h->Kp / 4;
-  hipLaunchKernelGGL(k_finalize_users, dim3(static_cast<unsigned>((nfin + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                     h->stream, fa);
-  HIP_TRY(h, hipGetLastError());
   CommitArgs ca{};
   ca.ring = h->ring;
   ca.slot_stride = slot_stride;
@@ -642,8 +859,9 @@ int one_clock(ps_mf_t *h) {
   ca.lambda = h->lambda;
   ca.rowmean = rowmean;
   const int64_t ncommit = h->M * h->Kp / 4;
-  hipLaunchKernelGGL(k_commit, dim3(static_cast<unsigned>((ncommit + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                     h->stream, ca);
+  const int64_t grid_users = (nfin + kBlock - 1) / kBlock, grid_items = (ncommit + kBlock - 1) / kBlock;
+  hipLaunchKernelGGL(k_commit, dim3(static_cast<unsigned>(grid_users + grid_items)), dim3(kBlock), 0, h->stream, fa,
+                     ca, static_cast<int32_t>(grid_users));
   HIP_TRY(h, hipGetLastError());
   if ((rc = record_end(h, PS_MF_KERNEL_COMMIT, ev))) return rc;
 
@@ -714,6 +932,16 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
       if (value < 1 || value > (1 << 30)) return fail(h, PS_MF_EINVAL, "unit size must be in [1, 2^30]");
       h->unit_max = static_cast<int32_t>(value);
       return PS_MF_OK;
+    case PS_MF_OPT_CELLS:
+      h->cells = value != 0;
+      return PS_MF_OK;
+    case PS_MF_OPT_TWO_STREAMS:
+      h->two_streams = value != 0;
+      return PS_MF_OK;
+    case PS_MF_OPT_HEAVY_MIN:
+      if (value < -1) return fail(h, PS_MF_EINVAL, "heavy threshold must be >= -1");
+      h->heavy_min = value;
+      return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
   }
@@ -766,9 +994,19 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   lp.owner = h->owner.data();
   lp.cls_of_worker = h->cls_of_worker.data();
   lp.threads = host_threads();
-  lp.tile_rows_item = std::max<int64_t>(64, h->tile_bytes / (static_cast<int64_t>(h->Kp) * 4));
-  lp.tile_rows_user = lp.tile_rows_item;
+  // item-major tiles of user rows are sized for one XCD's L2; the user-major sweep takes
+  // 4x larger item tiles: fewer units and partial rows per light user measured faster
+  lp.tile_rows_user = std::max<int64_t>(64, h->tile_bytes / (static_cast<int64_t>(h->Kp) * 4));
+  lp.tile_rows_item = 4 * lp.tile_rows_user;
   lp.unit_max = h->unit_max;
+  if (h->cells) {
+    // cells: one 1024-thread workgroup per cell, a 128 KiB LDS sub-tile of ts rows; a user
+    // is dense enough for them when it averages 16 or more ratings per item sub-tile
+    lp.cell_rows = kTileFloats / h->Kp;
+    lp.cell_groups = kSweepBlock / shape_for(h->Kp).G;
+    lp.heavy_min = h->heavy_min >= 0 ? h->heavy_min
+                                      : std::max<int64_t>(256, 16 * h->M / lp.cell_rows);
+  }
   std::string err;
   const int rc = psmf::build_layout(lp, user, item, value, n, h->layout, err);
   if (rc == -1) return fail(h, PS_MF_EINVAL, "%s", err.c_str());
@@ -788,12 +1026,28 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
     DeviceBlock &d = h->dblocks[b];
     d.nnz = L.nnz;
     if ((r = upload(h, &d.ucount, L.ucount)) || (r = upload(h, &d.icount, L.icount)) ||
-        (r = upload(h, &d.icount_cls, L.icount_cls)) || (r = upload_units(h, d.by_user, L.by_user)) ||
-        (r = upload_units(h, d.by_item, L.by_item)))
+        (r = upload(h, &d.icount_cls, L.icount_cls)) || (r = upload(h, &d.col, L.col)) ||
+        (r = upload(h, &d.val, L.val)) ||
+        (r = upload_units(h, d.by_user, L.by_user)) || (r = upload_units(h, d.by_item, L.by_item)) ||
+        (r = upload_cells(h, d.cells_user, L.cells_user)) || (r = upload_cells(h, d.cells_item, L.cells_item)))
       return undo(r);
-    max_units_u = std::max<int64_t>(max_units_u, d.by_user.nunits + 1);  // + the padding units' row
-    max_units_i = std::max<int64_t>(max_units_i, d.by_item.nunits + 1);
-    loss_len += d.by_user.grid;
+    // partial rows of units and cells, + the row the padding units write
+    max_units_u = std::max<int64_t>(max_units_u, L.partial_rows_user + 1);
+    max_units_i = std::max<int64_t>(max_units_i, L.partial_rows_item + 1);
+    {
+      std::vector<int32_t> su;
+      std::vector<int64_t> sb;
+      for (int64_t i = 0; i < h->N; ++i)
+        for (int64_t t = L.row_ptr[i]; t < L.row_ptr[i + 1]; t += kLossSegment) {
+          su.push_back(static_cast<int32_t>(i));
+          sb.push_back(t);
+        }
+      sb.push_back(L.nnz);
+      d.nseg = static_cast<int64_t>(su.size());
+      if ((r = upload(h, &d.seg_user, su)) || (r = upload(h, &d.seg_beg, sb))) return undo(r);
+    }
+    d.loss_grid = (d.nseg + kBlock / shape_for(h->Kp).G - 1) / (kBlock / shape_for(h->Kp).G);
+    loss_len += d.loss_grid;
   }
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->partial_u), static_cast<size_t>(max_units_u * h->Kp) * sizeof(float))) ||
       (r = dev_alloc(h, reinterpret_cast<void **>(&h->partial_i), static_cast<size_t>(max_units_i * h->Kp) * sizeof(float))))
@@ -867,10 +1121,10 @@ int ps_mf_loss(ps_mf_t *h, double *out) {
   int64_t off = 0;
   for (int b = 0; b < h->B; ++b) {
     const DeviceBlock &d = h->dblocks[b];
-    if (d.by_user.nunits == 0) continue;
-    UnitArgs ua = unit_args(h, d.by_user, nullptr, 0, h->N * h->Kp, h->M);
-    HIP_TRY(h, dispatch<LaunchLoss>(h->Kp, ua, sl, d.by_user.grid, h->loss_partial + off, h->stream));
-    off += d.by_user.grid;
+    if (d.nnz == 0) continue;
+    HIP_TRY(h, dispatch<LaunchLoss>(h->Kp, d.seg_user, d.seg_beg, d.nseg, d.col, d.val, L, R, d.loss_grid,
+                                     h->loss_partial + off, h->stream));
+    off += d.loss_grid;
   }
   if (off == 0) {
     *out = 0.0;
@@ -972,7 +1226,11 @@ void ps_mf_destroy(ps_mf_t *h) {
     (void)hipEventDestroy(ev.a);
     (void)hipEventDestroy(ev.b);
   }
+  if (h->side_stream) (void)hipStreamSynchronize(h->side_stream);
   for (void *p : h->allocations) (void)hipFree(p);
+  if (h->side_stream) (void)hipStreamDestroy(h->side_stream);
+  if (h->fork) (void)hipEventDestroy(h->fork);
+  if (h->join) (void)hipEventDestroy(h->join);
   if (h->own_stream && h->stream) (void)hipStreamDestroy(h->stream);
   delete h;
 }

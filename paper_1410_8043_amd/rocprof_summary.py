@@ -27,7 +27,7 @@ import sys
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCE = os.path.join(_HERE, "csrc", "ps_mf.hip")
-SWEEP_KERNEL = "k_units"
+SWEEP_KERNEL = "k_sweep"
 
 
 def kernel_source_sha256() -> str:
@@ -84,7 +84,7 @@ def _copy_value(cnt, counter: str) -> float:
     raise KeyError(f"{counter} of the calibration copy kernel not found")
 
 
-def traffic(fetch_dir: str, write_dir: str, copy_bytes: int, launches_per_clock: int = 2):
+def traffic(fetch_dir: str, write_dir: str, copy_bytes: int, launches_per_clock: int = 1):
     """HBM bytes per clock of the sweep (its launches of one clock summed), calibrated."""
     f, w = counters(fetch_dir), counters(write_dir)
     copy_f = _copy_value(f, "FETCH_SIZE")

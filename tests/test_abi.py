@@ -130,3 +130,18 @@ def test_empty_and_single_rating_layouts():
         g.load_ratings(np.array([4]), np.array([3]), np.array([2.0]))
         assert np.array_equal(g.export_index(ps_mf.IDX_ROW_PTR), [0, 0, 0, 0, 0, 1])
         assert np.array_equal(g.export_index(ps_mf.IDX_ITEM_COUNT), [0, 0, 0, 1])
+
+
+@pytest.mark.parametrize("cells,heavy_min", [(False, -1), (True, 1), (True, 40), (True, -1)])
+@pytest.mark.parametrize("K", [8, 128, 512])
+def test_host_layout_with_and_without_cells(cells, heavy_min, K):
+    """The exported integer layout does not depend on how the sweeps are scheduled."""
+    from paper_1410_8043_amd import synth
+    spec = synth.scaled(synth.CONFIGS["full"], 0.01)
+    w = synth.generate(spec, K=1)
+    with ps_mf.PsMf(spec.N, spec.M, K, spec.P, 3, 0.01, 0.05, host_only=True, cells=cells,
+                    heavy_min=heavy_min) as g:
+        g.load_ratings(w.user, w.item, w.val)
+        o = oracle.Oracle(spec.N, spec.M, 4, spec.P, 3, 0.01, 0.05)
+        o.load(w.user, w.item, w.val)
+        compare_layout(g, o, 1, spec.N, spec.M)

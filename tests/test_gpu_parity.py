@@ -34,12 +34,14 @@ def say(msg):
 
 
 def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, policy=0, step=0, B=1,
-             seed=0, owner=None, check_versions=False):
-    say(f"case N={N} M={M} K={K} P={P} s={s} policy={policy} step={step} B={B} nnz={len(w_user)} clocks={clocks}")
+             seed=0, owner=None, check_versions=False, **handle_opts):
+    say(f"case N={N} M={M} K={K} P={P} s={s} policy={policy} step={step} B={B} nnz={len(w_user)} clocks={clocks} "
+        f"{handle_opts}")
     o = oracle.Oracle(N, M, K, P, s, eta, lam, policy, step, B, seed, owner)
     o.load(w_user, w_item, w_val)
     o.set_factors(L0, R0)
-    with ps_mf.PsMf(N, M, K, P, s, eta, lam, policy=policy, step=step, B=B, mb_seed=seed, owner=owner) as g:
+    with ps_mf.PsMf(N, M, K, P, s, eta, lam, policy=policy, step=step, B=B, mb_seed=seed, owner=owner,
+                    **handle_opts) as g:
         g.load_ratings(w_user, w_item, w_val)
         g.set_factors(L0, R0)
         g.clock(clocks)
@@ -109,6 +111,17 @@ def test_full_shape_scaled(gpu, s):
     w = synth.generate(spec)
     run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta,
              lam=spec.lam, clocks=10, check_versions=True)
+
+
+@pytest.mark.parametrize("cells,heavy_min", [(False, -1), (True, 1), (True, 100), (True, -1)])
+@pytest.mark.parametrize("K", [32, 128, 512])
+def test_lds_cells_and_units_agree_with_oracle(gpu, cells, heavy_min, K):
+    """The LDS-staged cell path (users with at least heavy_min ratings) and the L2 unit path,
+    alone and mixed, on the full workload's laws at 2% size, s=3 (four worker classes)."""
+    spec = synth.scaled(synth.CONFIGS["full"], 0.02)
+    w = synth.generate(spec, K=K)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=K, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=6, check_versions=True, cells=cells, heavy_min=heavy_min)
 
 
 @pytest.mark.parametrize("policy", [oracle.SSP_WORST, oracle.ESSP])
