@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--cells", type=int, default=None, help="1/0: LDS-staged cells for the dense part")
     ap.add_argument("--heavy-min", type=int, default=None, help="ratings from which a user goes to the cells")
     ap.add_argument("--two-streams", type=int, default=None, help="1/0: units on a second stream beside the cells")
+    ap.add_argument("--hot-steps", type=int, default=None,
+                    help="LDS sub-tiles of the most rated items whose light-user ratings go to cells (-1: auto)")
     ap.add_argument("--copy-calibration-bytes", type=int, default=0,
                     help="run one plain copy kernel (y = x * 2) of this many bytes before timing, for "
                          "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE")
@@ -112,7 +114,7 @@ def main():
     stream = torch.cuda.current_stream()
     g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, B=spec.B,
                    mb_seed=spec.seed, timing=not args.no_timing, stream=stream, tile_bytes=args.tile_bytes,
-                   unit_max=args.unit_max, cells=args.cells, heavy_min=args.heavy_min,
+                   unit_max=args.unit_max, cells=args.cells, heavy_min=args.heavy_min, hot_steps=args.hot_steps,
                    two_streams=args.two_streams)
     t_load = time.perf_counter()
     g.load_ratings(w.user, w.item, w.val)

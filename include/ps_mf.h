@@ -58,13 +58,15 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_ENOMEM (-2) /* host or device allocation failed; the handle stays destroyable */
 #define PS_MF_EDEVICE (-3) /* a HIP call failed (no device, launch error, fault) */
 #define PS_MF_ESTATE (-4) /* call out of order (e.g. clock before load and set_factors) */
+#define PS_MF_EINTERNAL (-5) /* the library's own consistency check of its layout failed (a bug) */
 
 /* option keys (ps_mf_set_option); all must be set before ps_mf_load_ratings */
 #define PS_MF_OPT_POLICY 1    /* PS_MF_SSP_LAZY (default), PS_MF_SSP_WORST, PS_MF_ESSP */
 #define PS_MF_OPT_STEP 2      /* PS_MF_STEP_ROWMEAN (default), PS_MF_STEP_SUM */
 #define PS_MF_OPT_MB_BLOCKS 3 /* B >= 1 minibatch blocks (default 1: full shard per clock) */
 #define PS_MF_OPT_MB_SEED 4   /* 64-bit seed of the block hash (default 0) */
-#define PS_MF_OPT_HOST_ONLY 5 /* 1: build and export the integer layout only; never touch a device */
+#define PS_MF_OPT_HOST_ONLY 5 /* 1: build, self-check and export the integer layout only; never touch
+                                 a device (a failed self-check returns PS_MF_EINTERNAL) */
 #define PS_MF_OPT_TIMING 6    /* 1: record HIP events around every kernel (ps_mf_kernel_time) */
 #define PS_MF_OPT_TILE_BYTES 7 /* bytes of user rows per tile of the item-major sweep (default 3 MiB,
                                   sized to one XCD's 4 MiB L2); >= 1 */
@@ -75,6 +77,10 @@ typedef struct ps_mf ps_mf_t;
                                   -1 (default): 16 x items / LDS sub-tile rows, at least 256 */
 #define PS_MF_OPT_TWO_STREAMS 11 /* 1 (default): run the L2 work units on a second, internal stream
                                     (default priority) beside the cells; 0: one stream */
+#define PS_MF_OPT_HOT_STEPS 12 /* LDS sub-tiles of a block's most rated items whose ratings by the
+                                  remaining (light) users also go to cells; 0: none;
+                                  -1 (default): automatic (one sub-tile).  Needs
+                                  PS_MF_OPT_CELLS = 1; at most 1024 */
 
 #define PS_MF_SSP_LAZY 0
 #define PS_MF_SSP_WORST 1

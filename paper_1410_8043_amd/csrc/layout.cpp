@@ -4,6 +4,8 @@
 #include <algorithm>
 #include <atomic>
 #include <cmath>
+#include <cstring>
+#include <exception>
 #include <functional>
 #include <new>
 #include <numeric>
@@ -155,22 +157,42 @@ void build_units(int64_t nb, int64_t nx, int64_t ntiles, const std::function<int
   U.nreal = nu;
 }
 
-// number of distinct (x, tile) runs for a tile function (entries sorted by x already)
+// number of distinct (x, tile) runs for a tile function (entries sorted by x already);
+// threads take slices of by_x cut at changes of x, so no run spans two slices
 int64_t count_runs(int64_t nb, const std::vector<int64_t> &by_x, const std::function<int32_t(int64_t)> &xrow,
                    const std::function<int32_t(int64_t)> &tile, int64_t ntiles, const std::vector<uint8_t> &in_units,
-                   std::vector<int64_t> &last) {
-  last.assign(static_cast<size_t>(ntiles), -1);
-  int64_t runs = 0;
-  for (int64_t e = 0; e < nb; ++e) {
-    if (!in_units[by_x[e]]) continue;
-    const int64_t x = xrow(by_x[e]);
-    const int32_t t = tile(by_x[e]);
-    if (last[t] != x) {
-      last[t] = x;
-      ++runs;
-    }
+                   int threads) {
+  const int T = nb >= (1 << 20) ? std::max(1, threads) : 1;
+  std::vector<int64_t> cut(static_cast<size_t>(T) + 1, nb);
+  cut[0] = 0;
+  for (int t = 1; t < T; ++t) {
+    int64_t e = std::max(cut[t - 1], nb * t / T);
+    while (e > cut[t - 1] && e < nb && xrow(by_x[e]) == xrow(by_x[e - 1])) ++e;
+    cut[t] = e;
   }
-  return runs;
+  std::vector<int64_t> runs(static_cast<size_t>(T), 0);
+  auto work = [&](int t) {
+    std::vector<int64_t> last(static_cast<size_t>(ntiles), -1);
+    for (int64_t e = cut[t]; e < cut[t + 1]; ++e) {
+      if (!in_units[by_x[e]]) continue;
+      const int64_t x = xrow(by_x[e]);
+      const int32_t tl = tile(by_x[e]);
+      if (last[tl] != x) {
+        last[tl] = x;
+        ++runs[t];
+      }
+    }
+  };
+  if (T == 1) {
+    work(0);
+  } else {
+    std::vector<std::thread> pool;
+    for (int t = 0; t < T; ++t) pool.emplace_back(work, t);
+    for (auto &th : pool) th.join();
+  }
+  int64_t total = 0;
+  for (int64_t r : runs) total += r;
+  return total;
 }
 
 // Append the ratings [lo, hi) of the (already ordered) list `ents` as one 8-aligned run.
@@ -343,6 +365,194 @@ void build_item_cells(const LayoutParams &p, const BlockLayout &L, const std::ve
   }
 }
 
+// Light users x hot items, user-major: light users of one class with hot ratings, sorted
+// by their hot-rating count, ng per cell; the steps are the hot sub-tiles (hot items in
+// popularity order, ts per sub-tile).  Each such user owns one more partial row.
+void build_user_cells_hot(const LayoutParams &p, const BlockLayout &L, const std::vector<int32_t> &ucls,
+                          const std::vector<uint8_t> &heavy, const std::vector<int32_t> &hot_pos,
+                          const std::vector<int32_t> &hot_items, CellSet &C, std::vector<int64_t> &extra) {
+  const int64_t N = p.users, ts = p.cell_rows, ng = p.cell_groups;
+  const int64_t nhot = static_cast<int64_t>(hot_items.size());
+  if (nhot == 0) return;
+  C.ts = static_cast<int32_t>(ts);
+  C.ng = static_cast<int32_t>(ng);
+  if (extra.empty()) extra.assign(static_cast<size_t>(N), 0);
+  const int64_t nsub = (nhot + ts - 1) / ts;
+  const int32_t step0 = static_cast<int32_t>(C.step_rows.size() / ts);
+  for (int64_t t = 0; t < nsub * ts; ++t) C.step_rows.push_back(t < nhot ? hot_items[t] : -1);
+  // each light user's hot entries, sorted by hot position (sub-tile, then place)
+  std::vector<std::vector<int32_t>> by_cls(static_cast<size_t>(p.nclass));
+  std::vector<int64_t> hot_cnt(static_cast<size_t>(N), 0);
+  for (int64_t i = 0; i < N; ++i) {
+    if (heavy[i]) continue;
+    for (int64_t e = L.row_ptr[i]; e < L.row_ptr[i + 1]; ++e) hot_cnt[i] += hot_pos[L.col[e]] >= 0;
+    if (hot_cnt[i] > 0) by_cls[ucls[i]].push_back(static_cast<int32_t>(i));
+  }
+  std::vector<int64_t> ents;
+  const std::function<int32_t(int64_t)> local = [&](int64_t e) { return static_cast<int32_t>(hot_pos[L.col[e]] % ts); };
+  if (C.cell_step_ptr.empty()) C.cell_step_ptr.push_back(0);
+  for (int32_t c = 0; c < p.nclass; ++c) {
+    auto &us = by_cls[c];
+    std::stable_sort(us.begin(), us.end(), [&](int32_t a, int32_t b) { return hot_cnt[a] > hot_cnt[b]; });
+    for (size_t g0 = 0; g0 < us.size(); g0 += static_cast<size_t>(ng)) {
+      C.cell_cls.push_back(c);
+      for (int64_t q = 0; q < ng; ++q) {
+        const size_t k = g0 + static_cast<size_t>(q);
+        C.cell_x.push_back(k < us.size() ? us[k] : -1);
+        C.cell_out.push_back(-1);
+      }
+      // per member: its hot entries grouped by sub-tile
+      std::vector<std::vector<int64_t>> mine(static_cast<size_t>(ng));
+      for (int64_t q = 0; q < ng && g0 + q < us.size(); ++q) {
+        const int32_t u = us[g0 + q];
+        for (int64_t e = L.row_ptr[u]; e < L.row_ptr[u + 1]; ++e)
+          if (hot_pos[L.col[e]] >= 0) mine[q].push_back(e);
+        std::stable_sort(mine[q].begin(), mine[q].end(),
+                         [&](int64_t a, int64_t b) { return hot_pos[L.col[a]] < hot_pos[L.col[b]]; });
+      }
+      for (int64_t st = 0; st < nsub; ++st) {
+        C.cell_steps.push_back(step0 + static_cast<int32_t>(st));
+        for (int64_t q = 0; q < ng; ++q) {
+          if (g0 + q >= us.size()) { empty_run(C); continue; }
+          const auto &m = mine[q];
+          const auto lo = std::lower_bound(m.begin(), m.end(), st * ts,
+                                           [&](int64_t e, int64_t v) { return hot_pos[L.col[e]] < v; });
+          const auto hi = std::lower_bound(m.begin(), m.end(), (st + 1) * ts,
+                                           [&](int64_t e, int64_t v) { return hot_pos[L.col[e]] < v; });
+          append_run(C, m, lo - m.begin(), hi - m.begin(), local, L.val);
+        }
+      }
+      C.cell_step_ptr.push_back(static_cast<int32_t>(C.cell_steps.size()));
+      for (size_t k = g0; k < std::min(us.size(), g0 + static_cast<size_t>(ng)); ++k) extra[us[k]] += 1;
+    }
+  }
+}
+
+// Light users x hot items, item-major: hot items in popularity order, ng per cell; for
+// each class the steps are consecutive ranges of ts of its light users that rated a hot
+// item (in id order), cut into ranges so that there are about cell_target cells.  Each
+// hot item owns one more partial row per (class, range).
+void build_item_cells_hot(const LayoutParams &p, const BlockLayout &L, const std::vector<int32_t> &ucls,
+                          const std::vector<uint8_t> &heavy, const std::vector<int32_t> &ent_user,
+                          const std::vector<int32_t> &hot_pos, const std::vector<int32_t> &hot_items, CellSet &C,
+                          std::vector<int64_t> &extra) {
+  const int64_t N = p.users, M = p.items, ts = p.cell_rows, ng = p.cell_groups;
+  const int64_t nb = static_cast<int64_t>(L.col.size());
+  const int64_t nhot = static_cast<int64_t>(hot_items.size());
+  if (nhot == 0) return;
+  C.ts = static_cast<int32_t>(ts);
+  C.ng = static_cast<int32_t>(ng);
+  if (extra.empty()) extra.assign(static_cast<size_t>(M), 0);
+  // light users with hot ratings, ranked within their class in id order
+  std::vector<uint8_t> has_hot(static_cast<size_t>(N), 0);
+  std::vector<int64_t> a, b;
+  for (int64_t e = 0; e < nb; ++e)
+    if (!heavy[ent_user[e]] && hot_pos[L.col[e]] >= 0) {
+      a.push_back(e);
+      has_hot[ent_user[e]] = 1;
+    }
+  if (a.empty()) return;
+  std::vector<int64_t> rank(static_cast<size_t>(N), -1), nlight(static_cast<size_t>(p.nclass), 0);
+  for (int64_t i = 0; i < N; ++i)
+    if (has_hot[i]) rank[i] = nlight[ucls[i]]++;
+  std::vector<int64_t> nsub(static_cast<size_t>(p.nclass)), sub_base(static_cast<size_t>(p.nclass) + 1, 0);
+  for (int32_t c = 0; c < p.nclass; ++c) {
+    nsub[c] = (nlight[c] + ts - 1) / ts;
+    sub_base[c + 1] = sub_base[c] + nsub[c];
+  }
+  const int32_t step0 = static_cast<int32_t>(C.step_rows.size() / ts);
+  C.step_rows.resize(C.step_rows.size() + static_cast<size_t>(sub_base[p.nclass] * ts), -1);
+  for (int64_t i = 0; i < N; ++i)
+    if (has_hot[i])
+      C.step_rows[(step0 + sub_base[ucls[i]] + rank[i] / ts) * ts + rank[i] % ts] = static_cast<int32_t>(i);
+  // entries by (hot position, class, user): canonical is (user, item)
+  b.resize(a.size());
+  counting_pass(a, b, p.nclass, [&](int64_t e) { return ucls[ent_user[e]]; });
+  counting_pass(b, a, nhot, [&](int64_t e) { return hot_pos[L.col[e]]; });
+  // boundaries of (hot position h, class c, sub-tile st)
+  std::vector<int64_t> hc_base(static_cast<size_t>(nhot * p.nclass) + 1, 0);
+  for (int64_t h = 0; h < nhot; ++h)
+    for (int32_t c = 0; c < p.nclass; ++c) hc_base[h * p.nclass + c + 1] = hc_base[h * p.nclass + c] + nsub[c] + 1;
+  std::vector<int64_t> bnd(static_cast<size_t>(hc_base[nhot * p.nclass]), 0);
+  {
+    int64_t e = 0;
+    const int64_t na = static_cast<int64_t>(a.size());
+    for (int64_t h = 0; h < nhot; ++h)
+      for (int32_t c = 0; c < p.nclass; ++c) {
+        int64_t *o = bnd.data() + hc_base[h * p.nclass + c];
+        for (int64_t st = 0; st < nsub[c]; ++st) {
+          o[st] = e;
+          while (e < na && hot_pos[L.col[a[e]]] == h && ucls[ent_user[a[e]]] == c && rank[ent_user[a[e]]] / ts == st) ++e;
+        }
+        o[nsub[c]] = e;
+      }
+  }
+  // Hot items differ a lot in popularity, and a cell step lasts as long as its longest run:
+  // an item of class weight w gets m = max(1, round(w / w_med)) lane groups ("slots"), slot
+  // r taking the users whose place in the sub-tile is r mod m; slots are sorted by weight
+  // per slot and packed ng to a cell.
+  struct Slot { int32_t h, r, m; int64_t w; };
+  std::vector<std::vector<Slot>> slots(static_cast<size_t>(p.nclass));
+  int64_t cells_per_range = 0;
+  for (int32_t c = 0; c < p.nclass; ++c) {
+    if (nsub[c] == 0) continue;
+    std::vector<int64_t> wts;
+    for (int64_t h = 0; h < nhot; ++h) {
+      const int64_t *o = bnd.data() + hc_base[h * p.nclass + c];
+      if (o[nsub[c]] > o[0]) wts.push_back(o[nsub[c]] - o[0]);
+    }
+    if (wts.empty()) continue;
+    std::vector<int64_t> sorted_w = wts;
+    std::nth_element(sorted_w.begin(), sorted_w.begin() + sorted_w.size() / 2, sorted_w.end());
+    const int64_t w_med = std::max<int64_t>(1, sorted_w[sorted_w.size() / 2]);
+    for (int64_t h = 0; h < nhot; ++h) {
+      const int64_t *o = bnd.data() + hc_base[h * p.nclass + c];
+      const int64_t w = o[nsub[c]] - o[0];
+      if (w == 0) continue;
+      const int32_t m = static_cast<int32_t>(std::min<int64_t>(ts, std::max<int64_t>(1, (2 * w + w_med) / (2 * w_med))));
+      for (int32_t r = 0; r < m; ++r) slots[c].push_back({static_cast<int32_t>(h), r, m, w});
+    }
+    std::stable_sort(slots[c].begin(), slots[c].end(),
+                     [](const Slot &x, const Slot &y) { return x.w * y.m > y.w * x.m; });
+    cells_per_range += (static_cast<int64_t>(slots[c].size()) + ng - 1) / ng;
+  }
+  if (cells_per_range == 0) return;
+  const int64_t R = std::max<int64_t>(1, (p.cell_target + cells_per_range - 1) / cells_per_range);
+  const std::function<int32_t(int64_t)> local = [&](int64_t e) { return static_cast<int32_t>(rank[ent_user[e]] % ts); };
+  if (C.cell_step_ptr.empty()) C.cell_step_ptr.push_back(0);
+  std::vector<int64_t> run;
+  for (int32_t c = 0; c < p.nclass; ++c) {
+    if (slots[c].empty()) continue;
+    const auto &sl = slots[c];
+    const int64_t ns = static_cast<int64_t>(sl.size());
+    const int64_t Rc = std::min<int64_t>(R, nsub[c]);
+    for (int64_t g0 = 0; g0 < ns; g0 += ng) {
+      for (int64_t r = 0; r < Rc; ++r) {
+        const int64_t s0 = r * nsub[c] / Rc, s1 = (r + 1) * nsub[c] / Rc;
+        C.cell_cls.push_back(c);
+        for (int64_t q = 0; q < ng; ++q) {
+          C.cell_x.push_back(g0 + q < ns ? hot_items[sl[g0 + q].h] : -1);
+          C.cell_out.push_back(-1);
+        }
+        for (int64_t st = s0; st < s1; ++st) {
+          C.cell_steps.push_back(step0 + static_cast<int32_t>(sub_base[c] + st));
+          for (int64_t q = 0; q < ng; ++q) {
+            if (g0 + q >= ns) { empty_run(C); continue; }
+            const Slot &z = sl[g0 + q];
+            const int64_t *o = bnd.data() + hc_base[static_cast<int64_t>(z.h) * p.nclass + c];
+            run.clear();
+            for (int64_t e = o[st]; e < o[st + 1]; ++e)
+              if (local(a[e]) % z.m == z.r) run.push_back(a[e]);
+            append_run(C, run, 0, static_cast<int64_t>(run.size()), local, L.val);
+          }
+        }
+        C.cell_step_ptr.push_back(static_cast<int32_t>(C.cell_steps.size()));
+        for (int64_t q = 0; q < ng && g0 + q < ns; ++q) extra[hot_items[sl[g0 + q].h]] += 1;
+      }
+    }
+  }
+}
+
 // cell_out of every used (cell, group): the next of x's cell rows from cell_base[x] on
 void assign_cell_rows(CellSet &C, std::vector<int64_t> cell_base) {
   for (size_t k = 0; k < C.cell_x.size(); ++k)
@@ -380,16 +590,64 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
         for (int64_t t = lo; t < hi; ++t) blk[t] = block_of(p.seed, p.B, user[t], item[t]);
       });
     }
-    // ---- canonical order: stable LSD counting sorts by item, then user, then block
-    std::vector<int64_t> a(static_cast<size_t>(n)), b(static_cast<size_t>(n));
-    std::iota(a.begin(), a.end(), int64_t(0));
-    counting_pass(a, b, M, [&](int64_t x) { return item[x]; });
-    counting_pass(b, a, N, [&](int64_t x) { return user[x]; });
-    if (p.B > 1) {
-      counting_pass(a, b, p.B, [&](int64_t x) { return blk[x]; });
-      a.swap(b);
+    // ---- canonical order (block, user, item, load index): a parallel stable counting sort
+    // by (block, user) -- each thread scatters its own contiguous slice of the input, so
+    // equal keys keep their load order -- then each (block, user) segment sorted by
+    // (item, load index)
+    std::vector<int64_t> a(static_cast<size_t>(n));
+    const int64_t nkeys = static_cast<int64_t>(p.B) * N;
+    if (nkeys > 4 * n + (int64_t(1) << 22)) {
+      // many blocks and few ratings: stable LSD counting passes by item, user, block
+      std::vector<int64_t> b(static_cast<size_t>(n));
+      std::iota(a.begin(), a.end(), int64_t(0));
+      counting_pass(a, b, M, [&](int64_t x) { return item[x]; });
+      counting_pass(b, a, N, [&](int64_t x) { return user[x]; });
+      if (p.B > 1) {
+        counting_pass(a, b, p.B, [&](int64_t x) { return blk[x]; });
+        a.swap(b);
+      }
+    } else {
+      auto key = [&](int64_t t) { return (p.B > 1 ? static_cast<int64_t>(blk[t]) * N : 0) + user[t]; };
+      const int T = n >= (1 << 20) ? std::max(1, std::min<int>(p.threads, static_cast<int>((int64_t(1) << 28) / (nkeys + 1)))) : 1;
+      std::vector<std::vector<int64_t>> cnt(static_cast<size_t>(T));
+      std::vector<int64_t> seg(static_cast<size_t>(nkeys) + 1, 0);
+      std::vector<std::thread> pool;
+      auto each = [&](auto &&fn) {
+        if (T == 1) {
+          fn(0);
+          return;
+        }
+        pool.clear();
+        for (int t = 0; t < T; ++t) pool.emplace_back([&fn, t] { fn(t); });
+        for (auto &th : pool) th.join();
+      };
+      each([&](int t) {
+        cnt[t].assign(static_cast<size_t>(nkeys), 0);
+        for (int64_t x = n * t / T; x < n * (t + 1) / T; ++x) cnt[t][key(x)] += 1;
+      });
+      // exclusive offsets: key-major, thread-minor
+      for (int64_t k = 0; k < nkeys; ++k) {
+        int64_t tot = 0;
+        for (int t = 0; t < T; ++t) {
+          const int64_t c = cnt[t][k];
+          cnt[t][k] = seg[k] + tot;
+          tot += c;
+        }
+        seg[k + 1] = seg[k] + tot;
+      }
+      each([&](int t) {
+        std::vector<int64_t> &o = cnt[t];
+        for (int64_t x = n * t / T; x < n * (t + 1) / T; ++x) a[o[key(x)]++] = x;
+      });
+      std::vector<std::vector<int64_t>>().swap(cnt);
+      each([&](int t) {
+        for (int64_t k = nkeys * t / T; k < nkeys * (t + 1) / T; ++k)
+          if (seg[k + 1] - seg[k] > 1)
+            std::sort(a.begin() + seg[k], a.begin() + seg[k + 1], [&](int64_t x, int64_t y) {
+              return item[x] != item[y] ? item[x] < item[y] : x < y;
+            });
+      });
     }
-    std::vector<int64_t>().swap(b);
     // ---- worker class of each user; class-pure user tiles for the item-major sweep
     std::vector<int32_t> ucls(static_cast<size_t>(N));
     for (int64_t i = 0; i < N; ++i) ucls[i] = p.cls_of_worker[p.owner[i]];
@@ -418,45 +676,64 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
       L.icount.assign(static_cast<size_t>(M), 0);
       L.icount_cls.assign(static_cast<size_t>(M * p.nclass), 0);
       std::vector<int32_t> ent_user(static_cast<size_t>(nb));
+      parallel_for(p.threads, nb, [&](int64_t x0, int64_t x1) {
+        for (int64_t x = x0; x < x1; ++x) ent_user[x] = user[L.perm[x]];
+      });
       for (int64_t x = 0; x < nb; ++x) {
-        const int64_t t = L.perm[x];
-        ent_user[x] = user[t];
-        L.ucount[user[t]] += 1;
-        L.icount[item[t]] += 1;
-        L.icount_cls[static_cast<size_t>(item[t]) * p.nclass + ucls[user[t]]] += 1;
+        const int32_t u = ent_user[x], j = L.col[x];
+        L.ucount[u] += 1;
+        L.icount[j] += 1;
+        L.icount_cls[static_cast<size_t>(j) * p.nclass + ucls[u]] += 1;
       }
       L.row_ptr.assign(static_cast<size_t>(N) + 1, 0);
       for (int64_t i = 0; i < N; ++i) L.row_ptr[i + 1] = L.row_ptr[i] + L.ucount[i];
 
-      // ---- cells (the dense part: heavy users, staged through LDS) and units (the rest)
+      // ---- cells (the dense part, staged through LDS) and units (the rest).  Heavy users'
+      // ratings all go to cells; with hot_steps > 0 so do the other users' ratings of the
+      // hot_steps * cell_rows most rated items of the block.
+      const bool use_cells = p.cell_rows > 0 && p.cell_groups > 0;
       std::vector<uint8_t> heavy(static_cast<size_t>(N), 0);
-      if (p.cell_rows > 0 && p.cell_groups > 0)
+      if (use_cells)
         for (int64_t i = 0; i < N; ++i) heavy[i] = L.ucount[i] >= p.heavy_min;
-      std::vector<uint8_t> in_units(static_cast<size_t>(nb));
-      for (int64_t x = 0; x < nb; ++x) in_units[x] = !heavy[ent_user[x]];
-      std::vector<int64_t> extra_u, extra_i, base_u, base_i;
-      if (p.cell_rows > 0 && p.cell_groups > 0) {
-        build_user_cells(p, L, ucls, heavy, L.cells_user, extra_u);
-        build_item_cells(p, L, ucls, heavy, ent_user, L.cells_item, extra_i);
+      std::vector<int32_t> hot_items, hot_pos(static_cast<size_t>(M), -1);
+      if (use_cells && p.hot_steps > 0) {
+        hot_items.resize(static_cast<size_t>(M));
+        std::iota(hot_items.begin(), hot_items.end(), 0);
+        std::stable_sort(hot_items.begin(), hot_items.end(),
+                         [&](int32_t x, int32_t y) { return L.icount[x] > L.icount[y]; });
+        hot_items.resize(static_cast<size_t>(std::min<int64_t>(M, int64_t(p.hot_steps) * p.cell_rows)));
+        while (!hot_items.empty() && L.icount[hot_items.back()] == 0) hot_items.pop_back();
+        for (size_t h = 0; h < hot_items.size(); ++h) hot_pos[hot_items[h]] = static_cast<int32_t>(h);
       }
+      std::vector<uint8_t> in_units(static_cast<size_t>(nb));
+      for (int64_t x = 0; x < nb; ++x) in_units[x] = !heavy[ent_user[x]] && hot_pos[L.col[x]] < 0;
       // ---- units.  Tiles start at the L2-sized row count and grow (x2) while the units
       // would average fewer than 16 ratings (each unit costs one partial row).
       const int64_t min_avg = 16;
       int64_t n_units_entries = 0;
       for (int64_t x = 0; x < nb; ++x) n_units_entries += in_units[x];
+      // The two sweep directions only read the block's arrays: build them concurrently.
+      std::vector<int64_t> extra_u, extra_i, base_u, base_i;
+      std::exception_ptr user_side_error;
+      std::thread user_side([&] {
+      try {
+      if (use_cells) {
+        build_user_cells(p, L, ucls, heavy, L.cells_user, extra_u);
+        build_user_cells_hot(p, L, ucls, heavy, hot_pos, hot_items, L.cells_user, extra_u);
+      }
       // user-major: x = user, y = item, tile = (class, item range)
       {
         const std::function<int32_t(int64_t)> xr = [&](int64_t e) { return ent_user[e]; };
         const std::function<int32_t(int64_t)> yr = [&](int64_t e) { return L.col[e]; };
         int64_t rows = std::max<int64_t>(1, std::min<int64_t>(p.tile_rows_item, M));
-        std::vector<int64_t> by_x(static_cast<size_t>(nb)), last;
+        std::vector<int64_t> by_x(static_cast<size_t>(nb));
         std::iota(by_x.begin(), by_x.end(), int64_t(0));  // canonical is sorted by user
         for (;;) {
           const int64_t nt = (M + rows - 1) / rows;
           const std::function<int32_t(int64_t)> tl = [&, rows, nt](int64_t e) {
             return static_cast<int32_t>(ucls[ent_user[e]] * nt + L.col[e] / rows);
           };
-          if (rows >= M || count_runs(nb, by_x, xr, tl, nt * p.nclass, in_units, last) * min_avg <= n_units_entries)
+          if (rows >= M || count_runs(nb, by_x, xr, tl, nt * p.nclass, in_units, p.threads) * min_avg <= n_units_entries)
             break;
           rows *= 2;
         }
@@ -469,11 +746,23 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
         assign_cell_rows(L.cells_user, base_u);
         L.partial_rows_user = L.by_user.x_pp[N];
       }
+      } catch (...) {
+        user_side_error = std::current_exception();
+      }
+      });
+      struct Join {
+        std::thread &t;
+        ~Join() { if (t.joinable()) t.join(); }
+      } join_user_side{user_side};
+      if (use_cells) {
+        build_item_cells(p, L, ucls, heavy, ent_user, L.cells_item, extra_i);
+        build_item_cells_hot(p, L, ucls, heavy, ent_user, hot_pos, hot_items, L.cells_item, extra_i);
+      }
       // item-major: x = item, y = user, tile = class-pure user range
       {
         const std::function<int32_t(int64_t)> xr = [&](int64_t e) { return L.col[e]; };
         const std::function<int32_t(int64_t)> yr = [&](int64_t e) { return ent_user[e]; };
-        std::vector<int64_t> by_x(static_cast<size_t>(nb)), tmp(static_cast<size_t>(nb)), last;
+        std::vector<int64_t> by_x(static_cast<size_t>(nb)), tmp(static_cast<size_t>(nb));
         std::iota(tmp.begin(), tmp.end(), int64_t(0));
         counting_pass(tmp, by_x, M, xr);
         std::vector<int64_t>().swap(tmp);
@@ -491,7 +780,7 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
             return static_cast<int32_t>(cls_base[ucls[u]] + rank_in_cls[u] / rows);
           };
           if (rows >= N ||
-              count_runs(nb, by_x, xr, tl, std::max<int64_t>(nt, 1), in_units, last) * min_avg <= n_units_entries)
+              count_runs(nb, by_x, xr, tl, std::max<int64_t>(nt, 1), in_units, p.threads) * min_avg <= n_units_entries)
             break;
           rows *= 2;
         }
@@ -508,12 +797,149 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
         assign_cell_rows(L.cells_item, base_i);
         L.partial_rows_item = L.by_item.x_pp[M];
       }
+      user_side.join();
+      if (user_side_error) std::rethrow_exception(user_side_error);
     }
     return 0;
   } catch (const std::bad_alloc &) {
     err = "host allocation failed while building the layout";
     return -2;
   }
+}
+
+namespace {
+
+struct Triple {
+  int32_t x, y;
+  float v;
+  bool operator<(const Triple &o) const {
+    if (x != o.x) return x < o.x;
+    if (y != o.y) return y < o.y;
+    return std::memcmp(&v, &o.v, sizeof v) < 0;
+  }
+  bool operator==(const Triple &o) const { return x == o.x && y == o.y && std::memcmp(&v, &o.v, sizeof v) == 0; }
+};
+
+// one direction: `want` holds the block's (x, y, value) triples; ucls_of_entry(x, y) is the
+// class the unit or cell must read
+int check_direction(const char *dir, int64_t nx, int64_t ny, std::vector<Triple> want, const UnitSet &U,
+                    const CellSet &C, const std::function<int32_t(int32_t, int32_t)> &cls_of, std::string &err) {
+  auto bad = [&](const std::string &what) {
+    err = std::string(dir) + ": " + what;
+    return -1;
+  };
+  std::vector<Triple> got;
+  got.reserve(want.size());
+  const int64_t nunits = static_cast<int64_t>(U.unit_x.size());
+  if (U.x_pp.size() != static_cast<size_t>(nx) + 1) return bad("x_pp has the wrong length");
+  const int64_t nrows = U.x_pp[nx];
+  std::vector<int32_t> written(static_cast<size_t>(nrows), 0);
+  if (nunits % kWaveUnits) return bad("unit count is not a multiple of the wave size");
+  for (int64_t w = 0; w < nunits; w += kWaveUnits)
+    for (int64_t k = w + 1; k < w + kWaveUnits; ++k)
+      if (U.unit_cls[k] != U.unit_cls[w]) return bad("units of one wave read different classes");
+  for (int x = 0; x < kXcds; ++x)
+    if (U.xcd_off[x] > U.xcd_off[x + 1] || U.xcd_off[x] % kWaveUnits) return bad("bad XCD chunk offsets");
+  if (U.xcd_off[0] != 0 || U.xcd_off[kXcds] != nunits) return bad("XCD chunks do not cover the units");
+  for (int64_t k = 0; k < nunits; ++k) {
+    const int32_t x = U.unit_x[k], len = U.unit_len[k], out = U.unit_out[k];
+    const int64_t beg = U.unit_beg[k];
+    if (len == 0) {
+      if (out != nrows) return bad("an empty unit does not write the spare row");
+      continue;
+    }
+    if (x < 0 || x >= nx) return bad("unit row out of range");
+    if (beg % kUnitAlign || beg + (len + kUnitAlign - 1) / kUnitAlign * kUnitAlign > static_cast<int64_t>(U.y.size()))
+      return bad("unit entries misaligned or out of range");
+    if (out < U.x_pp[x] || out >= U.x_pp[x + 1]) return bad("unit writes a partial row of another x");
+    written[out] += 1;
+    for (int64_t t = beg; t < beg + len; ++t) {
+      const int32_t y = U.y[t];
+      if (y < 0 || y >= ny) return bad("unit gathers a row out of range");
+      if (cls_of(x, y) != U.unit_cls[k]) return bad("unit reads the slot of another class");
+      got.push_back({x, y, U.val[t]});
+    }
+    for (int64_t t = beg + len; t < beg + (len + kUnitAlign - 1) / kUnitAlign * kUnitAlign; ++t)
+      if (U.y[t] != 0 || U.val[t] != 0.f) return bad("unit padding is not (row 0, value 0)");
+  }
+  const int64_t ncells = static_cast<int64_t>(C.cell_cls.size());
+  if (ncells > 0) {
+    const int64_t ng = C.ng, ts = C.ts;
+    if (C.cell_step_ptr.size() != static_cast<size_t>(ncells) + 1 || C.cell_x.size() != static_cast<size_t>(ncells * ng) ||
+        C.cell_out.size() != C.cell_x.size() || C.run_beg.size() != C.cell_steps.size() * static_cast<size_t>(ng) ||
+        C.run_len.size() != C.run_beg.size() || C.step_rows.size() % static_cast<size_t>(ts))
+      return bad("cell arrays have inconsistent lengths");
+    const int64_t nsteps = static_cast<int64_t>(C.step_rows.size()) / ts;
+    for (int64_t c = 0; c < ncells; ++c) {
+      if (C.cell_step_ptr[c] > C.cell_step_ptr[c + 1]) return bad("cell step pointers decrease");
+      for (int64_t q = 0; q < ng; ++q) {
+        const int32_t x = C.cell_x[c * ng + q], out = C.cell_out[c * ng + q];
+        if (x >= nx) return bad("cell row out of range");
+        if (x < 0 && out >= 0) return bad("an unused cell group writes a partial row");
+        if (x >= 0) {
+          if (out < U.x_pp[x] || out >= U.x_pp[x + 1]) return bad("cell writes a partial row of another x");
+          written[out] += 1;
+        }
+        for (int64_t k = C.cell_step_ptr[c]; k < C.cell_step_ptr[c + 1]; ++k) {
+          const int64_t st = C.cell_steps[k];
+          if (st < 0 || st >= nsteps) return bad("cell step out of range");
+          const int64_t beg = C.run_beg[k * ng + q], len = C.run_len[k * ng + q];
+          if (x < 0 && len) return bad("an unused cell group has ratings");
+          if (beg % kUnitAlign || beg + (len + kUnitAlign - 1) / kUnitAlign * kUnitAlign > static_cast<int64_t>(C.ly.size()))
+            return bad("cell run misaligned or out of range");
+          for (int64_t t = beg; t < beg + len; ++t) {
+            if (C.ly[t] >= ts) return bad("cell index beyond the sub-tile");
+            const int32_t y = C.step_rows[st * ts + C.ly[t]];
+            if (y < 0 || y >= ny) return bad("cell rating reads an empty or out-of-range staged row");
+            if (cls_of(x, y) != C.cell_cls[c]) return bad("cell reads the slot of another class");
+            got.push_back({x, y, C.lv[t]});
+          }
+          for (int64_t t = beg + len; t < beg + (len + kUnitAlign - 1) / kUnitAlign * kUnitAlign; ++t)
+            if (C.ly[t] != 0 || C.lv[t] != 0.f) return bad("cell padding is not (row 0, value 0)");
+        }
+      }
+    }
+    for (int32_t r : C.step_rows)
+      if (r < -1 || r >= ny) return bad("staged row out of range");
+  }
+  for (int64_t r = 0; r < nrows; ++r)
+    if (written[r] != 1) return bad("partial row " + std::to_string(r) + " is written " + std::to_string(written[r]) + " times");
+  if (got.size() != want.size())
+    return bad("units and cells hold " + std::to_string(got.size()) + " ratings, the block " + std::to_string(want.size()));
+  std::sort(got.begin(), got.end());
+  std::sort(want.begin(), want.end());
+  for (size_t t = 0; t < got.size(); ++t)
+    if (!(got[t] == want[t])) return bad("units and cells do not hold the block's ratings exactly once");
+  return 0;
+}
+
+}  // namespace
+
+int check_layout(const LayoutParams &p, const BlockLayout &L, std::string &err) {
+  const int64_t N = p.users, M = p.items;
+  std::vector<int32_t> ucls(static_cast<size_t>(N));
+  for (int64_t i = 0; i < N; ++i) ucls[i] = p.cls_of_worker[p.owner[i]];
+  std::vector<Triple> by_user, by_item;
+  by_user.reserve(static_cast<size_t>(L.nnz));
+  by_item.reserve(static_cast<size_t>(L.nnz));
+  for (int64_t i = 0; i < N; ++i)
+    for (int64_t e = L.row_ptr[i]; e < L.row_ptr[i + 1]; ++e) {
+      by_user.push_back({static_cast<int32_t>(i), L.col[e], L.val[e]});
+      by_item.push_back({L.col[e], static_cast<int32_t>(i), L.val[e]});
+    }
+  if (static_cast<int64_t>(by_user.size()) != L.nnz) {
+    err = "row pointers do not cover the block";
+    return -1;
+  }
+  const std::function<int32_t(int32_t, int32_t)> cu = [&](int32_t x, int32_t) { return ucls[x]; };
+  const std::function<int32_t(int32_t, int32_t)> ci = [&](int32_t, int32_t y) { return ucls[y]; };
+  if (check_direction("user-major", N, M, std::move(by_user), L.by_user, L.cells_user, cu, err)) return -1;
+  if (check_direction("item-major", M, N, std::move(by_item), L.by_item, L.cells_item, ci, err)) return -1;
+  if (L.partial_rows_user != L.by_user.x_pp[N] || L.partial_rows_item != L.by_item.x_pp[M]) {
+    err = "partial row counts disagree with the row offsets";
+    return -1;
+  }
+  return 0;
 }
 
 }  // namespace psmf

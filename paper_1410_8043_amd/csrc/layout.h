@@ -53,8 +53,9 @@ struct UnitSet {
 // sequence of steps; a step is a sub-tile of ts gathered rows that the workgroup copies
 // into LDS before every lane group sweeps its row's ratings inside the sub-tile:
 //   user-major: x = heavy users of one class (similar degree), steps = item ranges;
+//               x = light users of one class, steps = the sub-tiles of the hot items;
 //   item-major: x = items (similar heavy-rater count), steps = ranges of the class's
-//               heavy users.
+//               heavy users; x = hot items, steps = ranges of the class's light users.
 // The ratings of (cell, k-th step, group) are ly/lv[run_beg .. run_beg + run_len): ly the
 // row's position inside the sub-tile.  Runs start at multiples of kUnitAlign and are
 // padded to one.  Each used (cell, group) writes one partial row cell_out.
@@ -101,12 +102,21 @@ struct LayoutParams {
   int32_t cell_rows = 0;            // ts: gathered rows per LDS sub-tile (0: no cells)
   int32_t cell_groups = 0;          // ng: lane groups per cell workgroup
   int64_t heavy_min = 1 << 30;      // users with at least this many ratings in the block go to cells
-  int32_t cell_target = 1024;       // about this many user-major cells in total
+  int32_t cell_target = 1024;       // about this many cells per family and direction
+  int32_t hot_steps = 0;            // sub-tiles of the most rated items whose ratings by the other
+                                    // (light) users also go to cells
 };
 
 // Validates the COO input (EINVAL message in err) and fills one BlockLayout per block.
 // Returns 0, -1 (invalid input) or -2 (allocation failure).
 int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item, const float *val, int64_t n,
                  std::vector<BlockLayout> &out, std::string &err);
+
+// Self-check of one block's layout against its canonical entries: in each sweep direction
+// the units and cells together hold every entry exactly once (same stationary row,
+// gathered row and value), every unit and cell reads the ring slot of its ratings' user
+// class (wave-uniform for units), padding is (row 0, value 0), and the partial rows of
+// each x are written exactly once each.  Returns 0, or -1 with err naming the first fault.
+int check_layout(const LayoutParams &p, const BlockLayout &L, std::string &err);
 
 }  // namespace psmf

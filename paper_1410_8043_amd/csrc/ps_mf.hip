@@ -42,8 +42,16 @@
 namespace {
 
 constexpr int kBlock = 256;       // threads per workgroup of the small kernels (4 wavefronts)
-constexpr int kSweepBlock = 1024; // threads per workgroup of the sweep (16 wavefronts: one per CU)
-constexpr int kTileFloats = 32768; // LDS sub-tile of a cell: 128 KiB = ts rows of Kp floats
+#ifndef PS_MF_CELL_THREADS
+#define PS_MF_CELL_THREADS 1024
+#endif
+#ifndef PS_MF_CELL_TILE_FLOATS
+#define PS_MF_CELL_TILE_FLOATS 32768
+#endif
+constexpr int kSweepBlock = PS_MF_CELL_THREADS;     // threads per cell workgroup (1024: 16 wavefronts)
+constexpr int kTileFloats = PS_MF_CELL_TILE_FLOATS; // LDS sub-tile of a cell (32768: 128 KiB = ts rows of Kp floats)
+static_assert(kSweepBlock % 256 == 0 && kSweepBlock <= 1024, "cell workgroups hold whole 256-thread quarters");
+static_assert(kTileFloats % 512 == 0 && kTileFloats * 4 <= 160 * 1024, "a cell sub-tile holds whole 512-wide rows in LDS");
 constexpr int kLossSegment = 512;  // ratings per lane group of the loss
 constexpr int kMaxKp = 512;
 constexpr int kXcds = psmf::kXcds;
@@ -55,6 +63,9 @@ constexpr int kRowsInFlight = PS_MF_ROWS_IN_FLIGHT;  // gathered rows loaded bef
 // at 128 per lane with 16 wavefronts per CU)
 template <int E>
 constexpr int rows_in_flight() { return E >= 32 ? 1 : kRowsInFlight; }
+// the cells also hold the next 8 (row, value) pairs: two rows in flight from 16 floats on
+template <int E>
+constexpr int cell_rows_in_flight() { return E >= 32 ? 1 : E >= 16 ? 2 : kRowsInFlight; }
 
 // ------------------------------------------------------------------ device helpers
 // A factor row of Kp = G*E floats is spread over a lane group of G lanes: lane g holds the
@@ -76,6 +87,31 @@ __device__ __forceinline__ void store_row(float *__restrict__ row, const float (
     *reinterpret_cast<float4 *>(row + 4 * (q * G + g)) = make_float4(d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]);
 }
 
+// LDS rows of a cell: with G = 8 lanes per group, the two groups of a 16-lane LDS access
+// would read the same 32 of the 64 banks (rows are multiples of 512 bytes apart); odd
+// groups therefore hold their chunks in the order 1,0,3,2,... (register chunk h is row
+// chunk h ^ 1) and the pair reads different halves.  The stationary row and the partial
+// row of such a group use the same order.
+template <int G, int E>
+constexpr bool swizzled() { return G == 8 && E >= 8; }
+
+template <int G, int E>
+__device__ __forceinline__ void load_row_sw(float (&d)[E], const float *__restrict__ row, int g, int rot) {
+#pragma unroll
+  for (int q = 0; q < E / 4; ++q) {
+    const float4 t = *reinterpret_cast<const float4 *>(row + 4 * ((q ^ rot) * G + g));
+    d[4 * q] = t.x; d[4 * q + 1] = t.y; d[4 * q + 2] = t.z; d[4 * q + 3] = t.w;
+  }
+}
+
+template <int G, int E>
+__device__ __forceinline__ void store_row_sw(float *__restrict__ row, const float (&d)[E], int g, int rot) {
+#pragma unroll
+  for (int q = 0; q < E / 4; ++q)
+    *reinterpret_cast<float4 *>(row + 4 * ((q ^ rot) * G + g)) =
+        make_float4(d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]);
+}
+
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
@@ -85,10 +121,12 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 template <int G>
 __device__ __forceinline__ float group_sum(float v) {
   static_assert(G == 2 || G == 4 || G == 8 || G == 16, "lane groups live inside one DPP row");
-  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
-  if constexpr (G >= 4) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));
-  if constexpr (G >= 8) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, false));
-  if constexpr (G >= 16) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, false));
+  // every source lane of these patterns lies inside the row, so bound_ctrl (zero for an
+  // invalid source) never applies; with it the compiler folds each move into v_add_f32_dpp
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, true));
+  if constexpr (G >= 4) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, true));
+  if constexpr (G >= 8) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, true));
+  if constexpr (G >= 16) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, true));
   return v;
 }
 
@@ -166,9 +204,17 @@ __device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g)
   load_row<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  // the next 8 (row, value) pairs are loaded while the current 8 are swept
+  i32x4 ni0 = {0, 0, 0, 0}, ni1 = {0, 0, 0, 0};
+  f32x4 nv0 = {0.f, 0.f, 0.f, 0.f}, nv1 = {0.f, 0.f, 0.f, 0.f};
+  if (n > 0) { ni0 = yi[0]; ni1 = yi[1]; nv0 = vr[0]; nv1 = vr[1]; }
   for (int t0 = 0; t0 < n; t0 += 8) {
-    const i32x4 i0 = yi[t0 / 4], i1 = yi[t0 / 4 + 1];
-    const f32x4 v0 = vr[t0 / 4], v1 = vr[t0 / 4 + 1];
+    const i32x4 i0 = ni0, i1 = ni1;
+    const f32x4 v0 = nv0, v1 = nv1;
+    if (t0 + 8 < n) {
+      ni0 = yi[t0 / 4 + 2]; ni1 = yi[t0 / 4 + 3];
+      nv0 = vr[t0 / 4 + 2]; nv1 = vr[t0 / 4 + 3];
+    }
     const int idx[8] = {i0[0], i0[1], i0[2], i0[3], i1[0], i1[1], i1[2], i1[3]};
     const float val[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
 #pragma unroll
@@ -180,8 +226,9 @@ __device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g)
         load_row_rsrc<G, E>(y[w], ys, static_cast<uint32_t>(idx[q + w]) * (Kp * 4u), g);
 #pragma unroll
       for (int w = 0; w < RF; ++w) {
-        // padding entries (past the unit's n ratings) contribute nothing
-        const float err = (t0 + q + w < n) ? residual<G, E>(x, y[w], val[q + w]) : 0.f;
+        // padding entries (row 0, value 0, past the unit's n ratings) contribute nothing
+        const float e_all = residual<G, E>(x, y[w], val[q + w]);
+        const float err = (t0 + q + w < n) ? e_all : 0.f;
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] = fmaf(err, y[w][e], acc[e]);
       }
@@ -209,7 +256,7 @@ struct CellArgs {
 template <int G, int E>
 __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4 *tile) {
   constexpr int Kp = G * E;
-  constexpr int RF = rows_in_flight<E>();
+  constexpr int RF = cell_rows_in_flight<E>();
   constexpr int NG = kSweepBlock / G;
   constexpr int Q4 = Kp / 4;  // float4 per row
   const int g = threadIdx.x & (G - 1);
@@ -218,10 +265,13 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
   const float *__restrict__ V = c.ring + sv * c.slot_stride;
   const float4 *__restrict__ Y4 = reinterpret_cast<const float4 *>(V + c.y_off);
   const int32_t xr = c.cell_x[cell * NG + grp];
+  const int rot = swizzled<G, E>() ? (grp & 1) : 0;
+  const uint32_t lane_bytes = static_cast<uint32_t>(rot * G + g) * 16u;  // < 32 * G: below a row's size
+  const char *tile_bytes = reinterpret_cast<const char *>(tile);
   float x[E], acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) { x[e] = 0.f; acc[e] = 0.f; }
-  if (xr >= 0) load_row<G, E>(x, V + c.x_off + static_cast<int64_t>(xr) * Kp, g);
+  if (xr >= 0) load_row_sw<G, E>(x, V + c.x_off + static_cast<int64_t>(xr) * Kp, g, rot);
   const int32_t k0 = c.cell_step_ptr[cell], k1 = c.cell_step_ptr[cell + 1];
   for (int32_t k = k0; k < k1; ++k) {
     const int32_t *rows = c.step_rows + static_cast<int64_t>(c.cell_steps[k]) * c.ts;
@@ -230,14 +280,35 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
       const int32_t r = rows[idx / Q4];
       tile[idx] = r >= 0 ? Y4[static_cast<int64_t>(r) * Q4 + idx % Q4] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    __syncthreads();
     const int32_t beg = c.run_beg[static_cast<int64_t>(k) * NG + grp];
     const int n = c.run_len[static_cast<int64_t>(k) * NG + grp];
     const uint16_t *__restrict__ li = c.ly + beg;
     const float *__restrict__ lv = c.lv + beg;
+    // the first 8 (row, value) pairs are loaded before the barrier, then always the next 8
+    // while the current 8 are swept
+    uint4 ni = make_uint4(0u, 0u, 0u, 0u);
+    f32x4 nv0 = {0.f, 0.f, 0.f, 0.f}, nv1 = {0.f, 0.f, 0.f, 0.f};
+    if (n > 0) {
+      ni = *reinterpret_cast<const uint4 *>(li);
+      nv0 = *reinterpret_cast<const f32x4 *>(lv);
+      nv1 = *reinterpret_cast<const f32x4 *>(lv + 4);
+    }
+    __syncthreads();
     for (int t0 = 0; t0 < n; t0 += 8) {
-      const uint4 i8 = *reinterpret_cast<const uint4 *>(li + t0);  // 8 x uint16
-      const f32x4 v0 = *reinterpret_cast<const f32x4 *>(lv + t0), v1 = *reinterpret_cast<const f32x4 *>(lv + t0 + 4);
+      if constexpr (E >= 32) {  // 512-wide rows: no registers to spare for the prefetch
+        if (t0 > 0) {
+          ni = *reinterpret_cast<const uint4 *>(li + t0);
+          nv0 = *reinterpret_cast<const f32x4 *>(lv + t0);
+          nv1 = *reinterpret_cast<const f32x4 *>(lv + t0 + 4);
+        }
+      }
+      const uint4 i8 = ni;  // 8 x uint16
+      const f32x4 v0 = nv0, v1 = nv1;
+      if (E < 32 && t0 + 8 < n) {
+        ni = *reinterpret_cast<const uint4 *>(li + t0 + 8);
+        nv0 = *reinterpret_cast<const f32x4 *>(lv + t0 + 8);
+        nv1 = *reinterpret_cast<const f32x4 *>(lv + t0 + 12);
+      }
       const int idx[8] = {static_cast<int>(i8.x & 0xffff), static_cast<int>(i8.x >> 16),
                           static_cast<int>(i8.y & 0xffff), static_cast<int>(i8.y >> 16),
                           static_cast<int>(i8.z & 0xffff), static_cast<int>(i8.z >> 16),
@@ -249,15 +320,20 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
         float y[RF][E];
 #pragma unroll
         for (int w = 0; w < RF; ++w) {
+          // byte address of register chunk 0 (even chunks) and chunk 1 (odd chunks) of the row
+          const uint32_t b0 = (static_cast<uint32_t>(idx[q + w]) * (Kp * 4u)) | lane_bytes;
+          const uint32_t b1 = swizzled<G, E>() ? (b0 ^ (G * 16u)) : (b0 + G * 16u);
 #pragma unroll
           for (int h = 0; h < E / 4; ++h) {
-            const float4 tt = tile[idx[q + w] * Q4 + h * G + g];
+            const float4 tt = *reinterpret_cast<const float4 *>(tile_bytes + ((h & 1) ? b1 : b0) + (h & ~1) * G * 16);
             y[w][4 * h] = tt.x; y[w][4 * h + 1] = tt.y; y[w][4 * h + 2] = tt.z; y[w][4 * h + 3] = tt.w;
           }
         }
 #pragma unroll
         for (int w = 0; w < RF; ++w) {
-          const float err = (t0 + q + w < n) ? residual<G, E>(x, y[w], val[q + w]) : 0.f;
+          // padding entries (row 0, value 0, past the run's n ratings) contribute nothing
+          const float e_all = residual<G, E>(x, y[w], val[q + w]);
+          const float err = (t0 + q + w < n) ? e_all : 0.f;
 #pragma unroll
           for (int e = 0; e < E; ++e) acc[e] = fmaf(err, y[w][e], acc[e]);
         }
@@ -265,7 +341,7 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
     }
   }
   const int32_t out = c.cell_out[cell * NG + grp];
-  if (out >= 0) store_row<G, E>(c.partial + static_cast<int64_t>(out) * Kp, acc, g);
+  if (out >= 0) store_row_sw<G, E>(c.partial + static_cast<int64_t>(out) * Kp, acc, g, rot);
 }
 
 // The LDS-staged cells of both sweep directions in one launch (one 1024-thread workgroup
@@ -415,49 +491,59 @@ struct CommitArgs {
 };
 
 // R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class n_j^(class) R^{v(class)}_j).
-// One thread per 4 columns.
-__device__ __forceinline__ void commit_items(const CommitArgs &a, int64_t idx) {
-  const int64_t q4 = a.Kp / 4;
-  if (idx >= a.items * q4) return;
-  const int64_t j = idx / q4;
+// One workgroup per item: thread t sums the float4 column t mod (Kp/4) of every
+// (kBlock / (Kp/4))-th partial row, starting at row t / (Kp/4); the column sums are then
+// added in row-lane order through LDS (popular items own thousands of partial rows).
+__device__ __forceinline__ void commit_item(const CommitArgs &a, int64_t j, float4 *red) {
+  const int q4 = a.Kp / 4;
+  const int lanes = kBlock / q4;  // row lanes: Kp is a power of two in [8, 512], so 2..128
+  const int k4 = static_cast<int>(threadIdx.x) % q4, lane = static_cast<int>(threadIdx.x) / q4;
   const int n = a.icount[j];
   float4 *R4 = reinterpret_cast<float4 *>(a.ring + a.r_off);
   const int64_t ss4 = a.slot_stride / 4;
-  const float4 rc = R4[a.slot_c * ss4 + idx];
-  float4 out = rc;
-  if (n > 0) {
-    const float4 *part4 = reinterpret_cast<const float4 *>(a.partial);
-    const int64_t k4 = idx - j * q4;
-    float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 4
-    for (int64_t p = a.item_pp[j]; p < a.item_pp[j + 1]; ++p) {
-      const float4 t = part4[p * q4 + k4];
-      d.x += t.x; d.y += t.y; d.z += t.z; d.w += t.w;
-    }
-    float4 lam = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int q = 0; q < a.nclass; ++q) {
-      const int cnt = a.icount_cls[j * a.nclass + q];
-      if (cnt) {
-        const float c = static_cast<float>(cnt);
-        const float4 r = R4[a.cls_slot[q] * ss4 + idx];
-        lam = make_float4(fmaf(c, r.x, lam.x), fmaf(c, r.y, lam.y), fmaf(c, r.z, lam.z), fmaf(c, r.w, lam.w));
-      }
-    }
-    const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
-    out = make_float4(rc.x + sc * (d.x - a.lambda * lam.x), rc.y + sc * (d.y - a.lambda * lam.y),
-                      rc.z + sc * (d.z - a.lambda * lam.z), rc.w + sc * (d.w - a.lambda * lam.w));
+  const int64_t idx = j * q4 + k4;
+  if (n == 0) {  // uniform over the workgroup
+    if (lane == 0) R4[a.slot_n * ss4 + idx] = R4[a.slot_c * ss4 + idx];
+    return;
   }
-  R4[a.slot_n * ss4 + idx] = out;
+  float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
+  const float4 *part4 = reinterpret_cast<const float4 *>(a.partial);
+#pragma unroll 4
+  for (int64_t p = a.item_pp[j] + lane; p < a.item_pp[j + 1]; p += lanes) {
+    const float4 t = part4[p * q4 + k4];
+    d.x += t.x; d.y += t.y; d.z += t.z; d.w += t.w;
+  }
+  red[threadIdx.x] = d;
+  __syncthreads();
+  if (lane != 0) return;
+  for (int l = 1; l < lanes; ++l) {
+    const float4 t = red[l * q4 + k4];
+    d.x += t.x; d.y += t.y; d.z += t.z; d.w += t.w;
+  }
+  const float4 rc = R4[a.slot_c * ss4 + idx];
+  float4 lam = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int q = 0; q < a.nclass; ++q) {
+    const int cnt = a.icount_cls[j * a.nclass + q];
+    if (cnt) {
+      const float c = static_cast<float>(cnt);
+      const float4 r = R4[a.cls_slot[q] * ss4 + idx];
+      lam = make_float4(fmaf(c, r.x, lam.x), fmaf(c, r.y, lam.y), fmaf(c, r.z, lam.z), fmaf(c, r.w, lam.w));
+    }
+  }
+  const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
+  R4[a.slot_n * ss4 + idx] = make_float4(rc.x + sc * (d.x - a.lambda * lam.x), rc.y + sc * (d.y - a.lambda * lam.y),
+                                         rc.z + sc * (d.z - a.lambda * lam.z), rc.w + sc * (d.w - a.lambda * lam.w));
 }
 
-// Version c+1 of both factors in one launch: workgroups [0, grid_users) finalize L, the
-// rest commit R (they write different rows of the new slot and read only partial rows and
-// versions <= c).
+// Version c+1 of both factors in one launch: workgroups [0, grid_users) finalize L (one
+// thread per 4 columns of a user), the rest commit R (one workgroup per item).  They write
+// different rows of the new slot and read only partial rows and versions <= c.
 __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, int32_t grid_users) {
+  __shared__ float4 red[kBlock];
   if (static_cast<int32_t>(blockIdx.x) < grid_users)
     finalize_users(fa, static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x);
   else
-    commit_items(ca, static_cast<int64_t>(blockIdx.x - grid_users) * kBlock + threadIdx.x);
+    commit_item(ca, static_cast<int64_t>(blockIdx.x) - grid_users, red);
 }
 
 // ------------------------------------------------------------------ kernel dispatch on Kp
@@ -583,6 +669,7 @@ struct ps_mf {
   hipStream_t side_stream = nullptr;  // runs the work units beside the cells (default priority)
   hipEvent_t fork = nullptr, join = nullptr;
   bool two_streams = true;
+  int32_t hot_steps = -1;  // LDS sub-tiles of hot items whose light-user ratings go to cells (-1: auto)
   float *ring = nullptr;
   float *partial_u = nullptr, *partial_i = nullptr;
   int32_t *ucls = nullptr;
@@ -858,8 +945,7 @@ int one_clock(ps_mf_t *h) {
   ca.eta = h->eta;
   ca.lambda = h->lambda;
   ca.rowmean = rowmean;
-  const int64_t ncommit = h->M * h->Kp / 4;
-  const int64_t grid_users = (nfin + kBlock - 1) / kBlock, grid_items = (ncommit + kBlock - 1) / kBlock;
+  const int64_t grid_users = (nfin + kBlock - 1) / kBlock, grid_items = h->M;
   hipLaunchKernelGGL(k_commit, dim3(static_cast<unsigned>(grid_users + grid_items)), dim3(kBlock), 0, h->stream, fa,
                      ca, static_cast<int32_t>(grid_users));
   HIP_TRY(h, hipGetLastError());
@@ -938,6 +1024,10 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
     case PS_MF_OPT_TWO_STREAMS:
       h->two_streams = value != 0;
       return PS_MF_OK;
+    case PS_MF_OPT_HOT_STEPS:
+      if (value < -1 || value > 1024) return fail(h, PS_MF_EINVAL, "hot item sub-tiles must be in [-1, 1024]");
+      h->hot_steps = static_cast<int32_t>(value);
+      return PS_MF_OK;
     case PS_MF_OPT_HEAVY_MIN:
       if (value < -1) return fail(h, PS_MF_EINVAL, "heavy threshold must be >= -1");
       h->heavy_min = value;
@@ -1006,13 +1096,22 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
     lp.cell_groups = kSweepBlock / shape_for(h->Kp).G;
     lp.heavy_min = h->heavy_min >= 0 ? h->heavy_min
                                       : std::max<int64_t>(256, 16 * h->M / lp.cell_rows);
+    // automatic: one sub-tile of hot items (at K = 128 on the 100M-rating workload one
+    // measured best among 0..4)
+    lp.hot_steps = h->hot_steps >= 0 ? h->hot_steps : 1;
   }
   std::string err;
   const int rc = psmf::build_layout(lp, user, item, value, n, h->layout, err);
   if (rc == -1) return fail(h, PS_MF_EINVAL, "%s", err.c_str());
   if (rc) return fail(h, PS_MF_ENOMEM, "%s", err.c_str());
+  if (h->host_only) {
+    for (int b = 0; b < h->B; ++b)
+      if (psmf::check_layout(lp, h->layout[b], err))
+        return fail(h, PS_MF_EINTERNAL, "layout self-check of block %d: %s", b, err.c_str());
+    h->loaded = true;
+    return PS_MF_OK;
+  }
   h->loaded = true;
-  if (h->host_only) return PS_MF_OK;
 
   int r = ensure_device(h);
   if (r) { h->loaded = false; return r; }

@@ -132,16 +132,40 @@ def test_empty_and_single_rating_layouts():
         assert np.array_equal(g.export_index(ps_mf.IDX_ITEM_COUNT), [0, 0, 0, 1])
 
 
-@pytest.mark.parametrize("cells,heavy_min", [(False, -1), (True, 1), (True, 40), (True, -1)])
+@pytest.mark.parametrize("cells,heavy_min,hot_steps", [(False, -1, 0), (True, 1, 0), (True, 40, 0), (True, -1, 0),
+                                                       (True, -1, 1), (True, 40, 3), (True, 1, 2), (True, -1, -1)])
 @pytest.mark.parametrize("K", [8, 128, 512])
-def test_host_layout_with_and_without_cells(cells, heavy_min, K):
-    """The exported integer layout does not depend on how the sweeps are scheduled."""
+def test_host_layout_with_and_without_cells(cells, heavy_min, hot_steps, K):
+    """The exported integer layout does not depend on how the sweeps are scheduled, and the
+    library's self-check (run on every host-only load) accepts each schedule."""
     from paper_1410_8043_amd import synth
     spec = synth.scaled(synth.CONFIGS["full"], 0.01)
     w = synth.generate(spec, K=1)
     with ps_mf.PsMf(spec.N, spec.M, K, spec.P, 3, 0.01, 0.05, host_only=True, cells=cells,
-                    heavy_min=heavy_min) as g:
+                    heavy_min=heavy_min, hot_steps=hot_steps) as g:
         g.load_ratings(w.user, w.item, w.val)
         o = oracle.Oracle(spec.N, spec.M, 4, spec.P, 3, 0.01, 0.05)
         o.load(w.user, w.item, w.val)
         compare_layout(g, o, 1, spec.N, spec.M)
+
+
+@pytest.mark.parametrize("policy,s", [(0, 0), (0, 2), (1, 3), (2, 4)])
+@pytest.mark.parametrize("B", [1, 3])
+def test_host_layout_self_check_with_hot_cells_and_custom_owner(policy, s, B):
+    """Cells of both families with several worker classes, minibatch blocks and an owner map
+    that scatters users over workers: the self-check holds and the exported layout is the
+    oracle's."""
+    rng = np.random.default_rng(100 * s + B)
+    N, M, P, n = 700, 300, 6, 60000
+    # a few dense users and items so that every cell family is populated
+    user = np.concatenate([rng.integers(0, N, n // 2), rng.integers(0, 24, n // 2)]).astype(np.int32)
+    item = np.concatenate([rng.integers(0, 40, n // 2), rng.integers(0, M, n // 2)]).astype(np.int32)
+    val = rng.integers(1, 6, user.size).astype(np.float32)
+    owner = rng.integers(0, P, N).astype(np.int32)
+    seed = 0x14108043 + 17 * B
+    with ps_mf.PsMf(N, M, 16, P, s, 0.01, 0.05, policy=policy, B=B, mb_seed=seed, owner=owner, host_only=True,
+                    cells=True, heavy_min=64, hot_steps=2) as g:
+        g.load_ratings(user, item, val)
+        o = oracle.Oracle(N, M, 16, P, s, 0.01, 0.05, policy, oracle.ROWMEAN, B, seed, owner)
+        o.load(user, item, val)
+        compare_layout(g, o, B, N, M)

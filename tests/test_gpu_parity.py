@@ -113,15 +113,18 @@ def test_full_shape_scaled(gpu, s):
              lam=spec.lam, clocks=10, check_versions=True)
 
 
-@pytest.mark.parametrize("cells,heavy_min", [(False, -1), (True, 1), (True, 100), (True, -1)])
+@pytest.mark.parametrize("cells,heavy_min,hot_steps", [(False, -1, 0), (True, 1, 0), (True, 100, 0), (True, -1, 0),
+                                                       (True, -1, 2), (True, 100, 1), (True, 1, 3),
+                                                       (True, 10 ** 9, 2)])
 @pytest.mark.parametrize("K", [32, 128, 512])
-def test_lds_cells_and_units_agree_with_oracle(gpu, cells, heavy_min, K):
-    """The LDS-staged cell path (users with at least heavy_min ratings) and the L2 unit path,
-    alone and mixed, on the full workload's laws at 2% size, s=3 (four worker classes)."""
+def test_lds_cells_and_units_agree_with_oracle(gpu, cells, heavy_min, hot_steps, K):
+    """The LDS-staged cells (users with at least heavy_min ratings; with hot_steps > 0 also the
+    other users' ratings of the most rated items) and the L2 unit path, alone and mixed, on
+    the full workload's laws at 2% size, s=3 (four worker classes)."""
     spec = synth.scaled(synth.CONFIGS["full"], 0.02)
     w = synth.generate(spec, K=K)
     run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=K, P=spec.P, s=3, eta=spec.eta,
-             lam=spec.lam, clocks=6, check_versions=True, cells=cells, heavy_min=heavy_min)
+             lam=spec.lam, clocks=6, check_versions=True, cells=cells, heavy_min=heavy_min, hot_steps=hot_steps)
 
 
 @pytest.mark.parametrize("policy", [oracle.SSP_WORST, oracle.ESSP])
