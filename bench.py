@@ -51,7 +51,7 @@ def parse():
     ap.add_argument("--copy-calibration-bytes", type=int, default=0,
                     help="run one plain copy kernel (y = x * 2) of this many bytes before timing, for "
                          "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE")
-    ap.add_argument("--traffic-file", default=os.path.join(ROOT, "profiles", "k_sweep_full_traffic.json"),
+    ap.add_argument("--traffic-file", default=os.path.join(ROOT, "profiles", "sweep_full_traffic.json"),
                     help="measured HBM traffic of the sweep (used while the kernel source is unchanged)")
     return ap.parse_args()
 
@@ -153,7 +153,8 @@ def main():
         commit_ms = (ms_c - base_commit[0]) / (n_c - base_commit[1])
         flops = 6.0 * K * nnz_clock                  # 3K fp32 FMA per rating update
         achieved = flops / (sweep_ms * 1e-3) / 1e12  # TFLOP/s
-        roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
+        roof = {"kernel": "sweep (k_cells and k_units, concurrent)", "bound": "alu",
+                "achieved": round(achieved, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4),
                 "traffic": measured_traffic(args.traffic_file, args.config, s, args.policy)}
         # compulsory HBM bytes of one clock: each rating once (int32 item + fp32 value),

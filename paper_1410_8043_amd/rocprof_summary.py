@@ -1,12 +1,14 @@
 """Summaries of rocprofv3 result databases for the ps_mf kernels.
 
     python -m paper_1410_8043_amd.rocprof_summary stats <dir>
-        per-kernel calls, total and average duration from a --kernel-trace --stats run;
+        per-kernel calls, total and average duration from a --kernel-trace --stats run,
+        and the average span of the sweep (its kernels of one clock run concurrently on
+        two streams: from the first start to the last end);
     python -m paper_1410_8043_amd.rocprof_summary counters <dir> [<dir> ...]
         per-kernel counter values (sum over a dispatch's dimensions) of --pmc runs;
     python -m paper_1410_8043_amd.rocprof_summary traffic --fetch <dir> --write <dir> \
             --copy-bytes N --out profiles/<name>.json
-        HBM bytes per clock of the sweep kernel from one FETCH_SIZE and one WRITE_SIZE run,
+        HBM bytes per clock of the sweep kernels from one FETCH_SIZE and one WRITE_SIZE run,
         scaled by what the same counters read for a plain copy kernel (torch's elementwise
         y = x * 2 over N bytes), written as JSON next to the sha256 of the kernel
         source, so that bench.py reports it only while the kernel is unchanged.
@@ -27,7 +29,7 @@ import sys
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCE = os.path.join(_HERE, "csrc", "ps_mf.hip")
-SWEEP_KERNEL = "k_sweep"
+SWEEP_KERNELS = ("k_cells", "k_units")  # the two concurrent kernels of one clock's sweep
 
 
 def kernel_source_sha256() -> str:
@@ -54,6 +56,28 @@ def stats(d: str):
     rows = con.execute("select name, total_calls, total_duration, average, percentage from top_kernels").fetchall()
     # the top_kernels view reports microseconds
     return [(short_name(n), int(c), tot / 1e3, avg / 1e3, pct) for n, c, tot, avg, pct in rows]
+
+
+def sweep_spans(d: str):
+    """Per clock: (span, [duration of each sweep kernel]) in ms, the i-th dispatch of every
+    sweep kernel taken as clock i (each clock launches each of them at most once)."""
+    con = _db(d)
+    rows = con.execute("select name, start, end from kernels order by start").fetchall()
+    per = {k: [] for k in SWEEP_KERNELS}
+    for name, start, end in rows:
+        sn = short_name(name)
+        for k in SWEEP_KERNELS:
+            if sn.startswith(k):
+                per[k].append((start, end))
+    present = [k for k in SWEEP_KERNELS if per[k]]
+    if not present:
+        return []
+    clocks = min(len(per[k]) for k in present)
+    out = []
+    for i in range(clocks):
+        ivs = [per[k][i] for k in present]
+        out.append(((max(e for _, e in ivs) - min(s for s, _ in ivs)) / 1e6, [(e - s) / 1e6 for s, e in ivs]))
+    return out
 
 
 def counters(d: str):
@@ -84,28 +108,40 @@ def _copy_value(cnt, counter: str) -> float:
     raise KeyError(f"{counter} of the calibration copy kernel not found")
 
 
-def traffic(fetch_dir: str, write_dir: str, copy_bytes: int, launches_per_clock: int = 1):
-    """HBM bytes per clock of the sweep (its launches of one clock summed), calibrated."""
+def _sweep_values(cnt, counter: str):
+    """[(kernel, [value per dispatch])] of the sweep kernels"""
+    out = []
+    for k in SWEEP_KERNELS:
+        try:
+            out.append((k, _find(cnt, k, counter)))
+        except KeyError:
+            pass
+    if not out:
+        raise KeyError(f"{counter} of the sweep kernels not found")
+    return out
+
+
+def traffic(fetch_dir: str, write_dir: str, copy_bytes: int):
+    """HBM bytes per clock of the sweep (its kernels of one clock summed), calibrated."""
     f, w = counters(fetch_dir), counters(write_dir)
     copy_f = _copy_value(f, "FETCH_SIZE")
     copy_w = _copy_value(w, "WRITE_SIZE")
     fetch_scale = copy_bytes / (copy_f * 1024.0)
     write_scale = copy_bytes / (copy_w * 1024.0)
-    sf = _find(f, SWEEP_KERNEL, "FETCH_SIZE")
-    sw = _find(w, SWEEP_KERNEL, "WRITE_SIZE")
-    clocks = len(sf) // launches_per_clock
-    fetch = sum(sf[: clocks * launches_per_clock]) * 1024.0 * fetch_scale / clocks
-    write = sum(sw[: clocks * launches_per_clock]) * 1024.0 * write_scale / clocks
+    sf, sw = _sweep_values(f, "FETCH_SIZE"), _sweep_values(w, "WRITE_SIZE")
+    clocks = min(len(v) for _, v in sf + sw)
+    fetch = sum(sum(v[:clocks]) for _, v in sf) * 1024.0 * fetch_scale / clocks
+    write = sum(sum(v[:clocks]) for _, v in sw) * 1024.0 * write_scale / clocks
     return {
-        "kernel": SWEEP_KERNEL,
-        "launches_per_clock": launches_per_clock,
+        "kernels": [k for k, _ in sf],
+        "clocks": clocks,
         "fetch_bytes_per_clock": fetch,
         "write_bytes_per_clock": write,
         "traffic_bytes_per_clock": fetch + write,
         "copy_calibration": {"bytes": copy_bytes, "fetch_kib": copy_f, "write_kib": copy_w,
                              "fetch_scale": fetch_scale, "write_scale": write_scale},
-        "per_launch_fetch_kib": sf,
-        "per_launch_write_kib": sw,
+        "per_launch_fetch_kib": {k: v for k, v in sf},
+        "per_launch_write_kib": {k: v for k, v in sw},
         "kernel_source_sha256": kernel_source_sha256(),
     }
 
@@ -130,6 +166,12 @@ def main(argv=None):
     if args.cmd == "stats":
         for name, calls, tot, avg, pct in stats(args.dir):
             print(f"{calls:6d} calls  total {tot:10.3f} ms  avg {avg:9.4f} ms  {pct:5.1f}%  {name}")
+        spans = sweep_spans(args.dir)
+        if spans:
+            avg = sum(sp for sp, _ in spans) / len(spans)
+            print(f"sweep span (first start to last end of {' + '.join(SWEEP_KERNELS)} per clock): "
+                  f"{len(spans)} clocks, avg {avg:.4f} ms, min {min(sp for sp, _ in spans):.4f} ms, "
+                  f"max {max(sp for sp, _ in spans):.4f} ms")
     elif args.cmd == "counters":
         for d in args.dirs:
             for (k, cname), vals in sorted(counters(d).items()):
