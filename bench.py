@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--two-streams", type=int, default=None, help="1/0: units on a second stream beside the cells")
     ap.add_argument("--hot-steps", type=int, default=None,
                     help="LDS sub-tiles of the most rated items whose light-user ratings go to cells (-1: auto)")
+    ap.add_argument("--dense-min", type=int, default=None,
+                    help="ratings from which a 64x64 tile is swept by the matrix-core cells (0: none, -1: auto)")
     ap.add_argument("--copy-calibration-bytes", type=int, default=0,
                     help="run one plain copy kernel (y = x * 2) of this many bytes before timing, for "
                          "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE")
@@ -115,13 +117,16 @@ def main():
     g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, B=spec.B,
                    mb_seed=spec.seed, timing=not args.no_timing, stream=stream, tile_bytes=args.tile_bytes,
                    unit_max=args.unit_max, cells=args.cells, heavy_min=args.heavy_min, hot_steps=args.hot_steps,
-                   two_streams=args.two_streams)
+                   two_streams=args.two_streams, dense_min=args.dense_min)
     t_load = time.perf_counter()
     g.load_ratings(w.user, w.item, w.val)
     g.set_factors(w.L0, w.R0)
     t_load = time.perf_counter() - t_load
     print(f"[bench] layout + upload {t_load:.1f} s", file=sys.stderr, flush=True)
     nnz_clock = w.nnz / spec.B  # mean ratings per clock (exact for B=1)
+    split = sum(g.export_index(ps_mf.IDX_SPLIT, b) for b in range(spec.B))
+    print(f"[bench] ratings per direction in dense tiles / LDS cells / L2 units: {split[:3].tolist()} (user-major), "
+          f"{split[3:].tolist()} (item-major)", file=sys.stderr, flush=True)
 
     if args.copy_calibration_bytes > 0:
         src = torch.ones(args.copy_calibration_bytes // 4, dtype=torch.float32, device="cuda")
@@ -153,7 +158,7 @@ def main():
         commit_ms = (ms_c - base_commit[0]) / (n_c - base_commit[1])
         flops = 6.0 * K * nnz_clock                  # 3K fp32 FMA per rating update
         achieved = flops / (sweep_ms * 1e-3) / 1e12  # TFLOP/s
-        roof = {"kernel": "sweep (k_cells and k_units, concurrent)", "bound": "alu",
+        roof = {"kernel": "sweep (k_dense, k_cells and k_units, concurrent)", "bound": "alu",
                 "achieved": round(achieved, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4),
                 "traffic": measured_traffic(args.traffic_file, args.config, s, args.policy)}
@@ -187,7 +192,7 @@ def main():
                                f"P={spec.P}, s={s}, policy={args.policy}, B={spec.B}, eta={spec.eta}, "
                                f"lambda={spec.lam}",
                    "global_batch": int(nnz_clock), "parallelism": "1 GPU, P logical workers",
-                   "loss_after": loss, **extra},
+                   "loss_after": loss, "dense_cells_units": [int(x) for x in split[:3]], **extra},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

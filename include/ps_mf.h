@@ -81,6 +81,13 @@ typedef struct ps_mf ps_mf_t;
                                   remaining (light) users also go to cells; 0: none;
                                   -1 (default): automatic (one sub-tile).  Needs
                                   PS_MF_OPT_CELLS = 1; at most 1024 */
+#define PS_MF_OPT_DENSE_MIN 13 /* ratings from which a 64 x 64 tile (64 users of one worker class
+                                  ranked by rating count x 64 items ranked by rating count) is
+                                  swept with matrix-core products as a dense block; 0: none;
+                                  -1 (default): automatic (1229, i.e. 30% full, when the padded
+                                  rank is in [16, 128], else none); at most 4096.  A value > 0
+                                  with a padded rank outside [16, 128] makes
+                                  ps_mf_load_ratings fail with PS_MF_EINVAL */
 
 #define PS_MF_SSP_LAZY 0
 #define PS_MF_SSP_WORST 1
@@ -97,6 +104,10 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_IDX_USER_COUNT 4  /* int32 [users]: ratings of each user in block b */
 #define PS_MF_IDX_ITEM_COUNT 5  /* int32 [items]: ratings of each item in block b (all workers) */
 #define PS_MF_IDX_VERSION_LOG 6 /* int64 [clocks*P]: v(p,c) at entry c*P + p (clock-major, Section 3.2) */
+#define PS_MF_IDX_SPLIT 7       /* int64 [6]: how block b's ratings are swept: ratings in dense
+                                   (matrix-core) tiles, in LDS-staged cells and in L2 work units,
+                                   for the user-major then the item-major direction (each triple
+                                   sums to the block's rating count) */
 
 /* kernel ids (ps_mf_kernel_time) */
 #define PS_MF_KERNEL_SWEEP 0  /* residual, dL segment-sum and dR accumulation of one clock */

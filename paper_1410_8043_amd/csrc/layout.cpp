@@ -7,6 +7,7 @@
 #include <cstring>
 #include <exception>
 #include <functional>
+#include <limits>
 #include <new>
 #include <numeric>
 #include <thread>
@@ -195,21 +196,26 @@ int64_t count_runs(int64_t nb, const std::vector<int64_t> &by_x, const std::func
   return total;
 }
 
-// Append the ratings [lo, hi) of the (already ordered) list `ents` as one 8-aligned run.
+// Append the ratings [lo, hi) of the (already ordered) list `ents` as one 8-aligned run,
+// leaving out the entries e with skip[e] != 0 (those stored in dense tiles).
 void append_run(CellSet &C, const std::vector<int64_t> &ents, int64_t lo, int64_t hi,
-                const std::function<int32_t(int64_t)> &local, const std::vector<float> &val) {
+                const std::function<int32_t(int64_t)> &local, const std::vector<float> &val,
+                const std::vector<uint8_t> &skip) {
   const int64_t beg = static_cast<int64_t>(C.ly.size());
   C.run_beg.push_back(static_cast<int32_t>(beg));
-  C.run_len.push_back(static_cast<int32_t>(hi - lo));
+  int64_t len = 0;
   for (int64_t q = lo; q < hi; ++q) {
+    if (skip[ents[q]]) continue;
     C.ly.push_back(static_cast<uint16_t>(local(ents[q])));
     C.lv.push_back(val[ents[q]]);
+    ++len;
   }
+  C.run_len.push_back(static_cast<int32_t>(len));
   while (C.ly.size() % kUnitAlign) {
     C.ly.push_back(0);
     C.lv.push_back(0.f);
   }
-  C.nnz += hi - lo;
+  C.nnz += len;
 }
 
 void empty_run(CellSet &C) {
@@ -221,17 +227,18 @@ void empty_run(CellSet &C) {
 // item ranges of ts items; the item space is cut into R ranges of steps so that there are
 // about cell_target cells.  Each heavy user owns R partial rows.
 void build_user_cells(const LayoutParams &p, const BlockLayout &L, const std::vector<int32_t> &ucls,
-                      const std::vector<uint8_t> &heavy, CellSet &C, std::vector<int64_t> &extra) {
+                      const std::vector<uint8_t> &heavy, const std::vector<int64_t> &deg,
+                      const std::vector<uint8_t> &in_dense, CellSet &C, std::vector<int64_t> &extra) {
   const int64_t N = p.users, M = p.items, ts = p.cell_rows, ng = p.cell_groups;
   C.ts = static_cast<int32_t>(ts);
   C.ng = static_cast<int32_t>(ng);
-  extra.assign(static_cast<size_t>(N), 0);
+  if (extra.empty()) extra.assign(static_cast<size_t>(N), 0);
   std::vector<std::vector<int32_t>> by_cls(static_cast<size_t>(p.nclass));
   for (int64_t i = 0; i < N; ++i)
     if (heavy[i]) by_cls[ucls[i]].push_back(static_cast<int32_t>(i));
   int64_t groups = 0;
   for (auto &v : by_cls) {
-    std::stable_sort(v.begin(), v.end(), [&](int32_t a, int32_t b) { return L.ucount[a] > L.ucount[b]; });
+    std::stable_sort(v.begin(), v.end(), [&](int32_t a, int32_t b) { return deg[a] > deg[b]; });
     groups += (static_cast<int64_t>(v.size()) + ng - 1) / ng;
   }
   if (groups == 0) return;
@@ -263,7 +270,7 @@ void build_user_cells(const LayoutParams &p, const BlockLayout &L, const std::ve
             const int32_t *b = L.col.data() + L.row_ptr[u], *e = L.col.data() + L.row_ptr[u + 1];
             const int64_t lo = std::lower_bound(b, e, static_cast<int32_t>(st * ts)) - L.col.data();
             const int64_t hi = std::lower_bound(b, e, static_cast<int32_t>(std::min<int64_t>((st + 1) * ts, M))) - L.col.data();
-            append_run(C, ents, lo, hi, local, L.val);
+            append_run(C, ents, lo, hi, local, L.val, in_dense);
           }
         }
         C.cell_step_ptr.push_back(static_cast<int32_t>(C.cell_steps.size()));
@@ -278,13 +285,13 @@ void build_user_cells(const LayoutParams &p, const BlockLayout &L, const std::ve
 // that there are about cell_target cells.  Each item owns one partial row per (class,
 // range).
 void build_item_cells(const LayoutParams &p, const BlockLayout &L, const std::vector<int32_t> &ucls,
-                      const std::vector<uint8_t> &heavy, const std::vector<int32_t> &ent_user, CellSet &C,
-                      std::vector<int64_t> &extra) {
+                      const std::vector<uint8_t> &heavy, const std::vector<int32_t> &ent_user,
+                      const std::vector<uint8_t> &in_dense, CellSet &C, std::vector<int64_t> &extra) {
   const int64_t N = p.users, M = p.items, ts = p.cell_rows, ng = p.cell_groups;
   const int64_t nb = static_cast<int64_t>(L.col.size());
   C.ts = static_cast<int32_t>(ts);
   C.ng = static_cast<int32_t>(ng);
-  extra.assign(static_cast<size_t>(M), 0);
+  if (extra.empty()) extra.assign(static_cast<size_t>(M), 0);
   // heavy users of each class in id order; their rank and sub-tile
   std::vector<int64_t> hrank(static_cast<size_t>(N), -1), nheavy(static_cast<size_t>(p.nclass), 0);
   for (int64_t i = 0; i < N; ++i)
@@ -301,7 +308,7 @@ void build_item_cells(const LayoutParams &p, const BlockLayout &L, const std::ve
   // heavy entries ordered by (item, class, user): canonical is (user, item)
   std::vector<int64_t> a, b;
   for (int64_t e = 0; e < nb; ++e)
-    if (heavy[ent_user[e]]) a.push_back(e);
+    if (heavy[ent_user[e]] && !in_dense[e]) a.push_back(e);
   b.resize(a.size());
   counting_pass(a, b, p.nclass, [&](int64_t e) { return ucls[ent_user[e]]; });
   counting_pass(b, a, M, [&](int64_t e) { return L.col[e]; });
@@ -355,7 +362,7 @@ void build_item_cells(const LayoutParams &p, const BlockLayout &L, const std::ve
             const int64_t k = g0 + q;
             if (k >= static_cast<int64_t>(items.size())) { empty_run(C); continue; }
             const int64_t *o = bnd.data() + jc_base[items[k] * p.nclass + c];
-            append_run(C, a, o[st], o[st + 1], local, L.val);
+            append_run(C, a, o[st], o[st + 1], local, L.val, in_dense);
           }
         }
         C.cell_step_ptr.push_back(static_cast<int32_t>(C.cell_steps.size()));
@@ -370,7 +377,8 @@ void build_item_cells(const LayoutParams &p, const BlockLayout &L, const std::ve
 // popularity order, ts per sub-tile).  Each such user owns one more partial row.
 void build_user_cells_hot(const LayoutParams &p, const BlockLayout &L, const std::vector<int32_t> &ucls,
                           const std::vector<uint8_t> &heavy, const std::vector<int32_t> &hot_pos,
-                          const std::vector<int32_t> &hot_items, CellSet &C, std::vector<int64_t> &extra) {
+                          const std::vector<int32_t> &hot_items, const std::vector<uint8_t> &in_dense, CellSet &C,
+                          std::vector<int64_t> &extra) {
   const int64_t N = p.users, ts = p.cell_rows, ng = p.cell_groups;
   const int64_t nhot = static_cast<int64_t>(hot_items.size());
   if (nhot == 0) return;
@@ -385,7 +393,7 @@ void build_user_cells_hot(const LayoutParams &p, const BlockLayout &L, const std
   std::vector<int64_t> hot_cnt(static_cast<size_t>(N), 0);
   for (int64_t i = 0; i < N; ++i) {
     if (heavy[i]) continue;
-    for (int64_t e = L.row_ptr[i]; e < L.row_ptr[i + 1]; ++e) hot_cnt[i] += hot_pos[L.col[e]] >= 0;
+    for (int64_t e = L.row_ptr[i]; e < L.row_ptr[i + 1]; ++e) hot_cnt[i] += hot_pos[L.col[e]] >= 0 && !in_dense[e];
     if (hot_cnt[i] > 0) by_cls[ucls[i]].push_back(static_cast<int32_t>(i));
   }
   std::vector<int64_t> ents;
@@ -406,7 +414,7 @@ void build_user_cells_hot(const LayoutParams &p, const BlockLayout &L, const std
       for (int64_t q = 0; q < ng && g0 + q < us.size(); ++q) {
         const int32_t u = us[g0 + q];
         for (int64_t e = L.row_ptr[u]; e < L.row_ptr[u + 1]; ++e)
-          if (hot_pos[L.col[e]] >= 0) mine[q].push_back(e);
+          if (hot_pos[L.col[e]] >= 0 && !in_dense[e]) mine[q].push_back(e);
         std::stable_sort(mine[q].begin(), mine[q].end(),
                          [&](int64_t a, int64_t b) { return hot_pos[L.col[a]] < hot_pos[L.col[b]]; });
       }
@@ -419,7 +427,7 @@ void build_user_cells_hot(const LayoutParams &p, const BlockLayout &L, const std
                                            [&](int64_t e, int64_t v) { return hot_pos[L.col[e]] < v; });
           const auto hi = std::lower_bound(m.begin(), m.end(), (st + 1) * ts,
                                            [&](int64_t e, int64_t v) { return hot_pos[L.col[e]] < v; });
-          append_run(C, m, lo - m.begin(), hi - m.begin(), local, L.val);
+          append_run(C, m, lo - m.begin(), hi - m.begin(), local, L.val, in_dense);
         }
       }
       C.cell_step_ptr.push_back(static_cast<int32_t>(C.cell_steps.size()));
@@ -434,8 +442,8 @@ void build_user_cells_hot(const LayoutParams &p, const BlockLayout &L, const std
 // hot item owns one more partial row per (class, range).
 void build_item_cells_hot(const LayoutParams &p, const BlockLayout &L, const std::vector<int32_t> &ucls,
                           const std::vector<uint8_t> &heavy, const std::vector<int32_t> &ent_user,
-                          const std::vector<int32_t> &hot_pos, const std::vector<int32_t> &hot_items, CellSet &C,
-                          std::vector<int64_t> &extra) {
+                          const std::vector<int32_t> &hot_pos, const std::vector<int32_t> &hot_items,
+                          const std::vector<uint8_t> &in_dense, CellSet &C, std::vector<int64_t> &extra) {
   const int64_t N = p.users, M = p.items, ts = p.cell_rows, ng = p.cell_groups;
   const int64_t nb = static_cast<int64_t>(L.col.size());
   const int64_t nhot = static_cast<int64_t>(hot_items.size());
@@ -447,7 +455,7 @@ void build_item_cells_hot(const LayoutParams &p, const BlockLayout &L, const std
   std::vector<uint8_t> has_hot(static_cast<size_t>(N), 0);
   std::vector<int64_t> a, b;
   for (int64_t e = 0; e < nb; ++e)
-    if (!heavy[ent_user[e]] && hot_pos[L.col[e]] >= 0) {
+    if (!heavy[ent_user[e]] && hot_pos[L.col[e]] >= 0 && !in_dense[e]) {
       a.push_back(e);
       has_hot[ent_user[e]] = 1;
     }
@@ -543,7 +551,7 @@ void build_item_cells_hot(const LayoutParams &p, const BlockLayout &L, const std
             run.clear();
             for (int64_t e = o[st]; e < o[st + 1]; ++e)
               if (local(a[e]) % z.m == z.r) run.push_back(a[e]);
-            append_run(C, run, 0, static_cast<int64_t>(run.size()), local, L.val);
+            append_run(C, run, 0, static_cast<int64_t>(run.size()), local, L.val, in_dense);
           }
         }
         C.cell_step_ptr.push_back(static_cast<int32_t>(C.cell_steps.size()));
@@ -553,10 +561,171 @@ void build_item_cells_hot(const LayoutParams &p, const BlockLayout &L, const std
   }
 }
 
-// cell_out of every used (cell, group): the next of x's cell rows from cell_base[x] on
-void assign_cell_rows(CellSet &C, std::vector<int64_t> cell_base) {
+// cell_out of every used (cell, group), then of every used (dense cell, row): the next of
+// x's rows from cell_base[x] on
+void assign_cell_rows(CellSet &C, DenseSet &D, std::vector<int64_t> cell_base) {
   for (size_t k = 0; k < C.cell_x.size(); ++k)
     if (C.cell_x[k] >= 0) C.cell_out[k] = static_cast<int32_t>(cell_base[C.cell_x[k]]++);
+  for (size_t k = 0; k < D.cell_x.size(); ++k)
+    if (D.cell_x[k] >= 0) D.cell_out[k] = static_cast<int32_t>(cell_base[D.cell_x[k]]++);
+}
+
+// Dense tiles of one block (see DenseSet) and the cells of both directions.  Users of
+// each class are ranked by their rating count in the block and items by theirs (ties by
+// id); tile (c, ut, it) = users of class c at ranks [64 ut, 64 ut + 64) x items at ranks
+// [64 it, 64 it + 64).  A tile with at least dense_min ratings is dense: its entries go
+// to the dense blocks (of duplicate (user, item) pairs only the first, the others stay
+// with the sparse part) and in_dense[e] is set for them.  A user or item row owns one
+// partial row per dense cell it belongs to (extra_u / extra_i).
+void build_dense(const LayoutParams &p, const BlockLayout &L, const std::vector<int32_t> &ucls,
+                 std::vector<uint8_t> &in_dense, DenseSet &DU, DenseSet &DI, std::vector<int64_t> &extra_u,
+                 std::vector<int64_t> &extra_i) {
+  const int64_t N = p.users, M = p.items, T = kDenseRows;
+  if (p.dense_min <= 0 || L.nnz == 0) return;
+  const int64_t nit = (M + T - 1) / T;
+  std::vector<int32_t> item_at(static_cast<size_t>(M)), irank(static_cast<size_t>(M));
+  std::iota(item_at.begin(), item_at.end(), 0);
+  std::stable_sort(item_at.begin(), item_at.end(), [&](int32_t x, int32_t y) { return L.icount[x] > L.icount[y]; });
+  for (int64_t r = 0; r < M; ++r) irank[item_at[r]] = static_cast<int32_t>(r);
+  std::vector<std::vector<int32_t>> ulist(static_cast<size_t>(p.nclass));
+  for (int64_t i = 0; i < N; ++i)
+    if (L.ucount[i] > 0) ulist[ucls[i]].push_back(static_cast<int32_t>(i));
+  // dense item tiles of each (class, user tile), ascending
+  struct UTile { int32_t c, ut; std::vector<int32_t> its; };
+  std::vector<UTile> utiles;
+  std::vector<int64_t> cnt(static_cast<size_t>(nit), 0);
+  for (int32_t c = 0; c < p.nclass; ++c) {
+    auto &us = ulist[c];
+    std::stable_sort(us.begin(), us.end(), [&](int32_t a, int32_t b) { return L.ucount[a] > L.ucount[b]; });
+    for (int64_t u0 = 0; u0 < static_cast<int64_t>(us.size()); u0 += T) {
+      const int64_t u1 = std::min<int64_t>(u0 + T, static_cast<int64_t>(us.size()));
+      int64_t total = 0;
+      for (int64_t q = u0; q < u1; ++q) total += L.ucount[us[q]];
+      if (total < p.dense_min) break;  // later tiles of the class hold fewer ratings
+      std::fill(cnt.begin(), cnt.end(), 0);
+      for (int64_t q = u0; q < u1; ++q)
+        for (int64_t e = L.row_ptr[us[q]]; e < L.row_ptr[us[q] + 1]; ++e) cnt[irank[L.col[e]] / T] += 1;
+      UTile t{c, static_cast<int32_t>(u0 / T), {}};
+      for (int64_t it = 0; it < nit; ++it)
+        if (cnt[it] >= p.dense_min) t.its.push_back(static_cast<int32_t>(it));
+      if (!t.its.empty()) utiles.push_back(std::move(t));
+    }
+  }
+  int64_t ntiles = 0;
+  for (const auto &t : utiles) ntiles += static_cast<int64_t>(t.its.size());
+  if (ntiles == 0) return;
+  // entries of the dense tiles
+  std::vector<uint8_t> dense_it(static_cast<size_t>(nit), 0);
+  for (const auto &t : utiles) {
+    for (int32_t it : t.its) dense_it[it] = 1;
+    const auto &us = ulist[t.c];
+    for (int64_t q = int64_t(t.ut) * T; q < std::min<int64_t>((int64_t(t.ut) + 1) * T, us.size()); ++q)
+      for (int64_t e = L.row_ptr[us[q]]; e < L.row_ptr[us[q] + 1]; ++e)
+        if (dense_it[irank[L.col[e]] / T] && (e == L.row_ptr[us[q]] || L.col[e - 1] != L.col[e])) in_dense[e] = 1;
+    for (int32_t it : t.its) dense_it[it] = 0;
+  }
+  const int64_t per_cell = std::max<int64_t>(1, (ntiles + p.dense_target - 1) / std::max(1, p.dense_target));
+  // step index of every dense tile in each direction: tile t of utiles[u] is tile_base[u] + t
+  std::vector<int64_t> tile_base(utiles.size() + 1, 0);
+  for (size_t u = 0; u < utiles.size(); ++u) tile_base[u + 1] = tile_base[u] + static_cast<int64_t>(utiles[u].its.size());
+  std::vector<int64_t> step_u(static_cast<size_t>(ntiles)), step_i(static_cast<size_t>(ntiles));
+  // A cell = (x tile, class, a run of at most per_cell dense y tiles, given as tile ids);
+  // cells are emitted longest first.
+  struct Seg { int32_t c, xt; std::vector<int32_t> ys; std::vector<int64_t> tiles; };
+  auto cut = [&](std::vector<Seg> &segs, int32_t c, int32_t xt, const std::vector<int32_t> &ys,
+                 const std::vector<int64_t> &tiles) {
+    const int64_t n = static_cast<int64_t>(ys.size());
+    const int64_t parts = (n + per_cell - 1) / per_cell;
+    for (int64_t r = 0; r < parts; ++r)
+      segs.push_back({c, xt, std::vector<int32_t>(ys.begin() + r * n / parts, ys.begin() + (r + 1) * n / parts),
+                      std::vector<int64_t>(tiles.begin() + r * n / parts, tiles.begin() + (r + 1) * n / parts)});
+  };
+  auto emit = [&](DenseSet &D, std::vector<Seg> &segs, bool user_major, std::vector<int64_t> &extra,
+                  std::vector<int64_t> &step_of) {
+    std::stable_sort(segs.begin(), segs.end(), [](const Seg &a, const Seg &b) { return a.ys.size() > b.ys.size(); });
+    D.cell_step_ptr.assign(1, 0);
+    D.step_rows.reserve(static_cast<size_t>(ntiles * T));
+    int64_t k = 0;
+    for (const auto &g : segs) {
+      D.cell_cls.push_back(g.c);
+      for (int64_t q = 0; q < T; ++q) {
+        int32_t x = -1;
+        const int64_t pos = int64_t(g.xt) * T + q;
+        if (user_major) x = pos < static_cast<int64_t>(ulist[g.c].size()) ? ulist[g.c][pos] : -1;
+        else x = pos < M ? item_at[pos] : -1;
+        D.cell_x.push_back(x);
+        D.cell_out.push_back(-1);
+        if (x >= 0) extra[x] += 1;
+      }
+      for (size_t t = 0; t < g.ys.size(); ++t) {
+        for (int64_t q = 0; q < T; ++q) {
+          const int64_t pos = int64_t(g.ys[t]) * T + q;
+          if (user_major) D.step_rows.push_back(pos < M ? item_at[pos] : -1);
+          else D.step_rows.push_back(pos < static_cast<int64_t>(ulist[g.c].size()) ? ulist[g.c][pos] : -1);
+        }
+        step_of[g.tiles[t]] = k++;
+      }
+      D.cell_step_ptr.push_back(static_cast<int32_t>(k));
+    }
+    D.dval.assign(static_cast<size_t>(k * kDenseTile), std::numeric_limits<float>::quiet_NaN());
+  };
+  if (extra_u.empty()) extra_u.assign(static_cast<size_t>(N), 0);
+  if (extra_i.empty()) extra_i.assign(static_cast<size_t>(M), 0);
+  {
+    std::vector<Seg> segs;
+    for (size_t u = 0; u < utiles.size(); ++u) {
+      std::vector<int64_t> ids(utiles[u].its.size());
+      std::iota(ids.begin(), ids.end(), tile_base[u]);
+      cut(segs, utiles[u].c, utiles[u].ut, utiles[u].its, ids);
+    }
+    emit(DU, segs, true, extra_u, step_u);
+  }
+  {
+    // (item tile, class) -> its dense user tiles, ascending
+    std::vector<std::vector<std::vector<int32_t>>> uts(static_cast<size_t>(nit),
+                                                        std::vector<std::vector<int32_t>>(static_cast<size_t>(p.nclass)));
+    std::vector<std::vector<std::vector<int64_t>>> ids(static_cast<size_t>(nit),
+                                                        std::vector<std::vector<int64_t>>(static_cast<size_t>(p.nclass)));
+    for (size_t u = 0; u < utiles.size(); ++u)
+      for (size_t t = 0; t < utiles[u].its.size(); ++t) {
+        const int32_t it = utiles[u].its[t];
+        uts[it][utiles[u].c].push_back(utiles[u].ut);
+        ids[it][utiles[u].c].push_back(tile_base[u] + static_cast<int64_t>(t));
+      }
+    std::vector<Seg> segs;
+    for (int64_t it = 0; it < nit; ++it)
+      for (int32_t c = 0; c < p.nclass; ++c)
+        if (!uts[it][c].empty()) cut(segs, c, static_cast<int32_t>(it), uts[it][c], ids[it][c]);
+    emit(DI, segs, false, extra_i, step_i);
+  }
+  // the values: one pass over the rows of each dense user tile fills both directions' blocks
+  // (user tiles write disjoint steps; parallel_for hands each thread the tiles u with
+  // u * 2^16 in its range)
+  parallel_for(p.threads, static_cast<int64_t>(utiles.size()) << 16, [&](int64_t lo, int64_t hi) {
+    std::vector<int64_t> ku(static_cast<size_t>(nit), -1), ki(static_cast<size_t>(nit), -1);
+    for (int64_t u = (lo + 0xffff) >> 16; u < (hi + 0xffff) >> 16; ++u) {
+      const UTile &t = utiles[u];
+      for (size_t x = 0; x < t.its.size(); ++x) {
+        ku[t.its[x]] = step_u[tile_base[u] + x];
+        ki[t.its[x]] = step_i[tile_base[u] + x];
+      }
+      const auto &us = ulist[t.c];
+      for (int64_t q = int64_t(t.ut) * T; q < std::min<int64_t>((int64_t(t.ut) + 1) * T, us.size()); ++q) {
+        const int32_t ul = static_cast<int32_t>(q - int64_t(t.ut) * T);
+        for (int64_t e = L.row_ptr[us[q]]; e < L.row_ptr[us[q] + 1]; ++e) {
+          if (!in_dense[e]) continue;
+          const int32_t r = irank[L.col[e]];
+          const int32_t it = r / static_cast<int32_t>(T), il = r - it * static_cast<int32_t>(T);
+          DU.dval[static_cast<size_t>(ku[it] * kDenseTile + dense_frag_index(ul, il))] = L.val[e];
+          DI.dval[static_cast<size_t>(ki[it] * kDenseTile + dense_frag_index(il, ul))] = L.val[e];
+        }
+      }
+      for (int32_t it : t.its) ku[it] = ki[it] = -1;
+    }
+  });
+  int64_t nd = 0;
+  for (uint8_t f : in_dense) nd += f;
+  DU.nnz = DI.nnz = nd;
 }
 
 }  // namespace
@@ -688,13 +857,20 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
       L.row_ptr.assign(static_cast<size_t>(N) + 1, 0);
       for (int64_t i = 0; i < N; ++i) L.row_ptr[i + 1] = L.row_ptr[i] + L.ucount[i];
 
-      // ---- cells (the dense part, staged through LDS) and units (the rest).  Heavy users'
-      // ratings all go to cells; with hot_steps > 0 so do the other users' ratings of the
-      // hot_steps * cell_rows most rated items of the block.
+      // ---- dense tiles (matrix-core cells), then cells (staged through LDS) and units (the
+      // rest) for the other ratings.  Heavy users' remaining ratings all go to cells; with
+      // hot_steps > 0 so do the other users' ratings of the hot_steps * cell_rows most
+      // rated items of the block.
+      std::vector<uint8_t> in_dense(static_cast<size_t>(nb), 0);
+      std::vector<int64_t> extra_u, extra_i, base_u, base_i;
+      build_dense(p, L, ucls, in_dense, L.dense_user, L.dense_item, extra_u, extra_i);
+      std::vector<int64_t> rem(L.ucount.begin(), L.ucount.end());  // ratings outside the dense tiles
+      if (L.dense_user.nnz > 0)
+        for (int64_t x = 0; x < nb; ++x) rem[ent_user[x]] -= in_dense[x];
       const bool use_cells = p.cell_rows > 0 && p.cell_groups > 0;
       std::vector<uint8_t> heavy(static_cast<size_t>(N), 0);
       if (use_cells)
-        for (int64_t i = 0; i < N; ++i) heavy[i] = L.ucount[i] >= p.heavy_min;
+        for (int64_t i = 0; i < N; ++i) heavy[i] = rem[i] > 0 && L.ucount[i] >= p.heavy_min;
       std::vector<int32_t> hot_items, hot_pos(static_cast<size_t>(M), -1);
       if (use_cells && p.hot_steps > 0) {
         hot_items.resize(static_cast<size_t>(M));
@@ -706,20 +882,19 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
         for (size_t h = 0; h < hot_items.size(); ++h) hot_pos[hot_items[h]] = static_cast<int32_t>(h);
       }
       std::vector<uint8_t> in_units(static_cast<size_t>(nb));
-      for (int64_t x = 0; x < nb; ++x) in_units[x] = !heavy[ent_user[x]] && hot_pos[L.col[x]] < 0;
+      for (int64_t x = 0; x < nb; ++x) in_units[x] = !in_dense[x] && !heavy[ent_user[x]] && hot_pos[L.col[x]] < 0;
       // ---- units.  Tiles start at the L2-sized row count and grow (x2) while the units
       // would average fewer than 16 ratings (each unit costs one partial row).
       const int64_t min_avg = 16;
       int64_t n_units_entries = 0;
       for (int64_t x = 0; x < nb; ++x) n_units_entries += in_units[x];
       // The two sweep directions only read the block's arrays: build them concurrently.
-      std::vector<int64_t> extra_u, extra_i, base_u, base_i;
       std::exception_ptr user_side_error;
       std::thread user_side([&] {
       try {
       if (use_cells) {
-        build_user_cells(p, L, ucls, heavy, L.cells_user, extra_u);
-        build_user_cells_hot(p, L, ucls, heavy, hot_pos, hot_items, L.cells_user, extra_u);
+        build_user_cells(p, L, ucls, heavy, rem, in_dense, L.cells_user, extra_u);
+        build_user_cells_hot(p, L, ucls, heavy, hot_pos, hot_items, in_dense, L.cells_user, extra_u);
       }
       // user-major: x = user, y = item, tile = (class, item range)
       {
@@ -743,7 +918,7 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
         };
         const std::function<int32_t(int64_t)> ct = [nt](int64_t t) { return static_cast<int32_t>(t / nt); };
         build_units(nb, N, nt * p.nclass, xr, yr, tl, ct, L.val, p.unit_max, in_units, extra_u, base_u, L.by_user);
-        assign_cell_rows(L.cells_user, base_u);
+        assign_cell_rows(L.cells_user, L.dense_user, base_u);
         L.partial_rows_user = L.by_user.x_pp[N];
       }
       } catch (...) {
@@ -755,8 +930,8 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
         ~Join() { if (t.joinable()) t.join(); }
       } join_user_side{user_side};
       if (use_cells) {
-        build_item_cells(p, L, ucls, heavy, ent_user, L.cells_item, extra_i);
-        build_item_cells_hot(p, L, ucls, heavy, ent_user, hot_pos, hot_items, L.cells_item, extra_i);
+        build_item_cells(p, L, ucls, heavy, ent_user, in_dense, L.cells_item, extra_i);
+        build_item_cells_hot(p, L, ucls, heavy, ent_user, hot_pos, hot_items, in_dense, L.cells_item, extra_i);
       }
       // item-major: x = item, y = user, tile = class-pure user range
       {
@@ -794,7 +969,7 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
           for (int64_t t = cls_base[c]; t < cls_base[c + 1]; ++t) tile_cls[t] = c;
         const std::function<int32_t(int64_t)> ct = [&](int64_t t) { return tile_cls[t]; };
         build_units(nb, M, nt, xr, yr, tl, ct, L.val, p.unit_max, in_units, extra_i, base_i, L.by_item);
-        assign_cell_rows(L.cells_item, base_i);
+        assign_cell_rows(L.cells_item, L.dense_item, base_i);
         L.partial_rows_item = L.by_item.x_pp[M];
       }
       user_side.join();
@@ -823,7 +998,8 @@ struct Triple {
 // one direction: `want` holds the block's (x, y, value) triples; ucls_of_entry(x, y) is the
 // class the unit or cell must read
 int check_direction(const char *dir, int64_t nx, int64_t ny, std::vector<Triple> want, const UnitSet &U,
-                    const CellSet &C, const std::function<int32_t(int32_t, int32_t)> &cls_of, std::string &err) {
+                    const CellSet &C, const DenseSet &D, const std::function<int32_t(int32_t, int32_t)> &cls_of,
+                    std::string &err) {
   auto bad = [&](const std::string &what) {
     err = std::string(dir) + ": " + what;
     return -1;
@@ -902,10 +1078,47 @@ int check_direction(const char *dir, int64_t nx, int64_t ny, std::vector<Triple>
     for (int32_t r : C.step_rows)
       if (r < -1 || r >= ny) return bad("staged row out of range");
   }
+  const int64_t ndense = static_cast<int64_t>(D.cell_cls.size());
+  if (ndense > 0) {
+    const int64_t T = kDenseRows;
+    const int64_t nsteps = static_cast<int64_t>(D.step_rows.size()) / T;
+    if (D.cell_step_ptr.size() != static_cast<size_t>(ndense) + 1 || D.cell_x.size() != static_cast<size_t>(ndense * T) ||
+        D.cell_out.size() != D.cell_x.size() || D.step_rows.size() % T ||
+        D.dval.size() != static_cast<size_t>(nsteps * kDenseTile) || D.cell_step_ptr[0] != 0 ||
+        D.cell_step_ptr[ndense] != nsteps)
+      return bad("dense cell arrays have inconsistent lengths");
+    for (int32_t r : D.step_rows)
+      if (r < -1 || r >= ny) return bad("dense staged row out of range");
+    int64_t held = 0;
+    for (int64_t c = 0; c < ndense; ++c) {
+      if (D.cell_step_ptr[c] > D.cell_step_ptr[c + 1]) return bad("dense cell step pointers decrease");
+      for (int64_t q = 0; q < T; ++q) {
+        const int32_t x = D.cell_x[c * T + q], out = D.cell_out[c * T + q];
+        if (x >= nx) return bad("dense cell row out of range");
+        if (x < 0 && out >= 0) return bad("an unused dense row writes a partial row");
+        if (x >= 0) {
+          if (out < U.x_pp[x] || out >= U.x_pp[x + 1]) return bad("dense cell writes a partial row of another x");
+          written[out] += 1;
+        }
+      }
+      for (int64_t k = D.cell_step_ptr[c]; k < D.cell_step_ptr[c + 1]; ++k)
+        for (int32_t q = 0; q < T; ++q)
+          for (int32_t t = 0; t < T; ++t) {
+            const float v = D.dval[static_cast<size_t>(k * kDenseTile + dense_frag_index(q, t))];
+            if (std::isnan(v)) continue;
+            const int32_t x = D.cell_x[c * T + q], y = D.step_rows[k * T + t];
+            if (x < 0 || y < 0) return bad("a dense rating sits on an empty row");
+            if (cls_of(x, y) != D.cell_cls[c]) return bad("dense cell reads the slot of another class");
+            got.push_back({x, y, v});
+            ++held;
+          }
+    }
+    if (held != D.nnz) return bad("dense cells hold " + std::to_string(held) + " ratings, not " + std::to_string(D.nnz));
+  }
   for (int64_t r = 0; r < nrows; ++r)
     if (written[r] != 1) return bad("partial row " + std::to_string(r) + " is written " + std::to_string(written[r]) + " times");
   if (got.size() != want.size())
-    return bad("units and cells hold " + std::to_string(got.size()) + " ratings, the block " + std::to_string(want.size()));
+    return bad("units, cells and dense cells hold " + std::to_string(got.size()) + " ratings, the block " + std::to_string(want.size()));
   std::sort(got.begin(), got.end());
   std::sort(want.begin(), want.end());
   for (size_t t = 0; t < got.size(); ++t)
@@ -933,8 +1146,8 @@ int check_layout(const LayoutParams &p, const BlockLayout &L, std::string &err) 
   }
   const std::function<int32_t(int32_t, int32_t)> cu = [&](int32_t x, int32_t) { return ucls[x]; };
   const std::function<int32_t(int32_t, int32_t)> ci = [&](int32_t, int32_t y) { return ucls[y]; };
-  if (check_direction("user-major", N, M, std::move(by_user), L.by_user, L.cells_user, cu, err)) return -1;
-  if (check_direction("item-major", M, N, std::move(by_item), L.by_item, L.cells_item, ci, err)) return -1;
+  if (check_direction("user-major", N, M, std::move(by_user), L.by_user, L.cells_user, L.dense_user, cu, err)) return -1;
+  if (check_direction("item-major", M, N, std::move(by_item), L.by_item, L.cells_item, L.dense_item, ci, err)) return -1;
   if (L.partial_rows_user != L.by_user.x_pp[N] || L.partial_rows_item != L.by_item.x_pp[M]) {
     err = "partial row counts disagree with the row offsets";
     return -1;

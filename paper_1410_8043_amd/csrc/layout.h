@@ -12,6 +12,18 @@ namespace psmf {
 constexpr int kXcds = 8;       // MI355X: 8 accelerator complex dies, each with its own L2
 constexpr int kUnitAlign = 8;  // a unit's ratings start at, and are padded to, a multiple of this
 constexpr int kWaveUnits = 32; // units of one wavefront (at most 32 lane groups) share a worker class
+constexpr int kDenseRows = 64; // rows on each side of a dense tile (4 wavefronts x 16 MFMA rows)
+constexpr int kDenseTile = kDenseRows * kDenseRows;
+
+// Position of rating (x, y) of a dense tile (x, y local in [0, 64)) in its 4096-float
+// block of values: the order in which the MFMA cell reads them.  Wavefront w = x / 16
+// holds rows x of the stationary side; for its 16-row slice yb = y / 16 of the staged
+// side, lane l = (x % 16) + 16 * ((y % 16) / 4) reads the 4 values y % 4 = 0..3 as one
+// float4 (the C/D fragment of a 16x16x4 fp32 MFMA whose rows are y and columns x).
+inline int32_t dense_frag_index(int32_t x, int32_t y) {
+  const int32_t w = x >> 4, yb = y >> 4, lane = (x & 15) + 16 * ((y & 15) >> 2);
+  return (((w * 4 + yb) * 64 + lane) << 2) + (y & 3);
+}
 
 // SplitMix64 (Steele, Lea & Flood 2014): one step of the sequential generator from
 // `state`.  Used for the minibatch block of a rating.
@@ -73,6 +85,26 @@ struct CellSet {
   int64_t nnz = 0;                     // ratings covered by the cells
 };
 
+// The densest part of a block as 64 x 64 tiles, swept with matrix-core (MFMA) products
+// instead of per-rating dot products.  A tile is 64 users of one worker class (ranked
+// by their rating count in the block) x 64 items (ranked by their rating count) holding
+// at least dense_min ratings; both sweep directions walk the same tiles:
+//   user-major: a cell is one user tile (x = 64 users) and a run of its dense item
+//               tiles (steps, y = 64 items each);
+//   item-major: a cell is one item tile (x = 64 items) and a run of the dense user
+//               tiles of one class (steps).
+// A step's ratings are stored as a 64 x 64 block in dense_frag_index order, NaN where
+// there is no rating.  Each used (cell, x row) writes one partial row cell_out.
+struct DenseSet {
+  std::vector<int32_t> cell_x;         // [ncells * 64], -1 = no row
+  std::vector<int32_t> cell_cls;       // [ncells]
+  std::vector<int32_t> cell_step_ptr;  // [ncells + 1] into the steps
+  std::vector<int32_t> step_rows;      // [nsteps * 64] staged rows of each step, -1 = no row
+  std::vector<float> dval;             // [nsteps * 4096]
+  std::vector<int32_t> cell_out;       // [ncells * 64], -1 for unused rows
+  int64_t nnz = 0;                     // ratings covered
+};
+
 struct BlockLayout {
   int64_t nnz = 0;
   // ratings of the block in canonical (user, item, load index) order
@@ -85,6 +117,7 @@ struct BlockLayout {
   std::vector<int32_t> icount_cls;  // [items * nclass]: raters of the item per worker class
   UnitSet by_user, by_item;
   CellSet cells_user, cells_item;
+  DenseSet dense_user, dense_item;
   int64_t partial_rows_user = 0, partial_rows_item = 0;  // rows of x_pp (units and cells)
 };
 
@@ -105,6 +138,9 @@ struct LayoutParams {
   int32_t cell_target = 1024;       // about this many cells per family and direction
   int32_t hot_steps = 0;            // sub-tiles of the most rated items whose ratings by the other
                                     // (light) users also go to cells
+  int32_t dense_min = 0;            // ratings from which a 64 x 64 tile goes to the MFMA cells
+                                    // (0: none)
+  int32_t dense_target = 1024;      // about this many dense cells per direction
 };
 
 // Validates the COO input (EINVAL message in err) and fills one BlockLayout per block.
@@ -113,7 +149,7 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
                  std::vector<BlockLayout> &out, std::string &err);
 
 // Self-check of one block's layout against its canonical entries: in each sweep direction
-// the units and cells together hold every entry exactly once (same stationary row,
+// the units, cells and dense cells together hold every entry exactly once (same stationary row,
 // gathered row and value), every unit and cell reads the ring slot of its ratings' user
 // class (wave-uniform for units), padding is (row 0, value 0), and the partial rows of
 // each x are written exactly once each.  Returns 0, or -1 with err naming the first fault.

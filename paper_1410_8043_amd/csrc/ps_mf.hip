@@ -53,6 +53,11 @@ constexpr int kTileFloats = PS_MF_CELL_TILE_FLOATS; // LDS sub-tile of a cell (3
 static_assert(kSweepBlock % 256 == 0 && kSweepBlock <= 1024, "cell workgroups hold whole 256-thread quarters");
 static_assert(kTileFloats % 512 == 0 && kTileFloats * 4 <= 160 * 1024, "a cell sub-tile holds whole 512-wide rows in LDS");
 constexpr int kLossSegment = 512;  // ratings per lane group of the loss
+// automatic threshold of the dense (MFMA) tiles: ratings per 64 x 64 tile
+#ifndef PS_MF_DENSE_AUTO
+#define PS_MF_DENSE_AUTO 1229
+#endif
+constexpr int kDenseAuto = PS_MF_DENSE_AUTO;
 constexpr int kMaxKp = 512;
 constexpr int kXcds = psmf::kXcds;
 #ifndef PS_MF_ROWS_IN_FLIGHT
@@ -378,6 +383,214 @@ __global__ __launch_bounds__(kBlock) void k_units(UnitSweepArgs s) {
   run_unit<G, E>(a, unit, threadIdx.x & (G - 1));
 }
 
+// ------------------------------------------------------------------ dense (MFMA) cells
+// A dense cell sweeps one 64-row x tile (users or items, one worker class) against a run
+// of 64-row y tiles whose ratings are stored as dense 64 x 64 blocks (NaN = no rating).
+// Wavefront w keeps x rows 16w .. 16w+15 in registers; per step the workgroup stages the
+// 64 y rows in LDS and each wavefront, for every 16-row slice of them, computes with
+// v_mfma_f32_16x16x4_f32
+//   S^T = Y_s X_w^T                (16 y x 16 x, contraction over the rank),
+//   E^T = D^T - S^T where rated, 0 elsewhere (the residuals, Section 3.1),
+//   acc += E Y_s                   (16 x rows x Kp, contraction over the 16 y rows),
+// so each rated (x, y) adds e_xy Y_y to acc_x exactly as the per-rating sweeps do.  Fragment
+// layouts of the 16x16x4 fp32 MFMA (lane l, i = l % 16, g = l / 16): A operand A[i][g],
+// B operand B[g][i], C/D holds D[4g + v][i] in register v.
+//   GEMM 1: A[i][g] = Y[16 ys + i][k], B[g][i] = X[16 w + i][k] with the rank index
+//           k = 16 q + 4 g + j for the j-th product of chunk q (any order of k sums the same);
+//   GEMM 2: A[i][g] = E[16 w + i][16 ys + 4 g + r] is register r of S^T's fragment, B[g][i]
+//           = Y[16 ys + 4 g + r][col(c, i)]; output block c holds the columns
+//           col(c, i) = 16 C4 (c / C4) + C4 i + c % C4, so each lane reads and stores C4
+//           consecutive floats (C4 = 4 from Kp = 64 on).
+constexpr int kDenseThreads = 256;  // 4 wavefronts x 16 x rows
+constexpr int kDenseRowsDev = psmf::kDenseRows;
+static_assert(kDenseThreads / 64 * 16 == kDenseRowsDev, "one wavefront per 16 x rows");
+
+struct DenseArgs {
+  const int32_t *cell_x, *cell_cls, *cell_step_ptr, *step_rows, *cell_out;
+  const float *dval;
+  const int32_t *cls_slot;
+  const float *ring;
+  int64_t slot_stride, x_off, y_off;
+  float *partial;
+};
+
+struct DenseSweepArgs {
+  DenseArgs da, db;
+  int32_t ncell_a;
+};
+
+// float4 chunk h of staged row y in LDS: chunks are XOR-swizzled by the row so that the
+// 8 lanes of one ds_read_b128 pass (8 rows, same chunk; or one row, 8 chunks) hit
+// different banks
+template <int Kp>
+__device__ __forceinline__ int dense_lds_chunk(int y, int h) {
+  constexpr int H = Kp / 4;
+  constexpr int SW = H < 16 ? H : 16;
+  return y * H + (h ^ (y & (SW - 1)));
+}
+
+template <int C4>
+struct VecOf;
+template <>
+struct VecOf<1> { typedef float T; };
+template <>
+struct VecOf<2> { typedef float2 T; };
+template <>
+struct VecOf<4> { typedef float4 T; };
+
+template <int C4>
+__device__ __forceinline__ float vec_at(const typename VecOf<C4>::T &v, int c) {
+  if constexpr (C4 == 1) return v;
+  else if constexpr (C4 == 2) return c == 0 ? v.x : v.y;
+  else return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
+}
+
+template <int Kp>
+__device__ __forceinline__ void dense_stage_load(const DenseArgs &a, const float *__restrict__ Y, int64_t k,
+                                                 float4 (&pre)[Kp / 16]) {
+  constexpr int H = Kp / 4;
+  const int32_t *rows = a.step_rows + k * kDenseRowsDev;
+#pragma unroll
+  for (int m = 0; m < Kp / 16; ++m) {
+    const int u = static_cast<int>(threadIdx.x) + kDenseThreads * m;
+    const int32_t r = rows[u / H];
+    pre[m] = r >= 0 ? *reinterpret_cast<const float4 *>(Y + static_cast<int64_t>(r) * Kp + 4 * (u % H))
+                    : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+}
+
+template <int Kp>
+__device__ __forceinline__ void dense_stage_store(float4 *lds, const float4 (&pre)[Kp / 16]) {
+  constexpr int H = Kp / 4;
+#pragma unroll
+  for (int m = 0; m < Kp / 16; ++m) {
+    const int u = static_cast<int>(threadIdx.x) + kDenseThreads * m;
+    lds[dense_lds_chunk<Kp>(u / H, u % H)] = pre[m];
+  }
+}
+
+template <int Kp>
+__device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, float4 (*lds)[kDenseRowsDev * Kp / 4]) {
+  constexpr int NQ = Kp / 16;             // rank chunks of 16 (GEMM 1) = output blocks of 16 columns (GEMM 2)
+  constexpr int C4 = NQ < 4 ? NQ : 4;     // output blocks read / stored together
+  typedef typename VecOf<C4>::T VecT;
+  const int lane = static_cast<int>(threadIdx.x) & 63, w = static_cast<int>(threadIdx.x) >> 6;
+  const int i = lane & 15, g = lane >> 4;
+  const int sv = a.cls_slot[a.cell_cls[cell]];  // one class per cell: uniform
+  const float *__restrict__ V = a.ring + sv * a.slot_stride;
+  const float *__restrict__ X = V + a.x_off;
+  const float *__restrict__ Y = V + a.y_off;
+  // stationary rows in the B-operand layout of GEMM 1: xb[q] = X[16w + i][16q + 4g .. +3]
+  float4 xb[NQ];
+  {
+    const int32_t xr = a.cell_x[cell * kDenseRowsDev + 16 * w + i];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+      xb[q] = xr >= 0 ? *reinterpret_cast<const float4 *>(X + static_cast<int64_t>(xr) * Kp + 16 * q + 4 * g)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  f32x4 acc[NQ];
+#pragma unroll
+  for (int c = 0; c < NQ; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int64_t k0 = a.cell_step_ptr[cell], k1 = a.cell_step_ptr[cell + 1];
+  const f32x4 *__restrict__ dv = reinterpret_cast<const f32x4 *>(a.dval);
+  float4 pre[NQ];
+  f32x4 dcur[4], dnext[4];
+  if (k0 < k1) {
+    dense_stage_load<Kp>(a, Y, k0, pre);
+#pragma unroll
+    for (int yb = 0; yb < 4; ++yb) dcur[yb] = dv[(k0 * 16 + w * 4 + yb) * 64 + lane];
+    dense_stage_store<Kp>(lds[0], pre);
+  }
+  __syncthreads();
+  for (int64_t k = k0; k < k1; ++k) {
+    const int buf = static_cast<int>((k - k0) & 1);
+    const bool more = k + 1 < k1;
+    if (more) {  // the next step's rows and values, written to the other buffer after this step
+      dense_stage_load<Kp>(a, Y, k + 1, pre);
+#pragma unroll
+      for (int yb = 0; yb < 4; ++yb) dnext[yb] = dv[((k + 1) * 16 + w * 4 + yb) * 64 + lane];
+    }
+    const float4 *T4 = lds[buf];
+#pragma unroll
+    for (int y2 = 0; y2 < 4; y2 += 2) {
+      // GEMM 1 for two 16-row slices at once (two independent accumulation chains)
+      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const float4 a0 = T4[dense_lds_chunk<Kp>(16 * y2 + i, 4 * q + g)];
+        const float4 a1 = T4[dense_lds_chunk<Kp>(16 * y2 + 16 + i, 4 * q + g)];
+        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, xb[q].x, s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, xb[q].x, s1, 0, 0, 0);
+        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, xb[q].y, s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.y, xb[q].y, s1, 0, 0, 0);
+        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.z, xb[q].z, s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, xb[q].z, s1, 0, 0, 0);
+        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, xb[q].w, s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, xb[q].w, s1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const f32x4 sv4 = h ? s1 : s0;
+        const f32x4 d = dcur[y2 + h];
+        // residual where rated (D is NaN elsewhere), as the A operand of GEMM 2
+        float e[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) e[v] = d[v] == d[v] ? d[v] - sv4[v] : 0.f;
+        const int ys = y2 + h;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const char *row = reinterpret_cast<const char *>(T4);
+#pragma unroll
+          for (int cg = 0; cg < NQ / C4; ++cg) {
+            const int f = 16 * C4 * cg + C4 * i;  // first float of this lane's columns
+            const int y = 16 * ys + 4 * g + r;
+            const VecT b = *reinterpret_cast<const VecT *>(row + 16 * dense_lds_chunk<Kp>(y, f >> 2) + 4 * (f & 3));
+#pragma unroll
+            for (int cc = 0; cc < C4; ++cc)
+              acc[C4 * cg + cc] = __builtin_amdgcn_mfma_f32_16x16x4f32(e[r], vec_at<C4>(b, cc), acc[C4 * cg + cc], 0, 0, 0);
+          }
+        }
+      }
+    }
+    if (more) {
+      dense_stage_store<Kp>(lds[buf ^ 1], pre);
+#pragma unroll
+      for (int yb = 0; yb < 4; ++yb) dcur[yb] = dnext[yb];
+    }
+    __syncthreads();
+  }
+  // acc[c][v] = dX[16w + 4g + v][col(c, i)]
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int32_t out = a.cell_out[cell * kDenseRowsDev + 16 * w + 4 * g + v];
+    if (out < 0) continue;
+    float *dst = a.partial + static_cast<int64_t>(out) * Kp;
+#pragma unroll
+    for (int cg = 0; cg < NQ / C4; ++cg) {
+      const int f = 16 * C4 * cg + C4 * i;
+      if constexpr (C4 == 4) {
+        *reinterpret_cast<float4 *>(dst + f) =
+            make_float4(acc[4 * cg][v], acc[4 * cg + 1][v], acc[4 * cg + 2][v], acc[4 * cg + 3][v]);
+      } else if constexpr (C4 == 2) {
+        *reinterpret_cast<float2 *>(dst + f) = make_float2(acc[2 * cg][v], acc[2 * cg + 1][v]);
+      } else {
+        dst[f] = acc[cg][v];
+      }
+    }
+  }
+}
+
+// The dense cells of both sweep directions in one launch: workgroups [0, ncell_a) take set
+// A, the rest set B.
+template <int Kp>
+__global__ __launch_bounds__(kDenseThreads, 2) void k_dense(DenseSweepArgs s) {
+  __shared__ float4 lds[2][kDenseRowsDev * Kp / 4];
+  const int b = static_cast<int>(blockIdx.x);
+  if (b < s.ncell_a) run_dense<Kp>(s.da, b, lds);
+  else run_dense<Kp>(s.db, b - s.ncell_a, lds);
+}
+
 // Squared loss over the canonical CSR of a block at one ring slot: one lane group per
 // segment (a user's ratings, cut at kLossSegment), e in fp32, e^2 accumulated in fp64,
 // one partial per workgroup (fixed order, so the result is deterministic).
@@ -596,6 +809,21 @@ struct LaunchUnits {
     return hipGetLastError();
   }
 };
+// padded ranks with a dense (MFMA) cell kernel
+bool dense_supported(int Kp) { return Kp >= 16 && Kp <= 128; }
+
+hipError_t launch_dense(int Kp, const DenseSweepArgs &a, int64_t grid, hipStream_t st) {
+  const dim3 gd(static_cast<unsigned>(grid)), bd(kDenseThreads);
+  switch (Kp) {
+    case 16: hipLaunchKernelGGL(k_dense<16>, gd, bd, 0, st, a); break;
+    case 32: hipLaunchKernelGGL(k_dense<32>, gd, bd, 0, st, a); break;
+    case 64: hipLaunchKernelGGL(k_dense<64>, gd, bd, 0, st, a); break;
+    case 128: hipLaunchKernelGGL(k_dense<128>, gd, bd, 0, st, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <int G, int E>
 struct LaunchLoss {
   static hipError_t run(const int32_t *seg_user, const int64_t *seg_beg, int64_t nseg, const int32_t *col,
@@ -627,6 +855,13 @@ struct DeviceCells {
   float *lv = nullptr;
 };
 
+struct DeviceDense {
+  int64_t ncells = 0;
+  int32_t *cell_x = nullptr, *cell_cls = nullptr, *cell_step_ptr = nullptr, *step_rows = nullptr,
+          *cell_out = nullptr;
+  float *dval = nullptr;
+};
+
 struct DeviceBlock {
   int64_t nnz = 0, loss_grid = 0;
   int32_t *ucount = nullptr, *icount = nullptr, *icount_cls = nullptr;
@@ -637,6 +872,7 @@ struct DeviceBlock {
   float *val = nullptr;
   DeviceUnits by_user, by_item;
   DeviceCells cells_user, cells_item;
+  DeviceDense dense_user, dense_item;
 };
 
 struct ps_mf {
@@ -652,6 +888,7 @@ struct ps_mf {
   int32_t unit_max = 1024;
   bool cells = true;             // stage the dense part (heavy users) through LDS
   int64_t heavy_min = -1;        // ratings from which a user goes to the cells (-1: automatic)
+  int32_t dense_min = -1;        // ratings from which a 64 x 64 tile goes to the MFMA cells (-1: automatic, 0: none)
   std::vector<int32_t> owner;
   // host state
   bool loaded = false, has_factors = false;
@@ -761,6 +998,34 @@ int upload_cells(ps_mf_t *h, DeviceCells &d, const psmf::CellSet &c) {
   d.padded = (d.ncells + kXcds - 1) / kXcds * kXcds;
   d.ts = c.ts;
   return PS_MF_OK;
+}
+
+int upload_dense(ps_mf_t *h, DeviceDense &d, const psmf::DenseSet &D) {
+  int r;
+  if ((r = upload(h, &d.cell_x, D.cell_x)) || (r = upload(h, &d.cell_cls, D.cell_cls)) ||
+      (r = upload(h, &d.cell_step_ptr, D.cell_step_ptr)) || (r = upload(h, &d.step_rows, D.step_rows)) ||
+      (r = upload(h, &d.cell_out, D.cell_out)) || (r = upload(h, &d.dval, D.dval)))
+    return r;
+  d.ncells = static_cast<int64_t>(D.cell_cls.size());
+  return PS_MF_OK;
+}
+
+DenseArgs dense_args(const ps_mf_t *h, const DeviceDense &d, float *partial, int64_t x_off, int64_t y_off,
+                     const int32_t *cls_slot) {
+  DenseArgs a{};
+  a.cell_x = d.cell_x;
+  a.cell_cls = d.cell_cls;
+  a.cell_step_ptr = d.cell_step_ptr;
+  a.step_rows = d.step_rows;
+  a.cell_out = d.cell_out;
+  a.dval = d.dval;
+  a.cls_slot = cls_slot;
+  a.ring = h->ring;
+  a.slot_stride = (h->N + h->M) * h->Kp;
+  a.x_off = x_off;
+  a.y_off = y_off;
+  a.partial = partial;
+  return a;
 }
 
 CellArgs cell_args(const ps_mf_t *h, const DeviceCells &d, float *partial, int64_t x_off, int64_t y_off,
@@ -896,15 +1161,23 @@ int one_clock(ps_mf_t *h) {
     const int64_t gu = db.by_user.nunits > 0 ? db.by_user.grid : 0;
     const int64_t gi = db.by_item.nunits > 0 ? db.by_item.grid : 0;
     us.grid_a = static_cast<int32_t>(gu);
-    if (ncells > 0 && gu + gi > 0 && h->side_stream) {
-      // cells on the handle's stream, units on the side stream, both after what precedes
+    DenseSweepArgs ds{};
+    ds.da = dense_args(h, db.dense_user, h->partial_u, 0, r_off, cls_slot);
+    ds.db = dense_args(h, db.dense_item, h->partial_i, r_off, 0, cls_slot);
+    ds.ncell_a = static_cast<int32_t>(db.dense_user.ncells);
+    const int64_t ndense = db.dense_user.ncells + db.dense_item.ncells;
+    if (ncells + ndense > 0 && gu + gi > 0 && h->side_stream) {
+      // dense cells and cells on the handle's stream, units on the side stream, all after
+      // what precedes
       HIP_TRY(h, hipEventRecord(h->fork, h->stream));
       HIP_TRY(h, hipStreamWaitEvent(h->side_stream, h->fork, 0));
       HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, us, gu + gi, h->side_stream));
-      HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
+      if (ndense > 0) HIP_TRY(h, launch_dense(h->Kp, ds, ndense, h->stream));
+      if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
       HIP_TRY(h, hipEventRecord(h->join, h->side_stream));
       HIP_TRY(h, hipStreamWaitEvent(h->stream, h->join, 0));
     } else {
+      if (ndense > 0) HIP_TRY(h, launch_dense(h->Kp, ds, ndense, h->stream));
       if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
       if (gu + gi > 0) HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, us, gu + gi, h->stream));
     }
@@ -1032,6 +1305,11 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
       if (value < -1) return fail(h, PS_MF_EINVAL, "heavy threshold must be >= -1");
       h->heavy_min = value;
       return PS_MF_OK;
+    case PS_MF_OPT_DENSE_MIN:
+      if (value < -1 || value > psmf::kDenseTile)
+        return fail(h, PS_MF_EINVAL, "dense tile threshold must be in [-1, %d]", psmf::kDenseTile);
+      h->dense_min = static_cast<int32_t>(value);
+      return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
   }
@@ -1100,6 +1378,9 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
     // measured best among 0..4)
     lp.hot_steps = h->hot_steps >= 0 ? h->hot_steps : 1;
   }
+  if (h->dense_min > 0 && !dense_supported(h->Kp))
+    return fail(h, PS_MF_EINVAL, "dense tiles need a padded rank in [16, 128], not %d", h->Kp);
+  lp.dense_min = h->dense_min >= 0 ? h->dense_min : (dense_supported(h->Kp) ? kDenseAuto : 0);
   std::string err;
   const int rc = psmf::build_layout(lp, user, item, value, n, h->layout, err);
   if (rc == -1) return fail(h, PS_MF_EINVAL, "%s", err.c_str());
@@ -1128,7 +1409,8 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
         (r = upload(h, &d.icount_cls, L.icount_cls)) || (r = upload(h, &d.col, L.col)) ||
         (r = upload(h, &d.val, L.val)) ||
         (r = upload_units(h, d.by_user, L.by_user)) || (r = upload_units(h, d.by_item, L.by_item)) ||
-        (r = upload_cells(h, d.cells_user, L.cells_user)) || (r = upload_cells(h, d.cells_item, L.cells_item)))
+        (r = upload_cells(h, d.cells_user, L.cells_user)) || (r = upload_cells(h, d.cells_item, L.cells_item)) ||
+        (r = upload_dense(h, d.dense_user, L.dense_user)) || (r = upload_dense(h, d.dense_item, L.dense_item)))
       return undo(r);
     // partial rows of units and cells, + the row the padding units write
     max_units_u = std::max<int64_t>(max_units_u, L.partial_rows_user + 1);
@@ -1279,6 +1561,21 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
   const void *src = nullptr;
   size_t esz = 0;
   int64_t n = 0;
+  int64_t split[6] = {0, 0, 0, 0, 0, 0};
+  if (kind == PS_MF_IDX_SPLIT) {
+    const psmf::BlockLayout &L = h->layout[block];
+    auto unit_ratings = [](const psmf::UnitSet &u) {
+      int64_t t = 0;
+      for (int32_t len : u.unit_len) t += len;
+      return t;
+    };
+    split[0] = L.dense_user.nnz;
+    split[1] = L.cells_user.nnz;
+    split[2] = unit_ratings(L.by_user);
+    split[3] = L.dense_item.nnz;
+    split[4] = L.cells_item.nnz;
+    split[5] = unit_ratings(L.by_item);
+  }
   switch (kind) {
     case PS_MF_IDX_OWNER: src = h->owner.data(); esz = 4; n = h->N; break;
     case PS_MF_IDX_ROW_PTR: src = h->layout[block].row_ptr.data(); esz = 8; n = h->N + 1; break;
@@ -1287,6 +1584,7 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     case PS_MF_IDX_USER_COUNT: src = h->layout[block].ucount.data(); esz = 4; n = h->N; break;
     case PS_MF_IDX_ITEM_COUNT: src = h->layout[block].icount.data(); esz = 4; n = h->M; break;
     case PS_MF_IDX_VERSION_LOG: src = h->vlog.data(); esz = 8; n = static_cast<int64_t>(h->vlog.size()); break;
+    case PS_MF_IDX_SPLIT: src = split; esz = 8; n = 6; break;
     default: return fail(h, PS_MF_EINVAL, "unknown index kind %d", kind);
   }
   *len = n;

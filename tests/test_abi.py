@@ -169,3 +169,68 @@ def test_host_layout_self_check_with_hot_cells_and_custom_owner(policy, s, B):
         o = oracle.Oracle(N, M, 16, P, s, 0.01, 0.05, policy, oracle.ROWMEAN, B, seed, owner)
         o.load(user, item, val)
         compare_layout(g, o, B, N, M)
+
+
+def split_of(g, b=0):
+    s = g.export_index(ps_mf.IDX_SPLIT, b)
+    assert s.shape == (6,)
+    return s
+
+
+@pytest.mark.parametrize("dense_min", [1, 9, 200])
+@pytest.mark.parametrize("policy,s,B", [(0, 0, 1), (0, 3, 1), (1, 2, 3), (2, 5, 2)])
+@pytest.mark.parametrize("K", [16, 100])
+def test_host_layout_self_check_with_dense_tiles(dense_min, policy, s, B, K):
+    """Dense (matrix-core) tiles next to cells and units: every rating is swept exactly once
+    per direction (self-check on load), duplicates of a (user, item) pair included, and the
+    exported canonical layout is still the oracle's."""
+    rng = np.random.default_rng(1000 * dense_min + 10 * s + B)
+    N, M, P, n = 900, 400, 6, 80000
+    # a block of heavy users x popular items (dense), plus scattered ratings and duplicates
+    user = np.concatenate([rng.integers(0, 150, n // 2), rng.integers(0, N, n // 2)]).astype(np.int32)
+    item = np.concatenate([rng.integers(0, 130, n // 2), rng.integers(0, M, n // 2)]).astype(np.int32)
+    val = rng.integers(1, 6, user.size).astype(np.float32)
+    owner = rng.integers(0, P, N).astype(np.int32)
+    seed = 0x14108043 + 31 * B
+    with ps_mf.PsMf(N, M, K, P, s, 0.01, 0.05, policy=policy, B=B, mb_seed=seed, owner=owner, host_only=True,
+                    cells=True, heavy_min=64, hot_steps=1, dense_min=dense_min) as g:
+        g.load_ratings(user, item, val)
+        o = oracle.Oracle(N, M, K, P, s, 0.01, 0.05, policy, oracle.ROWMEAN, B, seed, owner)
+        o.load(user, item, val)
+        compare_layout(g, o, B, N, M)
+        for b in range(B):
+            sp = split_of(g, b)
+            nb = g.export_index(ps_mf.IDX_COL, b).size
+            assert sp[:3].sum() == nb and sp[3:].sum() == nb
+            assert sp[0] == sp[3] and sp[0] > 0
+            if dense_min == 1 and B == 1:
+                # every tile with a rating is dense: only the repeats of a (user, item) pair
+                # stay sparse
+                assert sp[0] == np.unique(user.astype(np.int64) * M + item).size
+
+
+def test_dense_tiles_need_a_supported_rank():
+    for K, ok in [(8, False), (16, True), (128, True), (129, False)]:
+        with ps_mf.PsMf(40, 30, K, 2, 1, 0.01, 0.05, host_only=True, dense_min=5) as g:
+            u = np.arange(40, dtype=np.int32).repeat(30)
+            i = np.tile(np.arange(30, dtype=np.int32), 40)
+            if ok:
+                g.load_ratings(u, i, np.ones(u.size, np.float32))
+                assert split_of(g)[0] == u.size
+            else:
+                with pytest.raises(ps_mf.PsMfError) as e:
+                    g.load_ratings(u, i, np.ones(u.size, np.float32))
+                assert e.value.code == ps_mf.EINVAL
+    # the automatic threshold never fails: it leaves unsupported ranks without dense tiles
+    with ps_mf.PsMf(40, 30, 8, 2, 1, 0.01, 0.05, host_only=True) as g:
+        g.load_ratings(np.arange(40, dtype=np.int32).repeat(30), np.tile(np.arange(30, dtype=np.int32), 40),
+                       np.ones(1200, np.float32))
+        assert split_of(g)[0] == 0
+    h = ps_mf.ps_mf_create(4, 3, 16, 1, 0, 0.1, 0.1)
+    try:
+        for bad in (-2, 4097):
+            with pytest.raises(ps_mf.PsMfError) as e:
+                ps_mf.ps_mf_set_option(h, ps_mf.OPT_DENSE_MIN, bad)
+            assert e.value.code == ps_mf.EINVAL
+    finally:
+        ps_mf.ps_mf_destroy(h)

@@ -34,7 +34,7 @@ def say(msg):
 
 
 def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, policy=0, step=0, B=1,
-             seed=0, owner=None, check_versions=False, **handle_opts):
+             seed=0, owner=None, check_versions=False, min_dense=0, **handle_opts):
     say(f"case N={N} M={M} K={K} P={P} s={s} policy={policy} step={step} B={B} nnz={len(w_user)} clocks={clocks} "
         f"{handle_opts}")
     o = oracle.Oracle(N, M, K, P, s, eta, lam, policy, step, B, seed, owner)
@@ -43,6 +43,11 @@ def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, c
     with ps_mf.PsMf(N, M, K, P, s, eta, lam, policy=policy, step=step, B=B, mb_seed=seed, owner=owner,
                     **handle_opts) as g:
         g.load_ratings(w_user, w_item, w_val)
+        if min_dense:
+            # the case must put at least min_dense ratings into dense (MFMA) tiles
+            split = sum(g.export_index(ps_mf.IDX_SPLIT, b) for b in range(B))
+            say(f"  split (dense, cells, units) x (user-major, item-major): {split.tolist()}")
+            assert split[0] >= min_dense and split[3] == split[0]
         g.set_factors(L0, R0)
         g.clock(clocks)
         o.clock(clocks)
@@ -238,6 +243,53 @@ def test_checkpoint_resume_at_s0(gpu):
         b.clock(5)
         Lr, Rr = b.get_factors()
     assert max(np.abs(L10 - Lr).max(), np.abs(R10 - Rr).max()) <= FACTOR_TOL
+
+
+# ---------------------------------------------------------------- dense (MFMA) tiles
+@pytest.mark.parametrize("s,policy", [(0, oracle.SSP_LAZY), (2, oracle.SSP_LAZY), (2, oracle.SSP_WORST),
+                                      (2, oracle.ESSP)])
+@pytest.mark.parametrize("dense_min", [1, 150])
+def test_tiny_config_dense_tiles(gpu, s, policy, dense_min):
+    """The tiny workload with every 64 x 64 tile (dense_min = 1) or about half of them swept
+    by the matrix-core cells, the rest by cells and units."""
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta,
+             lam=spec.lam, clocks=spec.clocks, policy=policy, check_versions=True, dense_min=dense_min,
+             min_dense=spec.nnz // 4)
+
+
+@pytest.mark.parametrize("K", [16, 32, 64, 100, 128])
+@pytest.mark.parametrize("dense_min", [1, 300, 1229])
+def test_dense_tiles_mixed_with_cells_and_units(gpu, K, dense_min):
+    """The 100M-rating workload's laws at 5% size, s=3 (four worker classes): dense tiles of
+    heavy users x popular items next to LDS cells and L2 units, ragged tile edges."""
+    spec = synth.scaled(synth.CONFIGS["full"], 0.05)
+    w = synth.generate(spec, K=K)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=K, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=6, check_versions=True, dense_min=dense_min, heavy_min=100, hot_steps=1,
+             min_dense=4096)
+
+
+@pytest.mark.parametrize("K", [16, 33, 100, 128])
+def test_dense_tiles_ragged_rank_duplicates_and_empty_rows(gpu, K):
+    """Every tile dense: padded ranks, duplicate (user, item) pairs (the repeats stay
+    sparse), users and items without ratings and a scattering owner map."""
+    N, M = 300, 90
+    user, item, val, L0, R0 = small_problem(K + 1, N, M, 6000, K, dup=40)
+    keep = (user % 7 != 0) & (item % 5 != 0)
+    owner = np.random.default_rng(K).integers(0, 5, N).astype(np.int32)
+    run_both(gpu, user[keep], item[keep], val[keep], L0, R0, N=N, M=M, K=K, P=5, s=2, eta=0.05, lam=0.05,
+             clocks=6, owner=owner, check_versions=True, dense_min=1, min_dense=1000)
+
+
+@pytest.mark.parametrize("step", [oracle.ROWMEAN, oracle.SUM])
+def test_dense_tiles_medium_minibatch_blocks(gpu, step):
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.05)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3,
+             eta=spec.eta if step == oracle.ROWMEAN else 1e-4, lam=spec.lam, clocks=8, B=spec.B, seed=spec.seed,
+             step=step, dense_min=64, min_dense=4096)
 
 
 def test_timing_option_counts_launches(gpu):
