@@ -126,7 +126,7 @@ def main():
     nnz_clock = w.nnz / spec.B  # mean ratings per clock (exact for B=1)
     split = sum(g.export_index(ps_mf.IDX_SPLIT, b) for b in range(spec.B))
     print(f"[bench] ratings per direction in dense tiles / LDS cells / L2 units: {split[:3].tolist()} (user-major), "
-          f"{split[3:].tolist()} (item-major)", file=sys.stderr, flush=True)
+          f"{split[3:6].tolist()} (item-major); partial rows {split[6:].tolist()}", file=sys.stderr, flush=True)
 
     if args.copy_calibration_bytes > 0:
         src = torch.ones(args.copy_calibration_bytes // 4, dtype=torch.float32, device="cuda")

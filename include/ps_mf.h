@@ -68,9 +68,10 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_OPT_HOST_ONLY 5 /* 1: build, self-check and export the integer layout only; never touch
                                  a device (a failed self-check returns PS_MF_EINTERNAL) */
 #define PS_MF_OPT_TIMING 6    /* 1: record HIP events around every kernel (ps_mf_kernel_time) */
-#define PS_MF_OPT_TILE_BYTES 7 /* bytes of user rows per tile of the item-major sweep (default 3 MiB,
-                                  sized to one XCD's 4 MiB L2); >= 1 */
-#define PS_MF_OPT_UNIT_MAX 8   /* ratings per sweep work unit (default 1024); >= 1 */
+#define PS_MF_OPT_TILE_BYTES 7 /* bytes of user rows per tile of the item-major sweep (default 6 MiB:
+                                  about one XCD's 4 MiB L2; larger tiles mean fewer partial rows);
+                                  >= 1 */
+#define PS_MF_OPT_UNIT_MAX 8   /* ratings per sweep work unit (default 256); >= 1 */
 #define PS_MF_OPT_CELLS 9      /* 1 (default): sweep the dense part (users with many ratings) through
                                   LDS-staged cells; 0: every rating through the L2 work units */
 #define PS_MF_OPT_HEAVY_MIN 10 /* ratings in a block from which a user's ratings go to the cells;
@@ -79,7 +80,8 @@ typedef struct ps_mf ps_mf_t;
                                     (default priority) beside the cells; 0: one stream */
 #define PS_MF_OPT_HOT_STEPS 12 /* LDS sub-tiles of a block's most rated items whose ratings by the
                                   remaining (light) users also go to cells; 0: none;
-                                  -1 (default): automatic (one sub-tile).  Needs
+                                  -1 (default): automatic (none when dense tiles are in
+                                  use, else one sub-tile).  Needs
                                   PS_MF_OPT_CELLS = 1; at most 1024 */
 #define PS_MF_OPT_DENSE_MIN 13 /* ratings from which a 64 x 64 tile (64 users of one worker class
                                   ranked by rating count x 64 items ranked by rating count) is
@@ -104,10 +106,12 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_IDX_USER_COUNT 4  /* int32 [users]: ratings of each user in block b */
 #define PS_MF_IDX_ITEM_COUNT 5  /* int32 [items]: ratings of each item in block b (all workers) */
 #define PS_MF_IDX_VERSION_LOG 6 /* int64 [clocks*P]: v(p,c) at entry c*P + p (clock-major, Section 3.2) */
-#define PS_MF_IDX_SPLIT 7       /* int64 [6]: how block b's ratings are swept: ratings in dense
+#define PS_MF_IDX_SPLIT 7       /* int64 [8]: how block b's ratings are swept: ratings in dense
                                    (matrix-core) tiles, in LDS-staged cells and in L2 work units,
                                    for the user-major then the item-major direction (each triple
-                                   sums to the block's rating count) */
+                                   sums to the block's rating count); then the partial rows
+                                   (Kp floats each) the user-major and the item-major sweep
+                                   write per clock for the commit to sum */
 
 /* kernel ids (ps_mf_kernel_time) */
 #define PS_MF_KERNEL_SWEEP 0  /* residual, dL segment-sum and dR accumulation of one clock */

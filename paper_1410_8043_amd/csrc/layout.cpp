@@ -698,6 +698,12 @@ void build_dense(const LayoutParams &p, const BlockLayout &L, const std::vector<
         if (!uts[it][c].empty()) cut(segs, c, static_cast<int32_t>(it), uts[it][c], ids[it][c]);
     emit(DI, segs, false, extra_i, step_i);
   }
+  DU.step_twin.resize(static_cast<size_t>(ntiles));
+  DI.step_twin.resize(static_cast<size_t>(ntiles));
+  for (int64_t t = 0; t < ntiles; ++t) {
+    DU.step_twin[step_u[t]] = static_cast<int32_t>(step_i[t]);
+    DI.step_twin[step_i[t]] = static_cast<int32_t>(step_u[t]);
+  }
   // the values: one pass over the rows of each dense user tile fills both directions' blocks
   // (user tiles write disjoint steps; parallel_for hands each thread the tiles u with
   // u * 2^16 in its range)
@@ -1126,6 +1132,43 @@ int check_direction(const char *dir, int64_t nx, int64_t ny, std::vector<Triple>
   return 0;
 }
 
+// The two directions' dense steps pair up tile by tile (step_twin): the item-major twin of
+// a user-major step stages the users the user-major cell holds, belongs to a cell that
+// holds the items the user-major step stages, reads the same class and holds the same
+// values, transposed.  The user-major sweep writes its residuals where the item-major
+// sweep reads them on exactly this correspondence.
+int check_dense_twins(const DenseSet &U, const DenseSet &I, std::string &err) {
+  auto bad = [&](const std::string &what) {
+    err = "dense twins: " + what;
+    return -1;
+  };
+  const int64_t T = kDenseRows;
+  const int64_t nu = static_cast<int64_t>(U.step_rows.size()) / T, ni = static_cast<int64_t>(I.step_rows.size()) / T;
+  if (nu != ni || U.step_twin.size() != static_cast<size_t>(nu) || I.step_twin.size() != static_cast<size_t>(ni))
+    return bad("step counts or twin maps disagree");
+  std::vector<int64_t> cell_of_i(static_cast<size_t>(ni), -1);
+  for (size_t c = 0; c + 1 < I.cell_step_ptr.size(); ++c)
+    for (int64_t k = I.cell_step_ptr[c]; k < I.cell_step_ptr[c + 1]; ++k) cell_of_i[k] = static_cast<int64_t>(c);
+  for (size_t c = 0; c + 1 < U.cell_step_ptr.size(); ++c)
+    for (int64_t k = U.cell_step_ptr[c]; k < U.cell_step_ptr[c + 1]; ++k) {
+      const int64_t t = U.step_twin[k];
+      if (t < 0 || t >= ni || I.step_twin[t] != k) return bad("the twin map is not a bijection");
+      const int64_t ci = cell_of_i[t];
+      if (ci < 0 || I.cell_cls[ci] != U.cell_cls[c]) return bad("twin steps read different classes");
+      for (int64_t q = 0; q < T; ++q) {
+        if (I.step_rows[t * T + q] != U.cell_x[c * T + q]) return bad("a twin step stages other users");
+        if (I.cell_x[ci * T + q] != U.step_rows[k * T + q]) return bad("a twin cell holds other items");
+      }
+      for (int32_t x = 0; x < T; ++x)
+        for (int32_t y = 0; y < T; ++y) {
+          const float a = U.dval[static_cast<size_t>(k * kDenseTile + dense_frag_index(x, y))];
+          const float b = I.dval[static_cast<size_t>(t * kDenseTile + dense_frag_index(y, x))];
+          if (std::memcmp(&a, &b, sizeof a) != 0) return bad("twin steps hold different values");
+        }
+    }
+  return 0;
+}
+
 }  // namespace
 
 int check_layout(const LayoutParams &p, const BlockLayout &L, std::string &err) {
@@ -1148,6 +1191,7 @@ int check_layout(const LayoutParams &p, const BlockLayout &L, std::string &err) 
   const std::function<int32_t(int32_t, int32_t)> ci = [&](int32_t, int32_t y) { return ucls[y]; };
   if (check_direction("user-major", N, M, std::move(by_user), L.by_user, L.cells_user, L.dense_user, cu, err)) return -1;
   if (check_direction("item-major", M, N, std::move(by_item), L.by_item, L.cells_item, L.dense_item, ci, err)) return -1;
+  if (check_dense_twins(L.dense_user, L.dense_item, err)) return -1;
   if (L.partial_rows_user != L.by_user.x_pp[N] || L.partial_rows_item != L.by_item.x_pp[M]) {
     err = "partial row counts disagree with the row offsets";
     return -1;

@@ -20,7 +20,7 @@ constexpr int kDenseTile = kDenseRows * kDenseRows;
 // holds rows x of the stationary side; for its 16-row slice yb = y / 16 of the staged
 // side, lane l = (x % 16) + 16 * ((y % 16) / 4) reads the 4 values y % 4 = 0..3 as one
 // float4 (the C/D fragment of a 16x16x4 fp32 MFMA whose rows are y and columns x).
-inline int32_t dense_frag_index(int32_t x, int32_t y) {
+constexpr int32_t dense_frag_index(int32_t x, int32_t y) {
   const int32_t w = x >> 4, yb = y >> 4, lane = (x & 15) + 16 * ((y & 15) >> 2);
   return (((w * 4 + yb) * 64 + lane) << 2) + (y & 3);
 }
@@ -101,6 +101,7 @@ struct DenseSet {
   std::vector<int32_t> cell_step_ptr;  // [ncells + 1] into the steps
   std::vector<int32_t> step_rows;      // [nsteps * 64] staged rows of each step, -1 = no row
   std::vector<float> dval;             // [nsteps * 4096]
+  std::vector<int32_t> step_twin;      // [nsteps] the other direction's step of the same tile
   std::vector<int32_t> cell_out;       // [ncells * 64], -1 for unused rows
   int64_t nnz = 0;                     // ratings covered
 };

@@ -392,7 +392,10 @@ __global__ __launch_bounds__(kBlock) void k_units(UnitSweepArgs s) {
 //   S^T = Y_s X_w^T                (16 y x 16 x, contraction over the rank),
 //   E^T = D^T - S^T where rated, 0 elsewhere (the residuals, Section 3.1),
 //   acc += E Y_s                   (16 x rows x Kp, contraction over the 16 y rows),
-// so each rated (x, y) adds e_xy Y_y to acc_x exactly as the per-rating sweeps do.  Fragment
+// so each rated (x, y) adds e_xy Y_y to acc_x exactly as the per-rating sweeps do.  The
+// user-major pass also stores E in the item-major pass's fragment order, and the
+// item-major pass (FromE) starts from those residuals: it skips GEMM 1 (a quarter of the
+// dense products) and reads E where the user-major pass reads D.  Fragment
 // layouts of the 16x16x4 fp32 MFMA (lane l, i = l % 16, g = l / 16): A operand A[i][g],
 // B operand B[g][i], C/D holds D[4g + v][i] in register v.
 //   GEMM 1: A[i][g] = Y[16 ys + i][k], B[g][i] = X[16 w + i][k] with the rank index
@@ -407,16 +410,14 @@ static_assert(kDenseThreads / 64 * 16 == kDenseRowsDev, "one wavefront per 16 x 
 
 struct DenseArgs {
   const int32_t *cell_x, *cell_cls, *cell_step_ptr, *step_rows, *cell_out;
-  const float *dval;
+  const float *dval;        // D (user-major) or the stored residuals E (item-major), fragment order
+  float *eout;              // user-major: E in the item-major fragment order
+  const int32_t *step_twin; // user-major: the item-major step of the same tile
+  const float *zero;        // Kp zeros: the source of staged rows past the end of a ragged tile
   const int32_t *cls_slot;
   const float *ring;
   int64_t slot_stride, x_off, y_off;
   float *partial;
-};
-
-struct DenseSweepArgs {
-  DenseArgs da, db;
-  int32_t ncell_a;
 };
 
 // float4 chunk h of staged row y in LDS: chunks are XOR-swizzled by the row so that the
@@ -445,34 +446,40 @@ __device__ __forceinline__ float vec_at(const typename VecOf<C4>::T &v, int c) {
   else return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
 }
 
+typedef __attribute__((address_space(3))) char lds_char;
+
+// Stage the 64 y rows of step k into an LDS buffer with direct global-to-LDS loads
+// (global_load_lds_dwordx4): the loads of one wavefront write 64 consecutive 16-byte
+// chunks starting at a wave-uniform LDS address, so lane l fetches the row chunk that the
+// swizzle places at physical chunk p = 256 m + 64 w + l.  Rows -1 (past the end of a
+// ragged tile) read a zero row.  Completion is waited for (vmcnt) before the barrier that
+// hands the buffer to the readers.
 template <int Kp>
-__device__ __forceinline__ void dense_stage_load(const DenseArgs &a, const float *__restrict__ Y, int64_t k,
-                                                 float4 (&pre)[Kp / 16]) {
+__device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__restrict__ Y, int64_t k,
+                                            float4 *lds_buf) {
   constexpr int H = Kp / 4;
+  constexpr int SW = H < 16 ? H : 16;
   const int32_t *rows = a.step_rows + k * kDenseRowsDev;
+  const int lane = static_cast<int>(threadIdx.x) & 63, w = static_cast<int>(threadIdx.x) >> 6;
 #pragma unroll
   for (int m = 0; m < Kp / 16; ++m) {
-    const int u = static_cast<int>(threadIdx.x) + kDenseThreads * m;
-    const int32_t r = rows[u / H];
-    pre[m] = r >= 0 ? *reinterpret_cast<const float4 *>(Y + static_cast<int64_t>(r) * Kp + 4 * (u % H))
-                    : make_float4(0.f, 0.f, 0.f, 0.f);
+    const int p = kDenseThreads * m + 64 * w + lane;
+    const int y = p / H, h = (p % H) ^ (y & (SW - 1));
+    const int32_t r = rows[y];
+    const float *src = (r >= 0 ? Y + static_cast<int64_t>(r) * Kp : a.zero) + 4 * h;
+    lds_char *dst = (lds_char *)(lds_buf) + 16 * (kDenseThreads * m + 64 * w);  // generic -> LDS address space
+    __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
   }
 }
 
-template <int Kp>
-__device__ __forceinline__ void dense_stage_store(float4 *lds, const float4 (&pre)[Kp / 16]) {
-  constexpr int H = Kp / 4;
-#pragma unroll
-  for (int m = 0; m < Kp / 16; ++m) {
-    const int u = static_cast<int>(threadIdx.x) + kDenseThreads * m;
-    lds[dense_lds_chunk<Kp>(u / H, u % H)] = pre[m];
-  }
-}
-
-template <int Kp>
-__device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, float4 (*lds)[kDenseRowsDev * Kp / 4]) {
+// The two staging buffers are separate LDS variables and the step loop alternates them
+// statically: the compiler then knows that the DMA into one buffer does not alias the
+// reads of the other and does not wait for the DMA before those reads.
+template <int Kp, bool FromE>
+__device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, float4 *lds0, float4 *lds1) {
   constexpr int NQ = Kp / 16;             // rank chunks of 16 (GEMM 1) = output blocks of 16 columns (GEMM 2)
   constexpr int C4 = NQ < 4 ? NQ : 4;     // output blocks read / stored together
+  constexpr int NB = 4 * (NQ / C4);       // GEMM 2 operand reads per 16-row slice
   typedef typename VecOf<C4>::T VecT;
   const int lane = static_cast<int>(threadIdx.x) & 63, w = static_cast<int>(threadIdx.x) >> 6;
   const int i = lane & 15, g = lane >> 4;
@@ -480,9 +487,11 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
   const float *__restrict__ V = a.ring + sv * a.slot_stride;
   const float *__restrict__ X = V + a.x_off;
   const float *__restrict__ Y = V + a.y_off;
+  const int64_t k0 = a.cell_step_ptr[cell], k1 = a.cell_step_ptr[cell + 1];
+  if (k0 < k1) dense_stage<Kp>(a, Y, k0, lds0);
   // stationary rows in the B-operand layout of GEMM 1: xb[q] = X[16w + i][16q + 4g .. +3]
   float4 xb[NQ];
-  {
+  if constexpr (!FromE) {
     const int32_t xr = a.cell_x[cell * kDenseRowsDev + 16 * w + i];
 #pragma unroll
     for (int q = 0; q < NQ; ++q)
@@ -492,73 +501,95 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
   f32x4 acc[NQ];
 #pragma unroll
   for (int c = 0; c < NQ; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int64_t k0 = a.cell_step_ptr[cell], k1 = a.cell_step_ptr[cell + 1];
   const f32x4 *__restrict__ dv = reinterpret_cast<const f32x4 *>(a.dval);
-  float4 pre[NQ];
   f32x4 dcur[4], dnext[4];
   if (k0 < k1) {
-    dense_stage_load<Kp>(a, Y, k0, pre);
 #pragma unroll
     for (int yb = 0; yb < 4; ++yb) dcur[yb] = dv[(k0 * 16 + w * 4 + yb) * 64 + lane];
-    dense_stage_store<Kp>(lds[0], pre);
   }
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  for (int64_t k = k0; k < k1; ++k) {
-    const int buf = static_cast<int>((k - k0) & 1);
+  // one step: sweep the rows staged in T4 while the next step's rows go to `nextbuf`
+  auto step = [&](int64_t k, const float4 *T4, float4 *nextbuf) {
     const bool more = k + 1 < k1;
-    if (more) {  // the next step's rows and values, written to the other buffer after this step
-      dense_stage_load<Kp>(a, Y, k + 1, pre);
+    if (more) {  // the next step's rows (into the other buffer) and values
+      dense_stage<Kp>(a, Y, k + 1, nextbuf);
 #pragma unroll
       for (int yb = 0; yb < 4; ++yb) dnext[yb] = dv[((k + 1) * 16 + w * 4 + yb) * 64 + lane];
     }
-    const float4 *T4 = lds[buf];
+    const char *Tb = reinterpret_cast<const char *>(T4);
 #pragma unroll
     for (int y2 = 0; y2 < 4; y2 += 2) {
-      // GEMM 1 for two 16-row slices at once (two independent accumulation chains)
-      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+      float e[2][4];
+      if constexpr (FromE) {
+        // the residuals of the user-major pass (0 where there is no rating)
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const float4 a0 = T4[dense_lds_chunk<Kp>(16 * y2 + i, 4 * q + g)];
-        const float4 a1 = T4[dense_lds_chunk<Kp>(16 * y2 + 16 + i, 4 * q + g)];
-        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, xb[q].x, s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, xb[q].x, s1, 0, 0, 0);
-        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, xb[q].y, s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.y, xb[q].y, s1, 0, 0, 0);
-        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.z, xb[q].z, s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, xb[q].z, s1, 0, 0, 0);
-        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, xb[q].w, s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, xb[q].w, s1, 0, 0, 0);
-      }
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const f32x4 sv4 = h ? s1 : s0;
-        const f32x4 d = dcur[y2 + h];
-        // residual where rated (D is NaN elsewhere), as the A operand of GEMM 2
-        float e[4];
+          for (int v = 0; v < 4; ++v) e[h][v] = dcur[y2 + h][v];
+      } else {
+        // GEMM 1 for two 16-row slices at once (two independent accumulation chains); the
+        // operands of chunk q+1 are read from LDS before the products of chunk q
+        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+        float4 a0n = T4[dense_lds_chunk<Kp>(16 * y2 + i, g)];
+        float4 a1n = T4[dense_lds_chunk<Kp>(16 * y2 + 16 + i, g)];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) e[v] = d[v] == d[v] ? d[v] - sv4[v] : 0.f;
-        const int ys = y2 + h;
+        for (int q = 0; q < NQ; ++q) {
+          const float4 a0 = a0n, a1 = a1n;
+          if (q + 1 < NQ) {
+            a0n = T4[dense_lds_chunk<Kp>(16 * y2 + i, 4 * (q + 1) + g)];
+            a1n = T4[dense_lds_chunk<Kp>(16 * y2 + 16 + i, 4 * (q + 1) + g)];
+          }
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, xb[q].x, s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, xb[q].x, s1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, xb[q].y, s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.y, xb[q].y, s1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.z, xb[q].z, s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, xb[q].z, s1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, xb[q].w, s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, xb[q].w, s1, 0, 0, 0);
+        }
+        // residuals where rated (D is NaN elsewhere): the A operands of GEMM 2; stored for
+        // the item-major pass at its fragment position of (x = item, y = user)
+        float *eo = a.eout + static_cast<int64_t>(a.step_twin[k]) * psmf::kDenseTile;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const char *row = reinterpret_cast<const char *>(T4);
+        for (int h = 0; h < 2; ++h) {
+          const f32x4 sv4 = h ? s1 : s0;
+          const f32x4 d = dcur[y2 + h];
 #pragma unroll
-          for (int cg = 0; cg < NQ / C4; ++cg) {
-            const int f = 16 * C4 * cg + C4 * i;  // first float of this lane's columns
-            const int y = 16 * ys + 4 * g + r;
-            const VecT b = *reinterpret_cast<const VecT *>(row + 16 * dense_lds_chunk<Kp>(y, f >> 2) + 4 * (f & 3));
-#pragma unroll
-            for (int cc = 0; cc < C4; ++cc)
-              acc[C4 * cg + cc] = __builtin_amdgcn_mfma_f32_16x16x4f32(e[r], vec_at<C4>(b, cc), acc[C4 * cg + cc], 0, 0, 0);
+          for (int v = 0; v < 4; ++v) {
+            e[h][v] = d[v] == d[v] ? d[v] - sv4[v] : 0.f;
+            eo[psmf::dense_frag_index(16 * (y2 + h) + 4 * g + v, 16 * w + i)] = e[h][v];
           }
         }
       }
+      // GEMM 2 over both slices; operand read t = (h, r, cg), the next one read first
+      auto boff = [&](int t) {
+        const int h = t / NB, r = (t % NB) / (NQ / C4), cg = t % (NQ / C4);
+        const int f = 16 * C4 * cg + C4 * i;  // first float of this lane's columns
+        return 16 * dense_lds_chunk<Kp>(16 * (y2 + h) + 4 * g + r, f >> 2) + 4 * (f & 3);
+      };
+      VecT bn = *reinterpret_cast<const VecT *>(Tb + boff(0));
+#pragma unroll
+      for (int t = 0; t < 2 * NB; ++t) {
+        const VecT b = bn;
+        if (t + 1 < 2 * NB) bn = *reinterpret_cast<const VecT *>(Tb + boff(t + 1));
+        const int h = t / NB, r = (t % NB) / (NQ / C4), cg = t % (NQ / C4);
+#pragma unroll
+        for (int cc = 0; cc < C4; ++cc)
+          acc[C4 * cg + cc] = __builtin_amdgcn_mfma_f32_16x16x4f32(e[h][r], vec_at<C4>(b, cc), acc[C4 * cg + cc], 0, 0, 0);
+      }
     }
     if (more) {
-      dense_stage_store<Kp>(lds[buf ^ 1], pre);
 #pragma unroll
       for (int yb = 0; yb < 4; ++yb) dcur[yb] = dnext[yb];
     }
+    __builtin_amdgcn_s_waitcnt(0);  // the staged rows of step k+1 have landed
     __syncthreads();
+  };
+  for (int64_t k = k0; k < k1; k += 2) {
+    step(k, lds0, lds1);
+    if (k + 1 < k1) step(k + 1, lds1, lds0);
   }
   // acc[c][v] = dX[16w + 4g + v][col(c, i)]
 #pragma unroll
@@ -583,12 +614,13 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
 
 // The dense cells of both sweep directions in one launch: workgroups [0, ncell_a) take set
 // A, the rest set B.
-template <int Kp>
-__global__ __launch_bounds__(kDenseThreads, 2) void k_dense(DenseSweepArgs s) {
-  __shared__ float4 lds[2][kDenseRowsDev * Kp / 4];
-  const int b = static_cast<int>(blockIdx.x);
-  if (b < s.ncell_a) run_dense<Kp>(s.da, b, lds);
-  else run_dense<Kp>(s.db, b - s.ncell_a, lds);
+// One workgroup per dense cell of one direction: the user-major cells (residuals from D,
+// stored as E), then, in a second launch, the item-major cells (FromE).
+template <int Kp, bool FromE>
+__global__ __launch_bounds__(kDenseThreads, 2) void k_dense(DenseArgs a) {
+  __shared__ float4 lds0[kDenseRowsDev * Kp / 4];
+  __shared__ float4 lds1[kDenseRowsDev * Kp / 4];
+  run_dense<Kp, FromE>(a, static_cast<int64_t>(blockIdx.x), lds0, lds1);
 }
 
 // Squared loss over the canonical CSR of a block at one ring slot: one lane group per
@@ -812,13 +844,14 @@ struct LaunchUnits {
 // padded ranks with a dense (MFMA) cell kernel
 bool dense_supported(int Kp) { return Kp >= 16 && Kp <= 128; }
 
-hipError_t launch_dense(int Kp, const DenseSweepArgs &a, int64_t grid, hipStream_t st) {
+template <bool FromE>
+hipError_t launch_dense(int Kp, const DenseArgs &a, int64_t grid, hipStream_t st) {
   const dim3 gd(static_cast<unsigned>(grid)), bd(kDenseThreads);
   switch (Kp) {
-    case 16: hipLaunchKernelGGL(k_dense<16>, gd, bd, 0, st, a); break;
-    case 32: hipLaunchKernelGGL(k_dense<32>, gd, bd, 0, st, a); break;
-    case 64: hipLaunchKernelGGL(k_dense<64>, gd, bd, 0, st, a); break;
-    case 128: hipLaunchKernelGGL(k_dense<128>, gd, bd, 0, st, a); break;
+    case 16: hipLaunchKernelGGL((k_dense<16, FromE>), gd, bd, 0, st, a); break;
+    case 32: hipLaunchKernelGGL((k_dense<32, FromE>), gd, bd, 0, st, a); break;
+    case 64: hipLaunchKernelGGL((k_dense<64, FromE>), gd, bd, 0, st, a); break;
+    case 128: hipLaunchKernelGGL((k_dense<128, FromE>), gd, bd, 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -858,8 +891,9 @@ struct DeviceCells {
 struct DeviceDense {
   int64_t ncells = 0;
   int32_t *cell_x = nullptr, *cell_cls = nullptr, *cell_step_ptr = nullptr, *step_rows = nullptr,
-          *cell_out = nullptr;
+          *cell_out = nullptr, *step_twin = nullptr;
   float *dval = nullptr;
+  float *eval = nullptr;  // item-major set: the residuals the user-major pass stores each clock
 };
 
 struct DeviceBlock {
@@ -884,8 +918,8 @@ struct ps_mf {
   int32_t policy = PS_MF_SSP_LAZY, step = PS_MF_STEP_ROWMEAN, B = 1;
   uint64_t seed = 0;
   bool host_only = false, timing = false;
-  int64_t tile_bytes = 3 << 20;  // rows per L2 tile of the sweeps, in bytes
-  int32_t unit_max = 1024;
+  int64_t tile_bytes = 6 << 20;  // rows per L2 tile of the sweeps, in bytes
+  int32_t unit_max = 256;
   bool cells = true;             // stage the dense part (heavy users) through LDS
   int64_t heavy_min = -1;        // ratings from which a user goes to the cells (-1: automatic)
   int32_t dense_min = -1;        // ratings from which a 64 x 64 tile goes to the MFMA cells (-1: automatic, 0: none)
@@ -909,6 +943,7 @@ struct ps_mf {
   int32_t hot_steps = -1;  // LDS sub-tiles of hot items whose light-user ratings go to cells (-1: auto)
   float *ring = nullptr;
   float *partial_u = nullptr, *partial_i = nullptr;
+  float *zero_row = nullptr;  // Kp zeros (staging source of empty dense rows)
   int32_t *ucls = nullptr;
   int32_t *slot_table = nullptr;  // [(2s+1) * nclass]
   double *loss_partial = nullptr;
@@ -1000,25 +1035,35 @@ int upload_cells(ps_mf_t *h, DeviceCells &d, const psmf::CellSet &c) {
   return PS_MF_OK;
 }
 
-int upload_dense(ps_mf_t *h, DeviceDense &d, const psmf::DenseSet &D) {
+// the user-major set keeps D and the map to the item-major steps; the item-major set
+// keeps a residual buffer of its steps instead of its own copy of D
+int upload_dense(ps_mf_t *h, DeviceDense &d, const psmf::DenseSet &D, bool user_major) {
   int r;
   if ((r = upload(h, &d.cell_x, D.cell_x)) || (r = upload(h, &d.cell_cls, D.cell_cls)) ||
       (r = upload(h, &d.cell_step_ptr, D.cell_step_ptr)) || (r = upload(h, &d.step_rows, D.step_rows)) ||
-      (r = upload(h, &d.cell_out, D.cell_out)) || (r = upload(h, &d.dval, D.dval)))
+      (r = upload(h, &d.cell_out, D.cell_out)))
     return r;
+  if (user_major) {
+    if ((r = upload(h, &d.dval, D.dval)) || (r = upload(h, &d.step_twin, D.step_twin))) return r;
+  } else {
+    if ((r = dev_alloc(h, reinterpret_cast<void **>(&d.eval), D.dval.size() * sizeof(float)))) return r;
+  }
   d.ncells = static_cast<int64_t>(D.cell_cls.size());
   return PS_MF_OK;
 }
 
 DenseArgs dense_args(const ps_mf_t *h, const DeviceDense &d, float *partial, int64_t x_off, int64_t y_off,
-                     const int32_t *cls_slot) {
+                     const int32_t *cls_slot, const DeviceDense &twin) {
   DenseArgs a{};
   a.cell_x = d.cell_x;
   a.cell_cls = d.cell_cls;
   a.cell_step_ptr = d.cell_step_ptr;
   a.step_rows = d.step_rows;
   a.cell_out = d.cell_out;
-  a.dval = d.dval;
+  a.dval = d.dval ? d.dval : d.eval;
+  a.eout = twin.eval;
+  a.step_twin = d.step_twin;
+  a.zero = h->zero_row;
   a.cls_slot = cls_slot;
   a.ring = h->ring;
   a.slot_stride = (h->N + h->M) * h->Kp;
@@ -1161,23 +1206,29 @@ int one_clock(ps_mf_t *h) {
     const int64_t gu = db.by_user.nunits > 0 ? db.by_user.grid : 0;
     const int64_t gi = db.by_item.nunits > 0 ? db.by_item.grid : 0;
     us.grid_a = static_cast<int32_t>(gu);
-    DenseSweepArgs ds{};
-    ds.da = dense_args(h, db.dense_user, h->partial_u, 0, r_off, cls_slot);
-    ds.db = dense_args(h, db.dense_item, h->partial_i, r_off, 0, cls_slot);
-    ds.ncell_a = static_cast<int32_t>(db.dense_user.ncells);
+    // dense cells: the user-major pass stores the residuals that the item-major pass reads,
+    // so the two run one after the other on the handle's stream
+    const DenseArgs du = dense_args(h, db.dense_user, h->partial_u, 0, r_off, cls_slot, db.dense_item);
+    const DenseArgs di = dense_args(h, db.dense_item, h->partial_i, r_off, 0, cls_slot, db.dense_user);
     const int64_t ndense = db.dense_user.ncells + db.dense_item.ncells;
+    auto launch_dense_pair = [&]() -> hipError_t {
+      hipError_t e = hipSuccess;
+      if (db.dense_user.ncells > 0 && (e = launch_dense<false>(h->Kp, du, db.dense_user.ncells, h->stream))) return e;
+      if (db.dense_item.ncells > 0) e = launch_dense<true>(h->Kp, di, db.dense_item.ncells, h->stream);
+      return e;
+    };
     if (ncells + ndense > 0 && gu + gi > 0 && h->side_stream) {
       // dense cells and cells on the handle's stream, units on the side stream, all after
       // what precedes
       HIP_TRY(h, hipEventRecord(h->fork, h->stream));
       HIP_TRY(h, hipStreamWaitEvent(h->side_stream, h->fork, 0));
       HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, us, gu + gi, h->side_stream));
-      if (ndense > 0) HIP_TRY(h, launch_dense(h->Kp, ds, ndense, h->stream));
+      if (ndense > 0) HIP_TRY(h, launch_dense_pair());
       if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
       HIP_TRY(h, hipEventRecord(h->join, h->side_stream));
       HIP_TRY(h, hipStreamWaitEvent(h->stream, h->join, 0));
     } else {
-      if (ndense > 0) HIP_TRY(h, launch_dense(h->Kp, ds, ndense, h->stream));
+      if (ndense > 0) HIP_TRY(h, launch_dense_pair());
       if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
       if (gu + gi > 0) HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, us, gu + gi, h->stream));
     }
@@ -1374,13 +1425,16 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
     lp.cell_groups = kSweepBlock / shape_for(h->Kp).G;
     lp.heavy_min = h->heavy_min >= 0 ? h->heavy_min
                                       : std::max<int64_t>(256, 16 * h->M / lp.cell_rows);
-    // automatic: one sub-tile of hot items (at K = 128 on the 100M-rating workload one
-    // measured best among 0..4)
-    lp.hot_steps = h->hot_steps >= 0 ? h->hot_steps : 1;
   }
   if (h->dense_min > 0 && !dense_supported(h->Kp))
     return fail(h, PS_MF_EINVAL, "dense tiles need a padded rank in [16, 128], not %d", h->Kp);
   lp.dense_min = h->dense_min >= 0 ? h->dense_min : (dense_supported(h->Kp) ? kDenseAuto : 0);
+  if (h->cells) {
+    // automatic hot-item sub-tiles: none next to dense tiles, else one (on the 100M-rating
+    // K = 128 workload: 1 measured best among 0..4 without dense tiles; with them the
+    // light users' extra partial rows cost the commit more than the cells save)
+    lp.hot_steps = h->hot_steps >= 0 ? h->hot_steps : (lp.dense_min > 0 ? 0 : 1);
+  }
   std::string err;
   const int rc = psmf::build_layout(lp, user, item, value, n, h->layout, err);
   if (rc == -1) return fail(h, PS_MF_EINVAL, "%s", err.c_str());
@@ -1410,7 +1464,8 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
         (r = upload(h, &d.val, L.val)) ||
         (r = upload_units(h, d.by_user, L.by_user)) || (r = upload_units(h, d.by_item, L.by_item)) ||
         (r = upload_cells(h, d.cells_user, L.cells_user)) || (r = upload_cells(h, d.cells_item, L.cells_item)) ||
-        (r = upload_dense(h, d.dense_user, L.dense_user)) || (r = upload_dense(h, d.dense_item, L.dense_item)))
+        (r = upload_dense(h, d.dense_user, L.dense_user, true)) ||
+        (r = upload_dense(h, d.dense_item, L.dense_item, false)))
       return undo(r);
     // partial rows of units and cells, + the row the padding units write
     max_units_u = std::max<int64_t>(max_units_u, L.partial_rows_user + 1);
@@ -1441,6 +1496,7 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->loss_partial), static_cast<size_t>(h->loss_partial_len) * sizeof(double))))
     return undo(r);
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->loss_out), sizeof(double)))) return undo(r);
+  if ((r = upload(h, &h->zero_row, std::vector<float>(static_cast<size_t>(h->Kp), 0.f)))) return undo(r);
   // slot table: row c (c < s) and rows s .. 2s (periodic part), one entry per worker class
   std::vector<int32_t> table(static_cast<size_t>((2 * h->s + 1) * h->nclass));
   std::vector<int32_t> rep(static_cast<size_t>(h->nclass), -1);  // a worker of each class
@@ -1561,7 +1617,7 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
   const void *src = nullptr;
   size_t esz = 0;
   int64_t n = 0;
-  int64_t split[6] = {0, 0, 0, 0, 0, 0};
+  int64_t split[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   if (kind == PS_MF_IDX_SPLIT) {
     const psmf::BlockLayout &L = h->layout[block];
     auto unit_ratings = [](const psmf::UnitSet &u) {
@@ -1575,6 +1631,8 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     split[3] = L.dense_item.nnz;
     split[4] = L.cells_item.nnz;
     split[5] = unit_ratings(L.by_item);
+    split[6] = L.partial_rows_user;
+    split[7] = L.partial_rows_item;
   }
   switch (kind) {
     case PS_MF_IDX_OWNER: src = h->owner.data(); esz = 4; n = h->N; break;
@@ -1584,7 +1642,7 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     case PS_MF_IDX_USER_COUNT: src = h->layout[block].ucount.data(); esz = 4; n = h->N; break;
     case PS_MF_IDX_ITEM_COUNT: src = h->layout[block].icount.data(); esz = 4; n = h->M; break;
     case PS_MF_IDX_VERSION_LOG: src = h->vlog.data(); esz = 8; n = static_cast<int64_t>(h->vlog.size()); break;
-    case PS_MF_IDX_SPLIT: src = split; esz = 8; n = 6; break;
+    case PS_MF_IDX_SPLIT: src = split; esz = 8; n = 8; break;
     default: return fail(h, PS_MF_EINVAL, "unknown index kind %d", kind);
   }
   *len = n;

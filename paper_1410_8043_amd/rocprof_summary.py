@@ -29,7 +29,7 @@ import sys
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCE = os.path.join(_HERE, "csrc", "ps_mf.hip")
-SWEEP_KERNELS = ("k_cells", "k_units")  # the two concurrent kernels of one clock's sweep
+SWEEP_KERNELS = ("k_dense", "k_cells", "k_units")  # the concurrent kernels of one clock's sweep
 
 
 def kernel_source_sha256() -> str:
@@ -58,24 +58,27 @@ def stats(d: str):
     return [(short_name(n), int(c), tot / 1e3, avg / 1e3, pct) for n, c, tot, avg, pct in rows]
 
 
+def _is_sweep(name: str) -> bool:
+    return any(name.startswith(k) for k in SWEEP_KERNELS)
+
+
 def sweep_spans(d: str):
-    """Per clock: (span, [duration of each sweep kernel]) in ms, the i-th dispatch of every
-    sweep kernel taken as clock i (each clock launches each of them at most once)."""
+    """Per clock: (span, [duration of each sweep kernel]) in ms.  Every distinct sweep kernel
+    (by full name: the two dense passes are different instantiations) runs at most once per
+    clock, so its i-th dispatch is taken as clock i."""
     con = _db(d)
     rows = con.execute("select name, start, end from kernels order by start").fetchall()
-    per = {k: [] for k in SWEEP_KERNELS}
+    per = collections.OrderedDict()
     for name, start, end in rows:
         sn = short_name(name)
-        for k in SWEEP_KERNELS:
-            if sn.startswith(k):
-                per[k].append((start, end))
-    present = [k for k in SWEEP_KERNELS if per[k]]
-    if not present:
+        if _is_sweep(sn):
+            per.setdefault(sn, []).append((start, end))
+    if not per:
         return []
-    clocks = min(len(per[k]) for k in present)
+    clocks = min(len(v) for v in per.values())
     out = []
     for i in range(clocks):
-        ivs = [per[k][i] for k in present]
+        ivs = [v[i] for v in per.values()]
         out.append(((max(e for _, e in ivs) - min(s for s, _ in ivs)) / 1e6, [(e - s) / 1e6 for s, e in ivs]))
     return out
 
@@ -109,13 +112,8 @@ def _copy_value(cnt, counter: str) -> float:
 
 
 def _sweep_values(cnt, counter: str):
-    """[(kernel, [value per dispatch])] of the sweep kernels"""
-    out = []
-    for k in SWEEP_KERNELS:
-        try:
-            out.append((k, _find(cnt, k, counter)))
-        except KeyError:
-            pass
+    """[(kernel, [value per dispatch])] of the sweep kernels, one entry per distinct kernel"""
+    out = [(short_name(k), v) for (k, c), v in cnt.items() if c == counter and _is_sweep(short_name(k))]
     if not out:
         raise KeyError(f"{counter} of the sweep kernels not found")
     return out
@@ -169,7 +167,7 @@ def main(argv=None):
         spans = sweep_spans(args.dir)
         if spans:
             avg = sum(sp for sp, _ in spans) / len(spans)
-            print(f"sweep span (first start to last end of {' + '.join(SWEEP_KERNELS)} per clock): "
+            print(f"sweep span (first start to last end of the {' / '.join(SWEEP_KERNELS)} kernels of a clock): "
                   f"{len(spans)} clocks, avg {avg:.4f} ms, min {min(sp for sp, _ in spans):.4f} ms, "
                   f"max {max(sp for sp, _ in spans):.4f} ms")
     elif args.cmd == "counters":

@@ -173,7 +173,7 @@ def test_host_layout_self_check_with_hot_cells_and_custom_owner(policy, s, B):
 
 def split_of(g, b=0):
     s = g.export_index(ps_mf.IDX_SPLIT, b)
-    assert s.shape == (6,)
+    assert s.shape == (8,)
     return s
 
 
@@ -201,7 +201,7 @@ def test_host_layout_self_check_with_dense_tiles(dense_min, policy, s, B, K):
         for b in range(B):
             sp = split_of(g, b)
             nb = g.export_index(ps_mf.IDX_COL, b).size
-            assert sp[:3].sum() == nb and sp[3:].sum() == nb
+            assert sp[:3].sum() == nb and sp[3:6].sum() == nb
             assert sp[0] == sp[3] and sp[0] > 0
             if dense_min == 1 and B == 1:
                 # every tile with a rating is dense: only the repeats of a (user, item) pair
