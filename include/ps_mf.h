@@ -86,7 +86,7 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_OPT_DENSE_MIN 13 /* ratings from which a 64 x 64 tile (64 users of one worker class
                                   ranked by rating count x 64 items ranked by rating count) is
                                   swept with matrix-core products as a dense block; 0: none;
-                                  -1 (default): automatic (1229, i.e. 30% full, when the padded
+                                  -1 (default): automatic (800, i.e. 20% full, when the padded
                                   rank is in [16, 128], else none); at most 4096.  A value > 0
                                   with a padded rank outside [16, 128] makes
                                   ps_mf_load_ratings fail with PS_MF_EINVAL */

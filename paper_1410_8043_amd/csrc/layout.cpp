@@ -243,7 +243,8 @@ void build_user_cells(const LayoutParams &p, const BlockLayout &L, const std::ve
   }
   if (groups == 0) return;
   const int64_t nsub = (M + ts - 1) / ts;
-  const int64_t R = std::max<int64_t>(1, std::min<int64_t>(nsub, (p.cell_target + groups - 1) / groups));
+  const int64_t R = std::max<int64_t>(1, std::min<int64_t>(nsub / std::max(1, p.min_cell_steps),
+                                                            (p.cell_target + groups - 1) / groups));
   C.step_rows.resize(static_cast<size_t>(nsub * ts));
   for (int64_t t = 0; t < nsub * ts; ++t) C.step_rows[t] = t < M ? static_cast<int32_t>(t) : -1;
   std::vector<int64_t> ents(L.col.size());
@@ -346,7 +347,7 @@ void build_item_cells(const LayoutParams &p, const BlockLayout &L, const std::ve
   C.cell_step_ptr.push_back(0);
   for (int32_t c = 0; c < p.nclass; ++c) {
     if (nsub[c] == 0) continue;
-    const int64_t Rc = std::min<int64_t>(R, nsub[c]);
+    const int64_t Rc = std::max<int64_t>(1, std::min<int64_t>(R, nsub[c] / std::max(1, p.min_cell_steps)));
     for (int64_t g0 = 0; g0 < static_cast<int64_t>(items.size()); g0 += ng) {
       for (int64_t r = 0; r < Rc; ++r) {
         const int64_t s0 = r * nsub[c] / Rc, s1 = (r + 1) * nsub[c] / Rc;
@@ -533,7 +534,7 @@ void build_item_cells_hot(const LayoutParams &p, const BlockLayout &L, const std
     if (slots[c].empty()) continue;
     const auto &sl = slots[c];
     const int64_t ns = static_cast<int64_t>(sl.size());
-    const int64_t Rc = std::min<int64_t>(R, nsub[c]);
+    const int64_t Rc = std::max<int64_t>(1, std::min<int64_t>(R, nsub[c] / std::max(1, p.min_cell_steps)));
     for (int64_t g0 = 0; g0 < ns; g0 += ng) {
       for (int64_t r = 0; r < Rc; ++r) {
         const int64_t s0 = r * nsub[c] / Rc, s1 = (r + 1) * nsub[c] / Rc;
@@ -624,7 +625,8 @@ void build_dense(const LayoutParams &p, const BlockLayout &L, const std::vector<
         if (dense_it[irank[L.col[e]] / T] && (e == L.row_ptr[us[q]] || L.col[e - 1] != L.col[e])) in_dense[e] = 1;
     for (int32_t it : t.its) dense_it[it] = 0;
   }
-  const int64_t per_cell = std::max<int64_t>(1, (ntiles + p.dense_target - 1) / std::max(1, p.dense_target));
+  const int64_t per_cell = std::max<int64_t>(std::max(1, p.min_cell_steps),
+                                             (ntiles + p.dense_target - 1) / std::max(1, p.dense_target));
   // step index of every dense tile in each direction: tile t of utiles[u] is tile_base[u] + t
   std::vector<int64_t> tile_base(utiles.size() + 1, 0);
   for (size_t u = 0; u < utiles.size(); ++u) tile_base[u + 1] = tile_base[u] + static_cast<int64_t>(utiles[u].its.size());

@@ -142,6 +142,8 @@ struct LayoutParams {
   int32_t dense_min = 0;            // ratings from which a 64 x 64 tile goes to the MFMA cells
                                     // (0: none)
   int32_t dense_target = 1024;      // about this many dense cells per direction
+  int32_t min_cell_steps = 4;       // runs of cells and dense cells are not cut below this many
+                                    // steps (each cut costs every row of the cell a partial row)
 };
 
 // Validates the COO input (EINVAL message in err) and fills one BlockLayout per block.

@@ -55,9 +55,14 @@ static_assert(kTileFloats % 512 == 0 && kTileFloats * 4 <= 160 * 1024, "a cell s
 constexpr int kLossSegment = 512;  // ratings per lane group of the loss
 // automatic threshold of the dense (MFMA) tiles: ratings per 64 x 64 tile
 #ifndef PS_MF_DENSE_AUTO
-#define PS_MF_DENSE_AUTO 1229
+#define PS_MF_DENSE_AUTO 800
 #endif
 constexpr int kDenseAuto = PS_MF_DENSE_AUTO;
+// dense cells per direction the layout aims at (more cells: shorter runs and a shorter tail,
+// but one partial row per cell and row)
+#ifndef PS_MF_DENSE_CELLS
+#define PS_MF_DENSE_CELLS 1024
+#endif
 constexpr int kMaxKp = 512;
 constexpr int kXcds = psmf::kXcds;
 #ifndef PS_MF_ROWS_IN_FLIGHT
@@ -65,9 +70,14 @@ constexpr int kXcds = psmf::kXcds;
 #endif
 constexpr int kRowsInFlight = PS_MF_ROWS_IN_FLIGHT;  // gathered rows loaded before their use (divides 8)
 // rows in flight for E floats per lane: the 512-wide rows keep one (registers are capped
-// at 128 per lane with 16 wavefronts per CU)
+// at 128 per lane with 16 wavefronts per CU); narrow rows (E <= 8 floats per lane) keep
+// PS_MF_NARROW_ROWS_IN_FLIGHT, so that enough bytes are in flight per CU to cover the L2
+// latency
+#ifndef PS_MF_NARROW_ROWS_IN_FLIGHT
+#define PS_MF_NARROW_ROWS_IN_FLIGHT 8
+#endif
 template <int E>
-constexpr int rows_in_flight() { return E >= 32 ? 1 : kRowsInFlight; }
+constexpr int rows_in_flight() { return E >= 32 ? 1 : E >= 16 ? kRowsInFlight : PS_MF_NARROW_ROWS_IN_FLIGHT; }
 // the cells also hold the next 8 (row, value) pairs: two rows in flight from 16 floats on
 template <int E>
 constexpr int cell_rows_in_flight() { return E >= 32 ? 1 : E >= 16 ? 2 : kRowsInFlight; }
@@ -119,6 +129,63 @@ __device__ __forceinline__ void store_row_sw(float *__restrict__ row, const floa
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Data that a clock touches once -- rating streams, stationary rows, partial rows, dense
+// values and residuals -- may be loaded and stored non-temporally, so that it does not
+// evict from L2 the gathered rows that other work units reuse.  Which of the three
+// streams are non-temporal is a build choice (PS_MF_NT_LOADS: the sweeps' once-read
+// data; PS_MF_NT_STORES: partial rows and residuals; PS_MF_NT_COMMIT: the commit's
+// partial-row reads).
+#ifndef PS_MF_NT_LOADS
+#define PS_MF_NT_LOADS 0
+#endif
+#ifndef PS_MF_NT_STORES
+#define PS_MF_NT_STORES 1
+#endif
+#ifndef PS_MF_NT_COMMIT
+#define PS_MF_NT_COMMIT 1
+#endif
+template <class T>
+__device__ __forceinline__ T ld_once(const T *p) {
+  if constexpr (PS_MF_NT_LOADS != 0) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+template <class T>
+__device__ __forceinline__ void st_once(T *p, T v) {
+  if constexpr (PS_MF_NT_STORES != 0) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+template <class T>
+__device__ __forceinline__ T ld_partial(const T *p) {
+  if constexpr (PS_MF_NT_COMMIT != 0) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
+template <int G, int E>
+__device__ __forceinline__ void load_row_once(float (&d)[E], const float *__restrict__ row, int g) {
+#pragma unroll
+  for (int q = 0; q < E / 4; ++q) {
+    const f32x4 t = ld_once(reinterpret_cast<const f32x4 *>(row + 4 * (q * G + g)));
+    d[4 * q] = t[0]; d[4 * q + 1] = t[1]; d[4 * q + 2] = t[2]; d[4 * q + 3] = t[3];
+  }
+}
+
+template <int G, int E>
+__device__ __forceinline__ void store_row_once(float *__restrict__ row, const float (&d)[E], int g, int rot = 0) {
+#pragma unroll
+  for (int q = 0; q < E / 4; ++q)
+    st_once(reinterpret_cast<f32x4 *>(row + 4 * ((q ^ rot) * G + g)), f32x4{d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]});
+}
+
+template <int G, int E>
+__device__ __forceinline__ void load_row_sw_once(float (&d)[E], const float *__restrict__ row, int g, int rot) {
+#pragma unroll
+  for (int q = 0; q < E / 4; ++q) {
+    const f32x4 t = ld_once(reinterpret_cast<const f32x4 *>(row + 4 * ((q ^ rot) * G + g)));
+    d[4 * q] = t[0]; d[4 * q + 1] = t[1]; d[4 * q + 2] = t[2]; d[4 * q + 3] = t[3];
+  }
+}
 
 // Sum over the G lanes of an aligned lane group with DPP moves inside a 16-lane row:
 // quad_perm [1,0,3,2] (xor 1), quad_perm [2,3,0,1] (xor 2), row_half_mirror (the other
@@ -206,19 +273,19 @@ __device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g)
   const i32x4 *__restrict__ yi = reinterpret_cast<const i32x4 *>(a.y + beg);
   const f32x4 *__restrict__ vr = reinterpret_cast<const f32x4 *>(a.val + beg);
   float x[E], acc[E];
-  load_row<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
+  load_row_once<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
   // the next 8 (row, value) pairs are loaded while the current 8 are swept
   i32x4 ni0 = {0, 0, 0, 0}, ni1 = {0, 0, 0, 0};
   f32x4 nv0 = {0.f, 0.f, 0.f, 0.f}, nv1 = {0.f, 0.f, 0.f, 0.f};
-  if (n > 0) { ni0 = yi[0]; ni1 = yi[1]; nv0 = vr[0]; nv1 = vr[1]; }
+  if (n > 0) { ni0 = ld_once(yi); ni1 = ld_once(yi + 1); nv0 = ld_once(vr); nv1 = ld_once(vr + 1); }
   for (int t0 = 0; t0 < n; t0 += 8) {
     const i32x4 i0 = ni0, i1 = ni1;
     const f32x4 v0 = nv0, v1 = nv1;
     if (t0 + 8 < n) {
-      ni0 = yi[t0 / 4 + 2]; ni1 = yi[t0 / 4 + 3];
-      nv0 = vr[t0 / 4 + 2]; nv1 = vr[t0 / 4 + 3];
+      ni0 = ld_once(yi + t0 / 4 + 2); ni1 = ld_once(yi + t0 / 4 + 3);
+      nv0 = ld_once(vr + t0 / 4 + 2); nv1 = ld_once(vr + t0 / 4 + 3);
     }
     const int idx[8] = {i0[0], i0[1], i0[2], i0[3], i1[0], i1[1], i1[2], i1[3]};
     const float val[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
@@ -239,7 +306,7 @@ __device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g)
       }
     }
   }
-  store_row<G, E>(a.partial + static_cast<int64_t>(a.unit_out[unit]) * Kp, acc, g);
+  store_row_once<G, E>(a.partial + static_cast<int64_t>(a.unit_out[unit]) * Kp, acc, g);
 }
 
 struct CellArgs {
@@ -276,7 +343,7 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
   float x[E], acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) { x[e] = 0.f; acc[e] = 0.f; }
-  if (xr >= 0) load_row_sw<G, E>(x, V + c.x_off + static_cast<int64_t>(xr) * Kp, g, rot);
+  if (xr >= 0) load_row_sw_once<G, E>(x, V + c.x_off + static_cast<int64_t>(xr) * Kp, g, rot);
   const int32_t k0 = c.cell_step_ptr[cell], k1 = c.cell_step_ptr[cell + 1];
   for (int32_t k = k0; k < k1; ++k) {
     const int32_t *rows = c.step_rows + static_cast<int64_t>(c.cell_steps[k]) * c.ts;
@@ -291,33 +358,33 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
     const float *__restrict__ lv = c.lv + beg;
     // the first 8 (row, value) pairs are loaded before the barrier, then always the next 8
     // while the current 8 are swept
-    uint4 ni = make_uint4(0u, 0u, 0u, 0u);
+    u32x4 ni = {0u, 0u, 0u, 0u};
     f32x4 nv0 = {0.f, 0.f, 0.f, 0.f}, nv1 = {0.f, 0.f, 0.f, 0.f};
     if (n > 0) {
-      ni = *reinterpret_cast<const uint4 *>(li);
-      nv0 = *reinterpret_cast<const f32x4 *>(lv);
-      nv1 = *reinterpret_cast<const f32x4 *>(lv + 4);
+      ni = ld_once(reinterpret_cast<const u32x4 *>(li));
+      nv0 = ld_once(reinterpret_cast<const f32x4 *>(lv));
+      nv1 = ld_once(reinterpret_cast<const f32x4 *>(lv + 4));
     }
     __syncthreads();
     for (int t0 = 0; t0 < n; t0 += 8) {
       if constexpr (E >= 32) {  // 512-wide rows: no registers to spare for the prefetch
         if (t0 > 0) {
-          ni = *reinterpret_cast<const uint4 *>(li + t0);
-          nv0 = *reinterpret_cast<const f32x4 *>(lv + t0);
-          nv1 = *reinterpret_cast<const f32x4 *>(lv + t0 + 4);
+          ni = ld_once(reinterpret_cast<const u32x4 *>(li + t0));
+          nv0 = ld_once(reinterpret_cast<const f32x4 *>(lv + t0));
+          nv1 = ld_once(reinterpret_cast<const f32x4 *>(lv + t0 + 4));
         }
       }
-      const uint4 i8 = ni;  // 8 x uint16
+      const u32x4 i8 = ni;  // 8 x uint16
       const f32x4 v0 = nv0, v1 = nv1;
       if (E < 32 && t0 + 8 < n) {
-        ni = *reinterpret_cast<const uint4 *>(li + t0 + 8);
-        nv0 = *reinterpret_cast<const f32x4 *>(lv + t0 + 8);
-        nv1 = *reinterpret_cast<const f32x4 *>(lv + t0 + 12);
+        ni = ld_once(reinterpret_cast<const u32x4 *>(li + t0 + 8));
+        nv0 = ld_once(reinterpret_cast<const f32x4 *>(lv + t0 + 8));
+        nv1 = ld_once(reinterpret_cast<const f32x4 *>(lv + t0 + 12));
       }
-      const int idx[8] = {static_cast<int>(i8.x & 0xffff), static_cast<int>(i8.x >> 16),
-                          static_cast<int>(i8.y & 0xffff), static_cast<int>(i8.y >> 16),
-                          static_cast<int>(i8.z & 0xffff), static_cast<int>(i8.z >> 16),
-                          static_cast<int>(i8.w & 0xffff), static_cast<int>(i8.w >> 16)};
+      const int idx[8] = {static_cast<int>(i8[0] & 0xffff), static_cast<int>(i8[0] >> 16),
+                          static_cast<int>(i8[1] & 0xffff), static_cast<int>(i8[1] >> 16),
+                          static_cast<int>(i8[2] & 0xffff), static_cast<int>(i8[2] >> 16),
+                          static_cast<int>(i8[3] & 0xffff), static_cast<int>(i8[3] >> 16)};
       const float val[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
 #pragma unroll
       for (int q = 0; q < 8; q += RF) {
@@ -346,7 +413,7 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
     }
   }
   const int32_t out = c.cell_out[cell * NG + grp];
-  if (out >= 0) store_row_sw<G, E>(c.partial + static_cast<int64_t>(out) * Kp, acc, g, rot);
+  if (out >= 0) store_row_once<G, E>(c.partial + static_cast<int64_t>(out) * Kp, acc, g, rot);
 }
 
 // The LDS-staged cells of both sweep directions in one launch (one 1024-thread workgroup
@@ -490,13 +557,13 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
   const int64_t k0 = a.cell_step_ptr[cell], k1 = a.cell_step_ptr[cell + 1];
   if (k0 < k1) dense_stage<Kp>(a, Y, k0, lds0);
   // stationary rows in the B-operand layout of GEMM 1: xb[q] = X[16w + i][16q + 4g .. +3]
-  float4 xb[NQ];
+  f32x4 xb[NQ];
   if constexpr (!FromE) {
     const int32_t xr = a.cell_x[cell * kDenseRowsDev + 16 * w + i];
 #pragma unroll
     for (int q = 0; q < NQ; ++q)
-      xb[q] = xr >= 0 ? *reinterpret_cast<const float4 *>(X + static_cast<int64_t>(xr) * Kp + 16 * q + 4 * g)
-                      : make_float4(0.f, 0.f, 0.f, 0.f);
+      xb[q] = xr >= 0 ? ld_once(reinterpret_cast<const f32x4 *>(X + static_cast<int64_t>(xr) * Kp + 16 * q + 4 * g))
+                      : f32x4{0.f, 0.f, 0.f, 0.f};
   }
   f32x4 acc[NQ];
 #pragma unroll
@@ -505,7 +572,7 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
   f32x4 dcur[4], dnext[4];
   if (k0 < k1) {
 #pragma unroll
-    for (int yb = 0; yb < 4; ++yb) dcur[yb] = dv[(k0 * 16 + w * 4 + yb) * 64 + lane];
+    for (int yb = 0; yb < 4; ++yb) dcur[yb] = ld_once(dv + (k0 * 16 + w * 4 + yb) * 64 + lane);
   }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -515,7 +582,7 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
     if (more) {  // the next step's rows (into the other buffer) and values
       dense_stage<Kp>(a, Y, k + 1, nextbuf);
 #pragma unroll
-      for (int yb = 0; yb < 4; ++yb) dnext[yb] = dv[((k + 1) * 16 + w * 4 + yb) * 64 + lane];
+      for (int yb = 0; yb < 4; ++yb) dnext[yb] = ld_once(dv + ((k + 1) * 16 + w * 4 + yb) * 64 + lane);
     }
     const char *Tb = reinterpret_cast<const char *>(T4);
 #pragma unroll
@@ -540,14 +607,14 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
             a0n = T4[dense_lds_chunk<Kp>(16 * y2 + i, 4 * (q + 1) + g)];
             a1n = T4[dense_lds_chunk<Kp>(16 * y2 + 16 + i, 4 * (q + 1) + g)];
           }
-          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, xb[q].x, s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, xb[q].x, s1, 0, 0, 0);
-          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, xb[q].y, s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.y, xb[q].y, s1, 0, 0, 0);
-          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.z, xb[q].z, s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, xb[q].z, s1, 0, 0, 0);
-          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, xb[q].w, s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, xb[q].w, s1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, xb[q][0], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, xb[q][0], s1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, xb[q][1], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.y, xb[q][1], s1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.z, xb[q][2], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, xb[q][2], s1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, xb[q][3], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, xb[q][3], s1, 0, 0, 0);
         }
         // residuals where rated (D is NaN elsewhere): the A operands of GEMM 2; stored for
         // the item-major pass at its fragment position of (x = item, y = user)
@@ -559,7 +626,7 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             e[h][v] = d[v] == d[v] ? d[v] - sv4[v] : 0.f;
-            eo[psmf::dense_frag_index(16 * (y2 + h) + 4 * g + v, 16 * w + i)] = e[h][v];
+            st_once(eo + psmf::dense_frag_index(16 * (y2 + h) + 4 * g + v, 16 * w + i), e[h][v]);
           }
         }
       }
@@ -601,8 +668,8 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
     for (int cg = 0; cg < NQ / C4; ++cg) {
       const int f = 16 * C4 * cg + C4 * i;
       if constexpr (C4 == 4) {
-        *reinterpret_cast<float4 *>(dst + f) =
-            make_float4(acc[4 * cg][v], acc[4 * cg + 1][v], acc[4 * cg + 2][v], acc[4 * cg + 3][v]);
+        st_once(reinterpret_cast<f32x4 *>(dst + f),
+                f32x4{acc[4 * cg][v], acc[4 * cg + 1][v], acc[4 * cg + 2][v], acc[4 * cg + 3][v]});
       } else if constexpr (C4 == 2) {
         *reinterpret_cast<float2 *>(dst + f) = make_float2(acc[2 * cg][v], acc[2 * cg + 1][v]);
       } else {
@@ -703,13 +770,13 @@ __device__ __forceinline__ void finalize_users(const FinalArgs &a, int64_t idx) 
     if (a.slot_n != a.slot_c) ring4[a.slot_n * ss4 + idx] = ring4[a.slot_c * ss4 + idx];
     return;
   }
-  const float4 *part4 = reinterpret_cast<const float4 *>(a.partial);
+  const f32x4 *part4 = reinterpret_cast<const f32x4 *>(a.partial);
   const int64_t k4 = idx - i * q4;
   float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll 4
   for (int64_t p = a.user_pp[i]; p < a.user_pp[i + 1]; ++p) {
-    const float4 t = part4[p * q4 + k4];
-    d.x += t.x; d.y += t.y; d.z += t.z; d.w += t.w;
+    const f32x4 t = ld_partial(part4 + p * q4 + k4);
+    d.x += t[0]; d.y += t[1]; d.z += t[2]; d.w += t[3];
   }
   const float4 lc = ring4[a.slot_c * ss4 + idx];
   const float4 lv = ring4[a.cls_slot[a.ucls[i]] * ss4 + idx];
@@ -752,11 +819,11 @@ __device__ __forceinline__ void commit_item(const CommitArgs &a, int64_t j, floa
     return;
   }
   float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
-  const float4 *part4 = reinterpret_cast<const float4 *>(a.partial);
+  const f32x4 *part4 = reinterpret_cast<const f32x4 *>(a.partial);
 #pragma unroll 4
   for (int64_t p = a.item_pp[j] + lane; p < a.item_pp[j + 1]; p += lanes) {
-    const float4 t = part4[p * q4 + k4];
-    d.x += t.x; d.y += t.y; d.z += t.z; d.w += t.w;
+    const f32x4 t = ld_partial(part4 + p * q4 + k4);
+    d.x += t[0]; d.y += t[1]; d.z += t[2]; d.w += t[3];
   }
   red[threadIdx.x] = d;
   __syncthreads();
@@ -812,6 +879,37 @@ int padded_k(int K) {
   int Kp = 8;
   while (Kp < K) Kp *= 2;
   return Kp;
+}
+
+// lane-group shape of the work units: PS_MF_UNIT_WIDE = 1 spreads a row over 16 lanes
+// (fewer registers and memory instructions per row, one more DPP step per dot product)
+#ifndef PS_MF_UNIT_WIDE
+#define PS_MF_UNIT_WIDE 0
+#endif
+Shape unit_shape_for(int Kp) {
+  Shape sh = shape_for(Kp);
+  if (PS_MF_UNIT_WIDE && sh.G < 16 && Kp / 16 >= 4) sh = {16, Kp / 16};
+  return sh;
+}
+
+template <template <int, int> class F, class... Args>
+hipError_t dispatch_units(int Kp, Args &&...args) {
+  if (PS_MF_UNIT_WIDE) {
+    switch (Kp) {
+      case 64: return F<16, 4>::run(args...);
+      case 128: return F<16, 8>::run(args...);
+      default: break;
+    }
+  }
+  switch (Kp) {
+    case 8: return F<2, 4>::run(args...);
+    case 16: return F<4, 4>::run(args...);
+    case 32: return F<8, 4>::run(args...);
+    case 64: return F<8, 8>::run(args...);
+    case 128: return F<8, 16>::run(args...);
+    case 256: return F<16, 16>::run(args...);
+    default: return F<16, 32>::run(args...);
+  }
 }
 
 template <template <int, int> class F, class... Args>
@@ -1016,7 +1114,7 @@ int upload_units(ps_mf_t *h, DeviceUnits &d, const psmf::UnitSet &u) {
   d.nunits = u.nreal;
   int64_t most = 0;
   for (int x = 0; x < kXcds; ++x) most = std::max<int64_t>(most, u.xcd_off[x + 1] - u.xcd_off[x]);
-  const int groups = kBlock / shape_for(h->Kp).G;
+  const int groups = kBlock / unit_shape_for(h->Kp).G;
   d.grid = kXcds * ((most + groups - 1) / groups);
   return PS_MF_OK;
 }
@@ -1222,7 +1320,7 @@ int one_clock(ps_mf_t *h) {
       // what precedes
       HIP_TRY(h, hipEventRecord(h->fork, h->stream));
       HIP_TRY(h, hipStreamWaitEvent(h->side_stream, h->fork, 0));
-      HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, us, gu + gi, h->side_stream));
+      HIP_TRY(h, dispatch_units<LaunchUnits>(h->Kp, us, gu + gi, h->side_stream));
       if (ndense > 0) HIP_TRY(h, launch_dense_pair());
       if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
       HIP_TRY(h, hipEventRecord(h->join, h->side_stream));
@@ -1230,7 +1328,7 @@ int one_clock(ps_mf_t *h) {
     } else {
       if (ndense > 0) HIP_TRY(h, launch_dense_pair());
       if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
-      if (gu + gi > 0) HIP_TRY(h, dispatch<LaunchUnits>(h->Kp, us, gu + gi, h->stream));
+      if (gu + gi > 0) HIP_TRY(h, dispatch_units<LaunchUnits>(h->Kp, us, gu + gi, h->stream));
     }
   }
   if ((rc = record_end(h, PS_MF_KERNEL_SWEEP, ev))) return rc;
@@ -1429,6 +1527,7 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   if (h->dense_min > 0 && !dense_supported(h->Kp))
     return fail(h, PS_MF_EINVAL, "dense tiles need a padded rank in [16, 128], not %d", h->Kp);
   lp.dense_min = h->dense_min >= 0 ? h->dense_min : (dense_supported(h->Kp) ? kDenseAuto : 0);
+  lp.dense_target = PS_MF_DENSE_CELLS;
   if (h->cells) {
     // automatic hot-item sub-tiles: none next to dense tiles, else one (on the 100M-rating
     // K = 128 workload: 1 measured best among 0..4 without dense tiles; with them the
