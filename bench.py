@@ -146,6 +146,10 @@ def main():
     dt = time.perf_counter() - t0
     print(f"[bench] {args.steps} clocks in {dt * 1e3:.2f} ms", file=sys.stderr, flush=True)
     loss = g.loss()
+    # staleness profile of the clocks run (Fig. 1 left): share of parameter reads per clock
+    # differential -(d+1)
+    stale = g.export_index(ps_mf.IDX_STALENESS)
+    profile = {str(-(d + 1)): round(float(x) / max(1, int(stale.sum())), 4) for d, x in enumerate(stale)}
 
     value = nnz_clock * args.steps / dt
     K = spec.K
@@ -192,7 +196,8 @@ def main():
                                f"P={spec.P}, s={s}, policy={args.policy}, B={spec.B}, eta={spec.eta}, "
                                f"lambda={spec.lam}",
                    "global_batch": int(nnz_clock), "parallelism": "1 GPU, P logical workers",
-                   "loss_after": loss, "dense_cells_units": [int(x) for x in split[:3]], **extra},
+                   "loss_after": loss, "dense_cells_units": [int(x) for x in split[:3]],
+                   "staleness_profile": profile, **extra},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -112,6 +112,13 @@ typedef struct ps_mf ps_mf_t;
                                    sums to the block's rating count); then the partial rows
                                    (Kp floats each) the user-major and the item-major sweep
                                    write per clock for the commit to sum */
+#define PS_MF_IDX_STALENESS 8   /* int64 [s+1]: staleness profile of the clocks run since the last
+                                   ps_mf_set_factors (Section 2.2, Fig. 1 left): entry d counts
+                                   the parameter reads that saw version c - d at clock c, i.e.
+                                   whose clock differential (parameter age - local clock) is
+                                   -(d+1); every rating a worker processes reads its user row
+                                   and its item row at the worker's view.  BSP (s = 0) puts
+                                   every read at d = 0 (differential -1) */
 
 /* kernel ids (ps_mf_kernel_time) */
 #define PS_MF_KERNEL_SWEEP 0  /* residual, dL segment-sum and dR accumulation of one clock */

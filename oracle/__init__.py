@@ -18,9 +18,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libps_mf_oracle.so")
 
-SSP_LAZY, SSP_WORST, ESSP = 0, 1, 2
+SSP_LAZY, SSP_WORST, ESSP, SSP_ROW, ESSP_ROW = 0, 1, 2, 3, 4
 ROWMEAN, SUM = 0, 1
-X_OWNER, X_ROW_PTR, X_COL, X_PERM, X_USER_COUNT, X_ITEM_COUNT, X_VERSION_LOG = range(7)
+X_OWNER, X_ROW_PTR, X_COL, X_PERM, X_USER_COUNT, X_ITEM_COUNT, X_VERSION_LOG, X_STALENESS, X_ROW_VERSIONS = range(9)
 
 _lib = None
 

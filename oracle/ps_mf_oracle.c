@@ -23,6 +23,13 @@
  *   - the view is a whole committed version v = max(0, c - d(p,c)), d chosen by a
  *     deterministic policy: SSP_LAZY d = (c + p mod (s+1)) mod (s+1); SSP_WORST d = s;
  *     ESSP d = min(s, 1);
+ *   - or, under the per-row policies, every row has its own version in the cache of the
+ *     worker's client (Section 4: each PS process caches rows, a row served only while
+ *     fresh enough, read as version >= c - s).  SSP_ROW (SSPTable: refreshed only when
+ *     too stale): a row read at clock c that is not cached or cached at a version < c - s
+ *     is fetched at version c, else the cached version is read.  ESSP_ROW (ESSPTable: the
+ *     server pushes every registered row once all clients ticked; the push lands one
+ *     clock later): the first read fetches version c, later reads see c - min(s, 1);
  *   - step normalisation: SUM uses the summed per-rating steps; ROWMEAN divides each
  *     row's summed contribution by that row's rating count in the clock's minibatch;
  *   - the lambda term enters once per rating, at the view (Section 3.1 update rule);
@@ -47,10 +54,10 @@
 #define OR_ENOMEM -2
 #define OR_ESTATE -4
 
-enum { OR_LAZY = 0, OR_WORST = 1, OR_ESSP = 2 };
+enum { OR_LAZY = 0, OR_WORST = 1, OR_ESSP = 2, OR_SSP_ROW = 3, OR_ESSP_ROW = 4 };
 enum { OR_ROWMEAN = 0, OR_SUM = 1 };
 enum { OR_X_OWNER = 0, OR_X_ROW_PTR = 1, OR_X_COL = 2, OR_X_PERM = 3, OR_X_USER_COUNT = 4, OR_X_ITEM_COUNT = 5,
-       OR_X_VERSION_LOG = 6 };
+       OR_X_VERSION_LOG = 6, OR_X_STALENESS = 7, OR_X_ROW_VERSIONS = 8 };
 
 typedef struct {
   int64_t N, M;
@@ -74,7 +81,19 @@ typedef struct {
   /* version log, clock-major: entry c*P + p = v(p,c) */
   int64_t *vlog;
   int64_t vlog_len, vlog_cap;
+  /* staleness profile (Fig. 1 left): stale[d] = parameter reads at clock c that saw
+     version c - d, i.e. whose clock differential (parameter age - local clock) is -(d+1);
+     every rating a worker processes reads its user row and its item row */
+  int64_t *stale; /* s+1 */
   double *dL, *dR;
+  /* per-row caches (Section 4, the client cache of a PS process), used by the per-row
+     policies: worker p runs on client p mod C, C = min(P, s+1); each client caches the rows
+     its workers read with the version it holds (-1: not cached).  A user row is read only
+     by its owner's client. */
+  int64_t C;
+  int64_t *ucache; /* N */
+  int64_t *icache; /* C*M */
+  uint8_t *iread;  /* C*M scratch: item rows a client reads this clock */
 } oracle_t;
 
 /* SplitMix64 (Steele, Lea & Flood 2014): one step of the sequential generator from `state`. */
@@ -113,8 +132,19 @@ static int64_t view_version(const oracle_t *o, int64_t p, int64_t c) {
   return v < 0 ? 0 : v;
 }
 
+static int per_row(const oracle_t *o) { return o->policy == OR_SSP_ROW || o->policy == OR_ESSP_ROW; }
+
+/* the version a client's cache holds for a row it reads at clock c (cached: its current
+   version, -1 if none) */
+static int64_t row_read(const oracle_t *o, int64_t cached, int64_t c) {
+  if (o->policy == OR_SSP_ROW) return (cached < 0 || cached < c - o->s) ? c : cached;
+  /* ESSP_ROW */
+  if (cached < 0) return c;
+  return c - (o->s < 1 ? o->s : 1);
+}
+
 int oracle_view_version(const oracle_t *o, int64_t p, int64_t c, int64_t *v) {
-  if (!o || p < 0 || p >= o->P || c < 0) return OR_EINVAL;
+  if (!o || p < 0 || p >= o->P || c < 0 || per_row(o)) return OR_EINVAL;
   *v = view_version(o, p, c);
   return OR_OK;
 }
@@ -123,7 +153,8 @@ void oracle_destroy(oracle_t *o) {
   if (!o) return;
   free(o->owner); free(o->user); free(o->item); free(o->val);
   free(o->bstart); free(o->order); free(o->ucount); free(o->icount);
-  free(o->Lring); free(o->Rring); free(o->vlog); free(o->dL); free(o->dR);
+  free(o->Lring); free(o->Rring); free(o->vlog); free(o->dL); free(o->dR); free(o->stale);
+  free(o->ucache); free(o->icache); free(o->iread);
   free(o);
 }
 
@@ -132,14 +163,21 @@ int oracle_create(int64_t N, int64_t M, int32_t K, int32_t P, int32_t s, double 
   if (!out) return OR_EINVAL;
   *out = NULL;
   if (N <= 0 || M <= 0 || K <= 0 || P <= 0 || s < 0 || B < 1 || N > 0x7fffffff || M > 0x7fffffff) return OR_EINVAL;
-  if (policy < OR_LAZY || policy > OR_ESSP || (step != OR_ROWMEAN && step != OR_SUM)) return OR_EINVAL;
+  if (policy < OR_LAZY || policy > OR_ESSP_ROW || (step != OR_ROWMEAN && step != OR_SUM)) return OR_EINVAL;
   if (!isfinite(eta) || !isfinite(lambda)) return OR_EINVAL;
   oracle_t *o = (oracle_t *)calloc(1, sizeof(oracle_t));
   if (!o) return OR_ENOMEM;
   o->N = N; o->M = M; o->K = K; o->P = P; o->s = s; o->eta = eta; o->lambda = lambda;
   o->policy = policy; o->step = step; o->B = B; o->seed = seed;
   o->owner = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
-  if (!o->owner) { oracle_destroy(o); return OR_ENOMEM; }
+  o->stale = (int64_t *)calloc((size_t)s + 1, sizeof(int64_t));
+  o->C = P < (int64_t)s + 1 ? P : (int64_t)s + 1;
+  o->ucache = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+  o->icache = (int64_t *)malloc(sizeof(int64_t) * (size_t)(o->C * M));
+  o->iread = (uint8_t *)calloc((size_t)(o->C * M), 1);
+  if (!o->owner || !o->stale || !o->ucache || !o->icache || !o->iread) { oracle_destroy(o); return OR_ENOMEM; }
+  for (int64_t i = 0; i < N; ++i) o->ucache[i] = -1;
+  for (int64_t x = 0; x < o->C * M; ++x) o->icache[x] = -1;
   for (int64_t i = 0; i < N; ++i) {
     int32_t p = owner ? owner[i] : (int32_t)(i % P);
     if (p < 0 || p >= P) { oracle_destroy(o); return OR_EINVAL; }
@@ -218,6 +256,9 @@ int oracle_set_factors(oracle_t *o, const float *L0, const float *R0) {
   memcpy(o->Rring, R0, sizeof(float) * nr);
   o->clock = 0;
   o->vlog_len = 0;
+  memset(o->stale, 0, sizeof(int64_t) * ((size_t)o->s + 1));
+  for (int64_t i = 0; i < o->N; ++i) o->ucache[i] = -1;
+  for (int64_t x = 0; x < o->C * o->M; ++x) o->icache[x] = -1;
   o->has_factors = 1;
   return OR_OK;
 }
@@ -231,12 +272,34 @@ static int one_clock(oracle_t *o) {
   const int32_t b = (int32_t)(c % o->B);
   memset(o->dL, 0, sizeof(double) * (size_t)(o->N * K));
   memset(o->dR, 0, sizeof(double) * (size_t)(o->M * K));
+  if (per_row(o)) {
+    /* the rows each client reads this clock take the version its cache serves */
+    for (int64_t i = 0; i < o->N; ++i)
+      if (o->ucount[(int64_t)b * o->N + i] > 0) o->ucache[i] = row_read(o, o->ucache[i], c);
+    for (int64_t q = o->bstart[b]; q < o->bstart[b + 1]; ++q) {
+      const int64_t t = o->order[q];
+      o->iread[(int64_t)(o->owner[o->user[t]] % o->C) * o->M + o->item[t]] = 1;
+    }
+    for (int64_t x = 0; x < o->C * o->M; ++x)
+      if (o->iread[x]) {
+        o->icache[x] = row_read(o, o->icache[x], c);
+        o->iread[x] = 0;
+      }
+  }
   for (int64_t q = o->bstart[b]; q < o->bstart[b + 1]; ++q) {
     const int64_t t = o->order[q];
     const int64_t i = o->user[t], j = o->item[t];
-    const int64_t v = view_version(o, o->owner[i], c);
-    const float *Li = L_of(o, v) + i * K;
-    const float *Rj = R_of(o, v) + j * K;
+    int64_t vL, vR;
+    if (per_row(o)) {
+      vL = o->ucache[i];
+      vR = o->icache[(int64_t)(o->owner[i] % o->C) * o->M + j];
+    } else {
+      vL = vR = view_version(o, o->owner[i], c);
+    }
+    const float *Li = L_of(o, vL) + i * K;
+    const float *Rj = R_of(o, vR) + j * K;
+    o->stale[c - vL] += 1; /* this rating reads row L_i at version vL ... */
+    o->stale[c - vR] += 1; /* ... and row R_j at version vR */
     double dot = 0.0;
     for (int64_t k = 0; k < K; ++k) dot += (double)Li[k] * (double)Rj[k];
     const double e = (double)o->val[t] - dot;
@@ -248,7 +311,8 @@ static int one_clock(oracle_t *o) {
       dRj[k] += o->eta * si * (e * (double)Li[k] - o->lambda * (double)Rj[k]);
     }
   }
-  /* log the versions read at this clock */
+  /* log the versions read at this clock (one per worker: table-level policies only) */
+  if (per_row(o)) goto commit;
   if (o->vlog_len + o->P > o->vlog_cap) {
     int64_t cap = o->vlog_cap ? o->vlog_cap * 2 : 64 * (int64_t)o->P;
     while (cap < o->vlog_len + o->P) cap *= 2;
@@ -257,6 +321,7 @@ static int one_clock(oracle_t *o) {
     o->vlog = nv; o->vlog_cap = cap;
   }
   for (int64_t p = 0; p < o->P; ++p) o->vlog[o->vlog_len++] = view_version(o, p, c);
+commit:;
   /* commit: V_{c+1} = fp32(V_c + Delta); the Deltas are complete, so the slot that held
      version c-s may now be overwritten */
   const float *Lc = L_of(o, c), *Rc = R_of(o, c);
@@ -321,7 +386,8 @@ int oracle_rows_from_v0(const oracle_t *o, int32_t nclocks, int64_t nu, const in
   if (!o || nclocks < 0 || nu < 0 || ni < 0) return OR_EINVAL;
   if (!o->loaded || !o->has_factors || o->clock != 0) return OR_ESTATE;
   const int64_t K = o->K;
-  for (int64_t c = 0; c < nclocks; ++c)
+  if (per_row(o) && nclocks > 1) return OR_EINVAL; /* only clock 0 surely reads version 0 */
+  for (int64_t c = 0; c < nclocks && !per_row(o); ++c)
     for (int64_t p = 0; p < o->P; ++p)
       if (view_version(o, p, c) != 0) return OR_EINVAL;
   const float *L0 = L_of(o, 0), *R0 = R_of(o, 0);
@@ -380,7 +446,7 @@ bad:
  */
 int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t cap, int64_t *len) {
   if (!o || !len) return OR_EINVAL;
-  if (kind != OR_X_OWNER && kind != OR_X_VERSION_LOG) {
+  if (kind != OR_X_OWNER && kind != OR_X_VERSION_LOG && kind != OR_X_STALENESS && kind != OR_X_ROW_VERSIONS) {
     if (!o->loaded) return OR_ESTATE;
     if (b < 0 || b >= o->B) return OR_EINVAL;
   }
@@ -392,6 +458,8 @@ int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t
     case OR_X_USER_COUNT: n = o->N; break;
     case OR_X_ITEM_COUNT: n = o->M; break;
     case OR_X_VERSION_LOG: n = o->vlog_len; break;
+    case OR_X_STALENESS: n = (int64_t)o->s + 1; break;
+    case OR_X_ROW_VERSIONS: n = o->N + o->C * o->M; break;
     default: return OR_EINVAL;
   }
   *len = n;
@@ -412,6 +480,11 @@ int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t
     case OR_X_USER_COUNT: memcpy(buf, o->ucount + (int64_t)b * o->N, sizeof(int32_t) * (size_t)n); break;
     case OR_X_ITEM_COUNT: memcpy(buf, o->icount + (int64_t)b * o->M, sizeof(int32_t) * (size_t)n); break;
     case OR_X_VERSION_LOG: if (n) memcpy(buf, o->vlog, sizeof(int64_t) * (size_t)n); break;
+    case OR_X_STALENESS: memcpy(buf, o->stale, sizeof(int64_t) * (size_t)n); break;
+    case OR_X_ROW_VERSIONS:
+      memcpy(buf, o->ucache, sizeof(int64_t) * (size_t)o->N);
+      memcpy((int64_t *)buf + o->N, o->icache, sizeof(int64_t) * (size_t)(o->C * o->M));
+      break;
   }
   return OR_OK;
 }

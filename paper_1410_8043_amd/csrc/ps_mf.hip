@@ -1026,6 +1026,7 @@ struct ps_mf {
   bool loaded = false, has_factors = false;
   int64_t clock = 0;
   std::vector<int64_t> vlog;
+  std::vector<int64_t> worker_ratings;  // [B * P]: ratings of each worker in each block
   std::vector<psmf::BlockLayout> layout;
   int32_t nclass = 1;
   std::vector<int32_t> cls_of_worker;
@@ -1538,6 +1539,10 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   const int rc = psmf::build_layout(lp, user, item, value, n, h->layout, err);
   if (rc == -1) return fail(h, PS_MF_EINVAL, "%s", err.c_str());
   if (rc) return fail(h, PS_MF_ENOMEM, "%s", err.c_str());
+  h->worker_ratings.assign(static_cast<size_t>(h->B) * h->P, 0);
+  for (int b = 0; b < h->B; ++b)
+    for (int64_t i = 0; i < h->N; ++i)
+      h->worker_ratings[static_cast<size_t>(b) * h->P + h->owner[i]] += h->layout[b].ucount[i];
   if (h->host_only) {
     for (int b = 0; b < h->B; ++b)
       if (psmf::check_layout(lp, h->layout[b], err))
@@ -1705,7 +1710,8 @@ int ps_mf_get_clock(ps_mf_t *h, int64_t *clock) {
 
 int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64_t cap, int64_t *len) {
   if (!h || !len) return PS_MF_EINVAL;
-  if (kind != PS_MF_IDX_OWNER && kind != PS_MF_IDX_VERSION_LOG) {
+  if (kind == PS_MF_IDX_STALENESS && !h->loaded) return fail(h, PS_MF_ESTATE, "no ratings loaded");
+  if (kind != PS_MF_IDX_OWNER && kind != PS_MF_IDX_VERSION_LOG && kind != PS_MF_IDX_STALENESS) {
     if (!h->loaded) return fail(h, PS_MF_ESTATE, "no ratings loaded");
     if (block < 0 || block >= h->B) return fail(h, PS_MF_EINVAL, "block %d out of range", block);
   }
@@ -1733,7 +1739,18 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     split[6] = L.partial_rows_user;
     split[7] = L.partial_rows_item;
   }
+  std::vector<int64_t> stale;
+  if (kind == PS_MF_IDX_STALENESS) {
+    // the version log holds v(p, c) for every clock run; worker p reads two rows per rating
+    stale.assign(static_cast<size_t>(h->s) + 1, 0);
+    const int64_t clocks = static_cast<int64_t>(h->vlog.size()) / h->P;
+    for (int64_t c = 0; c < clocks; ++c)
+      for (int64_t p = 0; p < h->P; ++p)
+        stale[static_cast<size_t>(c - h->vlog[c * h->P + p])] +=
+            2 * h->worker_ratings[static_cast<size_t>(c % h->B) * h->P + p];
+  }
   switch (kind) {
+    case PS_MF_IDX_STALENESS: src = stale.data(); esz = 8; n = h->s + 1; break;
     case PS_MF_IDX_OWNER: src = h->owner.data(); esz = 4; n = h->N; break;
     case PS_MF_IDX_ROW_PTR: src = h->layout[block].row_ptr.data(); esz = 8; n = h->N + 1; break;
     case PS_MF_IDX_COL: src = h->layout[block].col.data(); esz = 4; n = h->layout[block].nnz; break;

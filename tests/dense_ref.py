@@ -82,3 +82,40 @@ def loss_dense(user, item, val, L, R):
     R = R.astype(np.float64)
     e = val.astype(np.float64) - np.einsum("tk,tk->t", L[user], R[item])
     return float(np.dot(e, e))
+
+
+def run_dense_rowviews(user, item, val, L0, R0, *, N, M, K, P, C, eta, lam, views, step=0, B=1, seed=0,
+                       owner=None):
+    """The same matrix algebra with a version per row: views[c] = (vL, vR) with vL[i] the
+    version of user row i read at clock c (by its owner's client) and vR[m][j] the version
+    of item row j that client m reads (entries of rows not read are ignored).  Users of
+    client m form E_m = W_m * (D - Lv Rv_m^T) with Lv, Rv_m gathered from those versions."""
+    owner = np.arange(N) % P if owner is None else np.asarray(owner)
+    client = owner % C
+    blocks = np.array([block_of(i, j, seed, B) for i, j in zip(user, item)]) if B > 1 else None
+    mats = [dense_mats(user, item, val, N, M, blocks, b) for b in range(B)]
+    hist = [(np.asarray(L0, np.float32).reshape(N, K).copy(), np.asarray(R0, np.float32).reshape(M, K).copy())]
+    for c, (vL, vR) in enumerate(views):
+        W, D = mats[c % B]
+        nu, ni = W.sum(1), W.sum(0)
+        Lv = np.stack([hist[max(int(vL[i]), 0)][0][i] for i in range(N)]).astype(np.float64)
+        dL = np.zeros((N, K))
+        dR = np.zeros((M, K))
+        for m in range(C):
+            rows = client == m
+            if not rows.any():
+                continue
+            Rv = np.stack([hist[max(int(vR[m][j]), 0)][1][j] for j in range(M)]).astype(np.float64)
+            Wm = W * rows[:, None]
+            E = Wm * (D - Lv @ Rv.T)
+            gL = -(E @ Rv) + lam * Wm.sum(1)[:, None] * Lv
+            gR = -(E.T @ Lv) + lam * Wm.sum(0)[:, None] * Rv
+            dL[rows] -= gL[rows]
+            dR -= gR
+        if step == 0:
+            dL /= np.where(nu > 0, nu, 1)[:, None]
+            dR /= np.where(ni > 0, ni, 1)[:, None]
+        Lc, Rc = hist[c]
+        hist.append(((Lc.astype(np.float64) + eta * dL).astype(np.float32),
+                     (Rc.astype(np.float64) + eta * dR).astype(np.float32)))
+    return hist

@@ -58,6 +58,7 @@ def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, c
         assert err <= FACTOR_TOL, err
         assert abs(loss - loss_o) <= LOSS_RTOL * max(loss_o, 1e-30), (loss, loss_o)
         assert np.array_equal(g.export_index(gpu_mod().IDX_VERSION_LOG), o.export(oracle.X_VERSION_LOG))
+        assert np.array_equal(g.export_index(gpu_mod().IDX_STALENESS), o.export(oracle.X_STALENESS))
         if check_versions:
             for v in range(max(0, clocks - s), clocks + 1):
                 Lv, Rv = g.get_version(v)

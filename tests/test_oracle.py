@@ -320,3 +320,176 @@ def test_argument_errors():
         o.load(np.array([2]), np.array([0]), np.array([1.0]))
     with pytest.raises(oracle.OracleError):
         o.clock(1)
+
+
+# ---------------------------------------------------------------- staleness profile (Fig. 1 left)
+def staleness_run(policy, s, P, clocks, B=1, seed=0, owner=None, N=40, M=30, nnz=600):
+    rng = np.random.default_rng(seed)
+    user, item, val, L0, R0 = rand_problem(rng, N, M, nnz, 4)
+    o = oracle.Oracle(N, M, 4, P, s, 0.01, 0.05, policy, oracle.ROWMEAN, B, 7, owner)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(clocks)
+    hist = o.export(oracle.X_STALENESS)
+    o.close()
+    return hist, user, item
+
+
+@pytest.mark.parametrize("policy", [oracle.SSP_LAZY, oracle.SSP_WORST, oracle.ESSP])
+def test_staleness_bsp_is_always_minus_one(policy):
+    # Fig. 1 caption: on a BSP system the clock differential is always -1 (s = 0)
+    hist, user, _ = staleness_run(policy, 0, 3, 5)
+    assert hist.tolist() == [2 * user.size * 5]
+
+
+@pytest.mark.parametrize("s", [1, 3, 7])
+def test_staleness_essp_is_one_clock_regardless_of_s(s):
+    # Section 4: reads observe staleness 1 regardless of s; clock 0 can only read version 0
+    hist, user, _ = staleness_run(oracle.ESSP, s, 4, 9)
+    want = np.zeros(s + 1, np.int64)
+    want[0] = 2 * user.size
+    want[1] = 2 * user.size * 8
+    assert np.array_equal(hist, want)
+
+
+@pytest.mark.parametrize("s", [1, 2, 4])
+def test_staleness_worst_is_the_guaranteed_prewindow(s):
+    # Section 3.2: the view holds every update of clocks <= c-s-1 and none of the window;
+    # before clock s the view is version 0
+    clocks = 2 * s + 3
+    hist, user, _ = staleness_run(oracle.SSP_WORST, s, 5, clocks)
+    want = np.zeros(s + 1, np.int64)
+    for c in range(clocks):
+        want[min(c, s)] += 2 * user.size
+    assert np.array_equal(hist, want)
+
+
+@pytest.mark.parametrize("s", [1, 3])
+def test_staleness_lazy_is_uniform_in_steady_state(s):
+    # Section 2.2: under SSP the distribution of clock differentials is (nearly) uniform.
+    # P = s+1 workers with one user each and equal shards: every full period of s+1 clocks
+    # after the first s adds the same count to every delay 0..s
+    P = s + 1
+    N, M = P, 50
+    user = np.repeat(np.arange(P, dtype=np.int32), M)
+    item = np.tile(np.arange(M, dtype=np.int32), P)
+    val = np.ones(user.size, np.float32)
+    rng = np.random.default_rng(1)
+    L0 = (0.1 * rng.standard_normal((N, 4))).astype(np.float32)
+    R0 = (0.1 * rng.standard_normal((M, 4))).astype(np.float32)
+
+    def hist_after(clocks):
+        o = oracle.Oracle(N, M, 4, P, s, 0.01, 0.05, oracle.SSP_LAZY, oracle.ROWMEAN, 1, 0)
+        o.load(user, item, val)
+        o.set_factors(L0, R0)
+        o.clock(clocks)
+        h = o.export(oracle.X_STALENESS)
+        o.close()
+        return h
+
+    # each of the P workers reads its 2M rows once at every delay per period
+    a, b = hist_after(s), hist_after(s + 3 * (s + 1))
+    assert np.array_equal(b - a, np.full(s + 1, 3 * P * 2 * M, np.int64))
+
+
+@pytest.mark.parametrize("policy", [oracle.SSP_LAZY, oracle.SSP_WORST, oracle.ESSP])
+@pytest.mark.parametrize("B", [1, 3])
+def test_staleness_counts_two_reads_per_processed_rating(policy, B):
+    # every rating of the clock's block is processed once and reads two rows
+    N, M, clocks = 40, 30, 7
+    hist, user, item = staleness_run(policy, 3, 4, clocks, B=B)
+    blocks = np.array([block_of(int(u), int(i), 7, B) for u, i in zip(user, item)])
+    processed = sum(int((blocks == c % B).sum()) for c in range(clocks))
+    assert hist.sum() == 2 * processed
+
+
+# ---------------------------------------------------------------- per-row caches (Section 4)
+@pytest.mark.parametrize("s", [1, 2, 3])
+@pytest.mark.parametrize("P", [1, 3])
+def test_ssp_row_with_every_row_read_each_clock_is_phase_zero_lazy(s, P):
+    # B = 1: every client reads all of its rows at every clock, so every cached row is
+    # fetched at clock 0 and refreshed together at s+1, 2(s+1), ...: the view of every read
+    # is c - (c mod (s+1)), i.e. SSP_LAZY with every worker in phase 0 (all users on worker 0)
+    rng = np.random.default_rng(10 * s + P)
+    N, M, K = 30, 20, 3
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 300, K, dup=5)
+    got = oracle.run(user, item, val, L0, R0, N=N, M=M, K=K, P=P, s=s, eta=0.05, lam=0.05, clocks=3 * s + 4,
+                     policy=oracle.SSP_ROW)
+    want = oracle.run(user, item, val, L0, R0, N=N, M=M, K=K, P=P, s=s, eta=0.05, lam=0.05, clocks=3 * s + 4,
+                      policy=oracle.SSP_LAZY, owner=np.zeros(N, np.int32))
+    assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+
+
+@pytest.mark.parametrize("s", [1, 3])
+def test_essp_row_with_every_row_read_each_clock_is_essp(s):
+    # B = 1: every row is first read at clock 0 (version 0), then pushed versions c - 1
+    rng = np.random.default_rng(s)
+    N, M, K = 30, 20, 3
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 300, K)
+    got = oracle.run(user, item, val, L0, R0, N=N, M=M, K=K, P=4, s=s, eta=0.05, lam=0.05, clocks=7,
+                     policy=oracle.ESSP_ROW)
+    want = oracle.run(user, item, val, L0, R0, N=N, M=M, K=K, P=4, s=s, eta=0.05, lam=0.05, clocks=7,
+                      policy=oracle.ESSP)
+    assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+
+
+# W4: users 0, 1 on workers (and clients) 0, 1; ratings (0,0)=3 in block 0, (1,0)=1 and
+# (0,1)=2 in block 1 (B = 2, seed 6), s = 1.  Versions read at each clock, by hand from
+# the freshness rules: [user rows], [client 0's item rows], [client 1's item rows]
+W4_VIEWS = {
+    oracle.SSP_ROW: [([0, -1], [0, -1], [-1, -1]), ([0, 1], [-1, 1], [1, -1]),
+                     ([2, -1], [2, -1], [-1, -1]), ([2, 3], [-1, 3], [3, -1])],
+    oracle.ESSP_ROW: [([0, -1], [0, -1], [-1, -1]), ([0, 1], [-1, 1], [1, -1]),
+                      ([1, -1], [1, -1], [-1, -1]), ([2, 2], [-1, 2], [2, -1])],
+}
+W4_CACHE_AFTER_4 = {oracle.SSP_ROW: [2, 3, 2, 3, 3, -1], oracle.ESSP_ROW: [2, 2, 1, 2, 2, -1]}
+W4_STALENESS = {oracle.SSP_ROW: [10, 2], oracle.ESSP_ROW: [5, 7]}
+
+
+@pytest.mark.parametrize("policy", [oracle.SSP_ROW, oracle.ESSP_ROW])
+def test_per_row_hand_example_w4(policy):
+    from dense_ref import run_dense_rowviews
+    assert [block_of(0, 0, 6, 2), block_of(1, 0, 6, 2), block_of(0, 1, 6, 2)] == [0, 1, 1]
+    user = np.array([0, 1, 0], np.int32)
+    item = np.array([0, 0, 1], np.int32)
+    val = np.array([3.0, 1.0, 2.0], np.float32)
+    L0 = np.array([[0.5, -0.25], [0.25, 0.5]], np.float32)
+    R0 = np.array([[1.0, 0.5], [0.75, -0.5]], np.float32)
+    o = oracle.Oracle(2, 2, 2, 2, 1, 0.1, 0.05, policy, oracle.ROWMEAN, 2, 6)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(4)
+    assert o.export(oracle.X_ROW_VERSIONS).tolist() == W4_CACHE_AFTER_4[policy]
+    assert o.export(oracle.X_STALENESS).tolist() == W4_STALENESS[policy]
+    assert o.export(oracle.X_VERSION_LOG).size == 0
+    views = [(vL, [v0, v1]) for vL, v0, v1 in W4_VIEWS[policy]]
+    hist = run_dense_rowviews(user, item, val, L0, R0, N=2, M=2, K=2, P=2, C=2, eta=0.1, lam=0.05, views=views,
+                              B=2, seed=6)
+    L, R = o.get_factors()
+    np.testing.assert_allclose(L, hist[4][0], rtol=0, atol=1e-6)
+    np.testing.assert_allclose(R, hist[4][1], rtol=0, atol=1e-6)
+    o.close()
+
+
+@pytest.mark.parametrize("policy", [oracle.SSP_ROW, oracle.ESSP_ROW])
+@pytest.mark.parametrize("s", [1, 3])
+def test_per_row_staleness_stays_in_the_window(policy, s):
+    # every read sees a version in [c - s, c]; ESSP_ROW reads are fresh (first reads) or
+    # one clock old; every processed rating reads two rows
+    N, M, clocks, B = 60, 40, 12, 4
+    rng = np.random.default_rng(s)
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 900, 3)
+    o = oracle.Oracle(N, M, 3, 5, s, 0.05, 0.05, policy, oracle.ROWMEAN, B, 9)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(clocks)
+    hist = o.export(oracle.X_STALENESS)
+    cache = o.export(oracle.X_ROW_VERSIONS)
+    o.close()
+    blocks = np.array([block_of(int(u), int(i), 9, B) for u, i in zip(user, item)])
+    assert hist.sum() == 2 * sum(int((blocks == c % B).sum()) for c in range(clocks))
+    if policy == oracle.ESSP_ROW:
+        assert hist[2:].sum() == 0 and hist[0] > 0 and hist[1] > 0
+    else:
+        assert hist[1:].sum() > 0  # intermittent reads keep rows cached across clocks
+    assert cache.min() >= -1 and cache.max() <= clocks - 1
