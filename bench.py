@@ -27,7 +27,7 @@ if ROOT not in sys.path:
 
 PEAK_FP32_VECTOR_TFLOPS = 157.3   # MI355X published fp32 vector peak (packed FMA)
 PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
-POLICIES = {"lazy": 0, "worst": 1, "essp": 2}
+POLICIES = {"lazy": 0, "worst": 1, "essp": 2, "ssp_row": 3, "essp_row": 4}
 
 
 def parse():

@@ -61,7 +61,8 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_EINTERNAL (-5) /* the library's own consistency check of its layout failed (a bug) */
 
 /* option keys (ps_mf_set_option); all must be set before ps_mf_load_ratings */
-#define PS_MF_OPT_POLICY 1    /* PS_MF_SSP_LAZY (default), PS_MF_SSP_WORST, PS_MF_ESSP */
+#define PS_MF_OPT_POLICY 1    /* PS_MF_SSP_LAZY (default), PS_MF_SSP_WORST, PS_MF_ESSP, PS_MF_SSP_ROW,
+                                 PS_MF_ESSP_ROW */
 #define PS_MF_OPT_STEP 2      /* PS_MF_STEP_ROWMEAN (default), PS_MF_STEP_SUM */
 #define PS_MF_OPT_MB_BLOCKS 3 /* B >= 1 minibatch blocks (default 1: full shard per clock) */
 #define PS_MF_OPT_MB_SEED 4   /* 64-bit seed of the block hash (default 0) */
@@ -91,9 +92,25 @@ typedef struct ps_mf ps_mf_t;
                                   with a padded rank outside [16, 128] makes
                                   ps_mf_load_ratings fail with PS_MF_EINVAL */
 
+/* Views (Section 3.2 SSP condition; Section 4 ESSPTable).  The table-level policies give
+   worker p at clock c one whole version v = max(0, c - d):
+     PS_MF_SSP_LAZY  d = (c + p mod (s+1)) mod (s+1) (a lazily refreshed cache, staggered);
+     PS_MF_SSP_WORST d = s (exactly the guaranteed pre-window);
+     PS_MF_ESSP      d = min(s, 1) (pushes land one clock later).
+   The per-row policies keep a version per row in the cache of each client: worker p runs
+   on client p mod min(P, s+1), a user row is read by its owner's client, an item row by
+   every client with a rating of it in the clock's minibatch:
+     PS_MF_SSP_ROW   a row that is not cached, or cached at a version < c - s, is fetched at
+                     version c; otherwise the cached version is read (SSPTable);
+     PS_MF_ESSP_ROW  the first read fetches version c, later reads see the server's push of
+                     version c - min(s, 1) (ESSPTable).
+   Under the per-row policies the version log stays empty; PS_MF_IDX_STALENESS and
+   PS_MF_IDX_ROW_VERSIONS report the reads. */
 #define PS_MF_SSP_LAZY 0
 #define PS_MF_SSP_WORST 1
 #define PS_MF_ESSP 2
+#define PS_MF_SSP_ROW 3
+#define PS_MF_ESSP_ROW 4
 
 #define PS_MF_STEP_ROWMEAN 0
 #define PS_MF_STEP_SUM 1
@@ -119,6 +136,11 @@ typedef struct ps_mf ps_mf_t;
                                    -(d+1); every rating a worker processes reads its user row
                                    and its item row at the worker's view.  BSP (s = 0) puts
                                    every read at d = 0 (differential -1) */
+#define PS_MF_IDX_ROW_VERSIONS 9 /* int64 [users + C*items], C = min(P, s+1): under a per-row
+                                   policy, the version each client's cache holds after the
+                                   last clock: user rows (read by their owner's client), then
+                                   client 0's item rows, client 1's, ...; -1 = never read.
+                                   Other policies: length 0 */
 
 /* kernel ids (ps_mf_kernel_time) */
 #define PS_MF_KERNEL_SWEEP 0  /* residual, dL segment-sum and dR accumulation of one clock */

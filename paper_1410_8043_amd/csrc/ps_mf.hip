@@ -223,6 +223,10 @@ struct UnitArgs {
   int64_t x_off, y_off;     // offsets of the stationary and the gathered table in a slot
   int64_t y_bytes;          // bytes of the gathered table (< 2^32)
   float *partial;           // [units, Kp]
+  // per-row policies: the ring slot of every stationary / gathered row (null: the class
+  // slot), tables of rows_per_class entries per worker class (0: one entry per row)
+  const int32_t *rs_x, *rs_y;
+  int64_t rs_x_cls, rs_y_cls;
 };
 
 // The unit processed by lane group `grp` of workgroup `block` (counted within its sweep;
@@ -259,21 +263,29 @@ __device__ __forceinline__ void load_row_rsrc(float (&d)[E], __amdgpu_buffer_rsr
 // (row, value) pairs are read 8 at a time with one 32-byte load per lane group (a unit
 // starts at a multiple of 8 entries and is padded to one); kRowsInFlight gathered rows
 // are loaded before they are used.
-template <int G, int E>
+template <int G, int E, bool PerRow>
 __device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g) {
   constexpr int Kp = G * E;
   constexpr int RF = rows_in_flight<E>();
-  // every unit of a wavefront reads the same ring slot (the layout pads class changes to
-  // whole wavefronts), so the slot and the buffer resource are wave-uniform
-  const int sv = __builtin_amdgcn_readfirstlane(a.cls_slot[a.unit_cls[unit]]);
+  // every unit of a wavefront reads the same class (the layout pads class changes to whole
+  // wavefronts), so the class slot and the buffer resource are wave-uniform; under the
+  // per-row policies each row has its own slot instead and the rows are read through
+  // 64-bit addresses
+  const int cls = __builtin_amdgcn_readfirstlane(a.unit_cls[unit]);
+  const int sv = PerRow ? 0 : __builtin_amdgcn_readfirstlane(a.cls_slot[cls]);
   const float *__restrict__ V = a.ring + sv * a.slot_stride;
   const __amdgpu_buffer_rsrc_t ys = table_rsrc(V + a.y_off, a.y_bytes);
+  const int32_t *__restrict__ rs_y = PerRow ? a.rs_y + cls * a.rs_y_cls : nullptr;
   const int64_t beg = a.unit_beg[unit];
   const int n = a.unit_len[unit];
   const i32x4 *__restrict__ yi = reinterpret_cast<const i32x4 *>(a.y + beg);
   const f32x4 *__restrict__ vr = reinterpret_cast<const f32x4 *>(a.val + beg);
   float x[E], acc[E];
-  load_row_once<G, E>(x, V + a.x_off + static_cast<int64_t>(a.unit_x[unit]) * Kp, g);
+  {
+    const int32_t xr = a.unit_x[unit];
+    const int64_t xs = PerRow ? a.rs_x[cls * a.rs_x_cls + xr] : sv;
+    load_row_once<G, E>(x, a.ring + xs * a.slot_stride + a.x_off + static_cast<int64_t>(xr) * Kp, g);
+  }
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
   // the next 8 (row, value) pairs are loaded while the current 8 are swept
@@ -294,8 +306,15 @@ __device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g)
       if (t0 + q >= n) break;  // only padding left
       float y[RF][E];
 #pragma unroll
-      for (int w = 0; w < RF; ++w)
-        load_row_rsrc<G, E>(y[w], ys, static_cast<uint32_t>(idx[q + w]) * (Kp * 4u), g);
+      for (int w = 0; w < RF; ++w) {
+        if constexpr (PerRow) {
+          const int32_t r = idx[q + w];
+          load_row<G, E>(y[w], a.ring + static_cast<int64_t>(rs_y[r]) * a.slot_stride + a.y_off +
+                                   static_cast<int64_t>(r) * Kp, g);
+        } else {
+          load_row_rsrc<G, E>(y[w], ys, static_cast<uint32_t>(idx[q + w]) * (Kp * 4u), g);
+        }
+      }
 #pragma unroll
       for (int w = 0; w < RF; ++w) {
         // padding entries (row 0, value 0, past the unit's n ratings) contribute nothing
@@ -319,6 +338,8 @@ struct CellArgs {
   int64_t slot_stride, x_off, y_off;
   int32_t ts;
   float *partial;
+  const int32_t *rs_x, *rs_y;  // per-row policies (see UnitArgs)
+  int64_t rs_x_cls, rs_y_cls;
 };
 
 // One cell per workgroup: lane group q keeps the stationary row x_q in registers; for each
@@ -333,7 +354,9 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
   constexpr int Q4 = Kp / 4;  // float4 per row
   const int g = threadIdx.x & (G - 1);
   const int grp = threadIdx.x / G;
-  const int sv = c.cls_slot[c.cell_cls[cell]];  // one class per cell: uniform
+  const int cls = c.cell_cls[cell];  // one class per cell: uniform
+  const bool per_row = c.rs_x != nullptr;
+  const int sv = per_row ? 0 : c.cls_slot[cls];
   const float *__restrict__ V = c.ring + sv * c.slot_stride;
   const float4 *__restrict__ Y4 = reinterpret_cast<const float4 *>(V + c.y_off);
   const int32_t xr = c.cell_x[cell * NG + grp];
@@ -343,14 +366,21 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
   float x[E], acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) { x[e] = 0.f; acc[e] = 0.f; }
-  if (xr >= 0) load_row_sw_once<G, E>(x, V + c.x_off + static_cast<int64_t>(xr) * Kp, g, rot);
+  if (xr >= 0) {
+    const int64_t xs = per_row ? c.rs_x[cls * c.rs_x_cls + xr] : sv;
+    load_row_sw_once<G, E>(x, c.ring + xs * c.slot_stride + c.x_off + static_cast<int64_t>(xr) * Kp, g, rot);
+  }
   const int32_t k0 = c.cell_step_ptr[cell], k1 = c.cell_step_ptr[cell + 1];
   for (int32_t k = k0; k < k1; ++k) {
     const int32_t *rows = c.step_rows + static_cast<int64_t>(c.cell_steps[k]) * c.ts;
     __syncthreads();  // the previous sub-tile is no longer read
     for (int idx = threadIdx.x; idx < c.ts * Q4; idx += kSweepBlock) {
       const int32_t r = rows[idx / Q4];
-      tile[idx] = r >= 0 ? Y4[static_cast<int64_t>(r) * Q4 + idx % Q4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 *src = Y4;
+      if (per_row && r >= 0)
+        src = reinterpret_cast<const float4 *>(c.ring + static_cast<int64_t>(c.rs_y[cls * c.rs_y_cls + r]) * c.slot_stride +
+                                               c.y_off);
+      tile[idx] = r >= 0 ? src[static_cast<int64_t>(r) * Q4 + idx % Q4] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     const int32_t beg = c.run_beg[static_cast<int64_t>(k) * NG + grp];
     const int n = c.run_len[static_cast<int64_t>(k) * NG + grp];
@@ -440,14 +470,14 @@ struct UnitSweepArgs {
   int32_t grid_a;
 };
 
-template <int G, int E>
+template <int G, int E, bool PerRow>
 __global__ __launch_bounds__(kBlock) void k_units(UnitSweepArgs s) {
   const int b = static_cast<int>(blockIdx.x);
   const bool first = b < s.grid_a;
   const UnitArgs &a = first ? s.ua : s.ub;
   const int64_t unit = unit_of(a, first ? b : b - s.grid_a, threadIdx.x / G, kBlock / G);
   if (unit < 0) return;  // whole groups leave together
-  run_unit<G, E>(a, unit, threadIdx.x & (G - 1));
+  run_unit<G, E, PerRow>(a, unit, threadIdx.x & (G - 1));
 }
 
 // ------------------------------------------------------------------ dense (MFMA) cells
@@ -485,6 +515,8 @@ struct DenseArgs {
   const float *ring;
   int64_t slot_stride, x_off, y_off;
   float *partial;
+  const int32_t *rs_x, *rs_y;  // per-row policies (see UnitArgs)
+  int64_t rs_x_cls, rs_y_cls;
 };
 
 // float4 chunk h of staged row y in LDS: chunks are XOR-swizzled by the row so that the
@@ -522,7 +554,7 @@ typedef __attribute__((address_space(3))) char lds_char;
 // ragged tile) read a zero row.  Completion is waited for (vmcnt) before the barrier that
 // hands the buffer to the readers.
 template <int Kp>
-__device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__restrict__ Y, int64_t k,
+__device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__restrict__ Y, int cls, int64_t k,
                                             float4 *lds_buf) {
   constexpr int H = Kp / 4;
   constexpr int SW = H < 16 ? H : 16;
@@ -533,7 +565,9 @@ __device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__r
     const int p = kDenseThreads * m + 64 * w + lane;
     const int y = p / H, h = (p % H) ^ (y & (SW - 1));
     const int32_t r = rows[y];
-    const float *src = (r >= 0 ? Y + static_cast<int64_t>(r) * Kp : a.zero) + 4 * h;
+    const float *base = Y;
+    if (a.rs_y && r >= 0) base = a.ring + static_cast<int64_t>(a.rs_y[cls * a.rs_y_cls + r]) * a.slot_stride + a.y_off;
+    const float *src = (r >= 0 ? base + static_cast<int64_t>(r) * Kp : a.zero) + 4 * h;
     lds_char *dst = (lds_char *)(lds_buf) + 16 * (kDenseThreads * m + 64 * w);  // generic -> LDS address space
     __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
   }
@@ -550,19 +584,22 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
   typedef typename VecOf<C4>::T VecT;
   const int lane = static_cast<int>(threadIdx.x) & 63, w = static_cast<int>(threadIdx.x) >> 6;
   const int i = lane & 15, g = lane >> 4;
-  const int sv = a.cls_slot[a.cell_cls[cell]];  // one class per cell: uniform
+  const int cls = a.cell_cls[cell];  // one class per cell: uniform
+  const int sv = a.rs_x ? 0 : a.cls_slot[cls];
   const float *__restrict__ V = a.ring + sv * a.slot_stride;
   const float *__restrict__ X = V + a.x_off;
   const float *__restrict__ Y = V + a.y_off;
   const int64_t k0 = a.cell_step_ptr[cell], k1 = a.cell_step_ptr[cell + 1];
-  if (k0 < k1) dense_stage<Kp>(a, Y, k0, lds0);
+  if (k0 < k1) dense_stage<Kp>(a, Y, cls, k0, lds0);
   // stationary rows in the B-operand layout of GEMM 1: xb[q] = X[16w + i][16q + 4g .. +3]
   f32x4 xb[NQ];
   if constexpr (!FromE) {
     const int32_t xr = a.cell_x[cell * kDenseRowsDev + 16 * w + i];
+    const float *Xr = X;
+    if (a.rs_x && xr >= 0) Xr = a.ring + static_cast<int64_t>(a.rs_x[cls * a.rs_x_cls + xr]) * a.slot_stride + a.x_off;
 #pragma unroll
     for (int q = 0; q < NQ; ++q)
-      xb[q] = xr >= 0 ? ld_once(reinterpret_cast<const f32x4 *>(X + static_cast<int64_t>(xr) * Kp + 16 * q + 4 * g))
+      xb[q] = xr >= 0 ? ld_once(reinterpret_cast<const f32x4 *>(Xr + static_cast<int64_t>(xr) * Kp + 16 * q + 4 * g))
                       : f32x4{0.f, 0.f, 0.f, 0.f};
   }
   f32x4 acc[NQ];
@@ -580,7 +617,7 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
   auto step = [&](int64_t k, const float4 *T4, float4 *nextbuf) {
     const bool more = k + 1 < k1;
     if (more) {  // the next step's rows (into the other buffer) and values
-      dense_stage<Kp>(a, Y, k + 1, nextbuf);
+      dense_stage<Kp>(a, Y, cls, k + 1, nextbuf);
 #pragma unroll
       for (int yb = 0; yb < 4; ++yb) dnext[yb] = ld_once(dv + ((k + 1) * 16 + w * 4 + yb) * 64 + lane);
     }
@@ -753,6 +790,7 @@ struct FinalArgs {
   const int64_t *user_pp;  // [users + 1]
   float eta, lambda;
   int32_t rowmean;
+  const int32_t *rs_u;     // per-row policies: ring slot of each user row's view (null: class slot)
 };
 
 // L^{c+1}_i = L^c_i + scale_i (sum of i's partial rows - n_i lambda L^v_i): the lambda term
@@ -779,7 +817,7 @@ __device__ __forceinline__ void finalize_users(const FinalArgs &a, int64_t idx) 
     d.x += t[0]; d.y += t[1]; d.z += t[2]; d.w += t[3];
   }
   const float4 lc = ring4[a.slot_c * ss4 + idx];
-  const float4 lv = ring4[a.cls_slot[a.ucls[i]] * ss4 + idx];
+  const float4 lv = ring4[(a.rs_u ? a.rs_u[i] : a.cls_slot[a.ucls[i]]) * ss4 + idx];
   const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
   const float nl = static_cast<float>(n) * a.lambda;
   ring4[a.slot_n * ss4 + idx] = make_float4(lc.x + sc * (d.x - nl * lv.x), lc.y + sc * (d.y - nl * lv.y),
@@ -800,6 +838,7 @@ struct CommitArgs {
   const int64_t *item_pp;     // [items + 1]
   float eta, lambda;
   int32_t rowmean;
+  const int32_t *rs_i;        // per-row policies: [nclass * items] ring slot of each class's view of an item row
 };
 
 // R^{c+1}_j = R^c_j + scale_j (sum of j's partial rows - lambda sum_class n_j^(class) R^{v(class)}_j).
@@ -838,13 +877,66 @@ __device__ __forceinline__ void commit_item(const CommitArgs &a, int64_t j, floa
     const int cnt = a.icount_cls[j * a.nclass + q];
     if (cnt) {
       const float c = static_cast<float>(cnt);
-      const float4 r = R4[a.cls_slot[q] * ss4 + idx];
+      const float4 r = R4[(a.rs_i ? a.rs_i[q * a.items + j] : a.cls_slot[q]) * ss4 + idx];
       lam = make_float4(fmaf(c, r.x, lam.x), fmaf(c, r.y, lam.y), fmaf(c, r.z, lam.z), fmaf(c, r.w, lam.w));
     }
   }
   const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
   R4[a.slot_n * ss4 + idx] = make_float4(rc.x + sc * (d.x - a.lambda * lam.x), rc.y + sc * (d.y - a.lambda * lam.y),
                                          rc.z + sc * (d.z - a.lambda * lam.z), rc.w + sc * (d.w - a.lambda * lam.w));
+}
+
+// ------------------------------------------------------------------ per-row views
+// Per-row policies (Section 4: each client caches rows; a row is served only while its
+// version is >= c - s): one thread per cached row, the user rows (read by their owner's
+// client when the user has a rating in the block) and the (client, item) rows (read when a
+// worker of the client has a rating of the item in the block).  A row read at clock c
+// takes the version the cache serves -- SSP_ROW: fetched at c when not cached or older
+// than c - s, else kept; ESSP_ROW: fetched at c on the first read, then the push of
+// version c - min(s, 1) -- and its slot in the ring.  Each read row adds its reads (one per
+// rating) to the staleness profile at delay c - v.
+constexpr int kMaxStaleBins = 1025;  // s <= 1024
+struct RowViewArgs {
+  int32_t *ver_u, *slot_u;          // [users]
+  int32_t *ver_i, *slot_i;          // [nclass * items], client-major
+  const int32_t *ucount;            // [users] ratings in the block
+  const int32_t *icount_cls;        // [items * nclass] ratings in the block per client
+  int64_t users, items, clock;
+  int32_t nclass, s, essp;
+  unsigned long long *stale;        // [s + 1]
+};
+
+__global__ __launch_bounds__(kBlock) void k_row_views(RowViewArgs a) {
+  __shared__ unsigned long long hist[kMaxStaleBins];
+  for (int t = static_cast<int>(threadIdx.x); t <= a.s; t += kBlock) hist[t] = 0ull;
+  __syncthreads();
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (idx < a.users + static_cast<int64_t>(a.nclass) * a.items) {
+    int32_t *ver, *slot;
+    int64_t reads;
+    if (idx < a.users) {
+      ver = a.ver_u + idx;
+      slot = a.slot_u + idx;
+      reads = a.ucount[idx];
+    } else {
+      const int64_t x = idx - a.users, m = x / a.items, j = x - m * a.items;
+      ver = a.ver_i + x;
+      slot = a.slot_i + x;
+      reads = a.icount_cls[j * a.nclass + m];
+    }
+    if (reads > 0) {
+      const int64_t old = *ver, c = a.clock;
+      int64_t v;
+      if (a.essp) v = old < 0 ? c : c - (a.s < 1 ? a.s : 1);
+      else v = (old < 0 || old < c - a.s) ? c : old;
+      *ver = static_cast<int32_t>(v);
+      *slot = static_cast<int32_t>(v % (a.s + 1));
+      atomicAdd(&hist[c - v], static_cast<unsigned long long>(reads));
+    }
+  }
+  __syncthreads();
+  for (int t = static_cast<int>(threadIdx.x); t <= a.s; t += kBlock)
+    if (hist[t]) atomicAdd(a.stale + t, hist[t]);
 }
 
 // Version c+1 of both factors in one launch: workgroups [0, grid_users) finalize L (one
@@ -935,7 +1027,8 @@ struct LaunchCells {
 template <int G, int E>
 struct LaunchUnits {
   static hipError_t run(const UnitSweepArgs &a, int64_t grid, hipStream_t st) {
-    hipLaunchKernelGGL((k_units<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a);
+    if (a.ua.rs_x) hipLaunchKernelGGL((k_units<G, E, true>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a);
+    else hipLaunchKernelGGL((k_units<G, E, false>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a);
     return hipGetLastError();
   }
 };
@@ -1043,6 +1136,10 @@ struct ps_mf {
   float *ring = nullptr;
   float *partial_u = nullptr, *partial_i = nullptr;
   float *zero_row = nullptr;  // Kp zeros (staging source of empty dense rows)
+  // per-row policies: cached version and ring slot of every user row and (client, item)
+  // row, and the staleness profile of the clocks run
+  int32_t *ver_u = nullptr, *slot_u = nullptr, *ver_i = nullptr, *slot_i = nullptr;
+  unsigned long long *stale = nullptr;
   int32_t *ucls = nullptr;
   int32_t *slot_table = nullptr;  // [(2s+1) * nclass]
   double *loss_partial = nullptr;
@@ -1215,6 +1312,23 @@ UnitArgs unit_args(const ps_mf_t *h, const DeviceUnits &d, float *partial, int64
   return a;
 }
 
+bool per_row_policy(const ps_mf_t *h) { return h->policy == PS_MF_SSP_ROW || h->policy == PS_MF_ESSP_ROW; }
+
+// per-row slot tables of one sweep direction: the user-major direction keeps users (one
+// entry each) and gathers items (one entry per client and item); item-major the reverse
+template <class A>
+void set_row_slots(const ps_mf_t *h, A &a, bool user_major) {
+  if (!per_row_policy(h)) {
+    a.rs_x = a.rs_y = nullptr;
+    a.rs_x_cls = a.rs_y_cls = 0;
+    return;
+  }
+  a.rs_x = user_major ? h->slot_u : h->slot_i;
+  a.rs_y = user_major ? h->slot_i : h->slot_u;
+  a.rs_x_cls = user_major ? 0 : h->M;
+  a.rs_y_cls = user_major ? h->M : 0;
+}
+
 int64_t delay_of(const ps_mf_t *h, int64_t p, int64_t c) {
   const int64_t s = h->s;
   switch (h->policy) {
@@ -1290,25 +1404,51 @@ int one_clock(ps_mf_t *h) {
   hipEvent_t ev = nullptr;
   int rc = record(h, &ev);
   if (rc) return rc;
+  if (per_row_policy(h)) {
+    RowViewArgs rv{};
+    rv.ver_u = h->ver_u;
+    rv.slot_u = h->slot_u;
+    rv.ver_i = h->ver_i;
+    rv.slot_i = h->slot_i;
+    rv.ucount = db.ucount;
+    rv.icount_cls = db.icount_cls;
+    rv.users = h->N;
+    rv.items = h->M;
+    rv.clock = c;
+    rv.nclass = h->nclass;
+    rv.s = h->s;
+    rv.essp = h->policy == PS_MF_ESSP_ROW;
+    rv.stale = h->stale;
+    const int64_t rows = h->N + static_cast<int64_t>(h->nclass) * h->M;
+    hipLaunchKernelGGL(k_row_views, dim3(static_cast<unsigned>((rows + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                       h->stream, rv);
+    HIP_TRY(h, hipGetLastError());
+  }
   {
     // set A = user-major (x = user / L, y = item / R); set B = item-major (x = item, y = user)
     CellSweepArgs cs{};
     cs.ca = cell_args(h, db.cells_user, h->partial_u, 0, r_off, cls_slot);
     cs.cb = cell_args(h, db.cells_item, h->partial_i, r_off, 0, cls_slot);
     cs.ncell_a = static_cast<int32_t>(db.cells_user.ncells);
+    set_row_slots(h, cs.ca, true);
+    set_row_slots(h, cs.cb, false);
     const int64_t ncells = db.cells_user.ncells + db.cells_item.ncells;
     UnitSweepArgs us{};
     us.ua = unit_args(h, db.by_user, h->partial_u, 0, r_off, h->M);
     us.ub = unit_args(h, db.by_item, h->partial_i, r_off, 0, h->N);
     us.ua.cls_slot = cls_slot;
     us.ub.cls_slot = cls_slot;
+    set_row_slots(h, us.ua, true);
+    set_row_slots(h, us.ub, false);
     const int64_t gu = db.by_user.nunits > 0 ? db.by_user.grid : 0;
     const int64_t gi = db.by_item.nunits > 0 ? db.by_item.grid : 0;
     us.grid_a = static_cast<int32_t>(gu);
     // dense cells: the user-major pass stores the residuals that the item-major pass reads,
     // so the two run one after the other on the handle's stream
-    const DenseArgs du = dense_args(h, db.dense_user, h->partial_u, 0, r_off, cls_slot, db.dense_item);
-    const DenseArgs di = dense_args(h, db.dense_item, h->partial_i, r_off, 0, cls_slot, db.dense_user);
+    DenseArgs du = dense_args(h, db.dense_user, h->partial_u, 0, r_off, cls_slot, db.dense_item);
+    DenseArgs di = dense_args(h, db.dense_item, h->partial_i, r_off, 0, cls_slot, db.dense_user);
+    set_row_slots(h, du, true);
+    set_row_slots(h, di, false);
     const int64_t ndense = db.dense_user.ncells + db.dense_item.ncells;
     auto launch_dense_pair = [&]() -> hipError_t {
       hipError_t e = hipSuccess;
@@ -1350,6 +1490,7 @@ int one_clock(ps_mf_t *h) {
   fa.eta = h->eta;
   fa.lambda = h->lambda;
   fa.rowmean = rowmean;
+  fa.rs_u = per_row_policy(h) ? h->slot_u : nullptr;
   const int64_t nfin = h->N * h->Kp / 4;
   CommitArgs ca{};
   ca.ring = h->ring;
@@ -1368,13 +1509,15 @@ int one_clock(ps_mf_t *h) {
   ca.eta = h->eta;
   ca.lambda = h->lambda;
   ca.rowmean = rowmean;
+  ca.rs_i = per_row_policy(h) ? h->slot_i : nullptr;
   const int64_t grid_users = (nfin + kBlock - 1) / kBlock, grid_items = h->M;
   hipLaunchKernelGGL(k_commit, dim3(static_cast<unsigned>(grid_users + grid_items)), dim3(kBlock), 0, h->stream, fa,
                      ca, static_cast<int32_t>(grid_users));
   HIP_TRY(h, hipGetLastError());
   if ((rc = record_end(h, PS_MF_KERNEL_COMMIT, ev))) return rc;
 
-  for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_version(h, p, c));
+  if (!per_row_policy(h))
+    for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_version(h, p, c));
   h->clock = c + 1;
   return PS_MF_OK;
 }
@@ -1413,7 +1556,7 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
   if (h->loaded) return fail(h, PS_MF_ESTATE, "options must be set before ps_mf_load_ratings");
   switch (key) {
     case PS_MF_OPT_POLICY:
-      if (value < PS_MF_SSP_LAZY || value > PS_MF_ESSP) return fail(h, PS_MF_EINVAL, "unknown policy %lld", (long long)value);
+      if (value < PS_MF_SSP_LAZY || value > PS_MF_ESSP_ROW) return fail(h, PS_MF_EINVAL, "unknown policy %lld", (long long)value);
       h->policy = static_cast<int32_t>(value);
       return PS_MF_OK;
     case PS_MF_OPT_STEP:
@@ -1499,9 +1642,11 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
     for (int64_t i = 0; i < h->N; ++i) h->owner[i] = static_cast<int32_t>(i % h->P);
   }
   // worker classes: workers that read the same version at every clock
-  h->nclass = (h->policy == PS_MF_SSP_LAZY) ? std::min<int32_t>(h->s + 1, h->P) : 1;
+  // (the per-row policies' clients are these classes: worker p on client p mod (s+1))
+  const bool staggered = h->policy == PS_MF_SSP_LAZY || per_row_policy(h);
+  h->nclass = staggered ? std::min<int32_t>(h->s + 1, h->P) : 1;
   h->cls_of_worker.resize(static_cast<size_t>(h->P));
-  for (int32_t p = 0; p < h->P; ++p) h->cls_of_worker[p] = (h->policy == PS_MF_SSP_LAZY) ? p % (h->s + 1) : 0;
+  for (int32_t p = 0; p < h->P; ++p) h->cls_of_worker[p] = staggered ? p % (h->s + 1) : 0;
 
   psmf::LayoutParams lp;
   lp.users = h->N;
@@ -1601,6 +1746,15 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
     return undo(r);
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->loss_out), sizeof(double)))) return undo(r);
   if ((r = upload(h, &h->zero_row, std::vector<float>(static_cast<size_t>(h->Kp), 0.f)))) return undo(r);
+  if (per_row_policy(h)) {
+    const size_t ni = static_cast<size_t>(h->nclass) * static_cast<size_t>(h->M);
+    if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->ver_u), h->N * sizeof(int32_t))) ||
+        (r = dev_alloc(h, reinterpret_cast<void **>(&h->slot_u), h->N * sizeof(int32_t))) ||
+        (r = dev_alloc(h, reinterpret_cast<void **>(&h->ver_i), ni * sizeof(int32_t))) ||
+        (r = dev_alloc(h, reinterpret_cast<void **>(&h->slot_i), ni * sizeof(int32_t))) ||
+        (r = dev_alloc(h, reinterpret_cast<void **>(&h->stale), (h->s + 1) * sizeof(unsigned long long))))
+      return undo(r);
+  }
   // slot table: row c (c < s) and rows s .. 2s (periodic part), one entry per worker class
   std::vector<int32_t> table(static_cast<size_t>((2 * h->s + 1) * h->nclass));
   std::vector<int32_t> rep(static_cast<size_t>(h->nclass), -1);  // a worker of each class
@@ -1633,6 +1787,15 @@ int ps_mf_set_factors(ps_mf_t *h, const float *L, const float *R) {
                          static_cast<size_t>(h->N), hipMemcpyHostToDevice));
   HIP_TRY(h, hipMemcpy2D(h->ring + h->N * h->Kp, h->Kp * sizeof(float), R, h->K * sizeof(float),
                          h->K * sizeof(float), static_cast<size_t>(h->M), hipMemcpyHostToDevice));
+  if (per_row_policy(h)) {
+    // no row cached yet (version -1); slots 0 keep every address inside the ring
+    const size_t ni = static_cast<size_t>(h->nclass) * static_cast<size_t>(h->M);
+    HIP_TRY(h, hipMemset(h->ver_u, 0xff, h->N * sizeof(int32_t)));
+    HIP_TRY(h, hipMemset(h->ver_i, 0xff, ni * sizeof(int32_t)));
+    HIP_TRY(h, hipMemset(h->slot_u, 0, h->N * sizeof(int32_t)));
+    HIP_TRY(h, hipMemset(h->slot_i, 0, ni * sizeof(int32_t)));
+    HIP_TRY(h, hipMemset(h->stale, 0, (h->s + 1) * sizeof(unsigned long long)));
+  }
   HIP_TRY(h, hipDeviceSynchronize());
   h->clock = 0;
   h->vlog.clear();
@@ -1710,8 +1873,10 @@ int ps_mf_get_clock(ps_mf_t *h, int64_t *clock) {
 
 int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64_t cap, int64_t *len) {
   if (!h || !len) return PS_MF_EINVAL;
-  if (kind == PS_MF_IDX_STALENESS && !h->loaded) return fail(h, PS_MF_ESTATE, "no ratings loaded");
-  if (kind != PS_MF_IDX_OWNER && kind != PS_MF_IDX_VERSION_LOG && kind != PS_MF_IDX_STALENESS) {
+  if ((kind == PS_MF_IDX_STALENESS || kind == PS_MF_IDX_ROW_VERSIONS) && !h->loaded)
+    return fail(h, PS_MF_ESTATE, "no ratings loaded");
+  if (kind != PS_MF_IDX_OWNER && kind != PS_MF_IDX_VERSION_LOG && kind != PS_MF_IDX_STALENESS &&
+      kind != PS_MF_IDX_ROW_VERSIONS) {
     if (!h->loaded) return fail(h, PS_MF_ESTATE, "no ratings loaded");
     if (block < 0 || block >= h->B) return fail(h, PS_MF_EINVAL, "block %d out of range", block);
   }
@@ -1739,17 +1904,37 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     split[6] = L.partial_rows_user;
     split[7] = L.partial_rows_item;
   }
-  std::vector<int64_t> stale;
+  std::vector<int64_t> stale, rowver;
   if (kind == PS_MF_IDX_STALENESS) {
-    // the version log holds v(p, c) for every clock run; worker p reads two rows per rating
     stale.assign(static_cast<size_t>(h->s) + 1, 0);
-    const int64_t clocks = static_cast<int64_t>(h->vlog.size()) / h->P;
-    for (int64_t c = 0; c < clocks; ++c)
-      for (int64_t p = 0; p < h->P; ++p)
-        stale[static_cast<size_t>(c - h->vlog[c * h->P + p])] +=
-            2 * h->worker_ratings[static_cast<size_t>(c % h->B) * h->P + p];
+    if (per_row_policy(h)) {
+      // counted on the device by the per-row view kernel
+      if (h->stale) {
+        HIP_TRY(h, hipStreamSynchronize(h->stream));
+        HIP_TRY(h, hipMemcpy(stale.data(), h->stale, stale.size() * sizeof(int64_t), hipMemcpyDeviceToHost));
+      }
+    } else {
+      // the version log holds v(p, c) for every clock run; worker p reads two rows per rating
+      const int64_t clocks = static_cast<int64_t>(h->vlog.size()) / h->P;
+      for (int64_t c = 0; c < clocks; ++c)
+        for (int64_t p = 0; p < h->P; ++p)
+          stale[static_cast<size_t>(c - h->vlog[c * h->P + p])] +=
+              2 * h->worker_ratings[static_cast<size_t>(c % h->B) * h->P + p];
+    }
+  }
+  if (kind == PS_MF_IDX_ROW_VERSIONS && per_row_policy(h)) {
+    const size_t nu = static_cast<size_t>(h->N), ni = static_cast<size_t>(h->nclass) * static_cast<size_t>(h->M);
+    rowver.assign(nu + ni, -1);
+    if (h->ver_u && h->has_factors) {
+      std::vector<int32_t> t(nu + ni);
+      HIP_TRY(h, hipStreamSynchronize(h->stream));
+      HIP_TRY(h, hipMemcpy(t.data(), h->ver_u, nu * sizeof(int32_t), hipMemcpyDeviceToHost));
+      HIP_TRY(h, hipMemcpy(t.data() + nu, h->ver_i, ni * sizeof(int32_t), hipMemcpyDeviceToHost));
+      for (size_t x = 0; x < nu + ni; ++x) rowver[x] = t[x];
+    }
   }
   switch (kind) {
+    case PS_MF_IDX_ROW_VERSIONS: src = rowver.data(); esz = 8; n = static_cast<int64_t>(rowver.size()); break;
     case PS_MF_IDX_STALENESS: src = stale.data(); esz = 8; n = h->s + 1; break;
     case PS_MF_IDX_OWNER: src = h->owner.data(); esz = 4; n = h->N; break;
     case PS_MF_IDX_ROW_PTR: src = h->layout[block].row_ptr.data(); esz = 8; n = h->N + 1; break;

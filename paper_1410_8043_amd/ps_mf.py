@@ -26,9 +26,9 @@ LIB_PATH = os.path.join(_HERE, "libps_mf.so")
 OK, EINVAL, ENOMEM, EDEVICE, ESTATE, EINTERNAL = 0, -1, -2, -3, -4, -5
 (OPT_POLICY, OPT_STEP, OPT_MB_BLOCKS, OPT_MB_SEED, OPT_HOST_ONLY, OPT_TIMING, OPT_TILE_BYTES, OPT_UNIT_MAX, OPT_CELLS,
  OPT_HEAVY_MIN, OPT_TWO_STREAMS, OPT_HOT_STEPS, OPT_DENSE_MIN) = range(1, 14)
-SSP_LAZY, SSP_WORST, ESSP = 0, 1, 2
+SSP_LAZY, SSP_WORST, ESSP, SSP_ROW, ESSP_ROW = 0, 1, 2, 3, 4
 STEP_ROWMEAN, STEP_SUM = 0, 1
-IDX_OWNER, IDX_ROW_PTR, IDX_COL, IDX_PERM, IDX_USER_COUNT, IDX_ITEM_COUNT, IDX_VERSION_LOG, IDX_SPLIT, IDX_STALENESS = range(9)
+IDX_OWNER, IDX_ROW_PTR, IDX_COL, IDX_PERM, IDX_USER_COUNT, IDX_ITEM_COUNT, IDX_VERSION_LOG, IDX_SPLIT, IDX_STALENESS, IDX_ROW_VERSIONS = range(10)
 KERNEL_SWEEP, KERNEL_COMMIT = 0, 1
 
 SYMBOLS = ("ps_mf_create", "ps_mf_set_option", "ps_mf_set_owner_map", "ps_mf_set_stream", "ps_mf_load_ratings",

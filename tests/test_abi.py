@@ -234,3 +234,28 @@ def test_dense_tiles_need_a_supported_rank():
             assert e.value.code == ps_mf.EINVAL
     finally:
         ps_mf.ps_mf_destroy(h)
+
+
+@pytest.mark.parametrize("policy", [ps_mf.SSP_ROW, ps_mf.ESSP_ROW])
+def test_per_row_policies_on_a_host_only_handle(policy):
+    """The per-row policies build the same integer layout (their clients are the worker
+    classes p mod (s+1)); before any clock no row is cached and no read is counted."""
+    from paper_1410_8043_amd import synth
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.03)
+    w = synth.generate(spec, K=1)
+    with ps_mf.PsMf(spec.N, spec.M, 16, spec.P, 3, 0.01, 0.05, policy=policy, B=spec.B, mb_seed=spec.seed,
+                    host_only=True) as g:
+        g.load_ratings(w.user, w.item, w.val)
+        o = oracle.Oracle(spec.N, spec.M, 16, spec.P, 3, 0.01, 0.05, policy, oracle.ROWMEAN, spec.B, spec.seed)
+        o.load(w.user, w.item, w.val)
+        compare_layout(g, o, spec.B, spec.N, spec.M)
+        rv = g.export_index(ps_mf.IDX_ROW_VERSIONS)
+        assert rv.size == spec.N + min(spec.P, 4) * spec.M and np.all(rv == -1)
+        assert g.export_index(ps_mf.IDX_STALENESS).tolist() == [0, 0, 0, 0]
+    h = ps_mf.ps_mf_create(4, 3, 2, 1, 0, 0.1, 0.1)
+    try:
+        with pytest.raises(ps_mf.PsMfError) as e:
+            ps_mf.ps_mf_set_option(h, ps_mf.OPT_POLICY, 5)
+        assert e.value.code == ps_mf.EINVAL
+    finally:
+        ps_mf.ps_mf_destroy(h)

@@ -59,6 +59,8 @@ def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, c
         assert abs(loss - loss_o) <= LOSS_RTOL * max(loss_o, 1e-30), (loss, loss_o)
         assert np.array_equal(g.export_index(gpu_mod().IDX_VERSION_LOG), o.export(oracle.X_VERSION_LOG))
         assert np.array_equal(g.export_index(gpu_mod().IDX_STALENESS), o.export(oracle.X_STALENESS))
+        if policy in (oracle.SSP_ROW, oracle.ESSP_ROW):
+            assert np.array_equal(g.export_index(gpu_mod().IDX_ROW_VERSIONS), o.export(oracle.X_ROW_VERSIONS))
         if check_versions:
             for v in range(max(0, clocks - s), clocks + 1):
                 Lv, Rv = g.get_version(v)
@@ -291,6 +293,38 @@ def test_dense_tiles_medium_minibatch_blocks(gpu, step):
     run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3,
              eta=spec.eta if step == oracle.ROWMEAN else 1e-4, lam=spec.lam, clocks=8, B=spec.B, seed=spec.seed,
              step=step, dense_min=64, min_dense=4096)
+
+
+# ---------------------------------------------------------------- per-row caches (Section 4)
+@pytest.mark.parametrize("policy", [oracle.SSP_ROW, oracle.ESSP_ROW])
+@pytest.mark.parametrize("s,B", [(0, 1), (1, 1), (1, 4), (3, 4), (7, 3)])
+def test_tiny_config_per_row_policies(gpu, policy, s, B):
+    """Per-row cached versions on the tiny workload, whole shards (B = 1) and minibatches
+    (rows read intermittently, so their cached versions differ row by row)."""
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta,
+             lam=spec.lam, clocks=12, policy=policy, B=B, seed=spec.seed, check_versions=True)
+
+
+@pytest.mark.parametrize("policy", [oracle.SSP_ROW, oracle.ESSP_ROW])
+@pytest.mark.parametrize("K", [32, 128])
+def test_per_row_policies_with_dense_tiles_cells_and_units(gpu, policy, K):
+    """The 100M-rating workload's laws at 5% size in 4 minibatch blocks, s = 3: per-row
+    slots through the dense tiles, the LDS cells, the L2 units and the commit."""
+    spec = synth.scaled(synth.CONFIGS["full"], 0.05)
+    w = synth.generate(spec, K=K)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=K, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=9, policy=policy, B=4, seed=spec.seed, check_versions=True, dense_min=300,
+             heavy_min=30, hot_steps=1, min_dense=4096)
+
+
+@pytest.mark.parametrize("policy", [oracle.SSP_ROW, oracle.ESSP_ROW])
+def test_per_row_policies_medium_minibatches_ragged_rank(gpu, policy):
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.05)
+    w = synth.generate(spec, K=33)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=33, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=10, policy=policy, B=spec.B, seed=spec.seed)
 
 
 def test_timing_option_counts_launches(gpu):
