@@ -88,8 +88,8 @@ typedef struct ps_mf ps_mf_t;
                                   ranked by rating count x 64 items ranked by rating count) is
                                   swept with matrix-core products as a dense block; 0: none;
                                   -1 (default): automatic (800, i.e. 20% full, when the padded
-                                  rank is in [16, 128], else none); at most 4096.  A value > 0
-                                  with a padded rank outside [16, 128] makes
+                                  rank is in [16, 256], else none); at most 4096.  A value > 0
+                                  with a padded rank outside [16, 256] makes
                                   ps_mf_load_ratings fail with PS_MF_EINVAL */
 
 /* Views (Section 3.2 SSP condition; Section 4 ESSPTable).  The table-level policies give

@@ -719,9 +719,14 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
 // The dense cells of both sweep directions in one launch: workgroups [0, ncell_a) take set
 // A, the rest set B.
 // One workgroup per dense cell of one direction: the user-major cells (residuals from D,
-// stored as E), then, in a second launch, the item-major cells (FromE).
+// stored as E), then, in a second launch, the item-major cells (FromE).  Up to Kp = 128 two
+// workgroups share a CU (64 KiB of LDS each); at Kp = 256 the two staging buffers take
+// 128 KiB, one workgroup fills a CU and its four wavefronts may use 512 registers each.
+template <int Kp>
+constexpr int dense_waves_per_simd() { return Kp <= 128 ? 2 : 1; }
+
 template <int Kp, bool FromE>
-__global__ __launch_bounds__(kDenseThreads, 2) void k_dense(DenseArgs a) {
+__global__ __launch_bounds__(kDenseThreads, dense_waves_per_simd<Kp>()) void k_dense(DenseArgs a) {
   __shared__ float4 lds0[kDenseRowsDev * Kp / 4];
   __shared__ float4 lds1[kDenseRowsDev * Kp / 4];
   run_dense<Kp, FromE>(a, static_cast<int64_t>(blockIdx.x), lds0, lds1);
@@ -1033,7 +1038,7 @@ struct LaunchUnits {
   }
 };
 // padded ranks with a dense (MFMA) cell kernel
-bool dense_supported(int Kp) { return Kp >= 16 && Kp <= 128; }
+bool dense_supported(int Kp) { return Kp >= 16 && Kp <= 256; }
 
 template <bool FromE>
 hipError_t launch_dense(int Kp, const DenseArgs &a, int64_t grid, hipStream_t st) {
@@ -1043,6 +1048,7 @@ hipError_t launch_dense(int Kp, const DenseArgs &a, int64_t grid, hipStream_t st
     case 32: hipLaunchKernelGGL((k_dense<32, FromE>), gd, bd, 0, st, a); break;
     case 64: hipLaunchKernelGGL((k_dense<64, FromE>), gd, bd, 0, st, a); break;
     case 128: hipLaunchKernelGGL((k_dense<128, FromE>), gd, bd, 0, st, a); break;
+    case 256: hipLaunchKernelGGL((k_dense<256, FromE>), gd, bd, 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1671,7 +1677,7 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
                                       : std::max<int64_t>(256, 16 * h->M / lp.cell_rows);
   }
   if (h->dense_min > 0 && !dense_supported(h->Kp))
-    return fail(h, PS_MF_EINVAL, "dense tiles need a padded rank in [16, 128], not %d", h->Kp);
+    return fail(h, PS_MF_EINVAL, "dense tiles need a padded rank in [16, 256], not %d", h->Kp);
   lp.dense_min = h->dense_min >= 0 ? h->dense_min : (dense_supported(h->Kp) ? kDenseAuto : 0);
   lp.dense_target = PS_MF_DENSE_CELLS;
   if (h->cells) {

@@ -210,7 +210,7 @@ def test_host_layout_self_check_with_dense_tiles(dense_min, policy, s, B, K):
 
 
 def test_dense_tiles_need_a_supported_rank():
-    for K, ok in [(8, False), (16, True), (128, True), (129, False)]:
+    for K, ok in [(8, False), (16, True), (128, True), (129, True), (256, True), (257, False)]:
         with ps_mf.PsMf(40, 30, K, 2, 1, 0.01, 0.05, host_only=True, dense_min=5) as g:
             u = np.arange(40, dtype=np.int32).repeat(30)
             i = np.tile(np.arange(30, dtype=np.int32), 40)

@@ -164,6 +164,15 @@ def test_large_shape_scaled(gpu):
              lam=spec.lam, clocks=10)
 
 
+@pytest.mark.parametrize("dense_min", [1, 200])
+def test_large_shape_scaled_dense_tiles_at_k256(gpu, dense_min):
+    """Rank 256: dense tiles with one workgroup per CU, next to cells and units."""
+    spec = synth.scaled(synth.CONFIGS["large"], 0.01)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=6, dense_min=dense_min, heavy_min=40, min_dense=4096)
+
+
 @pytest.mark.parametrize("s", [0, 3])
 def test_long_rows_take_the_workgroup_path(gpu, s):
     """Users with thousands of ratings (the capped Zipf head) exercise the long-row kernel."""
@@ -274,7 +283,7 @@ def test_dense_tiles_mixed_with_cells_and_units(gpu, K, dense_min):
              min_dense=4096)
 
 
-@pytest.mark.parametrize("K", [16, 33, 100, 128])
+@pytest.mark.parametrize("K", [16, 33, 100, 128, 200, 256])
 def test_dense_tiles_ragged_rank_duplicates_and_empty_rows(gpu, K):
     """Every tile dense: padded ranks, duplicate (user, item) pairs (the repeats stay
     sparse), users and items without ratings and a scattering owner map."""
