@@ -19,8 +19,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libps_mf_oracle.so")
 
 SSP_LAZY, SSP_WORST, ESSP, SSP_ROW, ESSP_ROW = 0, 1, 2, 3, 4
-ROWMEAN, SUM = 0, 1
-X_OWNER, X_ROW_PTR, X_COL, X_PERM, X_USER_COUNT, X_ITEM_COUNT, X_VERSION_LOG, X_STALENESS, X_ROW_VERSIONS = range(9)
+ROWMEAN, SUM, SEQ = 0, 1, 2
+(X_OWNER, X_ROW_PTR, X_COL, X_PERM, X_USER_COUNT, X_ITEM_COUNT, X_VERSION_LOG, X_STALENESS, X_ROW_VERSIONS,
+ X_SEQ_ORDER) = range(10)
 
 _lib = None
 
@@ -57,6 +58,7 @@ def _load():
         "oracle_export": [vp, i32, i32, vp, i64, ctypes.POINTER(i64)],
         "oracle_view_version": [vp, i64, i64, ctypes.POINTER(i64)],
         "oracle_splitmix64": [u64, ctypes.POINTER(u64)],
+        "oracle_set_strata": [vp, i32],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -92,7 +94,7 @@ def _c(a, dtype):
 class Oracle:
     """Clocked SSP/ESSP MF-SGD on the CPU; mirrors the library's call sequence."""
 
-    def __init__(self, N, M, K, P, s, eta, lam, policy=SSP_LAZY, step=ROWMEAN, B=1, seed=0, owner=None):
+    def __init__(self, N, M, K, P, s, eta, lam, policy=SSP_LAZY, step=ROWMEAN, B=1, seed=0, owner=None, strata=None):
         self._lib = _load()
         self.N, self.M, self.K, self.P, self.s = int(N), int(M), int(K), int(P), int(s)
         self._owner = None if owner is None else _c(owner, np.int32)
@@ -102,6 +104,8 @@ class Oracle:
                                      None if self._owner is None else self._owner.ctypes.data, ctypes.byref(h)),
              "oracle_create")
         self._h = h
+        if strata is not None:
+            _chk(self._lib.oracle_set_strata(self._h, int(strata)), "oracle_set_strata")
 
     def close(self):
         if self._h:

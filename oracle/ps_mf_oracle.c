@@ -32,6 +32,15 @@
  *     clock later): the first read fetches version c, later reads see c - min(s, 1);
  *   - step normalisation: SUM uses the summed per-rating steps; ROWMEAN divides each
  *     row's summed contribution by that row's rating count in the clock's minibatch;
+ *   - or SEQ: each worker applies the Section 3.1 update rating by rating to its own copy
+ *     of the rows it reads (read-my-writes inside the clock), starting from its view; at
+ *     the clock boundary it commits (copy - view) for every row it touched, and the
+ *     server adds the commits of all workers (Section 4: updates coalesced per clock).
+ *     The order inside a worker is stratified into G sub-epochs: user group
+ *     ug(i) = (i div P) mod G, item group ig(j) = j mod G, and rating (i, j) belongs to
+ *     sub-epoch (ig(j) - ug(i)) mod G; the sub-epochs run in order, each in canonical
+ *     order.  One sub-epoch's (user group, item group) strata share no row, so running
+ *     them side by side gives the same result;
  *   - the lambda term enters once per rating, at the view (Section 3.1 update rule);
  *   - minibatch block of a rating: splitmix64(seed ^ (i<<32 | j)) mod B, block c mod B
  *     at clock c; rows with no rating in the block are left unchanged;
@@ -55,9 +64,9 @@
 #define OR_ESTATE -4
 
 enum { OR_LAZY = 0, OR_WORST = 1, OR_ESSP = 2, OR_SSP_ROW = 3, OR_ESSP_ROW = 4 };
-enum { OR_ROWMEAN = 0, OR_SUM = 1 };
+enum { OR_ROWMEAN = 0, OR_SUM = 1, OR_SEQ = 2 };
 enum { OR_X_OWNER = 0, OR_X_ROW_PTR = 1, OR_X_COL = 2, OR_X_PERM = 3, OR_X_USER_COUNT = 4, OR_X_ITEM_COUNT = 5,
-       OR_X_VERSION_LOG = 6, OR_X_STALENESS = 7, OR_X_ROW_VERSIONS = 8 };
+       OR_X_VERSION_LOG = 6, OR_X_STALENESS = 7, OR_X_ROW_VERSIONS = 8, OR_X_SEQ_ORDER = 9 };
 
 typedef struct {
   int64_t N, M;
@@ -94,6 +103,13 @@ typedef struct {
   int64_t *ucache; /* N */
   int64_t *icache; /* C*M */
   uint8_t *iread;  /* C*M scratch: item rows a client reads this clock */
+  /* step SEQ: G sub-epochs; sorder holds the entries of each block (load indices, at
+     bstart[b] ..) in the order (sub-epoch, worker, user group, canonical); each worker's
+     copies of the rows it touched this clock (fp64): Lloc [N*K], Rloc [P*M*K] */
+  int32_t G;
+  int64_t *sorder;
+  double *Lloc, *Rloc;
+  uint8_t *utouch, *itouch; /* N, P*M */
 } oracle_t;
 
 /* SplitMix64 (Steele, Lea & Flood 2014): one step of the sequential generator from `state`. */
@@ -155,6 +171,7 @@ void oracle_destroy(oracle_t *o) {
   free(o->bstart); free(o->order); free(o->ucount); free(o->icount);
   free(o->Lring); free(o->Rring); free(o->vlog); free(o->dL); free(o->dR); free(o->stale);
   free(o->ucache); free(o->icache); free(o->iread);
+  free(o->sorder); free(o->Lloc); free(o->Rloc); free(o->utouch); free(o->itouch);
   free(o);
 }
 
@@ -163,12 +180,15 @@ int oracle_create(int64_t N, int64_t M, int32_t K, int32_t P, int32_t s, double 
   if (!out) return OR_EINVAL;
   *out = NULL;
   if (N <= 0 || M <= 0 || K <= 0 || P <= 0 || s < 0 || B < 1 || N > 0x7fffffff || M > 0x7fffffff) return OR_EINVAL;
-  if (policy < OR_LAZY || policy > OR_ESSP_ROW || (step != OR_ROWMEAN && step != OR_SUM)) return OR_EINVAL;
+  if (policy < OR_LAZY || policy > OR_ESSP_ROW || step < OR_ROWMEAN || step > OR_SEQ) return OR_EINVAL;
+  /* sequential steps start from one view per (worker, clock): table policies only */
+  if (step == OR_SEQ && policy > OR_ESSP) return OR_EINVAL;
   if (!isfinite(eta) || !isfinite(lambda)) return OR_EINVAL;
   oracle_t *o = (oracle_t *)calloc(1, sizeof(oracle_t));
   if (!o) return OR_ENOMEM;
   o->N = N; o->M = M; o->K = K; o->P = P; o->s = s; o->eta = eta; o->lambda = lambda;
   o->policy = policy; o->step = step; o->B = B; o->seed = seed;
+  o->G = 64;
   o->owner = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
   o->stale = (int64_t *)calloc((size_t)s + 1, sizeof(int64_t));
   o->C = P < (int64_t)s + 1 ? P : (int64_t)s + 1;
@@ -184,6 +204,39 @@ int oracle_create(int64_t N, int64_t M, int32_t K, int32_t P, int32_t s, double 
     o->owner[i] = p;
   }
   *out = o;
+  return OR_OK;
+}
+
+/* number of sub-epochs G of the SEQ step (default 64); before load */
+int oracle_set_strata(oracle_t *o, int32_t G) {
+  if (!o || G < 1) return OR_EINVAL;
+  if (o->loaded) return OR_ESTATE;
+  o->G = G;
+  return OR_OK;
+}
+
+/* sub-epoch of rating (i, j) under the SEQ step */
+static int64_t sub_epoch(const oracle_t *o, int64_t i, int64_t j) {
+  const int64_t ug = (i / o->P) % o->G, ig = j % o->G;
+  return ((ig - ug) % o->G + o->G) % o->G;
+}
+
+/* stable counting sort of a[0..n) by key(x) in [0, range) into out */
+static int stable_by_key(const oracle_t *o, const int64_t *a, int64_t n, int64_t range, int which, int64_t *out) {
+  int64_t *cnt = (int64_t *)calloc((size_t)range + 1, sizeof(int64_t));
+  if (!cnt) return OR_ENOMEM;
+  for (int64_t q = 0; q < n; ++q) {
+    const int64_t i = o->user[a[q]], j = o->item[a[q]];
+    const int64_t k = which == 0 ? (i / o->P) % o->G : sub_epoch(o, i, j) * o->P + o->owner[i];
+    cnt[k + 1] += 1;
+  }
+  for (int64_t k = 0; k < range; ++k) cnt[k + 1] += cnt[k];
+  for (int64_t q = 0; q < n; ++q) {
+    const int64_t i = o->user[a[q]], j = o->item[a[q]];
+    const int64_t k = which == 0 ? (i / o->P) % o->G : sub_epoch(o, i, j) * o->P + o->owner[i];
+    out[cnt[k]++] = a[q];
+  }
+  free(cnt);
   return OR_OK;
 }
 
@@ -235,6 +288,20 @@ int oracle_load(oracle_t *o, const int32_t *user, const int32_t *item, const flo
   for (int32_t b = 0; b < o->B; ++b)
     qsort(o->order + o->bstart[b], (size_t)(o->bstart[b + 1] - o->bstart[b]), sizeof(int64_t), cmp_canonical);
   free(blk); free(fill);
+  if (o->step == OR_SEQ) {
+    /* the order each worker applies its ratings in: canonical order, stably sorted by user
+       group, then by (sub-epoch, worker) */
+    o->sorder = (int64_t *)malloc(sizeof(int64_t) * n);
+    int64_t *tmp = (int64_t *)malloc(sizeof(int64_t) * n);
+    if (!o->sorder || !tmp) { free(tmp); return OR_ENOMEM; }
+    for (int32_t b = 0; b < o->B; ++b) {
+      const int64_t lo = o->bstart[b], nb = o->bstart[b + 1] - lo;
+      int rc = stable_by_key(o, o->order + lo, nb, o->G, 0, tmp);
+      if (!rc) rc = stable_by_key(o, tmp, nb, (int64_t)o->G * o->P, 1, o->sorder + lo);
+      if (rc) { free(tmp); return rc; }
+    }
+    free(tmp);
+  }
   o->loaded = 1;
   return OR_OK;
 }
@@ -266,6 +333,61 @@ int oracle_set_factors(oracle_t *o, const float *L0, const float *R0) {
 static float *L_of(const oracle_t *o, int64_t v) { return o->Lring + (size_t)(v % (o->s + 1)) * (size_t)(o->N * o->K); }
 static float *R_of(const oracle_t *o, int64_t v) { return o->Rring + (size_t)(v % (o->s + 1)) * (size_t)(o->M * o->K); }
 
+/* the SEQ step of one clock: every worker runs its ratings in its order on its own copies
+   of the rows, which start at its view; dL and dR receive sum over workers of
+   (copy - view) for the rows each touched */
+static int seq_sweep(oracle_t *o, int64_t c, int32_t b) {
+  const int64_t K = o->K, M = o->M;
+  if (!o->Lloc) {
+    o->Lloc = (double *)malloc(sizeof(double) * (size_t)(o->N * K));
+    o->Rloc = (double *)malloc(sizeof(double) * (size_t)(o->P * M * K));
+    o->utouch = (uint8_t *)calloc((size_t)o->N, 1);
+    o->itouch = (uint8_t *)calloc((size_t)(o->P * M), 1);
+    if (!o->Lloc || !o->Rloc || !o->utouch || !o->itouch) return OR_ENOMEM;
+  }
+  for (int64_t q = o->bstart[b]; q < o->bstart[b + 1]; ++q) {
+    const int64_t t = o->sorder[q];
+    const int64_t i = o->user[t], j = o->item[t], p = o->owner[i];
+    const int64_t v = view_version(o, p, c);
+    double *Li = o->Lloc + i * K, *Rj = o->Rloc + (p * M + j) * K;
+    if (!o->utouch[i]) { /* first read of L_i this clock: the view */
+      const float *src = L_of(o, v) + i * K;
+      for (int64_t k = 0; k < K; ++k) Li[k] = (double)src[k];
+      o->utouch[i] = 1;
+    }
+    if (!o->itouch[p * M + j]) { /* first read of R_j by worker p this clock */
+      const float *src = R_of(o, v) + j * K;
+      for (int64_t k = 0; k < K; ++k) Rj[k] = (double)src[k];
+      o->itouch[p * M + j] = 1;
+    }
+    o->stale[c - v] += 2; /* the rating reads L_i and R_j of the worker's view */
+    double dot = 0.0;
+    for (int64_t k = 0; k < K; ++k) dot += Li[k] * Rj[k];
+    const double e = (double)o->val[t] - dot;
+    for (int64_t k = 0; k < K; ++k) {
+      const double l = Li[k], r = Rj[k];
+      Li[k] = l + o->eta * (e * r - o->lambda * l);
+      Rj[k] = r + o->eta * (e * l - o->lambda * r);
+    }
+  }
+  for (int64_t i = 0; i < o->N; ++i) {
+    if (!o->utouch[i]) continue;
+    const float *Lv = L_of(o, view_version(o, o->owner[i], c)) + i * K;
+    for (int64_t k = 0; k < K; ++k) o->dL[i * K + k] = o->Lloc[i * K + k] - (double)Lv[k];
+    o->utouch[i] = 0;
+  }
+  for (int64_t p = 0; p < o->P; ++p) {
+    const float *Rv = R_of(o, view_version(o, p, c));
+    for (int64_t j = 0; j < M; ++j) {
+      if (!o->itouch[p * M + j]) continue;
+      const double *Rl = o->Rloc + (p * M + j) * K;
+      for (int64_t k = 0; k < K; ++k) o->dR[j * K + k] += Rl[k] - (double)Rv[j * K + k];
+      o->itouch[p * M + j] = 0;
+    }
+  }
+  return OR_OK;
+}
+
 /* one clock: every worker computes its update from its view; the sum is committed */
 static int one_clock(oracle_t *o) {
   const int64_t c = o->clock, K = o->K;
@@ -286,7 +408,11 @@ static int one_clock(oracle_t *o) {
         o->iread[x] = 0;
       }
   }
-  for (int64_t q = o->bstart[b]; q < o->bstart[b + 1]; ++q) {
+  if (o->step == OR_SEQ) {
+    int rc = seq_sweep(o, c, b);
+    if (rc) return rc;
+  }
+  for (int64_t q = o->bstart[b]; q < o->bstart[b + 1] && o->step != OR_SEQ; ++q) {
     const int64_t t = o->order[q];
     const int64_t i = o->user[t], j = o->item[t];
     int64_t vL, vR;
@@ -387,6 +513,7 @@ int oracle_rows_from_v0(const oracle_t *o, int32_t nclocks, int64_t nu, const in
   if (!o->loaded || !o->has_factors || o->clock != 0) return OR_ESTATE;
   const int64_t K = o->K;
   if (per_row(o) && nclocks > 1) return OR_EINVAL; /* only clock 0 surely reads version 0 */
+  if (o->step == OR_SEQ) return OR_EINVAL;        /* rows of a SEQ clock depend on whole chains */
   for (int64_t c = 0; c < nclocks && !per_row(o); ++c)
     for (int64_t p = 0; p < o->P; ++p)
       if (view_version(o, p, c) != 0) return OR_EINVAL;
@@ -443,6 +570,8 @@ bad:
  *   PERM(b)      int64 [nnz_b] load indices in the same order
  *   USER_COUNT(b) int32 [N], ITEM_COUNT(b) int32 [M]
  *   VERSION_LOG  int64 [clocks * P], entry c*P + p = v(p, c)
+ *   SEQ_ORDER(b) int64 [nnz_b] (step SEQ) load indices in the order the workers apply
+ *                them: (sub-epoch, worker, user group, canonical)
  */
 int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t cap, int64_t *len) {
   if (!o || !len) return OR_EINVAL;
@@ -460,6 +589,10 @@ int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t
     case OR_X_VERSION_LOG: n = o->vlog_len; break;
     case OR_X_STALENESS: n = (int64_t)o->s + 1; break;
     case OR_X_ROW_VERSIONS: n = o->N + o->C * o->M; break;
+    case OR_X_SEQ_ORDER:
+      if (o->step != OR_SEQ) return OR_EINVAL;
+      n = o->bstart[b + 1] - o->bstart[b];
+      break;
     default: return OR_EINVAL;
   }
   *len = n;
@@ -485,6 +618,7 @@ int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t
       memcpy(buf, o->ucache, sizeof(int64_t) * (size_t)o->N);
       memcpy((int64_t *)buf + o->N, o->icache, sizeof(int64_t) * (size_t)(o->C * o->M));
       break;
+    case OR_X_SEQ_ORDER: if (n) memcpy(buf, o->sorder + o->bstart[b], sizeof(int64_t) * (size_t)n); break;
   }
   return OR_OK;
 }

@@ -36,7 +36,7 @@ def test_hand_examples(case):
     i = np.array([r[1] for r in case["ratings"]], np.int32)
     v = np.array([r[2] for r in case["ratings"]], np.float32)
     o = oracle.Oracle(case["N"], case["M"], case["K"], case["P"], case["s"], case["eta"], case["lam"],
-                      case["policy"], case["step"], 1, 0, case["owner"])
+                      case["policy"], case["step"], 1, 0, case["owner"], strata=case["strata"])
     o.load(u, i, v)
     o.set_factors(case["L0"], case["R0"])
     for ex in sorted(case["expect"], key=lambda e: e["clock"]):
@@ -493,3 +493,180 @@ def test_per_row_staleness_stays_in_the_window(policy, s):
     else:
         assert hist[1:].sum() > 0  # intermittent reads keep rows cached across clocks
     assert cache.min() >= -1 and cache.max() <= clocks - 1
+
+
+# ---------------------------------------------------------------- sequential steps inside a worker (SEQ)
+def seq_order_by_definition(user, item, owner, P, G, B, seed):
+    """Load indices of each block in the order the workers apply them, from the stated
+    stratification: sub-epoch t = (j mod G - (i div P) mod G) mod G, then worker, user
+    group, and canonical (user, item, load index) order."""
+    blocks = np.array([block_of(int(u), int(i), seed, B) for u, i in zip(user, item)])
+    out = []
+    for b in range(B):
+        idx = [t for t in range(user.size) if blocks[t] == b]
+        key = lambda t: (((int(item[t]) % G) - (int(user[t]) // P) % G) % G, int(owner[user[t]]),
+                         (int(user[t]) // P) % G, int(user[t]), int(item[t]), t)
+        out.append(np.array(sorted(idx, key=key), np.int64))
+    return out
+
+
+@pytest.mark.parametrize("P,G,B", [(1, 1, 1), (1, 3, 1), (3, 2, 2), (4, 5, 3), (2, 64, 1)])
+def test_seq_order_is_the_stratified_order(P, G, B):
+    rng = np.random.default_rng(P * 100 + G)
+    N, M = 23, 17
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 150, 2, dup=5)
+    owner = rng.integers(0, P, size=N).astype(np.int32)
+    o = oracle.Oracle(N, M, 2, P, 1, 0.01, 0.0, oracle.SSP_LAZY, oracle.SEQ, B, 11, owner, strata=G)
+    o.load(user, item, val)
+    want = seq_order_by_definition(user, item, owner, P, G, B, 11)
+    for b in range(B):
+        assert np.array_equal(o.export(oracle.X_SEQ_ORDER, b), want[b])
+    o.close()
+
+
+def matching_problem(rng, P, users_per_worker, M, K):
+    """Every worker holds a matching: each of its users and each item at most once."""
+    user, item = [], []
+    for p in range(P):
+        us = p + P * np.arange(users_per_worker)
+        its = rng.choice(M, size=users_per_worker, replace=False)
+        user += us.tolist()
+        item += its.tolist()
+    user, item = np.array(user, np.int32), np.array(item, np.int32)
+    val = rng.integers(1, 6, size=user.size).astype(np.float32)
+    N = P * users_per_worker
+    L0 = (0.3 * rng.standard_normal((N, K))).astype(np.float32)
+    R0 = (0.3 * rng.standard_normal((M, K))).astype(np.float32)
+    return N, user, item, val, L0, R0
+
+
+@pytest.mark.parametrize("policy,s", [(oracle.SSP_LAZY, 0), (oracle.SSP_LAZY, 2), (oracle.SSP_WORST, 1),
+                                      (oracle.ESSP, 3)])
+def test_seq_equals_sum_when_no_row_is_read_back(policy, s):
+    # with a matching per worker no rating reads a row another rating of the same worker
+    # wrote, so applying the ratings one by one is the summed step of the same view
+    rng = np.random.default_rng(s + 10 * policy)
+    P, M, K = 4, 9, 3
+    N, user, item, val, L0, R0 = matching_problem(rng, P, 6, M, K)
+    res = []
+    for step in (oracle.SUM, oracle.SEQ):
+        o = oracle.Oracle(N, M, K, P, s, 0.05, 0.1, policy, step, 1, 0, strata=4)
+        o.load(user, item, val)
+        o.set_factors(L0, R0)
+        o.clock(6)
+        res.append(o.get_factors() + (o.export(oracle.X_VERSION_LOG), o.export(oracle.X_STALENESS)))
+        o.close()
+    for a, b in zip(res[0][:2], res[1][:2]):
+        np.testing.assert_allclose(a, b, rtol=1e-6, atol=1e-7)
+    assert np.array_equal(res[0][2], res[1][2]) and np.array_equal(res[0][3], res[1][3])
+
+
+@pytest.mark.parametrize("G,lam,dup", [(1, 0.0, 0), (1, 0.1, 4), (3, 0.05, 3), (7, 0.1, 0)])
+def test_seq_p1_s0_clock_is_a_chain_of_single_rating_steps(G, lam, dup):
+    # P = 1, s = 0: one SEQ clock applies the Section 3.1 rule once per rating, in the
+    # stratified order, each step reading the previous one's result.  The same chain is
+    # built from single-rating SUM clocks (each pinned by the closed form and finite
+    # differences above), one fresh oracle per rating.
+    rng = np.random.default_rng(G + dup)
+    N, M, K, eta = 7, 6, 3, 0.05
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 25, K, dup=dup)
+    o = oracle.Oracle(N, M, K, 1, 0, eta, lam, oracle.SSP_LAZY, oracle.SEQ, strata=G)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(1)
+    L_seq, R_seq = o.get_factors()
+    order = o.export(oracle.X_SEQ_ORDER)
+    o.close()
+    assert np.array_equal(order, seq_order_by_definition(user, item, np.zeros(N, np.int32), 1, G, 1, 0)[0])
+    L, R = L0.copy(), R0.copy()
+    for t in order:
+        one = oracle.Oracle(N, M, K, 1, 0, eta, lam, oracle.SSP_LAZY, oracle.SUM)
+        one.load(user[t:t + 1], item[t:t + 1], val[t:t + 1])
+        one.set_factors(L, R)
+        one.clock(1)
+        L, R = one.get_factors()
+        one.close()
+    # the chain rounds every step to fp32, the SEQ clock keeps the worker's copy in fp64
+    np.testing.assert_allclose(L_seq, L, rtol=0, atol=2e-6)
+    np.testing.assert_allclose(R_seq, R, rtol=0, atol=2e-6)
+
+
+def test_seq_workers_commit_the_sum_of_their_own_chains():
+    # s = 0, P = 3: each worker runs its chain from version c alone; the commit adds every
+    # worker's (copy - view).  Each worker's chain is rebuilt by a P = 1 SEQ oracle that
+    # holds only that worker's ratings, with the worker's users re-numbered so that they
+    # keep their user groups.
+    rng = np.random.default_rng(5)
+    P, G, N, M, K, eta, lam = 3, 2, 12, 8, 2, 0.04, 0.05
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 60, K)
+    o = oracle.Oracle(N, M, K, P, 0, eta, lam, oracle.SSP_LAZY, oracle.SEQ, strata=G)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(1)
+    L_all, R_all = o.get_factors()
+    o.close()
+    L_want, R_want = L0.astype(np.float64).copy(), R0.astype(np.float64).copy()
+    for p in range(P):
+        sel = (user % P) == p
+        # user i = p + P k has user group k mod G; as user k of a P = 1 worker it keeps it
+        Np = N // P
+        one = oracle.Oracle(Np, M, K, 1, 0, eta, lam, oracle.SSP_LAZY, oracle.SEQ, strata=G)
+        one.load(user[sel] // P, item[sel], val[sel])
+        one.set_factors(L0[p::P], R0)
+        one.clock(1)
+        Lp, Rp = one.get_factors()
+        one.close()
+        L_want[p::P] = Lp
+        R_want += Rp.astype(np.float64) - R0
+    np.testing.assert_allclose(L_all, L_want, rtol=0, atol=1e-6)
+    np.testing.assert_allclose(R_all, R_want, rtol=0, atol=1e-6)
+
+
+@pytest.mark.parametrize("P,G", [(1, 1), (1, 4), (4, 4)])
+def test_seq_descent_on_noiseless_planted_data(P, G):
+    rng = np.random.default_rng(3)
+    N, M, K = 30, 20, 3
+    U = rng.standard_normal((N, K)) * 0.5
+    V = rng.standard_normal((M, K)) * 0.5
+    cells = rng.choice(N * M, size=300, replace=False)
+    user, item = (cells // M).astype(np.int32), (cells % M).astype(np.int32)
+    val = np.einsum("nk,nk->n", U[user], V[item]).astype(np.float32)
+    o = oracle.Oracle(N, M, K, P, 0, 0.02, 0.0, oracle.SSP_LAZY, oracle.SEQ, strata=G)
+    o.load(user, item, val)
+    o.set_factors((0.3 * rng.standard_normal((N, K))).astype(np.float32),
+                  (0.3 * rng.standard_normal((M, K))).astype(np.float32))
+    losses = [o.loss()]
+    for _ in range(25):
+        o.clock(1)
+        losses.append(o.loss())
+    o.close()
+    assert all(b < a for a, b in zip(losses, losses[1:]))
+
+
+def test_seq_staleness_and_version_log_follow_the_table_policy():
+    rng = np.random.default_rng(8)
+    N, M, P, s, B = 20, 15, 3, 2, 2
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 120, 2)
+    hist = {}
+    for step in (oracle.ROWMEAN, oracle.SEQ):
+        o = oracle.Oracle(N, M, 2, P, s, 0.01, 0.05, oracle.SSP_LAZY, step, B, 4)
+        o.load(user, item, val)
+        o.set_factors(L0, R0)
+        o.clock(7)
+        hist[step] = (o.export(oracle.X_STALENESS), o.export(oracle.X_VERSION_LOG))
+        o.close()
+    assert np.array_equal(hist[oracle.ROWMEAN][0], hist[oracle.SEQ][0])
+    assert np.array_equal(hist[oracle.ROWMEAN][1], hist[oracle.SEQ][1])
+
+
+def test_seq_argument_errors():
+    for policy in (oracle.SSP_ROW, oracle.ESSP_ROW):
+        with pytest.raises(oracle.OracleError):
+            oracle.Oracle(4, 4, 2, 2, 1, 0.1, 0.0, policy, oracle.SEQ)
+    with pytest.raises(oracle.OracleError):
+        oracle.Oracle(4, 4, 2, 2, 1, 0.1, 0.0, oracle.SSP_LAZY, oracle.SEQ, strata=0)
+    o = oracle.Oracle(4, 4, 2, 2, 1, 0.1, 0.0, oracle.SSP_LAZY, oracle.SUM)
+    o.load(np.array([0], np.int32), np.array([1], np.int32), np.array([1.0], np.float32))
+    with pytest.raises(oracle.OracleError):
+        o.export(oracle.X_SEQ_ORDER)
+    o.close()
