@@ -24,6 +24,14 @@
  *     computed at the worker's view (no read-my-writes inside a clock);
  *   - STEP ROWMEAN (default) divides a row's summed contribution by its number of ratings
  *     in the clock's minibatch (items: across all workers); STEP SUM does not;
+ *   - or STEP SEQ: each worker applies the Section 3.1 rule rating by rating to its own
+ *     copy of the rows it touches (reading its own writes inside the clock), starting
+ *     from its view, and at the clock boundary version c+1 = version c + the sum over
+ *     workers of (copy - view) of the rows each touched.  A worker's ratings run in G
+ *     sub-epochs (PS_MF_OPT_SEQ_STRATA): user group (i div P) mod G, item group j mod G,
+ *     rating (i, j) in sub-epoch (item group - user group) mod G; sub-epochs in order,
+ *     each in (user, item, load index) order.  The strata of one sub-epoch share no row,
+ *     so they run side by side;
  *   - minibatch block of rating (i, j) = splitmix64(seed ^ (i << 32 | j)) mod B, where
  *     splitmix64(x) is one step of the SplitMix64 generator from state x; clock c
  *     processes block c mod B; rows with no rating in the block are unchanged;
@@ -63,7 +71,9 @@ typedef struct ps_mf ps_mf_t;
 /* option keys (ps_mf_set_option); all must be set before ps_mf_load_ratings */
 #define PS_MF_OPT_POLICY 1    /* PS_MF_SSP_LAZY (default), PS_MF_SSP_WORST, PS_MF_ESSP, PS_MF_SSP_ROW,
                                  PS_MF_ESSP_ROW */
-#define PS_MF_OPT_STEP 2      /* PS_MF_STEP_ROWMEAN (default), PS_MF_STEP_SUM */
+#define PS_MF_OPT_STEP 2      /* PS_MF_STEP_ROWMEAN (default), PS_MF_STEP_SUM, PS_MF_STEP_SEQ (table
+                                 policies only: with a per-row policy ps_mf_load_ratings fails
+                                 with PS_MF_EINVAL) */
 #define PS_MF_OPT_MB_BLOCKS 3 /* B >= 1 minibatch blocks (default 1: full shard per clock) */
 #define PS_MF_OPT_MB_SEED 4   /* 64-bit seed of the block hash (default 0) */
 #define PS_MF_OPT_HOST_ONLY 5 /* 1: build, self-check and export the integer layout only; never touch
@@ -91,6 +101,9 @@ typedef struct ps_mf ps_mf_t;
                                   rank is in [16, 256], else none); at most 4096.  A value > 0
                                   with a padded rank outside [16, 256] makes
                                   ps_mf_load_ratings fail with PS_MF_EINVAL */
+#define PS_MF_OPT_SEQ_STRATA 14 /* G: sub-epochs per clock of PS_MF_STEP_SEQ (default 64), in
+                                   [1, 4096].  Part of the semantics: it fixes the order in which
+                                   a worker applies its ratings */
 
 /* Views (Section 3.2 SSP condition; Section 4 ESSPTable).  The table-level policies give
    worker p at clock c one whole version v = max(0, c - d):
@@ -114,6 +127,7 @@ typedef struct ps_mf ps_mf_t;
 
 #define PS_MF_STEP_ROWMEAN 0
 #define PS_MF_STEP_SUM 1
+#define PS_MF_STEP_SEQ 2
 
 /* index kinds (ps_mf_export_index) */
 #define PS_MF_IDX_OWNER 0       /* int32 [users]: worker of each user */
@@ -141,6 +155,9 @@ typedef struct ps_mf ps_mf_t;
                                    last clock: user rows (read by their owner's client), then
                                    client 0's item rows, client 1's, ...; -1 = never read.
                                    Other policies: length 0 */
+#define PS_MF_IDX_SEQ_ORDER 10  /* int64 [nnz_b] under PS_MF_STEP_SEQ: load indices of block b in the
+                                   order the workers apply them, (sub-epoch, worker, user group,
+                                   user, item, load index); other steps: PS_MF_EINVAL */
 
 /* kernel ids (ps_mf_kernel_time) */
 #define PS_MF_KERNEL_SWEEP 0  /* residual, dL segment-sum and dR accumulation of one clock */

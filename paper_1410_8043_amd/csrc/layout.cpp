@@ -11,6 +11,7 @@
 #include <new>
 #include <numeric>
 #include <thread>
+#include <tuple>
 
 namespace psmf {
 
@@ -736,6 +737,89 @@ void build_dense(const LayoutParams &p, const BlockLayout &L, const std::vector<
   DU.nnz = DI.nnz = nd;
 }
 
+// The sequential step's order of one block (see SeqSet).
+void build_seq(const LayoutParams &p, BlockLayout &L, const std::vector<int32_t> &ent_user) {
+  const int64_t nb = L.nnz, M = p.items, G = p.seq_groups, P = p.workers;
+  SeqSet &S = L.seq;
+  S.G = static_cast<int32_t>(G);
+  auto ugroup = [&](int64_t e) { return (static_cast<int64_t>(ent_user[e]) / P) % G; };
+  auto epoch = [&](int64_t e) { return ((L.col[e] % G) - ugroup(e) + G) % G; };
+  // canonical positions, stably by user group, then by (sub-epoch, worker)
+  std::vector<int64_t> a(static_cast<size_t>(nb)), b(static_cast<size_t>(nb));
+  std::iota(a.begin(), a.end(), int64_t(0));
+  counting_pass(a, b, G, ugroup);
+  counting_pass(b, a, G * P, [&](int64_t e) { return epoch(e) * P + p.owner[ent_user[e]]; });
+  std::vector<int64_t>().swap(b);
+  S.user.resize(static_cast<size_t>(nb));
+  S.item.resize(static_cast<size_t>(nb));
+  S.val.resize(static_cast<size_t>(nb));
+  S.flag.assign(static_cast<size_t>(nb), 0);
+  S.canon.resize(static_cast<size_t>(nb));
+  for (int64_t x = 0; x < nb; ++x) {
+    const int64_t e = a[x];
+    S.user[x] = ent_user[e];
+    S.item[x] = L.col[e];
+    S.val[x] = L.val[e];
+    S.canon[x] = static_cast<int32_t>(e);
+  }
+  // chains: maximal runs of one (sub-epoch, worker, user group)
+  S.epoch_chain.assign(static_cast<size_t>(G) + 1, 0);
+  S.chain_beg.clear();
+  S.chain_worker.clear();
+  int64_t prev_key = -1;
+  for (int64_t x = 0; x < nb; ++x) {
+    const int64_t e = a[x];
+    const int64_t key = (epoch(e) * P + p.owner[ent_user[e]]) * G + ugroup(e);
+    if (key != prev_key) {
+      S.chain_beg.push_back(x);
+      S.chain_worker.push_back(p.owner[ent_user[e]]);
+      S.epoch_chain[static_cast<size_t>(epoch(e)) + 1] += 1;
+      prev_key = key;
+    }
+  }
+  S.chain_beg.push_back(nb);
+  for (int64_t t = 0; t < G; ++t) S.epoch_chain[t + 1] += S.epoch_chain[t];
+  const int64_t nch = static_cast<int64_t>(S.chain_worker.size());
+  // L flags on the first rating of each user run: the user's first and last run of the clock
+  std::vector<uint8_t> seen(static_cast<size_t>(p.users), 0);
+  for (int64_t ch = 0; ch < nch; ++ch)
+    for (int64_t x = S.chain_beg[ch]; x < S.chain_beg[ch + 1]; ++x)
+      if (x == S.chain_beg[ch] || S.user[x] != S.user[x - 1])
+        if (!seen[S.user[x]]) {
+          seen[S.user[x]] = 1;
+          S.flag[x] |= kSeqFirstL;
+        }
+  std::fill(seen.begin(), seen.end(), 0);
+  for (int64_t ch = nch - 1; ch >= 0; --ch)
+    for (int64_t x = S.chain_beg[ch + 1] - 1; x >= S.chain_beg[ch]; --x)
+      if ((x == S.chain_beg[ch] || S.user[x] != S.user[x - 1]) && !seen[S.user[x]]) {  // a run's start
+        seen[S.user[x]] = 1;
+        S.flag[x] |= kSeqLastL;
+      }
+  // R flags: each worker's first rating of an item, scanning the worker's chains in order;
+  // the (item, worker) pairs give the item worker lists, ascending in the worker
+  std::vector<std::vector<int64_t>> chains_of(static_cast<size_t>(P));
+  for (int64_t ch = 0; ch < nch; ++ch) chains_of[S.chain_worker[ch]].push_back(ch);
+  std::vector<int32_t> stamp(static_cast<size_t>(M), -1);
+  std::vector<int64_t> pair_item;
+  std::vector<int32_t> pair_worker;
+  for (int64_t w = 0; w < P; ++w)
+    for (int64_t ch : chains_of[w])
+      for (int64_t x = S.chain_beg[ch]; x < S.chain_beg[ch + 1]; ++x)
+        if (stamp[S.item[x]] != w) {
+          stamp[S.item[x]] = static_cast<int32_t>(w);
+          S.flag[x] |= kSeqFirstR;
+          pair_item.push_back(S.item[x]);
+          pair_worker.push_back(static_cast<int32_t>(w));
+        }
+  S.item_wptr.assign(static_cast<size_t>(M) + 1, 0);
+  for (int64_t j : pair_item) S.item_wptr[j + 1] += 1;
+  for (int64_t j = 0; j < M; ++j) S.item_wptr[j + 1] += S.item_wptr[j];
+  S.item_workers.resize(pair_item.size());
+  std::vector<int64_t> fill(S.item_wptr.begin(), S.item_wptr.end() - 1);
+  for (size_t q = 0; q < pair_item.size(); ++q) S.item_workers[fill[pair_item[q]]++] = pair_worker[q];
+}
+
 }  // namespace
 
 int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item, const float *val, int64_t n,
@@ -864,6 +948,10 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
       }
       L.row_ptr.assign(static_cast<size_t>(N) + 1, 0);
       for (int64_t i = 0; i < N; ++i) L.row_ptr[i + 1] = L.row_ptr[i] + L.ucount[i];
+      if (p.seq_groups > 0) {
+        build_seq(p, L, ent_user);
+        continue;
+      }
 
       // ---- dense tiles (matrix-core cells), then cells (staged through LDS) and units (the
       // rest) for the other ratings.  Heavy users' remaining ratings all go to cells; with
@@ -1171,10 +1259,89 @@ int check_dense_twins(const DenseSet &U, const DenseSet &I, std::string &err) {
   return 0;
 }
 
+// the sequential step's order against its definition, recomputed entry by entry
+int check_seq(const LayoutParams &p, const BlockLayout &L, std::string &err) {
+  const SeqSet &S = L.seq;
+  const int64_t nb = L.nnz, N = p.users, M = p.items, G = p.seq_groups, P = p.workers;
+  auto bad = [&](const std::string &what) {
+    err = "sequential order: " + what;
+    return -1;
+  };
+  if (S.G != G || static_cast<int64_t>(S.user.size()) != nb || static_cast<int64_t>(S.canon.size()) != nb ||
+      S.epoch_chain.size() != static_cast<size_t>(G) + 1 || S.chain_beg.size() != S.chain_worker.size() + 1)
+    return bad("array sizes");
+  std::vector<int32_t> cuser(static_cast<size_t>(nb));
+  for (int64_t i = 0; i < N; ++i)
+    for (int64_t e = L.row_ptr[i]; e < L.row_ptr[i + 1]; ++e) cuser[e] = static_cast<int32_t>(i);
+  std::vector<uint8_t> used(static_cast<size_t>(nb), 0);
+  auto skey = [&](int64_t x) {  // (sub-epoch, worker, user group, canonical position)
+    const int64_t i = S.user[x], j = S.item[x], ug = (i / P) % G;
+    return std::make_tuple(((j % G) - ug + G) % G, static_cast<int64_t>(p.owner[i]), ug, static_cast<int64_t>(S.canon[x]));
+  };
+  for (int64_t x = 0; x < nb; ++x) {
+    const int64_t e = S.canon[x];
+    if (e < 0 || e >= nb || used[e]) return bad("canonical positions are not a permutation");
+    used[e] = 1;
+    if (S.user[x] != cuser[e] || S.item[x] != L.col[e] || std::memcmp(&S.val[x], &L.val[e], sizeof(float)) != 0)
+      return bad("rating " + std::to_string(x) + " differs from its canonical entry");
+    if (x > 0 && !(skey(x - 1) < skey(x))) return bad("not sorted at " + std::to_string(x));
+  }
+  const int64_t nch = static_cast<int64_t>(S.chain_worker.size());
+  if (S.chain_beg[0] != 0 || S.chain_beg[nch] != nb || S.epoch_chain[0] != 0 || S.epoch_chain[G] != nch)
+    return bad("chain bounds");
+  for (int64_t t = 0; t < G; ++t)
+    for (int64_t ch = S.epoch_chain[t]; ch < S.epoch_chain[t + 1]; ++ch) {
+      const int64_t lo = S.chain_beg[ch], hi = S.chain_beg[ch + 1];
+      if (hi <= lo) return bad("empty chain");
+      for (int64_t x = lo; x < hi; ++x)
+        if (std::get<0>(skey(x)) != t || std::get<1>(skey(x)) != S.chain_worker[ch] ||
+            std::get<2>(skey(x)) != std::get<2>(skey(lo)))
+          return bad("chain " + std::to_string(ch) + " mixes strata");
+      if (ch > S.epoch_chain[t] && std::get<1>(skey(lo)) == std::get<1>(skey(lo - 1)) &&
+          std::get<2>(skey(lo)) == std::get<2>(skey(lo - 1)))
+        return bad("chain " + std::to_string(ch) + " is not maximal");
+    }
+  // flags by brute force: first / last run of each user, first (worker, item) in order
+  std::vector<int64_t> first_run(static_cast<size_t>(N), -1), last_run(static_cast<size_t>(N), -1);
+  std::vector<std::vector<int64_t>> first_r(static_cast<size_t>(M));
+  for (int64_t ch = 0; ch < nch; ++ch)
+    for (int64_t x = S.chain_beg[ch]; x < S.chain_beg[ch + 1]; ++x) {
+      const int32_t i = S.user[x];
+      if (x == S.chain_beg[ch] || S.user[x - 1] != i) {
+        if (first_run[i] < 0) first_run[i] = x;
+        last_run[i] = x;
+      }
+      bool seen_before = false;
+      for (int64_t y : first_r[S.item[x]])
+        if (p.owner[S.user[y]] == p.owner[i]) seen_before = true;
+      if (!seen_before) first_r[S.item[x]].push_back(x);
+    }
+  std::vector<uint8_t> want(static_cast<size_t>(nb), 0);
+  for (int64_t i = 0; i < N; ++i) {
+    if (first_run[i] >= 0) want[first_run[i]] |= kSeqFirstL;
+    if (last_run[i] >= 0) want[last_run[i]] |= kSeqLastL;
+  }
+  for (int64_t j = 0; j < M; ++j)
+    for (int64_t x : first_r[j]) want[x] |= kSeqFirstR;
+  for (int64_t x = 0; x < nb; ++x)
+    if (want[x] != S.flag[x]) return bad("flags of rating " + std::to_string(x));
+  if (S.item_wptr.size() != static_cast<size_t>(M) + 1) return bad("item worker pointers");
+  for (int64_t j = 0; j < M; ++j) {
+    std::vector<int32_t> w;
+    for (int64_t x : first_r[j]) w.push_back(p.owner[S.user[x]]);
+    std::sort(w.begin(), w.end());
+    if (S.item_wptr[j + 1] - S.item_wptr[j] != static_cast<int64_t>(w.size()) ||
+        !std::equal(w.begin(), w.end(), S.item_workers.begin() + S.item_wptr[j]))
+      return bad("workers of item " + std::to_string(j));
+  }
+  return 0;
+}
+
 }  // namespace
 
 int check_layout(const LayoutParams &p, const BlockLayout &L, std::string &err) {
   const int64_t N = p.users, M = p.items;
+  if (p.seq_groups > 0) return check_seq(p, L, err);
   std::vector<int32_t> ucls(static_cast<size_t>(N));
   for (int64_t i = 0; i < N; ++i) ucls[i] = p.cls_of_worker[p.owner[i]];
   std::vector<Triple> by_user, by_item;

@@ -106,6 +106,30 @@ struct DenseSet {
   int64_t nnz = 0;                     // ratings covered
 };
 
+// The sequential step (each worker applies its ratings one by one to its own copies of the
+// rows): the block's ratings in the order the workers apply them.  Worker p's ratings run in
+// G sub-epochs; in sub-epoch t the stratum (user group g, item group (g + t) mod G) of every
+// g, each in canonical order -- user group (i div P) mod G, item group j mod G.  A chain is
+// one (sub-epoch, worker, user group) stratum with ratings; chains are stored by sub-epoch,
+// and the strata of one sub-epoch share no row, so its chains run side by side.
+// Flags of a rating: kSeqFirstL / kSeqLastL on the first rating of a user's run inside a
+// chain when the run is the user's first / last of the clock (L_i is read from the view /
+// the run ends with the commit of L_i); kSeqFirstR when it is worker p's first rating of
+// item j in the clock (R_j is read from the view, later ones from the worker's copy).
+constexpr uint8_t kSeqFirstL = 1, kSeqLastL = 2, kSeqFirstR = 4;
+struct SeqSet {
+  int32_t G = 0;
+  std::vector<int64_t> epoch_chain;   // [G + 1]: the chains of sub-epoch t
+  std::vector<int64_t> chain_beg;     // [nchains + 1] into the rating arrays
+  std::vector<int32_t> chain_worker;  // [nchains]
+  std::vector<int32_t> user, item;    // [nnz] in application order
+  std::vector<float> val;
+  std::vector<uint8_t> flag;
+  std::vector<int32_t> canon;         // [nnz] canonical position of each rating (host only)
+  std::vector<int64_t> item_wptr;     // [items + 1]
+  std::vector<int32_t> item_workers;  // the workers with a rating of item j, ascending
+};
+
 struct BlockLayout {
   int64_t nnz = 0;
   // ratings of the block in canonical (user, item, load index) order
@@ -119,6 +143,7 @@ struct BlockLayout {
   UnitSet by_user, by_item;
   CellSet cells_user, cells_item;
   DenseSet dense_user, dense_item;
+  SeqSet seq;
   int64_t partial_rows_user = 0, partial_rows_item = 0;  // rows of x_pp (units and cells)
 };
 
@@ -144,6 +169,9 @@ struct LayoutParams {
   int32_t dense_target = 1024;      // about this many dense cells per direction
   int32_t min_cell_steps = 4;       // runs of cells and dense cells are not cut below this many
                                     // steps (each cut costs every row of the cell a partial row)
+  int32_t workers = 1;              // P
+  int32_t seq_groups = 0;           // G > 0: build the sequential step's order (SeqSet) instead of
+                                    // units, cells and dense tiles
 };
 
 // Validates the COO input (EINVAL message in err) and fills one BlockLayout per block.
@@ -155,7 +183,10 @@ int build_layout(const LayoutParams &p, const int32_t *user, const int32_t *item
 // the units, cells and dense cells together hold every entry exactly once (same stationary row,
 // gathered row and value), every unit and cell reads the ring slot of its ratings' user
 // class (wave-uniform for units), padding is (row 0, value 0), and the partial rows of
-// each x are written exactly once each.  Returns 0, or -1 with err naming the first fault.
+// each x are written exactly once each.  For the sequential step: the order holds every
+// entry once, sorted by (sub-epoch, worker, user group, canonical position), chains are
+// maximal runs of one stratum, and the flags and item worker lists match their
+// definitions.  Returns 0, or -1 with err naming the first fault.
 int check_layout(const LayoutParams &p, const BlockLayout &L, std::string &err);
 
 }  // namespace psmf

@@ -955,6 +955,127 @@ __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, 
     commit_item(ca, static_cast<int64_t>(blockIdx.x) - grid_users, red);
 }
 
+// ------------------------------------------------------------------ sequential step
+// Under STEP_SEQ every worker applies the Section 3.1 rule rating by rating to its own
+// copies of the rows.  A chain (one stratum: sub-epoch, worker, user group) is one lane
+// group; the chains of one sub-epoch share no row and run side by side in one launch, the
+// sub-epochs one launch after another.  Inside a chain the current user's row stays in
+// registers for the user's run; each rating loads the item row from the worker's copy
+// (from the view on the worker's first rating of the item in the clock), updates both rows
+// and stores the item row back.  A user row leaves its run in the work copy, or, after the
+// user's last run of the clock, as L^{c+1}_i = L^c_i + (copy - L^v_i) in the new slot.
+struct SeqArgs {
+  const int64_t *chain_beg;
+  const int32_t *chain_worker;
+  const int32_t *user, *item;
+  const float *val;
+  const uint8_t *flag;
+  const int32_t *wcls, *cls_slot;  // worker class, ring slot of each class's view
+  float *ring;
+  int64_t slot_stride, r_off;
+  int32_t slot_c, slot_n;
+  float *lwork;                    // [users, Kp] the user rows between their runs
+  float *rwork;                    // [P, items, Kp] each worker's copy of the item rows
+  int64_t rwork_stride;            // items * Kp
+  float eta, lambda;
+};
+
+template <int G, int E>
+__device__ __forceinline__ void seq_leave_user(const SeqArgs &a, int32_t i, uint8_t f, const float (&x)[E],
+                                               const float *Lv, int g) {
+  constexpr int Kp = G * E;
+  const int64_t off = static_cast<int64_t>(i) * Kp;
+  if (f & psmf::kSeqLastL) {
+    float lc[E], lv[E], o[E];
+    load_row<G, E>(lc, a.ring + a.slot_c * a.slot_stride + off, g);
+    load_row<G, E>(lv, Lv + off, g);
+#pragma unroll
+    for (int k = 0; k < E; ++k) o[k] = lc[k] + (x[k] - lv[k]);
+    store_row<G, E>(a.ring + a.slot_n * a.slot_stride + off, o, g);
+  } else {
+    store_row<G, E>(a.lwork + off, x, g);
+  }
+}
+
+template <int G, int E>
+__global__ __launch_bounds__(kBlock) void k_seq(SeqArgs a, int64_t c0, int64_t c1) {
+  constexpr int Kp = G * E;
+  const int g = static_cast<int>(threadIdx.x) % G;
+  const int64_t ch = c0 + (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / G;
+  if (ch >= c1) return;  // uniform over the lane group
+  const int64_t beg = a.chain_beg[ch], end = a.chain_beg[ch + 1];
+  const int32_t p = a.chain_worker[ch];
+  const float *Lv = a.ring + a.cls_slot[a.wcls[p]] * a.slot_stride;
+  const float *Rv = Lv + a.r_off;
+  float *Rw = a.rwork + static_cast<int64_t>(p) * a.rwork_stride;
+  float x[E];
+  int32_t cur = -1;
+  uint8_t fcur = 0;
+  for (int64_t n = beg; n < end; ++n) {
+    const int32_t i = a.user[n], j = a.item[n];
+    const float r = a.val[n];
+    const uint8_t f = a.flag[n];
+    if (i != cur) {
+      if (cur >= 0) seq_leave_user<G, E>(a, cur, fcur, x, Lv, g);
+      load_row<G, E>(x, ((f & psmf::kSeqFirstL) ? Lv : a.lwork) + static_cast<int64_t>(i) * Kp, g);
+      cur = i;
+      fcur = f;
+    }
+    float y[E];
+    load_row<G, E>(y, ((f & psmf::kSeqFirstR) ? Rv : Rw) + static_cast<int64_t>(j) * Kp, g);
+    const float e = residual<G, E>(x, y, r);
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      const float xl = x[k], yl = y[k];
+      x[k] = fmaf(a.eta, fmaf(e, yl, -a.lambda * xl), xl);
+      y[k] = fmaf(a.eta, fmaf(e, xl, -a.lambda * yl), yl);
+    }
+    store_row<G, E>(Rw + static_cast<int64_t>(j) * Kp, y, g);
+  }
+  if (cur >= 0) seq_leave_user<G, E>(a, cur, fcur, x, Lv, g);
+}
+
+struct SeqCommitArgs {
+  float *ring;
+  int64_t slot_stride, r_off;
+  int64_t users, items;
+  int32_t Kp;
+  int32_t slot_c, slot_n;
+  const int32_t *ucount;       // [users] ratings in the block (users without one keep L^c_i)
+  const int64_t *item_wptr;    // [items + 1]
+  const int32_t *item_workers; // the workers with a rating of each item
+  const int32_t *wcls, *cls_slot;
+  const float *rwork;
+  int64_t rwork_stride;
+};
+
+// One thread per float4 of a row: users without a rating in the block keep L^c_i (copied
+// when the new slot differs); R^{c+1}_j = R^c_j + sum over the workers with a rating of j
+// of (copy - R^{v(p)}_j).
+__global__ __launch_bounds__(kBlock) void k_seq_commit(SeqCommitArgs a) {
+  const int64_t q4 = a.Kp / 4;
+  int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  float4 *ring4 = reinterpret_cast<float4 *>(a.ring);
+  const int64_t ss4 = a.slot_stride / 4;
+  if (idx < a.users * q4) {
+    if (a.ucount[idx / q4] == 0 && a.slot_n != a.slot_c) ring4[a.slot_n * ss4 + idx] = ring4[a.slot_c * ss4 + idx];
+    return;
+  }
+  idx -= a.users * q4;
+  if (idx >= a.items * q4) return;
+  const int64_t j = idx / q4, r4 = a.r_off / 4 + idx;
+  float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
+  const float4 *rw4 = reinterpret_cast<const float4 *>(a.rwork);
+  for (int64_t q = a.item_wptr[j]; q < a.item_wptr[j + 1]; ++q) {
+    const int32_t w = a.item_workers[q];
+    const float4 loc = rw4[w * (a.rwork_stride / 4) + idx];
+    const float4 v = ring4[a.cls_slot[a.wcls[w]] * ss4 + r4];
+    d.x += loc.x - v.x; d.y += loc.y - v.y; d.z += loc.z - v.z; d.w += loc.w - v.w;
+  }
+  const float4 rc = ring4[a.slot_c * ss4 + r4];
+  ring4[a.slot_n * ss4 + r4] = make_float4(rc.x + d.x, rc.y + d.y, rc.z + d.z, rc.w + d.w);
+}
+
 // ------------------------------------------------------------------ kernel dispatch on Kp
 // lane-group shape per padded rank: G lanes x E floats, G <= 16 so that a group sits in
 // one DPP row, E a multiple of 4 for float4 access
@@ -1040,6 +1161,15 @@ struct LaunchUnits {
 // padded ranks with a dense (MFMA) cell kernel
 bool dense_supported(int Kp) { return Kp >= 16 && Kp <= 256; }
 
+template <int G, int E>
+struct LaunchSeq {
+  static hipError_t run(const SeqArgs &a, int64_t c0, int64_t c1, hipStream_t st) {
+    const int64_t groups = kBlock / G, grid = (c1 - c0 + groups - 1) / groups;
+    hipLaunchKernelGGL((k_seq<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a, c0, c1);
+    return hipGetLastError();
+  }
+};
+
 template <bool FromE>
 hipError_t launch_dense(int Kp, const DenseArgs &a, int64_t grid, hipStream_t st) {
   const dim3 gd(static_cast<unsigned>(grid)), bd(kDenseThreads);
@@ -1093,6 +1223,14 @@ struct DeviceDense {
   float *eval = nullptr;  // item-major set: the residuals the user-major pass stores each clock
 };
 
+struct DeviceSeq {
+  std::vector<int64_t> epoch_chain;  // host copy: the chains of each sub-epoch
+  int64_t *chain_beg = nullptr, *item_wptr = nullptr;
+  int32_t *chain_worker = nullptr, *user = nullptr, *item = nullptr, *item_workers = nullptr;
+  float *val = nullptr;
+  uint8_t *flag = nullptr;
+};
+
 struct DeviceBlock {
   int64_t nnz = 0, loss_grid = 0;
   int32_t *ucount = nullptr, *icount = nullptr, *icount_cls = nullptr;
@@ -1104,6 +1242,7 @@ struct DeviceBlock {
   DeviceUnits by_user, by_item;
   DeviceCells cells_user, cells_item;
   DeviceDense dense_user, dense_item;
+  DeviceSeq seq;
 };
 
 struct ps_mf {
@@ -1120,6 +1259,7 @@ struct ps_mf {
   bool cells = true;             // stage the dense part (heavy users) through LDS
   int64_t heavy_min = -1;        // ratings from which a user goes to the cells (-1: automatic)
   int32_t dense_min = -1;        // ratings from which a 64 x 64 tile goes to the MFMA cells (-1: automatic, 0: none)
+  int32_t seq_groups = 64;       // sub-epochs of the sequential step
   std::vector<int32_t> owner;
   // host state
   bool loaded = false, has_factors = false;
@@ -1148,6 +1288,8 @@ struct ps_mf {
   unsigned long long *stale = nullptr;
   int32_t *ucls = nullptr;
   int32_t *slot_table = nullptr;  // [(2s+1) * nclass]
+  int32_t *wcls = nullptr;        // [P] class of each worker
+  float *lwork = nullptr, *rwork = nullptr;  // sequential step: user rows between runs, workers' item rows
   double *loss_partial = nullptr;
   int64_t loss_partial_len = 0;
   double *loss_out = nullptr;
@@ -1396,7 +1538,70 @@ int record_end(ps_mf_t *h, int kernel, hipEvent_t a) {
   return PS_MF_OK;
 }
 
+// One clock of the sequential step: the sub-epochs one launch after another, then the
+// commit of R and of the untouched user rows.
+int seq_clock(ps_mf_t *h) {
+  const int64_t c = h->clock;
+  const int b = static_cast<int>(c % h->B);
+  const int32_t S1 = h->s + 1;
+  const DeviceBlock &db = h->dblocks[b];
+  const DeviceSeq &q = db.seq;
+  SeqArgs a{};
+  a.chain_beg = q.chain_beg;
+  a.chain_worker = q.chain_worker;
+  a.user = q.user;
+  a.item = q.item;
+  a.val = q.val;
+  a.flag = q.flag;
+  a.wcls = h->wcls;
+  a.cls_slot = h->slot_table + table_row(h, c) * h->nclass;
+  a.ring = h->ring;
+  a.slot_stride = (h->N + h->M) * h->Kp;
+  a.r_off = h->N * h->Kp;
+  a.slot_c = static_cast<int32_t>(c % S1);
+  a.slot_n = static_cast<int32_t>((c + 1) % S1);
+  a.lwork = h->lwork;
+  a.rwork = h->rwork;
+  a.rwork_stride = h->M * h->Kp;
+  a.eta = h->eta;
+  a.lambda = h->lambda;
+  hipEvent_t ev = nullptr;
+  int rc = record(h, &ev);
+  if (rc) return rc;
+  for (int32_t t = 0; t < h->seq_groups; ++t) {
+    const int64_t c0 = q.epoch_chain[t], c1 = q.epoch_chain[t + 1];
+    if (c1 > c0) HIP_TRY(h, dispatch<LaunchSeq>(h->Kp, a, c0, c1, h->stream));
+  }
+  if ((rc = record_end(h, PS_MF_KERNEL_SWEEP, ev))) return rc;
+  if ((rc = record(h, &ev))) return rc;
+  SeqCommitArgs ca{};
+  ca.ring = h->ring;
+  ca.slot_stride = a.slot_stride;
+  ca.r_off = a.r_off;
+  ca.users = h->N;
+  ca.items = h->M;
+  ca.Kp = h->Kp;
+  ca.slot_c = a.slot_c;
+  ca.slot_n = a.slot_n;
+  ca.ucount = db.ucount;
+  ca.item_wptr = q.item_wptr;
+  ca.item_workers = q.item_workers;
+  ca.wcls = h->wcls;
+  ca.cls_slot = a.cls_slot;
+  ca.rwork = h->rwork;
+  ca.rwork_stride = a.rwork_stride;
+  const int64_t threads = (h->N + h->M) * (h->Kp / 4);
+  hipLaunchKernelGGL(k_seq_commit, dim3(static_cast<unsigned>((threads + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                     h->stream, ca);
+  HIP_TRY(h, hipGetLastError());
+  if ((rc = record_end(h, PS_MF_KERNEL_COMMIT, ev))) return rc;
+  for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_version(h, p, c));
+  h->clock = c + 1;
+  return PS_MF_OK;
+}
+
 int one_clock(ps_mf_t *h) {
+  if (h->step == PS_MF_STEP_SEQ) return seq_clock(h);
   const int64_t c = h->clock;
   const int b = static_cast<int>(c % h->B);
   const int32_t S1 = h->s + 1;
@@ -1566,7 +1771,8 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
       h->policy = static_cast<int32_t>(value);
       return PS_MF_OK;
     case PS_MF_OPT_STEP:
-      if (value != PS_MF_STEP_ROWMEAN && value != PS_MF_STEP_SUM) return fail(h, PS_MF_EINVAL, "unknown step %lld", (long long)value);
+      if (value != PS_MF_STEP_ROWMEAN && value != PS_MF_STEP_SUM && value != PS_MF_STEP_SEQ)
+        return fail(h, PS_MF_EINVAL, "unknown step %lld", (long long)value);
       h->step = static_cast<int32_t>(value);
       return PS_MF_OK;
     case PS_MF_OPT_MB_BLOCKS:
@@ -1609,6 +1815,10 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
         return fail(h, PS_MF_EINVAL, "dense tile threshold must be in [-1, %d]", psmf::kDenseTile);
       h->dense_min = static_cast<int32_t>(value);
       return PS_MF_OK;
+    case PS_MF_OPT_SEQ_STRATA:
+      if (value < 1 || value > 4096) return fail(h, PS_MF_EINVAL, "sub-epochs must be in [1, 4096]");
+      h->seq_groups = static_cast<int32_t>(value);
+      return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
   }
@@ -1643,6 +1853,9 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   if (h->loaded) return fail(h, PS_MF_ESTATE, "ratings are already loaded");
   if (n < 0 || (n > 0 && (!user || !item || !value))) return fail(h, PS_MF_EINVAL, "bad rating arrays");
   if (n > 0x7fffffffLL) return fail(h, PS_MF_EINVAL, "at most 2^31-1 ratings");
+  const bool seq = h->step == PS_MF_STEP_SEQ;
+  if (seq && per_row_policy(h))
+    return fail(h, PS_MF_EINVAL, "the sequential step reads one view per worker and clock: use a table policy");
   if (h->owner.empty()) {
     h->owner.resize(static_cast<size_t>(h->N));
     for (int64_t i = 0; i < h->N; ++i) h->owner[i] = static_cast<int32_t>(i % h->P);
@@ -1680,6 +1893,12 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
     return fail(h, PS_MF_EINVAL, "dense tiles need a padded rank in [16, 256], not %d", h->Kp);
   lp.dense_min = h->dense_min >= 0 ? h->dense_min : (dense_supported(h->Kp) ? kDenseAuto : 0);
   lp.dense_target = PS_MF_DENSE_CELLS;
+  lp.workers = h->P;
+  if (seq) {
+    lp.seq_groups = h->seq_groups;
+    lp.dense_min = 0;
+    lp.cell_rows = lp.cell_groups = 0;
+  }
   if (h->cells) {
     // automatic hot-item sub-tiles: none next to dense tiles, else one (on the 100M-rating
     // K = 128 workload: 1 measured best among 0..4 without dense tiles; with them the
@@ -1716,12 +1935,23 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
     d.nnz = L.nnz;
     if ((r = upload(h, &d.ucount, L.ucount)) || (r = upload(h, &d.icount, L.icount)) ||
         (r = upload(h, &d.icount_cls, L.icount_cls)) || (r = upload(h, &d.col, L.col)) ||
-        (r = upload(h, &d.val, L.val)) ||
-        (r = upload_units(h, d.by_user, L.by_user)) || (r = upload_units(h, d.by_item, L.by_item)) ||
-        (r = upload_cells(h, d.cells_user, L.cells_user)) || (r = upload_cells(h, d.cells_item, L.cells_item)) ||
-        (r = upload_dense(h, d.dense_user, L.dense_user, true)) ||
-        (r = upload_dense(h, d.dense_item, L.dense_item, false)))
+        (r = upload(h, &d.val, L.val)))
       return undo(r);
+    if (seq) {
+      const psmf::SeqSet &S = L.seq;
+      DeviceSeq &q = d.seq;
+      q.epoch_chain = S.epoch_chain;
+      if ((r = upload(h, &q.chain_beg, S.chain_beg)) || (r = upload(h, &q.chain_worker, S.chain_worker)) ||
+          (r = upload(h, &q.user, S.user)) || (r = upload(h, &q.item, S.item)) || (r = upload(h, &q.val, S.val)) ||
+          (r = upload(h, &q.flag, S.flag)) || (r = upload(h, &q.item_wptr, S.item_wptr)) ||
+          (r = upload(h, &q.item_workers, S.item_workers)))
+        return undo(r);
+    } else if ((r = upload_units(h, d.by_user, L.by_user)) || (r = upload_units(h, d.by_item, L.by_item)) ||
+               (r = upload_cells(h, d.cells_user, L.cells_user)) || (r = upload_cells(h, d.cells_item, L.cells_item)) ||
+               (r = upload_dense(h, d.dense_user, L.dense_user, true)) ||
+               (r = upload_dense(h, d.dense_item, L.dense_item, false))) {
+      return undo(r);
+    }
     // partial rows of units and cells, + the row the padding units write
     max_units_u = std::max<int64_t>(max_units_u, L.partial_rows_user + 1);
     max_units_i = std::max<int64_t>(max_units_i, L.partial_rows_item + 1);
@@ -1772,6 +2002,14 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
       table[row * h->nclass + q] = static_cast<int32_t>(view_version(h, rep[q] < 0 ? 0 : rep[q], c) % (h->s + 1));
   }
   if ((r = upload(h, &h->slot_table, table))) return undo(r);
+  if ((r = upload(h, &h->wcls, h->cls_of_worker))) return undo(r);
+  if (seq) {
+    // the users' rows between their runs and every worker's copy of the item rows
+    const size_t rw = static_cast<size_t>(h->P) * static_cast<size_t>(h->M) * static_cast<size_t>(h->Kp);
+    if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->lwork), static_cast<size_t>(h->N * h->Kp) * sizeof(float))) ||
+        (r = dev_alloc(h, reinterpret_cast<void **>(&h->rwork), rw * sizeof(float))))
+      return undo(r);
+  }
   return PS_MF_OK;
 }
 
@@ -1886,6 +2124,8 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     if (!h->loaded) return fail(h, PS_MF_ESTATE, "no ratings loaded");
     if (block < 0 || block >= h->B) return fail(h, PS_MF_EINVAL, "block %d out of range", block);
   }
+  if (kind == PS_MF_IDX_SEQ_ORDER && h->step != PS_MF_STEP_SEQ)
+    return fail(h, PS_MF_EINVAL, "the order of the sequential step exists under PS_MF_STEP_SEQ only");
   if (kind == PS_MF_IDX_OWNER && h->owner.empty()) {
     h->owner.resize(static_cast<size_t>(h->N));
     for (int64_t i = 0; i < h->N; ++i) h->owner[i] = static_cast<int32_t>(i % h->P);
@@ -1910,7 +2150,12 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     split[6] = L.partial_rows_user;
     split[7] = L.partial_rows_item;
   }
-  std::vector<int64_t> stale, rowver;
+  std::vector<int64_t> stale, rowver, seq_order;
+  if (kind == PS_MF_IDX_SEQ_ORDER) {
+    const psmf::BlockLayout &L = h->layout[block];
+    seq_order.resize(L.seq.canon.size());
+    for (size_t x = 0; x < seq_order.size(); ++x) seq_order[x] = L.perm[L.seq.canon[x]];
+  }
   if (kind == PS_MF_IDX_STALENESS) {
     stale.assign(static_cast<size_t>(h->s) + 1, 0);
     if (per_row_policy(h)) {
@@ -1950,6 +2195,7 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     case PS_MF_IDX_ITEM_COUNT: src = h->layout[block].icount.data(); esz = 4; n = h->M; break;
     case PS_MF_IDX_VERSION_LOG: src = h->vlog.data(); esz = 8; n = static_cast<int64_t>(h->vlog.size()); break;
     case PS_MF_IDX_SPLIT: src = split; esz = 8; n = 8; break;
+    case PS_MF_IDX_SEQ_ORDER: src = seq_order.data(); esz = 8; n = static_cast<int64_t>(seq_order.size()); break;
     default: return fail(h, PS_MF_EINVAL, "unknown index kind %d", kind);
   }
   *len = n;

@@ -259,3 +259,63 @@ def test_per_row_policies_on_a_host_only_handle(policy):
         assert e.value.code == ps_mf.EINVAL
     finally:
         ps_mf.ps_mf_destroy(h)
+
+
+# ---------------------------------------------------------------- sequential step (STEP_SEQ)
+@pytest.mark.parametrize("P,G,B,policy,custom_owner", [(1, 1, 1, ps_mf.SSP_LAZY, False), (3, 4, 2, ps_mf.SSP_WORST, False),
+                                                       (5, 7, 3, ps_mf.ESSP, True), (4, 64, 1, ps_mf.SSP_LAZY, True)])
+def test_seq_order_is_bit_exact_with_oracle(P, G, B, policy, custom_owner):
+    """Host-only SEQ handle: the library's self-check of the order, chains and flags passes,
+    and its export of the order equals the oracle's, bit for bit."""
+    rng = np.random.default_rng(P * 7 + G)
+    N, M, n = 61, 37, 900
+    user = rng.integers(0, N, n).astype(np.int32)
+    item = rng.integers(0, M, n).astype(np.int32)
+    val = rng.integers(1, 6, n).astype(np.float32)
+    owner = rng.integers(0, P, N).astype(np.int32) if custom_owner else None
+    with ps_mf.PsMf(N, M, 8, P, 2, 0.01, 0.05, policy=policy, step=ps_mf.STEP_SEQ, strata=G, B=B, mb_seed=5,
+                    owner=owner, host_only=True) as g:
+        g.load_ratings(user, item, val)
+        o = oracle.Oracle(N, M, 8, P, 2, 0.01, 0.05, policy, oracle.SEQ, B, 5, owner, strata=G)
+        o.load(user, item, val)
+        compare_layout(g, o, B, N, M)
+        for b in range(B):
+            assert np.array_equal(g.export_index(ps_mf.IDX_SEQ_ORDER, b), o.export(oracle.X_SEQ_ORDER, b))
+        o.close()
+
+
+def test_seq_order_on_generated_workload():
+    from paper_1410_8043_amd import synth
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.02)
+    w = synth.generate(spec, K=1)
+    with ps_mf.PsMf(spec.N, spec.M, 16, spec.P, 3, 0.01, 0.05, step=ps_mf.STEP_SEQ, strata=16, B=spec.B,
+                    mb_seed=spec.seed, host_only=True) as g:
+        g.load_ratings(w.user, w.item, w.val)
+        o = oracle.Oracle(spec.N, spec.M, 16, spec.P, 3, 0.01, 0.05, oracle.SSP_LAZY, oracle.SEQ, spec.B, spec.seed,
+                          strata=16)
+        o.load(w.user, w.item, w.val)
+        for b in range(spec.B):
+            assert np.array_equal(g.export_index(ps_mf.IDX_SEQ_ORDER, b), o.export(oracle.X_SEQ_ORDER, b))
+        assert g.export_index(ps_mf.IDX_SPLIT).tolist() == [0] * 8
+        o.close()
+
+
+def test_seq_option_errors():
+    h = ps_mf.ps_mf_create(4, 3, 2, 2, 1, 0.1, 0.1)
+    try:
+        for v in (0, 4097):
+            with pytest.raises(ps_mf.PsMfError) as e:
+                ps_mf.ps_mf_set_option(h, ps_mf.OPT_SEQ_STRATA, v)
+            assert e.value.code == ps_mf.EINVAL
+        ps_mf.ps_mf_set_option(h, ps_mf.OPT_HOST_ONLY, 1)
+        ps_mf.ps_mf_load_ratings(h, np.array([0, 3]), np.array([2, 0]), np.array([1.0, 5.0]))
+        with pytest.raises(ps_mf.PsMfError) as e:
+            ps_mf.ps_mf_export_index(h, ps_mf.IDX_SEQ_ORDER, 0)
+        assert e.value.code == ps_mf.EINVAL
+    finally:
+        ps_mf.ps_mf_destroy(h)
+    for policy in (ps_mf.SSP_ROW, ps_mf.ESSP_ROW):
+        with ps_mf.PsMf(4, 3, 2, 2, 1, 0.1, 0.1, policy=policy, step=ps_mf.STEP_SEQ, host_only=True) as g:
+            with pytest.raises(ps_mf.PsMfError) as e:
+                g.load_ratings(np.array([0]), np.array([0]), np.array([1.0]))
+            assert e.value.code == ps_mf.EINVAL

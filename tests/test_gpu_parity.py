@@ -34,15 +34,18 @@ def say(msg):
 
 
 def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, policy=0, step=0, B=1,
-             seed=0, owner=None, check_versions=False, min_dense=0, **handle_opts):
+             seed=0, owner=None, check_versions=False, min_dense=0, strata=None, **handle_opts):
     say(f"case N={N} M={M} K={K} P={P} s={s} policy={policy} step={step} B={B} nnz={len(w_user)} clocks={clocks} "
-        f"{handle_opts}")
-    o = oracle.Oracle(N, M, K, P, s, eta, lam, policy, step, B, seed, owner)
+        f"strata={strata} {handle_opts}")
+    o = oracle.Oracle(N, M, K, P, s, eta, lam, policy, step, B, seed, owner, strata=strata)
     o.load(w_user, w_item, w_val)
     o.set_factors(L0, R0)
     with ps_mf.PsMf(N, M, K, P, s, eta, lam, policy=policy, step=step, B=B, mb_seed=seed, owner=owner,
-                    **handle_opts) as g:
+                    strata=strata, **handle_opts) as g:
         g.load_ratings(w_user, w_item, w_val)
+        if step == oracle.SEQ:
+            for b in range(B):
+                assert np.array_equal(g.export_index(ps_mf.IDX_SEQ_ORDER, b), o.export(oracle.X_SEQ_ORDER, b))
         if min_dense:
             # the case must put at least min_dense ratings into dense (MFMA) tiles
             split = sum(g.export_index(ps_mf.IDX_SPLIT, b) for b in range(B))
@@ -82,7 +85,7 @@ def test_hand_examples_through_abi(gpu, case):
     v = np.array([r[2] for r in case["ratings"]], np.float32)
     say(f"hand example {case['name']}")
     with gpu.PsMf(case["N"], case["M"], case["K"], case["P"], case["s"], case["eta"], case["lam"],
-                  policy=case["policy"], step=case["step"], owner=case["owner"]) as g:
+                  policy=case["policy"], step=case["step"], owner=case["owner"], strata=case["strata"]) as g:
         g.load_ratings(u, i, v)
         g.set_factors(case["L0"], case["R0"])
         for ex in sorted(case["expect"], key=lambda e: e["clock"]):
@@ -347,3 +350,65 @@ def test_timing_option_counts_launches(gpu):
         assert n == 7 and ms > 0
         ms, n = g.kernel_time(gpu.KERNEL_COMMIT)
         assert n == 7 and ms > 0
+
+
+# ---------------------------------------------------------------- sequential steps inside a worker (STEP_SEQ)
+@pytest.mark.parametrize("s", [0, 2])
+@pytest.mark.parametrize("policy", [oracle.SSP_LAZY, oracle.SSP_WORST, oracle.ESSP])
+@pytest.mark.parametrize("G", [1, 8, 64])
+def test_tiny_config_seq(gpu, s, policy, G):
+    """Each worker applies its ratings one by one to its own rows (G sub-epochs of
+    row-disjoint strata), on the 20,000-rating K=16 workload, 10 clocks."""
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta,
+             lam=spec.lam, clocks=spec.clocks, policy=policy, step=oracle.SEQ, strata=G, check_versions=True)
+
+
+@pytest.mark.parametrize("s,G", [(0, 64), (3, 64), (7, 16)])
+def test_full_shape_scaled_seq(gpu, s, G):
+    spec = synth.scaled(synth.CONFIGS["full"], 0.02)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta,
+             lam=spec.lam, clocks=10, step=oracle.SEQ, strata=G, check_versions=True)
+
+
+def test_medium_shape_scaled_seq_minibatch_blocks(gpu):
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.05)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=spec.clocks, B=spec.B, seed=spec.seed, step=oracle.SEQ, strata=32)
+
+
+def test_contention_and_large_shapes_scaled_seq(gpu):
+    spec = synth.scaled(synth.CONFIGS["contention"], 0.03)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=15, eta=spec.eta,
+             lam=spec.lam, clocks=8, step=oracle.SEQ, strata=64)
+    spec = synth.scaled(synth.CONFIGS["large"], 0.005)
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=4, step=oracle.SEQ, strata=64)
+
+
+@pytest.mark.parametrize("K", [1, 7, 33, 100, 200, 512])
+def test_ragged_rank_seq(gpu, K):
+    N, M = 300, 90
+    user, item, val, L0, R0 = small_problem(K, N, M, 3000, K, dup=20)
+    run_both(gpu, user, item, val, L0, R0, N=N, M=M, K=K, P=5, s=2, eta=0.05, lam=0.05, clocks=6, step=oracle.SEQ,
+             strata=6)
+
+
+def test_seq_zero_degree_rows_custom_owner_single_and_empty(gpu):
+    N, M, K = 200, 80, 16
+    user, item, val, L0, R0 = small_problem(3, N, M, 1500, K)
+    keep = (user % 3 != 0) & (item % 4 != 0)
+    owner = np.random.default_rng(4).integers(0, 6, N).astype(np.int32)
+    run_both(gpu, user[keep], item[keep], val[keep], L0, R0, N=N, M=M, K=K, P=6, s=3, eta=0.05, lam=0.05,
+             clocks=8, owner=owner, step=oracle.SEQ, strata=5, B=3, seed=2, check_versions=True)
+    L0 = np.full((3, 4), 0.5, np.float32)
+    R0 = np.full((2, 4), 0.25, np.float32)
+    run_both(gpu, np.array([2], np.int32), np.array([1], np.int32), np.array([3.0], np.float32), L0, R0,
+             N=3, M=2, K=4, P=2, s=1, eta=0.1, lam=0.1, clocks=4, step=oracle.SEQ, strata=3)
+    run_both(gpu, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32), L0, R0,
+             N=3, M=2, K=4, P=2, s=1, eta=0.1, lam=0.1, clocks=3, step=oracle.SEQ)
