@@ -28,6 +28,7 @@ if ROOT not in sys.path:
 PEAK_FP32_VECTOR_TFLOPS = 157.3   # MI355X published fp32 vector peak (packed FMA)
 PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
 POLICIES = {"lazy": 0, "worst": 1, "essp": 2, "ssp_row": 3, "essp_row": 4}
+STEPS = {"rowmean": 0, "sum": 1, "seq": 2}
 
 
 def parse():
@@ -38,6 +39,10 @@ def parse():
     ap.add_argument("--config", default="full")
     ap.add_argument("--s", type=int, default=None, help="staleness (default: 3 for the full config)")
     ap.add_argument("--policy", default="lazy", choices=sorted(POLICIES))
+    ap.add_argument("--step", default="rowmean", choices=sorted(STEPS),
+                    help="rowmean/sum: one fixed view per worker and clock; seq: every worker applies its "
+                         "ratings one by one to its own rows")
+    ap.add_argument("--strata", type=int, default=None, help="sub-epochs per clock of the seq step")
     ap.add_argument("--cpu-sample", type=int, default=50_000_000,
                     help="ratings in the oracle's timed sample (0 disables the CPU baseline)")
     ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
@@ -53,19 +58,21 @@ def parse():
     ap.add_argument("--copy-calibration-bytes", type=int, default=0,
                     help="run one plain copy kernel (y = x * 2) of this many bytes before timing, for "
                          "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE")
-    ap.add_argument("--traffic-file", default=os.path.join(ROOT, "profiles", "sweep_full_traffic.json"),
-                    help="measured HBM traffic of the sweep (used while the kernel source is unchanged)")
+    ap.add_argument("--traffic-file", default=None,
+                    help="measured HBM traffic of the sweep, used while the kernel source is unchanged (default: "
+                         "profiles/sweep_full_traffic.json, or profiles/seq_full_traffic.json for --step seq)")
     return ap.parse_args()
 
 
-def cpu_baseline(w, spec, K, s, policy, nsample):
+def cpu_baseline(w, spec, K, s, policy, step, strata, nsample):
     """The oracle, single-threaded, on the ratings of a prefix of users (one clock)."""
     import oracle
 
     order = np.argsort(w.user, kind="stable")
     take = order[:nsample]
     u, i, v = w.user[take], w.item[take], w.val[take]
-    o = oracle.Oracle(spec.N, spec.M, K, spec.P, s, spec.eta, spec.lam, policy, oracle.ROWMEAN, spec.B, spec.seed)
+    o = oracle.Oracle(spec.N, spec.M, K, spec.P, s, spec.eta, spec.lam, policy, step, spec.B, spec.seed,
+                      strata=strata)
     o.load(u, i, v)
     o.set_factors(w.L0, w.R0)
     t0 = time.perf_counter()
@@ -78,7 +85,7 @@ def cpu_baseline(w, spec, K, s, policy, nsample):
                       f"{platform.processor() or platform.machine()}, 1 thread"}
 
 
-def measured_traffic(path, config, s, policy):
+def measured_traffic(path, config, s, policy, step):
     """HBM bytes per clock of the sweep from committed rocprofv3 counter runs, or None when
     they are missing, were taken on another workload, or the kernel source has changed."""
     from paper_1410_8043_amd import rocprof_summary
@@ -90,13 +97,19 @@ def measured_traffic(path, config, s, policy):
         return None
     if t.get("kernel_source_sha256") != rocprof_summary.kernel_source_sha256():
         return None
-    if t.get("workload") != {"config": config, "s": s, "policy": policy}:
+    want = {"config": config, "s": s, "policy": policy}
+    if step != "rowmean":
+        want["step"] = step
+    if t.get("workload") != want:
         return None
     return round(t["traffic_bytes_per_clock"])
 
 
 def main():
     args = parse()
+    if args.traffic_file is None:
+        name = "seq_full_traffic.json" if args.step == "seq" else "sweep_full_traffic.json"
+        args.traffic_file = os.path.join(ROOT, "profiles", name)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the multi-GPU path is a design, not part of this build)", file=sys.stderr)
@@ -108,13 +121,16 @@ def main():
     spec = synth.CONFIGS[args.config]
     s = args.s if args.s is not None else (3 if 3 in spec.s_values else spec.s_values[0])
     policy = POLICIES[args.policy]
+    step = STEPS[args.step]
+    seq = args.step == "seq"
     torch.cuda.set_device(0)
     t_gen = time.perf_counter()
     w = synth.generate(spec)
     t_gen = time.perf_counter() - t_gen
     print(f"[bench] generated {args.config}: {w.nnz} ratings in {t_gen:.1f} s", file=sys.stderr, flush=True)
     stream = torch.cuda.current_stream()
-    g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, B=spec.B,
+    g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, step=step, strata=args.strata,
+                   B=spec.B,
                    mb_seed=spec.seed, timing=not args.no_timing, stream=stream, tile_bytes=args.tile_bytes,
                    unit_max=args.unit_max, cells=args.cells, heavy_min=args.heavy_min, hot_steps=args.hot_steps,
                    two_streams=args.two_streams, dense_min=args.dense_min)
@@ -125,8 +141,13 @@ def main():
     print(f"[bench] layout + upload {t_load:.1f} s", file=sys.stderr, flush=True)
     nnz_clock = w.nnz / spec.B  # mean ratings per clock (exact for B=1)
     split = sum(g.export_index(ps_mf.IDX_SPLIT, b) for b in range(spec.B))
-    print(f"[bench] ratings per direction in dense tiles / LDS cells / L2 units: {split[:3].tolist()} (user-major), "
-          f"{split[3:6].tolist()} (item-major); partial rows {split[6:].tolist()}", file=sys.stderr, flush=True)
+    if seq:
+        print(f"[bench] sequential step: {int(split[0])} chains, {int(split[1])} user runs, {int(split[2])} ratings "
+              f"over {spec.B} blocks", file=sys.stderr, flush=True)
+    else:
+        print(f"[bench] ratings per direction in dense tiles / LDS cells / L2 units: {split[:3].tolist()} "
+              f"(user-major), {split[3:6].tolist()} (item-major); partial rows {split[6:].tolist()}",
+              file=sys.stderr, flush=True)
 
     if args.copy_calibration_bytes > 0:
         src = torch.ones(args.copy_calibration_bytes // 4, dtype=torch.float32, device="cuda")
@@ -160,12 +181,22 @@ def main():
         ms_c, n_c = g.kernel_time(ps_mf.KERNEL_COMMIT)
         sweep_ms = (ms_s - base_sweep[0]) / (n_s - base_sweep[1])
         commit_ms = (ms_c - base_commit[0]) / (n_c - base_commit[1])
-        flops = 6.0 * K * nnz_clock                  # 3K fp32 FMA per rating update
-        achieved = flops / (sweep_ms * 1e-3) / 1e12  # TFLOP/s
-        roof = {"kernel": "sweep (k_dense, k_cells and k_units, concurrent)", "bound": "alu",
-                "achieved": round(achieved, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4),
-                "traffic": measured_traffic(args.traffic_file, args.config, s, args.policy)}
+        traffic = measured_traffic(args.traffic_file, args.config, s, args.policy, args.step)
+        if seq:
+            # each rating reads and writes its item row in the worker's copy (2 x 4K bytes) and
+            # reads its 16-byte record; each user run reads and writes the user row
+            runs_clock = float(split[1]) / spec.B
+            bytes_clock = nnz_clock * (8.0 * K + 16) + runs_clock * 8.0 * K
+            achieved = bytes_clock / (sweep_ms * 1e-3) / 1e9  # GB/s
+            roof = {"kernel": "k_seq (one launch per sub-epoch)", "bound": "hbm", "achieved": round(achieved, 1),
+                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                    "traffic": traffic}
+        else:
+            flops = 6.0 * K * nnz_clock                  # 3K fp32 FMA per rating update
+            achieved = flops / (sweep_ms * 1e-3) / 1e12  # TFLOP/s
+            roof = {"kernel": "sweep (k_dense, k_cells and k_units, concurrent)", "bound": "alu",
+                    "achieved": round(achieved, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), "traffic": traffic}
         # compulsory HBM bytes of one clock: each rating once (int32 item + fp32 value),
         # the view version read, the base version read when s > 0, the new version written
         table = (spec.N + spec.M) * K * 4
@@ -177,7 +208,7 @@ def main():
     cpu = None
     if args.cpu_sample > 0:
         print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, spec, K, s, policy, min(args.cpu_sample, w.nnz))
+        cpu = cpu_baseline(w, spec, K, s, policy, step, args.strata, min(args.cpu_sample, w.nnz))
 
     line = {
         "metric": "rating-updates/sec at K=128, 100M ratings (1 GPU); % of HBM roofline",
@@ -194,9 +225,11 @@ def main():
         "data": "synthetic (seeded, Netflix-shaped)",
         "config": {"workload": f"{args.config}: {spec.N} users x {spec.M} items, {w.nnz} ratings, K={K}, "
                                f"P={spec.P}, s={s}, policy={args.policy}, B={spec.B}, eta={spec.eta}, "
-                               f"lambda={spec.lam}",
+                               f"lambda={spec.lam}" + (f", step=seq, strata={args.strata or 256}" if seq else ""),
                    "global_batch": int(nnz_clock), "parallelism": "1 GPU, P logical workers",
-                   "loss_after": loss, "dense_cells_units": [int(x) for x in split[:3]],
+                   "loss_after": loss,
+                   **({"chains_runs_ratings": [int(x) for x in split[:3]]} if seq else
+                      {"dense_cells_units": [int(x) for x in split[:3]]}),
                    "staleness_profile": profile, **extra},
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -101,7 +101,7 @@ typedef struct ps_mf ps_mf_t;
                                   rank is in [16, 256], else none); at most 4096.  A value > 0
                                   with a padded rank outside [16, 256] makes
                                   ps_mf_load_ratings fail with PS_MF_EINVAL */
-#define PS_MF_OPT_SEQ_STRATA 14 /* G: sub-epochs per clock of PS_MF_STEP_SEQ (default 64), in
+#define PS_MF_OPT_SEQ_STRATA 14 /* G: sub-epochs per clock of PS_MF_STEP_SEQ (default 256), in
                                    [1, 4096].  Part of the semantics: it fixes the order in which
                                    a worker applies its ratings */
 
@@ -142,7 +142,10 @@ typedef struct ps_mf ps_mf_t;
                                    for the user-major then the item-major direction (each triple
                                    sums to the block's rating count); then the partial rows
                                    (Kp floats each) the user-major and the item-major sweep
-                                   write per clock for the commit to sum */
+                                   write per clock for the commit to sum.  Under
+                                   PS_MF_STEP_SEQ: the chains, the user runs (a user's
+                                   ratings inside one chain) and the ratings of block b,
+                                   then zeros */
 #define PS_MF_IDX_STALENESS 8   /* int64 [s+1]: staleness profile of the clocks run since the last
                                    ps_mf_set_factors (Section 2.2, Fig. 1 left): entry d counts
                                    the parameter reads that saw version c - d at clock c, i.e.

@@ -188,7 +188,7 @@ int oracle_create(int64_t N, int64_t M, int32_t K, int32_t P, int32_t s, double 
   if (!o) return OR_ENOMEM;
   o->N = N; o->M = M; o->K = K; o->P = P; o->s = s; o->eta = eta; o->lambda = lambda;
   o->policy = policy; o->step = step; o->B = B; o->seed = seed;
-  o->G = 64;
+  o->G = 256;
   o->owner = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
   o->stale = (int64_t *)calloc((size_t)s + 1, sizeof(int64_t));
   o->C = P < (int64_t)s + 1 ? P : (int64_t)s + 1;
@@ -207,7 +207,7 @@ int oracle_create(int64_t N, int64_t M, int32_t K, int32_t P, int32_t s, double 
   return OR_OK;
 }
 
-/* number of sub-epochs G of the SEQ step (default 64); before load */
+/* number of sub-epochs G of the SEQ step (default 256); before load */
 int oracle_set_strata(oracle_t *o, int32_t G) {
   if (!o || G < 1) return OR_EINVAL;
   if (o->loaded) return OR_ESTATE;

@@ -780,22 +780,25 @@ void build_seq(const LayoutParams &p, BlockLayout &L, const std::vector<int32_t>
   S.chain_beg.push_back(nb);
   for (int64_t t = 0; t < G; ++t) S.epoch_chain[t + 1] += S.epoch_chain[t];
   const int64_t nch = static_cast<int64_t>(S.chain_worker.size());
-  // L flags on the first rating of each user run: the user's first and last run of the clock
+  // run starts, and the user's first run of the clock
   std::vector<uint8_t> seen(static_cast<size_t>(p.users), 0);
   for (int64_t ch = 0; ch < nch; ++ch)
     for (int64_t x = S.chain_beg[ch]; x < S.chain_beg[ch + 1]; ++x)
-      if (x == S.chain_beg[ch] || S.user[x] != S.user[x - 1])
+      if (x == S.chain_beg[ch] || S.user[x] != S.user[x - 1]) {
+        S.flag[x] |= kSeqRunStart;
         if (!seen[S.user[x]]) {
           seen[S.user[x]] = 1;
           S.flag[x] |= kSeqFirstL;
         }
-  std::fill(seen.begin(), seen.end(), 0);
-  for (int64_t ch = nch - 1; ch >= 0; --ch)
-    for (int64_t x = S.chain_beg[ch + 1] - 1; x >= S.chain_beg[ch]; --x)
-      if ((x == S.chain_beg[ch] || S.user[x] != S.user[x - 1]) && !seen[S.user[x]]) {  // a run's start
-        seen[S.user[x]] = 1;
-        S.flag[x] |= kSeqLastL;
       }
+  // items read again within the prefetch distance: the distance to the latest occurrence
+  for (int64_t ch = 0; ch < nch; ++ch)
+    for (int64_t x = S.chain_beg[ch]; x < S.chain_beg[ch + 1]; ++x)
+      for (int64_t k = 1; k <= kSeqAhead && x - k >= S.chain_beg[ch]; ++k)
+        if (S.item[x - k] == S.item[x]) {
+          S.flag[x] |= static_cast<uint8_t>(k << kSeqDistShift);
+          break;
+        }
   // R flags: each worker's first rating of an item, scanning the worker's chains in order;
   // the (item, worker) pairs give the item worker lists, ascending in the worker
   std::vector<std::vector<int64_t>> chains_of(static_cast<size_t>(P));
@@ -1301,26 +1304,29 @@ int check_seq(const LayoutParams &p, const BlockLayout &L, std::string &err) {
           std::get<2>(skey(lo)) == std::get<2>(skey(lo - 1)))
         return bad("chain " + std::to_string(ch) + " is not maximal");
     }
-  // flags by brute force: first / last run of each user, first (worker, item) in order
-  std::vector<int64_t> first_run(static_cast<size_t>(N), -1), last_run(static_cast<size_t>(N), -1);
+  // flags by brute force: run starts, first run of each user, first (worker, item) in order,
+  // items repeated within the prefetch distance
+  std::vector<int64_t> first_run(static_cast<size_t>(N), -1);
   std::vector<std::vector<int64_t>> first_r(static_cast<size_t>(M));
+  std::vector<uint8_t> want(static_cast<size_t>(nb), 0);
   for (int64_t ch = 0; ch < nch; ++ch)
     for (int64_t x = S.chain_beg[ch]; x < S.chain_beg[ch + 1]; ++x) {
       const int32_t i = S.user[x];
       if (x == S.chain_beg[ch] || S.user[x - 1] != i) {
+        want[x] |= kSeqRunStart;
         if (first_run[i] < 0) first_run[i] = x;
-        last_run[i] = x;
       }
       bool seen_before = false;
       for (int64_t y : first_r[S.item[x]])
         if (p.owner[S.user[y]] == p.owner[i]) seen_before = true;
       if (!seen_before) first_r[S.item[x]].push_back(x);
+      int64_t dist = 0;
+      for (int64_t y = S.chain_beg[ch]; y < x; ++y)
+        if (S.item[y] == S.item[x] && x - y <= kSeqAhead) dist = x - y;  // the latest wins
+      want[x] |= static_cast<uint8_t>(dist << kSeqDistShift);
     }
-  std::vector<uint8_t> want(static_cast<size_t>(nb), 0);
-  for (int64_t i = 0; i < N; ++i) {
+  for (int64_t i = 0; i < N; ++i)
     if (first_run[i] >= 0) want[first_run[i]] |= kSeqFirstL;
-    if (last_run[i] >= 0) want[last_run[i]] |= kSeqLastL;
-  }
   for (int64_t j = 0; j < M; ++j)
     for (int64_t x : first_r[j]) want[x] |= kSeqFirstR;
   for (int64_t x = 0; x < nb; ++x)

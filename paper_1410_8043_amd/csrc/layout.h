@@ -112,11 +112,16 @@ struct DenseSet {
 // g, each in canonical order -- user group (i div P) mod G, item group j mod G.  A chain is
 // one (sub-epoch, worker, user group) stratum with ratings; chains are stored by sub-epoch,
 // and the strata of one sub-epoch share no row, so its chains run side by side.
-// Flags of a rating: kSeqFirstL / kSeqLastL on the first rating of a user's run inside a
-// chain when the run is the user's first / last of the clock (L_i is read from the view /
-// the run ends with the commit of L_i); kSeqFirstR when it is worker p's first rating of
-// item j in the clock (R_j is read from the view, later ones from the worker's copy).
-constexpr uint8_t kSeqFirstL = 1, kSeqLastL = 2, kSeqFirstR = 4;
+// Flags of a rating: kSeqRunStart on the first rating of a user's run inside a chain, with
+// kSeqFirstL when the run is the user's first of the clock (L_i is read from the view, later
+// runs from the work copy); kSeqFirstR when it is worker p's first rating of item j in the
+// clock (R_j is read from the view, later ones from the worker's copy).  Bits 4..7 hold the
+// distance k in [1, kSeqAhead] to the latest of the kSeqAhead ratings before it in the chain
+// with the same item (0: none): the sweep fetches item rows kSeqAhead ratings ahead, before
+// those ratings store theirs, so such a rating takes the row that rating k back wrote.
+constexpr uint8_t kSeqFirstL = 1, kSeqRunStart = 2, kSeqFirstR = 4;
+constexpr int kSeqAhead = 8;
+constexpr int kSeqDistShift = 4;
 struct SeqSet {
   int32_t G = 0;
   std::vector<int64_t> epoch_chain;   // [G + 1]: the chains of sub-epoch t

@@ -34,6 +34,7 @@
 #include <new>
 #include <string>
 #include <thread>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/ps_mf.h"
@@ -957,82 +958,154 @@ __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, 
 
 // ------------------------------------------------------------------ sequential step
 // Under STEP_SEQ every worker applies the Section 3.1 rule rating by rating to its own
-// copies of the rows.  A chain (one stratum: sub-epoch, worker, user group) is one lane
-// group; the chains of one sub-epoch share no row and run side by side in one launch, the
-// sub-epochs one launch after another.  Inside a chain the current user's row stays in
-// registers for the user's run; each rating loads the item row from the worker's copy
-// (from the view on the worker's first rating of the item in the clock), updates both rows
-// and stores the item row back.  A user row leaves its run in the work copy, or, after the
-// user's last run of the clock, as L^{c+1}_i = L^c_i + (copy - L^v_i) in the new slot.
+// copies of the rows.  A chain (one stratum: sub-epoch, worker, user group) is one
+// wavefront; the chains of one sub-epoch share no row and run side by side in one launch,
+// the sub-epochs one launch after another.  Lane l holds elements [l*E, (l+1)*E) of a row
+// (E = Kp/64, at least 1), so the chain's control -- rating records, flags, branches -- is
+// uniform over the wavefront, the records come through scalar loads, and a dot product is
+// a 16-lane DPP sum plus the four row sums.  Inside a chain the current user's row stays in
+// registers for the user's run and leaves it into the work copy; each rating updates its
+// item row in the worker's copy (read from the view on the worker's first rating of the
+// item in the clock).  Every rating depends on the rows the previous ones wrote, so the
+// records are fetched 2*kSeqAhead ratings ahead and the item rows (and, at a run start, the
+// user row) kSeqAhead ahead, in register rings whose slots are fixed at compile time.  A
+// rating whose item occurs among the kSeqAhead ratings before it takes the row the latest
+// of them wrote from a ring of the last kSeqAhead written rows (its prefetched copy may
+// predate that store), so no rating waits on its own chain's stores.
+typedef const __attribute__((address_space(4))) i32x4 *const_rec_ptr;  // read-only during the sweep
 struct SeqArgs {
   const int64_t *chain_beg;
   const int32_t *chain_worker;
-  const int32_t *user, *item;
-  const float *val;
-  const uint8_t *flag;
+  const i32x4 *rec;                // [nnz] (user, item, value bits, flags) in application order
   const int32_t *wcls, *cls_slot;  // worker class, ring slot of each class's view
-  float *ring;
+  const float *ring;
   int64_t slot_stride, r_off;
-  int32_t slot_c, slot_n;
   float *lwork;                    // [users, Kp] the user rows between their runs
   float *rwork;                    // [P, items, Kp] each worker's copy of the item rows
   int64_t rwork_stride;            // items * Kp
+  int32_t Kp;
   float eta, lambda;
 };
 
-template <int G, int E>
-__device__ __forceinline__ void seq_leave_user(const SeqArgs &a, int32_t i, uint8_t f, const float (&x)[E],
-                                               const float *Lv, int g) {
-  constexpr int Kp = G * E;
-  const int64_t off = static_cast<int64_t>(i) * Kp;
-  if (f & psmf::kSeqLastL) {
-    float lc[E], lv[E], o[E];
-    load_row<G, E>(lc, a.ring + a.slot_c * a.slot_stride + off, g);
-    load_row<G, E>(lv, Lv + off, g);
-#pragma unroll
-    for (int k = 0; k < E; ++k) o[k] = lc[k] + (x[k] - lv[k]);
-    store_row<G, E>(a.ring + a.slot_n * a.slot_stride + off, o, g);
+// a row of Kp = 64*E floats (Kp < 64: E = 1 and lanes >= Kp hold zeros)
+template <int E>
+__device__ __forceinline__ void wave_load_row(float (&d)[E], const float *__restrict__ row, int lane, int Kp) {
+  if constexpr (E == 1) {
+    d[0] = lane < Kp ? row[lane] : 0.f;
+  } else if constexpr (E == 2) {
+    const float2 t = *reinterpret_cast<const float2 *>(row + 2 * lane);
+    d[0] = t.x; d[1] = t.y;
   } else {
-    store_row<G, E>(a.lwork + off, x, g);
+#pragma unroll
+    for (int q = 0; q < E / 4; ++q) {
+      const float4 t = *reinterpret_cast<const float4 *>(row + E * lane + 4 * q);
+      d[4 * q] = t.x; d[4 * q + 1] = t.y; d[4 * q + 2] = t.z; d[4 * q + 3] = t.w;
+    }
   }
 }
 
-template <int G, int E>
+template <int E>
+__device__ __forceinline__ void wave_store_row(float *__restrict__ row, const float (&d)[E], int lane, int Kp) {
+  if constexpr (E == 1) {
+    if (lane < Kp) row[lane] = d[0];
+  } else if constexpr (E == 2) {
+    *reinterpret_cast<float2 *>(row + 2 * lane) = make_float2(d[0], d[1]);
+  } else {
+#pragma unroll
+    for (int q = 0; q < E / 4; ++q)
+      *reinterpret_cast<float4 *>(row + E * lane + 4 * q) = make_float4(d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]);
+  }
+}
+
+// sum over the 64 lanes: the 16-lane row sums, then the four rows through scalar registers
+__device__ __forceinline__ float wave_sum(float v) {
+  v = group_sum<16>(v);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
+// f(integral_constant<int, K>, base + K) for K = K0 .. N-1 while f returns true
+template <int K0, int N, class F>
+__device__ __forceinline__ void seq_unrolled(F &f, int64_t base) {
+  if (!f(std::integral_constant<int, K0>{}, base + K0)) return;
+  if constexpr (K0 + 1 < N) seq_unrolled<K0 + 1, N>(f, base);
+}
+
+template <int E>
 __global__ __launch_bounds__(kBlock) void k_seq(SeqArgs a, int64_t c0, int64_t c1) {
-  constexpr int Kp = G * E;
-  const int g = static_cast<int>(threadIdx.x) % G;
-  const int64_t ch = c0 + (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / G;
-  if (ch >= c1) return;  // uniform over the lane group
+  constexpr int D = psmf::kSeqAhead, D2 = 2 * psmf::kSeqAhead;
+  const int lane = static_cast<int>(threadIdx.x) % 64, Kp = a.Kp;
+  const int64_t ch = c0 + __builtin_amdgcn_readfirstlane((static_cast<int>(blockIdx.x) * kBlock +
+                                                          static_cast<int>(threadIdx.x)) / 64);
+  if (ch >= c1) return;  // uniform over the wavefront
   const int64_t beg = a.chain_beg[ch], end = a.chain_beg[ch + 1];
   const int32_t p = a.chain_worker[ch];
   const float *Lv = a.ring + a.cls_slot[a.wcls[p]] * a.slot_stride;
   const float *Rv = Lv + a.r_off;
   float *Rw = a.rwork + static_cast<int64_t>(p) * a.rwork_stride;
+  const const_rec_ptr rec = (const_rec_ptr)(a.rec);
+  i32x4 meta[D2];
+  float yq[D][E], lq[D][E], wq[D][E];
+  auto fetch = [&](const i32x4 &m, float (&y)[E], float (&x)[E]) {
+    wave_load_row<E>(y, ((m[3] & psmf::kSeqFirstR) ? Rv : Rw) + static_cast<int64_t>(m[1]) * Kp, lane, Kp);
+    if (m[3] & psmf::kSeqRunStart)
+      wave_load_row<E>(x, ((m[3] & psmf::kSeqFirstL) ? Lv : a.lwork) + static_cast<int64_t>(m[0]) * Kp, lane, Kp);
+  };
+#pragma unroll
+  for (int k = 0; k < D2; ++k)
+    if (beg + k < end) meta[k] = rec[beg + k];
+#pragma unroll
+  for (int k = 0; k < D; ++k)
+    if (beg + k < end) fetch(meta[k], yq[k], lq[k]);
   float x[E];
   int32_t cur = -1;
-  uint8_t fcur = 0;
-  for (int64_t n = beg; n < end; ++n) {
-    const int32_t i = a.user[n], j = a.item[n];
-    const float r = a.val[n];
-    const uint8_t f = a.flag[n];
-    if (i != cur) {
-      if (cur >= 0) seq_leave_user<G, E>(a, cur, fcur, x, Lv, g);
-      load_row<G, E>(x, ((f & psmf::kSeqFirstL) ? Lv : a.lwork) + static_cast<int64_t>(i) * Kp, g);
-      cur = i;
-      fcur = f;
+  // one rating; K is the ring position (a compile-time constant, so the rings stay in
+  // registers); false once the chain is done
+  auto step = [&](auto kc, int64_t n) -> bool {
+    constexpr int K = decltype(kc)::value;
+    if (n >= end) return false;
+    const i32x4 m = meta[K];
+    const int32_t flags = m[3];
+    if (flags & psmf::kSeqRunStart) {
+      if (cur >= 0) wave_store_row<E>(a.lwork + static_cast<int64_t>(cur) * Kp, x, lane, Kp);
+#pragma unroll
+      for (int e = 0; e < E; ++e) x[e] = lq[K % D][e];
+      cur = m[0];
     }
     float y[E];
-    load_row<G, E>(y, ((f & psmf::kSeqFirstR) ? Rv : Rw) + static_cast<int64_t>(j) * Kp, g);
-    const float e = residual<G, E>(x, y, r);
 #pragma unroll
-    for (int k = 0; k < E; ++k) {
-      const float xl = x[k], yl = y[k];
-      x[k] = fmaf(a.eta, fmaf(e, yl, -a.lambda * xl), xl);
-      y[k] = fmaf(a.eta, fmaf(e, xl, -a.lambda * yl), yl);
+    for (int e = 0; e < E; ++e) y[e] = yq[K % D][e];
+    const int dist = flags >> psmf::kSeqDistShift;
+    if (dist) {  // the row rating n - dist wrote
+#pragma unroll
+      for (int q = 1; q <= D; ++q)
+        if (dist == q) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) y[e] = wq[(K - q + D2) % D][e];
+        }
     }
-    store_row<G, E>(Rw + static_cast<int64_t>(j) * Kp, y, g);
-  }
-  if (cur >= 0) seq_leave_user<G, E>(a, cur, fcur, x, Lv, g);
+    float dot = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) dot = fmaf(x[e], y[e], dot);
+    const float err = __int_as_float(m[2]) - wave_sum(dot);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float xl = x[e], yl = y[e];
+      x[e] = fmaf(a.eta, fmaf(err, yl, -a.lambda * xl), xl);
+      y[e] = fmaf(a.eta, fmaf(err, xl, -a.lambda * yl), yl);
+    }
+    wave_store_row<E>(Rw + static_cast<int64_t>(m[1]) * Kp, y, lane, Kp);
+#pragma unroll
+    for (int e = 0; e < E; ++e) wq[K % D][e] = y[e];
+    if (n + D < end) fetch(meta[(K + D) % D2], yq[K % D], lq[K % D]);
+    if (n + D2 < end) meta[K] = rec[n + D2];
+    return true;
+  };
+  for (int64_t base = beg; base < end; base += D2) seq_unrolled<0, D2>(step, base);
+  if (cur >= 0) wave_store_row<E>(a.lwork + static_cast<int64_t>(cur) * Kp, x, lane, Kp);
 }
 
 struct SeqCommitArgs {
@@ -1041,7 +1114,9 @@ struct SeqCommitArgs {
   int64_t users, items;
   int32_t Kp;
   int32_t slot_c, slot_n;
-  const int32_t *ucount;       // [users] ratings in the block (users without one keep L^c_i)
+  const int32_t *ucount;       // [users] ratings in the block
+  const int32_t *ucls;         // [users] class of the user's worker
+  const float *lwork;
   const int64_t *item_wptr;    // [items + 1]
   const int32_t *item_workers; // the workers with a rating of each item
   const int32_t *wcls, *cls_slot;
@@ -1049,16 +1124,25 @@ struct SeqCommitArgs {
   int64_t rwork_stride;
 };
 
-// One thread per float4 of a row: users without a rating in the block keep L^c_i (copied
-// when the new slot differs); R^{c+1}_j = R^c_j + sum over the workers with a rating of j
-// of (copy - R^{v(p)}_j).
+// One thread per float4 of a row: L^{c+1}_i = L^c_i + (copy - L^v_i) for the users with a
+// rating in the block, the others keep L^c_i (copied when the new slot differs);
+// R^{c+1}_j = R^c_j + sum over the workers with a rating of j of (copy - R^{v(p)}_j).
 __global__ __launch_bounds__(kBlock) void k_seq_commit(SeqCommitArgs a) {
   const int64_t q4 = a.Kp / 4;
   int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   float4 *ring4 = reinterpret_cast<float4 *>(a.ring);
   const int64_t ss4 = a.slot_stride / 4;
   if (idx < a.users * q4) {
-    if (a.ucount[idx / q4] == 0 && a.slot_n != a.slot_c) ring4[a.slot_n * ss4 + idx] = ring4[a.slot_c * ss4 + idx];
+    const int64_t i = idx / q4;
+    if (a.ucount[i] == 0) {
+      if (a.slot_n != a.slot_c) ring4[a.slot_n * ss4 + idx] = ring4[a.slot_c * ss4 + idx];
+      return;
+    }
+    const float4 loc = reinterpret_cast<const float4 *>(a.lwork)[idx];
+    const float4 v = ring4[a.cls_slot[a.ucls[i]] * ss4 + idx];
+    const float4 lc = ring4[a.slot_c * ss4 + idx];
+    ring4[a.slot_n * ss4 + idx] = make_float4(lc.x + (loc.x - v.x), lc.y + (loc.y - v.y), lc.z + (loc.z - v.z),
+                                              lc.w + (loc.w - v.w));
     return;
   }
   idx -= a.users * q4;
@@ -1161,14 +1245,21 @@ struct LaunchUnits {
 // padded ranks with a dense (MFMA) cell kernel
 bool dense_supported(int Kp) { return Kp >= 16 && Kp <= 256; }
 
-template <int G, int E>
-struct LaunchSeq {
-  static hipError_t run(const SeqArgs &a, int64_t c0, int64_t c1, hipStream_t st) {
-    const int64_t groups = kBlock / G, grid = (c1 - c0 + groups - 1) / groups;
-    hipLaunchKernelGGL((k_seq<G, E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a, c0, c1);
-    return hipGetLastError();
+template <int E>
+hipError_t launch_seq(const SeqArgs &a, int64_t c0, int64_t c1, hipStream_t st) {
+  const int64_t waves = kBlock / 64, grid = (c1 - c0 + waves - 1) / waves;
+  hipLaunchKernelGGL((k_seq<E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a, c0, c1);
+  return hipGetLastError();
+}
+// one chain per wavefront: E = Kp / 64 floats per lane (at least one)
+hipError_t dispatch_seq(int Kp, const SeqArgs &a, int64_t c0, int64_t c1, hipStream_t st) {
+  switch (Kp) {
+    case 128: return launch_seq<2>(a, c0, c1, st);
+    case 256: return launch_seq<4>(a, c0, c1, st);
+    case 512: return launch_seq<8>(a, c0, c1, st);
+    default: return launch_seq<1>(a, c0, c1, st);  // 8 .. 64
   }
-};
+}
 
 template <bool FromE>
 hipError_t launch_dense(int Kp, const DenseArgs &a, int64_t grid, hipStream_t st) {
@@ -1226,9 +1317,8 @@ struct DeviceDense {
 struct DeviceSeq {
   std::vector<int64_t> epoch_chain;  // host copy: the chains of each sub-epoch
   int64_t *chain_beg = nullptr, *item_wptr = nullptr;
-  int32_t *chain_worker = nullptr, *user = nullptr, *item = nullptr, *item_workers = nullptr;
-  float *val = nullptr;
-  uint8_t *flag = nullptr;
+  int32_t *chain_worker = nullptr, *item_workers = nullptr;
+  int32_t *rec = nullptr;            // [nnz * 4] (user, item, value bits, flags)
 };
 
 struct DeviceBlock {
@@ -1259,7 +1349,7 @@ struct ps_mf {
   bool cells = true;             // stage the dense part (heavy users) through LDS
   int64_t heavy_min = -1;        // ratings from which a user goes to the cells (-1: automatic)
   int32_t dense_min = -1;        // ratings from which a 64 x 64 tile goes to the MFMA cells (-1: automatic, 0: none)
-  int32_t seq_groups = 64;       // sub-epochs of the sequential step
+  int32_t seq_groups = 256;      // sub-epochs of the sequential step
   std::vector<int32_t> owner;
   // host state
   bool loaded = false, has_factors = false;
@@ -1549,20 +1639,16 @@ int seq_clock(ps_mf_t *h) {
   SeqArgs a{};
   a.chain_beg = q.chain_beg;
   a.chain_worker = q.chain_worker;
-  a.user = q.user;
-  a.item = q.item;
-  a.val = q.val;
-  a.flag = q.flag;
+  a.rec = reinterpret_cast<const i32x4 *>(q.rec);
   a.wcls = h->wcls;
   a.cls_slot = h->slot_table + table_row(h, c) * h->nclass;
   a.ring = h->ring;
   a.slot_stride = (h->N + h->M) * h->Kp;
   a.r_off = h->N * h->Kp;
-  a.slot_c = static_cast<int32_t>(c % S1);
-  a.slot_n = static_cast<int32_t>((c + 1) % S1);
   a.lwork = h->lwork;
   a.rwork = h->rwork;
   a.rwork_stride = h->M * h->Kp;
+  a.Kp = h->Kp;
   a.eta = h->eta;
   a.lambda = h->lambda;
   hipEvent_t ev = nullptr;
@@ -1570,7 +1656,7 @@ int seq_clock(ps_mf_t *h) {
   if (rc) return rc;
   for (int32_t t = 0; t < h->seq_groups; ++t) {
     const int64_t c0 = q.epoch_chain[t], c1 = q.epoch_chain[t + 1];
-    if (c1 > c0) HIP_TRY(h, dispatch<LaunchSeq>(h->Kp, a, c0, c1, h->stream));
+    if (c1 > c0) HIP_TRY(h, dispatch_seq(h->Kp, a, c0, c1, h->stream));
   }
   if ((rc = record_end(h, PS_MF_KERNEL_SWEEP, ev))) return rc;
   if ((rc = record(h, &ev))) return rc;
@@ -1581,9 +1667,11 @@ int seq_clock(ps_mf_t *h) {
   ca.users = h->N;
   ca.items = h->M;
   ca.Kp = h->Kp;
-  ca.slot_c = a.slot_c;
-  ca.slot_n = a.slot_n;
+  ca.slot_c = static_cast<int32_t>(c % S1);
+  ca.slot_n = static_cast<int32_t>((c + 1) % S1);
   ca.ucount = db.ucount;
+  ca.ucls = h->ucls;
+  ca.lwork = h->lwork;
   ca.item_wptr = q.item_wptr;
   ca.item_workers = q.item_workers;
   ca.wcls = h->wcls;
@@ -1941,9 +2029,15 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
       const psmf::SeqSet &S = L.seq;
       DeviceSeq &q = d.seq;
       q.epoch_chain = S.epoch_chain;
+      std::vector<int32_t> rec(S.user.size() * 4);
+      for (size_t x = 0; x < S.user.size(); ++x) {
+        rec[4 * x] = S.user[x];
+        rec[4 * x + 1] = S.item[x];
+        std::memcpy(&rec[4 * x + 2], &S.val[x], sizeof(float));
+        rec[4 * x + 3] = S.flag[x];
+      }
       if ((r = upload(h, &q.chain_beg, S.chain_beg)) || (r = upload(h, &q.chain_worker, S.chain_worker)) ||
-          (r = upload(h, &q.user, S.user)) || (r = upload(h, &q.item, S.item)) || (r = upload(h, &q.val, S.val)) ||
-          (r = upload(h, &q.flag, S.flag)) || (r = upload(h, &q.item_wptr, S.item_wptr)) ||
+          (r = upload(h, &q.rec, rec)) || (r = upload(h, &q.item_wptr, S.item_wptr)) ||
           (r = upload(h, &q.item_workers, S.item_workers)))
         return undo(r);
     } else if ((r = upload_units(h, d.by_user, L.by_user)) || (r = upload_units(h, d.by_item, L.by_item)) ||
@@ -2141,14 +2235,20 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
       for (int32_t len : u.unit_len) t += len;
       return t;
     };
-    split[0] = L.dense_user.nnz;
-    split[1] = L.cells_user.nnz;
-    split[2] = unit_ratings(L.by_user);
-    split[3] = L.dense_item.nnz;
-    split[4] = L.cells_item.nnz;
-    split[5] = unit_ratings(L.by_item);
-    split[6] = L.partial_rows_user;
-    split[7] = L.partial_rows_item;
+    if (h->step == PS_MF_STEP_SEQ) {
+      split[0] = static_cast<int64_t>(L.seq.chain_worker.size());
+      for (uint8_t f : L.seq.flag) split[1] += (f & psmf::kSeqRunStart) != 0;
+      split[2] = L.nnz;
+    } else {
+      split[0] = L.dense_user.nnz;
+      split[1] = L.cells_user.nnz;
+      split[2] = unit_ratings(L.by_user);
+      split[3] = L.dense_item.nnz;
+      split[4] = L.cells_item.nnz;
+      split[5] = unit_ratings(L.by_item);
+      split[6] = L.partial_rows_user;
+      split[7] = L.partial_rows_item;
+    }
   }
   std::vector<int64_t> stale, rowver, seq_order;
   if (kind == PS_MF_IDX_SEQ_ORDER) {

@@ -58,8 +58,8 @@ def stats(d: str):
     return [(short_name(n), int(c), tot / 1e3, avg / 1e3, pct) for n, c, tot, avg, pct in rows]
 
 
-def _is_sweep(name: str) -> bool:
-    return any(name.startswith(k) for k in SWEEP_KERNELS)
+def _is_sweep(name: str, kernels=SWEEP_KERNELS) -> bool:
+    return any(name.startswith(k) for k in kernels)
 
 
 def sweep_spans(d: str):
@@ -111,25 +111,28 @@ def _copy_value(cnt, counter: str) -> float:
     raise KeyError(f"{counter} of the calibration copy kernel not found")
 
 
-def _sweep_values(cnt, counter: str):
+def _sweep_values(cnt, counter: str, kernels=SWEEP_KERNELS):
     """[(kernel, [value per dispatch])] of the sweep kernels, one entry per distinct kernel"""
-    out = [(short_name(k), v) for (k, c), v in cnt.items() if c == counter and _is_sweep(short_name(k))]
+    out = [(short_name(k), v) for (k, c), v in cnt.items() if c == counter and _is_sweep(short_name(k), kernels)]
     if not out:
         raise KeyError(f"{counter} of the sweep kernels not found")
     return out
 
 
-def traffic(fetch_dir: str, write_dir: str, copy_bytes: int):
-    """HBM bytes per clock of the sweep (its kernels of one clock summed), calibrated."""
+def traffic(fetch_dir: str, write_dir: str, copy_bytes: int, kernels=SWEEP_KERNELS, per_clock: int = 1):
+    """HBM bytes per clock of the sweep (its kernels of one clock summed), calibrated.  Each
+    distinct sweep kernel runs per_clock times a clock (the sequential step: once per
+    sub-epoch)."""
     f, w = counters(fetch_dir), counters(write_dir)
     copy_f = _copy_value(f, "FETCH_SIZE")
     copy_w = _copy_value(w, "WRITE_SIZE")
     fetch_scale = copy_bytes / (copy_f * 1024.0)
     write_scale = copy_bytes / (copy_w * 1024.0)
-    sf, sw = _sweep_values(f, "FETCH_SIZE"), _sweep_values(w, "WRITE_SIZE")
-    clocks = min(len(v) for _, v in sf + sw)
-    fetch = sum(sum(v[:clocks]) for _, v in sf) * 1024.0 * fetch_scale / clocks
-    write = sum(sum(v[:clocks]) for _, v in sw) * 1024.0 * write_scale / clocks
+    sf, sw = _sweep_values(f, "FETCH_SIZE", kernels), _sweep_values(w, "WRITE_SIZE", kernels)
+    clocks = min(len(v) for _, v in sf + sw) // per_clock
+    n = clocks * per_clock
+    fetch = sum(sum(v[:n]) for _, v in sf) * 1024.0 * fetch_scale / clocks
+    write = sum(sum(v[:n]) for _, v in sw) * 1024.0 * write_scale / clocks
     return {
         "kernels": [k for k, _ in sf],
         "clocks": clocks,
@@ -160,6 +163,9 @@ def main(argv=None):
     c.add_argument("--config", default="full")
     c.add_argument("--s", type=int, default=3)
     c.add_argument("--policy", default="lazy")
+    c.add_argument("--step", default="rowmean")
+    c.add_argument("--kernels", default=",".join(SWEEP_KERNELS), help="comma-separated kernel name prefixes")
+    c.add_argument("--per-clock", type=int, default=1, help="dispatches of each kernel per clock")
     args = ap.parse_args(argv)
     if args.cmd == "stats":
         for name, calls, tot, avg, pct in stats(args.dir):
@@ -175,9 +181,11 @@ def main(argv=None):
             for (k, cname), vals in sorted(counters(d).items()):
                 print(f"{short_name(k)[:48]:48s} {cname:18s} " + " ".join(f"{v:.5g}" for v in vals[:8]))
     else:
-        t = traffic(args.fetch, args.write, args.copy_bytes)
+        t = traffic(args.fetch, args.write, args.copy_bytes, tuple(args.kernels.split(",")), args.per_clock)
         t["command"] = args.command
         t["workload"] = {"config": args.config, "s": args.s, "policy": args.policy}
+        if args.step != "rowmean":
+            t["workload"]["step"] = args.step
         with open(args.out, "w") as f:
             json.dump(t, f, indent=1)
         print(json.dumps({k: v for k, v in t.items() if not k.startswith("per_launch")}, indent=1))

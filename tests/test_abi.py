@@ -296,7 +296,13 @@ def test_seq_order_on_generated_workload():
         o.load(w.user, w.item, w.val)
         for b in range(spec.B):
             assert np.array_equal(g.export_index(ps_mf.IDX_SEQ_ORDER, b), o.export(oracle.X_SEQ_ORDER, b))
-        assert g.export_index(ps_mf.IDX_SPLIT).tolist() == [0] * 8
+        # block 0: its ratings, one user run per (user, sub-epoch) pair with ratings
+        split = g.export_index(ps_mf.IDX_SPLIT, 0).tolist()
+        sel = o.export(oracle.X_SEQ_ORDER, 0)
+        u, i = w.user[sel].astype(np.int64), w.item[sel].astype(np.int64)
+        runs = np.unique(u * 16 + ((i % 16) - (u // spec.P) % 16) % 16).size
+        assert split[1] == runs and split[2] == sel.size
+        assert 0 < split[0] <= split[1] <= split[2] and split[3:] == [0] * 5
         o.close()
 
 
