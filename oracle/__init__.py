@@ -18,10 +18,10 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libps_mf_oracle.so")
 
-SSP_LAZY, SSP_WORST, ESSP, SSP_ROW, ESSP_ROW = 0, 1, 2, 3, 4
+SSP_LAZY, SSP_WORST, ESSP, SSP_ROW, ESSP_ROW, VAP = 0, 1, 2, 3, 4, 5
 ROWMEAN, SUM, SEQ = 0, 1, 2
 (X_OWNER, X_ROW_PTR, X_COL, X_PERM, X_USER_COUNT, X_ITEM_COUNT, X_VERSION_LOG, X_STALENESS, X_ROW_VERSIONS,
- X_SEQ_ORDER) = range(10)
+ X_SEQ_ORDER, X_VAP_NORMS) = range(11)
 
 _lib = None
 
@@ -59,6 +59,8 @@ def _load():
         "oracle_view_version": [vp, i64, i64, ctypes.POINTER(i64)],
         "oracle_splitmix64": [u64, ctypes.POINTER(u64)],
         "oracle_set_strata": [vp, i32],
+        "oracle_set_value_bound": [vp, dbl],
+        "oracle_set_eta_decay": [vp, i32],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -94,7 +96,8 @@ def _c(a, dtype):
 class Oracle:
     """Clocked SSP/ESSP MF-SGD on the CPU; mirrors the library's call sequence."""
 
-    def __init__(self, N, M, K, P, s, eta, lam, policy=SSP_LAZY, step=ROWMEAN, B=1, seed=0, owner=None, strata=None):
+    def __init__(self, N, M, K, P, s, eta, lam, policy=SSP_LAZY, step=ROWMEAN, B=1, seed=0, owner=None, strata=None,
+                 value_bound=None, eta_decay=False):
         self._lib = _load()
         self.N, self.M, self.K, self.P, self.s = int(N), int(M), int(K), int(P), int(s)
         self._owner = None if owner is None else _c(owner, np.int32)
@@ -106,6 +109,10 @@ class Oracle:
         self._h = h
         if strata is not None:
             _chk(self._lib.oracle_set_strata(self._h, int(strata)), "oracle_set_strata")
+        if value_bound is not None:
+            _chk(self._lib.oracle_set_value_bound(self._h, float(value_bound)), "oracle_set_value_bound")
+        if eta_decay:
+            _chk(self._lib.oracle_set_eta_decay(self._h, 1), "oracle_set_eta_decay")
 
     def close(self):
         if self._h:
@@ -177,7 +184,8 @@ class Oracle:
     def export(self, kind, block=0):
         n = ctypes.c_int64()
         _chk(self._lib.oracle_export(self._h, kind, block, None, 0, ctypes.byref(n)), "oracle_export")
-        dt = np.int32 if kind in (X_OWNER, X_COL, X_USER_COUNT, X_ITEM_COUNT) else np.int64
+        dt = (np.int32 if kind in (X_OWNER, X_COL, X_USER_COUNT, X_ITEM_COUNT) else
+              np.float64 if kind == X_VAP_NORMS else np.int64)
         buf = np.empty(n.value, dtype=dt)
         _chk(self._lib.oracle_export(self._h, kind, block, buf.ctypes.data if n.value else None, n.value,
                                      ctypes.byref(n)), "oracle_export")

@@ -30,6 +30,12 @@
  *     is fetched at version c, else the cached version is read.  ESSP_ROW (ESSPTable: the
  *     server pushes every registered row once all clients ticked; the push lands one
  *     clock later): the first read fetches version c, later reads see c - min(s, 1);
+ *   - or VAP (Section 2.1 / Section 3, the VAP condition): the in-transit updates of a
+ *     view, x_c - x_v, must satisfy |x_c - x_v|_inf <= v_t = v0 / sqrt(t), t = c + 1; every
+ *     worker reads the stalest version v = c - d, d <= min(c, s), within that bound (the
+ *     max-norm of fp32 differences, compared in fp64);
+ *   - optional step schedule eta_c = eta / sqrt(c + 1) (the schedule of Section 3's
+ *     theorems), else constant eta;
  *   - step normalisation: SUM uses the summed per-rating steps; ROWMEAN divides each
  *     row's summed contribution by that row's rating count in the clock's minibatch;
  *   - or SEQ: each worker applies the Section 3.1 update rating by rating to its own copy
@@ -63,10 +69,10 @@
 #define OR_ENOMEM -2
 #define OR_ESTATE -4
 
-enum { OR_LAZY = 0, OR_WORST = 1, OR_ESSP = 2, OR_SSP_ROW = 3, OR_ESSP_ROW = 4 };
+enum { OR_LAZY = 0, OR_WORST = 1, OR_ESSP = 2, OR_SSP_ROW = 3, OR_ESSP_ROW = 4, OR_VAP = 5 };
 enum { OR_ROWMEAN = 0, OR_SUM = 1, OR_SEQ = 2 };
 enum { OR_X_OWNER = 0, OR_X_ROW_PTR = 1, OR_X_COL = 2, OR_X_PERM = 3, OR_X_USER_COUNT = 4, OR_X_ITEM_COUNT = 5,
-       OR_X_VERSION_LOG = 6, OR_X_STALENESS = 7, OR_X_ROW_VERSIONS = 8, OR_X_SEQ_ORDER = 9 };
+       OR_X_VERSION_LOG = 6, OR_X_STALENESS = 7, OR_X_ROW_VERSIONS = 8, OR_X_SEQ_ORDER = 9, OR_X_VAP_NORMS = 10 };
 
 typedef struct {
   int64_t N, M;
@@ -110,6 +116,13 @@ typedef struct {
   int64_t *sorder;
   double *Lloc, *Rloc;
   uint8_t *utouch, *itouch; /* N, P*M */
+  /* policy VAP: the value bound v0, the delay d of each clock run and, per clock, the
+     in-transit norms |x_c - x_{c-d}|_inf for d = 0..s (-1 where c - d < 0) */
+  double v0;
+  int64_t *vap_d;
+  double *vap_norm;
+  int64_t vap_cap;
+  int eta_decay;
 } oracle_t;
 
 /* SplitMix64 (Steele, Lea & Flood 2014): one step of the sequential generator from `state`. */
@@ -138,6 +151,7 @@ static int64_t delay_of(const oracle_t *o, int64_t p, int64_t c) {
   switch (o->policy) {
     case OR_LAZY: return (c + p % (s + 1)) % (s + 1);
     case OR_WORST: return s;
+    case OR_VAP: return o->vap_d[c]; /* chosen when clock c starts */
     default: return s < 1 ? s : 1; /* ESSP */
   }
 }
@@ -161,6 +175,7 @@ static int64_t row_read(const oracle_t *o, int64_t cached, int64_t c) {
 
 int oracle_view_version(const oracle_t *o, int64_t p, int64_t c, int64_t *v) {
   if (!o || p < 0 || p >= o->P || c < 0 || per_row(o)) return OR_EINVAL;
+  if (o->policy == OR_VAP && c >= o->clock) return OR_EINVAL; /* chosen when the clock runs */
   *v = view_version(o, p, c);
   return OR_OK;
 }
@@ -172,6 +187,7 @@ void oracle_destroy(oracle_t *o) {
   free(o->Lring); free(o->Rring); free(o->vlog); free(o->dL); free(o->dR); free(o->stale);
   free(o->ucache); free(o->icache); free(o->iread);
   free(o->sorder); free(o->Lloc); free(o->Rloc); free(o->utouch); free(o->itouch);
+  free(o->vap_d); free(o->vap_norm);
   free(o);
 }
 
@@ -180,15 +196,16 @@ int oracle_create(int64_t N, int64_t M, int32_t K, int32_t P, int32_t s, double 
   if (!out) return OR_EINVAL;
   *out = NULL;
   if (N <= 0 || M <= 0 || K <= 0 || P <= 0 || s < 0 || B < 1 || N > 0x7fffffff || M > 0x7fffffff) return OR_EINVAL;
-  if (policy < OR_LAZY || policy > OR_ESSP_ROW || step < OR_ROWMEAN || step > OR_SEQ) return OR_EINVAL;
+  if (policy < OR_LAZY || policy > OR_VAP || step < OR_ROWMEAN || step > OR_SEQ) return OR_EINVAL;
   /* sequential steps start from one view per (worker, clock): table policies only */
-  if (step == OR_SEQ && policy > OR_ESSP) return OR_EINVAL;
+  if (step == OR_SEQ && (policy == OR_SSP_ROW || policy == OR_ESSP_ROW)) return OR_EINVAL;
   if (!isfinite(eta) || !isfinite(lambda)) return OR_EINVAL;
   oracle_t *o = (oracle_t *)calloc(1, sizeof(oracle_t));
   if (!o) return OR_ENOMEM;
   o->N = N; o->M = M; o->K = K; o->P = P; o->s = s; o->eta = eta; o->lambda = lambda;
   o->policy = policy; o->step = step; o->B = B; o->seed = seed;
   o->G = 256;
+  o->v0 = INFINITY;
   o->owner = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
   o->stale = (int64_t *)calloc((size_t)s + 1, sizeof(int64_t));
   o->C = P < (int64_t)s + 1 ? P : (int64_t)s + 1;
@@ -212,6 +229,22 @@ int oracle_set_strata(oracle_t *o, int32_t G) {
   if (!o || G < 1) return OR_EINVAL;
   if (o->loaded) return OR_ESTATE;
   o->G = G;
+  return OR_OK;
+}
+
+/* the value bound v0 of the VAP policy (default: unbounded); before load; v0 >= 0 */
+int oracle_set_value_bound(oracle_t *o, double v0) {
+  if (!o || !(v0 >= 0)) return OR_EINVAL;
+  if (o->loaded) return OR_ESTATE;
+  o->v0 = v0;
+  return OR_OK;
+}
+
+/* step schedule eta_c = eta / sqrt(c + 1) (on != 0) or constant eta; before load */
+int oracle_set_eta_decay(oracle_t *o, int32_t on) {
+  if (!o) return OR_EINVAL;
+  if (o->loaded) return OR_ESTATE;
+  o->eta_decay = on != 0;
   return OR_OK;
 }
 
@@ -336,7 +369,7 @@ static float *R_of(const oracle_t *o, int64_t v) { return o->Rring + (size_t)(v 
 /* the SEQ step of one clock: every worker runs its ratings in its order on its own copies
    of the rows, which start at its view; dL and dR receive sum over workers of
    (copy - view) for the rows each touched */
-static int seq_sweep(oracle_t *o, int64_t c, int32_t b) {
+static int seq_sweep(oracle_t *o, int64_t c, int32_t b, double eta) {
   const int64_t K = o->K, M = o->M;
   if (!o->Lloc) {
     o->Lloc = (double *)malloc(sizeof(double) * (size_t)(o->N * K));
@@ -366,8 +399,8 @@ static int seq_sweep(oracle_t *o, int64_t c, int32_t b) {
     const double e = (double)o->val[t] - dot;
     for (int64_t k = 0; k < K; ++k) {
       const double l = Li[k], r = Rj[k];
-      Li[k] = l + o->eta * (e * r - o->lambda * l);
-      Rj[k] = r + o->eta * (e * l - o->lambda * r);
+      Li[k] = l + eta * (e * r - o->lambda * l);
+      Rj[k] = r + eta * (e * l - o->lambda * r);
     }
   }
   for (int64_t i = 0; i < o->N; ++i) {
@@ -388,10 +421,49 @@ static int seq_sweep(oracle_t *o, int64_t c, int32_t b) {
   return OR_OK;
 }
 
+/* VAP: the delay of clock c, the largest d <= min(c, s) whose in-transit updates
+   x_c - x_{c-d} stay within v0 / sqrt(c + 1) in max-norm (d = 0 always does) */
+static int vap_choose(oracle_t *o, int64_t c) {
+  const int64_t S1 = (int64_t)o->s + 1;
+  if (c >= o->vap_cap) {
+    int64_t cap = o->vap_cap ? 2 * o->vap_cap : 64;
+    while (cap <= c) cap *= 2;
+    int64_t *nd = (int64_t *)realloc(o->vap_d, sizeof(int64_t) * (size_t)cap);
+    if (!nd) return OR_ENOMEM;
+    o->vap_d = nd;
+    double *nn = (double *)realloc(o->vap_norm, sizeof(double) * (size_t)(cap * S1));
+    if (!nn) return OR_ENOMEM;
+    o->vap_norm = nn;
+    o->vap_cap = cap;
+  }
+  const double bound = o->v0 / sqrt((double)(c + 1));
+  int64_t d = 0;
+  for (int64_t k = 0; k < S1; ++k) {
+    double nrm = -1.0;
+    if (k <= c) {
+      float m = 0.0f;
+      const float *a = L_of(o, c), *b = L_of(o, c - k);
+      for (int64_t x = 0; x < o->N * o->K; ++x) { float t = fabsf(a[x] - b[x]); if (t > m) m = t; }
+      a = R_of(o, c); b = R_of(o, c - k);
+      for (int64_t x = 0; x < o->M * o->K; ++x) { float t = fabsf(a[x] - b[x]); if (t > m) m = t; }
+      nrm = (double)m;
+      if (nrm <= bound) d = k;
+    }
+    o->vap_norm[c * S1 + k] = nrm;
+  }
+  o->vap_d[c] = d;
+  return OR_OK;
+}
+
 /* one clock: every worker computes its update from its view; the sum is committed */
 static int one_clock(oracle_t *o) {
   const int64_t c = o->clock, K = o->K;
   const int32_t b = (int32_t)(c % o->B);
+  if (o->policy == OR_VAP) {
+    int rc = vap_choose(o, c);
+    if (rc) return rc;
+  }
+  const double eta_c = o->eta_decay ? o->eta / sqrt((double)(c + 1)) : o->eta;
   memset(o->dL, 0, sizeof(double) * (size_t)(o->N * K));
   memset(o->dR, 0, sizeof(double) * (size_t)(o->M * K));
   if (per_row(o)) {
@@ -409,7 +481,7 @@ static int one_clock(oracle_t *o) {
       }
   }
   if (o->step == OR_SEQ) {
-    int rc = seq_sweep(o, c, b);
+    int rc = seq_sweep(o, c, b, eta_c);
     if (rc) return rc;
   }
   for (int64_t q = o->bstart[b]; q < o->bstart[b + 1] && o->step != OR_SEQ; ++q) {
@@ -433,8 +505,8 @@ static int one_clock(oracle_t *o) {
     const double si = (o->step == OR_ROWMEAN) ? 1.0 / (double)o->icount[(int64_t)b * o->M + j] : 1.0;
     double *dLi = o->dL + i * K, *dRj = o->dR + j * K;
     for (int64_t k = 0; k < K; ++k) {
-      dLi[k] += o->eta * su * (e * (double)Rj[k] - o->lambda * (double)Li[k]);
-      dRj[k] += o->eta * si * (e * (double)Li[k] - o->lambda * (double)Rj[k]);
+      dLi[k] += eta_c * su * (e * (double)Rj[k] - o->lambda * (double)Li[k]);
+      dRj[k] += eta_c * si * (e * (double)Li[k] - o->lambda * (double)Rj[k]);
     }
   }
   /* log the versions read at this clock (one per worker: table-level policies only) */
@@ -514,6 +586,7 @@ int oracle_rows_from_v0(const oracle_t *o, int32_t nclocks, int64_t nu, const in
   const int64_t K = o->K;
   if (per_row(o) && nclocks > 1) return OR_EINVAL; /* only clock 0 surely reads version 0 */
   if (o->step == OR_SEQ) return OR_EINVAL;        /* rows of a SEQ clock depend on whole chains */
+  if (o->policy == OR_VAP || o->eta_decay) return OR_EINVAL;
   for (int64_t c = 0; c < nclocks && !per_row(o); ++c)
     for (int64_t p = 0; p < o->P; ++p)
       if (view_version(o, p, c) != 0) return OR_EINVAL;
@@ -572,10 +645,13 @@ bad:
  *   VERSION_LOG  int64 [clocks * P], entry c*P + p = v(p, c)
  *   SEQ_ORDER(b) int64 [nnz_b] (step SEQ) load indices in the order the workers apply
  *                them: (sub-epoch, worker, user group, canonical)
+ *   VAP_NORMS    double [clocks * (s+1)] (policy VAP) entry c*(s+1) + d = the in-transit
+ *                norm |x_c - x_{c-d}|_inf seen when clock c started, -1 where c - d < 0
  */
 int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t cap, int64_t *len) {
   if (!o || !len) return OR_EINVAL;
-  if (kind != OR_X_OWNER && kind != OR_X_VERSION_LOG && kind != OR_X_STALENESS && kind != OR_X_ROW_VERSIONS) {
+  if (kind != OR_X_OWNER && kind != OR_X_VERSION_LOG && kind != OR_X_STALENESS && kind != OR_X_ROW_VERSIONS &&
+      kind != OR_X_VAP_NORMS) {
     if (!o->loaded) return OR_ESTATE;
     if (b < 0 || b >= o->B) return OR_EINVAL;
   }
@@ -592,6 +668,10 @@ int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t
     case OR_X_SEQ_ORDER:
       if (o->step != OR_SEQ) return OR_EINVAL;
       n = o->bstart[b + 1] - o->bstart[b];
+      break;
+    case OR_X_VAP_NORMS:
+      if (o->policy != OR_VAP) return OR_EINVAL;
+      n = o->clock * ((int64_t)o->s + 1);
       break;
     default: return OR_EINVAL;
   }
@@ -619,6 +699,7 @@ int oracle_export(const oracle_t *o, int32_t kind, int32_t b, void *buf, int64_t
       memcpy((int64_t *)buf + o->N, o->icache, sizeof(int64_t) * (size_t)(o->C * o->M));
       break;
     case OR_X_SEQ_ORDER: if (n) memcpy(buf, o->sorder + o->bstart[b], sizeof(int64_t) * (size_t)n); break;
+    case OR_X_VAP_NORMS: if (n) memcpy(buf, o->vap_norm, sizeof(double) * (size_t)n); break;
   }
   return OR_OK;
 }

@@ -45,8 +45,22 @@ def delay(policy, p, c, s):
     return min(s, 1)
 
 
+def vap_delay(hist, c, s, v0):
+    """The value-bounded view: the largest d <= min(c, s) with max |x_c - x_{c-d}| (fp32
+    differences of the stored versions) <= v0 / sqrt(c + 1)."""
+    bound = v0 / np.sqrt(c + 1.0)
+    d = 0
+    for k in range(0, min(c, s) + 1):
+        diff = max(np.abs(hist[c][0] - hist[c - k][0]).max(initial=0), np.abs(hist[c][1] - hist[c - k][1]).max(initial=0))
+        if float(diff) <= bound:
+            d = k
+    return d
+
+
 def run_dense(user, item, val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, policy=0, step=0, B=1, seed=0,
-              owner=None):
+              owner=None, vap_v0=None, eta_decay=False):
+    """policy 0/1/2: SSP_LAZY / SSP_WORST / ESSP delays; vap_v0: the value-bounded view
+    instead; eta_decay: step eta / sqrt(c + 1) at clock c."""
     owner = np.arange(N) % P if owner is None else np.asarray(owner)
     blocks = np.array([block_of(i, j, seed, B) for i, j in zip(user, item)]) if B > 1 else None
     mats = [dense_mats(user, item, val, N, M, blocks, b) for b in range(B)]
@@ -56,11 +70,12 @@ def run_dense(user, item, val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, polic
         nu, ni = W.sum(1), W.sum(0)
         dL = np.zeros((N, K))
         dR = np.zeros((M, K))
+        d_vap = vap_delay(hist, c, s, vap_v0) if vap_v0 is not None else None
         for p in range(P):
             rows = owner == p
             if not rows.any():
                 continue
-            v = max(0, c - delay(policy, p, c, s))
+            v = max(0, c - (d_vap if d_vap is not None else delay(policy, p, c, s)))
             Lv, Rv = (x.astype(np.float64) for x in hist[v])
             Wp = W * rows[:, None]
             E = Wp * (D - Lv @ Rv.T)
@@ -72,8 +87,9 @@ def run_dense(user, item, val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, polic
             dL /= np.where(nu > 0, nu, 1)[:, None]
             dR /= np.where(ni > 0, ni, 1)[:, None]
         Lc, Rc = hist[c]
-        hist.append(((Lc.astype(np.float64) + eta * dL).astype(np.float32),
-                     (Rc.astype(np.float64) + eta * dR).astype(np.float32)))
+        eta_c = eta / np.sqrt(c + 1.0) if eta_decay else eta
+        hist.append(((Lc.astype(np.float64) + eta_c * dL).astype(np.float32),
+                     (Rc.astype(np.float64) + eta_c * dR).astype(np.float32)))
     return hist
 
 

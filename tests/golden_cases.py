@@ -4,7 +4,7 @@ import os
 import numpy as np
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
-POLICIES = {"LAZY": 0, "WORST": 1, "ESSP": 2}
+POLICIES = {"LAZY": 0, "WORST": 1, "ESSP": 2, "VAP": 5}
 STEPS = {"ROWMEAN": 0, "SUM": 1, "SEQ": 2}
 
 
@@ -21,7 +21,8 @@ def load_cases(fname="hand_examples.txt"):
                 cur = dict(name=tok[1], N=int(kv["N"]), M=int(kv["M"]), K=int(kv["K"]), P=int(kv["P"]),
                            s=int(kv["s"]), eta=float(kv["eta"]), lam=float(kv["lam"]),
                            policy=POLICIES[kv["policy"]], step=STEPS[kv["step"]], ratings=[], owner=None,
-                           expect=[], strata=int(kv["strata"]) if "strata" in kv else None)
+                           expect=[], strata=int(kv["strata"]) if "strata" in kv else None,
+                           v0=float(kv["v0"]) if "v0" in kv else None)
             elif tok[0] == "rating":
                 cur["ratings"].append((int(tok[1]), int(tok[2]), float(tok[3])))
             elif tok[0] in ("L0", "R0"):

@@ -36,7 +36,8 @@ def test_hand_examples(case):
     i = np.array([r[1] for r in case["ratings"]], np.int32)
     v = np.array([r[2] for r in case["ratings"]], np.float32)
     o = oracle.Oracle(case["N"], case["M"], case["K"], case["P"], case["s"], case["eta"], case["lam"],
-                      case["policy"], case["step"], 1, 0, case["owner"], strata=case["strata"])
+                      case["policy"], case["step"], 1, 0, case["owner"], strata=case["strata"],
+                      value_bound=case["v0"])
     o.load(u, i, v)
     o.set_factors(case["L0"], case["R0"])
     for ex in sorted(case["expect"], key=lambda e: e["clock"]):
@@ -669,4 +670,105 @@ def test_seq_argument_errors():
     o.load(np.array([0], np.int32), np.array([1], np.int32), np.array([1.0], np.float32))
     with pytest.raises(oracle.OracleError):
         o.export(oracle.X_SEQ_ORDER)
+    o.close()
+
+
+# ---------------------------------------------------------------- value-bounded views (VAP) and eta / sqrt(t)
+def run_oracle(user, item, val, L0, R0, N, M, K, P, s, clocks, policy, step=oracle.ROWMEAN, B=1, seed=0, **kw):
+    o = oracle.Oracle(N, M, K, P, s, 0.05, 0.05, policy, step, B, seed, **kw)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(clocks)
+    L, R = o.get_factors()
+    out = (L, R, o.export(oracle.X_VERSION_LOG), o.export(oracle.X_STALENESS))
+    o.close()
+    return out
+
+
+@pytest.mark.parametrize("step,B", [(oracle.ROWMEAN, 1), (oracle.SUM, 3), (oracle.SEQ, 2)])
+@pytest.mark.parametrize("s", [1, 3])
+def test_vap_unbounded_is_ssp_worst_and_zero_bound_is_bsp(step, B, s):
+    # Section 3 (VAP): with no bound every view may miss the whole window, i.e. the oldest
+    # version the ring holds (SSP_WORST); with bound 0 no update may be in transit (BSP)
+    rng = np.random.default_rng(s + 7 * B)
+    N, M, K, P = 30, 20, 3, 4
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 250, K)
+    args = (user, item, val, L0, R0, N, M, K, P)
+    wide = run_oracle(*args, s, 8, oracle.VAP, step, B, 3, value_bound=float("inf"))
+    worst = run_oracle(*args, s, 8, oracle.SSP_WORST, step, B, 3)
+    tight = run_oracle(*args, s, 8, oracle.VAP, step, B, 3, value_bound=0.0)
+    bsp = run_oracle(*args, 0, 8, oracle.SSP_WORST, step, B, 3)
+    for a, b in zip(wide, worst):
+        assert np.array_equal(a, b)
+    for a, b in zip(tight[:3], bsp[:3]):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("v0,s,P,step", [(0.1, 3, 3, oracle.ROWMEAN), (0.5, 2, 1, oracle.SUM),
+                                         (0.2, 4, 5, oracle.ROWMEAN)])
+def test_vap_matches_the_dense_brute_force(v0, s, P, step):
+    # the dense matrix-algebra form, choosing each clock's view from its own history
+    rng = np.random.default_rng(int(v0 * 1000) + s)
+    N, M, K = 12, 9, 3
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 70, K)
+    o = oracle.Oracle(N, M, K, P, s, 0.05, 0.05, oracle.VAP, step, value_bound=v0)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(10)
+    L, R = o.get_factors()
+    vlog = o.export(oracle.X_VERSION_LOG).reshape(10, P)
+    hist = run_dense(user, item, val, L0, R0, N=N, M=M, K=K, P=P, s=s, eta=0.05, lam=0.05, clocks=10, step=step,
+                     vap_v0=v0)
+    np.testing.assert_allclose(L, hist[10][0], rtol=0, atol=1e-6)
+    np.testing.assert_allclose(R, hist[10][1], rtol=0, atol=1e-6)
+    # the views really vary: some clocks read stale versions, some fresh
+    d = np.arange(10)[:, None] - vlog
+    assert (d > 0).any() and (d[1:] == 0).any()
+    o.close()
+
+
+def test_vap_views_satisfy_the_value_bound_and_are_the_stalest_that_do():
+    rng = np.random.default_rng(12)
+    N, M, K, P, s, v0 = 25, 15, 2, 3, 3, 0.03
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 150, K)
+    o = oracle.Oracle(N, M, K, P, s, 0.05, 0.05, oracle.VAP, oracle.ROWMEAN, value_bound=v0)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    for c in range(12):
+        vers = {k: o.get_version(c - k) for k in range(0, min(c, s) + 1)}
+        o.clock(1)
+        v = int(o.export(oracle.X_VERSION_LOG)[-1])
+        norm = lambda k: max(np.abs(vers[0][0] - vers[k][0]).max(), np.abs(vers[0][1] - vers[k][1]).max())
+        bound = v0 / np.sqrt(c + 1.0)
+        assert norm(c - v) <= bound
+        assert all(norm(k) > bound for k in vers if k > c - v)
+        norms = o.export(oracle.X_VAP_NORMS).reshape(-1, s + 1)[c]
+        assert all(norms[k] == norm(k) for k in vers)
+    o.close()
+
+
+@pytest.mark.parametrize("step,policy,s", [(oracle.ROWMEAN, oracle.SSP_LAZY, 0), (oracle.SUM, oracle.SSP_WORST, 2)])
+def test_eta_decay_matches_the_dense_brute_force(step, policy, s):
+    # the step schedule of Section 3's theorems, eta_t = eta / sqrt(t), t = c + 1
+    rng = np.random.default_rng(4)
+    N, M, K = 10, 8, 3
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 50, K)
+    o = oracle.Oracle(N, M, K, 2, s, 0.05, 0.05, policy, step, eta_decay=True)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(6)
+    L, R = o.get_factors()
+    o.close()
+    hist = run_dense(user, item, val, L0, R0, N=N, M=M, K=K, P=2, s=s, eta=0.05, lam=0.05, clocks=6, step=step,
+                     policy=policy, eta_decay=True)
+    np.testing.assert_allclose(L, hist[6][0], rtol=0, atol=1e-6)
+    np.testing.assert_allclose(R, hist[6][1], rtol=0, atol=1e-6)
+
+
+def test_vap_argument_errors():
+    with pytest.raises(oracle.OracleError):
+        oracle.Oracle(4, 4, 2, 2, 1, 0.1, 0.0, oracle.VAP, oracle.ROWMEAN, value_bound=-1.0)
+    o = oracle.Oracle(4, 4, 2, 2, 1, 0.1, 0.0, oracle.SSP_LAZY, oracle.ROWMEAN)
+    with pytest.raises(oracle.OracleError):
+        o.export(oracle.X_VAP_NORMS)
     o.close()
