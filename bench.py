@@ -27,7 +27,7 @@ if ROOT not in sys.path:
 
 PEAK_FP32_VECTOR_TFLOPS = 157.3   # MI355X published fp32 vector peak (packed FMA)
 PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
-POLICIES = {"lazy": 0, "worst": 1, "essp": 2, "ssp_row": 3, "essp_row": 4}
+POLICIES = {"lazy": 0, "worst": 1, "essp": 2, "ssp_row": 3, "essp_row": 4, "vap": 5}
 STEPS = {"rowmean": 0, "sum": 1, "seq": 2}
 
 
@@ -43,6 +43,8 @@ def parse():
                     help="rowmean/sum: one fixed view per worker and clock; seq: every worker applies its "
                          "ratings one by one to its own rows")
     ap.add_argument("--strata", type=int, default=None, help="sub-epochs per clock of the seq step")
+    ap.add_argument("--value-bound", type=float, default=None, help="v0 of the vap policy (v_t = v0 / sqrt(t))")
+    ap.add_argument("--eta-decay", action="store_true", help="step eta / sqrt(c + 1) at clock c")
     ap.add_argument("--cpu-sample", type=int, default=50_000_000,
                     help="ratings in the oracle's timed sample (0 disables the CPU baseline)")
     ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
@@ -64,7 +66,7 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(w, spec, K, s, policy, step, strata, nsample):
+def cpu_baseline(w, spec, K, s, policy, step, strata, value_bound, eta_decay, nsample):
     """The oracle, single-threaded, on the ratings of a prefix of users (one clock)."""
     import oracle
 
@@ -72,7 +74,7 @@ def cpu_baseline(w, spec, K, s, policy, step, strata, nsample):
     take = order[:nsample]
     u, i, v = w.user[take], w.item[take], w.val[take]
     o = oracle.Oracle(spec.N, spec.M, K, spec.P, s, spec.eta, spec.lam, policy, step, spec.B, spec.seed,
-                      strata=strata)
+                      strata=strata, value_bound=value_bound, eta_decay=eta_decay)
     o.load(u, i, v)
     o.set_factors(w.L0, w.R0)
     t0 = time.perf_counter()
@@ -130,7 +132,7 @@ def main():
     print(f"[bench] generated {args.config}: {w.nnz} ratings in {t_gen:.1f} s", file=sys.stderr, flush=True)
     stream = torch.cuda.current_stream()
     g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, step=step, strata=args.strata,
-                   B=spec.B,
+                   value_bound=args.value_bound, eta_decay=args.eta_decay, B=spec.B,
                    mb_seed=spec.seed, timing=not args.no_timing, stream=stream, tile_bytes=args.tile_bytes,
                    unit_max=args.unit_max, cells=args.cells, heavy_min=args.heavy_min, hot_steps=args.hot_steps,
                    two_streams=args.two_streams, dense_min=args.dense_min)
@@ -208,7 +210,8 @@ def main():
     cpu = None
     if args.cpu_sample > 0:
         print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, spec, K, s, policy, step, args.strata, min(args.cpu_sample, w.nnz))
+        cpu = cpu_baseline(w, spec, K, s, policy, step, args.strata, args.value_bound, args.eta_decay,
+                           min(args.cpu_sample, w.nnz))
 
     line = {
         "metric": "rating-updates/sec at K=128, 100M ratings (1 GPU); % of HBM roofline",
@@ -225,7 +228,9 @@ def main():
         "data": "synthetic (seeded, Netflix-shaped)",
         "config": {"workload": f"{args.config}: {spec.N} users x {spec.M} items, {w.nnz} ratings, K={K}, "
                                f"P={spec.P}, s={s}, policy={args.policy}, B={spec.B}, eta={spec.eta}, "
-                               f"lambda={spec.lam}" + (f", step=seq, strata={args.strata or 256}" if seq else ""),
+                               f"lambda={spec.lam}" + (f", step=seq, strata={args.strata or 256}" if seq else "") +
+                               (f", v0={args.value_bound}" if args.policy == "vap" else "") +
+                               (", eta/sqrt(t)" if args.eta_decay else ""),
                    "global_batch": int(nnz_clock), "parallelism": "1 GPU, P logical workers",
                    "loss_after": loss,
                    **({"chains_runs_ratings": [int(x) for x in split[:3]]} if seq else

@@ -70,7 +70,7 @@ typedef struct ps_mf ps_mf_t;
 
 /* option keys (ps_mf_set_option); all must be set before ps_mf_load_ratings */
 #define PS_MF_OPT_POLICY 1    /* PS_MF_SSP_LAZY (default), PS_MF_SSP_WORST, PS_MF_ESSP, PS_MF_SSP_ROW,
-                                 PS_MF_ESSP_ROW */
+                                 PS_MF_ESSP_ROW, PS_MF_VAP */
 #define PS_MF_OPT_STEP 2      /* PS_MF_STEP_ROWMEAN (default), PS_MF_STEP_SUM, PS_MF_STEP_SEQ (table
                                  policies only: with a per-row policy ps_mf_load_ratings fails
                                  with PS_MF_EINVAL) */
@@ -104,6 +104,8 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_OPT_SEQ_STRATA 14 /* G: sub-epochs per clock of PS_MF_STEP_SEQ (default 256), in
                                    [1, 4096].  Part of the semantics: it fixes the order in which
                                    a worker applies its ratings */
+#define PS_MF_OPT_ETA_DECAY 15  /* 1: step eta / sqrt(c + 1) at clock c (the schedule of Section 3's
+                                   theorems); 0 (default): constant eta */
 
 /* Views (Section 3.2 SSP condition; Section 4 ESSPTable).  The table-level policies give
    worker p at clock c one whole version v = max(0, c - d):
@@ -118,12 +120,20 @@ typedef struct ps_mf ps_mf_t;
      PS_MF_ESSP_ROW  the first read fetches version c, later reads see the server's push of
                      version c - min(s, 1) (ESSPTable).
    Under the per-row policies the version log stays empty; PS_MF_IDX_STALENESS and
-   PS_MF_IDX_ROW_VERSIONS report the reads. */
+   PS_MF_IDX_ROW_VERSIONS report the reads.
+   The value-bounded policy (Section 2.1 and Section 3, the VAP condition: the in-transit
+   updates of a worker's view are bounded in max-norm by v_t = v0 / sqrt(t)):
+     PS_MF_VAP       every worker reads the stalest version v = c - d, d <= min(c, s), with
+                     |x_c - x_v|_inf <= v0 / sqrt(c + 1); the norm is the maximum of the fp32
+                     differences of the stored versions, compared in fp64.  v0 is set by
+                     ps_mf_set_value_bound (default: unbounded, i.e. PS_MF_SSP_WORST);
+                     s bounds how far back the ring reaches. */
 #define PS_MF_SSP_LAZY 0
 #define PS_MF_SSP_WORST 1
 #define PS_MF_ESSP 2
 #define PS_MF_SSP_ROW 3
 #define PS_MF_ESSP_ROW 4
+#define PS_MF_VAP 5
 
 #define PS_MF_STEP_ROWMEAN 0
 #define PS_MF_STEP_SUM 1
@@ -161,6 +171,9 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_IDX_SEQ_ORDER 10  /* int64 [nnz_b] under PS_MF_STEP_SEQ: load indices of block b in the
                                    order the workers apply them, (sub-epoch, worker, user group,
                                    user, item, load index); other steps: PS_MF_EINVAL */
+#define PS_MF_IDX_VAP_NORMS 11  /* double [clocks * (s+1)] under PS_MF_VAP: entry c*(s+1) + d is the
+                                   in-transit norm |x_c - x_{c-d}|_inf when clock c started
+                                   (-1 where c - d < 0); other policies: PS_MF_EINVAL */
 
 /* kernel ids (ps_mf_kernel_time) */
 #define PS_MF_KERNEL_SWEEP 0  /* residual, dL segment-sum and dR accumulation of one clock */
@@ -179,6 +192,11 @@ int ps_mf_create(int64_t users, int64_t items, int32_t K, int32_t P, int32_t s, 
 /* Set an option (keys above) before ps_mf_load_ratings; ESTATE after it, EINVAL for an
    unknown key or value. */
 int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value);
+
+/* The value bound v0 of PS_MF_VAP (Section 3: v_t = v0 / sqrt(t), t = c + 1 at clock c);
+   v0 >= 0, INFINITY allowed (the default).  Before load: ESTATE after it, EINVAL for a
+   negative or NaN bound. */
+int ps_mf_set_value_bound(ps_mf_t *h, double v0);
 
 /* Optional explicit data partition (Section 3.1: ratings partitioned over workers):
    owner[users] with values in [0, P); default owner(i) = i mod P.  Before load. */

@@ -956,6 +956,57 @@ __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, 
     commit_item(ca, static_cast<int64_t>(blockIdx.x) - grid_users, red);
 }
 
+// ------------------------------------------------------------------ value-bounded views
+// VAP (Section 3's condition on in-transit updates): at clock c every worker reads the
+// stalest version v = c - d, d <= min(c, s), with |x_c - x_v|_inf <= v0 / sqrt(c + 1).
+// k_vap_norms reduces, for d = 1 .. dmax, the max of the fp32 differences between the
+// slots of versions c and c - d (padding columns are zero in every slot) into this
+// clock's entry of the norm log (float bits, atomicMax over non-negative floats; NaN is
+// ignored); k_vap_pick then writes the slot the sweeps read and the version log entry.
+struct VapArgs {
+  const float *ring;
+  int64_t slot_stride;
+  int64_t n4;          // float4s of one slot
+  int64_t c;
+  int32_t S1, dmax;
+  unsigned *norms;     // [S1] this clock's norms
+};
+
+__global__ __launch_bounds__(kBlock) void k_vap_norms(VapArgs a) {
+  __shared__ float red[kBlock / 64];
+  const float4 *r4 = reinterpret_cast<const float4 *>(a.ring);
+  const int64_t ss4 = a.slot_stride / 4;
+  const int32_t slot_c = static_cast<int32_t>(a.c % a.S1);
+  for (int d = 1; d <= a.dmax; ++d) {
+    const int32_t sd = static_cast<int32_t>((a.c - d) % a.S1);
+    float m = 0.f;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < a.n4;
+         i += static_cast<int64_t>(gridDim.x) * kBlock) {
+      const float4 x = r4[slot_c * ss4 + i], y = r4[sd * ss4 + i];
+      m = fmaxf(m, fmaxf(fmaxf(fabsf(x.x - y.x), fabsf(x.y - y.y)), fmaxf(fabsf(x.z - y.z), fabsf(x.w - y.w))));
+    }
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x / 64] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float t = red[0];
+      for (int w = 1; w < kBlock / 64; ++w) t = fmaxf(t, red[w]);
+      atomicMax(a.norms + d, __float_as_uint(t));
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void k_vap_pick(const unsigned *norms, int32_t dmax, double bound, int64_t c, int32_t S1, int32_t *slot,
+                           int64_t *vlog) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  int32_t d = 0;
+  for (int32_t k = 1; k <= dmax; ++k)
+    if (static_cast<double>(__uint_as_float(norms[k])) <= bound) d = k;
+  slot[0] = static_cast<int32_t>((c - d) % S1);
+  vlog[c] = c - d;
+}
+
 // ------------------------------------------------------------------ sequential step
 // Under STEP_SEQ every worker applies the Section 3.1 rule rating by rating to its own
 // copies of the rows.  A chain (one stratum: sub-epoch, worker, user group) is one
@@ -1350,6 +1401,8 @@ struct ps_mf {
   int64_t heavy_min = -1;        // ratings from which a user goes to the cells (-1: automatic)
   int32_t dense_min = -1;        // ratings from which a 64 x 64 tile goes to the MFMA cells (-1: automatic, 0: none)
   int32_t seq_groups = 256;      // sub-epochs of the sequential step
+  double v0 = INFINITY;          // value bound of the VAP policy
+  bool eta_decay = false;        // step eta / sqrt(c + 1) at clock c
   std::vector<int32_t> owner;
   // host state
   bool loaded = false, has_factors = false;
@@ -1380,6 +1433,11 @@ struct ps_mf {
   int32_t *slot_table = nullptr;  // [(2s+1) * nclass]
   int32_t *wcls = nullptr;        // [P] class of each worker
   float *lwork = nullptr, *rwork = nullptr;  // sequential step: user rows between runs, workers' item rows
+  // VAP: the slot of the current clock's view, the version read and the norms of every clock
+  int32_t *vap_slot = nullptr;
+  int64_t *vap_v = nullptr;
+  unsigned *vap_norms = nullptr;
+  int64_t vap_cap = 0;
   double *loss_partial = nullptr;
   int64_t loss_partial_len = 0;
   double *loss_out = nullptr;
@@ -1628,6 +1686,81 @@ int record_end(ps_mf_t *h, int kernel, hipEvent_t a) {
   return PS_MF_OK;
 }
 
+float eta_at(const ps_mf_t *h, int64_t c) {
+  return h->eta_decay ? static_cast<float>(static_cast<double>(h->eta) / std::sqrt(static_cast<double>(c + 1)))
+                      : h->eta;
+}
+
+// room in the VAP logs for clock c (the logs double; old buffers stay allocated until the
+// handle is destroyed)
+int vap_reserve(ps_mf_t *h, int64_t c) {
+  if (c < h->vap_cap) return PS_MF_OK;
+  int64_t cap = std::max<int64_t>(1024, 2 * h->vap_cap);
+  while (cap <= c) cap *= 2;
+  const size_t S1 = static_cast<size_t>(h->s) + 1;
+  int64_t *v = nullptr;
+  unsigned *nr = nullptr;
+  int r;
+  if ((r = dev_alloc(h, reinterpret_cast<void **>(&v), static_cast<size_t>(cap) * sizeof(int64_t))) ||
+      (r = dev_alloc(h, reinterpret_cast<void **>(&nr), static_cast<size_t>(cap) * S1 * sizeof(unsigned))))
+    return r;
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  HIP_TRY(h, hipMemset(nr, 0, static_cast<size_t>(cap) * S1 * sizeof(unsigned)));
+  if (h->vap_cap > 0) {
+    HIP_TRY(h, hipMemcpy(v, h->vap_v, static_cast<size_t>(h->vap_cap) * sizeof(int64_t), hipMemcpyDeviceToDevice));
+    HIP_TRY(h, hipMemcpy(nr, h->vap_norms, static_cast<size_t>(h->vap_cap) * S1 * sizeof(unsigned),
+                         hipMemcpyDeviceToDevice));
+  }
+  h->vap_v = v;
+  h->vap_norms = nr;
+  h->vap_cap = cap;
+  return PS_MF_OK;
+}
+
+// The ring slot each worker class reads at clock c: the slot table's row, or under VAP the
+// slot that k_vap_pick writes (after the norm reduction, on the handle's stream).
+int clock_views(ps_mf_t *h, int64_t c, const int32_t **cls_slot) {
+  if (h->policy != PS_MF_VAP) {
+    *cls_slot = h->slot_table + table_row(h, c) * h->nclass;
+    return PS_MF_OK;
+  }
+  int r = vap_reserve(h, c);
+  if (r) return r;
+  const int32_t S1 = h->s + 1, dmax = static_cast<int32_t>(std::min<int64_t>(c, h->s));
+  unsigned *norms = h->vap_norms + c * S1;
+  if (dmax > 0) {
+    VapArgs a{};
+    a.ring = h->ring;
+    a.slot_stride = (h->N + h->M) * h->Kp;
+    a.n4 = a.slot_stride / 4;
+    a.c = c;
+    a.S1 = S1;
+    a.dmax = dmax;
+    a.norms = norms;
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(2048, (a.n4 + kBlock - 1) / kBlock));
+    hipLaunchKernelGGL(k_vap_norms, dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, h->stream, a);
+    HIP_TRY(h, hipGetLastError());
+  }
+  const double bound = h->v0 / std::sqrt(static_cast<double>(c + 1));
+  hipLaunchKernelGGL(k_vap_pick, dim3(1), dim3(64), 0, h->stream, norms, dmax, bound, c, S1, h->vap_slot, h->vap_v);
+  HIP_TRY(h, hipGetLastError());
+  *cls_slot = h->vap_slot;
+  return PS_MF_OK;
+}
+
+// the version log under VAP lives on the device: rebuild the host copy (P entries a clock)
+int vap_sync_log(ps_mf_t *h) {
+  if (h->policy != PS_MF_VAP) return PS_MF_OK;
+  h->vlog.clear();
+  if (h->clock == 0 || !h->vap_v) return PS_MF_OK;
+  std::vector<int64_t> v(static_cast<size_t>(h->clock));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  HIP_TRY(h, hipMemcpy(v.data(), h->vap_v, v.size() * sizeof(int64_t), hipMemcpyDeviceToHost));
+  for (int64_t c = 0; c < h->clock; ++c)
+    for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(v[c]);
+  return PS_MF_OK;
+}
+
 // One clock of the sequential step: the sub-epochs one launch after another, then the
 // commit of R and of the untouched user rows.
 int seq_clock(ps_mf_t *h) {
@@ -1641,7 +1774,8 @@ int seq_clock(ps_mf_t *h) {
   a.chain_worker = q.chain_worker;
   a.rec = reinterpret_cast<const i32x4 *>(q.rec);
   a.wcls = h->wcls;
-  a.cls_slot = h->slot_table + table_row(h, c) * h->nclass;
+  int rc = clock_views(h, c, &a.cls_slot);
+  if (rc) return rc;
   a.ring = h->ring;
   a.slot_stride = (h->N + h->M) * h->Kp;
   a.r_off = h->N * h->Kp;
@@ -1649,11 +1783,10 @@ int seq_clock(ps_mf_t *h) {
   a.rwork = h->rwork;
   a.rwork_stride = h->M * h->Kp;
   a.Kp = h->Kp;
-  a.eta = h->eta;
+  a.eta = eta_at(h, c);
   a.lambda = h->lambda;
   hipEvent_t ev = nullptr;
-  int rc = record(h, &ev);
-  if (rc) return rc;
+  if ((rc = record(h, &ev))) return rc;
   for (int32_t t = 0; t < h->seq_groups; ++t) {
     const int64_t c0 = q.epoch_chain[t], c1 = q.epoch_chain[t + 1];
     if (c1 > c0) HIP_TRY(h, dispatch_seq(h->Kp, a, c0, c1, h->stream));
@@ -1683,7 +1816,8 @@ int seq_clock(ps_mf_t *h) {
                      h->stream, ca);
   HIP_TRY(h, hipGetLastError());
   if ((rc = record_end(h, PS_MF_KERNEL_COMMIT, ev))) return rc;
-  for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_version(h, p, c));
+  if (h->policy != PS_MF_VAP)
+    for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_version(h, p, c));
   h->clock = c + 1;
   return PS_MF_OK;
 }
@@ -1695,14 +1829,15 @@ int one_clock(ps_mf_t *h) {
   const int32_t S1 = h->s + 1;
   const int32_t slot_c = static_cast<int32_t>(c % S1), slot_n = static_cast<int32_t>((c + 1) % S1);
   const DeviceBlock &db = h->dblocks[b];
-  const int32_t *cls_slot = h->slot_table + table_row(h, c) * h->nclass;
+  const int32_t *cls_slot = nullptr;
+  int rc = clock_views(h, c, &cls_slot);
+  if (rc) return rc;
   const int64_t slot_stride = (h->N + h->M) * h->Kp;
   const int64_t r_off = h->N * h->Kp;
   const int rowmean = h->step == PS_MF_STEP_ROWMEAN;
 
   hipEvent_t ev = nullptr;
-  int rc = record(h, &ev);
-  if (rc) return rc;
+  if ((rc = record(h, &ev))) return rc;
   if (per_row_policy(h)) {
     RowViewArgs rv{};
     rv.ver_u = h->ver_u;
@@ -1786,7 +1921,7 @@ int one_clock(ps_mf_t *h) {
   fa.cls_slot = cls_slot;
   fa.partial = h->partial_u;
   fa.user_pp = db.by_user.x_pp;
-  fa.eta = h->eta;
+  fa.eta = eta_at(h, c);
   fa.lambda = h->lambda;
   fa.rowmean = rowmean;
   fa.rs_u = per_row_policy(h) ? h->slot_u : nullptr;
@@ -1805,7 +1940,7 @@ int one_clock(ps_mf_t *h) {
   ca.cls_slot = cls_slot;
   ca.partial = h->partial_i;
   ca.item_pp = db.by_item.x_pp;
-  ca.eta = h->eta;
+  ca.eta = eta_at(h, c);
   ca.lambda = h->lambda;
   ca.rowmean = rowmean;
   ca.rs_i = per_row_policy(h) ? h->slot_i : nullptr;
@@ -1815,7 +1950,7 @@ int one_clock(ps_mf_t *h) {
   HIP_TRY(h, hipGetLastError());
   if ((rc = record_end(h, PS_MF_KERNEL_COMMIT, ev))) return rc;
 
-  if (!per_row_policy(h))
+  if (!per_row_policy(h) && h->policy != PS_MF_VAP)
     for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_version(h, p, c));
   h->clock = c + 1;
   return PS_MF_OK;
@@ -1855,7 +1990,7 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
   if (h->loaded) return fail(h, PS_MF_ESTATE, "options must be set before ps_mf_load_ratings");
   switch (key) {
     case PS_MF_OPT_POLICY:
-      if (value < PS_MF_SSP_LAZY || value > PS_MF_ESSP_ROW) return fail(h, PS_MF_EINVAL, "unknown policy %lld", (long long)value);
+      if (value < PS_MF_SSP_LAZY || value > PS_MF_VAP) return fail(h, PS_MF_EINVAL, "unknown policy %lld", (long long)value);
       h->policy = static_cast<int32_t>(value);
       return PS_MF_OK;
     case PS_MF_OPT_STEP:
@@ -1907,9 +2042,20 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
       if (value < 1 || value > 4096) return fail(h, PS_MF_EINVAL, "sub-epochs must be in [1, 4096]");
       h->seq_groups = static_cast<int32_t>(value);
       return PS_MF_OK;
+    case PS_MF_OPT_ETA_DECAY:
+      h->eta_decay = value != 0;
+      return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
   }
+}
+
+int ps_mf_set_value_bound(ps_mf_t *h, double v0) {
+  if (!h) return PS_MF_EINVAL;
+  if (h->loaded) return fail(h, PS_MF_ESTATE, "the value bound must be set before ps_mf_load_ratings");
+  if (!(v0 >= 0)) return fail(h, PS_MF_EINVAL, "the value bound must be >= 0 (infinity allowed)");
+  h->v0 = v0;
+  return PS_MF_OK;
 }
 
 int ps_mf_set_owner_map(ps_mf_t *h, const int32_t *owner) {
@@ -2097,6 +2243,9 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   }
   if ((r = upload(h, &h->slot_table, table))) return undo(r);
   if ((r = upload(h, &h->wcls, h->cls_of_worker))) return undo(r);
+  if (h->policy == PS_MF_VAP &&
+      ((r = upload(h, &h->vap_slot, std::vector<int32_t>(1, 0))) || (r = vap_reserve(h, 0))))
+    return undo(r);
   if (seq) {
     // the users' rows between their runs and every worker's copy of the item rows
     const size_t rw = static_cast<size_t>(h->P) * static_cast<size_t>(h->M) * static_cast<size_t>(h->Kp);
@@ -2134,6 +2283,8 @@ int ps_mf_set_factors(ps_mf_t *h, const float *L, const float *R) {
     HIP_TRY(h, hipMemset(h->slot_i, 0, ni * sizeof(int32_t)));
     HIP_TRY(h, hipMemset(h->stale, 0, (h->s + 1) * sizeof(unsigned long long)));
   }
+  if (h->vap_norms)
+    HIP_TRY(h, hipMemset(h->vap_norms, 0, static_cast<size_t>(h->vap_cap) * (h->s + 1) * sizeof(unsigned)));
   HIP_TRY(h, hipDeviceSynchronize());
   h->clock = 0;
   h->vlog.clear();
@@ -2214,12 +2365,32 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
   if ((kind == PS_MF_IDX_STALENESS || kind == PS_MF_IDX_ROW_VERSIONS) && !h->loaded)
     return fail(h, PS_MF_ESTATE, "no ratings loaded");
   if (kind != PS_MF_IDX_OWNER && kind != PS_MF_IDX_VERSION_LOG && kind != PS_MF_IDX_STALENESS &&
-      kind != PS_MF_IDX_ROW_VERSIONS) {
+      kind != PS_MF_IDX_ROW_VERSIONS && kind != PS_MF_IDX_VAP_NORMS) {
     if (!h->loaded) return fail(h, PS_MF_ESTATE, "no ratings loaded");
     if (block < 0 || block >= h->B) return fail(h, PS_MF_EINVAL, "block %d out of range", block);
   }
   if (kind == PS_MF_IDX_SEQ_ORDER && h->step != PS_MF_STEP_SEQ)
     return fail(h, PS_MF_EINVAL, "the order of the sequential step exists under PS_MF_STEP_SEQ only");
+  if (kind == PS_MF_IDX_VAP_NORMS && h->policy != PS_MF_VAP)
+    return fail(h, PS_MF_EINVAL, "in-transit norms exist under PS_MF_VAP only");
+  if (kind == PS_MF_IDX_VERSION_LOG || kind == PS_MF_IDX_STALENESS) {
+    const int r = vap_sync_log(h);
+    if (r) return r;
+  }
+  std::vector<double> vap_norms;
+  if (kind == PS_MF_IDX_VAP_NORMS && h->clock > 0) {
+    const int64_t S1 = h->s + 1;
+    std::vector<unsigned> bits(static_cast<size_t>(h->clock * S1));
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    HIP_TRY(h, hipMemcpy(bits.data(), h->vap_norms, bits.size() * sizeof(unsigned), hipMemcpyDeviceToHost));
+    vap_norms.resize(bits.size());
+    for (int64_t c = 0; c < h->clock; ++c)
+      for (int64_t d = 0; d < S1; ++d) {
+        float f;
+        std::memcpy(&f, &bits[c * S1 + d], sizeof f);
+        vap_norms[c * S1 + d] = d <= c ? static_cast<double>(f) : -1.0;
+      }
+  }
   if (kind == PS_MF_IDX_OWNER && h->owner.empty()) {
     h->owner.resize(static_cast<size_t>(h->N));
     for (int64_t i = 0; i < h->N; ++i) h->owner[i] = static_cast<int32_t>(i % h->P);
@@ -2296,6 +2467,7 @@ int ps_mf_export_index(ps_mf_t *h, int32_t kind, int32_t block, void *buf, int64
     case PS_MF_IDX_VERSION_LOG: src = h->vlog.data(); esz = 8; n = static_cast<int64_t>(h->vlog.size()); break;
     case PS_MF_IDX_SPLIT: src = split; esz = 8; n = 8; break;
     case PS_MF_IDX_SEQ_ORDER: src = seq_order.data(); esz = 8; n = static_cast<int64_t>(seq_order.size()); break;
+    case PS_MF_IDX_VAP_NORMS: src = vap_norms.data(); esz = 8; n = static_cast<int64_t>(vap_norms.size()); break;
     default: return fail(h, PS_MF_EINVAL, "unknown index kind %d", kind);
   }
   *len = n;

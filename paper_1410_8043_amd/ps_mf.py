@@ -25,14 +25,15 @@ LIB_PATH = os.path.join(_HERE, "libps_mf.so")
 
 OK, EINVAL, ENOMEM, EDEVICE, ESTATE, EINTERNAL = 0, -1, -2, -3, -4, -5
 (OPT_POLICY, OPT_STEP, OPT_MB_BLOCKS, OPT_MB_SEED, OPT_HOST_ONLY, OPT_TIMING, OPT_TILE_BYTES, OPT_UNIT_MAX, OPT_CELLS,
- OPT_HEAVY_MIN, OPT_TWO_STREAMS, OPT_HOT_STEPS, OPT_DENSE_MIN, OPT_SEQ_STRATA) = range(1, 15)
-SSP_LAZY, SSP_WORST, ESSP, SSP_ROW, ESSP_ROW = 0, 1, 2, 3, 4
+ OPT_HEAVY_MIN, OPT_TWO_STREAMS, OPT_HOT_STEPS, OPT_DENSE_MIN, OPT_SEQ_STRATA, OPT_ETA_DECAY) = range(1, 16)
+SSP_LAZY, SSP_WORST, ESSP, SSP_ROW, ESSP_ROW, VAP = 0, 1, 2, 3, 4, 5
 STEP_ROWMEAN, STEP_SUM, STEP_SEQ = 0, 1, 2
 (IDX_OWNER, IDX_ROW_PTR, IDX_COL, IDX_PERM, IDX_USER_COUNT, IDX_ITEM_COUNT, IDX_VERSION_LOG, IDX_SPLIT, IDX_STALENESS,
- IDX_ROW_VERSIONS, IDX_SEQ_ORDER) = range(11)
+ IDX_ROW_VERSIONS, IDX_SEQ_ORDER, IDX_VAP_NORMS) = range(12)
 KERNEL_SWEEP, KERNEL_COMMIT = 0, 1
 
-SYMBOLS = ("ps_mf_create", "ps_mf_set_option", "ps_mf_set_owner_map", "ps_mf_set_stream", "ps_mf_load_ratings",
+SYMBOLS = ("ps_mf_create", "ps_mf_set_option", "ps_mf_set_value_bound", "ps_mf_set_owner_map", "ps_mf_set_stream",
+           "ps_mf_load_ratings",
            "ps_mf_set_factors", "ps_mf_clock", "ps_mf_loss", "ps_mf_get_factors", "ps_mf_get_version",
            "ps_mf_get_clock", "ps_mf_export_index", "ps_mf_kernel_time", "ps_mf_last_error", "ps_mf_destroy")
 
@@ -46,6 +47,7 @@ def _load_lib():
     sig = {
         "ps_mf_create": [i64, i64, i32, i32, i32, f32, f32, ctypes.POINTER(vp)],
         "ps_mf_set_option": [vp, i32, i64],
+        "ps_mf_set_value_bound": [vp, dbl],
         "ps_mf_set_owner_map": [vp, vp],
         "ps_mf_set_stream": [vp, vp],
         "ps_mf_load_ratings": [vp, vp, vp, vp, i64],
@@ -98,6 +100,10 @@ def ps_mf_create(users, items, K, P, s, eta, lam):
 
 def ps_mf_set_option(h, key, value):
     _check(h, "ps_mf_set_option", _lib.ps_mf_set_option(h, int(key), int(value)))
+
+
+def ps_mf_set_value_bound(h, v0):
+    _check(h, "ps_mf_set_value_bound", _lib.ps_mf_set_value_bound(h, float(v0)))
 
 
 def ps_mf_set_owner_map(h, owner):
@@ -159,7 +165,8 @@ def ps_mf_get_clock(h):
 def ps_mf_export_index(h, kind, block=0):
     n = ctypes.c_int64()
     _check(h, "ps_mf_export_index", _lib.ps_mf_export_index(h, int(kind), int(block), None, 0, ctypes.byref(n)))
-    dt = np.int32 if kind in (IDX_OWNER, IDX_COL, IDX_USER_COUNT, IDX_ITEM_COUNT) else np.int64
+    dt = (np.int32 if kind in (IDX_OWNER, IDX_COL, IDX_USER_COUNT, IDX_ITEM_COUNT) else
+          np.float64 if kind == IDX_VAP_NORMS else np.int64)
     buf = np.empty(n.value, dtype=dt)
     _check(h, "ps_mf_export_index", _lib.ps_mf_export_index(h, int(kind), int(block),
                                                             buf.ctypes.data if n.value else None, n.value,
@@ -187,7 +194,8 @@ class PsMf:
 
     def __init__(self, users, items, K, P, s, eta, lam, *, policy=SSP_LAZY, step=STEP_ROWMEAN, B=1, mb_seed=0,
                  owner=None, host_only=False, timing=False, stream=None, tile_bytes=None, unit_max=None,
-                 cells=None, heavy_min=None, two_streams=None, hot_steps=None, dense_min=None, strata=None):
+                 cells=None, heavy_min=None, two_streams=None, hot_steps=None, dense_min=None, strata=None,
+                 value_bound=None, eta_decay=False):
         self.N, self.M, self.K, self.P, self.s = int(users), int(items), int(K), int(P), int(s)
         self.h = ps_mf_create(users, items, K, P, s, eta, lam)
         try:
@@ -215,6 +223,10 @@ class PsMf:
                 ps_mf_set_option(self.h, OPT_DENSE_MIN, dense_min)
             if strata is not None:
                 ps_mf_set_option(self.h, OPT_SEQ_STRATA, strata)
+            if value_bound is not None:
+                ps_mf_set_value_bound(self.h, value_bound)
+            if eta_decay:
+                ps_mf_set_option(self.h, OPT_ETA_DECAY, 1)
             if owner is not None:
                 ps_mf_set_owner_map(self.h, owner)
             if stream is not None:

@@ -255,7 +255,7 @@ def test_per_row_policies_on_a_host_only_handle(policy):
     h = ps_mf.ps_mf_create(4, 3, 2, 1, 0, 0.1, 0.1)
     try:
         with pytest.raises(ps_mf.PsMfError) as e:
-            ps_mf.ps_mf_set_option(h, ps_mf.OPT_POLICY, 5)
+            ps_mf.ps_mf_set_option(h, ps_mf.OPT_POLICY, 6)
         assert e.value.code == ps_mf.EINVAL
     finally:
         ps_mf.ps_mf_destroy(h)
@@ -325,3 +325,36 @@ def test_seq_option_errors():
             with pytest.raises(ps_mf.PsMfError) as e:
                 g.load_ratings(np.array([0]), np.array([0]), np.array([1.0]))
             assert e.value.code == ps_mf.EINVAL
+
+
+# ---------------------------------------------------------------- value-bounded views (PS_MF_VAP)
+def test_vap_arguments_and_host_layout():
+    h = ps_mf.ps_mf_create(4, 3, 2, 2, 1, 0.1, 0.1)
+    try:
+        for v0 in (-1.0, float("nan")):
+            with pytest.raises(ps_mf.PsMfError) as e:
+                ps_mf.ps_mf_set_value_bound(h, v0)
+            assert e.value.code == ps_mf.EINVAL
+        ps_mf.ps_mf_set_value_bound(h, float("inf"))
+        ps_mf.ps_mf_set_option(h, ps_mf.OPT_HOST_ONLY, 1)
+        ps_mf.ps_mf_load_ratings(h, np.array([0, 3]), np.array([2, 0]), np.array([1.0, 5.0]))
+        with pytest.raises(ps_mf.PsMfError) as e:
+            ps_mf.ps_mf_set_value_bound(h, 1.0)
+        assert e.value.code == ps_mf.ESTATE
+        with pytest.raises(ps_mf.PsMfError) as e:
+            ps_mf.ps_mf_export_index(h, ps_mf.IDX_VAP_NORMS, 0)
+        assert e.value.code == ps_mf.EINVAL
+    finally:
+        ps_mf.ps_mf_destroy(h)
+    rng = np.random.default_rng(3)
+    N, M, P = 40, 30, 3
+    user, item = rng.integers(0, N, 500).astype(np.int32), rng.integers(0, M, 500).astype(np.int32)
+    val = rng.integers(1, 6, 500).astype(np.float32)
+    with ps_mf.PsMf(N, M, 8, P, 2, 0.01, 0.05, policy=ps_mf.VAP, value_bound=0.1, B=2, mb_seed=4,
+                    host_only=True) as g:
+        g.load_ratings(user, item, val)
+        o = oracle.Oracle(N, M, 8, P, 2, 0.01, 0.05, oracle.VAP, oracle.ROWMEAN, 2, 4, value_bound=0.1)
+        o.load(user, item, val)
+        compare_layout(g, o, 2, N, M)
+        assert g.export_index(ps_mf.IDX_VAP_NORMS).size == 0 and g.export_index(ps_mf.IDX_VERSION_LOG).size == 0
+        o.close()

@@ -34,14 +34,16 @@ def say(msg):
 
 
 def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, policy=0, step=0, B=1,
-             seed=0, owner=None, check_versions=False, min_dense=0, strata=None, **handle_opts):
+             seed=0, owner=None, check_versions=False, min_dense=0, strata=None, value_bound=None, eta_decay=False,
+             **handle_opts):
     say(f"case N={N} M={M} K={K} P={P} s={s} policy={policy} step={step} B={B} nnz={len(w_user)} clocks={clocks} "
-        f"strata={strata} {handle_opts}")
-    o = oracle.Oracle(N, M, K, P, s, eta, lam, policy, step, B, seed, owner, strata=strata)
+        f"strata={strata} v0={value_bound} eta_decay={eta_decay} {handle_opts}")
+    o = oracle.Oracle(N, M, K, P, s, eta, lam, policy, step, B, seed, owner, strata=strata, value_bound=value_bound,
+                      eta_decay=eta_decay)
     o.load(w_user, w_item, w_val)
     o.set_factors(L0, R0)
     with ps_mf.PsMf(N, M, K, P, s, eta, lam, policy=policy, step=step, B=B, mb_seed=seed, owner=owner,
-                    strata=strata, **handle_opts) as g:
+                    strata=strata, value_bound=value_bound, eta_decay=eta_decay, **handle_opts) as g:
         g.load_ratings(w_user, w_item, w_val)
         if step == oracle.SEQ:
             for b in range(B):
@@ -64,6 +66,10 @@ def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, c
         assert np.array_equal(g.export_index(gpu_mod().IDX_STALENESS), o.export(oracle.X_STALENESS))
         if policy in (oracle.SSP_ROW, oracle.ESSP_ROW):
             assert np.array_equal(g.export_index(gpu_mod().IDX_ROW_VERSIONS), o.export(oracle.X_ROW_VERSIONS))
+        if policy == oracle.VAP:
+            gn, on = g.export_index(gpu_mod().IDX_VAP_NORMS), o.export(oracle.X_VAP_NORMS)
+            assert gn.shape == on.shape and np.array_equal(gn < 0, on < 0)
+            assert np.abs(gn - on).max(initial=0) <= 2 * FACTOR_TOL
         if check_versions:
             for v in range(max(0, clocks - s), clocks + 1):
                 Lv, Rv = g.get_version(v)
@@ -85,7 +91,8 @@ def test_hand_examples_through_abi(gpu, case):
     v = np.array([r[2] for r in case["ratings"]], np.float32)
     say(f"hand example {case['name']}")
     with gpu.PsMf(case["N"], case["M"], case["K"], case["P"], case["s"], case["eta"], case["lam"],
-                  policy=case["policy"], step=case["step"], owner=case["owner"], strata=case["strata"]) as g:
+                  policy=case["policy"], step=case["step"], owner=case["owner"], strata=case["strata"],
+                  value_bound=case["v0"]) as g:
         g.load_ratings(u, i, v)
         g.set_factors(case["L0"], case["R0"])
         for ex in sorted(case["expect"], key=lambda e: e["clock"]):
@@ -412,3 +419,68 @@ def test_seq_zero_degree_rows_custom_owner_single_and_empty(gpu):
              N=3, M=2, K=4, P=2, s=1, eta=0.1, lam=0.1, clocks=4, step=oracle.SEQ, strata=3)
     run_both(gpu, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32), L0, R0,
              N=3, M=2, K=4, P=2, s=1, eta=0.1, lam=0.1, clocks=3, step=oracle.SEQ)
+
+
+# ---------------------------------------------------------------- value-bounded views (VAP) and eta / sqrt(t)
+VAP_MARGIN = 1e-5  # decisions are compared only where the oracle's norm is this far from the bound (the
+                  # factors of the two sides agree to about 1e-6 over these runs)
+
+
+def pick_value_bound(user, item, val, L0, R0, candidates, *, N, M, K, P, s, eta, lam, clocks, step=0, B=1, seed=0,
+                     strata=None, eta_decay=False):
+    """The first candidate bound under which the oracle's every view decision (norm vs bound)
+    keeps VAP_MARGIN, so that fp32 differences cannot flip it, and which mixes stale and
+    fresh views."""
+    for v0 in candidates:
+        o = oracle.Oracle(N, M, K, P, s, eta, lam, oracle.VAP, step, B, seed, strata=strata, value_bound=v0,
+                          eta_decay=eta_decay)
+        o.load(user, item, val)
+        o.set_factors(L0, R0)
+        o.clock(clocks)
+        norms = o.export(oracle.X_VAP_NORMS).reshape(clocks, s + 1)
+        d = np.arange(clocks) - o.export(oracle.X_VERSION_LOG).reshape(clocks, P)[:, 0]
+        o.close()
+        bound = v0 / np.sqrt(np.arange(clocks) + 1.0)
+        gap = np.abs(norms[:, 1:] - bound[:, None])[norms[:, 1:] >= 0]
+        if (gap.size == 0 or gap.min() > VAP_MARGIN) and (d[1:] > 0).any() and (d[1:] == 0).any():
+            say(f"  value bound {v0}: delays {d.tolist()}, smallest margin {gap.min(initial=np.inf):.3g}")
+            return v0
+    raise AssertionError("no candidate bound keeps the decision margin")
+
+
+@pytest.mark.parametrize("s,step", [(1, oracle.ROWMEAN), (2, oracle.SUM), (3, oracle.SEQ)])
+def test_tiny_config_vap(gpu, s, step):
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    kw = dict(N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta, lam=spec.lam, clocks=spec.clocks, step=step,
+              strata=8 if step == oracle.SEQ else None)
+    v0 = pick_value_bound(w.user, w.item, w.val, w.L0, w.R0, [1e-4 * 1.25 ** k for k in range(80)], **kw)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, policy=oracle.VAP, value_bound=v0, check_versions=True, **kw)
+
+
+def test_vap_limits_and_eta_decay(gpu):
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    kw = dict(N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=2, eta=spec.eta, lam=spec.lam, clocks=spec.clocks)
+    for v0 in (0.0, float("inf")):
+        run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, policy=oracle.VAP, value_bound=v0, **kw)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, policy=oracle.SSP_LAZY, eta_decay=True, **kw)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, policy=oracle.SSP_WORST, step=oracle.SEQ, strata=16,
+             eta_decay=True, **kw)
+
+
+def test_full_shape_scaled_vap(gpu):
+    spec = synth.scaled(synth.CONFIGS["full"], 0.02)
+    w = synth.generate(spec)
+    kw = dict(N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3, eta=spec.eta, lam=spec.lam, clocks=8)
+    v0 = pick_value_bound(w.user, w.item, w.val, w.L0, w.R0, [1e-4 * 1.25 ** k for k in range(80)], **kw)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, policy=oracle.VAP, value_bound=v0, check_versions=True, **kw)
+
+
+def test_medium_shape_scaled_vap_minibatch_blocks_and_eta_decay(gpu):
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.05)
+    w = synth.generate(spec)
+    kw = dict(N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=3, eta=spec.eta, lam=spec.lam, clocks=12, B=spec.B,
+              seed=spec.seed, eta_decay=True)
+    v0 = pick_value_bound(w.user, w.item, w.val, w.L0, w.R0, [1e-4 * 1.25 ** k for k in range(80)], **kw)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, policy=oracle.VAP, value_bound=v0, **kw)
