@@ -962,7 +962,10 @@ __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, 
 // k_vap_norms reduces, for d = 1 .. dmax, the max of the fp32 differences between the
 // slots of versions c and c - d (padding columns are zero in every slot) into this
 // clock's entry of the norm log (float bits, atomicMax over non-negative floats; NaN is
-// ignored); k_vap_pick then writes the slot the sweeps read and the version log entry.
+// ignored): one pass reads every slot once, with the dmax running maxima in registers
+// (dmax <= kVapFused; beyond, one pass per d).  k_vap_pick then writes the slot the sweeps
+// read and the version log entry.
+constexpr int kVapFused = 8;
 struct VapArgs {
   const float *ring;
   int64_t slot_stride;
@@ -972,28 +975,56 @@ struct VapArgs {
   unsigned *norms;     // [S1] this clock's norms
 };
 
+__device__ __forceinline__ float f4_absdiff_max(const float4 x, const float4 y) {
+  return fmaxf(fmaxf(fabsf(x.x - y.x), fabsf(x.y - y.y)), fmaxf(fabsf(x.z - y.z), fabsf(x.w - y.w)));
+}
+
+// block max of m (every thread passes its value), added to *out by atomicMax
+__device__ __forceinline__ void vap_block_max(float m, float *red, unsigned *out) {
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x / 64] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = red[0];
+    for (int w = 1; w < kBlock / 64; ++w) t = fmaxf(t, red[w]);
+    atomicMax(out, __float_as_uint(t));
+  }
+  __syncthreads();
+}
+
 __global__ __launch_bounds__(kBlock) void k_vap_norms(VapArgs a) {
   __shared__ float red[kBlock / 64];
   const float4 *r4 = reinterpret_cast<const float4 *>(a.ring);
   const int64_t ss4 = a.slot_stride / 4;
   const int32_t slot_c = static_cast<int32_t>(a.c % a.S1);
+  if (a.dmax <= kVapFused) {
+    float m[kVapFused];
+    int32_t sd[kVapFused];
+#pragma unroll
+    for (int d = 0; d < kVapFused; ++d) {
+      m[d] = 0.f;
+      sd[d] = static_cast<int32_t>((a.c - d - 1 + (a.c < d + 1 ? a.S1 : 0)) % a.S1);  // used for d < dmax only
+    }
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < a.n4;
+         i += static_cast<int64_t>(gridDim.x) * kBlock) {
+      const float4 x = r4[slot_c * ss4 + i];
+#pragma unroll
+      for (int d = 0; d < kVapFused; ++d)
+        if (d < a.dmax) m[d] = fmaxf(m[d], f4_absdiff_max(x, r4[sd[d] * ss4 + i]));
+    }
+#pragma unroll
+    for (int d = 0; d < kVapFused; ++d)
+      if (d < a.dmax) vap_block_max(m[d], red, a.norms + d + 1);
+    return;
+  }
   for (int d = 1; d <= a.dmax; ++d) {
     const int32_t sd = static_cast<int32_t>((a.c - d) % a.S1);
     float m = 0.f;
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < a.n4;
          i += static_cast<int64_t>(gridDim.x) * kBlock) {
-      const float4 x = r4[slot_c * ss4 + i], y = r4[sd * ss4 + i];
-      m = fmaxf(m, fmaxf(fmaxf(fabsf(x.x - y.x), fabsf(x.y - y.y)), fmaxf(fabsf(x.z - y.z), fabsf(x.w - y.w))));
+      m = fmaxf(m, f4_absdiff_max(r4[slot_c * ss4 + i], r4[sd * ss4 + i]));
     }
-    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x / 64] = m;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      float t = red[0];
-      for (int w = 1; w < kBlock / 64; ++w) t = fmaxf(t, red[w]);
-      atomicMax(a.norms + d, __float_as_uint(t));
-    }
-    __syncthreads();
+    vap_block_max(m, red, a.norms + d);
   }
 }
 
