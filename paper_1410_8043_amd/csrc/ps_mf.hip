@@ -965,7 +965,7 @@ __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, 
 // ignored): one pass reads every slot once, with the dmax running maxima in registers
 // (dmax <= kVapFused; beyond, one pass per d).  k_vap_pick then writes the slot the sweeps
 // read and the version log entry.
-constexpr int kVapFused = 8;
+constexpr int kVapFused = 16;
 struct VapArgs {
   const float *ring;
   int64_t slot_stride;
