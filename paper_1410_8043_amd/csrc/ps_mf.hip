@@ -1120,8 +1120,8 @@ template <int E>
 __global__ __launch_bounds__(kBlock) void k_seq(SeqArgs a, int64_t c0, int64_t c1) {
   constexpr int D = psmf::kSeqAhead, D2 = 2 * psmf::kSeqAhead;
   const int lane = static_cast<int>(threadIdx.x) % 64, Kp = a.Kp;
-  const int64_t ch = c0 + __builtin_amdgcn_readfirstlane((static_cast<int>(blockIdx.x) * kBlock +
-                                                          static_cast<int>(threadIdx.x)) / 64);
+  const int64_t ch = c0 + static_cast<int64_t>(blockIdx.x) * (kBlock / 64) +
+                     __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / 64);
   if (ch >= c1) return;  // uniform over the wavefront
   const int64_t beg = a.chain_beg[ch], end = a.chain_beg[ch + 1];
   const int32_t p = a.chain_worker[ch];
