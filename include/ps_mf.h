@@ -106,6 +106,10 @@ typedef struct ps_mf ps_mf_t;
                                    a worker applies its ratings */
 #define PS_MF_OPT_ETA_DECAY 15  /* 1: step eta / sqrt(c + 1) at clock c (the schedule of Section 3's
                                    theorems); 0 (default): constant eta */
+#define PS_MF_OPT_SEQ_GRAPHS 16 /* 1 (default): under PS_MF_STEP_SEQ, capture each clock's sub-epoch
+                                   launches once per (block, view schedule) into a HIP graph on the
+                                   handle's stream and replay it (not with PS_MF_OPT_ETA_DECAY);
+                                   0: launch them one by one */
 
 /* Views (Section 3.2 SSP condition; Section 4 ESSPTable).  The table-level policies give
    worker p at clock c one whole version v = max(0, c - d):

@@ -1434,6 +1434,8 @@ struct ps_mf {
   int32_t seq_groups = 256;      // sub-epochs of the sequential step
   double v0 = INFINITY;          // value bound of the VAP policy
   bool eta_decay = false;        // step eta / sqrt(c + 1) at clock c
+  bool seq_graphs = true;        // replay each clock's sub-epoch launches from a captured HIP graph
+  std::vector<hipGraphExec_t> seq_exec;  // per (block, slot-table row)
   std::vector<int32_t> owner;
   // host state
   bool loaded = false, has_factors = false;
@@ -1818,9 +1820,38 @@ int seq_clock(ps_mf_t *h) {
   a.lambda = h->lambda;
   hipEvent_t ev = nullptr;
   if ((rc = record(h, &ev))) return rc;
-  for (int32_t t = 0; t < h->seq_groups; ++t) {
-    const int64_t c0 = q.epoch_chain[t], c1 = q.epoch_chain[t + 1];
-    if (c1 > c0) HIP_TRY(h, dispatch_seq(h->Kp, a, c0, c1, h->stream));
+  auto launch_epochs = [&]() -> hipError_t {
+    for (int32_t t = 0; t < h->seq_groups; ++t) {
+      const int64_t c0 = q.epoch_chain[t], c1 = q.epoch_chain[t + 1];
+      if (c1 > c0) {
+        const hipError_t e = dispatch_seq(h->Kp, a, c0, c1, h->stream);
+        if (e != hipSuccess) return e;
+      }
+    }
+    return hipSuccess;
+  };
+  // The launches of a clock depend on the block and the slot-table row only (VAP: the block;
+  // a per-clock step schedule: never the same), so each combination is captured once into a
+  // HIP graph and replayed: one submission instead of up to G.
+  const int64_t rows = 2 * static_cast<int64_t>(h->s) + 1;
+  const int64_t key = h->policy == PS_MF_VAP ? b : b * rows + table_row(h, c);
+  if (h->seq_graphs && !h->eta_decay) {
+    if (h->seq_exec.empty()) h->seq_exec.assign(static_cast<size_t>(h->B * rows), nullptr);
+    hipGraphExec_t &ex = h->seq_exec[static_cast<size_t>(key)];
+    if (!ex) {
+      hipGraph_t graph = nullptr;
+      HIP_TRY(h, hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal));
+      const hipError_t le = launch_epochs();
+      const hipError_t ce = hipStreamEndCapture(h->stream, &graph);
+      HIP_TRY(h, le);
+      HIP_TRY(h, ce);
+      const hipError_t ie = hipGraphInstantiate(&ex, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      HIP_TRY(h, ie);
+    }
+    HIP_TRY(h, hipGraphLaunch(ex, h->stream));
+  } else {
+    HIP_TRY(h, launch_epochs());
   }
   if ((rc = record_end(h, PS_MF_KERNEL_SWEEP, ev))) return rc;
   if ((rc = record(h, &ev))) return rc;
@@ -2075,6 +2106,9 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
       return PS_MF_OK;
     case PS_MF_OPT_ETA_DECAY:
       h->eta_decay = value != 0;
+      return PS_MF_OK;
+    case PS_MF_OPT_SEQ_GRAPHS:
+      h->seq_graphs = value != 0;
       return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
@@ -2538,6 +2572,8 @@ void ps_mf_destroy(ps_mf_t *h) {
     (void)hipEventDestroy(ev.b);
   }
   if (h->side_stream) (void)hipStreamSynchronize(h->side_stream);
+  for (hipGraphExec_t ex : h->seq_exec)
+    if (ex) (void)hipGraphExecDestroy(ex);
   for (void *p : h->allocations) (void)hipFree(p);
   if (h->side_stream) (void)hipStreamDestroy(h->side_stream);
   if (h->fork) (void)hipEventDestroy(h->fork);

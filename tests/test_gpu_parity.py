@@ -484,3 +484,31 @@ def test_medium_shape_scaled_vap_minibatch_blocks_and_eta_decay(gpu):
               seed=spec.seed, eta_decay=True)
     v0 = pick_value_bound(w.user, w.item, w.val, w.L0, w.R0, [1e-4 * 1.25 ** k for k in range(80)], **kw)
     run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, policy=oracle.VAP, value_bound=v0, **kw)
+
+
+@pytest.mark.parametrize("policy,s,B", [(oracle.SSP_LAZY, 2, 3), (oracle.VAP, 2, 2), (oracle.ESSP, 1, 1)])
+def test_seq_graph_replays_equal_eager_launches(gpu, policy, s, B):
+    """The sequential step replays a captured HIP graph per (block, view schedule); every
+    replay, with the program's own work and synchronizations between clocks, must equal
+    launching the sub-epochs one by one, bit for bit."""
+    N, M, K = 400, 150, 33
+    user, item, val, L0, R0 = small_problem(11, N, M, 6000, K, dup=30)
+    out = []
+    for graphs in (True, False):
+        with gpu.PsMf(N, M, K, 5, s, 0.02, 0.05, policy=policy, step=gpu.STEP_SEQ, strata=7, B=B, mb_seed=3,
+                      value_bound=0.05 if policy == oracle.VAP else None, seq_graphs=graphs) as g:
+            g.load_ratings(user, item, val)
+            g.set_factors(L0, R0)
+            hist = []
+            for _ in range(3 * (2 * s + 1) * B):
+                g.clock(1)
+                hist.append(g.loss())
+                hist.append(g.get_factors())
+            out.append((hist, g.export_index(gpu.IDX_VERSION_LOG)))
+    (ha, va), (hb, vb) = out
+    assert np.array_equal(va, vb)
+    for x, y in zip(ha, hb):
+        if isinstance(x, tuple):
+            assert np.array_equal(x[0], y[0]) and np.array_equal(x[1], y[1])
+        else:
+            assert x == y
