@@ -26,7 +26,7 @@
  *     in the clock's minibatch (items: across all workers); STEP SUM does not;
  *   - or STEP SEQ: each worker applies the Section 3.1 rule rating by rating to its own
  *     copy of the rows it touches (reading its own writes inside the clock), starting
- *     from its view, and at the clock boundary version c+1 = version c + the sum over
+ *     from its view (under a per-row policy, each row at its cached version), and at the clock boundary version c+1 = version c + the sum over
  *     workers of (copy - view) of the rows each touched.  A worker's ratings run in G
  *     sub-epochs (PS_MF_OPT_SEQ_STRATA): user group (i div P) mod G, item group j mod G,
  *     rating (i, j) in sub-epoch (item group - user group) mod G; sub-epochs in order,
@@ -71,9 +71,7 @@ typedef struct ps_mf ps_mf_t;
 /* option keys (ps_mf_set_option); all must be set before ps_mf_load_ratings */
 #define PS_MF_OPT_POLICY 1    /* PS_MF_SSP_LAZY (default), PS_MF_SSP_WORST, PS_MF_ESSP, PS_MF_SSP_ROW,
                                  PS_MF_ESSP_ROW, PS_MF_VAP */
-#define PS_MF_OPT_STEP 2      /* PS_MF_STEP_ROWMEAN (default), PS_MF_STEP_SUM, PS_MF_STEP_SEQ (table
-                                 policies only: with a per-row policy ps_mf_load_ratings fails
-                                 with PS_MF_EINVAL) */
+#define PS_MF_OPT_STEP 2      /* PS_MF_STEP_ROWMEAN (default), PS_MF_STEP_SUM, PS_MF_STEP_SEQ */
 #define PS_MF_OPT_MB_BLOCKS 3 /* B >= 1 minibatch blocks (default 1: full shard per clock) */
 #define PS_MF_OPT_MB_SEED 4   /* 64-bit seed of the block hash (default 0) */
 #define PS_MF_OPT_HOST_ONLY 5 /* 1: build, self-check and export the integer layout only; never touch

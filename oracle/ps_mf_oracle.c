@@ -39,7 +39,8 @@
  *   - step normalisation: SUM uses the summed per-rating steps; ROWMEAN divides each
  *     row's summed contribution by that row's rating count in the clock's minibatch;
  *   - or SEQ: each worker applies the Section 3.1 update rating by rating to its own copy
- *     of the rows it reads (read-my-writes inside the clock), starting from its view; at
+ *     of the rows it reads (read-my-writes inside the clock), starting from its view (under
+ *     a per-row policy, each row at the version its client's cache holds); at
  *     the clock boundary it commits (copy - view) for every row it touched, and the
  *     server adds the commits of all workers (Section 4: updates coalesced per clock).
  *     The order inside a worker is stratified into G sub-epochs: user group
@@ -197,8 +198,6 @@ int oracle_create(int64_t N, int64_t M, int32_t K, int32_t P, int32_t s, double 
   *out = NULL;
   if (N <= 0 || M <= 0 || K <= 0 || P <= 0 || s < 0 || B < 1 || N > 0x7fffffff || M > 0x7fffffff) return OR_EINVAL;
   if (policy < OR_LAZY || policy > OR_VAP || step < OR_ROWMEAN || step > OR_SEQ) return OR_EINVAL;
-  /* sequential steps start from one view per (worker, clock): table policies only */
-  if (step == OR_SEQ && (policy == OR_SSP_ROW || policy == OR_ESSP_ROW)) return OR_EINVAL;
   if (!isfinite(eta) || !isfinite(lambda)) return OR_EINVAL;
   oracle_t *o = (oracle_t *)calloc(1, sizeof(oracle_t));
   if (!o) return OR_ENOMEM;
@@ -366,6 +365,15 @@ int oracle_set_factors(oracle_t *o, const float *L0, const float *R0) {
 static float *L_of(const oracle_t *o, int64_t v) { return o->Lring + (size_t)(v % (o->s + 1)) * (size_t)(o->N * o->K); }
 static float *R_of(const oracle_t *o, int64_t v) { return o->Rring + (size_t)(v % (o->s + 1)) * (size_t)(o->M * o->K); }
 
+/* the version worker p's view holds for user row i / item row j at clock c: the worker's
+   whole view, or under a per-row policy the version its client's cache holds */
+static int64_t seq_view_L(const oracle_t *o, int64_t i, int64_t c) {
+  return per_row(o) ? o->ucache[i] : view_version(o, o->owner[i], c);
+}
+static int64_t seq_view_R(const oracle_t *o, int64_t p, int64_t j, int64_t c) {
+  return per_row(o) ? o->icache[(p % o->C) * o->M + j] : view_version(o, p, c);
+}
+
 /* the SEQ step of one clock: every worker runs its ratings in its order on its own copies
    of the rows, which start at its view; dL and dR receive sum over workers of
    (copy - view) for the rows each touched */
@@ -381,19 +389,20 @@ static int seq_sweep(oracle_t *o, int64_t c, int32_t b, double eta) {
   for (int64_t q = o->bstart[b]; q < o->bstart[b + 1]; ++q) {
     const int64_t t = o->sorder[q];
     const int64_t i = o->user[t], j = o->item[t], p = o->owner[i];
-    const int64_t v = view_version(o, p, c);
+    const int64_t vL = seq_view_L(o, i, c), vR = seq_view_R(o, p, j, c);
     double *Li = o->Lloc + i * K, *Rj = o->Rloc + (p * M + j) * K;
     if (!o->utouch[i]) { /* first read of L_i this clock: the view */
-      const float *src = L_of(o, v) + i * K;
+      const float *src = L_of(o, vL) + i * K;
       for (int64_t k = 0; k < K; ++k) Li[k] = (double)src[k];
       o->utouch[i] = 1;
     }
     if (!o->itouch[p * M + j]) { /* first read of R_j by worker p this clock */
-      const float *src = R_of(o, v) + j * K;
+      const float *src = R_of(o, vR) + j * K;
       for (int64_t k = 0; k < K; ++k) Rj[k] = (double)src[k];
       o->itouch[p * M + j] = 1;
     }
-    o->stale[c - v] += 2; /* the rating reads L_i and R_j of the worker's view */
+    o->stale[c - vL] += 1; /* the rating reads L_i ... */
+    o->stale[c - vR] += 1; /* ... and R_j of the worker's view */
     double dot = 0.0;
     for (int64_t k = 0; k < K; ++k) dot += Li[k] * Rj[k];
     const double e = (double)o->val[t] - dot;
@@ -405,16 +414,16 @@ static int seq_sweep(oracle_t *o, int64_t c, int32_t b, double eta) {
   }
   for (int64_t i = 0; i < o->N; ++i) {
     if (!o->utouch[i]) continue;
-    const float *Lv = L_of(o, view_version(o, o->owner[i], c)) + i * K;
+    const float *Lv = L_of(o, seq_view_L(o, i, c)) + i * K;
     for (int64_t k = 0; k < K; ++k) o->dL[i * K + k] = o->Lloc[i * K + k] - (double)Lv[k];
     o->utouch[i] = 0;
   }
   for (int64_t p = 0; p < o->P; ++p) {
-    const float *Rv = R_of(o, view_version(o, p, c));
     for (int64_t j = 0; j < M; ++j) {
       if (!o->itouch[p * M + j]) continue;
       const double *Rl = o->Rloc + (p * M + j) * K;
-      for (int64_t k = 0; k < K; ++k) o->dR[j * K + k] += Rl[k] - (double)Rv[j * K + k];
+      const float *Rv = R_of(o, seq_view_R(o, p, j, c)) + j * K;
+      for (int64_t k = 0; k < K; ++k) o->dR[j * K + k] += Rl[k] - (double)Rv[k];
       o->itouch[p * M + j] = 0;
     }
   }

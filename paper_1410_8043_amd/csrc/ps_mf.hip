@@ -1060,8 +1060,10 @@ struct SeqArgs {
   const int32_t *chain_worker;
   const i32x4 *rec;                // [nnz] (user, item, value bits, flags) in application order
   const int32_t *wcls, *cls_slot;  // worker class, ring slot of each class's view
+  const int32_t *rs_u, *rs_i;      // per-row policies: ring slot of each user row, of each
+                                   // (class, item) row ([nclass * items], class-major)
   const float *ring;
-  int64_t slot_stride, r_off;
+  int64_t slot_stride, r_off, items;
   float *lwork;                    // [users, Kp] the user rows between their runs
   float *rwork;                    // [P, items, Kp] each worker's copy of the item rows
   int64_t rwork_stride;            // items * Kp
@@ -1116,7 +1118,7 @@ __device__ __forceinline__ void seq_unrolled(F &f, int64_t base) {
   if constexpr (K0 + 1 < N) seq_unrolled<K0 + 1, N>(f, base);
 }
 
-template <int E>
+template <int E, bool PerRow>
 __global__ __launch_bounds__(kBlock) void k_seq(SeqArgs a, int64_t c0, int64_t c1) {
   constexpr int D = psmf::kSeqAhead, D2 = 2 * psmf::kSeqAhead;
   const int lane = static_cast<int>(threadIdx.x) % 64, Kp = a.Kp;
@@ -1125,16 +1127,25 @@ __global__ __launch_bounds__(kBlock) void k_seq(SeqArgs a, int64_t c0, int64_t c
   if (ch >= c1) return;  // uniform over the wavefront
   const int64_t beg = a.chain_beg[ch], end = a.chain_beg[ch + 1];
   const int32_t p = a.chain_worker[ch];
-  const float *Lv = a.ring + a.cls_slot[a.wcls[p]] * a.slot_stride;
+  const int32_t cls = a.wcls[p];
+  const float *Lv = a.ring + a.cls_slot[cls] * a.slot_stride;
   const float *Rv = Lv + a.r_off;
   float *Rw = a.rwork + static_cast<int64_t>(p) * a.rwork_stride;
   const const_rec_ptr rec = (const_rec_ptr)(a.rec);
+  // the view of a row: the worker's whole view, or the row's own cached version
+  auto view_L = [&](int32_t i) {
+    return (PerRow ? a.ring + a.rs_u[i] * a.slot_stride : Lv) + static_cast<int64_t>(i) * Kp;
+  };
+  auto view_R = [&](int32_t j) {
+    return (PerRow ? a.ring + a.rs_i[cls * a.items + j] * a.slot_stride + a.r_off : Rv) + static_cast<int64_t>(j) * Kp;
+  };
   i32x4 meta[D2];
   float yq[D][E], lq[D][E], wq[D][E];
   auto fetch = [&](const i32x4 &m, float (&y)[E], float (&x)[E]) {
-    wave_load_row<E>(y, ((m[3] & psmf::kSeqFirstR) ? Rv : Rw) + static_cast<int64_t>(m[1]) * Kp, lane, Kp);
+    wave_load_row<E>(y, (m[3] & psmf::kSeqFirstR) ? view_R(m[1]) : Rw + static_cast<int64_t>(m[1]) * Kp, lane, Kp);
     if (m[3] & psmf::kSeqRunStart)
-      wave_load_row<E>(x, ((m[3] & psmf::kSeqFirstL) ? Lv : a.lwork) + static_cast<int64_t>(m[0]) * Kp, lane, Kp);
+      wave_load_row<E>(x, (m[3] & psmf::kSeqFirstL) ? view_L(m[0]) : a.lwork + static_cast<int64_t>(m[0]) * Kp,
+                       lane, Kp);
   };
 #pragma unroll
   for (int k = 0; k < D2; ++k)
@@ -1198,6 +1209,7 @@ struct SeqCommitArgs {
   int32_t slot_c, slot_n;
   const int32_t *ucount;       // [users] ratings in the block
   const int32_t *ucls;         // [users] class of the user's worker
+  const int32_t *rs_u, *rs_i;  // per-row policies: the rows' own view slots (else null)
   const float *lwork;
   const int64_t *item_wptr;    // [items + 1]
   const int32_t *item_workers; // the workers with a rating of each item
@@ -1221,7 +1233,7 @@ __global__ __launch_bounds__(kBlock) void k_seq_commit(SeqCommitArgs a) {
       return;
     }
     const float4 loc = reinterpret_cast<const float4 *>(a.lwork)[idx];
-    const float4 v = ring4[a.cls_slot[a.ucls[i]] * ss4 + idx];
+    const float4 v = ring4[(a.rs_u ? a.rs_u[i] : a.cls_slot[a.ucls[i]]) * ss4 + idx];
     const float4 lc = ring4[a.slot_c * ss4 + idx];
     ring4[a.slot_n * ss4 + idx] = make_float4(lc.x + (loc.x - v.x), lc.y + (loc.y - v.y), lc.z + (loc.z - v.z),
                                               lc.w + (loc.w - v.w));
@@ -1235,7 +1247,7 @@ __global__ __launch_bounds__(kBlock) void k_seq_commit(SeqCommitArgs a) {
   for (int64_t q = a.item_wptr[j]; q < a.item_wptr[j + 1]; ++q) {
     const int32_t w = a.item_workers[q];
     const float4 loc = rw4[w * (a.rwork_stride / 4) + idx];
-    const float4 v = ring4[a.cls_slot[a.wcls[w]] * ss4 + r4];
+    const float4 v = ring4[(a.rs_i ? a.rs_i[a.wcls[w] * a.items + j] : a.cls_slot[a.wcls[w]]) * ss4 + r4];
     d.x += loc.x - v.x; d.y += loc.y - v.y; d.z += loc.z - v.z; d.w += loc.w - v.w;
   }
   const float4 rc = ring4[a.slot_c * ss4 + r4];
@@ -1330,7 +1342,8 @@ bool dense_supported(int Kp) { return Kp >= 16 && Kp <= 256; }
 template <int E>
 hipError_t launch_seq(const SeqArgs &a, int64_t c0, int64_t c1, hipStream_t st) {
   const int64_t waves = kBlock / 64, grid = (c1 - c0 + waves - 1) / waves;
-  hipLaunchKernelGGL((k_seq<E>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a, c0, c1);
+  if (a.rs_u) hipLaunchKernelGGL((k_seq<E, true>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a, c0, c1);
+  else hipLaunchKernelGGL((k_seq<E, false>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, a, c0, c1);
   return hipGetLastError();
 }
 // one chain per wavefront: E = Kp / 64 floats per lane (at least one)
@@ -1719,6 +1732,29 @@ int record_end(ps_mf_t *h, int kernel, hipEvent_t a) {
   return PS_MF_OK;
 }
 
+// per-row policies: the version and ring slot each cached row is read at in clock c
+int row_views(ps_mf_t *h, const DeviceBlock &db, int64_t c) {
+  RowViewArgs rv{};
+  rv.ver_u = h->ver_u;
+  rv.slot_u = h->slot_u;
+  rv.ver_i = h->ver_i;
+  rv.slot_i = h->slot_i;
+  rv.ucount = db.ucount;
+  rv.icount_cls = db.icount_cls;
+  rv.users = h->N;
+  rv.items = h->M;
+  rv.clock = c;
+  rv.nclass = h->nclass;
+  rv.s = h->s;
+  rv.essp = h->policy == PS_MF_ESSP_ROW;
+  rv.stale = h->stale;
+  const int64_t rows = h->N + static_cast<int64_t>(h->nclass) * h->M;
+  hipLaunchKernelGGL(k_row_views, dim3(static_cast<unsigned>((rows + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                     h->stream, rv);
+  HIP_TRY(h, hipGetLastError());
+  return PS_MF_OK;
+}
+
 float eta_at(const ps_mf_t *h, int64_t c) {
   return h->eta_decay ? static_cast<float>(static_cast<double>(h->eta) / std::sqrt(static_cast<double>(c + 1)))
                       : h->eta;
@@ -1809,6 +1845,12 @@ int seq_clock(ps_mf_t *h) {
   a.wcls = h->wcls;
   int rc = clock_views(h, c, &a.cls_slot);
   if (rc) return rc;
+  if (per_row_policy(h)) {
+    if ((rc = row_views(h, db, c))) return rc;
+    a.rs_u = h->slot_u;
+    a.rs_i = h->slot_i;
+  }
+  a.items = h->M;
   a.ring = h->ring;
   a.slot_stride = (h->N + h->M) * h->Kp;
   a.r_off = h->N * h->Kp;
@@ -1866,6 +1908,8 @@ int seq_clock(ps_mf_t *h) {
   ca.slot_n = static_cast<int32_t>((c + 1) % S1);
   ca.ucount = db.ucount;
   ca.ucls = h->ucls;
+  ca.rs_u = a.rs_u;
+  ca.rs_i = a.rs_i;
   ca.lwork = h->lwork;
   ca.item_wptr = q.item_wptr;
   ca.item_workers = q.item_workers;
@@ -1878,7 +1922,7 @@ int seq_clock(ps_mf_t *h) {
                      h->stream, ca);
   HIP_TRY(h, hipGetLastError());
   if ((rc = record_end(h, PS_MF_KERNEL_COMMIT, ev))) return rc;
-  if (h->policy != PS_MF_VAP)
+  if (h->policy != PS_MF_VAP && !per_row_policy(h))
     for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_version(h, p, c));
   h->clock = c + 1;
   return PS_MF_OK;
@@ -1900,26 +1944,7 @@ int one_clock(ps_mf_t *h) {
 
   hipEvent_t ev = nullptr;
   if ((rc = record(h, &ev))) return rc;
-  if (per_row_policy(h)) {
-    RowViewArgs rv{};
-    rv.ver_u = h->ver_u;
-    rv.slot_u = h->slot_u;
-    rv.ver_i = h->ver_i;
-    rv.slot_i = h->slot_i;
-    rv.ucount = db.ucount;
-    rv.icount_cls = db.icount_cls;
-    rv.users = h->N;
-    rv.items = h->M;
-    rv.clock = c;
-    rv.nclass = h->nclass;
-    rv.s = h->s;
-    rv.essp = h->policy == PS_MF_ESSP_ROW;
-    rv.stale = h->stale;
-    const int64_t rows = h->N + static_cast<int64_t>(h->nclass) * h->M;
-    hipLaunchKernelGGL(k_row_views, dim3(static_cast<unsigned>((rows + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                       h->stream, rv);
-    HIP_TRY(h, hipGetLastError());
-  }
+  if (per_row_policy(h) && (rc = row_views(h, db, c))) return rc;
   {
     // set A = user-major (x = user / L, y = item / R); set B = item-major (x = item, y = user)
     CellSweepArgs cs{};
@@ -2153,8 +2178,6 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   if (n < 0 || (n > 0 && (!user || !item || !value))) return fail(h, PS_MF_EINVAL, "bad rating arrays");
   if (n > 0x7fffffffLL) return fail(h, PS_MF_EINVAL, "at most 2^31-1 ratings");
   const bool seq = h->step == PS_MF_STEP_SEQ;
-  if (seq && per_row_policy(h))
-    return fail(h, PS_MF_EINVAL, "the sequential step reads one view per worker and clock: use a table policy");
   if (h->owner.empty()) {
     h->owner.resize(static_cast<size_t>(h->N));
     for (int64_t i = 0; i < h->N; ++i) h->owner[i] = static_cast<int32_t>(i % h->P);

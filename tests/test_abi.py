@@ -320,11 +320,10 @@ def test_seq_option_errors():
         assert e.value.code == ps_mf.EINVAL
     finally:
         ps_mf.ps_mf_destroy(h)
-    for policy in (ps_mf.SSP_ROW, ps_mf.ESSP_ROW):
+    for policy in (ps_mf.SSP_ROW, ps_mf.ESSP_ROW):  # the per-row caches work with the sequential step
         with ps_mf.PsMf(4, 3, 2, 2, 1, 0.1, 0.1, policy=policy, step=ps_mf.STEP_SEQ, host_only=True) as g:
-            with pytest.raises(ps_mf.PsMfError) as e:
-                g.load_ratings(np.array([0]), np.array([0]), np.array([1.0]))
-            assert e.value.code == ps_mf.EINVAL
+            g.load_ratings(np.array([0, 3]), np.array([0, 2]), np.array([1.0, 2.0]))
+            assert g.export_index(ps_mf.IDX_SEQ_ORDER).size == 2
 
 
 # ---------------------------------------------------------------- value-bounded views (PS_MF_VAP)

@@ -512,3 +512,22 @@ def test_seq_graph_replays_equal_eager_launches(gpu, policy, s, B):
             assert np.array_equal(x[0], y[0]) and np.array_equal(x[1], y[1])
         else:
             assert x == y
+
+
+@pytest.mark.parametrize("policy", [oracle.SSP_ROW, oracle.ESSP_ROW])
+@pytest.mark.parametrize("s,B", [(1, 1), (3, 4), (2, 3)])
+def test_tiny_config_seq_per_row_policies(gpu, policy, s, B):
+    """The sequential step under the per-row caches: each worker's copy starts from the
+    versions its client's cache holds; cached versions, staleness and factors against the
+    oracle."""
+    spec = synth.CONFIGS["tiny"]
+    w = synth.generate(spec)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=spec.K, P=spec.P, s=s, eta=spec.eta,
+             lam=spec.lam, clocks=spec.clocks, policy=policy, step=oracle.SEQ, strata=8, B=B, seed=5)
+
+
+def test_medium_shape_scaled_seq_per_row_ragged_rank(gpu):
+    spec = synth.scaled(synth.CONFIGS["medium"], 0.05)
+    w = synth.generate(spec, K=33)
+    run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=33, P=spec.P, s=3, eta=spec.eta,
+             lam=spec.lam, clocks=8, policy=oracle.SSP_ROW, step=oracle.SEQ, strata=32, B=spec.B, seed=spec.seed)

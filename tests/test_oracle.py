@@ -660,10 +660,52 @@ def test_seq_staleness_and_version_log_follow_the_table_policy():
     assert np.array_equal(hist[oracle.ROWMEAN][1], hist[oracle.SEQ][1])
 
 
+@pytest.mark.parametrize("s,P", [(1, 2), (2, 3), (3, 1)])
+def test_seq_under_ssp_row_with_every_row_read_each_clock_is_phase_zero_lazy(s, P):
+    # B = 1: every client reads all its rows at every clock, so every row's view is
+    # c - (c mod (s+1)).  Under SEQ a worker's chain depends on which users it owns, so the
+    # comparison keeps the workers: worker q becomes worker (s+1) q of P(s+1) workers, all
+    # in LAZY phase 0; G = 1 makes the order canonical inside each worker either way.
+    rng = np.random.default_rng(5 * s + P)
+    N, M, K = 24, 15, 3
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 200, K, dup=4)
+    # eta small enough that the summed sequential progress stays finite over these clocks
+    o = oracle.Oracle(N, M, K, P, s, 0.01, 0.05, oracle.SSP_ROW, oracle.SEQ, strata=1)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(3 * s + 4)
+    got = o.get_factors()
+    o.close()
+    owner = ((s + 1) * (np.arange(N) % P)).astype(np.int32)
+    o = oracle.Oracle(N, M, K, P * (s + 1), s, 0.01, 0.05, oracle.SSP_LAZY, oracle.SEQ, owner=owner, strata=1)
+    o.load(user, item, val)
+    o.set_factors(L0, R0)
+    o.clock(3 * s + 4)
+    want = o.get_factors()
+    o.close()
+    assert np.isfinite(got[0]).all() and np.isfinite(got[1]).all()
+    assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+
+
+@pytest.mark.parametrize("s", [1, 3])
+def test_seq_under_essp_row_with_every_row_read_each_clock_is_essp(s):
+    rng = np.random.default_rng(s)
+    N, M, K, P = 24, 15, 3, 4
+    user, item, val, L0, R0 = rand_problem(rng, N, M, 200, K)
+    res = []
+    for policy in (oracle.ESSP_ROW, oracle.ESSP):
+        o = oracle.Oracle(N, M, K, P, s, 0.01, 0.05, policy, oracle.SEQ, strata=3)
+        o.load(user, item, val)
+        o.set_factors(L0, R0)
+        o.clock(7)
+        res.append(o.get_factors() + (o.export(oracle.X_STALENESS),))
+        o.close()
+    assert np.isfinite(res[0][0]).all()
+    for a, b in zip(res[0], res[1]):
+        assert np.array_equal(a, b)
+
+
 def test_seq_argument_errors():
-    for policy in (oracle.SSP_ROW, oracle.ESSP_ROW):
-        with pytest.raises(oracle.OracleError):
-            oracle.Oracle(4, 4, 2, 2, 1, 0.1, 0.0, policy, oracle.SEQ)
     with pytest.raises(oracle.OracleError):
         oracle.Oracle(4, 4, 2, 2, 1, 0.1, 0.0, oracle.SSP_LAZY, oracle.SEQ, strata=0)
     o = oracle.Oracle(4, 4, 2, 2, 1, 0.1, 0.0, oracle.SSP_LAZY, oracle.SUM)
