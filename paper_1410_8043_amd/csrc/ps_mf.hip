@@ -1881,17 +1881,28 @@ int seq_clock(ps_mf_t *h) {
     if (h->seq_exec.empty()) h->seq_exec.assign(static_cast<size_t>(h->B * rows), nullptr);
     hipGraphExec_t &ex = h->seq_exec[static_cast<size_t>(key)];
     if (!ex) {
-      hipGraph_t graph = nullptr;
-      HIP_TRY(h, hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal));
-      const hipError_t le = launch_epochs();
-      const hipError_t ce = hipStreamEndCapture(h->stream, &graph);
-      HIP_TRY(h, le);
-      HIP_TRY(h, ce);
-      const hipError_t ie = hipGraphInstantiate(&ex, graph, nullptr, nullptr, 0);
-      (void)hipGraphDestroy(graph);
-      HIP_TRY(h, ie);
+      // a stream the caller is capturing already (the launches then go into the caller's
+      // graph), or one that cannot start a capture, gets the launches one by one
+      hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+      if (hipStreamIsCapturing(h->stream, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone ||
+          hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+        (void)hipGetLastError();
+        h->seq_graphs = false;
+      } else {
+        hipGraph_t graph = nullptr;
+        const hipError_t le = launch_epochs();
+        const hipError_t ce = hipStreamEndCapture(h->stream, &graph);
+        hipError_t ie = hipSuccess;
+        if (le == hipSuccess && ce == hipSuccess) ie = hipGraphInstantiate(&ex, graph, nullptr, nullptr, 0);
+        if (graph) (void)hipGraphDestroy(graph);
+        HIP_TRY(h, le);
+        HIP_TRY(h, ce);
+        HIP_TRY(h, ie);
+      }
     }
-    HIP_TRY(h, hipGraphLaunch(ex, h->stream));
+  }
+  if (h->seq_graphs && !h->eta_decay) {
+    HIP_TRY(h, hipGraphLaunch(h->seq_exec[static_cast<size_t>(key)], h->stream));
   } else {
     HIP_TRY(h, launch_epochs());
   }

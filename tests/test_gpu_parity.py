@@ -531,3 +531,36 @@ def test_medium_shape_scaled_seq_per_row_ragged_rank(gpu):
     w = synth.generate(spec, K=33)
     run_both(gpu, w.user, w.item, w.val, w.L0, w.R0, N=spec.N, M=spec.M, K=33, P=spec.P, s=3, eta=spec.eta,
              lam=spec.lam, clocks=8, policy=oracle.SSP_ROW, step=oracle.SEQ, strata=32, B=spec.B, seed=spec.seed)
+
+
+def test_seq_clock_inside_a_callers_graph_capture(gpu):
+    """A caller may capture a sequential clock into its own HIP graph (torch.cuda.graph on
+    the handle's stream): the library then launches the sub-epochs one by one into the
+    caller's capture.  With s = 0 and one block every clock runs the same launches, so every
+    replay advances the factors exactly like an eager clock."""
+    import torch
+
+    N, M, K = 300, 120, 16
+    user, item, val, L0, R0 = small_problem(21, N, M, 4000, K)
+    side = torch.cuda.Stream()
+    res = []
+    for captured in (False, True):
+        with gpu.PsMf(N, M, K, 4, 0, 0.02, 0.05, step=gpu.STEP_SEQ, strata=5, stream=side) as g:
+            g.load_ratings(user, item, val)
+            g.set_factors(L0, R0)
+            torch.cuda.synchronize()
+            if captured:
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(graph, stream=side):
+                    g.clock(1)
+                for _ in range(4):  # the capture itself ran nothing; each replay is one clock
+                    graph.replay()
+                    torch.cuda.synchronize()
+                    res.append(g.get_factors())  # s = 0: the one ring slot
+            else:
+                for _ in range(4):
+                    g.clock(1)
+                    torch.cuda.synchronize()
+                    res.append(g.get_factors())
+    for (La, Ra), (Lb, Rb) in zip(res[:4], res[4:]):
+        assert np.array_equal(La, Lb) and np.array_equal(Ra, Rb)
