@@ -232,7 +232,8 @@ def main():
                                (f", v0={args.value_bound}" if args.policy == "vap" else "") +
                                (", eta/sqrt(t)" if args.eta_decay else ""),
                    "global_batch": int(nnz_clock), "parallelism": "1 GPU, P logical workers",
-                   "loss_after": loss,
+                   # null when the run diverged (strict JSON has no NaN)
+                   "loss_after": loss if np.isfinite(loss) else None,
                    **({"chains_runs_ratings": [int(x) for x in split[:3]]} if seq else
                       {"dense_cells_units": [int(x) for x in split[:3]]}),
                    "staleness_profile": profile, **extra},
