@@ -28,9 +28,9 @@ _lib = None
 
 def build(verbose: bool = False) -> str:
     """Compile the oracle with gcc (no fast-math: fp64 evaluation order is kept)."""
-    src = os.path.join(_HERE, "ps_mf_oracle.c")
+    srcs = [os.path.join(_HERE, f) for f in ("ps_mf_oracle.c", "ps_lda_oracle.c")]
     tmp = LIB_PATH + ".tmp"
-    cmd = ["gcc", "-O2", "-fPIC", "-shared", "-std=gnu11", src, "-lm", "-o", tmp]
+    cmd = ["gcc", "-O2", "-fPIC", "-shared", "-std=gnu11", *srcs, "-lm", "-o", tmp]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
@@ -61,6 +61,11 @@ def _load():
         "oracle_set_strata": [vp, i32],
         "oracle_set_value_bound": [vp, dbl],
         "oracle_set_eta_decay": [vp, i32],
+        "lda_create": [i64, i64, i32, i32, i32, dbl, dbl, i32, i32, u64, ctypes.POINTER(vp)],
+        "lda_load": [vp, vp, vp, vp, i64],
+        "lda_clock": [vp, i32],
+        "lda_loglik": [vp, ctypes.POINTER(dbl)],
+        "lda_export": [vp, i32, i32, vp, i64, ctypes.POINTER(i64)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -68,6 +73,8 @@ def _load():
         f.restype = ctypes.c_int
     lib.oracle_destroy.argtypes = [vp]
     lib.oracle_destroy.restype = None
+    lib.lda_destroy.argtypes = [vp]
+    lib.lda_destroy.restype = None
     _lib = lib
     return lib
 
@@ -201,3 +208,68 @@ def run(user, item, val, L0, R0, *, N, M, K, P, s, eta, lam, clocks, policy=SSP_
     o.clock(clocks)
     L, R = o.get_factors()
     return L, R, o.loss(), o
+
+
+# ---- LDA by collapsed Gibbs sampling under SSP / ESSP (Section 5's topic-model workload) ----
+LDA_Z, LDA_NDK, LDA_NWK, LDA_VERSION_LOG, LDA_BLOCK_ORDER = range(5)
+
+
+class LdaOracle:
+    """Clocked SSP/ESSP collapsed Gibbs sampling for LDA on the CPU.
+
+    The shared word-topic counts (and topic totals, row V) are versioned per clock; the
+    doc-topic counts and the assignments stay with the worker that owns the document
+    (d mod P).  Policies: SSP_LAZY, SSP_WORST, ESSP.
+    """
+
+    def __init__(self, D, V, K, P, s, alpha, beta, policy=ESSP, B=2, seed=0):
+        self._lib = _load()
+        self.D, self.V, self.K, self.P, self.s, self.B = int(D), int(V), int(K), int(P), int(s), int(B)
+        h = ctypes.c_void_p()
+        _chk(self._lib.lda_create(self.D, self.V, self.K, self.P, self.s, float(alpha), float(beta), int(policy),
+                                  self.B, int(seed) & (2**64 - 1), ctypes.byref(h)), "lda_create")
+        self._h = h
+
+    def close(self):
+        if self._h:
+            self._lib.lda_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def load(self, doc, word, z0):
+        self._keep = (_c(doc, np.int32), _c(word, np.int32), _c(z0, np.int32))
+        n = self._keep[0].shape[0]
+        _chk(self._lib.lda_load(self._h, *(a.ctypes.data if n else None for a in self._keep), n), "lda_load")
+        self._keep = None
+
+    def clock(self, n=1):
+        _chk(self._lib.lda_clock(self._h, int(n)), "lda_clock")
+
+    def loglik(self) -> float:
+        out = ctypes.c_double()
+        _chk(self._lib.lda_loglik(self._h, ctypes.byref(out)), "lda_loglik")
+        return out.value
+
+    def export(self, kind, block=0):
+        n = ctypes.c_int64()
+        _chk(self._lib.lda_export(self._h, kind, block, None, 0, ctypes.byref(n)), "lda_export")
+        dt = np.int32 if kind in (LDA_Z, LDA_NDK, LDA_NWK) else np.int64
+        buf = np.empty(n.value, dtype=dt)
+        _chk(self._lib.lda_export(self._h, kind, block, buf.ctypes.data if n.value else None, n.value,
+                                  ctypes.byref(n)), "lda_export")
+        return buf
+
+    def z(self):
+        return self.export(LDA_Z)
+
+    def ndk(self):
+        return self.export(LDA_NDK).reshape(self.D, self.K)
+
+    def nwk(self):
+        """Latest version: [V+1, K], row V the topic totals."""
+        return self.export(LDA_NWK).reshape(self.V + 1, self.K)

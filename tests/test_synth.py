@@ -47,3 +47,20 @@ def test_normal_generator_moments():
     # counter-based: a prefix does not depend on the length asked for
     y = synth.normal((1000,), 0.5, 3, 9)
     assert np.array_equal(y, x[:1000].astype(np.float32))
+
+
+def test_lda_corpus_is_seeded_and_in_range():
+    from paper_1410_8043_amd.synth import lda_corpus as lc
+    spec = lc.scaled(lc.CORPORA["small"], 0.01)
+    a, b = lc.generate(spec), lc.generate(spec)
+    for x, y in ((a.doc, b.doc), (a.word, b.word), (a.z0, b.z0)):
+        np.testing.assert_array_equal(x, y)
+    assert a.ntok == a.doc.shape[0] == a.word.shape[0] == a.z0.shape[0]
+    assert a.doc.dtype == a.word.dtype == a.z0.dtype == np.int32
+    assert (np.diff(a.doc) >= 0).all() and a.doc.max() < spec.D
+    assert 0 <= a.word.min() and a.word.max() < spec.V
+    assert 0 <= a.z0.min() and a.z0.max() < spec.K
+    assert abs(a.ntok / spec.D - spec.mean_len) < 0.05 * spec.mean_len
+    # Zipf-shaped word frequencies: the most frequent words take a large share
+    cnt = np.sort(np.bincount(a.word, minlength=spec.V))[::-1]
+    assert cnt[:spec.V // 100].sum() > 0.1 * a.ntok  # uniform words would give 1%
