@@ -7,7 +7,8 @@ import subprocess
 _HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(_HERE)
 LIB_PATH = os.path.join(_HERE, "libps_mf.so")
-SOURCES = [os.path.join(_HERE, "csrc", "ps_mf.hip"), os.path.join(_HERE, "csrc", "layout.cpp")]
+SOURCES = [os.path.join(_HERE, "csrc", "ps_mf.hip"), os.path.join(_HERE, "csrc", "ps_lda.hip"),
+           os.path.join(_HERE, "csrc", "layout.cpp")]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -1,0 +1,640 @@
+// LDA by collapsed Gibbs sampling under clocked SSP / ESSP (arXiv 1410.8043, Section 5's
+// topic-modeling workload) on one gfx950 GPU: P logical workers, one wavefront each.
+//
+// Design:
+//   - the shared state is a ring of s+2 committed versions of the (V+1) x K int32 counts
+//     (word-topic rows, then the topic totals); the version of clock c+1 is built in its own
+//     slot: a device copy of version c, then every worker's changes added with integer
+//     atomics as they happen (integer sums: exact and order-free);
+//   - one wavefront per worker, lanes over topics (lane l holds topics l, l+64, ...): the
+//     collapsed conditional's K weights are computed in fp64 and quantised to integers, their
+//     prefix sums come from a wave-wide scan, and the drawn topic from one ballot;
+//   - a worker reads its view plus its own changes of the clock: these live in a private
+//     dense delta table (words x K) whose rows carry the clock that last wrote them, so a row
+//     from an older clock reads as zero and nothing is cleared between clocks; the worker's
+//     topic-total changes stay in registers and are added to the new version at its end;
+//   - the doc-topic row of the current document stays in registers while the worker's tokens
+//     of that document run (tokens are in (document, load index) order).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "ps_lda.h"
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kMaxTopicsPerLane = 8;  // K <= 512
+constexpr uint64_t kDrawSalt = 0x5851F42D4C957F2DULL;
+constexpr int kLoglikBlocks = 1024;
+constexpr int kLoglikThreads = 256;
+
+// one step of SplitMix64 (Steele, Lea and Flood 2014) from state x
+__host__ __device__ inline uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ULL;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+// the staleness of worker p's view at clock c under each policy
+__host__ __device__ inline int64_t view_of(int policy, int64_t s, int64_t p, int64_t c) {
+  int64_t d;
+  if (policy == PS_LDA_SSP_LAZY) d = (c + p % (s + 1)) % (s + 1);
+  else if (policy == PS_LDA_SSP_WORST) d = s;
+  else d = s < 1 ? s : 1;
+  return c - d < 0 ? 0 : c - d;
+}
+
+struct SweepArgs {
+  const int4 *rec;      // per block position: {word, document, load index, 0}
+  int32_t *z;           // per block position: current topic
+  int32_t *ndk;         // D x K
+  int32_t *ring;        // nslots x (V+1) x K
+  int32_t *delta;       // P x V x K, rows valid where tag == tagc
+  int32_t *tag;         // P x V
+  const int64_t *wbeg;  // P+1 block positions of this clock's block
+  int64_t slot_stride;  // (V+1) * K
+  int64_t V;
+  int64_t c;
+  double alpha, beta, Vbeta;
+  uint64_t seed;
+  int32_t K, s, policy, nslots, tagc;
+};
+
+// inclusive prefix sum of a 64-bit value over the wavefront
+__device__ inline uint64_t wave_scan(uint64_t x, int lane) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint64_t y = __shfl_up(x, o, kWave);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+template <int KPL>
+__global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
+  const int lane = threadIdx.x;
+  const int64_t p = blockIdx.x;
+  const int64_t q0 = a.wbeg[p], q1 = a.wbeg[p + 1];
+  if (q0 >= q1) return;
+  const int K = a.K;
+  const int64_t V = a.V, c = a.c;
+  const int64_t v = view_of(a.policy, a.s, p, c);
+  const int32_t *view = a.ring + (v % a.nslots) * a.slot_stride;
+  int32_t *next = a.ring + ((c + 1) % a.nslots) * a.slot_stride;
+  int32_t *mydelta = a.delta + p * V * K;
+  int32_t *mytag = a.tag + p * V;
+  const uint64_t rbase = a.seed ^ kDrawSalt ^ (static_cast<uint64_t>(c) << 40);
+
+  int vk[KPL], dk[KPL], nd[KPL];
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    const int k = j * kWave + lane;
+    vk[j] = k < K ? view[V * K + k] : 0;
+    dk[j] = 0;
+    nd[j] = 0;
+  }
+  int cur_doc = -1;
+  for (int64_t q = q0; q < q1; ++q) {
+    const int4 r = a.rec[q];
+    const int w = __builtin_amdgcn_readfirstlane(r.x);
+    const int d = __builtin_amdgcn_readfirstlane(r.y);
+    const int t = __builtin_amdgcn_readfirstlane(r.z);
+    const int k0 = __builtin_amdgcn_readfirstlane(a.z[q]);
+    const bool fresh = __builtin_amdgcn_readfirstlane(mytag[w]) != a.tagc;
+    const int64_t wrow = static_cast<int64_t>(w) * K;
+    int nw[KPL], dw[KPL];
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const int k = j * kWave + lane;
+      nw[j] = k < K ? view[wrow + k] : 0;
+      dw[j] = k < K ? mydelta[wrow + k] : 0;
+    }
+    if (d != cur_doc) {
+      if (cur_doc >= 0) {
+#pragma unroll
+        for (int j = 0; j < KPL; ++j)
+          if (j * kWave + lane < K) a.ndk[static_cast<int64_t>(cur_doc) * K + j * kWave + lane] = nd[j];
+      }
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) {
+        const int k = j * kWave + lane;
+        nd[j] = k < K ? a.ndk[static_cast<int64_t>(d) * K + k] : 0;
+      }
+      cur_doc = d;
+    }
+    if (fresh) {
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) dw[j] = 0;
+    }
+    // quantised weights of the collapsed conditional and their prefix sums in topic order
+    uint64_t cum[KPL];
+    uint64_t total = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const int k = j * kWave + lane;
+      uint64_t om = 0;
+      if (k < K) {
+        const int self = k == k0;
+        const int ndx = nd[j] - self;
+        const int nwx = max(nw[j] + dw[j] - self, 0);
+        const int nkx = max(vk[j] + dk[j] - self, 0);
+        const double num = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
+        const double pk = num / (static_cast<double>(nkx) + a.Vbeta);
+        om = static_cast<uint64_t>(floor(pk * 16777216.0));
+      }
+      const uint64_t incl = wave_scan(om, lane);
+      cum[j] = incl + total;
+      total += __shfl(incl, kWave - 1, kWave);
+    }
+    int k1 = k0;
+    if (total != 0) {
+      const uint64_t target = __umul64hi(splitmix64(rbase ^ static_cast<uint64_t>(static_cast<uint32_t>(t))), total);
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) {
+        const uint64_t m = __ballot(cum[j] > target);
+        if (m != 0) {
+          k1 = j * kWave + __ffsll(static_cast<unsigned long long>(m)) - 1;
+          break;
+        }
+      }
+    }
+    if (k1 != k0) {
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) {
+        const int k = j * kWave + lane;
+        const int dl = (k == k1) - (k == k0);
+        nd[j] += dl;
+        dk[j] += dl;
+        dw[j] += dl;
+        if (k < K) {
+          if (fresh || dl != 0) mydelta[wrow + k] = dw[j];
+          if (dl != 0) atomicAdd(next + wrow + k, dl);
+        }
+      }
+      if (lane == 0) {
+        a.z[q] = k1;
+        if (fresh) mytag[w] = a.tagc;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    const int k = j * kWave + lane;
+    if (k < K) {
+      a.ndk[static_cast<int64_t>(cur_doc) * K + k] = nd[j];
+      if (dk[j] != 0) atomicAdd(next + V * K + k, dk[j]);
+    }
+  }
+}
+
+// collapsed log p(w, z): per-thread terms over (word, topic) counts, topic totals and
+// documents, a fixed-order block reduction into one partial per block
+__global__ __launch_bounds__(kLoglikThreads) void k_lda_loglik(const int32_t *n, const int32_t *ndk, int64_t V,
+                                                               int32_t K, int64_t D, double alpha, double beta,
+                                                               double Vbeta, double *partial) {
+  __shared__ double red[kLoglikThreads];
+  const int64_t VK = V * K, total = VK + K + D;
+  const double lg_beta = lgamma(beta), lg_alpha = lgamma(alpha), Ka = K * alpha;
+  double acc = 0.0;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    if (i < VK) {
+      const int32_t x = n[i];
+      if (x > 0) acc += lgamma(x + beta) - lg_beta;
+    } else if (i < VK + K) {
+      acc += lgamma(Vbeta) - lgamma(n[i] + Vbeta);
+    } else {
+      const int32_t *row = ndk + (i - VK - K) * K;
+      int64_t len = 0;
+      double t = 0.0;
+      for (int k = 0; k < K; ++k) {
+        const int32_t x = row[k];
+        len += x;
+        if (x > 0) t += lgamma(x + alpha) - lg_alpha;
+      }
+      acc += t + lgamma(Ka) - lgamma(static_cast<double>(len) + Ka);
+    }
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int o = kLoglikThreads / 2; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) partial[blockIdx.x] = red[0];
+}
+
+__global__ __launch_bounds__(kLoglikThreads) void k_lda_sum(const double *partial, int n, double *out) {
+  __shared__ double red[kLoglikThreads];
+  double acc = 0.0;
+  for (int i = threadIdx.x; i < n; i += kLoglikThreads) acc += partial[i];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int o = kLoglikThreads / 2; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0];
+}
+
+}  // namespace
+
+struct ps_lda {
+  int64_t D = 0, V = 0;
+  int32_t K = 0, P = 0, s = 0;
+  double alpha = 0, beta = 0, Vbeta = 0;
+  int32_t policy = PS_LDA_ESSP, B = 2;
+  uint64_t seed = 0;
+  bool host_only = false, timing = false, loaded = false;
+  int64_t clock = 0, ntok = 0;
+  int device = -1;
+  hipStream_t stream = nullptr, user_stream = nullptr;
+  bool own_stream = false;
+  std::string err;
+  std::vector<void *> allocations;
+  std::vector<int64_t> wbeg;   // B x (P+1) block positions
+  std::vector<int64_t> order;  // load index at every block position
+  std::vector<int64_t> vlog;
+  int4 *rec = nullptr;
+  int32_t *z = nullptr, *ndk = nullptr, *ring = nullptr, *delta = nullptr, *tag = nullptr;
+  int64_t *wbeg_dev = nullptr;
+  double *partial = nullptr;
+  struct Ev {
+    hipEvent_t a, b;
+  };
+  std::vector<Ev> events;
+  double kernel_ms = 0;
+  int64_t kernel_count = 0;
+};
+
+namespace {
+
+int lda_fail(ps_lda_t *h, int code, const char *fmt, ...) {
+  if (h) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    h->err = buf;
+  }
+  return code;
+}
+
+#define LDA_TRY(h, expr)                                                                                       \
+  do {                                                                                                        \
+    hipError_t e_ = (expr);                                                                                   \
+    if (e_ != hipSuccess) {                                                                                   \
+      if (e_ == hipErrorOutOfMemory) return lda_fail(h, PS_LDA_ENOMEM, "%s: %s", #expr, hipGetErrorString(e_)); \
+      return lda_fail(h, PS_LDA_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_));                             \
+    }                                                                                                         \
+  } while (0)
+
+int lda_alloc(ps_lda_t *h, void **p, size_t bytes) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    if (e == hipErrorOutOfMemory) return lda_fail(h, PS_LDA_ENOMEM, "hipMalloc(%zu bytes): out of memory", bytes);
+    return lda_fail(h, PS_LDA_EDEVICE, "hipMalloc(%zu bytes): %s", bytes, hipGetErrorString(e));
+  }
+  h->allocations.push_back(*p);
+  return PS_LDA_OK;
+}
+
+int lda_device(ps_lda_t *h) {
+  if (h->device < 0) {
+    int dev = 0;
+    LDA_TRY(h, hipGetDevice(&dev));
+    h->device = dev;
+  }
+  LDA_TRY(h, hipSetDevice(h->device));
+  if (!h->stream) {
+    if (h->user_stream) {
+      h->stream = h->user_stream;
+    } else {
+      LDA_TRY(h, hipStreamCreateWithFlags(&h->stream, hipStreamNonBlocking));
+      h->own_stream = true;
+    }
+  }
+  return PS_LDA_OK;
+}
+
+int64_t slot_stride(const ps_lda_t *h) { return (h->V + 1) * h->K; }
+
+template <int KPL>
+void launch_sweep(const SweepArgs &a, int P, hipStream_t st) {
+  hipLaunchKernelGGL(k_lda_sweep<KPL>, dim3(P), dim3(kWave), 0, st, a);
+}
+
+int sweep(ps_lda_t *h) {
+  const int64_t c = h->clock, b = c % h->B, ns = h->s + 2, stride = slot_stride(h);
+  int32_t *cur = h->ring + (c % ns) * stride, *nxt = h->ring + ((c + 1) % ns) * stride;
+  LDA_TRY(h, hipMemcpyAsync(nxt, cur, sizeof(int32_t) * stride, hipMemcpyDeviceToDevice, h->stream));
+  SweepArgs a;
+  a.rec = h->rec;
+  a.z = h->z;
+  a.ndk = h->ndk;
+  a.ring = h->ring;
+  a.delta = h->delta;
+  a.tag = h->tag;
+  a.wbeg = h->wbeg_dev + b * (h->P + 1);
+  a.slot_stride = stride;
+  a.V = h->V;
+  a.c = c;
+  a.alpha = h->alpha;
+  a.beta = h->beta;
+  a.Vbeta = h->Vbeta;
+  a.seed = h->seed;
+  a.K = h->K;
+  a.s = h->s;
+  a.policy = h->policy;
+  a.nslots = static_cast<int32_t>(ns);
+  a.tagc = static_cast<int32_t>(c + 1);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (h->timing) {
+    LDA_TRY(h, hipEventCreate(&e0));
+    LDA_TRY(h, hipEventRecord(e0, h->stream));
+  }
+  switch ((h->K + kWave - 1) / kWave) {
+    case 1: launch_sweep<1>(a, h->P, h->stream); break;
+    case 2: launch_sweep<2>(a, h->P, h->stream); break;
+    case 3: launch_sweep<3>(a, h->P, h->stream); break;
+    case 4: launch_sweep<4>(a, h->P, h->stream); break;
+    case 5: launch_sweep<5>(a, h->P, h->stream); break;
+    case 6: launch_sweep<6>(a, h->P, h->stream); break;
+    case 7: launch_sweep<7>(a, h->P, h->stream); break;
+    default: launch_sweep<8>(a, h->P, h->stream); break;
+  }
+  LDA_TRY(h, hipGetLastError());
+  if (h->timing) {
+    LDA_TRY(h, hipEventCreate(&e1));
+    LDA_TRY(h, hipEventRecord(e1, h->stream));
+    h->events.push_back({e0, e1});
+  }
+  for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_of(h->policy, h->s, p, c));
+  h->clock = c + 1;
+  return PS_LDA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ps_lda_create(int64_t D, int64_t V, int32_t K, int32_t P, int32_t s, double alpha, double beta,
+                  ps_lda_t **out) {
+  if (!out) return PS_LDA_EINVAL;
+  *out = nullptr;
+  if (D < 1 || V < 1 || D > 0x7fffffff || V > 0x7fffffff) return PS_LDA_EINVAL;
+  if (K < 1 || K > kWave * kMaxTopicsPerLane || P < 1 || P > 65536 || s < 0 || s > 1024) return PS_LDA_EINVAL;
+  if (!(alpha > 0) || !(beta > 0) || !std::isfinite(alpha) || !std::isfinite(beta)) return PS_LDA_EINVAL;
+  ps_lda_t *h = new (std::nothrow) ps_lda_t();
+  if (!h) return PS_LDA_ENOMEM;
+  h->D = D;
+  h->V = V;
+  h->K = K;
+  h->P = P;
+  h->s = s;
+  h->alpha = alpha;
+  h->beta = beta;
+  h->Vbeta = static_cast<double>(V) * beta;
+  *out = h;
+  return PS_LDA_OK;
+}
+
+int ps_lda_set_option(ps_lda_t *h, int32_t key, int64_t value) {
+  if (!h) return PS_LDA_EINVAL;
+  if (h->loaded) return lda_fail(h, PS_LDA_ESTATE, "options must be set before ps_lda_load");
+  switch (key) {
+    case PS_LDA_OPT_POLICY:
+      if (value < PS_LDA_SSP_LAZY || value > PS_LDA_ESSP) return lda_fail(h, PS_LDA_EINVAL, "unknown policy %lld", (long long)value);
+      h->policy = static_cast<int32_t>(value);
+      return PS_LDA_OK;
+    case PS_LDA_OPT_MB_BLOCKS:
+      if (value < 1 || value > 65536) return lda_fail(h, PS_LDA_EINVAL, "blocks must be in [1, 65536]");
+      h->B = static_cast<int32_t>(value);
+      return PS_LDA_OK;
+    case PS_LDA_OPT_SEED:
+      h->seed = static_cast<uint64_t>(value);
+      return PS_LDA_OK;
+    case PS_LDA_OPT_HOST_ONLY:
+      h->host_only = value != 0;
+      return PS_LDA_OK;
+    case PS_LDA_OPT_TIMING:
+      h->timing = value != 0;
+      return PS_LDA_OK;
+    default:
+      return lda_fail(h, PS_LDA_EINVAL, "unknown option %d", key);
+  }
+}
+
+int ps_lda_set_stream(ps_lda_t *h, void *hip_stream) {
+  if (!h) return PS_LDA_EINVAL;
+  if (h->stream) (void)hipStreamSynchronize(h->stream);
+  if (h->stream && h->own_stream) {
+    (void)hipStreamDestroy(h->stream);
+    h->own_stream = false;
+  }
+  h->stream = nullptr;
+  h->user_stream = static_cast<hipStream_t>(hip_stream);
+  if (h->loaded && !h->host_only) return lda_device(h);
+  return PS_LDA_OK;
+}
+
+int ps_lda_load(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int32_t *z0, int64_t n) {
+  if (!h) return PS_LDA_EINVAL;
+  if (h->loaded) return lda_fail(h, PS_LDA_ESTATE, "tokens already loaded");
+  if (n < 0 || n > 0x7fffffff) return lda_fail(h, PS_LDA_EINVAL, "token count %lld out of range", (long long)n);
+  if (n > 0 && (!doc || !word || !z0)) return lda_fail(h, PS_LDA_EINVAL, "null token array");
+  for (int64_t t = 0; t < n; ++t) {
+    if (doc[t] < 0 || doc[t] >= h->D) return lda_fail(h, PS_LDA_EINVAL, "token %lld: document out of range", (long long)t);
+    if (word[t] < 0 || word[t] >= h->V) return lda_fail(h, PS_LDA_EINVAL, "token %lld: word out of range", (long long)t);
+    if (z0[t] < 0 || z0[t] >= h->K) return lda_fail(h, PS_LDA_EINVAL, "token %lld: topic out of range", (long long)t);
+  }
+  const int64_t P = h->P, B = h->B, K = h->K, V = h->V;
+  // processing order: block, worker (document mod P), document, load index
+  std::vector<std::pair<uint64_t, int64_t>> key(static_cast<size_t>(n));
+  std::vector<int64_t> count(static_cast<size_t>(B * P) + 1, 0);
+  for (int64_t t = 0; t < n; ++t) {
+    const uint64_t b = B == 1 ? 0 : splitmix64(h->seed ^ static_cast<uint64_t>(t)) % static_cast<uint64_t>(B);
+    const uint64_t bucket = b * static_cast<uint64_t>(P) + static_cast<uint64_t>(doc[t] % P);
+    key[t] = {(bucket << 32) | static_cast<uint32_t>(doc[t]), t};
+    count[bucket + 1] += 1;
+  }
+  std::sort(key.begin(), key.end());
+  for (int64_t i = 0; i < B * P; ++i) count[i + 1] += count[i];
+  h->wbeg.assign(static_cast<size_t>(B * (P + 1)), 0);
+  for (int64_t b = 0; b < B; ++b)
+    for (int64_t p = 0; p <= P; ++p) h->wbeg[b * (P + 1) + p] = count[b * P + p];
+  h->order.resize(static_cast<size_t>(n));
+  for (int64_t q = 0; q < n; ++q) h->order[q] = key[q].second;
+  h->ntok = n;
+  if (h->host_only) {
+    h->loaded = true;
+    return PS_LDA_OK;
+  }
+  int rc = lda_device(h);
+  if (rc) return rc;
+  std::vector<int4> rec(static_cast<size_t>(n));
+  std::vector<int32_t> zq(static_cast<size_t>(n));
+  std::vector<int32_t> ndk(static_cast<size_t>(h->D * K), 0);
+  std::vector<int32_t> n0(static_cast<size_t>((V + 1) * K), 0);
+  for (int64_t q = 0; q < n; ++q) {
+    const int64_t t = h->order[q];
+    rec[q] = make_int4(word[t], doc[t], static_cast<int>(t), 0);
+    zq[q] = z0[t];
+    ndk[static_cast<int64_t>(doc[t]) * K + z0[t]] += 1;
+    n0[static_cast<int64_t>(word[t]) * K + z0[t]] += 1;
+    n0[V * K + z0[t]] += 1;
+  }
+  const int64_t stride = slot_stride(h), ns = h->s + 2;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->rec), sizeof(int4) * n))) return rc;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->z), sizeof(int32_t) * n))) return rc;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->ndk), sizeof(int32_t) * h->D * K))) return rc;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->ring), sizeof(int32_t) * stride * ns))) return rc;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->delta), sizeof(int32_t) * P * V * K))) return rc;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->tag), sizeof(int32_t) * P * V))) return rc;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->wbeg_dev), sizeof(int64_t) * h->wbeg.size()))) return rc;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->partial), sizeof(double) * (kLoglikBlocks + 1)))) return rc;
+  if (n > 0) {
+    LDA_TRY(h, hipMemcpy(h->rec, rec.data(), sizeof(int4) * n, hipMemcpyHostToDevice));
+    LDA_TRY(h, hipMemcpy(h->z, zq.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice));
+  }
+  LDA_TRY(h, hipMemcpy(h->ndk, ndk.data(), sizeof(int32_t) * ndk.size(), hipMemcpyHostToDevice));
+  LDA_TRY(h, hipMemset(h->ring, 0, sizeof(int32_t) * stride * ns));
+  LDA_TRY(h, hipMemcpy(h->ring, n0.data(), sizeof(int32_t) * n0.size(), hipMemcpyHostToDevice));
+  LDA_TRY(h, hipMemset(h->tag, 0, sizeof(int32_t) * P * V));
+  LDA_TRY(h, hipMemcpy(h->wbeg_dev, h->wbeg.data(), sizeof(int64_t) * h->wbeg.size(), hipMemcpyHostToDevice));
+  LDA_TRY(h, hipDeviceSynchronize());
+  h->loaded = true;
+  return PS_LDA_OK;
+}
+
+int ps_lda_clock(ps_lda_t *h, int32_t n) {
+  if (!h || n < 0) return PS_LDA_EINVAL;
+  if (!h->loaded) return lda_fail(h, PS_LDA_ESTATE, "ps_lda_clock before ps_lda_load");
+  if (h->host_only) return lda_fail(h, PS_LDA_ESTATE, "host-only handle: no device work");
+  if (h->clock + n >= 0x7fffffff) return lda_fail(h, PS_LDA_EINVAL, "clock count overflows");
+  int rc = lda_device(h);
+  if (rc) return rc;
+  for (int32_t i = 0; i < n; ++i)
+    if ((rc = sweep(h))) return rc;
+  return PS_LDA_OK;
+}
+
+int ps_lda_loglik(ps_lda_t *h, double *out) {
+  if (!h || !out) return PS_LDA_EINVAL;
+  if (!h->loaded || h->host_only) return lda_fail(h, PS_LDA_ESTATE, "no device state");
+  int rc = lda_device(h);
+  if (rc) return rc;
+  const int32_t *n = h->ring + (h->clock % (h->s + 2)) * slot_stride(h);
+  hipLaunchKernelGGL(k_lda_loglik, dim3(kLoglikBlocks), dim3(kLoglikThreads), 0, h->stream, n, h->ndk, h->V, h->K,
+                     h->D, h->alpha, h->beta, h->Vbeta, h->partial);
+  hipLaunchKernelGGL(k_lda_sum, dim3(1), dim3(kLoglikThreads), 0, h->stream, h->partial, kLoglikBlocks,
+                     h->partial + kLoglikBlocks);
+  LDA_TRY(h, hipGetLastError());
+  LDA_TRY(h, hipMemcpyAsync(out, h->partial + kLoglikBlocks, sizeof(double), hipMemcpyDeviceToHost, h->stream));
+  LDA_TRY(h, hipStreamSynchronize(h->stream));
+  return PS_LDA_OK;
+}
+
+int ps_lda_get_clock(ps_lda_t *h, int64_t *clock) {
+  if (!h || !clock) return PS_LDA_EINVAL;
+  *clock = h->clock;
+  return PS_LDA_OK;
+}
+
+int ps_lda_export(ps_lda_t *h, int32_t kind, int32_t block, void *buf, int64_t cap, int64_t *len) {
+  if (!h || !len) return PS_LDA_EINVAL;
+  if (!h->loaded && kind != PS_LDA_X_VERSION_LOG) return lda_fail(h, PS_LDA_ESTATE, "nothing loaded");
+  const bool device_kind = kind == PS_LDA_X_Z || kind == PS_LDA_X_NDK || kind == PS_LDA_X_NWK;
+  if (device_kind && h->host_only) return lda_fail(h, PS_LDA_ESTATE, "host-only handle: no device state");
+  int64_t n;
+  switch (kind) {
+    case PS_LDA_X_Z: n = h->ntok; break;
+    case PS_LDA_X_NDK: n = h->D * h->K; break;
+    case PS_LDA_X_NWK: n = slot_stride(h); break;
+    case PS_LDA_X_VERSION_LOG: n = static_cast<int64_t>(h->vlog.size()); break;
+    case PS_LDA_X_BLOCK_ORDER:
+      if (block < 0 || block >= h->B) return lda_fail(h, PS_LDA_EINVAL, "block %d out of range", block);
+      n = h->wbeg[block * (h->P + 1) + h->P] - h->wbeg[block * (h->P + 1)];
+      break;
+    default: return lda_fail(h, PS_LDA_EINVAL, "unknown export %d", kind);
+  }
+  *len = n;
+  if (!buf) return PS_LDA_OK;
+  if (cap < n) return lda_fail(h, PS_LDA_EINVAL, "buffer holds %lld, needs %lld", (long long)cap, (long long)n);
+  if (n == 0) return PS_LDA_OK;
+  if (device_kind) {
+    int rc = lda_device(h);
+    if (rc) return rc;
+    LDA_TRY(h, hipStreamSynchronize(h->stream));
+  }
+  switch (kind) {
+    case PS_LDA_X_Z: {
+      std::vector<int32_t> zq(static_cast<size_t>(n));
+      LDA_TRY(h, hipMemcpy(zq.data(), h->z, sizeof(int32_t) * n, hipMemcpyDeviceToHost));
+      int32_t *o = static_cast<int32_t *>(buf);
+      for (int64_t q = 0; q < n; ++q) o[h->order[q]] = zq[q];
+      break;
+    }
+    case PS_LDA_X_NDK: LDA_TRY(h, hipMemcpy(buf, h->ndk, sizeof(int32_t) * n, hipMemcpyDeviceToHost)); break;
+    case PS_LDA_X_NWK:
+      LDA_TRY(h, hipMemcpy(buf, h->ring + (h->clock % (h->s + 2)) * slot_stride(h), sizeof(int32_t) * n,
+                           hipMemcpyDeviceToHost));
+      break;
+    case PS_LDA_X_VERSION_LOG: std::memcpy(buf, h->vlog.data(), sizeof(int64_t) * n); break;
+    case PS_LDA_X_BLOCK_ORDER:
+      std::memcpy(buf, h->order.data() + h->wbeg[block * (h->P + 1)], sizeof(int64_t) * n);
+      break;
+  }
+  return PS_LDA_OK;
+}
+
+int ps_lda_kernel_time(ps_lda_t *h, double *ms, int64_t *count) {
+  if (!h || !ms || !count) return PS_LDA_EINVAL;
+  if (h->stream) LDA_TRY(h, hipStreamSynchronize(h->stream));
+  for (auto &ev : h->events) {
+    float t = 0;
+    LDA_TRY(h, hipEventElapsedTime(&t, ev.a, ev.b));
+    h->kernel_ms += t;
+    h->kernel_count += 1;
+    (void)hipEventDestroy(ev.a);
+    (void)hipEventDestroy(ev.b);
+  }
+  h->events.clear();
+  *ms = h->kernel_ms;
+  *count = h->kernel_count;
+  return PS_LDA_OK;
+}
+
+const char *ps_lda_last_error(const ps_lda_t *h) {
+  if (!h) return "null handle";
+  return h->err.c_str();
+}
+
+void ps_lda_destroy(ps_lda_t *h) {
+  if (!h) return;
+  if (h->stream) (void)hipStreamSynchronize(h->stream);
+  for (auto &ev : h->events) {
+    (void)hipEventDestroy(ev.a);
+    (void)hipEventDestroy(ev.b);
+  }
+  for (void *p : h->allocations) (void)hipFree(p);
+  if (h->own_stream && h->stream) (void)hipStreamDestroy(h->stream);
+  delete h;
+}
+
+}  // extern "C"

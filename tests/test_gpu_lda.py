@@ -1,0 +1,138 @@
+"""HIP collapsed-Gibbs LDA under SSP / ESSP vs the CPU oracle, through the C ABI (MI355X).
+
+The sampler's state is integer (assignments, doc-topic counts, versioned word-topic counts)
+and its draw is exact integer arithmetic over fp64 weights evaluated in the same IEEE
+operations on both sides, so the bar is bit-exact: every assignment and count after every
+checked clock.  The log-likelihood (fp64 sums of lgamma terms in different orders, the
+library's lgamma against the C library's) within a relative 1e-9.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1410_8043_amd.synth import lda_corpus as lc
+
+pytestmark = pytest.mark.gpu
+
+LL_RTOL = 1e-9
+POLICIES = [oracle.SSP_LAZY, oracle.SSP_WORST, oracle.ESSP]
+
+
+@pytest.fixture(scope="module")
+def lda():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_1410_8043_amd import ps_lda
+
+    return ps_lda
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def both(lda, spec, corpus, policy, clocks, check_every=None, **opts):
+    say(f"lda case {spec.name} D={spec.D} V={spec.V} K={spec.K} P={spec.P} s={spec.s} B={spec.B} "
+        f"alpha={spec.alpha} policy={policy} tokens={corpus.ntok} clocks={clocks}")
+    g = lda.PsLda(spec.D, spec.V, spec.K, spec.P, spec.s, spec.alpha, spec.beta, policy=policy, B=spec.B,
+                  seed=spec.seed, **opts)
+    g.load(corpus.doc, corpus.word, corpus.z0)
+    o = oracle.LdaOracle(spec.D, spec.V, spec.K, spec.P, spec.s, spec.alpha, spec.beta, policy, spec.B, spec.seed)
+    o.load(corpus.doc, corpus.word, corpus.z0)
+    step = check_every or clocks
+    done = 0
+    while done < clocks:
+        n = min(step, clocks - done)
+        g.clock(n)
+        o.clock(n)
+        done += n
+        np.testing.assert_array_equal(g.z(), o.z(), err_msg=f"assignments after {done} clocks")
+        np.testing.assert_array_equal(g.ndk(), o.ndk(), err_msg=f"doc-topic counts after {done} clocks")
+        np.testing.assert_array_equal(g.nwk(), o.nwk(), err_msg=f"word-topic counts after {done} clocks")
+    np.testing.assert_array_equal(g.export(lda.X_VERSION_LOG), o.export(oracle.LDA_VERSION_LOG))
+    assert g.get_clock() == clocks
+    assert g.loglik() == pytest.approx(o.loglik(), rel=LL_RTOL)
+    return g, o
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+@pytest.mark.parametrize("P,s,B", [(4, 2, 2), (3, 0, 1), (7, 3, 3), (1, 1, 2)])
+def test_tiny_corpus_bit_exact(lda, policy, P, s, B):
+    spec = lc.scaled(lc.CORPORA["tiny"], 1.0, P=P, s=s, B=B)
+    both(lda, spec, lc.generate(spec), policy, 10, check_every=3)
+
+
+@pytest.mark.parametrize("K", [1, 2, 63, 64, 65, 100, 130, 200, 320, 512])
+def test_every_topic_count_layout(lda, K):
+    # one to eight topics per lane, ragged last lane group
+    spec = lc.scaled(lc.CORPORA["tiny"], 0.3, K=K, V=80, P=3, s=1)
+    both(lda, spec, lc.generate(spec), oracle.ESSP, 5)
+
+
+@pytest.mark.parametrize("alpha", [1e-6, 1e-9])
+def test_integer_boundaries_and_zero_weights(lda, alpha):
+    # weights of a few units: draws land on prefix sums; alpha 1e-9: all-zero weights keep the topic
+    spec = lc.scaled(lc.CORPORA["tiny"], 1.0, D=300, V=10, K=6, P=3, s=1, mean_len=1, alpha=alpha, beta=0.5)
+    both(lda, spec, lc.generate(spec), oracle.ESSP, 6, check_every=2)
+
+
+def test_more_workers_than_documents(lda):
+    spec = lc.scaled(lc.CORPORA["tiny"], 1.0, D=40, P=300, s=2)
+    both(lda, spec, lc.generate(spec), oracle.SSP_LAZY, 6)
+
+
+def test_repeated_words_in_a_document(lda):
+    # tiny vocabulary: a worker's consecutive tokens share a word, its delta row is read back at once
+    spec = lc.scaled(lc.CORPORA["tiny"], 1.0, D=50, V=3, K=5, P=2, s=2, mean_len=40, beta=0.1)
+    both(lda, spec, lc.generate(spec), oracle.SSP_WORST, 8, check_every=2)
+
+
+def test_empty_corpus(lda):
+    g = lda.PsLda(5, 7, 3, 2, 1, 0.1, 0.1)
+    g.load([], [], [])
+    g.clock(3)
+    assert g.z().size == 0
+    assert (g.ndk() == 0).all() and (g.nwk() == 0).all()
+    assert g.loglik() == 0.0
+    assert g.export(lda.X_VERSION_LOG).size == 6
+
+
+def test_on_a_caller_stream_with_timing(lda):
+    import torch
+
+    spec = lc.scaled(lc.CORPORA["tiny"], 1.0)
+    corpus = lc.generate(spec)
+    st = torch.cuda.Stream()
+    g, _ = both(lda, spec, corpus, oracle.ESSP, 4, stream=st, timing=True)
+    ms, n = g.kernel_time()
+    assert n == 4 and ms > 0
+
+
+def test_full_corpus_bit_exact(lda):
+    # 4.0M tokens, 20k words, K = 100, P = 64, s = 3, half the tokens per clock
+    spec = lc.CORPORA["small"]
+    both(lda, spec, lc.generate(spec), oracle.ESSP, 3, check_every=1)
+
+
+def test_full_corpus_counts_stay_tallies(lda):
+    spec = lc.CORPORA["small"]
+    corpus = lc.generate(spec)
+    say(f"lda full-size tallies: tokens={corpus.ntok}")
+    g = lda.PsLda(spec.D, spec.V, spec.K, spec.P, spec.s, spec.alpha, spec.beta, policy=lda.SSP_LAZY, B=spec.B,
+                  seed=spec.seed)
+    g.load(corpus.doc, corpus.word, corpus.z0)
+    ll0 = g.loglik()
+    g.clock(8)
+    z = g.z()
+    ndk = np.zeros((spec.D, spec.K), np.int64)
+    np.add.at(ndk, (corpus.doc, z), 1)
+    n = np.zeros((spec.V + 1, spec.K), np.int64)
+    np.add.at(n, (corpus.word, z), 1)
+    n[spec.V] = np.bincount(z, minlength=spec.K)
+    np.testing.assert_array_equal(g.ndk(), ndk)
+    np.testing.assert_array_equal(g.nwk(), n)
+    assert g.loglik() > ll0
