@@ -6,9 +6,10 @@
 //     (word-topic rows, then the topic totals); the version of clock c+1 is built in its own
 //     slot: a device copy of version c, then every worker's changes added with integer
 //     atomics as they happen (integer sums: exact and order-free);
-//   - one wavefront per worker, lanes over topics (lane l holds topics l, l+64, ...): the
-//     collapsed conditional's K weights are computed in fp64 and quantised to integers, their
-//     prefix sums come from a wave-wide scan, and the drawn topic from one ballot;
+//   - one wavefront per worker, lanes over topics (lane l holds ceil(K/64) consecutive
+//     topics): the collapsed conditional's K weights are computed in fp64 and quantised to
+//     integers, their prefix sums come from per-lane sums and one DPP wave scan, and the
+//     drawn topic from one ballot;
 //   - a worker reads its view plus its own changes of the clock: these live in a private
 //     dense delta table (words x K) whose rows carry the clock that last wrote them, so a row
 //     from an older clock reads as zero and nothing is cleared between clocks; the worker's
@@ -24,6 +25,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <type_traits>
 #include <utility>
 #include <vector>
 
@@ -70,15 +72,76 @@ struct SweepArgs {
   int32_t K, s, policy, nslots, tagc;
 };
 
-// inclusive prefix sum of a 64-bit value over the wavefront
-__device__ inline uint64_t wave_scan(uint64_t x, int lane) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint64_t y = __shfl_up(x, o, kWave);
-    if (lane >= o) x += y;
-  }
+// one DPP lane move of a 64-bit value (both halves with the same control); lanes whose
+// source lies outside their row of 16 read 0
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+  const uint32_t lo = static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x)), CTRL, 0xF, 0xF, false));
+  const uint32_t hi = static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x >> 32)), CTRL, 0xF, 0xF, false));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x)), lane));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x >> 32)), lane));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// inclusive prefix sum of a 64-bit value over the wavefront: Hillis-Steele inside each row
+// of 16 lanes (DPP row shifts 1, 2, 4, 8), then the totals of the rows below added from
+// three lane reads; *total gets the wave's sum
+__device__ __forceinline__ uint64_t wave_scan(uint64_t x, int lane, uint64_t *total) {
+  x += dpp_u64<0x111>(x);
+  x += dpp_u64<0x112>(x);
+  x += dpp_u64<0x114>(x);
+  x += dpp_u64<0x118>(x);
+  const uint64_t r0 = readlane_u64(x, 15), r1 = readlane_u64(x, 31), r2 = readlane_u64(x, 47);
+  const uint64_t r3 = readlane_u64(x, 63);
+  const int row = lane >> 4;
+  x += (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
+  *total = r0 + r1 + r2 + r3;
   return x;
 }
+
+// what one token reads before it can be sampled: its view row and own-change row of the
+// word, the row's clock tag, and its current topic
+template <int KPL>
+struct TokenRows {
+  int nw[KPL], dw[KPL];
+  int tag, z;
+};
+
+template <int KPL>
+__device__ __forceinline__ void fetch_rows(const SweepArgs &a, const int32_t *view, const int32_t *mydelta,
+                                           const int32_t *mytag, int w, int64_t q, int lane, TokenRows<KPL> &o) {
+  const int64_t base = static_cast<int64_t>(w) * a.K;
+  o.tag = mytag[w];
+  o.z = a.z[q];
+  // lanes past the last topic re-read topic K-1 (every load issued on every path, so the
+  // waits before a use count exactly); their values are masked out
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    const int k = min(lane * KPL + j, a.K - 1);
+    const bool in = lane * KPL + j < a.K;
+    const int x = view[base + k], y = mydelta[base + k];
+    o.nw[j] = in ? x : 0;
+    o.dw[j] = in ? y : 0;
+  }
+}
+
+// Lane l holds topics l*KPL .. l*KPL+KPL-1 (consecutive, so one wave scan of the lanes'
+// sums orders every topic).  Tokens run in a three-step rotation whose buffer indices are
+// fixed at compile time: at the end of step q, after its own stores, the rows of token q+2
+// are fetched and the record of token q+3 (scalar loads: the records are read-only here,
+// and their counter is separate from the vector loads').  The fetch of token q+2 sees every
+// store up to token q; token q+1's stores come after it, so a token whose word equals the
+// previous token's takes that token's updated own-change row from registers.  Fetches past
+// the last token re-read the last one and are never used, which keeps every fetch
+// unconditional (so the waits before a use count exactly the newer loads).
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(4))) i32x4 *const_rec_ptr;
 
 template <int KPL>
 __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
@@ -93,103 +156,122 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
   int32_t *next = a.ring + ((c + 1) % a.nslots) * a.slot_stride;
   int32_t *mydelta = a.delta + p * V * K;
   int32_t *mytag = a.tag + p * V;
+  const const_rec_ptr rec = (const_rec_ptr)(a.rec);
   const uint64_t rbase = a.seed ^ kDrawSalt ^ (static_cast<uint64_t>(c) << 40);
+  const int64_t qlast = q1 - 1;
 
   int vk[KPL], dk[KPL], nd[KPL];
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {
-    const int k = j * kWave + lane;
+    const int k = lane * KPL + j;
     vk[j] = k < K ? view[V * K + k] : 0;
     dk[j] = 0;
     nd[j] = 0;
   }
   int cur_doc = -1;
-  for (int64_t q = q0; q < q1; ++q) {
-    const int4 r = a.rec[q];
-    const int w = __builtin_amdgcn_readfirstlane(r.x);
-    const int d = __builtin_amdgcn_readfirstlane(r.y);
-    const int t = __builtin_amdgcn_readfirstlane(r.z);
-    const int k0 = __builtin_amdgcn_readfirstlane(a.z[q]);
-    const bool fresh = __builtin_amdgcn_readfirstlane(mytag[w]) != a.tagc;
-    const int64_t wrow = static_cast<int64_t>(w) * K;
-    int nw[KPL], dw[KPL];
+  TokenRows<KPL> rows[3];
+  i32x4 recs[3];
+  recs[0] = rec[q0];
+  recs[1] = rec[min(q0 + 1, qlast)];
+  recs[2] = rec[min(q0 + 2, qlast)];
+  fetch_rows<KPL>(a, view, mydelta, mytag, recs[0][0], q0, lane, rows[0]);
+  fetch_rows<KPL>(a, view, mydelta, mytag, recs[1][0], min(q0 + 1, qlast), lane, rows[1]);
+  bool fwd = false, fwd_valid = false;
+  int fwd_dw[KPL];
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) {
-      const int k = j * kWave + lane;
-      nw[j] = k < K ? view[wrow + k] : 0;
-      dw[j] = k < K ? mydelta[wrow + k] : 0;
-    }
+  for (int j = 0; j < KPL; ++j) fwd_dw[j] = 0;
+
+  auto step = [&](auto phase, int64_t q) {
+    constexpr int C = decltype(phase)::value, N1 = (C + 1) % 3, N2 = (C + 2) % 3;
+    const int w = recs[C][0], d = recs[C][1], t = recs[C][2];
+    const int k0 = __builtin_amdgcn_readfirstlane(rows[C].z);
+    const bool valid = fwd ? fwd_valid : __builtin_amdgcn_readfirstlane(rows[C].tag) == a.tagc;
+    int dw[KPL];
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) dw[j] = fwd ? fwd_dw[j] : (valid ? rows[C].dw[j] : 0);
     if (d != cur_doc) {
       if (cur_doc >= 0) {
 #pragma unroll
         for (int j = 0; j < KPL; ++j)
-          if (j * kWave + lane < K) a.ndk[static_cast<int64_t>(cur_doc) * K + j * kWave + lane] = nd[j];
+          if (lane * KPL + j < K) a.ndk[static_cast<int64_t>(cur_doc) * K + lane * KPL + j] = nd[j];
       }
 #pragma unroll
       for (int j = 0; j < KPL; ++j) {
-        const int k = j * kWave + lane;
-        nd[j] = k < K ? a.ndk[static_cast<int64_t>(d) * K + k] : 0;
+        const int x = a.ndk[static_cast<int64_t>(d) * K + min(lane * KPL + j, K - 1)];
+        nd[j] = lane * KPL + j < K ? x : 0;
       }
       cur_doc = d;
     }
-    if (fresh) {
-#pragma unroll
-      for (int j = 0; j < KPL; ++j) dw[j] = 0;
-    }
-    // quantised weights of the collapsed conditional and their prefix sums in topic order
-    uint64_t cum[KPL];
-    uint64_t total = 0;
+    // quantised weights of the collapsed conditional, prefix sums in topic order
+    uint64_t loc[KPL];
+    uint64_t acc = 0;
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
-      const int k = j * kWave + lane;
+      const int k = lane * KPL + j;
       uint64_t om = 0;
       if (k < K) {
         const int self = k == k0;
         const int ndx = nd[j] - self;
-        const int nwx = max(nw[j] + dw[j] - self, 0);
+        const int nwx = max(rows[C].nw[j] + dw[j] - self, 0);
         const int nkx = max(vk[j] + dk[j] - self, 0);
         const double num = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
         const double pk = num / (static_cast<double>(nkx) + a.Vbeta);
         om = static_cast<uint64_t>(floor(pk * 16777216.0));
       }
-      const uint64_t incl = wave_scan(om, lane);
-      cum[j] = incl + total;
-      total += __shfl(incl, kWave - 1, kWave);
+      acc += om;
+      loc[j] = acc;
     }
+    uint64_t total;
+    const uint64_t excl = wave_scan(acc, lane, &total) - acc;
     int k1 = k0;
     if (total != 0) {
       const uint64_t target = __umul64hi(splitmix64(rbase ^ static_cast<uint64_t>(static_cast<uint32_t>(t))), total);
+      const uint64_t m = __ballot(excl + acc > target);
+      const int L = __ffsll(static_cast<unsigned long long>(m)) - 1;  // m != 0: the last lane's sum is the total
+      int jj = KPL - 1;
 #pragma unroll
-      for (int j = 0; j < KPL; ++j) {
-        const uint64_t m = __ballot(cum[j] > target);
-        if (m != 0) {
-          k1 = j * kWave + __ffsll(static_cast<unsigned long long>(m)) - 1;
-          break;
-        }
-      }
+      for (int j = KPL - 1; j >= 0; --j)
+        if (excl + loc[j] > target) jj = j;
+      k1 = __builtin_amdgcn_readlane(lane * KPL + jj, L);
     }
-    if (k1 != k0) {
+    const bool changed = k1 != k0;
+    if (changed) {
 #pragma unroll
       for (int j = 0; j < KPL; ++j) {
-        const int k = j * kWave + lane;
+        const int k = lane * KPL + j;
         const int dl = (k == k1) - (k == k0);
         nd[j] += dl;
         dk[j] += dl;
         dw[j] += dl;
         if (k < K) {
-          if (fresh || dl != 0) mydelta[wrow + k] = dw[j];
-          if (dl != 0) atomicAdd(next + wrow + k, dl);
+          if (!valid || dl != 0) mydelta[static_cast<int64_t>(w) * K + k] = dw[j];
+          if (dl != 0) atomicAdd(next + static_cast<int64_t>(w) * K + k, dl);
         }
       }
       if (lane == 0) {
         a.z[q] = k1;
-        if (fresh) mytag[w] = a.tagc;
+        if (!valid) mytag[w] = a.tagc;
       }
     }
+    fwd = q + 1 < q1 && recs[N1][0] == w;
+    if (fwd) {
+      fwd_valid = valid || changed;
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) fwd_dw[j] = dw[j];
+    }
+    fetch_rows<KPL>(a, view, mydelta, mytag, recs[N2][0], min(q + 2, qlast), lane, rows[N2]);
+    recs[C] = rec[min(q + 3, qlast)];
+  };
+  for (int64_t q = q0; q < q1; q += 3) {
+    step(std::integral_constant<int, 0>{}, q);
+    if (q + 1 >= q1) break;
+    step(std::integral_constant<int, 1>{}, q + 1);
+    if (q + 2 >= q1) break;
+    step(std::integral_constant<int, 2>{}, q + 2);
   }
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {
-    const int k = j * kWave + lane;
+    const int k = lane * KPL + j;
     if (k < K) {
       a.ndk[static_cast<int64_t>(cur_doc) * K + k] = nd[j];
       if (dk[j] != 0) atomicAdd(next + V * K + k, dk[j]);
