@@ -9,6 +9,13 @@ clock; inputs are seeded synthetic data resident in HBM before timing starts.
 
 Prints one JSON line: rating-updates/s, the dominant kernel's roofline position (HIP
 events on the library's stream) and the CPU oracle timed on a bounded sample.
+
+``--workload lda`` measures the second workload of the paper's Section 5 instead: LDA by
+collapsed Gibbs sampling under SSP / ESSP, one step = one clock of all P workers over one
+minibatch block of the tokens, on a seeded corpus drawn from the LDA generative process
+(the "small" corpus: 20,000 documents of Poisson(200) tokens, 20,000 Zipf-shaped words,
+K=100, P=64, s=3, ESSP, half of the tokens per clock); the line reports Gibbs-sampled
+tokens/s.
 """
 from __future__ import annotations
 
@@ -28,6 +35,7 @@ if ROOT not in sys.path:
 PEAK_FP32_VECTOR_TFLOPS = 157.3   # MI355X published fp32 vector peak (packed FMA)
 PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
 POLICIES = {"lazy": 0, "worst": 1, "essp": 2, "ssp_row": 3, "essp_row": 4, "vap": 5}
+LDA_POLICIES = {"lazy": 0, "worst": 1, "essp": 2}
 STEPS = {"rowmean": 0, "sum": 1, "seq": 2}
 
 
@@ -38,7 +46,13 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3, help="untimed clocks before timing")
     ap.add_argument("--config", default="full")
     ap.add_argument("--s", type=int, default=None, help="staleness (default: 3 for the full config)")
-    ap.add_argument("--policy", default="lazy", choices=sorted(POLICIES))
+    ap.add_argument("--workload", default="mf", choices=("mf", "lda"),
+                    help="mf: matrix-factorization SGD (default); lda: collapsed Gibbs sampling for LDA")
+    ap.add_argument("--corpus", default="small", help="lda corpus")
+    ap.add_argument("--workers", type=int, default=None, help="lda: P (default: the corpus's)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="lda: oracle clocks timed for about this long")
+    ap.add_argument("--policy", default=None, choices=sorted(POLICIES),
+                    help="default: lazy (mf), essp (lda: lazy, worst or essp)")
     ap.add_argument("--step", default="rowmean", choices=sorted(STEPS),
                     help="rowmean/sum: one fixed view per worker and clock; seq: every worker applies its "
                          "ratings one by one to its own rows")
@@ -107,15 +121,135 @@ def measured_traffic(path, config, s, policy, step):
     return round(t["traffic_bytes_per_clock"])
 
 
+def lda_cpu_baseline(corpus, spec, P, s, policy, seconds):
+    """The oracle, single-threaded, running whole clocks of the same corpus for about `seconds`."""
+    import oracle
+
+    o = oracle.LdaOracle(spec.D, spec.V, spec.K, P, s, spec.alpha, spec.beta, policy, spec.B, spec.seed)
+    o.load(corpus.doc, corpus.word, corpus.z0)
+    sizes = [o.export(oracle.LDA_BLOCK_ORDER, b).size for b in range(spec.B)]
+    clocks, tokens = 0, 0
+    t0 = time.perf_counter()
+    while clocks == 0 or time.perf_counter() - t0 < seconds:
+        o.clock(1)
+        tokens += sizes[clocks % spec.B]
+        clocks += 1
+    dt = time.perf_counter() - t0
+    o.close()
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"the first {clocks} clocks of the same corpus and settings ({tokens} token draws), "
+                      f"{dt:.1f} s on {platform.processor() or platform.machine()}, 1 thread"}
+
+
+def lda_main(args):
+    import torch
+
+    from paper_1410_8043_amd import ps_lda, rocprof_summary
+    from paper_1410_8043_amd.synth import lda_corpus as lc
+
+    spec = lc.CORPORA[args.corpus]
+    P = args.workers or spec.P
+    s = args.s if args.s is not None else spec.s
+    pname = args.policy or "essp"
+    if pname not in LDA_POLICIES:
+        raise SystemExit(f"--policy {pname} is not an LDA policy (lazy, worst, essp)")
+    policy = LDA_POLICIES[pname]
+    torch.cuda.set_device(0)
+    t_gen = time.perf_counter()
+    corpus = lc.generate(spec)
+    print(f"[bench] generated lda {args.corpus}: {corpus.ntok} tokens in {time.perf_counter() - t_gen:.1f} s",
+          file=sys.stderr, flush=True)
+    g = ps_lda.PsLda(spec.D, spec.V, spec.K, P, s, spec.alpha, spec.beta, policy=policy, B=spec.B, seed=spec.seed,
+                     timing=not args.no_timing, stream=torch.cuda.current_stream())
+    g.load(corpus.doc, corpus.word, corpus.z0)
+    # tokens and (worker, document) runs of each block: a run reads and writes its doc-topic row
+    tokens_b, runs_b = [], []
+    for b in range(spec.B):
+        d = corpus.doc[g.export(ps_lda.X_BLOCK_ORDER, b)]
+        tokens_b.append(d.size)
+        runs_b.append(int(d.size > 0) + int(np.count_nonzero(d[1:] != d[:-1])))
+    ll0 = g.loglik()
+    if args.copy_calibration_bytes > 0:
+        src = torch.ones(args.copy_calibration_bytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.mul(src, 2.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+    g.clock(args.warmup)
+    torch.cuda.synchronize()
+    base = g.kernel_time() if not args.no_timing else None
+    t0 = time.perf_counter()
+    g.clock(args.steps)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    print(f"[bench] {args.steps} clocks in {dt * 1e3:.2f} ms", file=sys.stderr, flush=True)
+    ll = g.loglik()
+    timed = [(args.warmup + i) % spec.B for i in range(args.steps)]
+    tokens = sum(tokens_b[b] for b in timed)
+    K = spec.K
+    roof, extra = None, {}
+    if not args.no_timing:
+        ms, n = g.kernel_time()
+        launch_ms = (ms - base[0]) / (n - base[1])
+        # per token: its 16-byte record, topic and row tag (4 + 4), the word's view row and own-
+        # change row (2 x 4K); per (worker, document) run: the doc-topic row read and written
+        bytes_launch = sum(tokens_b[b] * (8.0 * K + 24) + runs_b[b] * 8.0 * K for b in timed) / len(timed)
+        achieved = bytes_launch / (launch_ms * 1e-3) / 1e9
+        traffic = None
+        try:
+            with open(os.path.join(ROOT, "profiles", f"lda_{args.corpus}_traffic.json")) as f:
+                t = json.load(f)
+            src = os.path.join(ROOT, "paper_1410_8043_amd", "csrc", "ps_lda.hip")
+            if (t.get("kernel_source_sha256") == rocprof_summary.kernel_source_sha256(src) and
+                    t.get("workload") == {"config": args.corpus, "s": s, "policy": pname, "step": "lda"} and
+                    P == spec.P):
+                traffic = round(t["traffic_bytes_per_clock"])
+        except (OSError, ValueError):
+            pass
+        roof = {"kernel": "k_lda_sweep (one launch per clock)", "bound": "hbm", "achieved": round(achieved, 2),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 5), "traffic": traffic}
+        extra = {"sweep_ms": round(launch_ms, 4), "token_latency_us": round(launch_ms * 1e3 * P / (tokens / len(timed)), 4)}
+    g.close()
+    cpu = None
+    if args.cpu_sample > 0 and args.cpu_seconds > 0:
+        print("[bench] timing the oracle", file=sys.stderr, flush=True)
+        cpu = lda_cpu_baseline(corpus, spec, P, s, policy, args.cpu_seconds)
+    line = {
+        "metric": f"Gibbs-sampled tokens/sec, LDA K={K}, {corpus.ntok / 1e6:.1f}M tokens (1 GPU)",
+        "value": round(tokens / dt, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dt / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic (seeded LDA generative process, Zipf-shaped topics)",
+        "config": {"workload": f"lda {args.corpus}: {spec.D} documents, {spec.V} words, {corpus.ntok} tokens, K={K}, "
+                               f"P={P}, s={s}, policy={pname}, B={spec.B}, alpha={spec.alpha}, beta={spec.beta}",
+                   "global_batch": int(tokens / len(timed)), "parallelism": "1 GPU, P logical workers",
+                   "loglik_before": ll0, "loglik_after": ll, **extra},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
-    if args.traffic_file is None:
-        name = "seq_full_traffic.json" if args.step == "seq" else "sweep_full_traffic.json"
-        args.traffic_file = os.path.join(ROOT, "profiles", name)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the multi-GPU path is a design, not part of this build)", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "lda":
+        return lda_main(args)
+    if args.policy is None:
+        args.policy = "lazy"
+    if args.traffic_file is None:
+        name = "seq_full_traffic.json" if args.step == "seq" else "sweep_full_traffic.json"
+        args.traffic_file = os.path.join(ROOT, "profiles", name)
     import torch
 
     from paper_1410_8043_amd import ps_mf, synth

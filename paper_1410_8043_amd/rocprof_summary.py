@@ -1,4 +1,4 @@
-"""Summaries of rocprofv3 result databases for the ps_mf kernels.
+"""Summaries of rocprofv3 result databases for the ps_mf and ps_lda kernels.
 
     python -m paper_1410_8043_amd.rocprof_summary stats <dir>
         per-kernel calls, total and average duration from a --kernel-trace --stats run,
@@ -7,7 +7,8 @@
     python -m paper_1410_8043_amd.rocprof_summary counters <dir> [<dir> ...]
         per-kernel counter values (sum over a dispatch's dimensions) of --pmc runs;
     python -m paper_1410_8043_amd.rocprof_summary traffic --fetch <dir> --write <dir> \
-            --copy-bytes N --out profiles/<name>.json
+            --copy-bytes N --out profiles/<name>.json [--kernels k_lda_sweep --step lda \
+            --source paper_1410_8043_amd/csrc/ps_lda.hip]
         HBM bytes per clock of the sweep kernels from one FETCH_SIZE and one WRITE_SIZE run,
         scaled by what the same counters read for a plain copy kernel (torch's elementwise
         y = x * 2 over N bytes), written as JSON next to the sha256 of the kernel
@@ -32,8 +33,8 @@ KERNEL_SOURCE = os.path.join(_HERE, "csrc", "ps_mf.hip")
 SWEEP_KERNELS = ("k_dense", "k_cells", "k_units")  # the concurrent kernels of one clock's sweep
 
 
-def kernel_source_sha256() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
+def kernel_source_sha256(path: str = KERNEL_SOURCE) -> str:
+    with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()
 
 
@@ -119,7 +120,8 @@ def _sweep_values(cnt, counter: str, kernels=SWEEP_KERNELS):
     return out
 
 
-def traffic(fetch_dir: str, write_dir: str, copy_bytes: int, kernels=SWEEP_KERNELS, per_clock: int = 1):
+def traffic(fetch_dir: str, write_dir: str, copy_bytes: int, kernels=SWEEP_KERNELS, per_clock: int = 1,
+            source: str = KERNEL_SOURCE):
     """HBM bytes per clock of the sweep (its kernels of one clock summed), calibrated.  Each
     distinct sweep kernel runs per_clock times a clock (the sequential step: once per
     sub-epoch)."""
@@ -143,7 +145,8 @@ def traffic(fetch_dir: str, write_dir: str, copy_bytes: int, kernels=SWEEP_KERNE
                              "fetch_scale": fetch_scale, "write_scale": write_scale},
         "per_launch_fetch_kib": {k: v for k, v in sf},
         "per_launch_write_kib": {k: v for k, v in sw},
-        "kernel_source_sha256": kernel_source_sha256(),
+        "kernel_source": os.path.basename(source),
+        "kernel_source_sha256": kernel_source_sha256(source),
     }
 
 
@@ -166,6 +169,7 @@ def main(argv=None):
     c.add_argument("--step", default="rowmean")
     c.add_argument("--kernels", default=",".join(SWEEP_KERNELS), help="comma-separated kernel name prefixes")
     c.add_argument("--per-clock", type=int, default=1, help="dispatches of each kernel per clock")
+    c.add_argument("--source", default=KERNEL_SOURCE, help="the kernels' source file (its sha256 is recorded)")
     args = ap.parse_args(argv)
     if args.cmd == "stats":
         for name, calls, tot, avg, pct in stats(args.dir):
@@ -181,7 +185,8 @@ def main(argv=None):
             for (k, cname), vals in sorted(counters(d).items()):
                 print(f"{short_name(k)[:48]:48s} {cname:18s} " + " ".join(f"{v:.5g}" for v in vals[:8]))
     else:
-        t = traffic(args.fetch, args.write, args.copy_bytes, tuple(args.kernels.split(",")), args.per_clock)
+        t = traffic(args.fetch, args.write, args.copy_bytes, tuple(args.kernels.split(",")), args.per_clock,
+                    args.source)
         t["command"] = args.command
         t["workload"] = {"config": args.config, "s": args.s, "policy": args.policy}
         if args.step != "rowmean":
