@@ -41,6 +41,10 @@ CORPORA = {
     # workers sweep in well under a second per clock
     "small": CorpusSpec("small", D=20_000, V=20_000, K=100, mean_len=200, P=64, s=3, alpha=0.1, beta=0.01, B=2,
                         clocks=10, seed=BASE_SEED + 102),
+    # the paper's topic-model workload shape: 100M tokens, 100k words, K = 100, half of the
+    # tokens per clock, 512 workers (its 8 nodes x 64 cores)
+    "nyt": CorpusSpec("nyt", D=300_000, V=100_000, K=100, mean_len=333, P=512, s=3, alpha=0.1, beta=0.01, B=2,
+                      clocks=10, seed=BASE_SEED + 103),
 }
 
 

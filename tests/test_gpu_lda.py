@@ -136,3 +136,31 @@ def test_full_corpus_counts_stay_tallies(lda):
     np.testing.assert_array_equal(g.ndk(), ndk)
     np.testing.assert_array_equal(g.nwk(), n)
     assert g.loglik() > ll0
+
+
+def test_paper_scale_corpus_counts_stay_tallies(lda):
+    # the paper's topic-model shape as bench.py --workload lda --corpus nyt runs it: 100M
+    # tokens, 100k words, K = 100, P = 512, half of the tokens per clock
+    spec = lc.CORPORA["nyt"]
+    say("lda paper-scale corpus: generating")
+    corpus = lc.generate(spec)
+    say(f"lda paper-scale corpus: {corpus.ntok} tokens, loading")
+    g = lda.PsLda(spec.D, spec.V, spec.K, spec.P, spec.s, spec.alpha, spec.beta, policy=lda.ESSP, B=spec.B,
+                  seed=spec.seed)
+    g.load(corpus.doc, corpus.word, corpus.z0)
+    ll0 = g.loglik()
+    say("lda paper-scale corpus: 2 clocks")
+    g.clock(2)
+    z = g.z()
+    K = spec.K
+    ndk = np.bincount(corpus.doc.astype(np.int64) * K + z, minlength=spec.D * K).reshape(spec.D, K)
+    n = np.bincount(corpus.word.astype(np.int64) * K + z, minlength=spec.V * K).reshape(spec.V, K)
+    np.testing.assert_array_equal(g.ndk(), ndk)
+    nwk = g.nwk()
+    np.testing.assert_array_equal(nwk[:spec.V], n)
+    np.testing.assert_array_equal(nwk[spec.V], np.bincount(z, minlength=K))
+    moved = float((z != corpus.z0).mean())
+    say(f"lda paper-scale corpus: {moved:.3f} of the tokens moved")
+    assert 0.3 < moved < 1.0
+    assert g.loglik() > ll0
+    g.close()
