@@ -131,20 +131,35 @@ __device__ __forceinline__ void fetch_rows(const SweepArgs &a, const int32_t *vi
   }
 }
 
+// step(integral_constant<int, I>, q + I) for I = I0 .. N-1 while q + I < q1
+template <int I0, int N, class F>
+__device__ __forceinline__ void seq_steps(F &f, int64_t q, int64_t q1, bool &more) {
+  if (q + I0 >= q1) {
+    more = false;
+    return;
+  }
+  f(std::integral_constant<int, I0>{}, q + I0);
+  if constexpr (I0 + 1 < N) seq_steps<I0 + 1, N>(f, q, q1, more);
+}
+
 // Lane l holds topics l*KPL .. l*KPL+KPL-1 (consecutive, so one wave scan of the lanes'
-// sums orders every topic).  Tokens run in a three-step rotation whose buffer indices are
-// fixed at compile time: at the end of step q, after its own stores, the rows of token q+2
-// are fetched and the record of token q+3 (scalar loads: the records are read-only here,
-// and their counter is separate from the vector loads').  The fetch of token q+2 sees every
-// store up to token q; token q+1's stores come after it, so a token whose word equals the
-// previous token's takes that token's updated own-change row from registers.  Fetches past
-// the last token re-read the last one and are never used, which keeps every fetch
+// sums orders every topic).  Tokens run in a rotation of kDist+1 steps whose buffer indices
+// are fixed at compile time: at the end of step q, after its own stores, the rows of token
+// q+kDist are fetched and the record of token q+kDist+1 (scalar loads: the records are
+// read-only here, and their counter is separate from the vector loads').  The fetch of token
+// t sees every store up to token t-kDist; the stores of the kDist-1 tokens after that come
+// later, so the updated own-change rows of those tokens stay in registers, and a token whose
+// word matches one of them takes the latest such row instead of its fetched one.  Fetches
+// past the last token re-read the last one and are never used, which keeps every fetch
 // unconditional (so the waits before a use count exactly the newer loads).
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(4))) i32x4 *const_rec_ptr;
+constexpr int kDist = 3;
 
 template <int KPL>
 __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
+  constexpr int R = kDist + 1;  // ring entries
+  constexpr int F = kDist - 1;  // forwarded rows
   const int lane = threadIdx.x;
   const int64_t p = blockIdx.x;
   const int64_t q0 = a.wbeg[p], q1 = a.wbeg[p + 1];
@@ -169,26 +184,45 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     nd[j] = 0;
   }
   int cur_doc = -1;
-  TokenRows<KPL> rows[3];
-  i32x4 recs[3];
-  recs[0] = rec[q0];
-  recs[1] = rec[min(q0 + 1, qlast)];
-  recs[2] = rec[min(q0 + 2, qlast)];
-  fetch_rows<KPL>(a, view, mydelta, mytag, recs[0][0], q0, lane, rows[0]);
-  fetch_rows<KPL>(a, view, mydelta, mytag, recs[1][0], min(q0 + 1, qlast), lane, rows[1]);
-  bool fwd = false, fwd_valid = false;
-  int fwd_dw[KPL];
+  TokenRows<KPL> rows[R];
+  i32x4 recs[R];
 #pragma unroll
-  for (int j = 0; j < KPL; ++j) fwd_dw[j] = 0;
+  for (int i = 0; i < R; ++i) recs[i] = rec[min(q0 + i, qlast)];
+#pragma unroll
+  for (int i = 0; i < kDist; ++i) fetch_rows<KPL>(a, view, mydelta, mytag, recs[i][0], min(q0 + i, qlast), lane, rows[i]);
+  // the last F tokens' words (-1: none), row validity and updated own-change rows, latest first
+  int fw[F > 0 ? F : 1];
+  bool fvalid[F > 0 ? F : 1];
+  int fdw[F > 0 ? F : 1][KPL];
+#pragma unroll
+  for (int i = 0; i < F; ++i) {
+    fw[i] = -1;
+    fvalid[i] = false;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) fdw[i][j] = 0;
+  }
 
   auto step = [&](auto phase, int64_t q) {
-    constexpr int C = decltype(phase)::value, N1 = (C + 1) % 3, N2 = (C + 2) % 3;
+    constexpr int C = decltype(phase)::value;
     const int w = recs[C][0], d = recs[C][1], t = recs[C][2];
     const int k0 = __builtin_amdgcn_readfirstlane(rows[C].z);
-    const bool valid = fwd ? fwd_valid : __builtin_amdgcn_readfirstlane(rows[C].tag) == a.tagc;
+    bool valid = __builtin_amdgcn_readfirstlane(rows[C].tag) == a.tagc;
     int dw[KPL];
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) dw[j] = fwd ? fwd_dw[j] : (valid ? rows[C].dw[j] : 0);
+    for (int j = 0; j < KPL; ++j) dw[j] = rows[C].dw[j];
+    // the latest of the last F tokens with this word, if any, overrides the fetched row
+#pragma unroll
+    for (int i = F - 1; i >= 0; --i) {
+      if (fw[i] == w) {
+        valid = fvalid[i];
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) dw[j] = fdw[i][j];
+      }
+    }
+    if (!valid) {
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) dw[j] = 0;
+    }
     if (d != cur_doc) {
       if (cur_doc >= 0) {
 #pragma unroll
@@ -253,21 +287,28 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
         if (!valid) mytag[w] = a.tagc;
       }
     }
-    fwd = q + 1 < q1 && recs[N1][0] == w;
-    if (fwd) {
-      fwd_valid = valid || changed;
+    // this token becomes the latest forwarded row
 #pragma unroll
-      for (int j = 0; j < KPL; ++j) fwd_dw[j] = dw[j];
+    for (int i = F - 1; i > 0; --i) {
+      fw[i] = fw[i - 1];
+      fvalid[i] = fvalid[i - 1];
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) fdw[i][j] = fdw[i - 1][j];
     }
-    fetch_rows<KPL>(a, view, mydelta, mytag, recs[N2][0], min(q + 2, qlast), lane, rows[N2]);
-    recs[C] = rec[min(q + 3, qlast)];
+    if constexpr (F > 0) {
+      fw[0] = w;
+      fvalid[0] = valid || changed;
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) fdw[0][j] = dw[j];
+    }
+    constexpr int NF = (C + kDist) % R;
+    fetch_rows<KPL>(a, view, mydelta, mytag, recs[NF][0], min(q + kDist, qlast), lane, rows[NF]);
+    recs[C] = rec[min(q + R, qlast)];
   };
-  for (int64_t q = q0; q < q1; q += 3) {
-    step(std::integral_constant<int, 0>{}, q);
-    if (q + 1 >= q1) break;
-    step(std::integral_constant<int, 1>{}, q + 1);
-    if (q + 2 >= q1) break;
-    step(std::integral_constant<int, 2>{}, q + 2);
+  for (int64_t q = q0; q < q1; q += R) {
+    bool more = true;
+    seq_steps<0, R>(step, q, q1, more);
+    if (!more) break;
   }
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {

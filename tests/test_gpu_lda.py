@@ -112,10 +112,11 @@ def test_on_a_caller_stream_with_timing(lda):
     assert n == 4 and ms > 0
 
 
-def test_full_corpus_bit_exact(lda):
+@pytest.mark.parametrize("policy", POLICIES)
+def test_full_corpus_bit_exact(lda, policy):
     # 4.0M tokens, 20k words, K = 100, P = 64, s = 3, half the tokens per clock
     spec = lc.CORPORA["small"]
-    both(lda, spec, lc.generate(spec), oracle.ESSP, 3, check_every=1)
+    both(lda, spec, lc.generate(spec), policy, 3 if policy == oracle.ESSP else 5, check_every=1)
 
 
 def test_full_corpus_counts_stay_tallies(lda):
