@@ -34,6 +34,7 @@
  *
  * Build: compiled with ps_mf_oracle.c into libps_mf_oracle.so (gcc -O2, no fast math).
  */
+#define _GNU_SOURCE /* qsort_r */
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -106,10 +107,9 @@ int lda_create(int64_t D, int64_t V, int32_t K, int32_t P, int32_t s, double alp
   return LO_OK;
 }
 
-static const lda_t *g_lda;
-static int cmp_token(const void *a, const void *b) {
+static int cmp_token(const void *a, const void *b, void *arg) {
   const int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
-  const lda_t *o = g_lda;
+  const lda_t *o = (const lda_t *)arg;
   const int64_t px = o->doc[x] % o->P, py = o->doc[y] % o->P;
   if (px != py) return px < py ? -1 : 1;
   if (o->doc[x] != o->doc[y]) return o->doc[x] < o->doc[y] ? -1 : 1;
@@ -155,9 +155,8 @@ int lda_load(lda_t *o, const int32_t *doc, const int32_t *word, const int32_t *z
   }
   for (int32_t b = 0; b < o->B; ++b) o->bstart[b + 1] += o->bstart[b];
   for (int64_t t = 0; t < n; ++t) o->order[o->bstart[blk[t]] + fill[blk[t]]++] = t;
-  g_lda = o;
   for (int32_t b = 0; b < o->B; ++b)
-    qsort(o->order + o->bstart[b], (size_t)(o->bstart[b + 1] - o->bstart[b]), sizeof(int64_t), cmp_token);
+    qsort_r(o->order + o->bstart[b], (size_t)(o->bstart[b + 1] - o->bstart[b]), sizeof(int64_t), cmp_token, o);
   free(blk); free(fill);
   o->loaded = 1;
   return LO_OK;
