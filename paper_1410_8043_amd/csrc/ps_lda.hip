@@ -3,9 +3,9 @@
 //
 // Design:
 //   - the shared state is a ring of s+2 committed versions of the (V+1) x K int32 counts
-//     (word-topic rows, then the topic totals); the version of clock c+1 is built in its own
-//     slot: a device copy of version c, then every worker's changes added with integer
-//     atomics as they happen (integer sums: exact and order-free);
+//     (word-topic rows, then the topic totals); after the sampling kernel, a commit kernel
+//     writes the version of clock c+1 into its own slot: version c plus every worker's
+//     changes of the clock (integer sums: exact and order-free);
 //   - one wavefront per worker, lanes over topics (lane l holds ceil(K/64) consecutive
 //     topics): the collapsed conditional's K weights are computed in fp64 and quantised to
 //     integers, their prefix sums come from per-lane sums and one DPP wave scan, and the
@@ -63,6 +63,7 @@ struct SweepArgs {
   int32_t *ring;        // nslots x (V+1) x K
   int32_t *delta;       // P x V x K, rows valid where tag == tagc
   int32_t *tag;         // P x V
+  int32_t *tot;         // P x K: each worker's topic-total changes of the clock
   const int64_t *wbeg;  // P+1 block positions of this clock's block
   int64_t slot_stride;  // (V+1) * K
   int64_t V;
@@ -163,12 +164,14 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
   const int lane = threadIdx.x;
   const int64_t p = blockIdx.x;
   const int64_t q0 = a.wbeg[p], q1 = a.wbeg[p + 1];
-  if (q0 >= q1) return;
   const int K = a.K;
+  if (q0 >= q1) {  // no tokens this clock: no topic-total changes
+    for (int k = lane; k < K; k += kWave) a.tot[p * K + k] = 0;
+    return;
+  }
   const int64_t V = a.V, c = a.c;
   const int64_t v = view_of(a.policy, a.s, p, c);
   const int32_t *view = a.ring + (v % a.nslots) * a.slot_stride;
-  int32_t *next = a.ring + ((c + 1) % a.nslots) * a.slot_stride;
   int32_t *mydelta = a.delta + p * V * K;
   int32_t *mytag = a.tag + p * V;
   const const_rec_ptr rec = (const_rec_ptr)(a.rec);
@@ -279,7 +282,6 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
         dw[j] += dl;
         if (k < K) {
           if (!valid || dl != 0) mydelta[static_cast<int64_t>(w) * K + k] = dw[j];
-          if (dl != 0) atomicAdd(next + static_cast<int64_t>(w) * K + k, dl);
         }
       }
       if (lane == 0) {
@@ -315,8 +317,57 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     const int k = lane * KPL + j;
     if (k < K) {
       a.ndk[static_cast<int64_t>(cur_doc) * K + k] = nd[j];
-      if (dk[j] != 0) atomicAdd(next + V * K + k, dk[j]);
+      a.tot[p * K + k] = dk[j];
     }
+  }
+}
+
+// version c+1 = version c + every worker's changes of clock c.  One wavefront per word row
+// (lanes over topics as in the sweep): the workers' row tags are read 64 at a time, and the
+// own-change rows of the workers that wrote this word in this clock are added; the last
+// row (topic totals) adds the workers' topic-total changes.  Every sum is integer, so the
+// result does not depend on the order.
+template <int KPL>
+__global__ __launch_bounds__(kWave) void k_lda_commit(const int32_t *cur, int32_t *next, const int32_t *delta,
+                                                      const int32_t *tag, const int32_t *tot, int64_t V, int32_t K,
+                                                      int32_t P, int32_t tagc) {
+  const int lane = threadIdx.x;
+  const int64_t w = blockIdx.x;
+  int acc[KPL];
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    const int k = lane * KPL + j;
+    acc[j] = k < K ? cur[w * K + k] : 0;
+  }
+  if (w < V) {
+    for (int p0 = 0; p0 < P; p0 += kWave) {
+      const int pl = p0 + lane;
+      const bool hit = pl < P && tag[static_cast<int64_t>(pl) * V + w] == tagc;
+      uint64_t m = __ballot(hit);
+      while (m != 0) {
+        const int pp = p0 + __ffsll(static_cast<unsigned long long>(m)) - 1;
+        m &= m - 1;
+        const int32_t *row = delta + (static_cast<int64_t>(pp) * V + w) * K;
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+          const int k = lane * KPL + j;
+          if (k < K) acc[j] += row[k];
+        }
+      }
+    }
+  } else {
+    for (int pp = 0; pp < P; ++pp) {
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) {
+        const int k = lane * KPL + j;
+        if (k < K) acc[j] += tot[static_cast<int64_t>(pp) * K + k];
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    const int k = lane * KPL + j;
+    if (k < K) next[w * K + k] = acc[j];
   }
 }
 
@@ -389,7 +440,7 @@ struct ps_lda {
   std::vector<int64_t> order;  // load index at every block position
   std::vector<int64_t> vlog;
   int4 *rec = nullptr;
-  int32_t *z = nullptr, *ndk = nullptr, *ring = nullptr, *delta = nullptr, *tag = nullptr;
+  int32_t *z = nullptr, *ndk = nullptr, *ring = nullptr, *delta = nullptr, *tag = nullptr, *tot = nullptr;
   int64_t *wbeg_dev = nullptr;
   double *partial = nullptr;
   struct Ev {
@@ -462,10 +513,16 @@ void launch_sweep(const SweepArgs &a, int P, hipStream_t st) {
   hipLaunchKernelGGL(k_lda_sweep<KPL>, dim3(P), dim3(kWave), 0, st, a);
 }
 
+template <int KPL>
+void launch_commit(const ps_lda_t *h, const int32_t *cur, int32_t *nxt, int32_t tagc) {
+  hipLaunchKernelGGL(k_lda_commit<KPL>, dim3(static_cast<unsigned>(h->V + 1)), dim3(kWave), 0, h->stream, cur, nxt,
+                     h->delta, h->tag, h->tot, h->V, h->K, h->P, tagc);
+}
+
 int sweep(ps_lda_t *h) {
   const int64_t c = h->clock, b = c % h->B, ns = h->s + 2, stride = slot_stride(h);
-  int32_t *cur = h->ring + (c % ns) * stride, *nxt = h->ring + ((c + 1) % ns) * stride;
-  LDA_TRY(h, hipMemcpyAsync(nxt, cur, sizeof(int32_t) * stride, hipMemcpyDeviceToDevice, h->stream));
+  const int32_t *cur = h->ring + (c % ns) * stride;
+  int32_t *nxt = h->ring + ((c + 1) % ns) * stride;
   SweepArgs a;
   a.rec = h->rec;
   a.z = h->z;
@@ -473,6 +530,7 @@ int sweep(ps_lda_t *h) {
   a.ring = h->ring;
   a.delta = h->delta;
   a.tag = h->tag;
+  a.tot = h->tot;
   a.wbeg = h->wbeg_dev + b * (h->P + 1);
   a.slot_stride = stride;
   a.V = h->V;
@@ -507,6 +565,17 @@ int sweep(ps_lda_t *h) {
     LDA_TRY(h, hipEventRecord(e1, h->stream));
     h->events.push_back({e0, e1});
   }
+  switch ((h->K + kWave - 1) / kWave) {
+    case 1: launch_commit<1>(h, cur, nxt, a.tagc); break;
+    case 2: launch_commit<2>(h, cur, nxt, a.tagc); break;
+    case 3: launch_commit<3>(h, cur, nxt, a.tagc); break;
+    case 4: launch_commit<4>(h, cur, nxt, a.tagc); break;
+    case 5: launch_commit<5>(h, cur, nxt, a.tagc); break;
+    case 6: launch_commit<6>(h, cur, nxt, a.tagc); break;
+    case 7: launch_commit<7>(h, cur, nxt, a.tagc); break;
+    default: launch_commit<8>(h, cur, nxt, a.tagc); break;
+  }
+  LDA_TRY(h, hipGetLastError());
   for (int64_t p = 0; p < h->P; ++p) h->vlog.push_back(view_of(h->policy, h->s, p, c));
   h->clock = c + 1;
   return PS_LDA_OK;
@@ -629,6 +698,7 @@ int ps_lda_load(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int3
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->ring), sizeof(int32_t) * stride * ns))) return rc;
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->delta), sizeof(int32_t) * P * V * K))) return rc;
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->tag), sizeof(int32_t) * P * V))) return rc;
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->tot), sizeof(int32_t) * P * K))) return rc;
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->wbeg_dev), sizeof(int64_t) * h->wbeg.size()))) return rc;
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->partial), sizeof(double) * (kLoglikBlocks + 1)))) return rc;
   if (n > 0) {
