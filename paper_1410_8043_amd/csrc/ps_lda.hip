@@ -24,6 +24,7 @@
 #include <cstdio>
 #include <cstring>
 #include <new>
+#include <stdexcept>
 #include <string>
 #include <type_traits>
 #include <utility>
@@ -645,8 +646,23 @@ int ps_lda_set_stream(ps_lda_t *h, void *hip_stream) {
   return PS_LDA_OK;
 }
 
+namespace {
+int load_tokens(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int32_t *z0, int64_t n);
+}
+
 int ps_lda_load(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int32_t *z0, int64_t n) {
   if (!h) return PS_LDA_EINVAL;
+  try {
+    return load_tokens(h, doc, word, z0, n);
+  } catch (const std::bad_alloc &) {
+    return lda_fail(h, PS_LDA_ENOMEM, "host memory for the token layout of %lld tokens", (long long)n);
+  }
+}
+
+}  // extern "C"
+
+namespace {
+int load_tokens(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int32_t *z0, int64_t n) {
   if (h->loaded) return lda_fail(h, PS_LDA_ESTATE, "tokens already loaded");
   if (n < 0 || n > 0x7fffffff) return lda_fail(h, PS_LDA_EINVAL, "token count %lld out of range", (long long)n);
   if (n > 0 && (!doc || !word || !z0)) return lda_fail(h, PS_LDA_EINVAL, "null token array");
@@ -714,6 +730,9 @@ int ps_lda_load(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int3
   h->loaded = true;
   return PS_LDA_OK;
 }
+}  // namespace
+
+extern "C" {
 
 int ps_lda_clock(ps_lda_t *h, int32_t n) {
   if (!h || n < 0) return PS_LDA_EINVAL;
@@ -749,8 +768,27 @@ int ps_lda_get_clock(ps_lda_t *h, int64_t *clock) {
   return PS_LDA_OK;
 }
 
+}  // extern "C"
+
+namespace {
+int export_state(ps_lda_t *h, int32_t kind, int32_t block, void *buf, int64_t cap, int64_t *len);
+}
+
+extern "C" {
+
 int ps_lda_export(ps_lda_t *h, int32_t kind, int32_t block, void *buf, int64_t cap, int64_t *len) {
   if (!h || !len) return PS_LDA_EINVAL;
+  try {
+    return export_state(h, kind, block, buf, cap, len);
+  } catch (const std::bad_alloc &) {
+    return lda_fail(h, PS_LDA_ENOMEM, "host staging memory for export %d", kind);
+  }
+}
+
+}  // extern "C"
+
+namespace {
+int export_state(ps_lda_t *h, int32_t kind, int32_t block, void *buf, int64_t cap, int64_t *len) {
   if (!h->loaded && kind != PS_LDA_X_VERSION_LOG) return lda_fail(h, PS_LDA_ESTATE, "nothing loaded");
   const bool device_kind = kind == PS_LDA_X_Z || kind == PS_LDA_X_NDK || kind == PS_LDA_X_NWK;
   if (device_kind && h->host_only) return lda_fail(h, PS_LDA_ESTATE, "host-only handle: no device state");
@@ -795,6 +833,10 @@ int ps_lda_export(ps_lda_t *h, int32_t kind, int32_t block, void *buf, int64_t c
   }
   return PS_LDA_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int ps_lda_kernel_time(ps_lda_t *h, double *ms, int64_t *count) {
   if (!h || !ms || !count) return PS_LDA_EINVAL;

@@ -2183,8 +2183,27 @@ int ps_mf_set_stream(ps_mf_t *h, void *hip_stream) {
   return PS_MF_OK;
 }
 
+}  // extern "C"
+
+namespace {
+int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const float *value, int64_t n);
+}
+
+extern "C" {
+
 int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const float *value, int64_t n) {
   if (!h) return PS_MF_EINVAL;
+  try {
+    return load_ratings(h, user, item, value, n);
+  } catch (const std::bad_alloc &) {
+    return fail(h, PS_MF_ENOMEM, "host memory for the layout of %lld ratings", (long long)n);
+  }
+}
+
+}  // extern "C"
+
+namespace {
+int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const float *value, int64_t n) {
   if (h->loaded) return fail(h, PS_MF_ESTATE, "ratings are already loaded");
   if (n < 0 || (n > 0 && (!user || !item || !value))) return fail(h, PS_MF_EINVAL, "bad rating arrays");
   if (n > 0x7fffffffLL) return fail(h, PS_MF_EINVAL, "at most 2^31-1 ratings");
@@ -2354,6 +2373,10 @@ int ps_mf_load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, con
   }
   return PS_MF_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int ps_mf_set_factors(ps_mf_t *h, const float *L, const float *R) {
   if (!h || !L || !R) return PS_MF_EINVAL;
