@@ -119,6 +119,12 @@ def test_full_corpus_bit_exact(lda, policy):
     both(lda, spec, lc.generate(spec), policy, 3 if policy == oracle.ESSP else 5, check_every=1)
 
 
+def test_full_corpus_bit_exact_256_workers(lda):
+    # the same corpus in the launch shape bench.py --workload lda --workers 256 times
+    spec = lc.scaled(lc.CORPORA["small"], 1.0, P=256)
+    both(lda, spec, lc.generate(spec), oracle.ESSP, 2, check_every=1)
+
+
 def test_full_corpus_counts_stay_tallies(lda):
     spec = lc.CORPORA["small"]
     corpus = lc.generate(spec)
