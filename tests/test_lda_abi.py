@@ -77,3 +77,29 @@ def test_empty_load_has_empty_blocks():
     h = ps_lda.PsLda(3, 3, 2, 2, 1, 0.1, 0.1, B=3, host_only=True)
     h.load([], [], [])
     assert all(h.export(ps_lda.X_BLOCK_ORDER, b).size == 0 for b in range(3))
+
+
+def test_export_and_option_errors():
+    h = ps_lda.PsLda(4, 4, 2, 2, 1, 0.1, 0.1, B=2, host_only=True)
+    h.load([0, 1, 2, 3], [0, 1, 2, 3], [0, 1, 0, 1])
+    with pytest.raises(ps_lda.PsLdaError) as e:  # an option after the load
+        ps_lda._check(h._h, "ps_lda_set_option", ps_lda._lib.ps_lda_set_option(h._h, ps_lda.OPT_POLICY, 0))
+    assert e.value.code == ps_lda.ESTATE
+    n = ctypes.c_int64()
+    assert ps_lda._lib.ps_lda_export(h._h, 9, 0, None, 0, ctypes.byref(n)) == ps_lda.EINVAL  # unknown kind
+    assert b"unknown export" in ps_lda._lib.ps_lda_last_error(h._h)
+    assert ps_lda._lib.ps_lda_export(h._h, ps_lda.X_BLOCK_ORDER, 0, None, 0, ctypes.byref(n)) == ps_lda.OK
+    if n.value > 0:  # a buffer one element short
+        buf = np.empty(n.value, np.int64)
+        assert ps_lda._lib.ps_lda_export(h._h, ps_lda.X_BLOCK_ORDER, 0, buf.ctypes.data, n.value - 1,
+                                         ctypes.byref(n)) == ps_lda.EINVAL
+    assert h.export(ps_lda.X_VERSION_LOG).size == 0  # no clock run
+    assert h.get_clock() == 0
+
+
+def test_null_handle_calls_are_rejected():
+    n = ctypes.c_int64()
+    assert ps_lda._lib.ps_lda_clock(None, 1) == ps_lda.EINVAL
+    assert ps_lda._lib.ps_lda_export(None, 0, 0, None, 0, ctypes.byref(n)) == ps_lda.EINVAL
+    assert ps_lda._lib.ps_lda_last_error(None) == b"null handle"
+    ps_lda._lib.ps_lda_destroy(None)  # NULL-safe
