@@ -83,7 +83,9 @@ int ps_lda_set_option(ps_lda_t *h, int32_t key, int64_t value);
 /* hip_stream: a hipStream_t of the current device, or NULL for a stream the handle creates. */
 int ps_lda_set_stream(ps_lda_t *h, void *hip_stream);
 /* n tokens as host arrays: document, word, initial topic (0 <= doc < D, word < V, z0 < K).
-   Version 0 holds the counts of z0.  Synchronizes. */
+   Version 0 holds the counts of z0.  Synchronizes.  PS_LDA_EINVAL also when the integer
+   weights could leave 64 bits: (longest document + alpha)(n + beta) / (V beta) * 2^24 * K
+   must stay below 2^62. */
 int ps_lda_load(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int32_t *z0, int64_t n);
 /* run n clocks (asynchronous) */
 int ps_lda_clock(ps_lda_t *h, int32_t n);

@@ -122,6 +122,17 @@ int lda_load(lda_t *o, const int32_t *doc, const int32_t *word, const int32_t *z
   if (o->loaded) return LO_ESTATE;
   for (int64_t t = 0; t < n; ++t)
     if (doc[t] < 0 || doc[t] >= o->D || word[t] < 0 || word[t] >= o->V || z0[t] < 0 || z0[t] >= o->K) return LO_EINVAL;
+  {
+    /* the weights floor(p_k 2^24) and their sum must stay inside 64 bits: p_k is at most
+       (longest document + alpha)(tokens + beta) / (V beta) */
+    int64_t *len = (int64_t *)calloc((size_t)o->D, sizeof(int64_t)), lmax = 0;
+    if (!len) return LO_ENOMEM;
+    for (int64_t t = 0; t < n; ++t)
+      if (++len[doc[t]] > lmax) lmax = len[doc[t]];
+    free(len);
+    const double bound = ((double)lmax + o->alpha) * ((double)n + o->beta) / o->Vbeta * 16777216.0 * (double)o->K;
+    if (!(bound < 4611686018427387904.0)) return LO_EINVAL;
+  }
   const size_t nn = (size_t)(n > 0 ? n : 1), KV = (size_t)((o->V + 1) * o->K);
   o->doc = (int32_t *)malloc(sizeof(int32_t) * nn);
   o->word = (int32_t *)malloc(sizeof(int32_t) * nn);

@@ -672,6 +672,17 @@ int load_tokens(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int3
     if (z0[t] < 0 || z0[t] >= h->K) return lda_fail(h, PS_LDA_EINVAL, "token %lld: topic out of range", (long long)t);
   }
   const int64_t P = h->P, B = h->B, K = h->K, V = h->V;
+  {
+    // every weight floor(p_k 2^24) and their sum must stay far inside 64 bits: p_k is at
+    // most (longest document + alpha)(tokens + beta) / (V beta)
+    std::vector<int64_t> len(static_cast<size_t>(h->D), 0);
+    int64_t lmax = 0;
+    for (int64_t t = 0; t < n; ++t) lmax = std::max(lmax, ++len[doc[t]]);
+    const double bound = (static_cast<double>(lmax) + h->alpha) * (static_cast<double>(n) + h->beta) / h->Vbeta *
+                         16777216.0 * static_cast<double>(K);
+    if (!(bound < 4611686018427387904.0))
+      return lda_fail(h, PS_LDA_EINVAL, "topic weights could exceed 2^62 (raise beta or V): bound %.3g", bound);
+  }
   // processing order: block, worker (document mod P), document, load index
   std::vector<std::pair<uint64_t, int64_t>> key(static_cast<size_t>(n));
   std::vector<int64_t> count(static_cast<size_t>(B * P) + 1, 0);

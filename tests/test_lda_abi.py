@@ -103,3 +103,18 @@ def test_null_handle_calls_are_rejected():
     assert ps_lda._lib.ps_lda_export(None, 0, 0, None, 0, ctypes.byref(n)) == ps_lda.EINVAL
     assert ps_lda._lib.ps_lda_last_error(None) == b"null handle"
     ps_lda._lib.ps_lda_destroy(None)  # NULL-safe
+
+
+def test_weight_range_is_checked_on_both_sides():
+    # V beta = 2e-12: a stale view's weights could leave 64 bits; library and oracle refuse it
+    doc, word, z = [0] * 50, [0, 1] * 25, [0] * 50
+    h = ps_lda.PsLda(1, 2, 4, 1, 1, 0.1, 1e-12, host_only=True)
+    with pytest.raises(ps_lda.PsLdaError) as e:
+        h.load(doc, word, z)
+    assert e.value.code == ps_lda.EINVAL and b"2^62" in ps_lda._lib.ps_lda_last_error(h._h)
+    o = oracle.LdaOracle(1, 2, 4, 1, 1, 0.1, 1e-12)
+    with pytest.raises(oracle.OracleError):
+        o.load(doc, word, z)
+    # the same corpus with beta = 0.01 is accepted by both
+    ps_lda.PsLda(1, 2, 4, 1, 1, 0.1, 0.01, host_only=True).load(doc, word, z)
+    oracle.LdaOracle(1, 2, 4, 1, 1, 0.1, 0.01).load(doc, word, z)
