@@ -13,7 +13,8 @@
 //   - a worker reads its view plus its own changes of the clock: these live in a private
 //     dense delta table (words x K) whose rows carry the clock that last wrote them, so a row
 //     from an older clock reads as zero and nothing is cleared between clocks; the worker's
-//     topic-total changes stay in registers and are added to the new version at its end;
+//     topic-total changes stay in registers and go to its row of a P x K table at its end,
+//     which the commit adds with the tagged own-change rows;
 //   - the doc-topic row of the current document stays in registers while the worker's tokens
 //     of that document run (tokens are in (document, load index) order).
 #include <hip/hip_runtime.h>
