@@ -75,14 +75,14 @@ struct SweepArgs {
   int32_t K, s, policy, nslots, tagc;
 };
 
-// one DPP lane move of a 64-bit value (both halves with the same control); lanes whose
-// source lies outside their row of 16 read 0
-template <int CTRL>
+// one DPP lane move of a 64-bit value (both halves with the same control and row mask);
+// lanes whose source lies outside the pattern, or whose row the mask leaves out, read 0
+template <int CTRL, int ROW_MASK = 0xF>
 __device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
   const uint32_t lo = static_cast<uint32_t>(
-      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x)), CTRL, 0xF, 0xF, false));
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x)), CTRL, ROW_MASK, 0xF, false));
   const uint32_t hi = static_cast<uint32_t>(
-      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x >> 32)), CTRL, 0xF, 0xF, false));
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x >> 32)), CTRL, ROW_MASK, 0xF, false));
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
@@ -93,18 +93,17 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
 }
 
 // inclusive prefix sum of a 64-bit value over the wavefront: Hillis-Steele inside each row
-// of 16 lanes (DPP row shifts 1, 2, 4, 8), then the totals of the rows below added from
-// three lane reads; *total gets the wave's sum
-__device__ __forceinline__ uint64_t wave_scan(uint64_t x, int lane, uint64_t *total) {
+// of 16 lanes (DPP row shifts 1, 2, 4, 8); then row_bcast:15 adds the last lane of rows 0
+// and 2 into rows 1 and 3, and row_bcast:31 the last lane of row 1 (by then the sum of
+// rows 0-1) into rows 2 and 3; *total gets lane 63's sum
+__device__ __forceinline__ uint64_t wave_scan(uint64_t x, uint64_t *total) {
   x += dpp_u64<0x111>(x);
   x += dpp_u64<0x112>(x);
   x += dpp_u64<0x114>(x);
   x += dpp_u64<0x118>(x);
-  const uint64_t r0 = readlane_u64(x, 15), r1 = readlane_u64(x, 31), r2 = readlane_u64(x, 47);
-  const uint64_t r3 = readlane_u64(x, 63);
-  const int row = lane >> 4;
-  x += (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
-  *total = r0 + r1 + r2 + r3;
+  x += dpp_u64<0x142, 0xA>(x);
+  x += dpp_u64<0x143, 0xC>(x);
+  *total = readlane_u64(x, 63);
   return x;
 }
 
@@ -261,7 +260,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
       loc[j] = acc;
     }
     uint64_t total;
-    const uint64_t excl = wave_scan(acc, lane, &total) - acc;
+    const uint64_t excl = wave_scan(acc, &total) - acc;
     int k1 = k0;
     if (total != 0) {
       const uint64_t target = __umul64hi(splitmix64(rbase ^ static_cast<uint64_t>(static_cast<uint32_t>(t))), total);
