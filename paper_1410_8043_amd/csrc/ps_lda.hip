@@ -325,8 +325,9 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
 
 // version c+1 = version c + every worker's changes of clock c.  One wavefront per word row
 // (lanes over topics as in the sweep): the workers' row tags are read 64 at a time, and the
-// own-change rows of the workers that wrote this word in this clock are added; the last
-// row (topic totals) adds the workers' topic-total changes.  Every sum is integer, so the
+// own-change rows of the workers that wrote this word in this clock are added, several
+// loads in flight (a popular word has a writer in nearly every worker); the last row
+// (topic totals) adds the workers' topic-total changes.  Every sum is integer, so the
 // result does not depend on the order.
 template <int KPL>
 __global__ __launch_bounds__(kWave) void k_lda_commit(const int32_t *cur, int32_t *next, const int32_t *delta,
@@ -345,23 +346,53 @@ __global__ __launch_bounds__(kWave) void k_lda_commit(const int32_t *cur, int32_
       const int pl = p0 + lane;
       const bool hit = pl < P && tag[static_cast<int64_t>(pl) * V + w] == tagc;
       uint64_t m = __ballot(hit);
+      // the writers' rows, 8 in flight at a time; a slot past the last writer re-reads
+      // worker p0's row (in bounds) and is not added
+      constexpr int U = 8;
       while (m != 0) {
-        const int pp = p0 + __ffsll(static_cast<unsigned long long>(m)) - 1;
-        m &= m - 1;
-        const int32_t *row = delta + (static_cast<int64_t>(pp) * V + w) * K;
+        int pp[U];
+        bool ok[U];
 #pragma unroll
-        for (int j = 0; j < KPL; ++j) {
-          const int k = lane * KPL + j;
-          if (k < K) acc[j] += row[k];
+        for (int u = 0; u < U; ++u) {
+          ok[u] = m != 0;
+          pp[u] = p0 + (ok[u] ? __ffsll(static_cast<unsigned long long>(m)) - 1 : 0);
+          if (ok[u]) m &= m - 1;
+        }
+        int t[U][KPL];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int32_t *row = delta + (static_cast<int64_t>(pp[u]) * V + w) * K;
+#pragma unroll
+          for (int j = 0; j < KPL; ++j) {
+            const int k = lane * KPL + j;
+            t[u][j] = k < K ? row[k] : 0;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+          for (int j = 0; j < KPL; ++j)
+            if (ok[u]) acc[j] += t[u][j];
         }
       }
     }
   } else {
-    for (int pp = 0; pp < P; ++pp) {
+    // the topic-total rows, 16 workers' rows in flight at a time
+    constexpr int U = 16;
+    for (int p0 = 0; p0 < P; p0 += U) {
+      int t[U][KPL];
 #pragma unroll
-      for (int j = 0; j < KPL; ++j) {
-        const int k = lane * KPL + j;
-        if (k < K) acc[j] += tot[static_cast<int64_t>(pp) * K + k];
+      for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+          const int k = lane * KPL + j;
+          t[u][j] = (p0 + u < P && k < K) ? tot[static_cast<int64_t>(p0 + u) * K + k] : 0;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) acc[j] += t[u][j];
       }
     }
   }
