@@ -125,6 +125,12 @@ def test_full_corpus_bit_exact_256_workers(lda):
     both(lda, spec, lc.generate(spec), oracle.ESSP, 2, check_every=1)
 
 
+def test_full_corpus_bit_exact_256_topics(lda):
+    # four topics per lane at full size: the small corpus with K = 256
+    spec = lc.scaled(lc.CORPORA["small"], 1.0, K=256)
+    both(lda, spec, lc.generate(spec), oracle.SSP_LAZY, 2, check_every=1)
+
+
 def test_full_corpus_counts_stay_tallies(lda):
     spec = lc.CORPORA["small"]
     corpus = lc.generate(spec)
