@@ -177,3 +177,31 @@ def test_paper_scale_corpus_counts_stay_tallies(lda):
     assert 0.3 < moved < 1.0
     assert g.loglik() > ll0
     g.close()
+
+
+def test_policy_identities_at_full_size(lda):
+    # properties that hold at any size: ESSP reads one clock back whatever s >= 1 is, and at
+    # s = 0 every policy is BSP; each pair must agree bit for bit on the full small corpus
+    spec = lc.CORPORA["small"]
+    corpus = lc.generate(spec)
+
+    def run(policy, s, clocks=4):
+        g = lda.PsLda(spec.D, spec.V, spec.K, spec.P, s, spec.alpha, spec.beta, policy=policy, B=spec.B,
+                      seed=spec.seed)
+        g.load(corpus.doc, corpus.word, corpus.z0)
+        g.clock(clocks)
+        out = (g.z(), g.nwk(), g.export(lda.X_VERSION_LOG))
+        g.close()
+        return out
+
+    say("lda policy identities: ESSP s=1 vs s=7, and the three policies at s=0")
+    a, b = run(lda.ESSP, 1), run(lda.ESSP, 7)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    np.testing.assert_array_equal(a[2], b[2])
+    bsp = run(lda.ESSP, 0)
+    for pol in (lda.SSP_LAZY, lda.SSP_WORST):
+        x = run(pol, 0)
+        np.testing.assert_array_equal(x[0], bsp[0])
+        np.testing.assert_array_equal(x[1], bsp[1])
+    assert not np.array_equal(a[0], bsp[0])  # stale and fresh views do differ
