@@ -239,3 +239,28 @@ def test_argument_errors():
     o.load([], [], [])
     o.clock(2)
     assert o.loglik() == pytest.approx(0.0, abs=0)
+
+
+def test_policy_identities():
+    # ESSP reads one clock back whatever s >= 1 is; at s = 0 every policy is BSP
+    spec = _tiny(P=5)
+    corpus = lc.generate(spec)
+
+    def state(policy, s):
+        o = oracle.LdaOracle(spec.D, spec.V, spec.K, spec.P, s, spec.alpha, spec.beta, policy, spec.B, spec.seed)
+        o.load(corpus.doc, corpus.word, corpus.z0)
+        o.clock(6)
+        return o.z(), o.nwk()
+
+    a, b = state(oracle.ESSP, 1), state(oracle.ESSP, 7)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    bsp = state(oracle.ESSP, 0)
+    for pol in (oracle.SSP_LAZY, oracle.SSP_WORST):
+        x = state(pol, 0)
+        np.testing.assert_array_equal(x[0], bsp[0])
+        np.testing.assert_array_equal(x[1], bsp[1])
+    assert not np.array_equal(a[0], bsp[0])
+    # SSP_WORST at s = 1 is ESSP at s = 1 (both read exactly one clock back)
+    w = state(oracle.SSP_WORST, 1)
+    np.testing.assert_array_equal(w[0], a[0])
