@@ -24,11 +24,13 @@
  *     + every worker's changes of clock c (integer counts: exact in any summation order);
  *   - a count that excludes the token is the view's count (plus own changes) minus one for
  *     k0, floored at zero (a stale view may predate the token's current topic);
- *   - the draw is exact integer arithmetic: topic k weighs floor(p_k * 2^24), p_k evaluated
- *     in IEEE fp64 as ((n_dk + alpha) * (n_wk + beta)) / (n_k + Vbeta), Vbeta = V * beta; with
- *     W the sum of the weights and r = splitmix64(seed ^ 0x5851F42D4C957F2D ^ (c << 40) ^ t),
- *     the new topic is the first k whose prefix sum of weights exceeds floor(r W / 2^64); if W
- *     is 0 the topic stays;
+ *   - the draw is exact integer arithmetic: p_k is evaluated in IEEE fp64 as
+ *     ((n_dk + alpha) * (n_wk + beta)) / (n_k + Vbeta), Vbeta = V * beta; with e the binary
+ *     exponent of the token's largest p_k and c_K = ceil(log2 K), topic k weighs
+ *     floor(p_k * 2^(62 - c_K - e)) (exact scaling; the weights keep every p_k to within
+ *     2^-(62 - c_K) of the largest, and sum below 2^63); with W the sum of the weights and
+ *     r = splitmix64(seed ^ 0x5851F42D4C957F2D ^ (c << 40) ^ t), the new topic is the first k
+ *     whose prefix sum of weights exceeds floor(r W / 2^64);
  *   - log-likelihood: the collapsed log p(w, z) of the latest version and the doc-topic
  *     counts, in fp64.
  *
@@ -83,9 +85,9 @@ int ps_lda_set_option(ps_lda_t *h, int32_t key, int64_t value);
 /* hip_stream: a hipStream_t of the current device, or NULL for a stream the handle creates. */
 int ps_lda_set_stream(ps_lda_t *h, void *hip_stream);
 /* n tokens as host arrays: document, word, initial topic (0 <= doc < D, word < V, z0 < K).
-   Version 0 holds the counts of z0.  Synchronizes.  PS_LDA_EINVAL also when the integer
-   weights could leave 64 bits: (longest document + alpha)(n + beta) / (V beta) * 2^24 * K
-   must stay below 2^62. */
+   Version 0 holds the counts of z0.  Synchronizes.  PS_LDA_EINVAL also when some p_k could
+   leave the normal fp64 range: alpha beta / (n + V beta) must be at least 2^-1000 and
+   (longest document + alpha)(n + beta) / (V beta) at most 2^1000. */
 int ps_lda_load(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int32_t *z0, int64_t n);
 /* run n clocks (asynchronous) */
 int ps_lda_clock(ps_lda_t *h, int32_t n);

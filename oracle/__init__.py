@@ -66,6 +66,7 @@ def _load():
         "lda_clock": [vp, i32],
         "lda_loglik": [vp, ctypes.POINTER(dbl)],
         "lda_export": [vp, i32, i32, vp, i64, ctypes.POINTER(i64)],
+        "lda_token_draw": [vp, vp, vp, vp, i32, u64, vp, ctypes.POINTER(u64), ctypes.POINTER(i32)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -263,6 +264,18 @@ class LdaOracle:
         _chk(self._lib.lda_export(self._h, kind, block, buf.ctypes.data if n.value else None, n.value,
                                   ctypes.byref(n)), "lda_export")
         return buf
+
+    def token_draw(self, nd, nw, nk, k0, r):
+        """One token's draw from its counts n_dk, n_wk, n_k (each including the token, which
+        is in topic k0) and the random number r: (weights [K] as Python ints, their sum, topic)."""
+        nd, nw, nk = _c(nd, np.int32), _c(nw, np.int32), _c(nk, np.int32)
+        assert nd.shape == nw.shape == nk.shape == (self.K,)
+        w = np.zeros(self.K, np.uint64)
+        total, k = ctypes.c_uint64(), ctypes.c_int32()
+        _chk(self._lib.lda_token_draw(self._h, nd.ctypes.data, nw.ctypes.data, nk.ctypes.data, int(k0),
+                                      int(r) & (2**64 - 1), w.ctypes.data, ctypes.byref(total), ctypes.byref(k)),
+             "lda_token_draw")
+        return [int(x) for x in w], total.value, k.value
 
     def z(self):
         return self.export(LDA_Z)

@@ -25,11 +25,14 @@
  *   - excluding the token from a view that may predate its current topic: the view's
  *     counts minus one for k0, floored at zero;
  *   - the draw is exact integer arithmetic, so that any summation order gives the same
- *     topic: the weight of topic k is floor(p_k * 2^24) with p_k evaluated in fp64 as
- *     ((n_dk + alpha) * (n_wk + beta)) / (n_k + Vbeta), Vbeta = V * beta computed once; with
- *     W the sum of the weights and r = splitmix64(seed ^ 0x5851F42D4C957F2D ^ (c << 40) ^ t),
- *     the new topic is the first k whose prefix sum of weights exceeds floor(r * W / 2^64)
- *     (all weights zero: the topic stays);
+ *     topic: p_k is evaluated in fp64 as ((n_dk + alpha) * (n_wk + beta)) / (n_k + Vbeta),
+ *     Vbeta = V * beta computed once; with e the binary exponent of the largest p_k
+ *     (2^e <= max p_k < 2^(e+1)) and c_K = ceil(log2 K), topic k weighs
+ *     floor(p_k * 2^(62 - c_K - e)) (a scaling by a power of two is exact, and the largest
+ *     weight is at least 2^(62 - c_K), so each weight keeps p_k to within one part in
+ *     2^(62 - c_K) of the largest and the K weights sum below 2^63); with W the sum of the
+ *     weights and r = splitmix64(seed ^ 0x5851F42D4C957F2D ^ (c << 40) ^ t), the new topic
+ *     is the first k whose prefix sum of weights exceeds floor(r * W / 2^64);
  *   - log-likelihood: the collapsed log p(w, z) in fp64.
  *
  * Build: compiled with ps_mf_oracle.c into libps_mf_oracle.so (gcc -O2, no fast math).
@@ -60,6 +63,8 @@ typedef struct {
   int32_t *delta;           /* (V+1)*K: one worker's changes of the clock */
   int64_t *acc;             /* (V+1)*K: every worker's changes of the clock */
   uint64_t *w;              /* K weights */
+  double *pk;               /* K unnormalised probabilities */
+  int32_t clog2k;           /* ceil(log2 K) */
   int loaded;
   int64_t clock;
   int64_t *vlog;            /* clock-major v(p, c) */
@@ -89,7 +94,7 @@ static int32_t *lda_slot(const lda_t *o, int64_t v) {
 void lda_destroy(lda_t *o) {
   if (!o) return;
   free(o->doc); free(o->word); free(o->z); free(o->bstart); free(o->order); free(o->ndk); free(o->ring);
-  free(o->delta); free(o->acc); free(o->w); free(o->vlog);
+  free(o->delta); free(o->acc); free(o->w); free(o->pk); free(o->vlog);
   free(o);
 }
 
@@ -103,7 +108,15 @@ int lda_create(int64_t D, int64_t V, int32_t K, int32_t P, int32_t s, double alp
   if (!o) return LO_ENOMEM;
   o->D = D; o->V = V; o->K = K; o->P = P; o->s = s; o->policy = policy; o->B = B;
   o->alpha = alpha; o->beta = beta; o->Vbeta = (double)V * beta; o->seed = seed;
+  while ((1LL << o->clog2k) < (int64_t)K) o->clog2k += 1;
+  o->w = (uint64_t *)calloc((size_t)K, sizeof(uint64_t));
+  o->pk = (double *)calloc((size_t)K, sizeof(double));
   *out = o;
+  if (!o->w || !o->pk) {
+    lda_destroy(o);
+    *out = NULL;
+    return LO_ENOMEM;
+  }
   return LO_OK;
 }
 
@@ -123,15 +136,17 @@ int lda_load(lda_t *o, const int32_t *doc, const int32_t *word, const int32_t *z
   for (int64_t t = 0; t < n; ++t)
     if (doc[t] < 0 || doc[t] >= o->D || word[t] < 0 || word[t] >= o->V || z0[t] < 0 || z0[t] >= o->K) return LO_EINVAL;
   {
-    /* the weights floor(p_k 2^24) and their sum must stay inside 64 bits: p_k is at most
-       (longest document + alpha)(tokens + beta) / (V beta) */
+    /* every p_k must be a normal fp64 number, so that its exponent is defined: p_k lies
+       between alpha beta / (tokens + V beta) and (longest document + alpha)(tokens + beta) /
+       (V beta), and both must stay inside [2^-1000, 2^1000] */
     int64_t *len = (int64_t *)calloc((size_t)o->D, sizeof(int64_t)), lmax = 0;
     if (!len) return LO_ENOMEM;
     for (int64_t t = 0; t < n; ++t)
       if (++len[doc[t]] > lmax) lmax = len[doc[t]];
     free(len);
-    const double bound = ((double)lmax + o->alpha) * ((double)n + o->beta) / o->Vbeta * 16777216.0 * (double)o->K;
-    if (!(bound < 4611686018427387904.0)) return LO_EINVAL;
+    const double hi = ((double)lmax + o->alpha) * ((double)n + o->beta) / o->Vbeta;
+    const double lo = o->alpha * o->beta / ((double)n + o->Vbeta);
+    if (!(hi <= ldexp(1.0, 1000)) || !(lo >= ldexp(1.0, -1000))) return LO_EINVAL;
   }
   const size_t nn = (size_t)(n > 0 ? n : 1), KV = (size_t)((o->V + 1) * o->K);
   o->doc = (int32_t *)malloc(sizeof(int32_t) * nn);
@@ -143,11 +158,10 @@ int lda_load(lda_t *o, const int32_t *doc, const int32_t *word, const int32_t *z
   o->ring = (int32_t *)calloc(KV * (size_t)(o->s + 1), sizeof(int32_t));
   o->delta = (int32_t *)calloc(KV, sizeof(int32_t));
   o->acc = (int64_t *)calloc(KV, sizeof(int64_t));
-  o->w = (uint64_t *)calloc((size_t)o->K, sizeof(uint64_t));
   int32_t *blk = (int32_t *)malloc(sizeof(int32_t) * nn);
   int64_t *fill = (int64_t *)calloc((size_t)o->B, sizeof(int64_t));
-  if (!o->doc || !o->word || !o->z || !o->order || !o->bstart || !o->ndk || !o->ring || !o->delta || !o->acc || !o->w ||
-      !blk || !fill) {
+  if (!o->doc || !o->word || !o->z || !o->order || !o->bstart || !o->ndk || !o->ring || !o->delta || !o->acc || !blk ||
+      !fill) {
     free(blk); free(fill);
     return LO_ENOMEM;
   }
@@ -173,10 +187,11 @@ int lda_load(lda_t *o, const int32_t *doc, const int32_t *word, const int32_t *z
   return LO_OK;
 }
 
-/* one token: the new topic (the reading's exact integer draw) */
-static int32_t lda_draw(lda_t *o, const int32_t *nd, const int32_t *vw, const int32_t *dw, const int32_t *vk,
-                        const int32_t *dk, int32_t k0, uint64_t r) {
-  uint64_t total = 0;
+/* one token: the weights of its topics (into o->w) and their sum, from counts that
+   include the token (it is excluded here, each count floored at zero) */
+static uint64_t lda_weights(lda_t *o, const int32_t *nd, const int32_t *vw, const int32_t *dw, const int32_t *vk,
+                            const int32_t *dk, int32_t k0) {
+  double pmax = 0.0;
   for (int32_t k = 0; k < o->K; ++k) {
     const int32_t self = k == k0;
     int64_t ndk = (int64_t)nd[k] - self;
@@ -185,11 +200,22 @@ static int32_t lda_draw(lda_t *o, const int32_t *nd, const int32_t *vw, const in
     if (nwk < 0) nwk = 0;
     if (nk < 0) nk = 0;
     const double a = (double)ndk + o->alpha, b = (double)nwk + o->beta, c = (double)nk + o->Vbeta;
-    const double p = (a * b) / c;
-    o->w[k] = (uint64_t)floor(p * 16777216.0);
+    o->pk[k] = (a * b) / c;
+    if (o->pk[k] > pmax) pmax = o->pk[k];
+  }
+  /* scale so that the largest weight lies in [2^(62 - c_K), 2^(63 - c_K)) */
+  const int shift = 62 - o->clog2k - ilogb(pmax);
+  uint64_t total = 0;
+  for (int32_t k = 0; k < o->K; ++k) {
+    o->w[k] = (uint64_t)floor(ldexp(o->pk[k], shift));
     total += o->w[k];
   }
-  if (total == 0) return k0;
+  return total;
+}
+
+/* the first topic whose prefix sum of weights exceeds floor(r W / 2^64) */
+static int32_t lda_pick(const lda_t *o, uint64_t total, int32_t k0, uint64_t r) {
+  if (total == 0) return k0; /* not reached: the largest weight is at least 2^(62 - c_K) */
   const uint64_t target = (uint64_t)(((unsigned __int128)r * total) >> 64);
   uint64_t cum = 0;
   for (int32_t k = 0; k < o->K; ++k) {
@@ -197,6 +223,27 @@ static int32_t lda_draw(lda_t *o, const int32_t *nd, const int32_t *vw, const in
     if (cum > target) return k;
   }
   return o->K - 1; /* not reached: cum ends at total > target */
+}
+
+static int32_t lda_draw(lda_t *o, const int32_t *nd, const int32_t *vw, const int32_t *dw, const int32_t *vk,
+                        const int32_t *dk, int32_t k0, uint64_t r) {
+  return lda_pick(o, lda_weights(o, nd, vw, dw, vk, dk, k0), k0, r);
+}
+
+/* One token's weights and draw from its counts n_dk, n_wk and n_k (each including the
+   token, which sits in topic k0) and the random number r, for the tests' pins of the draw:
+   w_out[K] receives the weights, *k_out the drawn topic, *total_out their sum. */
+int lda_token_draw(lda_t *o, const int32_t *nd, const int32_t *nw, const int32_t *nk, int32_t k0, uint64_t r,
+                   uint64_t *w_out, uint64_t *total_out, int32_t *k_out) {
+  if (!o || !nd || !nw || !nk || !w_out || !total_out || !k_out || k0 < 0 || k0 >= o->K) return LO_EINVAL;
+  int32_t *zero = (int32_t *)calloc((size_t)o->K, sizeof(int32_t));
+  if (!zero) return LO_ENOMEM;
+  const uint64_t total = lda_weights(o, nd, nw, zero, nk, zero, k0);
+  memcpy(w_out, o->w, sizeof(uint64_t) * (size_t)o->K);
+  *total_out = total;
+  *k_out = lda_pick(o, total, k0, r);
+  free(zero);
+  return LO_OK;
 }
 
 static int lda_one_clock(lda_t *o) {

@@ -8,8 +8,9 @@
 //     changes of the clock (integer sums: exact and order-free);
 //   - one wavefront per worker, lanes over topics (lane l holds ceil(K/64) consecutive
 //     topics): the collapsed conditional's K weights are computed in fp64 and quantised to
-//     integers, their prefix sums come from per-lane sums and one DPP wave scan, and the
-//     drawn topic from one ballot;
+//     integers on a scale set by the largest of them (its exponent from a DPP wave max),
+//     their prefix sums come from per-lane sums and one DPP wave scan, and the drawn topic
+//     from one ballot;
 //   - a worker reads its view plus its own changes of the clock: these live in a private
 //     dense delta table (words x K) whose rows carry the clock that last wrote them, so a row
 //     from an older clock reads as zero and nothing is cleared between clocks; the worker's
@@ -73,6 +74,7 @@ struct SweepArgs {
   double alpha, beta, Vbeta;
   uint64_t seed;
   int32_t K, s, policy, nslots, tagc;
+  int32_t shift0;       // 62 - ceil(log2 K): the largest weight lies in [2^shift0, 2^(shift0+1))
 };
 
 // one DPP lane move of a 64-bit value (both halves with the same control and row mask);
@@ -105,6 +107,18 @@ __device__ __forceinline__ uint64_t wave_scan(uint64_t x, uint64_t *total) {
   x += dpp_u64<0x143, 0xC>(x);
   *total = readlane_u64(x, 63);
   return x;
+}
+
+// maximum of an int over the wavefront, returned in every lane: DPP quad_perm [1,0,3,2],
+// quad_perm [2,3,0,1], row_half_mirror and row_mirror give each lane its 16-lane row's
+// maximum (every source lane lies inside the row), then the four rows' maxima are read
+__device__ __forceinline__ int wave_max_i32(int x) {
+  x = max(x, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, true));
+  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, true));
+  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x141, 0xF, 0xF, true));
+  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x140, 0xF, 0xF, true));
+  return max(max(__builtin_amdgcn_readlane(x, 0), __builtin_amdgcn_readlane(x, 16)),
+             max(__builtin_amdgcn_readlane(x, 32), __builtin_amdgcn_readlane(x, 48)));
 }
 
 // what one token reads before it can be sampled: its view row and own-change row of the
@@ -240,29 +254,38 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
       }
       cur_doc = d;
     }
-    // quantised weights of the collapsed conditional, prefix sums in topic order
-    uint64_t loc[KPL];
-    uint64_t acc = 0;
+    // the collapsed conditional's weights p_k in fp64 (every p_k is a normal number: the
+    // load checks the range) and the exponent of the largest (the largest exponent)
+    double pk[KPL];
+    int emax = -2048;  // below every normal exponent: lanes past the last topic
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
       const int k = lane * KPL + j;
-      uint64_t om = 0;
+      pk[j] = 0.0;
       if (k < K) {
         const int self = k == k0;
         const int ndx = nd[j] - self;
         const int nwx = max(rows[C].nw[j] + dw[j] - self, 0);
         const int nkx = max(vk[j] + dk[j] - self, 0);
         const double num = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
-        const double pk = num / (static_cast<double>(nkx) + a.Vbeta);
-        om = static_cast<uint64_t>(floor(pk * 16777216.0));
+        pk[j] = num / (static_cast<double>(nkx) + a.Vbeta);
+        emax = max(emax, __builtin_amdgcn_frexp_exp(pk[j]) - 1);  // frexp: p = m 2^x, m in [0.5, 1)
       }
-      acc += om;
+    }
+    // integer weights floor(p_k 2^(shift0 - emax)) (the scaling is exact), prefix sums in
+    // topic order
+    const int shift = a.shift0 - wave_max_i32(emax);
+    uint64_t loc[KPL];
+    uint64_t acc = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      acc += static_cast<uint64_t>(floor(ldexp(pk[j], shift)));  // pk = 0 past the last topic
       loc[j] = acc;
     }
     uint64_t total;
     const uint64_t excl = wave_scan(acc, &total) - acc;
     int k1 = k0;
-    if (total != 0) {
+    if (total != 0) {  // always: the largest weight is at least 2^shift0
       const uint64_t target = __umul64hi(splitmix64(rbase ^ static_cast<uint64_t>(static_cast<uint32_t>(t))), total);
       const uint64_t m = __ballot(excl + acc > target);
       const int L = __ffsll(static_cast<unsigned long long>(m)) - 1;  // m != 0: the last lane's sum is the total
@@ -575,6 +598,9 @@ int sweep(ps_lda_t *h) {
   a.s = h->s;
   a.policy = h->policy;
   a.nslots = static_cast<int32_t>(ns);
+  int clog2k = 0;
+  while ((int64_t{1} << clog2k) < h->K) ++clog2k;
+  a.shift0 = 62 - clog2k;
   a.tagc = static_cast<int32_t>(c + 1);
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (h->timing) {
@@ -704,15 +730,16 @@ int load_tokens(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int3
   }
   const int64_t P = h->P, B = h->B, K = h->K, V = h->V;
   {
-    // every weight floor(p_k 2^24) and their sum must stay far inside 64 bits: p_k is at
-    // most (longest document + alpha)(tokens + beta) / (V beta)
+    // every p_k must be a normal fp64 number (its exponent sets the weights' scale): p_k
+    // lies between alpha beta / (tokens + V beta) and (longest document + alpha)(tokens +
+    // beta) / (V beta)
     std::vector<int64_t> len(static_cast<size_t>(h->D), 0);
     int64_t lmax = 0;
     for (int64_t t = 0; t < n; ++t) lmax = std::max(lmax, ++len[doc[t]]);
-    const double bound = (static_cast<double>(lmax) + h->alpha) * (static_cast<double>(n) + h->beta) / h->Vbeta *
-                         16777216.0 * static_cast<double>(K);
-    if (!(bound < 4611686018427387904.0))
-      return lda_fail(h, PS_LDA_EINVAL, "topic weights could exceed 2^62 (raise beta or V): bound %.3g", bound);
+    const double hi = (static_cast<double>(lmax) + h->alpha) * (static_cast<double>(n) + h->beta) / h->Vbeta;
+    const double lo = h->alpha * h->beta / (static_cast<double>(n) + h->Vbeta);
+    if (!(hi <= std::ldexp(1.0, 1000)) || !(lo >= std::ldexp(1.0, -1000)))
+      return lda_fail(h, PS_LDA_EINVAL, "topic weights leave [2^-1000, 2^1000]: from %.3g to %.3g", lo, hi);
   }
   // processing order: block, worker (document mod P), document, load index
   std::vector<std::pair<uint64_t, int64_t>> key(static_cast<size_t>(n));

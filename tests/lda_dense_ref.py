@@ -4,10 +4,11 @@ A different code shape from the oracle: every committed version of the shared co
 kept (a list of dense [V+1, K] arrays, row V the topic totals) and the view of worker p at
 clock c is read from that history directly; each worker works on a private copy of its
 view that it updates in place, and the clock's new version is the latest version plus
-the sum over workers of (copy - view).  Same reading of the draw: weights
-floor(p_k * 2^24) with p_k = ((n_dk + alpha)(n_wk + beta)) / (n_k + V beta) over counts that
-exclude the token (floored at zero), the new topic the first whose prefix sum of weights
-exceeds floor(r W / 2^64).
+the sum over workers of (copy - view).  Same reading of the draw: with
+p_k = ((n_dk + alpha)(n_wk + beta)) / (n_k + V beta) over counts that exclude the token
+(floored at zero), e the binary exponent of the largest p_k and c_K = ceil(log2 K), the
+weights are floor(p_k 2^(62 - c_K - e)); the new topic is the first whose prefix sum of
+weights exceeds floor(r W / 2^64).
 """
 import numpy as np
 
@@ -28,10 +29,12 @@ def draw(nd, nw, nk, k0, alpha, beta, Vb, r):
     a = (nd.astype(np.int64) - self_).astype(np.float64) + alpha
     b = np.maximum(nw.astype(np.int64) - self_, 0).astype(np.float64) + beta
     c = np.maximum(nk.astype(np.int64) - self_, 0).astype(np.float64) + Vb
-    w = [int(x) for x in np.floor((a * b) / c * 16777216.0)]
+    p = (a * b) / c
+    # frexp: p = m 2^x with m in [0.5, 1), so the binary exponent is x - 1
+    e = int(np.frexp(p)[1].max()) - 1
+    shift = 62 - (K - 1).bit_length() - e
+    w = [int(x) for x in np.floor(np.ldexp(p, shift))]
     total = sum(w)
-    if total == 0:
-        return k0
     target = (r * total) >> 64
     cum = 0
     for k in range(K):

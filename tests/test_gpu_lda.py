@@ -6,6 +6,9 @@ operations on both sides, so the bar is bit-exact: every assignment and count af
 checked clock.  The log-likelihood (fp64 sums of lgamma terms in different orders, the
 library's lgamma against the C library's) within a relative 1e-9.
 """
+import hashlib
+import json
+import os
 import sys
 
 import numpy as np
@@ -74,8 +77,9 @@ def test_every_topic_count_layout(lda, K):
 
 
 @pytest.mark.parametrize("alpha", [1e-6, 1e-9])
-def test_integer_boundaries_and_zero_weights(lda, alpha):
-    # weights of a few units: draws land on prefix sums; alpha 1e-9: all-zero weights keep the topic
+def test_extreme_weight_ratios(lda, alpha):
+    # one- and two-token documents with a tiny alpha: a token's weights span six to nine
+    # decades, and the scale is set by its own topic
     spec = lc.scaled(lc.CORPORA["tiny"], 1.0, D=300, V=10, K=6, P=3, s=1, mean_len=1, alpha=alpha, beta=0.5)
     both(lda, spec, lc.generate(spec), oracle.ESSP, 6, check_every=2)
 
@@ -151,30 +155,47 @@ def test_full_corpus_counts_stay_tallies(lda):
     assert g.loglik() > ll0
 
 
-def test_paper_scale_corpus_counts_stay_tallies(lda):
+def _digest(a):
+    """SHA-256 of an integer array as little-endian int32 in C order."""
+    a = np.ascontiguousarray(a)
+    return hashlib.sha256(a.astype("<i4").tobytes()).hexdigest()
+
+
+def test_paper_scale_corpus_against_the_oracle(lda):
     # the paper's topic-model shape as bench.py --workload lda --corpus nyt runs it: 100M
-    # tokens, 100k words, K = 100, P = 512, half of the tokens per clock
+    # tokens, 100k words, K = 100, P = 512 (eight ballot rounds of 64 workers in the
+    # commit), half of the tokens per clock, ESSP.  The oracle's state after each of two
+    # clocks is stored as SHA-256 digests (tests/golden/make_lda_nyt_golden.py, a few CPU
+    # minutes); the GPU's assignments and counts must hash the same, i.e. be equal bit for
+    # bit, and the counts must be the tallies of the assignments.
+    with open(os.path.join(os.path.dirname(__file__), "golden", "lda_nyt_oracle.json")) as f:
+        gold = json.load(f)
     spec = lc.CORPORA["nyt"]
+    assert gold["corpus"]["name"] == spec.name and gold["policy"] == "ESSP"
     say("lda paper-scale corpus: generating")
     corpus = lc.generate(spec)
+    assert corpus.ntok == gold["corpus"]["ntok"]
+    for key in ("doc", "word", "z0"):
+        assert _digest(getattr(corpus, key)) == gold["corpus"][key], f"the generator's {key} changed"
     say(f"lda paper-scale corpus: {corpus.ntok} tokens, loading")
     g = lda.PsLda(spec.D, spec.V, spec.K, spec.P, spec.s, spec.alpha, spec.beta, policy=lda.ESSP, B=spec.B,
                   seed=spec.seed)
     g.load(corpus.doc, corpus.word, corpus.z0)
     ll0 = g.loglik()
-    say("lda paper-scale corpus: 2 clocks")
-    g.clock(2)
-    z = g.z()
     K = spec.K
-    ndk = np.bincount(corpus.doc.astype(np.int64) * K + z, minlength=spec.D * K).reshape(spec.D, K)
-    n = np.bincount(corpus.word.astype(np.int64) * K + z, minlength=spec.V * K).reshape(spec.V, K)
-    np.testing.assert_array_equal(g.ndk(), ndk)
-    nwk = g.nwk()
-    np.testing.assert_array_equal(nwk[:spec.V], n)
+    for entry in gold["clocks"]:
+        g.clock(1)
+        z, ndk, nwk = g.z(), g.ndk(), g.nwk()
+        say(f"lda paper-scale corpus: clock {entry['clock']}, {float((z != corpus.z0).mean()):.3f} moved")
+        assert _digest(z) == entry["z"], f"assignments after clock {entry['clock']}"
+        assert _digest(ndk) == entry["ndk"], f"doc-topic counts after clock {entry['clock']}"
+        assert _digest(nwk) == entry["nwk"], f"word-topic counts after clock {entry['clock']}"
+        assert g.loglik() == pytest.approx(entry["loglik"], rel=LL_RTOL)
+    np.testing.assert_array_equal(ndk, np.bincount(corpus.doc.astype(np.int64) * K + z,
+                                                   minlength=spec.D * K).reshape(spec.D, K))
+    np.testing.assert_array_equal(nwk[:spec.V], np.bincount(corpus.word.astype(np.int64) * K + z,
+                                                            minlength=spec.V * K).reshape(spec.V, K))
     np.testing.assert_array_equal(nwk[spec.V], np.bincount(z, minlength=K))
-    moved = float((z != corpus.z0).mean())
-    say(f"lda paper-scale corpus: {moved:.3f} of the tokens moved")
-    assert 0.3 < moved < 1.0
     assert g.loglik() > ll0
     g.close()
 

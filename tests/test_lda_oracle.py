@@ -17,6 +17,7 @@ Each check rests on something other than the oracle's own code:
 """
 import itertools
 import math
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -163,10 +164,10 @@ def test_matches_brute_force_history(policy, P, s, B):
 
 
 @pytest.mark.parametrize("alpha", [1e-6, 1e-9])
-def test_matches_brute_force_on_integer_boundaries(alpha):
-    # one- and two-token documents with a tiny alpha: the weights are a few units (alpha 1e-6:
-    # at most 16 per topic), so draws often land exactly on a prefix sum, and with alpha 1e-9
-    # every weight of a lone token is zero and its topic must stay
+def test_matches_brute_force_with_extreme_weight_ratios(alpha):
+    # one- and two-token documents with a tiny alpha: a lone token's topics weigh between
+    # about alpha and 1, so the weights span six to nine decades and the scale is set by
+    # the token's own topic
     spec = _tiny(D=120, V=10, K=6, P=3, s=1, B=2, mean_len=1, alpha=alpha, beta=0.5)
     corpus = lc.generate(spec)
     clocks = 6
@@ -177,6 +178,110 @@ def test_matches_brute_force_on_integer_boundaries(alpha):
     np.testing.assert_array_equal(o.z(), z)
     np.testing.assert_array_equal(o.ndk(), ndk)
     np.testing.assert_array_equal(o.nwk(), n)
+
+
+def _paper_shape_token(rng, K, n_k, doc_topics, word_topics, k0):
+    """Counts of one token at the 100M-token, V = 100k, K = 100 shape (each topic holds about
+    1e6 tokens): a document of about 300 tokens over a few topics, a word used by a few
+    topics, every count including the token itself (topic k0)."""
+    nk = rng.integers(int(0.8 * n_k), int(1.2 * n_k), K).astype(np.int32)
+    nd = np.zeros(K, np.int32)
+    nd[doc_topics] = rng.integers(1, 120, len(doc_topics))
+    nw = np.zeros(K, np.int32)
+    nw[word_topics] = rng.integers(1, 3000, len(word_topics))
+    nd[k0] = max(nd[k0], 1)
+    nw[k0] = max(nw[k0], 1)
+    return nd, nw, nk
+
+
+def _exact_probabilities(nd, nw, nk, k0, alpha, beta, V):
+    """The collapsed conditional in exact rational arithmetic (alpha and beta as the exact
+    values of their doubles), the token excluded from every count."""
+    a, b = Fraction(alpha), Fraction(beta)
+    p = []
+    for k in range(len(nd)):
+        self_ = int(k == k0)
+        p.append((int(nd[k]) - self_ + a) * (int(nw[k]) - self_ + b) / (int(nk[k]) - self_ + V * b))
+    total = sum(p)
+    return [x / total for x in p]
+
+
+def test_draw_weights_at_the_paper_shape():
+    # Section 5's topic-model shape: V = 100k words, K = 100 topics, 100M tokens, so every
+    # topic total n_k is about 1e6.  A topic that neither the document nor the word uses
+    # weighs only alpha beta / (n_k + V beta), about 1e-9 -- 3e-9 to 3e-5 of the token's total
+    # weight here -- and must still keep its exact share.  Flooring loses less than one unit
+    # per weight, so with pi_k the exact probability, |w_k / W - pi_k| <= (1 + K pi_k) / W,
+    # W >= 2^(62 - c_K): every share is within 2^-40 of the exact one, every weight is
+    # positive, and the smoothing-only topics are within 2^-24 of their own value (a fixed
+    # absolute scale such as floor(p_k 2^24) floors them to zero)
+    K, V, alpha, beta, n_k = 100, 100_000, 0.1, 0.01, 1_000_000
+    o = oracle.LdaOracle(1, V, K, 1, 0, alpha, beta, oracle.ESSP, 1, 1)
+    rng = np.random.default_rng(1410)
+    ck = (K - 1).bit_length()
+    for trial in range(40):
+        doc_topics = rng.choice(K, int(rng.integers(1, 8)), replace=False)
+        word_topics = rng.choice(K, int(rng.integers(1, 6)), replace=False)
+        k0 = int(rng.choice(doc_topics))
+        nd, nw, nk = _paper_shape_token(rng, K, n_k, doc_topics, word_topics, k0)
+        w, total, _ = o.token_draw(nd, nw, nk, k0, int(rng.integers(0, 2**63)))
+        assert total == sum(w) and total < 2**63
+        assert 2 ** (62 - ck) <= max(w) < 2 ** (63 - ck)
+        exact = _exact_probabilities(nd, nw, nk, k0, alpha, beta, V)
+        smoothing_only = [k for k in range(K) if nd[k] - (k == k0) == 0 and nw[k] - (k == k0) == 0]
+        assert smoothing_only, "the shape always leaves topics with neither document nor word counts"
+        for k in range(K):
+            err = abs(Fraction(w[k], total) - exact[k])
+            assert err <= (1 + K * exact[k]) / total, (trial, k)
+            assert err <= Fraction(1, 2**40), (trial, k)
+            assert w[k] > 0, (trial, k)
+        for k in smoothing_only:
+            assert exact[k] < 1e-4
+            assert abs(Fraction(w[k], total) - exact[k]) <= exact[k] / 2**24, (trial, k)
+
+
+def test_draw_on_prefix_sum_boundaries():
+    # the new topic is the first whose prefix sum of weights exceeds floor(r W / 2^64): a
+    # random number that puts the target exactly on a prefix sum selects the next topic
+    K, V = 7, 50
+    o = oracle.LdaOracle(1, V, K, 1, 0, 0.3, 0.2, oracle.ESSP, 1, 1)
+    nd = np.array([3, 0, 1, 0, 5, 2, 1], np.int32)
+    nw = np.array([1, 2, 0, 0, 4, 1, 0], np.int32)
+    nk = np.array([40, 31, 12, 9, 55, 20, 8], np.int32)
+    w, total, _ = o.token_draw(nd, nw, nk, 0, 0)
+    cum = np.cumsum(np.array(w, dtype=object))
+    for k in range(K - 1):
+        # the smallest r with floor(r W / 2^64) = cum[k]
+        r = -((-int(cum[k]) << 64) // total)
+        assert (r * total) >> 64 == cum[k]
+        assert o.token_draw(nd, nw, nk, 0, r)[2] == k + 1, k
+        # one below: the target is cum[k] - 1, still topic k
+        assert o.token_draw(nd, nw, nk, 0, r - 1)[2] == k, k
+    assert o.token_draw(nd, nw, nk, 0, 0)[2] == 0
+    assert o.token_draw(nd, nw, nk, 0, 2**64 - 1)[2] == K - 1
+
+
+def test_draw_matches_the_exact_conditional_in_frequency():
+    # drawing with uniformly random r, topic frequencies follow the exact conditional
+    # (including a topic the document does not use); 200k draws, standard error <= 0.0011
+    K, V = 5, 30
+    o = oracle.LdaOracle(1, V, K, 1, 0, 0.5, 0.1, oracle.ESSP, 1, 1)
+    nd = np.array([4, 0, 2, 1, 3], np.int32)
+    nw = np.array([2, 1, 0, 1, 5], np.int32)
+    nk = np.array([30, 14, 22, 9, 41], np.int32)
+    exact = [float(x) for x in _exact_probabilities(nd, nw, nk, 4, 0.5, 0.1, V)]
+    rng = np.random.default_rng(3)
+    hits = np.zeros(K)
+    for r in rng.integers(0, 2**64, 200_000, dtype=np.uint64):
+        hits[o.token_draw(nd, nw, nk, 4, int(r))[2]] += 1
+    np.testing.assert_allclose(hits / hits.sum(), exact, atol=0.006)
+
+
+def test_load_rejects_weights_outside_the_normal_range():
+    # beta so small that the smoothing weight alpha beta / (n + V beta) is subnormal
+    o = oracle.LdaOracle(2, 5, 2, 1, 0, 1e-200, 1e-200)
+    with pytest.raises(oracle.OracleError):
+        o.load([0, 1], [0, 1], [0, 1])
 
 
 @pytest.mark.parametrize("policy", POLICIES)
