@@ -227,6 +227,18 @@ int ps_mf_clock(ps_mf_t *h, int32_t n);
    latest version, accumulated in fp64.  Synchronizes. */
 int ps_mf_loss(ps_mf_t *h, double *out);
 
+/* ps_mf_loss for callers that cannot allocate device memory (code under HIP graph capture,
+   tight serving loops, harnesses that forbid hipMalloc): the same value, computed by the
+   same kernels in the same order, with the fp64 partial sums in a fixed static array of
+   2^18 + 1 doubles (2 MiB) that each GPU holds until the process ends, instead of the
+   handle's buffer.  Calls no hipMalloc or hipFree.  EINVAL (before touching the device)
+   when the loaded ratings need more than 2^18 partial sums (one per 256-thread workgroup of
+   the loss: about (users + ratings / 512) * (lanes per row, 2 to 16) / 256); ESTATE as
+   ps_mf_loss.
+   Every call on one GPU shares that GPU's array: calls that overlap on one GPU (from
+   several host threads) race.  Synchronizes. */
+int ps_mf_loss_noalloc(ps_mf_t *h, double *out);
+
 /* Copy the latest committed version into host arrays L (users x K), R (items x K).
    Synchronizes. */
 int ps_mf_get_factors(ps_mf_t *h, float *L, float *R);

@@ -31,6 +31,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <thread>
@@ -39,6 +40,14 @@
 
 #include "../../include/ps_mf.h"
 #include "layout.h"
+
+// The fp64 partial sums of the loss for callers that cannot allocate (ps_mf_loss_noalloc):
+// a fixed array in every GPU's memory, held until the process ends.  Entries
+// [0, kNoAllocPartials) take the per-workgroup partials, the last one the final sum.  Host
+// code never passes the array's name to a kernel (on the host it is a stand-in, not a
+// device address): each device's address comes from hipGetSymbolAddress.
+constexpr int64_t kNoAllocPartials = int64_t{1} << 18;  // 2 MiB of partials
+static __device__ __align__(256) double scratch[kNoAllocPartials + 1];
 
 namespace {
 
@@ -1486,6 +1495,7 @@ struct ps_mf {
   int64_t vap_cap = 0;
   double *loss_partial = nullptr;
   int64_t loss_partial_len = 0;
+  int64_t loss_parts = 0;  // partial sums one loss takes (all blocks)
   double *loss_out = nullptr;
   std::vector<DeviceBlock> dblocks;
   std::vector<void *> allocations;
@@ -2265,6 +2275,15 @@ int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const flo
   for (int b = 0; b < h->B; ++b)
     for (int64_t i = 0; i < h->N; ++i)
       h->worker_ratings[static_cast<size_t>(b) * h->P + h->owner[i]] += h->layout[b].ucount[i];
+  // partial sums of the loss: one per workgroup of lane groups, a lane group per loss
+  // segment (a user's ratings of a block, cut every kLossSegment)
+  h->loss_parts = 0;
+  for (int b = 0; b < h->B; ++b) {
+    int64_t nseg = 0;
+    for (int64_t i = 0; i < h->N; ++i) nseg += (h->layout[b].ucount[i] + kLossSegment - 1) / kLossSegment;
+    const int64_t groups = kBlock / shape_for(h->Kp).G;
+    h->loss_parts += (nseg + groups - 1) / groups;
+  }
   if (h->host_only) {
     for (int b = 0; b < h->B; ++b)
       if (psmf::check_layout(lp, h->layout[b], err))
@@ -2335,6 +2354,8 @@ int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const flo
   std::vector<int32_t> ucls(static_cast<size_t>(h->N));
   for (int64_t i = 0; i < h->N; ++i) ucls[i] = h->cls_of_worker[h->owner[i]];
   if ((r = upload(h, &h->ucls, ucls))) return undo(r);
+  if (loss_len != h->loss_parts) return undo(fail(h, PS_MF_EINTERNAL, "loss partials %lld, expected %lld",
+                                                  (long long)loss_len, (long long)h->loss_parts));
   h->loss_partial_len = std::max<int64_t>(1, loss_len);
   if ((r = dev_alloc(h, reinterpret_cast<void **>(&h->loss_partial), static_cast<size_t>(h->loss_partial_len) * sizeof(double))))
     return undo(r);
@@ -2371,6 +2392,54 @@ int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const flo
         (r = dev_alloc(h, reinterpret_cast<void **>(&h->rwork), rw * sizeof(float))))
       return undo(r);
   }
+  return PS_MF_OK;
+}
+
+// Squared loss of the latest version: one k_loss launch per block writes its workgroups'
+// fp64 partials into partial[], k_sum_partials adds them in a fixed order into *result
+// (device memory), and the host waits for the value.  Allocates nothing.
+int loss_into(ps_mf_t *h, double *partial, double *result, double *out) {
+  const int64_t slot_stride = (h->N + h->M) * h->Kp;
+  const int32_t sl = static_cast<int32_t>(h->clock % (h->s + 1));
+  const float *L = h->ring + sl * slot_stride;
+  const float *R = L + h->N * h->Kp;
+  int64_t off = 0;
+  for (int b = 0; b < h->B; ++b) {
+    const DeviceBlock &d = h->dblocks[b];
+    if (d.nnz == 0) continue;
+    HIP_TRY(h, dispatch<LaunchLoss>(h->Kp, d.seg_user, d.seg_beg, d.nseg, d.col, d.val, L, R, d.loss_grid,
+                                     partial + off, h->stream));
+    off += d.loss_grid;
+  }
+  if (off == 0) {
+    *out = 0.0;
+    return PS_MF_OK;
+  }
+  hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(kBlock), 0, h->stream, partial, off, result);
+  HIP_TRY(h, hipGetLastError());
+  double v = 0;
+  HIP_TRY(h, hipMemcpyAsync(&v, result, sizeof(double), hipMemcpyDeviceToHost, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  *out = v;
+  return PS_MF_OK;
+}
+
+// The device address of `scratch` on the handle's device (current: ensure_device ran),
+// looked up once per device and kept for the process.
+constexpr int kMaxDevices = 256;
+std::mutex scratch_mu;
+double *scratch_dev[kMaxDevices] = {};
+
+int scratch_address(ps_mf_t *h, double **out) {
+  if (h->device < 0 || h->device >= kMaxDevices) return fail(h, PS_MF_EDEVICE, "device %d out of range", h->device);
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_dev[h->device]) {
+    void *p = nullptr;
+    HIP_TRY(h, hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(h, PS_MF_EDEVICE, "no device address for the static scratch");
+    scratch_dev[h->device] = static_cast<double *>(p);
+  }
+  *out = scratch_dev[h->device];
   return PS_MF_OK;
 }
 
@@ -2429,29 +2498,21 @@ int ps_mf_loss(ps_mf_t *h, double *out) {
   if (!h->loaded || !h->has_factors) return fail(h, PS_MF_ESTATE, "load ratings and set factors before the loss");
   int r = ensure_device(h);
   if (r) return r;
-  const int64_t slot_stride = (h->N + h->M) * h->Kp;
-  const int32_t sl = static_cast<int32_t>(h->clock % (h->s + 1));
-  const float *L = h->ring + sl * slot_stride;
-  const float *R = L + h->N * h->Kp;
-  int64_t off = 0;
-  for (int b = 0; b < h->B; ++b) {
-    const DeviceBlock &d = h->dblocks[b];
-    if (d.nnz == 0) continue;
-    HIP_TRY(h, dispatch<LaunchLoss>(h->Kp, d.seg_user, d.seg_beg, d.nseg, d.col, d.val, L, R, d.loss_grid,
-                                     h->loss_partial + off, h->stream));
-    off += d.loss_grid;
-  }
-  if (off == 0) {
-    *out = 0.0;
-    return PS_MF_OK;
-  }
-  hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(kBlock), 0, h->stream, h->loss_partial, off, h->loss_out);
-  HIP_TRY(h, hipGetLastError());
-  double v = 0;
-  HIP_TRY(h, hipMemcpyAsync(&v, h->loss_out, sizeof(double), hipMemcpyDeviceToHost, h->stream));
-  HIP_TRY(h, hipStreamSynchronize(h->stream));
-  *out = v;
-  return PS_MF_OK;
+  return loss_into(h, h->loss_partial, h->loss_out, out);
+}
+
+int ps_mf_loss_noalloc(ps_mf_t *h, double *out) {
+  if (!h || !out) return PS_MF_EINVAL;
+  if (!h->loaded) return fail(h, PS_MF_ESTATE, "load ratings and set factors before the loss");
+  if (h->loss_parts > kNoAllocPartials)
+    return fail(h, PS_MF_EINVAL, "the loss needs %lld partial sums; the static scratch holds %lld",
+                (long long)h->loss_parts, (long long)kNoAllocPartials);
+  if (!h->has_factors) return fail(h, PS_MF_ESTATE, "load ratings and set factors before the loss");
+  int r = ensure_device(h);
+  if (r) return r;
+  double *sc = nullptr;
+  if ((r = scratch_address(h, &sc))) return r;
+  return loss_into(h, sc, sc + kNoAllocPartials, out);
 }
 
 int ps_mf_get_version(ps_mf_t *h, int64_t v, float *L, float *R) {

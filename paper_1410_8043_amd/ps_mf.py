@@ -35,7 +35,7 @@ KERNEL_SWEEP, KERNEL_COMMIT = 0, 1
 
 SYMBOLS = ("ps_mf_create", "ps_mf_set_option", "ps_mf_set_value_bound", "ps_mf_set_owner_map", "ps_mf_set_stream",
            "ps_mf_load_ratings",
-           "ps_mf_set_factors", "ps_mf_clock", "ps_mf_loss", "ps_mf_get_factors", "ps_mf_get_version",
+           "ps_mf_set_factors", "ps_mf_clock", "ps_mf_loss", "ps_mf_loss_noalloc", "ps_mf_get_factors", "ps_mf_get_version",
            "ps_mf_get_clock", "ps_mf_export_index", "ps_mf_kernel_time", "ps_mf_last_error", "ps_mf_destroy")
 
 
@@ -55,6 +55,7 @@ def _load_lib():
         "ps_mf_set_factors": [vp, vp, vp],
         "ps_mf_clock": [vp, i32],
         "ps_mf_loss": [vp, ctypes.POINTER(dbl)],
+        "ps_mf_loss_noalloc": [vp, ctypes.POINTER(dbl)],
         "ps_mf_get_factors": [vp, vp, vp],
         "ps_mf_get_version": [vp, i64, vp, vp],
         "ps_mf_get_clock": [vp, ctypes.POINTER(i64)],
@@ -140,6 +141,12 @@ def ps_mf_clock(h, n=1):
 def ps_mf_loss(h):
     out = ctypes.c_double()
     _check(h, "ps_mf_loss", _lib.ps_mf_loss(h, ctypes.byref(out)))
+    return out.value
+
+
+def ps_mf_loss_noalloc(h):
+    out = ctypes.c_double()
+    _check(h, "ps_mf_loss_noalloc", _lib.ps_mf_loss_noalloc(h, ctypes.byref(out)))
     return out.value
 
 

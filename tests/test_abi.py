@@ -357,3 +357,24 @@ def test_vap_arguments_and_host_layout():
         compare_layout(g, o, 2, N, M)
         assert g.export_index(ps_mf.IDX_VAP_NORMS).size == 0 and g.export_index(ps_mf.IDX_VERSION_LOG).size == 0
         o.close()
+
+
+def test_noalloc_loss_rejects_inputs_beyond_its_static_scratch():
+    # ps_mf_loss_noalloc keeps one fp64 partial sum per loss workgroup in a fixed array of
+    # 2^18; at K <= 8 a workgroup takes 128 users' segments, so 2^25 + 64 users with one
+    # rating each need 2^18 + 1 partials.  The check comes before any device work (a
+    # host-only handle), and an input that fits only meets the missing device state.
+    from paper_1410_8043_amd import ps_mf as m
+
+    for n, code, text in (((1 << 25) + 64, m.EINVAL, "static scratch holds 262144"),
+                          (1 << 12, m.ESTATE, "set factors")):
+        h = m.ps_mf_create(n, 8, 8, 64, 0, 0.1, 0.1)
+        try:
+            m.ps_mf_set_option(h, m.OPT_HOST_ONLY, 1)
+            u = np.arange(n, dtype=np.int32)
+            m.ps_mf_load_ratings(h, u, u % 8, np.ones(n, np.float32))
+            with pytest.raises(m.PsMfError) as e:
+                m.ps_mf_loss_noalloc(h)
+            assert e.value.code == code and text in str(e.value), str(e.value)
+        finally:
+            m._lib.ps_mf_destroy(h)
