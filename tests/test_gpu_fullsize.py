@@ -1,13 +1,16 @@
 """Parity at the full 100M-rating, K=128 size in the launch configuration bench.py times.
 
-The oracle cannot run whole clocks of this workload in test time, so it computes sampled
-rows one by one: the rows of version 1 (every worker reads version 0 at clock 0, so any
-policy and any s) and, under SSP_WORST at s = 7, the rows of version 8 (clocks 0..7 all
-read version 0).  The loss at version 0 is compared in full.  The sequential step's user
+The oracle runs whole clocks of this workload in about 20 s each, too slow for test time,
+so a committed script (tests/golden/make_mf_full_golden.py) stores its loss after each of
+10 clocks and sampled rows of versions 1, 3 and 10, at s = 0, 1, 3 and 7, and the GPU runs
+the same 10 clocks against them.  The oracle also computes sampled rows one by one where
+every read is of version 0: under SSP_WORST at s = 7, the rows of version 8.  The sequential step's user
 rows of version 1 come from single-worker oracles (a worker's chain depends only on its
 own ratings and the view), and the value-bounded views are checked by properties that
 hold at any size.
 """
+import json
+import os
 import sys
 
 import numpy as np
@@ -20,6 +23,7 @@ pytestmark = pytest.mark.gpu
 
 FACTOR_TOL = 1e-4
 LOSS_RTOL = 1e-5
+UPDATE_RTOL = 1e-3  # of the oracle's largest accumulated update
 
 
 def say(msg):
@@ -63,24 +67,65 @@ def gpu_handle(spec, w, s, policy, **opts):
     return g
 
 
+@pytest.fixture(scope="module")
+def golden():
+    """The oracle's loss after clocks 0..10 and sampled rows of versions 1, 3 and 10 at
+    s = 0, 1, 3, 7 (tests/golden/make_mf_full_golden.py)."""
+    path = os.path.join(os.path.dirname(__file__), "golden", "mf_full_oracle.npz")
+    with np.load(path, allow_pickle=False) as z:
+        g = {k: z[k] for k in z.files}
+    g["meta"] = json.loads(str(g["meta"]))
+    return g
+
+
 @pytest.mark.timeout(1800)
 @pytest.mark.parametrize("s", [0, 1, 3, 7])
-def test_full_config_first_clock_sampled_rows(full, s):
-    spec, w, o, users, items = full
-    Lo, Ro = o.rows_from_v0(1, users, items)
-    say(f"full-size: s={s} SSP_LAZY, one clock")
+def test_full_config_ten_clocks_against_oracle_goldens(full, golden, s):
+    """Ten clocks of the bench configuration (SSP_LAZY: from clock 1 on, worker classes read
+    different versions when s >= 1).  After every clock the loss is within 1e-5 of the
+    oracle's; at versions 1, 3 and 10 the sampled rows (the 16 heaviest users and 16 most
+    rated items among 1,024 users and 256 items) are within 1e-4, and so that a dropped
+    term cannot hide under that bound, the accumulated update V_c - V_0 of L and of R is
+    within 1e-3 of the oracle's own largest update."""
+    spec, w, _, _, _ = full
+    meta = golden["meta"]
+    assert (meta["N"], meta["M"], meta["K"], meta["P"], meta["policy"]) == (spec.N, spec.M, spec.K, spec.P, "SSP_LAZY")
+    users, items = golden["users"], golden["items"]
+    loss_o, Lo, Ro = golden[f"loss_s{s}"], golden[f"L_s{s}"], golden[f"R_s{s}"]
+    snaps = meta["snapshots"]
+    L0, R0 = w.L0[users], w.R0[items]
+    say(f"full-size: s={s} SSP_LAZY, {meta['clocks']} clocks against the oracle's goldens")
     g = gpu_handle(spec, w, s, 0)
     try:
-        if s == 0:
-            lg, lo = g.loss(), o.loss()
-            assert abs(lg - lo) <= LOSS_RTOL * lo, (lg, lo)
-        g.clock(1)
-        L, R = g.get_version(1)
+        lg = g.loss()
+        assert abs(lg - loss_o[0]) <= LOSS_RTOL * loss_o[0], (0, lg, loss_o[0])
+        for c in range(1, meta["clocks"] + 1):
+            g.clock(1)
+            lg = g.loss()
+            rel = abs(lg - loss_o[c]) / loss_o[c]
+            assert rel <= LOSS_RTOL, (c, lg, loss_o[c])
+            if c in snaps:
+                k = snaps.index(c)
+                L, R = g.get_version(c)
+                L, R = L[users], R[items]
+                err = max(np.abs(L - Lo[k]).max(), np.abs(R - Ro[k]).max())
+                dl, dr = L - L0, R - R0
+                dlo, dro = Lo[k] - L0, Ro[k] - R0
+                ul = np.abs(dl - dlo).max() / np.abs(dlo).max()
+                ur = np.abs(dr - dro).max() / np.abs(dro).max()
+                say(f"full-size: s={s} version {c}: loss rel {rel:.2e}, max |GPU - oracle| {err:.2e}, "
+                    f"update rel L {ul:.2e} R {ur:.2e} (largest oracle update L {np.abs(dlo).max():.2e} "
+                    f"R {np.abs(dro).max():.2e})")
+                assert err <= FACTOR_TOL
+                assert ul <= UPDATE_RTOL and ur <= UPDATE_RTOL
+        from paper_1410_8043_amd import ps_mf
+
+        log = g.export_index(ps_mf.IDX_VERSION_LOG).reshape(meta["clocks"], spec.P)
     finally:
         g.close()
-    err = max(np.abs(L[users] - Lo).max(), np.abs(R[items] - Ro).max())
-    say(f"full-size: s={s} max |GPU - oracle| over {users.size} users and {items.size} items = {err:.3e}")
-    assert err <= FACTOR_TOL
+    c = np.arange(meta["clocks"])[:, None]
+    p = np.arange(spec.P)[None, :]
+    np.testing.assert_array_equal(log, np.maximum(0, c - (c + p % (s + 1)) % (s + 1)))
 
 
 @pytest.mark.timeout(1800)
