@@ -59,10 +59,15 @@ def parse():
     ap.add_argument("--strata", type=int, default=None, help="sub-epochs per clock of the seq step")
     ap.add_argument("--value-bound", type=float, default=None, help="v0 of the vap policy (v_t = v0 / sqrt(t))")
     ap.add_argument("--eta-decay", action="store_true", help="step eta / sqrt(c + 1) at clock c")
-    ap.add_argument("--cpu-sample", type=int, default=50_000_000,
+    ap.add_argument("--cpu-sample", type=int, default=10_000_000,
                     help="ratings in the oracle's timed sample (0 disables the CPU baseline)")
+    ap.add_argument("--all-s", type=int, default=1,
+                    help="1 (default): also time every other staleness bound of the configuration (one handle "
+                         "each, same ratings) and report them under config.per_s; 0: only --s")
     ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
-    ap.add_argument("--tile-bytes", type=int, default=None, help="bytes of rows per L2 tile of the sweeps")
+    ap.add_argument("--tile-bytes", type=int, default=None, help="bytes of user rows per L2 tile of the item-major sweep")
+    ap.add_argument("--item-tile-bytes", type=int, default=None,
+                    help="bytes of item rows per L2 tile of the user-major sweep (default 4 x --tile-bytes)")
     ap.add_argument("--unit-max", type=int, default=None, help="ratings per sweep work unit")
     ap.add_argument("--cells", type=int, default=None, help="1/0: LDS-staged cells for the dense part")
     ap.add_argument("--heavy-min", type=int, default=None, help="ratings from which a user goes to the cells")
@@ -80,8 +85,42 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(w, spec, K, s, policy, step, strata, value_bound, eta_decay, nsample):
-    """The oracle, single-threaded, on the ratings of a prefix of users (one clock)."""
+def host_cpu():
+    """The host CPU's model name (from /proc/cpuinfo) and the number of cores this process may use."""
+    model = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        nproc = os.cpu_count() or 1
+    return model, nproc
+
+
+def pinned_to_one_core(fn):
+    """Run fn with this process pinned to one of its allowed cores (as taskset -c would), then
+    restore the affinity; returns (fn's result, the core)."""
+    try:
+        allowed = sorted(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        return fn(), None
+    core = allowed[0]
+    os.sched_setaffinity(0, {core})
+    try:
+        return fn(), core
+    finally:
+        os.sched_setaffinity(0, set(allowed))
+
+
+def cpu_baseline(w, spec, K, s, policy, step, strata, value_bound, eta_decay, nsample, repeats=5):
+    """The oracle, single-threaded and pinned to one core, on the ratings of a prefix of users:
+    the median of `repeats` timed clocks (every clock sweeps the same ratings)."""
     import oracle
 
     order = np.argsort(w.user, kind="stable")
@@ -91,14 +130,25 @@ def cpu_baseline(w, spec, K, s, policy, step, strata, value_bound, eta_decay, ns
                       strata=strata, value_bound=value_bound, eta_decay=eta_decay)
     o.load(u, i, v)
     o.set_factors(w.L0, w.R0)
-    t0 = time.perf_counter()
-    o.clock(1)
-    dt = time.perf_counter() - t0
+
+    def timed():
+        out = []
+        for _ in range(repeats):
+            t0 = time.perf_counter()
+            o.clock(1)
+            out.append(time.perf_counter() - t0)
+        return out
+
+    times, core = pinned_to_one_core(timed)
     o.close()
+    dt = float(np.median(times))
+    model, nproc = host_cpu()
     return {"value": len(take) / dt, "unit": "rating-updates/s", "cores": 1, "kind": "oracle",
-            "sample": f"one clock over the {len(take)} ratings of users {int(u.min())}..{int(u.max())} "
-                      f"(users in id order) of the same workload, {dt:.1f} s on "
-                      f"{platform.processor() or platform.machine()}, 1 thread"}
+            "sample": f"median of {repeats} clocks, each over the {len(take)} ratings of users {int(u.min())}.."
+                      f"{int(u.max())} (users in id order) of the same workload: {dt:.2f} s per clock "
+                      f"(all: {', '.join(f'{x:.2f}' for x in times)} s); 1 thread pinned to core {core} of "
+                      f"{nproc} on {model}",
+            "host": {"cpu": model, "nproc": nproc, "pinned_core": core}}
 
 
 def measured_traffic(path, config, s, policy, step):
@@ -132,18 +182,24 @@ def lda_cpu_baseline(corpus, spec, P, s, policy, seconds, max_tokens=8_000_000):
     o = oracle.LdaOracle(D, spec.V, spec.K, P, s, spec.alpha, spec.beta, policy, spec.B, spec.seed)
     o.load(corpus.doc[:n], corpus.word[:n], corpus.z0[:n])
     sizes = [o.export(oracle.LDA_BLOCK_ORDER, b).size for b in range(spec.B)]
-    clocks, tokens = 0, 0
-    t0 = time.perf_counter()
-    while clocks == 0 or time.perf_counter() - t0 < seconds:
-        o.clock(1)
-        tokens += sizes[clocks % spec.B]
-        clocks += 1
-    dt = time.perf_counter() - t0
+
+    def timed():
+        clocks, tokens = 0, 0
+        t0 = time.perf_counter()
+        while clocks == 0 or time.perf_counter() - t0 < seconds:
+            o.clock(1)
+            tokens += sizes[clocks % spec.B]
+            clocks += 1
+        return clocks, tokens, time.perf_counter() - t0
+
+    (clocks, tokens, dt), core = pinned_to_one_core(timed)
     o.close()
+    model, nproc = host_cpu()
     what = "the same corpus" if n == corpus.ntok else f"the first {D} documents ({n} tokens) of the same corpus"
     return {"value": tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"the first {clocks} clocks of {what} with the same settings ({tokens} token draws), "
-                      f"{dt:.1f} s on {platform.processor() or platform.machine()}, 1 thread"}
+                      f"{dt:.1f} s, 1 thread pinned to core {core} of {nproc} on {model}",
+            "host": {"cpu": model, "nproc": nproc, "pinned_core": core}}
 
 
 def lda_main(args):
@@ -244,55 +300,35 @@ def lda_main(args):
     print(json.dumps(line), flush=True)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the multi-GPU path is a design, not part of this build)", file=sys.stderr)
-        sys.exit(2)
-    if args.workload == "lda":
-        return lda_main(args)
-    if args.policy is None:
-        args.policy = "lazy"
-    if args.traffic_file is None:
-        name = "seq_full_traffic.json" if args.step == "seq" else "sweep_full_traffic.json"
-        args.traffic_file = os.path.join(ROOT, "profiles", name)
+def measure_mf(args, spec, w, s, policy, step, stream, announce=True):
+    """Build a handle for staleness s, run the warmup and the timed clocks, and return what
+    the JSON line reports about them."""
     import torch
 
-    from paper_1410_8043_amd import ps_mf, synth
+    from paper_1410_8043_amd import ps_mf
 
-    spec = synth.CONFIGS[args.config]
-    s = args.s if args.s is not None else (3 if 3 in spec.s_values else spec.s_values[0])
-    policy = POLICIES[args.policy]
-    step = STEPS[args.step]
     seq = args.step == "seq"
-    torch.cuda.set_device(0)
-    t_gen = time.perf_counter()
-    w = synth.generate(spec)
-    t_gen = time.perf_counter() - t_gen
-    print(f"[bench] generated {args.config}: {w.nnz} ratings in {t_gen:.1f} s", file=sys.stderr, flush=True)
-    stream = torch.cuda.current_stream()
     g = ps_mf.PsMf(spec.N, spec.M, spec.K, spec.P, s, spec.eta, spec.lam, policy=policy, step=step, strata=args.strata,
                    value_bound=args.value_bound, eta_decay=args.eta_decay, B=spec.B,
                    mb_seed=spec.seed, timing=not args.no_timing, stream=stream, tile_bytes=args.tile_bytes,
                    unit_max=args.unit_max, cells=args.cells, heavy_min=args.heavy_min, hot_steps=args.hot_steps,
-                   two_streams=args.two_streams, dense_min=args.dense_min)
+                   two_streams=args.two_streams, dense_min=args.dense_min, item_tile_bytes=args.item_tile_bytes)
     t_load = time.perf_counter()
     g.load_ratings(w.user, w.item, w.val)
     g.set_factors(w.L0, w.R0)
     t_load = time.perf_counter() - t_load
-    print(f"[bench] layout + upload {t_load:.1f} s", file=sys.stderr, flush=True)
+    print(f"[bench] s={s}: layout + upload {t_load:.1f} s", file=sys.stderr, flush=True)
     nnz_clock = w.nnz / spec.B  # mean ratings per clock (exact for B=1)
     split = sum(g.export_index(ps_mf.IDX_SPLIT, b) for b in range(spec.B))
-    if seq:
+    if announce and seq:
         print(f"[bench] sequential step: {int(split[0])} chains, {int(split[1])} user runs, {int(split[2])} ratings "
               f"over {spec.B} blocks", file=sys.stderr, flush=True)
-    else:
+    elif announce:
         print(f"[bench] ratings per direction in dense tiles / LDS cells / L2 units: {split[:3].tolist()} "
               f"(user-major), {split[3:6].tolist()} (item-major); partial rows {split[6:].tolist()}",
               file=sys.stderr, flush=True)
 
-    if args.copy_calibration_bytes > 0:
+    if announce and args.copy_calibration_bytes > 0:
         src = torch.ones(args.copy_calibration_bytes // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         torch.mul(src, 2.0, out=dst)
@@ -308,77 +344,132 @@ def main():
     g.clock(args.steps)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    print(f"[bench] {args.steps} clocks in {dt * 1e3:.2f} ms", file=sys.stderr, flush=True)
+    print(f"[bench] s={s}: {args.steps} clocks in {dt * 1e3:.2f} ms", file=sys.stderr, flush=True)
     loss = g.loss()
     # staleness profile of the clocks run (Fig. 1 left): share of parameter reads per clock
     # differential -(d+1)
     stale = g.export_index(ps_mf.IDX_STALENESS)
     profile = {str(-(d + 1)): round(float(x) / max(1, int(stale.sum())), 4) for d, x in enumerate(stale)}
-
-    value = nnz_clock * args.steps / dt
+    out = {"s": s, "dt": dt, "value": nnz_clock * args.steps / dt, "nnz_clock": nnz_clock, "split": split,
+           "loss": loss, "profile": profile, "roof": None, "extra": {}}
     K = spec.K
-    roof = None
-    extra = {}
     if not args.no_timing:
         ms_s, n_s = g.kernel_time(ps_mf.KERNEL_SWEEP)
         ms_c, n_c = g.kernel_time(ps_mf.KERNEL_COMMIT)
         sweep_ms = (ms_s - base_sweep[0]) / (n_s - base_sweep[1])
         commit_ms = (ms_c - base_commit[0]) / (n_c - base_commit[1])
         traffic = measured_traffic(args.traffic_file, args.config, s, args.policy, args.step)
+        # compulsory HBM bytes of one clock: each rating once (int32 item + fp32 value),
+        # the view version read, the base version read when s > 0, the new version written
+        table = (spec.N + spec.M) * K * 4
+        hbm_bytes = 8 * nnz_clock + table * (2 if s == 0 else 3)
         if seq:
-            # each rating reads and writes its item row in the worker's copy (2 x 4K bytes) and
-            # reads its 16-byte record; each user run reads and writes the user row
-            runs_clock = float(split[1]) / spec.B
-            bytes_clock = nnz_clock * (8.0 * K + 16) + runs_clock * 8.0 * K
-            achieved = bytes_clock / (sweep_ms * 1e-3) / 1e9  # GB/s
+            # the sequential step is HBM-bound: priced against the compulsory bytes of a clock
+            # (the layout's own round trips of the workers' row copies are not algorithmic)
+            achieved = hbm_bytes / (sweep_ms * 1e-3) / 1e9  # GB/s
             roof = {"kernel": "k_seq (one launch per sub-epoch)", "bound": "hbm", "achieved": round(achieved, 1),
-                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 5),
                     "traffic": traffic}
+            # what the layout moves: each rating reads and writes its item row in the worker's
+            # copy (2 x 4K bytes) and reads its 16-byte record; each user run reads and writes
+            # the user row
+            runs_clock = float(split[1]) / spec.B
+            moved = nnz_clock * (8.0 * K + 16) + runs_clock * 8.0 * K
+            out["extra"]["layout_bytes_frac"] = round(moved / (sweep_ms * 1e-3) / (PEAK_HBM_GBS * 1e9), 4)
         else:
             flops = 6.0 * K * nnz_clock                  # 3K fp32 FMA per rating update
             achieved = flops / (sweep_ms * 1e-3) / 1e12  # TFLOP/s
             roof = {"kernel": "sweep (k_dense, k_cells and k_units, concurrent)", "bound": "alu",
                     "achieved": round(achieved, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), "traffic": traffic}
-        # compulsory HBM bytes of one clock: each rating once (int32 item + fp32 value),
-        # the view version read, the base version read when s > 0, the new version written
-        table = (spec.N + spec.M) * K * 4
-        hbm_bytes = 8 * nnz_clock + table * (2 if s == 0 else 3)
-        extra = {"sweep_ms": round(sweep_ms, 4), "commit_ms": round(commit_ms, 4),
-                 "hbm_algorithmic_frac": round(hbm_bytes / (dt / args.steps) / (PEAK_HBM_GBS * 1e9), 4)}
+        out["roof"] = roof
+        out["extra"].update({"sweep_ms": round(sweep_ms, 4), "commit_ms": round(commit_ms, 4),
+                             "hbm_algorithmic_frac": round(hbm_bytes / (dt / args.steps) / (PEAK_HBM_GBS * 1e9), 4)})
     g.close()
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU path is a design, not part of this build)", file=sys.stderr)
+        sys.exit(2)
+    if args.workload == "lda":
+        return lda_main(args)
+    if args.policy is None:
+        args.policy = "lazy"
+    if args.traffic_file is None:
+        name = "seq_full_traffic.json" if args.step == "seq" else "sweep_full_traffic.json"
+        args.traffic_file = os.path.join(ROOT, "profiles", name)
+    import torch
+
+    from paper_1410_8043_amd import synth
+
+    spec = synth.CONFIGS[args.config]
+    s = args.s if args.s is not None else (3 if 3 in spec.s_values else spec.s_values[0])
+    policy = POLICIES[args.policy]
+    step = STEPS[args.step]
+    seq = args.step == "seq"
+    torch.cuda.set_device(0)
+    t_gen = time.perf_counter()
+    w = synth.generate(spec)
+    t_gen = time.perf_counter() - t_gen
+    print(f"[bench] generated {args.config}: {w.nnz} ratings in {t_gen:.1f} s", file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream()
+    main_run = measure_mf(args, spec, w, s, policy, step, stream)
+    # the other staleness bounds of the configuration, each on its own handle over the same
+    # ratings, with the same warmup and timed clocks
+    per_s = {}
+    others = [x for x in spec.s_values if x != s] if args.all_s else []
+    for x in others:
+        r = measure_mf(args, spec, w, x, policy, step, stream, announce=False)
+        per_s[str(x)] = {"value": round(r["value"], 1), "ms_per_step": round(r["dt"] / args.steps * 1e3, 4),
+                         **({k: r["extra"][k] for k in ("sweep_ms", "commit_ms")} if r["extra"] else {}),
+                         **({"frac": r["roof"]["frac"]} if r["roof"] else {}),
+                         "loss_after": r["loss"] if np.isfinite(r["loss"]) else None}
+    if per_s:
+        r = main_run
+        per_s[str(s)] = {"value": round(r["value"], 1), "ms_per_step": round(r["dt"] / args.steps * 1e3, 4),
+                         **({k: r["extra"][k] for k in ("sweep_ms", "commit_ms")} if r["extra"] else {}),
+                         **({"frac": r["roof"]["frac"]} if r["roof"] else {}),
+                         "loss_after": r["loss"] if np.isfinite(r["loss"]) else None}
+        per_s = {k: per_s[k] for k in sorted(per_s, key=int)}
 
     cpu = None
     if args.cpu_sample > 0:
         print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, spec, K, s, policy, step, args.strata, args.value_bound, args.eta_decay,
+        cpu = cpu_baseline(w, spec, spec.K, s, policy, step, args.strata, args.value_bound, args.eta_decay,
                            min(args.cpu_sample, w.nnz))
 
+    r = main_run
+    loss, split = r["loss"], r["split"]
     line = {
         "metric": "rating-updates/sec at K=128, 100M ratings (1 GPU); % of HBM roofline",
-        "value": round(value, 1),
+        "value": round(r["value"], 1),
         "unit": "rating-updates/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(dt / args.steps * 1e3, 4),
+        "ms_per_step": round(r["dt"] / args.steps * 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded, Netflix-shaped)",
-        "config": {"workload": f"{args.config}: {spec.N} users x {spec.M} items, {w.nnz} ratings, K={K}, "
+        "config": {"workload": f"{args.config}: {spec.N} users x {spec.M} items, {w.nnz} ratings, K={spec.K}, "
                                f"P={spec.P}, s={s}, policy={args.policy}, B={spec.B}, eta={spec.eta}, "
                                f"lambda={spec.lam}" + (f", step=seq, strata={args.strata or 256}" if seq else "") +
                                (f", v0={args.value_bound}" if args.policy == "vap" else "") +
                                (", eta/sqrt(t)" if args.eta_decay else ""),
-                   "global_batch": int(nnz_clock), "parallelism": "1 GPU, P logical workers",
+                   "global_batch": int(r["nnz_clock"]), "parallelism": "1 GPU, P logical workers",
                    # null when the run diverged (strict JSON has no NaN)
                    "loss_after": loss if np.isfinite(loss) else None,
                    **({"chains_runs_ratings": [int(x) for x in split[:3]]} if seq else
                       {"dense_cells_units": [int(x) for x in split[:3]]}),
-                   "staleness_profile": profile, **extra},
-        "roofline": roof,
+                   "staleness_profile": r["profile"], **r["extra"],
+                   **({"per_s": per_s} if per_s else {})},
+        "roofline": r["roof"],
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

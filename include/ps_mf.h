@@ -108,6 +108,17 @@ typedef struct ps_mf ps_mf_t;
                                    launches once per (block, view schedule) into a HIP graph on the
                                    handle's stream and replay it (not with PS_MF_OPT_ETA_DECAY);
                                    0: launch them one by one */
+#define PS_MF_OPT_ITEM_TILE_BYTES 17 /* bytes of item rows per tile of the user-major sweep's work
+                                        units (each tile is read from one XCD's L2); -1 (default):
+                                        4 x PS_MF_OPT_TILE_BYTES; >= 1 otherwise */
+#define PS_MF_OPT_DEVICE 18     /* HIP device ordinal the handle runs on; -1 (default): the device
+                                   current at the handle's first device call.  A device that does
+                                   not exist makes that call fail with PS_MF_EDEVICE */
+#define PS_MF_OPT_POISON 19     /* debug, fixed-view steps only: 1 fills, before every commit, each
+                                   row of the new version's ring slot that the commit does not
+                                   read with NaN, so a row the commit failed to write shows as
+                                   NaN (s = 0: the commit updates in place; nothing is filled);
+                                   0 (default): off.  With PS_MF_STEP_SEQ load fails (EINVAL) */
 
 /* Views (Section 3.2 SSP condition; Section 4 ESSPTable).  The table-level policies give
    worker p at clock c one whole version v = max(0, c - d):

@@ -965,6 +965,35 @@ __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, 
     commit_item(ca, static_cast<int64_t>(blockIdx.x) - grid_users, red);
 }
 
+// Debug check of the commit (PS_MF_OPT_POISON): before the commit of clock c, every row of
+// the new version's slot that the commit will not read is set to NaN, so that a row the
+// commit fails to write stays NaN.  The commit reads the new slot (which held version c-s)
+// where a view is version c-s: a user row with ratings whose view slot is the new slot, an
+// item row with a rating by a worker class whose view slot is the new slot.  One thread
+// per float4 of the slot.
+__global__ __launch_bounds__(kBlock) void k_poison(FinalArgs fa, CommitArgs ca) {
+  const int64_t q4 = fa.Kp / 4;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (idx >= (fa.users + ca.items) * q4) return;
+  const int64_t row = idx / q4;
+  bool read = false;
+  if (row < fa.users) {
+    const int64_t i = row;
+    read = fa.ucount[i] > 0 && (fa.rs_u ? fa.rs_u[i] : fa.cls_slot[fa.ucls[i]]) == fa.slot_n;
+  } else {
+    const int64_t j = row - fa.users;
+    if (ca.icount[j] > 0)
+      for (int q = 0; q < ca.nclass; ++q)
+        if (ca.icount_cls[j * ca.nclass + q] > 0 &&
+            (ca.rs_i ? ca.rs_i[q * ca.items + j] : ca.cls_slot[q]) == fa.slot_n)
+          read = true;
+  }
+  if (!read) {
+    const float nan = __int_as_float(0x7fc00000);
+    reinterpret_cast<float4 *>(fa.ring)[fa.slot_n * (fa.slot_stride / 4) + idx] = make_float4(nan, nan, nan, nan);
+  }
+}
+
 // ------------------------------------------------------------------ value-bounded views
 // VAP (Section 3's condition on in-transit updates): at clock c every worker reads the
 // stalest version v = c - d, d <= min(c, s), with |x_c - x_v|_inf <= v0 / sqrt(c + 1).
@@ -1448,7 +1477,9 @@ struct ps_mf {
   int32_t policy = PS_MF_SSP_LAZY, step = PS_MF_STEP_ROWMEAN, B = 1;
   uint64_t seed = 0;
   bool host_only = false, timing = false;
-  int64_t tile_bytes = 6 << 20;  // rows per L2 tile of the sweeps, in bytes
+  int64_t tile_bytes = 6 << 20;  // rows per L2 tile of the item-major sweep, in bytes
+  int64_t item_tile_bytes = -1;  // rows per L2 tile of the user-major sweep (-1: 4 x tile_bytes)
+  bool poison = false;           // debug: NaN in the rows of the new slot the commit does not read
   int32_t unit_max = 256;
   bool cells = true;             // stage the dense part (heavy users) through LDS
   int64_t heavy_min = -1;        // ratings from which a user goes to the cells (-1: automatic)
@@ -1703,7 +1734,13 @@ int ensure_device(ps_mf_t *h) {
     HIP_TRY(h, hipGetDevice(&dev));
     h->device = dev;
   }
-  HIP_TRY(h, hipSetDevice(h->device));
+  {
+    const hipError_t e = hipSetDevice(h->device);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();  // not sticky: leave no error for the caller's next HIP call
+      return fail(h, PS_MF_EDEVICE, "hipSetDevice(%d): %s", h->device, hipGetErrorString(e));
+    }
+  }
   if (!h->stream) {
     if (h->user_stream) {
       h->stream = h->user_stream;
@@ -2053,6 +2090,12 @@ int one_clock(ps_mf_t *h) {
   ca.rowmean = rowmean;
   ca.rs_i = per_row_policy(h) ? h->slot_i : nullptr;
   const int64_t grid_users = (nfin + kBlock - 1) / kBlock, grid_items = h->M;
+  if (h->poison && slot_n != slot_c) {
+    const int64_t n4 = (h->N + h->M) * (h->Kp / 4);
+    hipLaunchKernelGGL(k_poison, dim3(static_cast<unsigned>((n4 + kBlock - 1) / kBlock)), dim3(kBlock), 0, h->stream,
+                       fa, ca);
+    HIP_TRY(h, hipGetLastError());
+  }
   hipLaunchKernelGGL(k_commit, dim3(static_cast<unsigned>(grid_users + grid_items)), dim3(kBlock), 0, h->stream, fa,
                      ca, static_cast<int32_t>(grid_users));
   HIP_TRY(h, hipGetLastError());
@@ -2156,6 +2199,18 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
     case PS_MF_OPT_SEQ_GRAPHS:
       h->seq_graphs = value != 0;
       return PS_MF_OK;
+    case PS_MF_OPT_ITEM_TILE_BYTES:
+      if (value < 1 && value != -1) return fail(h, PS_MF_EINVAL, "item tile bytes must be >= 1 or -1");
+      h->item_tile_bytes = value;
+      return PS_MF_OK;
+    case PS_MF_OPT_DEVICE:
+      if (value < -1 || value > 4095) return fail(h, PS_MF_EINVAL, "device ordinal must be in [-1, 4095]");
+      if (h->stream) return fail(h, PS_MF_ESTATE, "the device is already in use");
+      h->device = static_cast<int>(value);
+      return PS_MF_OK;
+    case PS_MF_OPT_POISON:
+      h->poison = value != 0;
+      return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
   }
@@ -2216,6 +2271,8 @@ namespace {
 int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const float *value, int64_t n) {
   if (h->loaded) return fail(h, PS_MF_ESTATE, "ratings are already loaded");
   if (n < 0 || (n > 0 && (!user || !item || !value))) return fail(h, PS_MF_EINVAL, "bad rating arrays");
+  if (h->poison && h->step == PS_MF_STEP_SEQ)
+    return fail(h, PS_MF_EINVAL, "the poison check covers the fixed-view commit only, not PS_MF_STEP_SEQ");
   if (n > 0x7fffffffLL) return fail(h, PS_MF_EINVAL, "at most 2^31-1 ratings");
   const bool seq = h->step == PS_MF_STEP_SEQ;
   if (h->owner.empty()) {
@@ -2241,7 +2298,9 @@ int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const flo
   // item-major tiles of user rows are sized for one XCD's L2; the user-major sweep takes
   // 4x larger item tiles: fewer units and partial rows per light user measured faster
   lp.tile_rows_user = std::max<int64_t>(64, h->tile_bytes / (static_cast<int64_t>(h->Kp) * 4));
-  lp.tile_rows_item = 4 * lp.tile_rows_user;
+  lp.tile_rows_item = h->item_tile_bytes > 0
+                          ? std::max<int64_t>(64, h->item_tile_bytes / (static_cast<int64_t>(h->Kp) * 4))
+                          : 4 * lp.tile_rows_user;
   lp.unit_max = h->unit_max;
   if (h->cells) {
     // cells: one 1024-thread workgroup per cell, a 128 KiB LDS sub-tile of ts rows; a user

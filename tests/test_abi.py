@@ -378,3 +378,49 @@ def test_noalloc_loss_rejects_inputs_beyond_its_static_scratch():
             assert e.value.code == code and text in str(e.value), str(e.value)
         finally:
             m._lib.ps_mf_destroy(h)
+
+
+def test_tile_device_and_poison_options_are_checked():
+    from paper_1410_8043_amd import ps_mf as m
+
+    h = m.ps_mf_create(4, 3, 2, 2, 1, 0.1, 0.1)
+    try:
+        for key, val in [(m.OPT_ITEM_TILE_BYTES, 0), (m.OPT_ITEM_TILE_BYTES, -2), (m.OPT_DEVICE, -2),
+                         (m.OPT_DEVICE, 4096)]:
+            with pytest.raises(m.PsMfError) as e:
+                m.ps_mf_set_option(h, key, val)
+            assert e.value.code == m.EINVAL
+        m.ps_mf_set_option(h, m.OPT_ITEM_TILE_BYTES, 1 << 20)
+        m.ps_mf_set_option(h, m.OPT_ITEM_TILE_BYTES, -1)
+        m.ps_mf_set_option(h, m.OPT_DEVICE, 0)
+        m.ps_mf_set_option(h, m.OPT_DEVICE, -1)
+    finally:
+        m.ps_mf_destroy(h)
+    # the poison check covers the fixed-view commit only: refused with the sequential step
+    with m.PsMf(4, 3, 2, 2, 1, 0.1, 0.1, step=m.STEP_SEQ, poison=True, host_only=True) as g:
+        with pytest.raises(m.PsMfError) as e:
+            g.load_ratings(np.array([0, 3]), np.array([2, 0]), np.array([1.0, 5.0]))
+        assert e.value.code == m.EINVAL and "poison" in str(e.value)
+    with m.PsMf(4, 3, 2, 2, 1, 0.1, 0.1, poison=True, host_only=True) as g:
+        g.load_ratings(np.array([0, 3]), np.array([2, 0]), np.array([1.0, 5.0]))
+
+
+@pytest.mark.parametrize("item_tile_bytes", [256, 16384])
+def test_user_major_item_tiles_split_the_units(item_tile_bytes):
+    # smaller item tiles cut each user's units at item-range boundaries (tiles double while
+    # units would average fewer than 16 ratings): more units and partial rows, the same
+    # ratings; the layout's own self-check (host-only) passes
+    from paper_1410_8043_amd import ps_mf as m
+
+    N, M, K = 2000, 1000, 16
+    rng = np.random.default_rng(17)
+    cells = rng.choice(N * M, 400_000, replace=False)
+    u, i = (cells // M).astype(np.int32), (cells % M).astype(np.int32)
+    v = rng.integers(1, 6, cells.size).astype(np.float32)
+    out = []
+    for itb in (None, item_tile_bytes):
+        with m.PsMf(N, M, K, 8, 3, 0.01, 0.05, host_only=True, item_tile_bytes=itb, dense_min=0, cells=0) as g:
+            g.load_ratings(u, i, v)
+            out.append(g.export_index(m.IDX_SPLIT))
+    assert out[0][2] == out[1][2] == cells.size
+    assert out[0][6] == N and out[1][6] >= 4 * N
