@@ -140,6 +140,7 @@ __device__ __forceinline__ void store_row_sw(float *__restrict__ row, const floa
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_char;
 
 // Data that a clock touches once -- rating streams, stationary rows, partial rows, dense
 // values and residuals -- may be loaded and stored non-temporally, so that it does not
@@ -348,6 +349,7 @@ struct CellArgs {
   int64_t slot_stride, x_off, y_off;
   int32_t ts;
   float *partial;
+  const float *zero;           // Kp zeros: the source of empty staged rows
   const int32_t *rs_x, *rs_y;  // per-row policies (see UnitArgs)
   int64_t rs_x_cls, rs_y_cls;
 };
@@ -368,7 +370,6 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
   const bool per_row = c.rs_x != nullptr;
   const int sv = per_row ? 0 : c.cls_slot[cls];
   const float *__restrict__ V = c.ring + sv * c.slot_stride;
-  const float4 *__restrict__ Y4 = reinterpret_cast<const float4 *>(V + c.y_off);
   const int32_t xr = c.cell_x[cell * NG + grp];
   const int rot = swizzled<G, E>() ? (grp & 1) : 0;
   const uint32_t lane_bytes = static_cast<uint32_t>(rot * G + g) * 16u;  // < 32 * G: below a row's size
@@ -381,16 +382,41 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
     load_row_sw_once<G, E>(x, c.ring + xs * c.slot_stride + c.x_off + static_cast<int64_t>(xr) * Kp, g, rot);
   }
   const int32_t k0 = c.cell_step_ptr[cell], k1 = c.cell_step_ptr[cell + 1];
+  // the sub-tile holds ts * Q4 = kTileFloats / 4 chunks of 16 bytes: NIT per thread, chunk
+  // idx = it * kSweepBlock + threadIdx.x (row idx / Q4, column chunk idx % Q4)
+  constexpr int NIT = kTileFloats / 4 / kSweepBlock;
+  static_assert(NIT * kSweepBlock * 4 == kTileFloats, "whole chunks per thread");
+  const int wave = static_cast<int>(threadIdx.x) >> 6;
+  // the row numbers of this thread's chunks of step k (independent loads); they are loaded
+  // one step ahead, during the previous step's sweep, and the step ids two steps ahead
+  int32_t rr[NIT];
+  auto load_rows = [&](int32_t step_id) {
+    const int32_t *rows = c.step_rows + static_cast<int64_t>(step_id) * c.ts;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) rr[it] = rows[(it * kSweepBlock + static_cast<int>(threadIdx.x)) / Q4];
+  };
+  int32_t next_id = 0;
+  if (k0 < k1) {
+    load_rows(c.cell_steps[k0]);
+    if (k0 + 1 < k1) next_id = c.cell_steps[k0 + 1];
+  }
   for (int32_t k = k0; k < k1; ++k) {
-    const int32_t *rows = c.step_rows + static_cast<int64_t>(c.cell_steps[k]) * c.ts;
+    // the direct global-to-LDS loads back to back: a wavefront's load of iteration it
+    // writes the 64 consecutive chunks it * kSweepBlock + 64 * wave + lane of the tile
+    const float *base[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      base[it] = V + c.y_off;
+      if (per_row && rr[it] >= 0)
+        base[it] = c.ring + static_cast<int64_t>(c.rs_y[cls * c.rs_y_cls + rr[it]]) * c.slot_stride + c.y_off;
+    }
     __syncthreads();  // the previous sub-tile is no longer read
-    for (int idx = threadIdx.x; idx < c.ts * Q4; idx += kSweepBlock) {
-      const int32_t r = rows[idx / Q4];
-      const float4 *src = Y4;
-      if (per_row && r >= 0)
-        src = reinterpret_cast<const float4 *>(c.ring + static_cast<int64_t>(c.rs_y[cls * c.rs_y_cls + r]) * c.slot_stride +
-                                               c.y_off);
-      tile[idx] = r >= 0 ? src[static_cast<int64_t>(r) * Q4 + idx % Q4] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int idx = it * kSweepBlock + static_cast<int>(threadIdx.x);
+      const float *src = (rr[it] >= 0 ? base[it] + static_cast<int64_t>(rr[it]) * Kp : c.zero) + 4 * (idx % Q4);
+      lds_char *dst = (lds_char *)(tile) + 16 * (it * kSweepBlock + 64 * wave);  // generic -> LDS address space
+      __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
     }
     const int32_t beg = c.run_beg[static_cast<int64_t>(k) * NG + grp];
     const int n = c.run_len[static_cast<int64_t>(k) * NG + grp];
@@ -405,7 +431,12 @@ __device__ __forceinline__ void run_cell(const CellArgs &c, int64_t cell, float4
       nv0 = ld_once(reinterpret_cast<const f32x4 *>(lv));
       nv1 = ld_once(reinterpret_cast<const f32x4 *>(lv + 4));
     }
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's chunks have landed in LDS
     __syncthreads();
+    if (k + 1 < k1) {  // the next step's row numbers, while this one is swept
+      load_rows(next_id);
+      if (k + 2 < k1) next_id = c.cell_steps[k + 2];
+    }
     for (int t0 = 0; t0 < n; t0 += 8) {
       if constexpr (E >= 32) {  // 512-wide rows: no registers to spare for the prefetch
         if (t0 > 0) {
@@ -555,7 +586,26 @@ __device__ __forceinline__ float vec_at(const typename VecOf<C4>::T &v, int c) {
   else return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
 }
 
-typedef __attribute__((address_space(3))) char lds_char;
+// 4 x 4 transpose across the four lanes of a DPP quad: lane b of the quad holds row b in
+// x[0..3] and returns column b (element r from lane r).  Two exchange stages: partners
+// b ^ 1 swap the off-diagonal entries of each 2 x 2 block, then partners b ^ 2 swap the
+// off-diagonal 2 x 2 blocks.  Every lane of the wavefront must be active.
+__device__ __forceinline__ float dpp_quad_xor1(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float dpp_quad_xor2(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, true));
+}
+__device__ __forceinline__ f32x4 quad_transpose(f32x4 x, int b) {
+  const bool odd = (b & 1) != 0, hi = (b & 2) != 0;
+  const float p0 = dpp_quad_xor1(odd ? x[0] : x[1]);
+  const float p1 = dpp_quad_xor1(odd ? x[2] : x[3]);
+  if (odd) { x[0] = p0; x[2] = p1; } else { x[1] = p0; x[3] = p1; }
+  const float q0 = dpp_quad_xor2(hi ? x[0] : x[2]);
+  const float q1 = dpp_quad_xor2(hi ? x[1] : x[3]);
+  if (hi) { x[0] = q0; x[1] = q1; } else { x[2] = q0; x[3] = q1; }
+  return x;
+}
 
 // Stage the 64 y rows of step k into an LDS buffer with direct global-to-LDS loads
 // (global_load_lds_dwordx4): the loads of one wavefront write 64 consecutive 16-byte
@@ -563,21 +613,35 @@ typedef __attribute__((address_space(3))) char lds_char;
 // swizzle places at physical chunk p = 256 m + 64 w + l.  Rows -1 (past the end of a
 // ragged tile) read a zero row.  Completion is waited for (vmcnt) before the barrier that
 // hands the buffer to the readers.
+// The staged row number of each of this thread's chunks of step k (independent loads).
 template <int Kp>
-__device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__restrict__ Y, int cls, int64_t k,
-                                            float4 *lds_buf) {
+__device__ __forceinline__ void dense_rows(const DenseArgs &a, int64_t k, int32_t (&r)[Kp / 16]) {
   constexpr int H = Kp / 4;
-  constexpr int SW = H < 16 ? H : 16;
   const int32_t *rows = a.step_rows + k * kDenseRowsDev;
   const int lane = static_cast<int>(threadIdx.x) & 63, w = static_cast<int>(threadIdx.x) >> 6;
 #pragma unroll
-  for (int m = 0; m < Kp / 16; ++m) {
+  for (int m = 0; m < Kp / 16; ++m) r[m] = rows[(kDenseThreads * m + 64 * w + lane) / H];
+}
+
+template <int Kp>
+__device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__restrict__ Y, int cls,
+                                            const int32_t (&r)[Kp / 16], float4 *lds_buf) {
+  constexpr int H = Kp / 4;
+  constexpr int SW = H < 16 ? H : 16;
+  constexpr int NM = Kp / 16;
+  const int lane = static_cast<int>(threadIdx.x) & 63, w = static_cast<int>(threadIdx.x) >> 6;
+  // the loads into LDS back to back (the row numbers were loaded beforehand)
+  const float *base[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    base[m] = Y;
+    if (a.rs_y && r[m] >= 0) base[m] = a.ring + static_cast<int64_t>(a.rs_y[cls * a.rs_y_cls + r[m]]) * a.slot_stride + a.y_off;
+  }
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
     const int p = kDenseThreads * m + 64 * w + lane;
     const int y = p / H, h = (p % H) ^ (y & (SW - 1));
-    const int32_t r = rows[y];
-    const float *base = Y;
-    if (a.rs_y && r >= 0) base = a.ring + static_cast<int64_t>(a.rs_y[cls * a.rs_y_cls + r]) * a.slot_stride + a.y_off;
-    const float *src = (r >= 0 ? base + static_cast<int64_t>(r) * Kp : a.zero) + 4 * h;
+    const float *src = (r[m] >= 0 ? base[m] + static_cast<int64_t>(r[m]) * Kp : a.zero) + 4 * h;
     lds_char *dst = (lds_char *)(lds_buf) + 16 * (kDenseThreads * m + 64 * w);  // generic -> LDS address space
     __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
   }
@@ -600,7 +664,13 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
   const float *__restrict__ X = V + a.x_off;
   const float *__restrict__ Y = V + a.y_off;
   const int64_t k0 = a.cell_step_ptr[cell], k1 = a.cell_step_ptr[cell + 1];
-  if (k0 < k1) dense_stage<Kp>(a, Y, cls, k0, lds0);
+  // row numbers of the next step to stage (loaded a step ahead of their staging)
+  int32_t rnext[NQ];
+  if (k0 < k1) {
+    dense_rows<Kp>(a, k0, rnext);
+    dense_stage<Kp>(a, Y, cls, rnext, lds0);
+    if (k0 + 1 < k1) dense_rows<Kp>(a, k0 + 1, rnext);
+  }
   // stationary rows in the B-operand layout of GEMM 1: xb[q] = X[16w + i][16q + 4g .. +3]
   f32x4 xb[NQ];
   if constexpr (!FromE) {
@@ -627,7 +697,8 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
   auto step = [&](int64_t k, const float4 *T4, float4 *nextbuf) {
     const bool more = k + 1 < k1;
     if (more) {  // the next step's rows (into the other buffer) and values
-      dense_stage<Kp>(a, Y, cls, k + 1, nextbuf);
+      dense_stage<Kp>(a, Y, cls, rnext, nextbuf);
+      if (k + 2 < k1) dense_rows<Kp>(a, k + 2, rnext);
 #pragma unroll
       for (int yb = 0; yb < 4; ++yb) dnext[yb] = ld_once(dv + ((k + 1) * 16 + w * 4 + yb) * 64 + lane);
     }
@@ -664,17 +735,24 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
           s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, xb[q][3], s1, 0, 0, 0);
         }
         // residuals where rated (D is NaN elsewhere): the A operands of GEMM 2; stored for
-        // the item-major pass at its fragment position of (x = item, y = user)
-        float *eo = a.eout + static_cast<int64_t>(a.step_twin[k]) * psmf::kDenseTile;
+        // the item-major pass at its fragment position of (x = item, y = user).  Lane
+        // (i, g) holds E[item 16 ys + 4 g + v][user 16 w + i] in register v; after a 4 x 4
+        // transpose inside each quad of lanes (i = 4 q + b) it holds E[item 16 ys + 4 g + b]
+        // [user 16 w + 4 q + r] in register r, which is the float4 of lane 4 g + b + 16 q of
+        // the item-major fragment block (ys, w): one contiguous 1 KiB store per wavefront
+        f32x4 *eo = reinterpret_cast<f32x4 *>(a.eout + static_cast<int64_t>(a.step_twin[k]) * psmf::kDenseTile);
+        const int elane = 4 * g + (i & 3) + 16 * (i >> 2);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const f32x4 sv4 = h ? s1 : s0;
           const f32x4 d = dcur[y2 + h];
+          f32x4 et;
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             e[h][v] = d[v] == d[v] ? d[v] - sv4[v] : 0.f;
-            st_once(eo + psmf::dense_frag_index(16 * (y2 + h) + 4 * g + v, 16 * w + i), e[h][v]);
+            et[v] = e[h][v];
           }
+          st_once(eo + ((y2 + h) * 4 + w) * 64 + elane, quad_transpose(et, i & 3));
         }
       }
       // GEMM 2 over both slices; operand read t = (h, r, cg), the next one read first
@@ -1672,6 +1750,7 @@ CellArgs cell_args(const ps_mf_t *h, const DeviceCells &d, float *partial, int64
   a.y_off = y_off;
   a.ts = d.ts;
   a.partial = partial;
+  a.zero = h->zero_row;
   return a;
 }
 
