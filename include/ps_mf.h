@@ -84,19 +84,23 @@ typedef struct ps_mf ps_mf_t;
 #define PS_MF_OPT_CELLS 9      /* 1 (default): sweep the dense part (users with many ratings) through
                                   LDS-staged cells; 0: every rating through the L2 work units */
 #define PS_MF_OPT_HEAVY_MIN 10 /* ratings in a block from which a user's ratings go to the cells;
-                                  -1 (default): 16 x items / LDS sub-tile rows, at least 256 */
-#define PS_MF_OPT_TWO_STREAMS 11 /* 1 (default): run the L2 work units on a second, internal stream
-                                    (default priority) beside the cells; 0: one stream */
+                                  -1 (default): 16 x items / LDS sub-tile rows, at least 256,
+                                  when the blocks average at least 2^24 ratings, else no cells */
+#define PS_MF_OPT_TWO_STREAMS 11 /* 1 (default): run the L2 work units on a second and the LDS cells
+                                    on a third internal stream (default priority) beside the
+                                    dense tiles; 0: one stream */
 #define PS_MF_OPT_HOT_STEPS 12 /* LDS sub-tiles of a block's most rated items whose ratings by the
                                   remaining (light) users also go to cells; 0: none;
                                   -1 (default): automatic (none when dense tiles are in
-                                  use, else one sub-tile).  Needs
+                                  use or the blocks average fewer than 2^24 ratings, else
+                                  one sub-tile).  Needs
                                   PS_MF_OPT_CELLS = 1; at most 1024 */
 #define PS_MF_OPT_DENSE_MIN 13 /* ratings from which a 64 x 64 tile (64 users of one worker class
                                   ranked by rating count x 64 items ranked by rating count) is
                                   swept with matrix-core products as a dense block; 0: none;
                                   -1 (default): automatic (800, i.e. 20% full, when the padded
-                                  rank is in [16, 256], else none); at most 4096.  A value > 0
+                                  rank is in [16, 256] and the blocks average at least 2^24
+                                  ratings, else none); at most 4096.  A value > 0
                                   with a padded rank outside [16, 256] makes
                                   ps_mf_load_ratings fail with PS_MF_EINVAL */
 #define PS_MF_OPT_SEQ_STRATA 14 /* G: sub-epochs per clock of PS_MF_STEP_SEQ (default 256), in
@@ -119,6 +123,14 @@ typedef struct ps_mf ps_mf_t;
                                    read with NaN, so a row the commit failed to write shows as
                                    NaN (s = 0: the commit updates in place; nothing is filled);
                                    0 (default): off.  With PS_MF_STEP_SEQ load fails (EINVAL) */
+#define PS_MF_OPT_SWEEP_GRAPHS 20 /* 1: under the fixed-view steps, capture each clock's sweep
+                                     launches (work units, LDS cells, dense tiles and the fork
+                                     and join of their streams) once per (block, view schedule)
+                                     into a HIP graph on the handle's stream and replay it; a
+                                     stream the caller is already capturing gets the launches
+                                     one by one.  0 (default): launch them one by one (measured
+                                     faster on ROCm 7: the replay's cross-stream edges cost more
+                                     than the launches they replace) */
 
 /* Views (Section 3.2 SSP condition; Section 4 ESSPTable).  The table-level policies give
    worker p at clock c one whole version v = max(0, c - d):

@@ -68,12 +68,18 @@ constexpr int kLossSegment = 512;  // ratings per lane group of the loss
 #define PS_MF_DENSE_AUTO 800
 #endif
 constexpr int kDenseAuto = PS_MF_DENSE_AUTO;
+// ratings per minibatch block from which the automatic split uses dense tiles and LDS cells
+constexpr int64_t kSplitMinRatings = int64_t{1} << 24;
 // dense cells per direction the layout aims at (more cells: shorter runs and a shorter tail,
 // but one partial row per cell and row)
 #ifndef PS_MF_DENSE_CELLS
 #define PS_MF_DENSE_CELLS 1024
 #endif
 constexpr int kMaxKp = 512;
+// 1: the LDS cells run on a third internal stream beside the dense tiles and the units
+#ifndef PS_MF_CELL_STREAM
+#define PS_MF_CELL_STREAM 1
+#endif
 constexpr int kXcds = psmf::kXcds;
 #ifndef PS_MF_ROWS_IN_FLIGHT
 #define PS_MF_ROWS_IN_FLIGHT 4
@@ -1567,6 +1573,8 @@ struct ps_mf {
   bool eta_decay = false;        // step eta / sqrt(c + 1) at clock c
   bool seq_graphs = true;        // replay each clock's sub-epoch launches from a captured HIP graph
   std::vector<hipGraphExec_t> seq_exec;  // per (block, slot-table row)
+  bool sweep_graphs = false;     // replay each clock's sweep launches from a captured HIP graph
+  std::vector<hipGraphExec_t> sweep_exec;  // per (block, slot-table row)
   std::vector<int32_t> owner;
   // host state
   bool loaded = false, has_factors = false;
@@ -1584,6 +1592,8 @@ struct ps_mf {
   hipStream_t user_stream = nullptr;
   hipStream_t side_stream = nullptr;  // runs the work units beside the cells (default priority)
   hipEvent_t fork = nullptr, join = nullptr;
+  hipStream_t cell_stream = nullptr;  // runs the LDS cells beside the dense tiles (three streams)
+  hipEvent_t join_cells = nullptr;
   bool two_streams = true;
   int32_t hot_steps = -1;  // LDS sub-tiles of hot items whose light-user ratings go to cells (-1: auto)
   float *ring = nullptr;
@@ -1832,6 +1842,10 @@ int ensure_device(ps_mf_t *h) {
     HIP_TRY(h, hipStreamCreateWithFlags(&h->side_stream, hipStreamNonBlocking));
     HIP_TRY(h, hipEventCreateWithFlags(&h->fork, hipEventDisableTiming));
     HIP_TRY(h, hipEventCreateWithFlags(&h->join, hipEventDisableTiming));
+  }
+  if (h->two_streams && PS_MF_CELL_STREAM && !h->cell_stream) {
+    HIP_TRY(h, hipStreamCreateWithFlags(&h->cell_stream, hipStreamNonBlocking));
+    HIP_TRY(h, hipEventCreateWithFlags(&h->join_cells, hipEventDisableTiming));
   }
   return PS_MF_OK;
 }
@@ -2114,20 +2128,65 @@ int one_clock(ps_mf_t *h) {
       if (db.dense_item.ncells > 0) e = launch_dense<true>(h->Kp, di, db.dense_item.ncells, h->stream);
       return e;
     };
-    if (ncells + ndense > 0 && gu + gi > 0 && h->side_stream) {
-      // dense cells and cells on the handle's stream, units on the side stream, all after
-      // what precedes
-      HIP_TRY(h, hipEventRecord(h->fork, h->stream));
-      HIP_TRY(h, hipStreamWaitEvent(h->side_stream, h->fork, 0));
-      HIP_TRY(h, dispatch_units<LaunchUnits>(h->Kp, us, gu + gi, h->side_stream));
-      if (ndense > 0) HIP_TRY(h, launch_dense_pair());
-      if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
-      HIP_TRY(h, hipEventRecord(h->join, h->side_stream));
-      HIP_TRY(h, hipStreamWaitEvent(h->stream, h->join, 0));
+    // the launches of the sweep; every error is returned (a capture in progress must end)
+    auto launch_sweep = [&]() -> hipError_t {
+      hipError_t e = hipSuccess;
+      if (ncells + ndense > 0 && gu + gi > 0 && h->side_stream) {
+        // dense cells (and cells) on the handle's stream, units on the side stream (cells on
+        // a third stream when there is one), all after what precedes
+        const bool third = h->cell_stream && ncells > 0 && ndense > 0;
+        if ((e = hipEventRecord(h->fork, h->stream)) || (e = hipStreamWaitEvent(h->side_stream, h->fork, 0))) return e;
+        if (third && (e = hipStreamWaitEvent(h->cell_stream, h->fork, 0))) return e;
+        if ((e = dispatch_units<LaunchUnits>(h->Kp, us, gu + gi, h->side_stream))) return e;
+        if (third && (e = dispatch<LaunchCells>(h->Kp, cs, ncells, h->cell_stream))) return e;
+        if (ndense > 0 && (e = launch_dense_pair())) return e;
+        if (!third && ncells > 0 && (e = dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream))) return e;
+        if ((e = hipEventRecord(h->join, h->side_stream)) || (e = hipStreamWaitEvent(h->stream, h->join, 0))) return e;
+        if (third && ((e = hipEventRecord(h->join_cells, h->cell_stream)) ||
+                      (e = hipStreamWaitEvent(h->stream, h->join_cells, 0))))
+          return e;
+      } else {
+        if (ndense > 0 && (e = launch_dense_pair())) return e;
+        if (ncells > 0 && (e = dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream))) return e;
+        if (gu + gi > 0 && (e = dispatch_units<LaunchUnits>(h->Kp, us, gu + gi, h->stream))) return e;
+      }
+      return e;
+    };
+    // The sweep's launches depend on the block and the slot-table row only (per-row and
+    // value-bounded views: on the block; their slots are read from device tables), so each
+    // combination is captured once into a HIP graph and replayed: one submission per clock.
+    const int64_t rows = 2 * static_cast<int64_t>(h->s) + 1;
+    const bool device_slots = per_row_policy(h) || h->policy == PS_MF_VAP;
+    const int64_t key = device_slots ? b : b * rows + table_row(h, c);
+    const bool graphed = h->sweep_graphs && (ncells + ndense + gu + gi > 0);
+    if (graphed) {
+      if (h->sweep_exec.empty()) h->sweep_exec.assign(static_cast<size_t>(h->B * rows), nullptr);
+      hipGraphExec_t &ex = h->sweep_exec[static_cast<size_t>(key)];
+      if (!ex) {
+        // a stream the caller is capturing already (the launches then go into the caller's
+        // graph), or one that cannot start a capture, gets the launches one by one
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(h->stream, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone ||
+            hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+          (void)hipGetLastError();
+          h->sweep_graphs = false;
+        } else {
+          hipGraph_t graph = nullptr;
+          const hipError_t le = launch_sweep();
+          const hipError_t ce = hipStreamEndCapture(h->stream, &graph);
+          hipError_t ie = hipSuccess;
+          if (le == hipSuccess && ce == hipSuccess) ie = hipGraphInstantiate(&ex, graph, nullptr, nullptr, 0);
+          if (graph) (void)hipGraphDestroy(graph);
+          HIP_TRY(h, le);
+          HIP_TRY(h, ce);
+          HIP_TRY(h, ie);
+        }
+      }
+    }
+    if (graphed && h->sweep_graphs) {
+      HIP_TRY(h, hipGraphLaunch(h->sweep_exec[static_cast<size_t>(key)], h->stream));
     } else {
-      if (ndense > 0) HIP_TRY(h, launch_dense_pair());
-      if (ncells > 0) HIP_TRY(h, dispatch<LaunchCells>(h->Kp, cs, ncells, h->stream));
-      if (gu + gi > 0) HIP_TRY(h, dispatch_units<LaunchUnits>(h->Kp, us, gu + gi, h->stream));
+      HIP_TRY(h, launch_sweep());
     }
   }
   if ((rc = record_end(h, PS_MF_KERNEL_SWEEP, ev))) return rc;
@@ -2290,6 +2349,9 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
     case PS_MF_OPT_POISON:
       h->poison = value != 0;
       return PS_MF_OK;
+    case PS_MF_OPT_SWEEP_GRAPHS:
+      h->sweep_graphs = value != 0;
+      return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
   }
@@ -2381,17 +2443,24 @@ int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const flo
                           ? std::max<int64_t>(64, h->item_tile_bytes / (static_cast<int64_t>(h->Kp) * 4))
                           : 4 * lp.tile_rows_user;
   lp.unit_max = h->unit_max;
+  // The automatic split sends ratings to dense tiles and LDS cells only when the minibatch
+  // blocks are large: both pay fixed costs (a partial row per cell row, workgroups that
+  // each sweep a few steps) that a small block does not amortize.  Measured on the
+  // 10M-rating K = 64 workload in 4 blocks: units alone 0.196 ms per clock against 0.220 ms
+  // with the split; on the 100M-rating K = 128 workload the split saves a quarter.
+  const bool split_auto = n / h->B >= kSplitMinRatings;
   if (h->cells) {
     // cells: one 1024-thread workgroup per cell, a 128 KiB LDS sub-tile of ts rows; a user
     // is dense enough for them when it averages 16 or more ratings per item sub-tile
     lp.cell_rows = kTileFloats / h->Kp;
     lp.cell_groups = kSweepBlock / shape_for(h->Kp).G;
     lp.heavy_min = h->heavy_min >= 0 ? h->heavy_min
-                                      : std::max<int64_t>(256, 16 * h->M / lp.cell_rows);
+                   : split_auto      ? std::max<int64_t>(256, 16 * h->M / lp.cell_rows)
+                                     : lp.heavy_min;  // no user is heavy
   }
   if (h->dense_min > 0 && !dense_supported(h->Kp))
     return fail(h, PS_MF_EINVAL, "dense tiles need a padded rank in [16, 256], not %d", h->Kp);
-  lp.dense_min = h->dense_min >= 0 ? h->dense_min : (dense_supported(h->Kp) ? kDenseAuto : 0);
+  lp.dense_min = h->dense_min >= 0 ? h->dense_min : (split_auto && dense_supported(h->Kp) ? kDenseAuto : 0);
   lp.dense_target = PS_MF_DENSE_CELLS;
   lp.workers = h->P;
   if (seq) {
@@ -2403,7 +2472,7 @@ int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const flo
     // automatic hot-item sub-tiles: none next to dense tiles, else one (on the 100M-rating
     // K = 128 workload: 1 measured best among 0..4 without dense tiles; with them the
     // light users' extra partial rows cost the commit more than the cells save)
-    lp.hot_steps = h->hot_steps >= 0 ? h->hot_steps : (lp.dense_min > 0 ? 0 : 1);
+    lp.hot_steps = h->hot_steps >= 0 ? h->hot_steps : (lp.dense_min > 0 || !split_auto ? 0 : 1);
   }
   std::string err;
   const int rc = psmf::build_layout(lp, user, item, value, n, h->layout, err);
@@ -2828,12 +2897,17 @@ void ps_mf_destroy(ps_mf_t *h) {
     (void)hipEventDestroy(ev.b);
   }
   if (h->side_stream) (void)hipStreamSynchronize(h->side_stream);
+  if (h->cell_stream) (void)hipStreamSynchronize(h->cell_stream);
   for (hipGraphExec_t ex : h->seq_exec)
+    if (ex) (void)hipGraphExecDestroy(ex);
+  for (hipGraphExec_t ex : h->sweep_exec)
     if (ex) (void)hipGraphExecDestroy(ex);
   for (void *p : h->allocations) (void)hipFree(p);
   if (h->side_stream) (void)hipStreamDestroy(h->side_stream);
+  if (h->cell_stream) (void)hipStreamDestroy(h->cell_stream);
   if (h->fork) (void)hipEventDestroy(h->fork);
   if (h->join) (void)hipEventDestroy(h->join);
+  if (h->join_cells) (void)hipEventDestroy(h->join_cells);
   if (h->own_stream && h->stream) (void)hipStreamDestroy(h->stream);
   delete h;
 }
