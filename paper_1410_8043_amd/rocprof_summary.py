@@ -6,6 +6,11 @@
         two streams: from the first start to the last end);
     python -m paper_1410_8043_amd.rocprof_summary counters <dir> [<dir> ...]
         per-kernel counter values (sum over a dispatch's dimensions) of --pmc runs;
+    python -m paper_1410_8043_amd.rocprof_summary derived <dir> [<dir> ...]
+        per-kernel figures derived from --pmc runs (average over dispatches): duration in
+        cycles (GRBM_GUI_ACTIVE counts every XCD), busy fractions of the texture address and
+        data units (one per CU), of the L2 channels and of the matrix cores, the L2 hit rate
+        and the average L1-to-L2 read latency -- whichever of them the runs collected;
     python -m paper_1410_8043_amd.rocprof_summary traffic --fetch <dir> --write <dir> \
             --copy-bytes N --out profiles/<name>.json [--kernels k_lda_sweep --step lda \
             --source paper_1410_8043_amd/csrc/ps_lda.hip]
@@ -95,6 +100,49 @@ def counters(d: str):
     return out
 
 
+# MI355X: 8 XCDs, 256 CUs (one texture address / data unit each), 16 L2 channels per XCD,
+# 4 SIMDs per CU
+XCDS, CUS, L2_CHANNELS, SIMDS = 8, 256, 128, 1024
+
+
+def derived(dirs):
+    """{kernel: {figure: value}} from the counters of one or more --pmc runs (each counter
+    averaged over the kernel's dispatches)."""
+    avg = collections.defaultdict(dict)
+    for d in dirs:
+        for (k, c), v in counters(d).items():
+            avg[short_name(k)][c] = sum(v) / len(v)
+    out = {}
+    for k, c in avg.items():
+        f = {}
+        cyc = c.get("GRBM_GUI_ACTIVE")
+        if cyc:
+            cyc /= XCDS
+            f["cycles"] = cyc
+            if "TA_TA_BUSY_sum" in c:
+                f["ta_busy"] = c["TA_TA_BUSY_sum"] / CUS / cyc
+            if "TA_ADDR_STALLED_BY_TC_CYCLES_sum" in c:
+                f["ta_stalled_by_l1"] = c["TA_ADDR_STALLED_BY_TC_CYCLES_sum"] / CUS / cyc
+            if "TD_TD_BUSY_sum" in c:
+                f["td_busy"] = c["TD_TD_BUSY_sum"] / CUS / cyc
+            if "TCC_BUSY_sum" in c:
+                f["l2_busy"] = c["TCC_BUSY_sum"] / L2_CHANNELS / cyc
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+                f["mfma_busy"] = c["SQ_VALU_MFMA_BUSY_CYCLES"] / SIMDS / cyc
+        if c.get("TCC_REQ_sum"):
+            f["l2_hit"] = c.get("TCC_HIT_sum", 0.0) / c["TCC_REQ_sum"]
+            f["l2_requests"] = c["TCC_REQ_sum"]
+        if c.get("TCP_TCC_READ_REQ_sum"):
+            f["l1_l2_read_latency"] = c.get("TCP_TCC_READ_REQ_LATENCY_sum", 0.0) / c["TCP_TCC_READ_REQ_sum"]
+        if c.get("SQ_WAVE_CYCLES"):
+            f["wave_wait_frac"] = c.get("SQ_WAIT_INST_ANY", 0.0) / c["SQ_WAVE_CYCLES"]
+        for name in ("SQ_INSTS_VALU", "SQ_INSTS_VMEM_RD", "SQ_INSTS_MFMA", "SQ_WAVES"):
+            if name in c:
+                f[name] = c[name]
+        out[k] = f
+    return out
+
+
 def _find(cnt, kernel_prefix: str, counter: str):
     for (k, c), v in cnt.items():
         if c == counter and short_name(k).startswith(kernel_prefix):
@@ -157,6 +205,8 @@ def main(argv=None):
     a.add_argument("dir")
     b = sub.add_parser("counters")
     b.add_argument("dirs", nargs="+")
+    e = sub.add_parser("derived")
+    e.add_argument("dirs", nargs="+")
     c = sub.add_parser("traffic")
     c.add_argument("--fetch", required=True)
     c.add_argument("--write", required=True)
@@ -180,6 +230,11 @@ def main(argv=None):
             print(f"sweep span (first start to last end of the {' / '.join(SWEEP_KERNELS)} kernels of a clock): "
                   f"{len(spans)} clocks, avg {avg:.4f} ms, min {min(sp for sp, _ in spans):.4f} ms, "
                   f"max {max(sp for sp, _ in spans):.4f} ms")
+    elif args.cmd == "derived":
+        for k, f in sorted(derived(args.dirs).items()):
+            print(k)
+            for name, v in f.items():
+                print(f"    {name:22s} {v:.4g}")
     elif args.cmd == "counters":
         for d in args.dirs:
             for (k, cname), vals in sorted(counters(d).items()):

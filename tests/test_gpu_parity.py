@@ -514,6 +514,53 @@ def test_seq_graph_replays_equal_eager_launches(gpu, policy, s, B):
             assert x == y
 
 
+@pytest.mark.parametrize("policy,s,B", [(oracle.SSP_LAZY, 2, 3), (oracle.VAP, 2, 2), (oracle.SSP_ROW, 1, 2),
+                                      (oracle.SSP_WORST, 0, 1)])
+def test_sweep_graph_replays_equal_eager_launches(gpu, policy, s, B):
+    """With PS_MF_OPT_SWEEP_GRAPHS each clock's sweep (units, LDS cells and dense tiles on
+    their three streams) is replayed from a HIP graph per (block, view schedule); every
+    replay, with the program's own work and synchronizations between clocks, must equal
+    launching the sweep one kernel at a time, bit for bit, and stay within the tolerances
+    of the oracle."""
+    spec = synth.scaled(synth.CONFIGS["full"], 0.05)
+    w = synth.generate(spec, K=64)
+    opts = dict(dense_min=300, heavy_min=64, hot_steps=0)
+    clocks = (2 * s + 1) * B + 2  # every (block, view schedule) graph, some replayed
+    say(f"sweep graphs: full@0.05 nnz={w.nnz} policy={policy} s={s} B={B} clocks={clocks}")
+    out = []
+    for graphs in (True, False):
+        with gpu.PsMf(spec.N, spec.M, 64, spec.P, s, spec.eta, spec.lam, policy=policy, B=B, mb_seed=spec.seed,
+                      value_bound=0.003 if policy == oracle.VAP else None, sweep_graphs=graphs, **opts) as g:
+            g.load_ratings(w.user, w.item, w.val)
+            split = g.export_index(gpu.IDX_SPLIT)
+            assert split[0] > 0 and split[1] > 0 and split[2] > 0, split
+            g.set_factors(w.L0, w.R0)
+            hist = []
+            for _ in range(clocks):
+                g.clock(1)
+                hist.append(g.loss())
+                hist.append(g.get_factors())
+            out.append((hist, g.export_index(gpu.IDX_VERSION_LOG)))
+    (ha, va), (hb, vb) = out
+    assert np.array_equal(va, vb)
+    for x, y in zip(ha, hb):
+        if isinstance(x, tuple):
+            assert np.array_equal(x[0], y[0]) and np.array_equal(x[1], y[1])
+        else:
+            assert x == y
+    o = oracle.Oracle(spec.N, spec.M, 64, spec.P, s, spec.eta, spec.lam, policy, oracle.ROWMEAN, B, spec.seed,
+                      value_bound=0.003 if policy == oracle.VAP else None)
+    o.load(w.user, w.item, w.val)
+    o.set_factors(w.L0, w.R0)
+    o.clock(clocks)
+    Lo, Ro = o.get_factors()
+    loss_o = o.loss()
+    o.close()
+    L, R = ha[-1]
+    assert max(np.abs(L - Lo).max(), np.abs(R - Ro).max()) <= FACTOR_TOL
+    assert abs(ha[-2] - loss_o) <= LOSS_RTOL * loss_o
+
+
 @pytest.mark.parametrize("policy", [oracle.SSP_ROW, oracle.ESSP_ROW])
 @pytest.mark.parametrize("s,B", [(1, 1), (3, 4), (2, 3)])
 def test_tiny_config_seq_per_row_policies(gpu, policy, s, B):
