@@ -731,6 +731,9 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
             a0n = T4[dense_lds_chunk<Kp>(16 * y2 + i, 4 * (q + 1) + g)];
             a1n = T4[dense_lds_chunk<Kp>(16 * y2 + 16 + i, 4 * (q + 1) + g)];
           }
+          // keep the reads of chunk q+1 ahead of the products of chunk q (the scheduler
+          // would otherwise sink them to their use and wait for them there)
+          __builtin_amdgcn_sched_barrier(0);
           s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, xb[q][0], s0, 0, 0, 0);
           s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, xb[q][0], s1, 0, 0, 0);
           s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, xb[q][1], s0, 0, 0, 0);
@@ -739,6 +742,7 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
           s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, xb[q][2], s1, 0, 0, 0);
           s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, xb[q][3], s0, 0, 0, 0);
           s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, xb[q][3], s1, 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
         }
         // residuals where rated (D is NaN elsewhere): the A operands of GEMM 2; stored for
         // the item-major pass at its fragment position of (x = item, y = user).  Lane
@@ -772,10 +776,14 @@ __device__ __forceinline__ void run_dense(const DenseArgs &a, int64_t cell, floa
       for (int t = 0; t < 2 * NB; ++t) {
         const VecT b = bn;
         if (t + 1 < 2 * NB) bn = *reinterpret_cast<const VecT *>(Tb + boff(t + 1));
+        // keep each read ahead of the products before it (the scheduler would otherwise
+        // sink it to its use and wait for it there)
+        __builtin_amdgcn_sched_barrier(0);
         const int h = t / NB, r = (t % NB) / (NQ / C4), cg = t % (NQ / C4);
 #pragma unroll
         for (int cc = 0; cc < C4; ++cc)
           acc[C4 * cg + cc] = __builtin_amdgcn_mfma_f32_16x16x4f32(e[h][r], vec_at<C4>(b, cc), acc[C4 * cg + cc], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     if (more) {

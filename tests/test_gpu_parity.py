@@ -16,6 +16,8 @@ pytestmark = pytest.mark.gpu
 
 FACTOR_TOL = 1e-4
 LOSS_RTOL = 1e-5
+UPDATE_RTOL = 1e-2   # of the oracle's largest accumulated update of the factor
+UPDATE_FLOOR = 1e-6  # for cases whose updates are themselves near fp32 rounding
 
 
 @pytest.fixture(scope="module")
@@ -61,6 +63,14 @@ def run_both(ps_mf, w_user, w_item, w_val, L0, R0, *, N, M, K, P, s, eta, lam, c
         err = max(np.abs(L - Lo).max(initial=0), np.abs(R - Ro).max(initial=0))
         loss, loss_o = g.loss(), o.loss()
         assert err <= FACTOR_TOL, err
+        # scale-aware: each factor's deviation from the oracle is small next to the oracle's
+        # own accumulated update of that factor, so a dropped term (an R commit, the lambda
+        # part) cannot hide under the absolute tolerance when the updates are small
+        for V, Vo, V0 in ((L, Lo, L0), (R, Ro, R0)):
+            if V.size:
+                upd = np.abs(Vo.astype(np.float64) - np.asarray(V0, np.float64)).max()
+                dev = np.abs(V.astype(np.float64) - Vo).max()
+                assert dev <= max(UPDATE_RTOL * upd, UPDATE_FLOOR), (dev, upd)
         assert abs(loss - loss_o) <= LOSS_RTOL * max(loss_o, 1e-30), (loss, loss_o)
         assert np.array_equal(g.export_index(gpu_mod().IDX_VERSION_LOG), o.export(oracle.X_VERSION_LOG))
         assert np.array_equal(g.export_index(gpu_mod().IDX_STALENESS), o.export(oracle.X_STALENESS))
