@@ -424,3 +424,24 @@ def test_user_major_item_tiles_split_the_units(item_tile_bytes):
             out.append(g.export_index(m.IDX_SPLIT))
     assert out[0][2] == out[1][2] == cells.size
     assert out[0][6] == N and out[1][6] >= 4 * N
+
+
+def test_automatic_split_uses_dense_tiles_and_cells_only_on_large_blocks():
+    """With the automatic thresholds, blocks of fewer than 2^24 ratings send every rating
+    through the work units; larger blocks put their densest part into dense (matrix-core)
+    tiles and LDS cells.  The same 17.6M ratings as one block and as two blocks."""
+    from paper_1410_8043_amd import synth
+
+    spec = synth.scaled(synth.CONFIGS["full"], 0.42)
+    w = synth.generate(spec, K=1)
+    assert w.nnz >= 1 << 24 > w.nnz // 2
+    for B in (1, 2):
+        with ps_mf.PsMf(spec.N, spec.M, 128, spec.P, 3, spec.eta, spec.lam, B=B, mb_seed=spec.seed,
+                        host_only=True) as g:
+            g.load_ratings(w.user, w.item, w.val)
+            split = sum(g.export_index(ps_mf.IDX_SPLIT, b) for b in range(B))
+        assert split[0] + split[1] + split[2] == w.nnz and split[3:6].tolist() == split[0:3].tolist()
+        if B == 1:
+            assert split[0] > 0 and split[1] > 0 and split[2] > 0, split
+        else:
+            assert split[0] == 0 and split[1] == 0 and split[2] == w.nnz, split
