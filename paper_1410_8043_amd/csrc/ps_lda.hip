@@ -77,48 +77,63 @@ struct SweepArgs {
   int32_t shift0;       // 62 - ceil(log2 K): the largest weight lies in [2^shift0, 2^(shift0+1))
 };
 
-// one DPP lane move of a 64-bit value (both halves with the same control and row mask);
-// lanes whose source lies outside the pattern, or whose row the mask leaves out, read 0
-template <int CTRL, int ROW_MASK = 0xF>
-__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
-  const uint32_t lo = static_cast<uint32_t>(
-      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x)), CTRL, ROW_MASK, 0xF, false));
-  const uint32_t hi = static_cast<uint32_t>(
-      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x >> 32)), CTRL, ROW_MASK, 0xF, false));
-  return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-
 __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
   const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x)), lane));
   const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x >> 32)), lane));
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-// inclusive prefix sum of a 64-bit value over the wavefront: Hillis-Steele inside each row
-// of 16 lanes (DPP row shifts 1, 2, 4, 8); then row_bcast:15 adds the last lane of rows 0
-// and 2 into rows 1 and 3, and row_bcast:31 the last lane of row 1 (by then the sum of
-// rows 0-1) into rows 2 and 3; *total gets lane 63's sum
+// inclusive prefix sum of a 64-bit value over the wavefront (all 64 lanes active):
+// Hillis-Steele inside each row of 16 lanes (DPP row shifts 1, 2, 4, 8; a lane without a
+// source adds 0), then row_bcast:15 adds the last lane of rows 0 and 2 into rows 1 and 3,
+// and row_bcast:31 the last lane of row 1 (by then the sum of rows 0-1) into rows 2 and 3
+// (rows the mask leaves out keep their value); *total gets lane 63's sum.  Each step is one
+// add of the low halves with the carry into VCC and one add of the high halves with that
+// carry, both reading the shifted operand through DPP.  The s_nop keeps two wait states
+// between a half's write and the next DPP read of it.
 __device__ __forceinline__ uint64_t wave_scan(uint64_t x, uint64_t *total) {
-  x += dpp_u64<0x111>(x);
-  x += dpp_u64<0x112>(x);
-  x += dpp_u64<0x114>(x);
-  x += dpp_u64<0x118>(x);
-  x += dpp_u64<0x142, 0xA>(x);
-  x += dpp_u64<0x143, 0xC>(x);
+  uint32_t lo = static_cast<uint32_t>(x), hi = static_cast<uint32_t>(x >> 32);
+#define PS_LDA_SCAN_STEP(DPP)                                          \
+  "s_nop 1\n\t"                                                         \
+  "v_add_co_u32_dpp %0, vcc, %0, %0 " DPP "\n\t"                        \
+  "v_addc_co_u32_dpp %1, vcc, %1, %1, vcc " DPP "\n\t"
+  asm volatile(PS_LDA_SCAN_STEP("row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1")
+               PS_LDA_SCAN_STEP("row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1")
+               PS_LDA_SCAN_STEP("row_shr:4 row_mask:0xf bank_mask:0xf bound_ctrl:1")
+               PS_LDA_SCAN_STEP("row_shr:8 row_mask:0xf bank_mask:0xf bound_ctrl:1")
+               PS_LDA_SCAN_STEP("row_bcast:15 row_mask:0xa bank_mask:0xf")
+               PS_LDA_SCAN_STEP("row_bcast:31 row_mask:0xc bank_mask:0xf")
+               "s_nop 1"
+               : "+v"(lo), "+v"(hi)
+               :
+               : "vcc");
+#undef PS_LDA_SCAN_STEP
+  x = (static_cast<uint64_t>(hi) << 32) | lo;
   *total = readlane_u64(x, 63);
   return x;
 }
 
-// maximum of an int over the wavefront, returned in every lane: DPP quad_perm [1,0,3,2],
+// maximum of an int over the wavefront, in lane 63 and returned: DPP quad_perm [1,0,3,2],
 // quad_perm [2,3,0,1], row_half_mirror and row_mirror give each lane its 16-lane row's
-// maximum (every source lane lies inside the row), then the four rows' maxima are read
+// maximum (every source lane lies inside the row), then row_bcast:15 and row_bcast:31 carry
+// the rows' maxima into row 3 (rows the mask leaves out keep their value)
 __device__ __forceinline__ int wave_max_i32(int x) {
-  x = max(x, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, true));
-  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, true));
-  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x141, 0xF, 0xF, true));
-  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x140, 0xF, 0xF, true));
-  return max(max(__builtin_amdgcn_readlane(x, 0), __builtin_amdgcn_readlane(x, 16)),
-             max(__builtin_amdgcn_readlane(x, 32), __builtin_amdgcn_readlane(x, 48)));
+  asm volatile(
+      "s_nop 1\n\t"
+      "v_max_i32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_i32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_i32_dpp %0, %0, %0 row_half_mirror row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_i32_dpp %0, %0, %0 row_mirror row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_i32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_i32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+      "s_nop 1"
+      : "+v"(x));
+  return __builtin_amdgcn_readlane(x, 63);
 }
 
 // what one token reads before it can be sampled: its view row and own-change row of the
@@ -129,27 +144,42 @@ struct TokenRows {
   int tag, z;
 };
 
+// a row's element at a byte offset from the row's start: a uniform base with a 32-bit lane
+// offset, i.e. the scalar-base form of the global memory instructions (the empty asm keeps
+// the offset's widening next to its use, where instruction selection folds it into that
+// form, instead of hoisted out of the loop as a 64-bit lane address)
+__device__ __forceinline__ uint32_t lane_off(uint32_t off) {
+  asm("" : "+v"(off));
+  return off;
+}
+__device__ __forceinline__ int32_t &at(int32_t *row, uint32_t off) {
+  return *reinterpret_cast<int32_t *>(reinterpret_cast<char *>(row) + lane_off(off));
+}
+__device__ __forceinline__ int32_t at(const int32_t *row, uint32_t off) {
+  return *reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(row) + lane_off(off));
+}
+
+// koff[j]: the byte offset of this lane's topic j in a row (lanes past the last topic
+// re-read topic K-1: every load is issued on every path, so the waits before a use count
+// exactly; their values are masked)
 template <int KPL>
-__device__ __forceinline__ void fetch_rows(const SweepArgs &a, const int32_t *view, const int32_t *mydelta,
-                                           const int32_t *mytag, int w, int64_t q, int lane, TokenRows<KPL> &o) {
-  const int64_t base = static_cast<int64_t>(w) * a.K;
+__device__ __forceinline__ void fetch_rows(const int32_t *view, const int32_t *mydelta, const int32_t *mytag,
+                                           const int32_t *z, int K, const uint32_t (&koff)[KPL], int w, int i,
+                                           TokenRows<KPL> &o) {
+  const int32_t *vrow = view + static_cast<int64_t>(w) * K;
+  const int32_t *drow = mydelta + static_cast<int64_t>(w) * K;
   o.tag = mytag[w];
-  o.z = a.z[q];
-  // lanes past the last topic re-read topic K-1 (every load issued on every path, so the
-  // waits before a use count exactly); their values are masked out
+  o.z = z[i];
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {
-    const int k = min(lane * KPL + j, a.K - 1);
-    const bool in = lane * KPL + j < a.K;
-    const int x = view[base + k], y = mydelta[base + k];
-    o.nw[j] = in ? x : 0;
-    o.dw[j] = in ? y : 0;
+    o.nw[j] = at(vrow, koff[j]);
+    o.dw[j] = at(drow, koff[j]);
   }
 }
 
 // step(integral_constant<int, I>, q + I) for I = I0 .. N-1 while q + I < q1
 template <int I0, int N, class F>
-__device__ __forceinline__ void seq_steps(F &f, int64_t q, int64_t q1, bool &more) {
+__device__ __forceinline__ void seq_steps(F &f, int q, int q1, bool &more) {
   if (q + I0 >= q1) {
     more = false;
     return;
@@ -161,16 +191,22 @@ __device__ __forceinline__ void seq_steps(F &f, int64_t q, int64_t q1, bool &mor
 // Lane l holds topics l*KPL .. l*KPL+KPL-1 (consecutive, so one wave scan of the lanes'
 // sums orders every topic).  Tokens run in a rotation of kDist+1 steps whose buffer indices
 // are fixed at compile time: at the end of step q, after its own stores, the rows of token
-// q+kDist are fetched and the record of token q+kDist+1 (scalar loads: the records are
-// read-only here, and their counter is separate from the vector loads').  The fetch of token
-// t sees every store up to token t-kDist; the stores of the kDist-1 tokens after that come
-// later, so the updated own-change rows of those tokens stay in registers, and a token whose
-// word matches one of them takes the latest such row instead of its fetched one.  Fetches
-// past the last token re-read the last one and are never used, which keeps every fetch
-// unconditional (so the waits before a use count exactly the newer loads).
+// q+kDist are fetched.  The fetch of token t sees every store up to token t-kDist; the
+// stores of the kDist-1 tokens after that come later, so the updated own-change rows of
+// those tokens stay in registers, and a token whose word matches one of them takes the
+// latest such row instead of its fetched one.  Fetches past the last token re-read the
+// last one and are never used, which keeps every fetch unconditional (so the waits before
+// a use count exactly the newer loads).
+//
+// The token records come in blocks of 64, one per lane (a vector load), read with lane
+// reads: the block at base holds tokens base .. base+63 and serves the tokens base ..
+// base+kRecStep-1 and the fetches up to kDist tokens further; the next block is loaded
+// when this one starts, kRecStep tokens before its first use.  (Records loaded one at a
+// time by scalar loads, a token ahead of their fetch, put the scalar load's latency into
+// every token: a wait for a scalar load waits for all of them.)
 typedef int i32x4 __attribute__((ext_vector_type(4)));
-typedef const __attribute__((address_space(4))) i32x4 *const_rec_ptr;
 constexpr int kDist = 3;
+constexpr int kRecStep = 60;  // a multiple of the rotation, at most 64 - kDist
 
 template <int KPL>
 __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
@@ -189,9 +225,14 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
   const int32_t *view = a.ring + (v % a.nslots) * a.slot_stride;
   int32_t *mydelta = a.delta + p * V * K;
   int32_t *mytag = a.tag + p * V;
-  const const_rec_ptr rec = (const_rec_ptr)(a.rec);
+  // this worker's tokens of the block, indexed from 0 (a worker has fewer than 2^31)
+  const i32x4 *rec = reinterpret_cast<const i32x4 *>(a.rec) + q0;
+  int32_t *z = a.z + q0;
+  const int n = static_cast<int>(q1 - q0), last = n - 1;
   const uint64_t rbase = a.seed ^ kDrawSalt ^ (static_cast<uint64_t>(c) << 40);
-  const int64_t qlast = q1 - 1;
+  uint32_t koff[KPL];
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) koff[j] = 4u * static_cast<uint32_t>(min(lane * KPL + j, K - 1));
 
   int vk[KPL], dk[KPL], nd[KPL];
 #pragma unroll
@@ -203,11 +244,19 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
   }
   int cur_doc = -1;
   TokenRows<KPL> rows[R];
-  i32x4 recs[R];
+  // token records: the current block and the next one; rnd holds the draw's random value of
+  // each token of the current block (SplitMix64 of its load index, computed once per block)
+  int base = 0;
+  i32x4 rv = rec[min(base + lane, last)];
+  i32x4 rv_next = rec[min(base + kRecStep + lane, last)];
+  uint64_t rnd = splitmix64(rbase ^ static_cast<uint64_t>(static_cast<uint32_t>(rv[2])));
+  auto field = [&](int i, int f) { return __builtin_amdgcn_readlane(rv[f], i - base); };
 #pragma unroll
-  for (int i = 0; i < R; ++i) recs[i] = rec[min(q0 + i, qlast)];
-#pragma unroll
-  for (int i = 0; i < kDist; ++i) fetch_rows<KPL>(a, view, mydelta, mytag, recs[i][0], min(q0 + i, qlast), lane, rows[i]);
+  for (int i = 0; i < kDist; ++i) {
+    const int qi = min(i, last);
+    fetch_rows<KPL>(view, mydelta, mytag, z, K, koff, field(qi, 0), qi, rows[i]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   // the last F tokens' words (-1: none), row validity and updated own-change rows, latest first
   int fw[F > 0 ? F : 1];
   bool fvalid[F > 0 ? F : 1];
@@ -220,9 +269,9 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     for (int j = 0; j < KPL; ++j) fdw[i][j] = 0;
   }
 
-  auto step = [&](auto phase, int64_t q) {
+  auto step = [&](auto phase, int i) {
     constexpr int C = decltype(phase)::value;
-    const int w = recs[C][0], d = recs[C][1], t = recs[C][2];
+    const int w = field(i, 0), d = field(i, 1);
     const int k0 = __builtin_amdgcn_readfirstlane(rows[C].z);
     bool valid = __builtin_amdgcn_readfirstlane(rows[C].tag) == a.tagc;
     int dw[KPL];
@@ -230,11 +279,11 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     for (int j = 0; j < KPL; ++j) dw[j] = rows[C].dw[j];
     // the latest of the last F tokens with this word, if any, overrides the fetched row
 #pragma unroll
-    for (int i = F - 1; i >= 0; --i) {
-      if (fw[i] == w) {
-        valid = fvalid[i];
+    for (int f = F - 1; f >= 0; --f) {
+      if (fw[f] == w) {
+        valid = fvalid[f];
 #pragma unroll
-        for (int j = 0; j < KPL; ++j) dw[j] = fdw[i][j];
+        for (int j = 0; j < KPL; ++j) dw[j] = fdw[f][j];
       }
     }
     if (!valid) {
@@ -243,34 +292,37 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     }
     if (d != cur_doc) {
       if (cur_doc >= 0) {
+        int32_t *old = a.ndk + static_cast<int64_t>(cur_doc) * K;
 #pragma unroll
         for (int j = 0; j < KPL; ++j)
-          if (lane * KPL + j < K) a.ndk[static_cast<int64_t>(cur_doc) * K + lane * KPL + j] = nd[j];
+          if (lane * KPL + j < K) at(old, koff[j]) = nd[j];
       }
+      const int32_t *row = a.ndk + static_cast<int64_t>(d) * K;
 #pragma unroll
       for (int j = 0; j < KPL; ++j) {
-        const int x = a.ndk[static_cast<int64_t>(d) * K + min(lane * KPL + j, K - 1)];
+        const int x = at(row, koff[j]);
         nd[j] = lane * KPL + j < K ? x : 0;
       }
       cur_doc = d;
     }
     // the collapsed conditional's weights p_k in fp64 (every p_k is a normal number: the
     // load checks the range) and the exponent of the largest (the largest exponent)
+    // (computed on every lane, without a branch: lanes past the last topic hold topic K-1's
+    // rows and zero counts, and their results are masked)
     double pk[KPL];
     int emax = -2048;  // below every normal exponent: lanes past the last topic
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
       const int k = lane * KPL + j;
-      pk[j] = 0.0;
-      if (k < K) {
-        const int self = k == k0;
-        const int ndx = nd[j] - self;
-        const int nwx = max(rows[C].nw[j] + dw[j] - self, 0);
-        const int nkx = max(vk[j] + dk[j] - self, 0);
-        const double num = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
-        pk[j] = num / (static_cast<double>(nkx) + a.Vbeta);
-        emax = max(emax, __builtin_amdgcn_frexp_exp(pk[j]) - 1);  // frexp: p = m 2^x, m in [0.5, 1)
-      }
+      const int self = k == k0;
+      const int ndx = nd[j] - self;
+      const int nwx = max(rows[C].nw[j] + dw[j] - self, 0);
+      const int nkx = max(vk[j] + dk[j] - self, 0);
+      const double num = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
+      const double p = num / (static_cast<double>(nkx) + a.Vbeta);
+      const bool in = k < K;
+      pk[j] = in ? p : 0.0;
+      if (in) emax = max(emax, __builtin_amdgcn_frexp_exp(p) - 1);  // frexp: p = m 2^x, m in [0.5, 1)
     }
     // integer weights floor(p_k 2^(shift0 - emax)) (the scaling is exact), prefix sums in
     // topic order
@@ -286,7 +338,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     const uint64_t excl = wave_scan(acc, &total) - acc;
     int k1 = k0;
     if (total != 0) {  // always: the largest weight is at least 2^shift0
-      const uint64_t target = __umul64hi(splitmix64(rbase ^ static_cast<uint64_t>(static_cast<uint32_t>(t))), total);
+      const uint64_t target = __umul64hi(readlane_u64(rnd, i - base), total);
       const uint64_t m = __ballot(excl + acc > target);
       const int L = __ffsll(static_cast<unsigned long long>(m)) - 1;  // m != 0: the last lane's sum is the total
       int jj = KPL - 1;
@@ -297,6 +349,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     }
     const bool changed = k1 != k0;
     if (changed) {
+      int32_t *drow = mydelta + static_cast<int64_t>(w) * K;
 #pragma unroll
       for (int j = 0; j < KPL; ++j) {
         const int k = lane * KPL + j;
@@ -305,21 +358,21 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
         dk[j] += dl;
         dw[j] += dl;
         if (k < K) {
-          if (!valid || dl != 0) mydelta[static_cast<int64_t>(w) * K + k] = dw[j];
+          if (!valid || dl != 0) at(drow, koff[j]) = dw[j];
         }
       }
       if (lane == 0) {
-        a.z[q] = k1;
+        z[i] = k1;
         if (!valid) mytag[w] = a.tagc;
       }
     }
     // this token becomes the latest forwarded row
 #pragma unroll
-    for (int i = F - 1; i > 0; --i) {
-      fw[i] = fw[i - 1];
-      fvalid[i] = fvalid[i - 1];
+    for (int f = F - 1; f > 0; --f) {
+      fw[f] = fw[f - 1];
+      fvalid[f] = fvalid[f - 1];
 #pragma unroll
-      for (int j = 0; j < KPL; ++j) fdw[i][j] = fdw[i - 1][j];
+      for (int j = 0; j < KPL; ++j) fdw[f][j] = fdw[f - 1][j];
     }
     if constexpr (F > 0) {
       fw[0] = w;
@@ -328,19 +381,36 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
       for (int j = 0; j < KPL; ++j) fdw[0][j] = dw[j];
     }
     constexpr int NF = (C + kDist) % R;
-    fetch_rows<KPL>(a, view, mydelta, mytag, recs[NF][0], min(q + kDist, qlast), lane, rows[NF]);
-    recs[C] = rec[min(q + R, qlast)];
+    const int qf = min(i + kDist, last);
+    fetch_rows<KPL>(view, mydelta, mytag, z, K, koff, field(qf, 0), qf, rows[NF]);
   };
-  for (int64_t q = q0; q < q1; q += R) {
-    bool more = true;
-    seq_steps<0, R>(step, q, q1, more);
-    if (!more) break;
+  // whole rotations without an exit inside (an exit path would join the loop's back edge
+  // with its latest fetch still in flight, and the wait at the top of the loop would then
+  // drain every fetch), then the last tokens
+  int i = 0;
+  for (;;) {
+    const int lim = min(base + kRecStep, n);
+    for (; i + R <= lim; i += R) {
+      bool more = true;
+      seq_steps<0, R>(step, i, n, more);
+    }
+    if (n <= base + kRecStep) break;
+    // i = base + kRecStep: the next block of records
+    base = i;
+    rv = rv_next;
+    rv_next = rec[min(base + kRecStep + lane, last)];
+    rnd = splitmix64(rbase ^ static_cast<uint64_t>(static_cast<uint32_t>(rv[2])));
   }
+  if (i < n) {
+    bool more = true;
+    seq_steps<0, R - 1>(step, i, n, more);
+  }
+  int32_t *drow_end = a.ndk + static_cast<int64_t>(cur_doc) * K;
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {
     const int k = lane * KPL + j;
     if (k < K) {
-      a.ndk[static_cast<int64_t>(cur_doc) * K + k] = nd[j];
+      at(drow_end, koff[j]) = nd[j];
       a.tot[p * K + k] = dk[j];
     }
   }
