@@ -83,6 +83,19 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
+// the high 64 bits of the 128-bit product a * b, on the vector unit: four 32 x 32 + 64
+// multiply-adds (the operands are first moved into vector registers, where the scalar
+// unit's form of the same product takes about fifteen instructions)
+__device__ __forceinline__ uint64_t umulhi64_vec(uint64_t a, uint64_t b) {
+  uint32_t a0 = static_cast<uint32_t>(a), a1 = static_cast<uint32_t>(a >> 32);
+  asm("" : "+v"(a0), "+v"(a1));
+  const uint32_t b0 = static_cast<uint32_t>(b), b1 = static_cast<uint32_t>(b >> 32);
+  const uint64_t t = static_cast<uint64_t>(a0) * b0;
+  const uint64_t u = static_cast<uint64_t>(a1) * b0 + (t >> 32);
+  const uint64_t w = static_cast<uint64_t>(a0) * b1 + static_cast<uint32_t>(u);
+  return static_cast<uint64_t>(a1) * b1 + (u >> 32) + (w >> 32);
+}
+
 // inclusive prefix sum of a 64-bit value over the wavefront (all 64 lanes active):
 // Hillis-Steele inside each row of 16 lanes (DPP row shifts 1, 2, 4, 8; a lane without a
 // source adds 0), then row_bcast:15 adds the last lane of rows 0 and 2 into rows 1 and 3,
@@ -194,9 +207,10 @@ __device__ __forceinline__ void seq_steps(F &f, int q, int q1, bool &more) {
 // q+kDist are fetched.  The fetch of token t sees every store up to token t-kDist; the
 // stores of the kDist-1 tokens after that come later, so the updated own-change rows of
 // those tokens stay in registers, and a token whose word matches one of them takes the
-// latest such row instead of its fetched one.  Fetches past the last token re-read the
-// last one and are never used, which keeps every fetch unconditional (so the waits before
-// a use count exactly the newer loads).
+// latest such row instead of its fetched one.  Fetches past the last token read the
+// last token's word (the record block repeats it) and topic entries past it (the topic
+// array has kDist entries of padding) and are never used, which keeps every fetch
+// unconditional (so the waits before a use count exactly the newer loads).
 //
 // The token records come in blocks of 64, one per lane (a vector load), read with lane
 // reads: the block at base holds tokens base .. base+63 and serves the tokens base ..
@@ -253,18 +267,17 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
   auto field = [&](int i, int f) { return __builtin_amdgcn_readlane(rv[f], i - base); };
 #pragma unroll
   for (int i = 0; i < kDist; ++i) {
-    const int qi = min(i, last);
-    fetch_rows<KPL>(view, mydelta, mytag, z, K, koff, field(qi, 0), qi, rows[i]);
+    fetch_rows<KPL>(view, mydelta, mytag, z, K, koff, field(i, 0), i, rows[i]);
     __builtin_amdgcn_sched_barrier(0);
   }
   // the last F tokens' words (-1: none), row validity and updated own-change rows, latest first
   int fw[F > 0 ? F : 1];
-  bool fvalid[F > 0 ? F : 1];
+  int fvalid[F > 0 ? F : 1];
   int fdw[F > 0 ? F : 1][KPL];
 #pragma unroll
   for (int i = 0; i < F; ++i) {
     fw[i] = -1;
-    fvalid[i] = false;
+    fvalid[i] = 0;
 #pragma unroll
     for (int j = 0; j < KPL; ++j) fdw[i][j] = 0;
   }
@@ -273,7 +286,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     constexpr int C = decltype(phase)::value;
     const int w = field(i, 0), d = field(i, 1);
     const int k0 = __builtin_amdgcn_readfirstlane(rows[C].z);
-    bool valid = __builtin_amdgcn_readfirstlane(rows[C].tag) == a.tagc;
+    int valid = __builtin_amdgcn_readfirstlane(rows[C].tag) == a.tagc;
     int dw[KPL];
 #pragma unroll
     for (int j = 0; j < KPL; ++j) dw[j] = rows[C].dw[j];
@@ -286,10 +299,11 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
         for (int j = 0; j < KPL; ++j) dw[j] = fdw[f][j];
       }
     }
-    if (!valid) {
+    // an own-change row from an older clock reads as zero (an and with a uniform mask keeps
+    // the validity an integer rather than a lane mask)
+    const int vmask = -valid;
 #pragma unroll
-      for (int j = 0; j < KPL; ++j) dw[j] = 0;
-    }
+    for (int j = 0; j < KPL; ++j) dw[j] &= vmask;
     if (d != cur_doc) {
       if (cur_doc >= 0) {
         int32_t *old = a.ndk + static_cast<int64_t>(cur_doc) * K;
@@ -338,7 +352,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     const uint64_t excl = wave_scan(acc, &total) - acc;
     int k1 = k0;
     if (total != 0) {  // always: the largest weight is at least 2^shift0
-      const uint64_t target = __umul64hi(readlane_u64(rnd, i - base), total);
+      const uint64_t target = umulhi64_vec(readlane_u64(rnd, i - base), total);
       const uint64_t m = __ballot(excl + acc > target);
       const int L = __ffsll(static_cast<unsigned long long>(m)) - 1;  // m != 0: the last lane's sum is the total
       int jj = KPL - 1;
@@ -376,13 +390,12 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     }
     if constexpr (F > 0) {
       fw[0] = w;
-      fvalid[0] = valid || changed;
+      fvalid[0] = valid | static_cast<int>(changed);
 #pragma unroll
       for (int j = 0; j < KPL; ++j) fdw[0][j] = dw[j];
     }
     constexpr int NF = (C + kDist) % R;
-    const int qf = min(i + kDist, last);
-    fetch_rows<KPL>(view, mydelta, mytag, z, K, koff, field(qf, 0), qf, rows[NF]);
+    fetch_rows<KPL>(view, mydelta, mytag, z, K, koff, field(i + kDist, 0), i + kDist, rows[NF]);
   };
   // whole rotations without an exit inside (an exit path would join the loop's back edge
   // with its latest fetch still in flight, and the wait at the top of the loop would then
@@ -848,7 +861,8 @@ int load_tokens(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int3
   }
   const int64_t stride = slot_stride(h), ns = h->s + 2;
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->rec), sizeof(int4) * n))) return rc;
-  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->z), sizeof(int32_t) * n))) return rc;
+  // kDist entries past the end: a worker's fetches past its last token read them (unused)
+  if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->z), sizeof(int32_t) * (n + kDist)))) return rc;
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->ndk), sizeof(int32_t) * h->D * K))) return rc;
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->ring), sizeof(int32_t) * stride * ns))) return rc;
   if ((rc = lda_alloc(h, reinterpret_cast<void **>(&h->delta), sizeof(int32_t) * P * V * K))) return rc;
