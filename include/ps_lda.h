@@ -66,6 +66,9 @@ typedef struct ps_lda ps_lda_t;
 #define PS_LDA_OPT_SEED 3      /* 64-bit seed of the block hash and the draws (default 0) */
 #define PS_LDA_OPT_HOST_ONLY 4 /* 1: build and export the token layout only; never touch a device */
 #define PS_LDA_OPT_TIMING 5    /* 1: HIP events around every sampling kernel (ps_lda_kernel_time) */
+#define PS_LDA_OPT_FLAT_ADDRESSING 6 /* 1: the sampling kernel addresses its tables with 64-bit
+                                        offsets (default 0: 32-bit buffer offsets whenever every
+                                        table is under 2 GiB, 64-bit otherwise); same results */
 
 #define PS_LDA_SSP_LAZY 0
 #define PS_LDA_SSP_WORST 1

@@ -69,7 +69,7 @@ struct SweepArgs {
   int32_t *tot;         // P x K: each worker's topic-total changes of the clock
   const int64_t *wbeg;  // P+1 block positions of this clock's block
   int64_t slot_stride;  // (V+1) * K
-  int64_t V;
+  int64_t V, D;
   int64_t c;
   double alpha, beta, Vbeta;
   uint64_t seed;
@@ -157,36 +157,64 @@ struct TokenRows {
   int tag, z;
 };
 
-// a row's element at a byte offset from the row's start: a uniform base with a 32-bit lane
-// offset, i.e. the scalar-base form of the global memory instructions (the empty asm keeps
-// the offset's widening next to its use, where instruction selection folds it into that
-// form, instead of hoisted out of the loop as a 64-bit lane address)
-__device__ __forceinline__ uint32_t lane_off(uint32_t off) {
-  asm("" : "+v"(off));
-  return off;
-}
-__device__ __forceinline__ int32_t &at(int32_t *row, uint32_t off) {
-  return *reinterpret_cast<int32_t *>(reinterpret_cast<char *>(row) + lane_off(off));
-}
-__device__ __forceinline__ int32_t at(const int32_t *row, uint32_t off) {
-  return *reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(row) + lane_off(off));
-}
+// A table of int32 counts read and written at (row offset + lane offset) bytes.  The buffer
+// form (Buf = true) goes through a buffer resource (CDNA word 3 0x00020000: raw, untyped
+// dword access): a 32-bit lane offset (the topic) plus a 32-bit uniform offset (the row), so
+// that a row's address costs one scalar multiply; the host picks it when every such table
+// is under 2^31 bytes.  The flat form takes 64-bit row offsets for larger tables.
+template <bool Buf>
+struct Table;
+
+template <>
+struct Table<true> {
+  using Off = uint32_t;
+  __amdgpu_buffer_rsrc_t rs;
+  __device__ __forceinline__ Table(const int32_t *base, int64_t num_bytes)
+      : rs(__builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(base), static_cast<short>(0),
+                                             static_cast<int>(static_cast<uint32_t>(num_bytes)), 0x00020000)) {}
+  __device__ __forceinline__ int ld(uint32_t lane_off, Off row_off) const {
+    return static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<int>(lane_off), static_cast<int>(row_off), 0));
+  }
+  __device__ __forceinline__ int ld(Off row_off) const {
+    return static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(rs, 0, static_cast<int>(row_off), 0));
+  }
+  __device__ __forceinline__ void st(int v, uint32_t lane_off, Off row_off) const {
+    __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(v), rs, static_cast<int>(lane_off), static_cast<int>(row_off), 0);
+  }
+  __device__ __forceinline__ void st(int v, Off row_off) const {
+    __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(v), rs, 0, static_cast<int>(row_off), 0);
+  }
+};
+
+template <>
+struct Table<false> {
+  using Off = uint64_t;
+  char *base;
+  __device__ __forceinline__ Table(const int32_t *b, int64_t) : base(reinterpret_cast<char *>(const_cast<int32_t *>(b))) {}
+  __device__ __forceinline__ int ld(uint32_t lane_off, Off row_off) const {
+    return *reinterpret_cast<const int32_t *>(base + row_off + lane_off);
+  }
+  __device__ __forceinline__ int ld(Off row_off) const { return *reinterpret_cast<const int32_t *>(base + row_off); }
+  __device__ __forceinline__ void st(int v, uint32_t lane_off, Off row_off) const {
+    *reinterpret_cast<int32_t *>(base + row_off + lane_off) = v;
+  }
+  __device__ __forceinline__ void st(int v, Off row_off) const { *reinterpret_cast<int32_t *>(base + row_off) = v; }
+};
 
 // koff[j]: the byte offset of this lane's topic j in a row (lanes past the last topic
 // re-read topic K-1: every load is issued on every path, so the waits before a use count
-// exactly; their values are masked)
-template <int KPL>
-__device__ __forceinline__ void fetch_rows(const int32_t *view, const int32_t *mydelta, const int32_t *mytag,
-                                           const int32_t *z, int K, const uint32_t (&koff)[KPL], int w, int i,
-                                           TokenRows<KPL> &o) {
-  const int32_t *vrow = view + static_cast<int64_t>(w) * K;
-  const int32_t *drow = mydelta + static_cast<int64_t>(w) * K;
-  o.tag = mytag[w];
-  o.z = z[i];
+// exactly; their values are masked); rb: the word's row offset in bytes
+template <int KPL, bool Buf>
+__device__ __forceinline__ void fetch_rows(const Table<Buf> &view, const Table<Buf> &mydelta, const Table<Buf> &mytag,
+                                           const Table<Buf> &z, const uint32_t (&koff)[KPL],
+                                           typename Table<Buf>::Off rb, int w, int i, TokenRows<KPL> &o) {
+  using Off = typename Table<Buf>::Off;
+  o.tag = mytag.ld(Off{4} * static_cast<uint32_t>(w));
+  o.z = z.ld(Off{4} * static_cast<uint32_t>(i));
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {
-    o.nw[j] = at(vrow, koff[j]);
-    o.dw[j] = at(drow, koff[j]);
+    o.nw[j] = view.ld(koff[j], rb);
+    o.dw[j] = mydelta.ld(koff[j], rb);
   }
 }
 
@@ -222,8 +250,9 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 constexpr int kDist = 3;
 constexpr int kRecStep = 60;  // a multiple of the rotation, at most 64 - kDist
 
-template <int KPL>
+template <int KPL, bool Buf>
 __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
+  using Off = typename Table<Buf>::Off;
   constexpr int R = kDist + 1;  // ring entries
   constexpr int F = kDist - 1;  // forwarded rows
   const int lane = threadIdx.x;
@@ -236,13 +265,16 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
   }
   const int64_t V = a.V, c = a.c;
   const int64_t v = view_of(a.policy, a.s, p, c);
-  const int32_t *view = a.ring + (v % a.nslots) * a.slot_stride;
-  int32_t *mydelta = a.delta + p * V * K;
-  int32_t *mytag = a.tag + p * V;
+  const int32_t *view_p = a.ring + (v % a.nslots) * a.slot_stride;
+  const Table<Buf> view(view_p, a.slot_stride * 4);
+  const Table<Buf> mydelta(a.delta + p * V * K, V * K * 4);
+  const Table<Buf> mytag(a.tag + p * V, V * 4);
+  const Table<Buf> ndk(a.ndk, a.D * K * 4);
   // this worker's tokens of the block, indexed from 0 (a worker has fewer than 2^31)
   const i32x4 *rec = reinterpret_cast<const i32x4 *>(a.rec) + q0;
-  int32_t *z = a.z + q0;
   const int n = static_cast<int>(q1 - q0), last = n - 1;
+  const Table<Buf> z(a.z + q0, (static_cast<int64_t>(n) + kDist) * 4);
+  const Off rowb = Off{4} * static_cast<uint32_t>(K);  // bytes per row
   const uint64_t rbase = a.seed ^ kDrawSalt ^ (static_cast<uint64_t>(c) << 40);
   uint32_t koff[KPL];
 #pragma unroll
@@ -252,7 +284,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {
     const int k = lane * KPL + j;
-    vk[j] = k < K ? view[V * K + k] : 0;
+    vk[j] = k < K ? view_p[V * K + k] : 0;
     dk[j] = 0;
     nd[j] = 0;
   }
@@ -267,7 +299,8 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
   auto field = [&](int i, int f) { return __builtin_amdgcn_readlane(rv[f], i - base); };
 #pragma unroll
   for (int i = 0; i < kDist; ++i) {
-    fetch_rows<KPL>(view, mydelta, mytag, z, K, koff, field(i, 0), i, rows[i]);
+    const int wi = field(i, 0);
+    fetch_rows<KPL, Buf>(view, mydelta, mytag, z, koff, rowb * static_cast<Off>(wi), wi, i, rows[i]);
     __builtin_amdgcn_sched_barrier(0);
   }
   // the last F tokens' words (-1: none), row validity and updated own-change rows, latest first
@@ -306,15 +339,13 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     for (int j = 0; j < KPL; ++j) dw[j] &= vmask;
     if (d != cur_doc) {
       if (cur_doc >= 0) {
-        int32_t *old = a.ndk + static_cast<int64_t>(cur_doc) * K;
 #pragma unroll
         for (int j = 0; j < KPL; ++j)
-          if (lane * KPL + j < K) at(old, koff[j]) = nd[j];
+          if (lane * KPL + j < K) ndk.st(nd[j], koff[j], rowb * static_cast<Off>(cur_doc));
       }
-      const int32_t *row = a.ndk + static_cast<int64_t>(d) * K;
 #pragma unroll
       for (int j = 0; j < KPL; ++j) {
-        const int x = at(row, koff[j]);
+        const int x = ndk.ld(koff[j], rowb * static_cast<Off>(d));
         nd[j] = lane * KPL + j < K ? x : 0;
       }
       cur_doc = d;
@@ -363,7 +394,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     }
     const bool changed = k1 != k0;
     if (changed) {
-      int32_t *drow = mydelta + static_cast<int64_t>(w) * K;
+      const Off rb = rowb * static_cast<Off>(w);
 #pragma unroll
       for (int j = 0; j < KPL; ++j) {
         const int k = lane * KPL + j;
@@ -372,12 +403,12 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
         dk[j] += dl;
         dw[j] += dl;
         if (k < K) {
-          if (!valid || dl != 0) at(drow, koff[j]) = dw[j];
+          if (!valid || dl != 0) mydelta.st(dw[j], koff[j], rb);
         }
       }
       if (lane == 0) {
-        z[i] = k1;
-        if (!valid) mytag[w] = a.tagc;
+        z.st(k1, Off{4} * static_cast<uint32_t>(i));
+        if (!valid) mytag.st(a.tagc, Off{4} * static_cast<uint32_t>(w));
       }
     }
     // this token becomes the latest forwarded row
@@ -395,7 +426,8 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
       for (int j = 0; j < KPL; ++j) fdw[0][j] = dw[j];
     }
     constexpr int NF = (C + kDist) % R;
-    fetch_rows<KPL>(view, mydelta, mytag, z, K, koff, field(i + kDist, 0), i + kDist, rows[NF]);
+    const int wf = field(i + kDist, 0);
+    fetch_rows<KPL, Buf>(view, mydelta, mytag, z, koff, rowb * static_cast<Off>(wf), wf, i + kDist, rows[NF]);
   };
   // whole rotations without an exit inside (an exit path would join the loop's back edge
   // with its latest fetch still in flight, and the wait at the top of the loop would then
@@ -418,12 +450,11 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     bool more = true;
     seq_steps<0, R - 1>(step, i, n, more);
   }
-  int32_t *drow_end = a.ndk + static_cast<int64_t>(cur_doc) * K;
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {
     const int k = lane * KPL + j;
     if (k < K) {
-      at(drow_end, koff[j]) = nd[j];
+      ndk.st(nd[j], koff[j], rowb * static_cast<Off>(cur_doc));
       a.tot[p * K + k] = dk[j];
     }
   }
@@ -568,6 +599,7 @@ struct ps_lda {
   int32_t policy = PS_LDA_ESSP, B = 2;
   uint64_t seed = 0;
   bool host_only = false, timing = false, loaded = false;
+  bool flat = false;  // 64-bit addresses in the sampling kernel even where the buffer form fits
   int64_t clock = 0, ntok = 0;
   int device = -1;
   hipStream_t stream = nullptr, user_stream = nullptr;
@@ -647,8 +679,9 @@ int lda_device(ps_lda_t *h) {
 int64_t slot_stride(const ps_lda_t *h) { return (h->V + 1) * h->K; }
 
 template <int KPL>
-void launch_sweep(const SweepArgs &a, int P, hipStream_t st) {
-  hipLaunchKernelGGL(k_lda_sweep<KPL>, dim3(P), dim3(kWave), 0, st, a);
+void launch_sweep(const SweepArgs &a, int P, bool flat, hipStream_t st) {
+  if (flat) hipLaunchKernelGGL((k_lda_sweep<KPL, false>), dim3(P), dim3(kWave), 0, st, a);
+  else hipLaunchKernelGGL((k_lda_sweep<KPL, true>), dim3(P), dim3(kWave), 0, st, a);
 }
 
 template <int KPL>
@@ -672,6 +705,7 @@ int sweep(ps_lda_t *h) {
   a.wbeg = h->wbeg_dev + b * (h->P + 1);
   a.slot_stride = stride;
   a.V = h->V;
+  a.D = h->D;
   a.c = c;
   a.alpha = h->alpha;
   a.beta = h->beta;
@@ -685,20 +719,24 @@ int sweep(ps_lda_t *h) {
   while ((int64_t{1} << clog2k) < h->K) ++clog2k;
   a.shift0 = 62 - clog2k;
   a.tagc = static_cast<int32_t>(c + 1);
+  // the buffer form of the sampling kernel's tables needs each under 2^31 bytes: the ring
+  // slot, a worker's own-change rows and row tags, the doc-topic rows and a worker's topics
+  const int64_t big = std::max({stride, h->V * h->K, h->D * h->K, h->ntok + kDist}) * 4;
+  const bool flat = h->flat || big >= (int64_t{1} << 31);
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (h->timing) {
     LDA_TRY(h, hipEventCreate(&e0));
     LDA_TRY(h, hipEventRecord(e0, h->stream));
   }
   switch ((h->K + kWave - 1) / kWave) {
-    case 1: launch_sweep<1>(a, h->P, h->stream); break;
-    case 2: launch_sweep<2>(a, h->P, h->stream); break;
-    case 3: launch_sweep<3>(a, h->P, h->stream); break;
-    case 4: launch_sweep<4>(a, h->P, h->stream); break;
-    case 5: launch_sweep<5>(a, h->P, h->stream); break;
-    case 6: launch_sweep<6>(a, h->P, h->stream); break;
-    case 7: launch_sweep<7>(a, h->P, h->stream); break;
-    default: launch_sweep<8>(a, h->P, h->stream); break;
+    case 1: launch_sweep<1>(a, h->P, flat, h->stream); break;
+    case 2: launch_sweep<2>(a, h->P, flat, h->stream); break;
+    case 3: launch_sweep<3>(a, h->P, flat, h->stream); break;
+    case 4: launch_sweep<4>(a, h->P, flat, h->stream); break;
+    case 5: launch_sweep<5>(a, h->P, flat, h->stream); break;
+    case 6: launch_sweep<6>(a, h->P, flat, h->stream); break;
+    case 7: launch_sweep<7>(a, h->P, flat, h->stream); break;
+    default: launch_sweep<8>(a, h->P, flat, h->stream); break;
   }
   LDA_TRY(h, hipGetLastError());
   if (h->timing) {
@@ -767,6 +805,9 @@ int ps_lda_set_option(ps_lda_t *h, int32_t key, int64_t value) {
       return PS_LDA_OK;
     case PS_LDA_OPT_TIMING:
       h->timing = value != 0;
+      return PS_LDA_OK;
+    case PS_LDA_OPT_FLAT_ADDRESSING:
+      h->flat = value != 0;
       return PS_LDA_OK;
     default:
       return lda_fail(h, PS_LDA_EINVAL, "unknown option %d", key);

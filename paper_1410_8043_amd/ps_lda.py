@@ -15,7 +15,7 @@ from paper_1410_8043_amd import ps_mf as _mf
 
 LIB_PATH = _mf.LIB_PATH
 OK, EINVAL, ENOMEM, EDEVICE, ESTATE = 0, -1, -2, -3, -4
-OPT_POLICY, OPT_MB_BLOCKS, OPT_SEED, OPT_HOST_ONLY, OPT_TIMING = range(1, 6)
+OPT_POLICY, OPT_MB_BLOCKS, OPT_SEED, OPT_HOST_ONLY, OPT_TIMING, OPT_FLAT_ADDRESSING = range(1, 7)
 SSP_LAZY, SSP_WORST, ESSP = 0, 1, 2
 X_Z, X_NDK, X_NWK, X_VERSION_LOG, X_BLOCK_ORDER = range(5)
 
@@ -78,11 +78,11 @@ class PsLda:
     """One handle: create, set options, load tokens, run clocks, read the state back."""
 
     def __init__(self, D, V, K, P, s, alpha, beta, policy=ESSP, B=2, seed=0, host_only=False, timing=False,
-                 stream=None):
+                 stream=None, flat=False):
         self.D, self.V, self.K, self.P, self.s, self.B = int(D), int(V), int(K), int(P), int(s), int(B)
         self._h = ps_lda_create(D, V, K, P, s, alpha, beta)
         for key, val in ((OPT_POLICY, policy), (OPT_MB_BLOCKS, B), (OPT_SEED, int(seed) & (2**64 - 1)),
-                         (OPT_HOST_ONLY, int(host_only)), (OPT_TIMING, int(timing))):
+                         (OPT_HOST_ONLY, int(host_only)), (OPT_TIMING, int(timing)), (OPT_FLAT_ADDRESSING, int(flat))):
             if key == OPT_SEED and val >= 2**63:
                 val -= 2**64  # the C side takes the 64 bits as int64_t
             _check(self._h, "ps_lda_set_option", _lib.ps_lda_set_option(self._h, key, int(val)))

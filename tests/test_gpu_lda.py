@@ -84,6 +84,14 @@ def test_extreme_weight_ratios(lda, alpha):
     both(lda, spec, lc.generate(spec), oracle.ESSP, 6, check_every=2)
 
 
+@pytest.mark.parametrize("K", [2, 100, 256, 512])
+@pytest.mark.parametrize("policy", POLICIES)
+def test_flat_addressing_bit_exact(lda, policy, K):
+    # the 64-bit form of the sampling kernel (used for tables over 2 GiB), forced on small ones
+    spec = lc.scaled(lc.CORPORA["tiny"], 1.0, K=K, P=5, s=2, B=2)
+    both(lda, spec, lc.generate(spec), policy, 6, check_every=3, flat=True)
+
+
 def test_more_workers_than_documents(lda):
     spec = lc.scaled(lc.CORPORA["tiny"], 1.0, D=40, P=300, s=2)
     both(lda, spec, lc.generate(spec), oracle.SSP_LAZY, 6)

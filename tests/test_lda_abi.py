@@ -24,6 +24,14 @@ def test_library_exports_every_declared_lda_symbol():
     assert set(names) == set(ps_lda.SYMBOLS)
 
 
+def test_option_and_export_keys_match_the_header():
+    text = open(os.path.join(ROOT, "include", "ps_lda.h")).read()
+    keys = dict(re.findall(r"#define PS_LDA_((?:OPT|X)_[A-Z_]+) (\d+)", text))
+    assert len(keys) == 11
+    for name, value in keys.items():
+        assert getattr(ps_lda, name) == int(value), name
+
+
 @pytest.mark.parametrize("args", [
     (0, 5, 2, 1, 0, 0.1, 0.1), (5, 0, 2, 1, 0, 0.1, 0.1), (5, 5, 0, 1, 0, 0.1, 0.1), (5, 5, 513, 1, 0, 0.1, 0.1),
     (5, 5, 2, 0, 0, 0.1, 0.1), (5, 5, 2, 1, -1, 0.1, 0.1), (5, 5, 2, 1, 0, 0.0, 0.1), (5, 5, 2, 1, 0, 0.1, -1.0),
