@@ -248,7 +248,7 @@ __device__ __forceinline__ void seq_steps(F &f, int q, int q1, bool &more) {
 // every token: a wait for a scalar load waits for all of them.)
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 constexpr int kDist = 3;
-constexpr int kRecStep = 60;  // a multiple of the rotation, at most 64 - kDist
+constexpr int kRecStep = (64 - kDist) / (kDist + 1) * (kDist + 1);  // a multiple of the rotation, at most 64 - kDist
 
 template <int KPL, bool Buf>
 __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
