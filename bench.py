@@ -73,7 +73,9 @@ def parse():
     ap.add_argument("--heavy-min", type=int, default=None, help="ratings from which a user goes to the cells")
     ap.add_argument("--two-streams", type=int, default=None, help="1/0: units on a second stream beside the cells")
     ap.add_argument("--sweep-graphs", type=int, default=None,
-                    help="1/0: replay each clock's sweep launches from a captured HIP graph (default: 1)")
+                    help="1/0: replay each clock's sweep launches from a captured HIP graph (default: 0)")
+    ap.add_argument("--unit-commit", type=int, default=None,
+                    help="1/0: a user's only work unit writes its new version (default: 1)")
     ap.add_argument("--hot-steps", type=int, default=None,
                     help="LDS sub-tiles of the most rated items whose light-user ratings go to cells (-1: auto)")
     ap.add_argument("--dense-min", type=int, default=None,
@@ -315,7 +317,7 @@ def measure_mf(args, spec, w, s, policy, step, stream, announce=True):
                    mb_seed=spec.seed, timing=not args.no_timing, stream=stream, tile_bytes=args.tile_bytes,
                    unit_max=args.unit_max, cells=args.cells, heavy_min=args.heavy_min, hot_steps=args.hot_steps,
                    two_streams=args.two_streams, dense_min=args.dense_min, item_tile_bytes=args.item_tile_bytes,
-                   sweep_graphs=args.sweep_graphs)
+                   sweep_graphs=args.sweep_graphs, unit_commit=args.unit_commit)
     t_load = time.perf_counter()
     g.load_ratings(w.user, w.item, w.val)
     g.set_factors(w.L0, w.R0)

@@ -131,6 +131,12 @@ typedef struct ps_mf ps_mf_t;
                                      one by one.  0 (default): launch them one by one (measured
                                      faster on ROCm 7: the replay's cross-stream edges cost more
                                      than the launches they replace) */
+#define PS_MF_OPT_UNIT_COMMIT 21 /* 1 (default): under the fixed-view steps, a user whose ratings of
+                                    the block all lie in one work unit has its new version written
+                                    by that unit (the commit's formula, same arithmetic) when its
+                                    view is not the new version's ring slot, and the commit skips
+                                    it; 0 (and with PS_MF_OPT_SWEEP_GRAPHS): every user through
+                                    the commit.  Same results */
 
 /* Views (Section 3.2 SSP condition; Section 4 ESSPTable).  The table-level policies give
    worker p at clock c one whole version v = max(0, c - d):

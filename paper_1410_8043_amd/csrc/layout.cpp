@@ -83,6 +83,8 @@ void build_units(int64_t nb, int64_t nx, int64_t ntiles, const std::function<int
   for (const Unit &u : units) ucnt[u.x] += 1;
   U.x_pp.assign(static_cast<size_t>(nx) + 1, 0);
   for (int64_t x = 0; x < nx; ++x) U.x_pp[x + 1] = U.x_pp[x] + ucnt[x] + (extra.empty() ? 0 : extra[x]);
+  U.sole.assign(static_cast<size_t>(nx), 0);
+  for (int64_t x = 0; x < nx; ++x) U.sole[x] = ucnt[x] == 1 && (extra.empty() || extra[x] == 0);
   cell_base.assign(static_cast<size_t>(nx), 0);
   for (int64_t x = 0; x < nx; ++x) cell_base[x] = U.x_pp[x] + ucnt[x];
   const int64_t spare = U.x_pp[nx];

@@ -56,6 +56,7 @@ struct UnitSet {
   std::vector<int64_t> unit_beg;
   std::vector<int64_t> xcd_off;   // [kXcds + 1]
   std::vector<int64_t> x_pp;      // [rows of x + 1]
+  std::vector<uint8_t> sole;      // [rows of x]: 1 where x's only partial row is one unit's
   int64_t ntiles = 0;
   int64_t nreal = 0;              // units with ratings; empty padding units write partial row nreal
 };

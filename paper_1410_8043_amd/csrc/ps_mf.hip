@@ -244,7 +244,22 @@ struct UnitArgs {
   // slot), tables of rows_per_class entries per worker class (0: one entry per row)
   const int32_t *rs_x, *rs_y;
   int64_t rs_x_cls, rs_y_cls;
+  // user-major units: sole[x] = 1 where x's only partial row is one unit's.  Such a unit
+  // writes x's new version itself (as the commit would) when x's view is not the new
+  // version's slot: no one reads x's row of that slot during the sweep.  Null: never.
+  const uint8_t *sole;
+  const int32_t *xcount;    // [x] ratings of x in the block
+  int32_t slot_c, slot_n;
+  const float *base_rows;   // the x table of version c (slot_c)
+  float *new_rows;          // the x table of version c + 1 (slot_n)
+  float eta, lambda;
+  int32_t rowmean;
 };
+
+// one element of a committed row: base + scale (sum of partial rows - n lambda view)
+__device__ __forceinline__ float commit_elem(float base, float sc, float d, float nl, float view) {
+  return fmaf(sc, fmaf(-nl, view, d), base);
+}
 
 // The unit processed by lane group `grp` of workgroup `block` (counted within its sweep;
 // the first sweep's grid is a multiple of 8, so workgroup b of either sweep runs on XCD
@@ -298,11 +313,9 @@ __device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g)
   const i32x4 *__restrict__ yi = reinterpret_cast<const i32x4 *>(a.y + beg);
   const f32x4 *__restrict__ vr = reinterpret_cast<const f32x4 *>(a.val + beg);
   float x[E], acc[E];
-  {
-    const int32_t xr = a.unit_x[unit];
-    const int64_t xs = PerRow ? a.rs_x[cls * a.rs_x_cls + xr] : sv;
-    load_row_once<G, E>(x, a.ring + xs * a.slot_stride + a.x_off + static_cast<int64_t>(xr) * Kp, g);
-  }
+  const int32_t xr = a.unit_x[unit];
+  const int64_t xs = PerRow ? a.rs_x[cls * a.rs_x_cls + xr] : sv;
+  load_row_once<G, E>(x, a.ring + xs * a.slot_stride + a.x_off + static_cast<int64_t>(xr) * Kp, g);
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
   // the next 8 (row, value) pairs are loaded while the current 8 are swept
@@ -342,7 +355,24 @@ __device__ __forceinline__ void run_unit(const UnitArgs &a, int64_t unit, int g)
       }
     }
   }
-  store_row_once<G, E>(a.partial + static_cast<int64_t>(a.unit_out[unit]) * Kp, acc, g);
+  if (a.sole && n > 0 && a.sole[xr] && xs != a.slot_n) {
+    // x's new version, exactly as the commit forms it from one partial row
+    float base[E];
+    if (xs == a.slot_c) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) base[e] = x[e];
+    } else {
+      load_row_once<G, E>(base, a.base_rows + static_cast<int64_t>(xr) * Kp, g);
+    }
+    const int cnt = a.xcount[xr];
+    const float sc = a.rowmean ? a.eta / static_cast<float>(cnt) : a.eta;
+    const float nl = static_cast<float>(cnt) * a.lambda;
+#pragma unroll
+    for (int e = 0; e < E; ++e) base[e] = commit_elem(base[e], sc, acc[e] + 0.f, nl, x[e]);
+    store_row_once<G, E>(a.new_rows + static_cast<int64_t>(xr) * Kp, base, g);
+  } else {
+    store_row_once<G, E>(a.partial + static_cast<int64_t>(a.unit_out[unit]) * Kp, acc, g);
+  }
 }
 
 struct CellArgs {
@@ -898,6 +928,7 @@ struct FinalArgs {
   float eta, lambda;
   int32_t rowmean;
   const int32_t *rs_u;     // per-row policies: ring slot of each user row's view (null: class slot)
+  const uint8_t *sole;     // users whose unit writes the new version (when its view slot is not slot_n)
 };
 
 // L^{c+1}_i = L^c_i + scale_i (sum of i's partial rows - n_i lambda L^v_i): the lambda term
@@ -915,6 +946,8 @@ __device__ __forceinline__ void finalize_users(const FinalArgs &a, int64_t idx) 
     if (a.slot_n != a.slot_c) ring4[a.slot_n * ss4 + idx] = ring4[a.slot_c * ss4 + idx];
     return;
   }
+  const int32_t sv = a.rs_u ? a.rs_u[i] : a.cls_slot[a.ucls[i]];
+  if (a.sole && a.sole[i] && sv != a.slot_n) return;  // its unit wrote the new version
   const f32x4 *part4 = reinterpret_cast<const f32x4 *>(a.partial);
   const int64_t k4 = idx - i * q4;
   float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -924,11 +957,11 @@ __device__ __forceinline__ void finalize_users(const FinalArgs &a, int64_t idx) 
     d.x += t[0]; d.y += t[1]; d.z += t[2]; d.w += t[3];
   }
   const float4 lc = ring4[a.slot_c * ss4 + idx];
-  const float4 lv = ring4[(a.rs_u ? a.rs_u[i] : a.cls_slot[a.ucls[i]]) * ss4 + idx];
+  const float4 lv = ring4[sv * ss4 + idx];
   const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
   const float nl = static_cast<float>(n) * a.lambda;
-  ring4[a.slot_n * ss4 + idx] = make_float4(lc.x + sc * (d.x - nl * lv.x), lc.y + sc * (d.y - nl * lv.y),
-                                            lc.z + sc * (d.z - nl * lv.z), lc.w + sc * (d.w - nl * lv.w));
+  ring4[a.slot_n * ss4 + idx] = make_float4(commit_elem(lc.x, sc, d.x, nl, lv.x), commit_elem(lc.y, sc, d.y, nl, lv.y),
+                                            commit_elem(lc.z, sc, d.z, nl, lv.z), commit_elem(lc.w, sc, d.w, nl, lv.w));
 }
 
 struct CommitArgs {
@@ -1058,8 +1091,8 @@ __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, 
 }
 
 // Debug check of the commit (PS_MF_OPT_POISON): before the commit of clock c, every row of
-// the new version's slot that the commit will not read is set to NaN, so that a row the
-// commit fails to write stays NaN.  The commit reads the new slot (which held version c-s)
+// the new version's slot that the commit will not read is set to NaN (but the user rows the
+// work units wrote in the sweep), so that a row the commit fails to write stays NaN.  The commit reads the new slot (which held version c-s)
 // where a view is version c-s: a user row with ratings whose view slot is the new slot, an
 // item row with a rating by a worker class whose view slot is the new slot.  One thread
 // per float4 of the slot.
@@ -1071,7 +1104,9 @@ __global__ __launch_bounds__(kBlock) void k_poison(FinalArgs fa, CommitArgs ca) 
   bool read = false;
   if (row < fa.users) {
     const int64_t i = row;
-    read = fa.ucount[i] > 0 && (fa.rs_u ? fa.rs_u[i] : fa.cls_slot[fa.ucls[i]]) == fa.slot_n;
+    const int32_t sv = fa.rs_u ? fa.rs_u[i] : fa.cls_slot[fa.ucls[i]];
+    read = fa.ucount[i] > 0 && sv == fa.slot_n;
+    if (fa.sole && fa.ucount[i] > 0 && fa.sole[i] && sv != fa.slot_n) return;  // its unit wrote the new row
   } else {
     const int64_t j = row - fa.users;
     if (ca.icount[j] > 0)
@@ -1520,6 +1555,7 @@ struct DeviceUnits {
   float *val = nullptr;
   int32_t *unit_x = nullptr, *unit_cls = nullptr, *unit_len = nullptr, *unit_out = nullptr;
   int64_t *unit_beg = nullptr, *xcd_off = nullptr, *x_pp = nullptr;
+  uint8_t *sole = nullptr;  // user-major set: rows whose only partial row is one unit's
 };
 
 struct DeviceCells {
@@ -1582,6 +1618,7 @@ struct ps_mf {
   bool seq_graphs = true;        // replay each clock's sub-epoch launches from a captured HIP graph
   std::vector<hipGraphExec_t> seq_exec;  // per (block, slot-table row)
   bool sweep_graphs = false;     // replay each clock's sweep launches from a captured HIP graph
+  bool unit_commit = true;       // a user's only unit writes its new version (see UnitArgs::sole)
   std::vector<hipGraphExec_t> sweep_exec;  // per (block, slot-table row)
   std::vector<int32_t> owner;
   // host state
@@ -2101,6 +2138,45 @@ int one_clock(ps_mf_t *h) {
   const int64_t r_off = h->N * h->Kp;
   const int rowmean = h->step == PS_MF_STEP_ROWMEAN;
 
+  // the commit's arguments (the sweep's work units take the direct-write part of them)
+  FinalArgs fa{};
+  fa.ring = h->ring;
+  fa.slot_stride = slot_stride;
+  fa.users = h->N;
+  fa.Kp = h->Kp;
+  fa.slot_c = slot_c;
+  fa.slot_n = slot_n;
+  fa.ucount = db.ucount;
+  fa.ucls = h->ucls;
+  fa.cls_slot = cls_slot;
+  fa.partial = h->partial_u;
+  fa.user_pp = db.by_user.x_pp;
+  fa.eta = eta_at(h, c);
+  fa.lambda = h->lambda;
+  fa.rowmean = rowmean;
+  fa.rs_u = per_row_policy(h) ? h->slot_u : nullptr;
+  // (not inside a captured sweep graph: its launches would replay this clock's slots and eta)
+  fa.sole = h->unit_commit && !h->sweep_graphs ? db.by_user.sole : nullptr;
+  const int64_t nfin = h->N * h->Kp / 4;
+  CommitArgs ca{};
+  ca.ring = h->ring;
+  ca.slot_stride = slot_stride;
+  ca.r_off = r_off;
+  ca.items = h->M;
+  ca.Kp = h->Kp;
+  ca.slot_c = slot_c;
+  ca.slot_n = slot_n;
+  ca.icount = db.icount;
+  ca.icount_cls = db.icount_cls;
+  ca.nclass = h->nclass;
+  ca.cls_slot = cls_slot;
+  ca.partial = h->partial_i;
+  ca.item_pp = db.by_item.x_pp;
+  ca.eta = eta_at(h, c);
+  ca.lambda = h->lambda;
+  ca.rowmean = rowmean;
+  ca.rs_i = per_row_policy(h) ? h->slot_i : nullptr;
+  const int64_t grid_users = (nfin + kBlock - 1) / kBlock, grid_items = h->M;
   hipEvent_t ev = nullptr;
   if ((rc = record(h, &ev))) return rc;
   if (per_row_policy(h) && (rc = row_views(h, db, c))) return rc;
@@ -2118,6 +2194,17 @@ int one_clock(ps_mf_t *h) {
     us.ub = unit_args(h, db.by_item, h->partial_i, r_off, 0, h->N);
     us.ua.cls_slot = cls_slot;
     us.ub.cls_slot = cls_slot;
+    if (fa.sole) {
+      us.ua.sole = fa.sole;
+      us.ua.xcount = db.ucount;
+      us.ua.slot_c = slot_c;
+      us.ua.slot_n = slot_n;
+      us.ua.base_rows = h->ring + slot_c * slot_stride;
+      us.ua.new_rows = h->ring + slot_n * slot_stride;
+      us.ua.eta = fa.eta;
+      us.ua.lambda = fa.lambda;
+      us.ua.rowmean = fa.rowmean;
+    }
     set_row_slots(h, us.ua, true);
     set_row_slots(h, us.ub, false);
     const int64_t gu = db.by_user.nunits > 0 ? db.by_user.grid : 0;
@@ -2200,42 +2287,6 @@ int one_clock(ps_mf_t *h) {
   if ((rc = record_end(h, PS_MF_KERNEL_SWEEP, ev))) return rc;
 
   if ((rc = record(h, &ev))) return rc;
-  FinalArgs fa{};
-  fa.ring = h->ring;
-  fa.slot_stride = slot_stride;
-  fa.users = h->N;
-  fa.Kp = h->Kp;
-  fa.slot_c = slot_c;
-  fa.slot_n = slot_n;
-  fa.ucount = db.ucount;
-  fa.ucls = h->ucls;
-  fa.cls_slot = cls_slot;
-  fa.partial = h->partial_u;
-  fa.user_pp = db.by_user.x_pp;
-  fa.eta = eta_at(h, c);
-  fa.lambda = h->lambda;
-  fa.rowmean = rowmean;
-  fa.rs_u = per_row_policy(h) ? h->slot_u : nullptr;
-  const int64_t nfin = h->N * h->Kp / 4;
-  CommitArgs ca{};
-  ca.ring = h->ring;
-  ca.slot_stride = slot_stride;
-  ca.r_off = r_off;
-  ca.items = h->M;
-  ca.Kp = h->Kp;
-  ca.slot_c = slot_c;
-  ca.slot_n = slot_n;
-  ca.icount = db.icount;
-  ca.icount_cls = db.icount_cls;
-  ca.nclass = h->nclass;
-  ca.cls_slot = cls_slot;
-  ca.partial = h->partial_i;
-  ca.item_pp = db.by_item.x_pp;
-  ca.eta = eta_at(h, c);
-  ca.lambda = h->lambda;
-  ca.rowmean = rowmean;
-  ca.rs_i = per_row_policy(h) ? h->slot_i : nullptr;
-  const int64_t grid_users = (nfin + kBlock - 1) / kBlock, grid_items = h->M;
   if (h->poison && slot_n != slot_c) {
     const int64_t n4 = (h->N + h->M) * (h->Kp / 4);
     hipLaunchKernelGGL(k_poison, dim3(static_cast<unsigned>((n4 + kBlock - 1) / kBlock)), dim3(kBlock), 0, h->stream,
@@ -2359,6 +2410,9 @@ int ps_mf_set_option(ps_mf_t *h, int32_t key, int64_t value) {
       return PS_MF_OK;
     case PS_MF_OPT_SWEEP_GRAPHS:
       h->sweep_graphs = value != 0;
+      return PS_MF_OK;
+    case PS_MF_OPT_UNIT_COMMIT:
+      h->unit_commit = value != 0;
       return PS_MF_OK;
     default:
       return fail(h, PS_MF_EINVAL, "unknown option key %d", key);
@@ -2539,6 +2593,7 @@ int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const flo
           (r = upload(h, &q.item_workers, S.item_workers)))
         return undo(r);
     } else if ((r = upload_units(h, d.by_user, L.by_user)) || (r = upload_units(h, d.by_item, L.by_item)) ||
+               (r = upload(h, &d.by_user.sole, L.by_user.sole)) ||
                (r = upload_cells(h, d.cells_user, L.cells_user)) || (r = upload_cells(h, d.cells_item, L.cells_item)) ||
                (r = upload_dense(h, d.dense_user, L.dense_user, true)) ||
                (r = upload_dense(h, d.dense_item, L.dense_item, false))) {

@@ -26,7 +26,7 @@ LIB_PATH = os.path.join(_HERE, "libps_mf.so")
 OK, EINVAL, ENOMEM, EDEVICE, ESTATE, EINTERNAL = 0, -1, -2, -3, -4, -5
 (OPT_POLICY, OPT_STEP, OPT_MB_BLOCKS, OPT_MB_SEED, OPT_HOST_ONLY, OPT_TIMING, OPT_TILE_BYTES, OPT_UNIT_MAX, OPT_CELLS,
  OPT_HEAVY_MIN, OPT_TWO_STREAMS, OPT_HOT_STEPS, OPT_DENSE_MIN, OPT_SEQ_STRATA, OPT_ETA_DECAY,
- OPT_SEQ_GRAPHS, OPT_ITEM_TILE_BYTES, OPT_DEVICE, OPT_POISON, OPT_SWEEP_GRAPHS) = range(1, 21)
+ OPT_SEQ_GRAPHS, OPT_ITEM_TILE_BYTES, OPT_DEVICE, OPT_POISON, OPT_SWEEP_GRAPHS, OPT_UNIT_COMMIT) = range(1, 22)
 SSP_LAZY, SSP_WORST, ESSP, SSP_ROW, ESSP_ROW, VAP = 0, 1, 2, 3, 4, 5
 STEP_ROWMEAN, STEP_SUM, STEP_SEQ = 0, 1, 2
 (IDX_OWNER, IDX_ROW_PTR, IDX_COL, IDX_PERM, IDX_USER_COUNT, IDX_ITEM_COUNT, IDX_VERSION_LOG, IDX_SPLIT, IDX_STALENESS,
@@ -204,7 +204,7 @@ class PsMf:
                  owner=None, host_only=False, timing=False, stream=None, tile_bytes=None, unit_max=None,
                  cells=None, heavy_min=None, two_streams=None, hot_steps=None, dense_min=None, strata=None,
                  value_bound=None, eta_decay=False, seq_graphs=None, item_tile_bytes=None, device=None,
-                 poison=False, sweep_graphs=None):
+                 poison=False, sweep_graphs=None, unit_commit=None):
         self.N, self.M, self.K, self.P, self.s = int(users), int(items), int(K), int(P), int(s)
         self.h = ps_mf_create(users, items, K, P, s, eta, lam)
         try:
@@ -246,6 +246,8 @@ class PsMf:
                 ps_mf_set_option(self.h, OPT_POISON, 1)
             if sweep_graphs is not None:
                 ps_mf_set_option(self.h, OPT_SWEEP_GRAPHS, int(bool(sweep_graphs)))
+            if unit_commit is not None:
+                ps_mf_set_option(self.h, OPT_UNIT_COMMIT, int(bool(unit_commit)))
             if owner is not None:
                 ps_mf_set_owner_map(self.h, owner)
             if stream is not None:

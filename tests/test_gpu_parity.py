@@ -325,6 +325,56 @@ def test_dense_tiles_medium_minibatch_blocks(gpu, step):
 
 
 # ---------------------------------------------------------------- per-row caches (Section 4)
+@pytest.mark.parametrize("config,policy,s,B", [("full", oracle.SSP_LAZY, 3, 1), ("full", oracle.SSP_LAZY, 0, 1),
+                                                ("full", oracle.ESSP, 2, 1), ("full", oracle.SSP_ROW, 1, 1),
+                                                ("full", oracle.VAP, 3, 1), ("medium", oracle.SSP_LAZY, 3, 4),
+                                                ("medium", oracle.SSP_WORST, 2, 4), ("medium", oracle.ESSP_ROW, 2, 4)])
+def test_unit_written_rows_equal_commit_written_rows(gpu, config, policy, s, B):
+    """PS_MF_OPT_UNIT_COMMIT: the work unit of a user whose ratings all lie in it writes the
+    user's new version itself (when the user's view is not the new version's slot) and the
+    commit skips the user.  Every clock's factors, loss and version log must equal the commit
+    writing every row, bit for bit, and stay within the oracle's tolerances; the poisoned
+    commit (rows the commit does not write are NaN before it) must stay finite."""
+    spec = synth.scaled(synth.CONFIGS[config], 0.05)
+    K = 64 if config == "full" else spec.K
+    w = synth.generate(spec, K=K)
+    opts = dict(dense_min=300, heavy_min=64, hot_steps=0) if config == "full" else {}
+    vb = 0.003 if policy == oracle.VAP else None
+    clocks = 2 * s + 3
+    say(f"unit commit: {config}@0.05 nnz={w.nnz} policy={policy} s={s} B={B} clocks={clocks}")
+    out = []
+    for unit_commit, poison in ((True, True), (False, False)):
+        with gpu.PsMf(spec.N, spec.M, K, spec.P, s, spec.eta, spec.lam, policy=policy, B=B, mb_seed=spec.seed,
+                      value_bound=vb, unit_commit=unit_commit, poison=poison, **opts) as g:
+            g.load_ratings(w.user, w.item, w.val)
+            g.set_factors(w.L0, w.R0)
+            hist = []
+            for _ in range(clocks):
+                g.clock(1)
+                hist.append(g.loss())
+                hist.append(g.get_factors())
+            out.append((hist, g.export_index(gpu.IDX_VERSION_LOG)))
+    (ha, va), (hb, vb_) = out
+    assert np.array_equal(va, vb_)
+    for x, y in zip(ha, hb):
+        if isinstance(x, tuple):
+            assert np.isfinite(x[0]).all() and np.isfinite(x[1]).all()
+            assert np.array_equal(x[0], y[0]) and np.array_equal(x[1], y[1])
+        else:
+            assert x == y
+    o = oracle.Oracle(spec.N, spec.M, K, spec.P, s, spec.eta, spec.lam, policy, oracle.ROWMEAN, B, spec.seed,
+                      value_bound=vb)
+    o.load(w.user, w.item, w.val)
+    o.set_factors(w.L0, w.R0)
+    o.clock(clocks)
+    Lo, Ro = o.get_factors()
+    loss_o = o.loss()
+    o.close()
+    L, R = ha[-1]
+    assert max(np.abs(L - Lo).max(), np.abs(R - Ro).max()) <= FACTOR_TOL
+    assert abs(ha[-2] - loss_o) <= LOSS_RTOL * loss_o
+
+
 @pytest.mark.parametrize("policy", [oracle.SSP_ROW, oracle.ESSP_ROW])
 @pytest.mark.parametrize("s,B", [(0, 1), (1, 1), (1, 4), (3, 4), (7, 3)])
 def test_tiny_config_per_row_policies(gpu, policy, s, B):
