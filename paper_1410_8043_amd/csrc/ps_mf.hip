@@ -1092,10 +1092,10 @@ __global__ __launch_bounds__(kBlock) void k_commit(FinalArgs fa, CommitArgs ca, 
 
 // Debug check of the commit (PS_MF_OPT_POISON): before the commit of clock c, every row of
 // the new version's slot that the commit will not read is set to NaN (but the user rows the
-// work units wrote in the sweep), so that a row the commit fails to write stays NaN.  The commit reads the new slot (which held version c-s)
-// where a view is version c-s: a user row with ratings whose view slot is the new slot, an
-// item row with a rating by a worker class whose view slot is the new slot.  One thread
-// per float4 of the slot.
+// work units wrote in the sweep), so that a row the commit fails to write stays NaN.  The
+// commit reads the new slot (which held version c-s) where a view is version c-s: a user
+// row with ratings whose view slot is the new slot, an item row with a rating by a worker
+// class whose view slot is the new slot.  One thread per float4 of the slot.
 __global__ __launch_bounds__(kBlock) void k_poison(FinalArgs fa, CommitArgs ca) {
   const int64_t q4 = fa.Kp / 4;
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
