@@ -30,6 +30,16 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(ps_mf.SYMBOLS)
 
 
+def test_every_header_constant_matches_the_binding():
+    """Every #define PS_MF_<NAME> <value> of include/ps_mf.h (error codes, option keys,
+    policies, steps, exports, timing kinds) has the same value in the Python binding."""
+    text = open(os.path.join(ROOT, "include", "ps_mf.h")).read()
+    consts = dict(re.findall(r"#define PS_MF_([A-Z_0-9]+) \(?(-?\d+)\)?", text))
+    assert len(consts) == 50, len(consts)
+    for name, value in consts.items():
+        assert getattr(ps_mf, name) == int(value), name
+
+
 @pytest.mark.parametrize("args", [
     (0, 1, 1, 1, 0, 0.1, 0.1), (1, 0, 1, 1, 0, 0.1, 0.1), (1, 1, 0, 1, 0, 0.1, 0.1), (1, 1, 513, 1, 0, 0.1, 0.1),
     (1, 1, 1, 0, 0, 0.1, 0.1), (1, 1, 1, 1, -1, 0.1, 0.1), (1, 1, 1, 1, 0, float("nan"), 0.1),
