@@ -88,9 +88,12 @@ int ps_lda_set_option(ps_lda_t *h, int32_t key, int64_t value);
 /* hip_stream: a hipStream_t of the current device, or NULL for a stream the handle creates. */
 int ps_lda_set_stream(ps_lda_t *h, void *hip_stream);
 /* n tokens as host arrays: document, word, initial topic (0 <= doc < D, word < V, z0 < K).
-   Version 0 holds the counts of z0.  Synchronizes.  PS_LDA_EINVAL also when some p_k could
-   leave the normal fp64 range: alpha beta / (n + V beta) must be at least 2^-1000 and
-   (longest document + alpha)(n + beta) / (V beta) at most 2^1000. */
+   Version 0 holds the counts of z0.  Synchronizes.  PS_LDA_EINVAL also when a weight p_k,
+   its numerator (n_dk + alpha)(n_wk + beta) or its denominator n_k + V beta could leave
+   [2^-700, 2^700] (p_k must be a normal fp64 number, and the sampler divides by a short form
+   that is exact there): each of alpha beta, (longest document + alpha)(n + beta), V beta,
+   n + V beta, alpha beta / (n + V beta) and (longest document + alpha)(n + beta) / (V beta)
+   must lie in that range. */
 int ps_lda_load(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int32_t *z0, int64_t n);
 /* run n clocks (asynchronous) */
 int ps_lda_clock(ps_lda_t *h, int32_t n);

@@ -102,21 +102,22 @@ __device__ __forceinline__ uint64_t umulhi64_vec(uint64_t a, uint64_t b) {
 // and row_bcast:31 the last lane of row 1 (by then the sum of rows 0-1) into rows 2 and 3
 // (rows the mask leaves out keep their value); *total gets lane 63's sum.  Each step is one
 // add of the low halves with the carry into VCC and one add of the high halves with that
-// carry, both reading the shifted operand through DPP.  The s_nop keeps two wait states
-// between a half's write and the next DPP read of it.
+// carry, both reading the shifted operand through DPP.  A DPP read needs two wait states
+// after the write of its operand: s_nop 1 before the first step (the input's write), and
+// between steps one s_nop 0 plus the other half's add; the s_nop 0 at the end is the wait
+// state that a lane read of the result needs after its write.
 __device__ __forceinline__ uint64_t wave_scan(uint64_t x, uint64_t *total) {
   uint32_t lo = static_cast<uint32_t>(x), hi = static_cast<uint32_t>(x >> 32);
 #define PS_LDA_SCAN_STEP(DPP)                                          \
-  "s_nop 1\n\t"                                                         \
   "v_add_co_u32_dpp %0, vcc, %0, %0 " DPP "\n\t"                        \
   "v_addc_co_u32_dpp %1, vcc, %1, %1, vcc " DPP "\n\t"
-  asm volatile(PS_LDA_SCAN_STEP("row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1")
-               PS_LDA_SCAN_STEP("row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1")
-               PS_LDA_SCAN_STEP("row_shr:4 row_mask:0xf bank_mask:0xf bound_ctrl:1")
-               PS_LDA_SCAN_STEP("row_shr:8 row_mask:0xf bank_mask:0xf bound_ctrl:1")
-               PS_LDA_SCAN_STEP("row_bcast:15 row_mask:0xa bank_mask:0xf")
-               PS_LDA_SCAN_STEP("row_bcast:31 row_mask:0xc bank_mask:0xf")
-               "s_nop 1"
+  asm volatile("s_nop 1\n\t"
+               PS_LDA_SCAN_STEP("row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1") "s_nop 0\n\t"
+               PS_LDA_SCAN_STEP("row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1") "s_nop 0\n\t"
+               PS_LDA_SCAN_STEP("row_shr:4 row_mask:0xf bank_mask:0xf bound_ctrl:1") "s_nop 0\n\t"
+               PS_LDA_SCAN_STEP("row_shr:8 row_mask:0xf bank_mask:0xf bound_ctrl:1") "s_nop 0\n\t"
+               PS_LDA_SCAN_STEP("row_bcast:15 row_mask:0xa bank_mask:0xf") "s_nop 0\n\t"
+               PS_LDA_SCAN_STEP("row_bcast:31 row_mask:0xc bank_mask:0xf") "s_nop 0"
                : "+v"(lo), "+v"(hi)
                :
                : "vcc");
@@ -126,28 +127,22 @@ __device__ __forceinline__ uint64_t wave_scan(uint64_t x, uint64_t *total) {
   return x;
 }
 
-// maximum of an int over the wavefront, in lane 63 and returned: DPP quad_perm [1,0,3,2],
-// quad_perm [2,3,0,1], row_half_mirror and row_mirror give each lane its 16-lane row's
-// maximum (every source lane lies inside the row), then row_bcast:15 and row_bcast:31 carry
-// the rows' maxima into row 3 (rows the mask leaves out keep their value)
-__device__ __forceinline__ int wave_max_i32(int x) {
-  asm volatile(
-      "s_nop 1\n\t"
-      "v_max_i32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
-      "s_nop 1\n\t"
-      "v_max_i32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
-      "s_nop 1\n\t"
-      "v_max_i32_dpp %0, %0, %0 row_half_mirror row_mask:0xf bank_mask:0xf\n\t"
-      "s_nop 1\n\t"
-      "v_max_i32_dpp %0, %0, %0 row_mirror row_mask:0xf bank_mask:0xf\n\t"
-      "s_nop 1\n\t"
-      "v_max_i32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
-      "s_nop 1\n\t"
-      "v_max_i32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
-      "s_nop 1"
-      : "+v"(x));
-  return __builtin_amdgcn_readlane(x, 63);
-}
+// One step of a wavefront maximum: x = max(x, x of the lane that CTRL names), by one DPP
+// instruction (lanes that the row mask leaves out keep x).  A DPP read needs two wait
+// states after the write of its operand: WAIT is the number of instructions the caller
+// places between the write and the step (0, 1 or 2 and more), and the step adds s_nop 1,
+// s_nop 0 or nothing.  Four steps (quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror,
+// row_mirror) give each lane its 16-lane row's maximum (every source lane lies inside the
+// row), then row_bcast:15 (rows 1 and 3) and row_bcast:31 (rows 2 and 3) carry the rows'
+// maxima into row 3, so lane 63 holds the wavefront's.
+#define PS_LDA_MAX_STEP(x, WAIT, CTRL)                                                  \
+  do {                                                                                  \
+    if constexpr ((WAIT) >= 2) asm volatile("v_max_i32_dpp %0, %0, %0 " CTRL : "+v"(x)); \
+    else if constexpr ((WAIT) == 1)                                                     \
+      asm volatile("s_nop 0\n\tv_max_i32_dpp %0, %0, %0 " CTRL : "+v"(x));              \
+    else                                                                                \
+      asm volatile("s_nop 1\n\tv_max_i32_dpp %0, %0, %0 " CTRL : "+v"(x));              \
+  } while (0)
 
 // what one token reads before it can be sampled: its view row and own-change row of the
 // word, the row's clock tag, and its current topic
@@ -350,12 +345,26 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
       }
       cur_doc = d;
     }
-    // the collapsed conditional's weights p_k in fp64 (every p_k is a normal number: the
-    // load checks the range) and the exponent of the largest (the largest exponent)
-    // (computed on every lane, without a branch: lanes past the last topic hold topic K-1's
-    // rows and zero counts, and their results are masked)
-    double pk[KPL];
-    int emax = -2048;  // below every normal exponent: lanes past the last topic
+    // the collapsed conditional's weights p_k = num_k / den_k in fp64 and the exponent of
+    // the largest (computed on every lane, without a branch: lanes past the last topic hold
+    // topic K-1's rows and zero counts, and their results are masked).
+    // * The exponent is found without waiting for the divisions: with frexp exponents (x =
+    //   m 2^e, m in [0.5, 1)) num / den lies in [2^(e_num - e_den - 1), 2^(e_num - e_den + 1))
+    //   and never rounds up to the upper end, so the largest weight's frexp exponent is the
+    //   wavefront maximum E of e_num - e_den + 1 over the topics, or E - 1; it is E exactly
+    //   when some weight reaches 2^(E - 1).
+    // * The divisions are the hardware reciprocal, two Newton steps, the product and one
+    //   correction: the instructions the compiler emits for a correctly rounded fp64
+    //   division, without its range scaling (v_div_scale) and special-case fixup
+    //   (v_div_fixup). Those leave their operands unchanged when num, den and num / den
+    //   are normal with exponents well inside +-768 (no scaling, no overflow, no
+    //   denormal), which the load guarantees: every num, den and p lies in
+    //   [2^-700, 2^700].  So each p_k is the correctly rounded quotient, as the oracle's.
+    // * The maximum's six DPP steps are interleaved with the Newton steps of the KPL
+    //   divisions, pinned by scheduling barriers: the two instructions between steps are
+    //   the wait states a DPP read needs.
+    double num[KPL], den[KPL], rcp[KPL], err[KPL], pk[KPL];
+    int ex = -4096;  // below every exponent: lanes past the last topic
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
       const int k = lane * KPL + j;
@@ -363,15 +372,58 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
       const int ndx = nd[j] - self;
       const int nwx = max(rows[C].nw[j] + dw[j] - self, 0);
       const int nkx = max(vk[j] + dk[j] - self, 0);
-      const double num = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
-      const double p = num / (static_cast<double>(nkx) + a.Vbeta);
-      const bool in = k < K;
-      pk[j] = in ? p : 0.0;
-      if (in) emax = max(emax, __builtin_amdgcn_frexp_exp(p) - 1);  // frexp: p = m 2^x, m in [0.5, 1)
+      num[j] = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
+      den[j] = static_cast<double>(nkx) + a.Vbeta;
+      if (k < K) ex = max(ex, __builtin_amdgcn_frexp_exp(num[j]) - __builtin_amdgcn_frexp_exp(den[j]) + 1);
+      rcp[j] = __builtin_amdgcn_rcp(den[j]);
     }
+    // between two steps: the KPL operations of one Newton step
+#define PS_LDA_GAP KPL
+    __builtin_amdgcn_sched_barrier(0);
+    PS_LDA_MAX_STEP(ex, 0, "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) err[j] = fma(-den[j], rcp[j], 1.0);
+    __builtin_amdgcn_sched_barrier(0);
+    PS_LDA_MAX_STEP(ex, PS_LDA_GAP, "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) rcp[j] = fma(rcp[j], err[j], rcp[j]);
+    __builtin_amdgcn_sched_barrier(0);
+    PS_LDA_MAX_STEP(ex, PS_LDA_GAP, "row_half_mirror row_mask:0xf bank_mask:0xf");
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) err[j] = fma(-den[j], rcp[j], 1.0);
+    __builtin_amdgcn_sched_barrier(0);
+    PS_LDA_MAX_STEP(ex, PS_LDA_GAP, "row_mirror row_mask:0xf bank_mask:0xf");
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) rcp[j] = fma(rcp[j], err[j], rcp[j]);
+    __builtin_amdgcn_sched_barrier(0);
+    PS_LDA_MAX_STEP(ex, PS_LDA_GAP, "row_bcast:15 row_mask:0xa bank_mask:0xf");
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) pk[j] = num[j] * rcp[j];
+    __builtin_amdgcn_sched_barrier(0);
+    PS_LDA_MAX_STEP(ex, PS_LDA_GAP, "row_bcast:31 row_mask:0xc bank_mask:0xf");
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) err[j] = fma(-den[j], pk[j], num[j]);
+    __builtin_amdgcn_sched_barrier(0);
+#undef PS_LDA_GAP
+    const int ehi = __builtin_amdgcn_readlane(ex, 63);  // the KPL corrections before it: its wait state
+    int top = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const double p = fma(err[j], rcp[j], pk[j]);
+      pk[j] = lane * KPL + j < K ? p : 0.0;
+      top |= pk[j] >= ldexp(1.0, ehi - 1);
+    }
+    // the largest p_k lies in [2^emax, 2^(emax + 1))
+    const int emax = (__ballot(top) != 0 ? ehi : ehi - 1) - 1;
     // integer weights floor(p_k 2^(shift0 - emax)) (the scaling is exact), prefix sums in
     // topic order
-    const int shift = a.shift0 - wave_max_i32(emax);
+    const int shift = a.shift0 - emax;
     uint64_t loc[KPL];
     uint64_t acc = 0;
 #pragma unroll
@@ -854,16 +906,27 @@ int load_tokens(ps_lda_t *h, const int32_t *doc, const int32_t *word, const int3
   }
   const int64_t P = h->P, B = h->B, K = h->K, V = h->V;
   {
-    // every p_k must be a normal fp64 number (its exponent sets the weights' scale): p_k
-    // lies between alpha beta / (tokens + V beta) and (longest document + alpha)(tokens +
-    // beta) / (V beta)
+    // every weight p_k = num / den of the sampler, its numerator (n_dk + alpha)(n_wk + beta)
+    // and its denominator n_k + V beta must lie in [2^-700, 2^700]: then p_k is a normal fp64
+    // number (its exponent sets the weights' scale) and the sampler's short division (no
+    // range scaling, no special cases) is exact.  num lies between alpha beta and (longest
+    // document + alpha)(tokens + beta), den between V beta and tokens + V beta, and p_k
+    // between alpha beta / (tokens + V beta) and (longest document + alpha)(tokens + beta) /
+    // (V beta)
     std::vector<int64_t> len(static_cast<size_t>(h->D), 0);
     int64_t lmax = 0;
     for (int64_t t = 0; t < n; ++t) lmax = std::max(lmax, ++len[doc[t]]);
-    const double hi = (static_cast<double>(lmax) + h->alpha) * (static_cast<double>(n) + h->beta) / h->Vbeta;
-    const double lo = h->alpha * h->beta / (static_cast<double>(n) + h->Vbeta);
-    if (!(hi <= std::ldexp(1.0, 1000)) || !(lo >= std::ldexp(1.0, -1000)))
-      return lda_fail(h, PS_LDA_EINVAL, "topic weights leave [2^-1000, 2^1000]: from %.3g to %.3g", lo, hi);
+    const double num_hi = (static_cast<double>(lmax) + h->alpha) * (static_cast<double>(n) + h->beta);
+    const double num_lo = h->alpha * h->beta;
+    const double den_hi = static_cast<double>(n) + h->Vbeta, den_lo = h->Vbeta;
+    const double lo = num_lo / den_hi, hi = num_hi / den_lo;
+    const double top = std::ldexp(1.0, 700), bottom = std::ldexp(1.0, -700);
+    for (const double x : {num_lo, num_hi, den_lo, den_hi, lo, hi})
+      if (!(x >= bottom && x <= top))
+        return lda_fail(h, PS_LDA_EINVAL,
+                        "topic weights, their numerators or denominators leave [2^-700, 2^700]: weights from "
+                        "%.3g to %.3g, numerators from %.3g to %.3g, denominators from %.3g to %.3g",
+                        lo, hi, num_lo, num_hi, den_lo, den_hi);
   }
   // processing order: block, worker (document mod P), document, load index
   std::vector<std::pair<uint64_t, int64_t>> key(static_cast<size_t>(n));

@@ -113,8 +113,8 @@ def test_null_handle_calls_are_rejected():
     ps_lda._lib.ps_lda_destroy(None)  # NULL-safe
 
 
-@pytest.mark.parametrize("alpha,beta,where", [(0.1, 1e-300, "2^-1000"), (1e300, 1e300, "2^1000")])
-def test_weight_range_is_checked_on_both_sides(alpha, beta, where):
+@pytest.mark.parametrize("alpha,beta", [(0.1, 1e-300), (1e300, 1e300)])
+def test_weight_range_is_checked_on_both_sides(alpha, beta):
     # every p_k must be a normal fp64 number (its exponent sets the token's weight scale):
     # alpha beta / (n + V beta) below 2^-1000, or (longest document + alpha)(n + beta) /
     # (V beta) above 2^1000, is refused by library and oracle alike
@@ -122,10 +122,23 @@ def test_weight_range_is_checked_on_both_sides(alpha, beta, where):
     h = ps_lda.PsLda(1, 2, 4, 1, 1, alpha, beta, host_only=True)
     with pytest.raises(ps_lda.PsLdaError) as e:
         h.load(doc, word, z)
-    assert e.value.code == ps_lda.EINVAL and b"2^1000" in ps_lda._lib.ps_lda_last_error(h._h)
+    assert e.value.code == ps_lda.EINVAL and b"2^700" in ps_lda._lib.ps_lda_last_error(h._h)
     o = oracle.LdaOracle(1, 2, 4, 1, 1, alpha, beta)
     with pytest.raises(oracle.OracleError):
         o.load(doc, word, z)
     # the same corpus with alpha = 0.1 and beta = 0.01 is accepted by both
     ps_lda.PsLda(1, 2, 4, 1, 1, 0.1, 0.01, host_only=True).load(doc, word, z)
     oracle.LdaOracle(1, 2, 4, 1, 1, 0.1, 0.01).load(doc, word, z)
+
+
+def test_library_keeps_weights_numerators_and_denominators_in_its_division_range():
+    # beta = 1e-215 gives weights between about 2^-722 and 2^724: normal numbers, which the
+    # oracle accepts, but outside [2^-700, 2^700], where the library's short division is exact
+    doc, word, z = [0] * 50, [0, 1] * 25, [0] * 50
+    oracle.LdaOracle(1, 2, 4, 1, 1, 0.1, 1e-215).load(doc, word, z)
+    h = ps_lda.PsLda(1, 2, 4, 1, 1, 0.1, 1e-215, host_only=True)
+    with pytest.raises(ps_lda.PsLdaError) as e:
+        h.load(doc, word, z)
+    assert e.value.code == ps_lda.EINVAL and b"2^700" in ps_lda._lib.ps_lda_last_error(h._h)
+    # inside the range on every count: accepted
+    ps_lda.PsLda(1, 2, 4, 1, 1, 1e-100, 1e-100, host_only=True).load(doc, word, z)
