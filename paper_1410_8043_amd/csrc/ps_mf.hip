@@ -939,25 +939,30 @@ __device__ __forceinline__ void finalize_users(const FinalArgs &a, int64_t idx) 
   const int64_t q4 = a.Kp / 4;
   if (idx >= a.users * q4) return;
   const int64_t i = idx / q4;
-  const int n = a.ucount[i];
   float4 *ring4 = reinterpret_cast<float4 *>(a.ring);
   const int64_t ss4 = a.slot_stride / 4;
+  // what depends on i alone is loaded at once, so that the row's chain of dependent loads
+  // is the view slot, then the partial rows and the view row
+  const int n = a.ucount[i];
+  const int32_t vs = a.rs_u ? a.rs_u[i] : a.ucls[i];  // the row's view slot, or its class
+  const int64_t p0 = a.user_pp[i], p1 = a.user_pp[i + 1];
+  const bool sole = a.sole && a.sole[i];
+  const float4 lc = ring4[a.slot_c * ss4 + idx];
   if (n == 0) {
-    if (a.slot_n != a.slot_c) ring4[a.slot_n * ss4 + idx] = ring4[a.slot_c * ss4 + idx];
+    if (a.slot_n != a.slot_c) ring4[a.slot_n * ss4 + idx] = lc;
     return;
   }
-  const int32_t sv = a.rs_u ? a.rs_u[i] : a.cls_slot[a.ucls[i]];
-  if (a.sole && a.sole[i] && sv != a.slot_n) return;  // its unit wrote the new version
+  const int32_t sv = a.rs_u ? vs : a.cls_slot[vs];
+  if (sole && sv != a.slot_n) return;  // its unit wrote the new version
   const f32x4 *part4 = reinterpret_cast<const f32x4 *>(a.partial);
   const int64_t k4 = idx - i * q4;
+  const float4 lv = ring4[sv * ss4 + idx];
   float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll 4
-  for (int64_t p = a.user_pp[i]; p < a.user_pp[i + 1]; ++p) {
+  for (int64_t p = p0; p < p1; ++p) {
     const f32x4 t = ld_partial(part4 + p * q4 + k4);
     d.x += t[0]; d.y += t[1]; d.z += t[2]; d.w += t[3];
   }
-  const float4 lc = ring4[a.slot_c * ss4 + idx];
-  const float4 lv = ring4[sv * ss4 + idx];
   const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
   const float nl = static_cast<float>(n) * a.lambda;
   ring4[a.slot_n * ss4 + idx] = make_float4(commit_elem(lc.x, sc, d.x, nl, lv.x), commit_elem(lc.y, sc, d.y, nl, lv.y),
@@ -989,18 +994,21 @@ __device__ __forceinline__ void commit_item(const CommitArgs &a, int64_t j, floa
   const int q4 = a.Kp / 4;
   const int lanes = kBlock / q4;  // row lanes: Kp is a power of two in [8, 512], so 2..128
   const int k4 = static_cast<int>(threadIdx.x) % q4, lane = static_cast<int>(threadIdx.x) / q4;
-  const int n = a.icount[j];
   float4 *R4 = reinterpret_cast<float4 *>(a.ring + a.r_off);
   const int64_t ss4 = a.slot_stride / 4;
   const int64_t idx = j * q4 + k4;
+  const int n = a.icount[j];
+  const int64_t p0 = a.item_pp[j], p1 = a.item_pp[j + 1];
+  float4 rc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (lane == 0) rc = R4[a.slot_c * ss4 + idx];  // loaded before the partial rows
   if (n == 0) {  // uniform over the workgroup
-    if (lane == 0) R4[a.slot_n * ss4 + idx] = R4[a.slot_c * ss4 + idx];
+    if (lane == 0) R4[a.slot_n * ss4 + idx] = rc;
     return;
   }
   float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
   const f32x4 *part4 = reinterpret_cast<const f32x4 *>(a.partial);
 #pragma unroll 4
-  for (int64_t p = a.item_pp[j] + lane; p < a.item_pp[j + 1]; p += lanes) {
+  for (int64_t p = p0 + lane; p < p1; p += lanes) {
     const f32x4 t = ld_partial(part4 + p * q4 + k4);
     d.x += t[0]; d.y += t[1]; d.z += t[2]; d.w += t[3];
   }
@@ -1011,14 +1019,26 @@ __device__ __forceinline__ void commit_item(const CommitArgs &a, int64_t j, floa
     const float4 t = red[l * q4 + k4];
     d.x += t.x; d.y += t.y; d.z += t.z; d.w += t.w;
   }
-  const float4 rc = R4[a.slot_c * ss4 + idx];
+  // the classes' view rows, four classes' loads at a time (a class without a rating of the
+  // item reads the current row instead and adds nothing), summed in class order
   float4 lam = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int q = 0; q < a.nclass; ++q) {
-    const int cnt = a.icount_cls[j * a.nclass + q];
-    if (cnt) {
-      const float c = static_cast<float>(cnt);
-      const float4 r = R4[(a.rs_i ? a.rs_i[q * a.items + j] : a.cls_slot[q]) * ss4 + idx];
-      lam = make_float4(fmaf(c, r.x, lam.x), fmaf(c, r.y, lam.y), fmaf(c, r.z, lam.z), fmaf(c, r.w, lam.w));
+  for (int q0 = 0; q0 < a.nclass; q0 += 4) {
+    int cnt[4];
+    float4 r[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) cnt[u] = q0 + u < a.nclass ? a.icount_cls[j * a.nclass + q0 + u] : 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t slot = cnt[u] ? (a.rs_i ? a.rs_i[(q0 + u) * a.items + j] : a.cls_slot[q0 + u]) : a.slot_c;
+      r[u] = R4[slot * ss4 + idx];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (cnt[u]) {
+        const float c = static_cast<float>(cnt[u]);
+        lam = make_float4(fmaf(c, r[u].x, lam.x), fmaf(c, r[u].y, lam.y), fmaf(c, r[u].z, lam.z),
+                          fmaf(c, r[u].w, lam.w));
+      }
     }
   }
   const float sc = a.rowmean ? a.eta / static_cast<float>(n) : a.eta;
