@@ -313,8 +313,19 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
   auto step = [&](auto phase, int i) {
     constexpr int C = decltype(phase)::value;
     const int w = field(i, 0), d = field(i, 1);
+    // read early (a value from a lane read wants wait states before a load or a vector
+    // instruction uses it): the word of the token whose rows this step fetches, and this
+    // token's draw value
+    const int wf = field(i + kDist, 0);
+    const uint64_t ru = readlane_u64(rnd, i - base);
     const int k0 = __builtin_amdgcn_readfirstlane(rows[C].z);
-    int valid = __builtin_amdgcn_readfirstlane(rows[C].tag) == a.tagc;
+    // 1 when the fetched own-change row is of this clock, formed on the scalar unit (the
+    // compiler would turn the compare's flag into an integer on the vector unit)
+    int valid;
+    asm("s_cmp_eq_u32 %1, %2\n\ts_cselect_b32 %0, 1, 0"
+        : "=s"(valid)
+        : "s"(__builtin_amdgcn_readfirstlane(rows[C].tag)), "s"(a.tagc)
+        : "scc");
     int dw[KPL];
 #pragma unroll
     for (int j = 0; j < KPL; ++j) dw[j] = rows[C].dw[j];
@@ -435,7 +446,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     const uint64_t excl = wave_scan(acc, &total) - acc;
     int k1 = k0;
     if (total != 0) {  // always: the largest weight is at least 2^shift0
-      const uint64_t target = umulhi64_vec(readlane_u64(rnd, i - base), total);
+      const uint64_t target = umulhi64_vec(ru, total);
       const uint64_t m = __ballot(excl + acc > target);
       const int L = __ffsll(static_cast<unsigned long long>(m)) - 1;  // m != 0: the last lane's sum is the total
       int jj = KPL - 1;
@@ -478,7 +489,6 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
       for (int j = 0; j < KPL; ++j) fdw[0][j] = dw[j];
     }
     constexpr int NF = (C + kDist) % R;
-    const int wf = field(i + kDist, 0);
     fetch_rows<KPL, Buf>(view, mydelta, mytag, z, koff, rowb * static_cast<Off>(wf), wf, i + kDist, rows[NF]);
   };
   // whole rotations without an exit inside (an exit path would join the loop's back edge
