@@ -179,6 +179,12 @@ struct Table<true> {
   __device__ __forceinline__ void st(int v, Off row_off) const {
     __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(v), rs, 0, static_cast<int>(row_off), 0);
   }
+  // a store that the hardware drops unless keep, without a branch: the dropped lanes' offset
+  // is 2^31 + row_off, past every table of this form (each is under 2^31 bytes, and so is
+  // row_off, so the sum does not wrap), and a buffer store outside its resource is discarded
+  __device__ __forceinline__ void st_if(bool keep, int v, uint32_t lane_off, Off row_off) const {
+    st(v, keep ? lane_off : 0x80000000u, row_off);
+  }
 };
 
 template <>
@@ -194,6 +200,9 @@ struct Table<false> {
     *reinterpret_cast<int32_t *>(base + row_off + lane_off) = v;
   }
   __device__ __forceinline__ void st(int v, Off row_off) const { *reinterpret_cast<int32_t *>(base + row_off) = v; }
+  __device__ __forceinline__ void st_if(bool keep, int v, uint32_t lane_off, Off row_off) const {
+    if (keep) st(v, lane_off, row_off);
+  }
 };
 
 // koff[j]: the byte offset of this lane's topic j in a row (lanes past the last topic
@@ -275,12 +284,13 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
 #pragma unroll
   for (int j = 0; j < KPL; ++j) koff[j] = 4u * static_cast<uint32_t>(min(lane * KPL + j, K - 1));
 
-  int vk[KPL], dk[KPL], nd[KPL];
+  // topic totals: the view's, and the current ones (the view's plus this worker's changes)
+  int vk[KPL], nk[KPL], nd[KPL];
 #pragma unroll
   for (int j = 0; j < KPL; ++j) {
     const int k = lane * KPL + j;
     vk[j] = k < K ? view_p[V * K + k] : 0;
-    dk[j] = 0;
+    nk[j] = vk[j];
     nd[j] = 0;
   }
   int cur_doc = -1;
@@ -375,17 +385,19 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     //   divisions, pinned by scheduling barriers: the two instructions between steps are
     //   the wait states a DPP read needs.
     double num[KPL], den[KPL], rcp[KPL], err[KPL], pk[KPL];
-    int ex = -4096;  // below every exponent: lanes past the last topic
+    int ex = -4096;  // the lane's largest e_num - e_den; below every exponent past the last topic
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
       const int k = lane * KPL + j;
       const int self = k == k0;
       const int ndx = nd[j] - self;
       const int nwx = max(rows[C].nw[j] + dw[j] - self, 0);
-      const int nkx = max(vk[j] + dk[j] - self, 0);
+      const int nkx = max(nk[j] - self, 0);
       num[j] = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
       den[j] = static_cast<double>(nkx) + a.Vbeta;
-      if (k < K) ex = max(ex, __builtin_amdgcn_frexp_exp(num[j]) - __builtin_amdgcn_frexp_exp(den[j]) + 1);
+      const int e = __builtin_amdgcn_frexp_exp(num[j]) - __builtin_amdgcn_frexp_exp(den[j]);
+      if (j == 0) ex = k < K ? e : -4096;
+      else if (k < K) ex = max(ex, e);
       rcp[j] = __builtin_amdgcn_rcp(den[j]);
     }
     // between two steps: the KPL operations of one Newton step
@@ -422,7 +434,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     for (int j = 0; j < KPL; ++j) err[j] = fma(-den[j], pk[j], num[j]);
     __builtin_amdgcn_sched_barrier(0);
 #undef PS_LDA_GAP
-    const int ehi = __builtin_amdgcn_readlane(ex, 63);  // the KPL corrections before it: its wait state
+    const int ehi = __builtin_amdgcn_readlane(ex, 63) + 1;  // the KPL corrections before it: its wait state
     int top = 0;
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
@@ -463,16 +475,13 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
         const int k = lane * KPL + j;
         const int dl = (k == k1) - (k == k0);
         nd[j] += dl;
-        dk[j] += dl;
+        nk[j] += dl;
         dw[j] += dl;
-        if (k < K) {
-          if (!valid || dl != 0) mydelta.st(dw[j], koff[j], rb);
-        }
+        mydelta.st_if(k < K && (!valid || dl != 0), dw[j], koff[j], rb);
       }
-      if (lane == 0) {
-        z.st(k1, Off{4} * static_cast<uint32_t>(i));
-        if (!valid) mytag.st(a.tagc, Off{4} * static_cast<uint32_t>(w));
-      }
+      // lane 0 stores the new topic, and the row's clock tag when the row was of an older clock
+      z.st_if(lane == 0, k1, 0u, Off{4} * static_cast<uint32_t>(i));
+      mytag.st_if(lane == 0 && !valid, a.tagc, 0u, Off{4} * static_cast<uint32_t>(w));
     }
     // this token becomes the latest forwarded row
 #pragma unroll
@@ -517,7 +526,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     const int k = lane * KPL + j;
     if (k < K) {
       ndk.st(nd[j], koff[j], rowb * static_cast<Off>(cur_doc));
-      a.tot[p * K + k] = dk[j];
+      a.tot[p * K + k] = nk[j] - vk[j];
     }
   }
 }
