@@ -284,6 +284,11 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
 #pragma unroll
   for (int j = 0; j < KPL; ++j) koff[j] = 4u * static_cast<uint32_t>(min(lane * KPL + j, K - 1));
 
+  // alpha per topic slot, 0 past the last topic: there the document count is 0 as well, so
+  // the weight's numerator and the weight are 0 (the denominator is at least V beta)
+  double alpha_k[KPL];
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) alpha_k[j] = lane * KPL + j < K ? a.alpha : 0.0;
   // topic totals: the view's, and the current ones (the view's plus this worker's changes)
   int vk[KPL], nk[KPL], nd[KPL];
 #pragma unroll
@@ -368,7 +373,8 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     }
     // the collapsed conditional's weights p_k = num_k / den_k in fp64 and the exponent of
     // the largest (computed on every lane, without a branch: lanes past the last topic hold
-    // topic K-1's rows and zero counts, and their results are masked).
+    // topic K-1's rows, a zero document count and alpha = 0, so their weights are 0, and
+    // their exponents are masked).
     // * The exponent is found without waiting for the divisions: with frexp exponents (x =
     //   m 2^e, m in [0.5, 1)) num / den lies in [2^(e_num - e_den - 1), 2^(e_num - e_den + 1))
     //   and never rounds up to the upper end, so the largest weight's frexp exponent is the
@@ -393,7 +399,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
       const int ndx = nd[j] - self;
       const int nwx = max(rows[C].nw[j] + dw[j] - self, 0);
       const int nkx = max(nk[j] - self, 0);
-      num[j] = (static_cast<double>(ndx) + a.alpha) * (static_cast<double>(nwx) + a.beta);
+      num[j] = (static_cast<double>(ndx) + alpha_k[j]) * (static_cast<double>(nwx) + a.beta);
       den[j] = static_cast<double>(nkx) + a.Vbeta;
       const int e = __builtin_amdgcn_frexp_exp(num[j]) - __builtin_amdgcn_frexp_exp(den[j]);
       if (j == 0) ex = k < K ? e : -4096;
@@ -438,8 +444,7 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     int top = 0;
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
-      const double p = fma(err[j], rcp[j], pk[j]);
-      pk[j] = lane * KPL + j < K ? p : 0.0;
+      pk[j] = fma(err[j], rcp[j], pk[j]);  // 0 past the last topic
       top |= pk[j] >= ldexp(1.0, ehi - 1);
     }
     // the largest p_k lies in [2^emax, 2^(emax + 1))
