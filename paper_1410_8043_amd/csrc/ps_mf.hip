@@ -56,10 +56,10 @@ constexpr int kBlock = 256;       // threads per workgroup of the small kernels 
 #define PS_MF_CELL_THREADS 1024
 #endif
 #ifndef PS_MF_CELL_TILE_FLOATS
-#define PS_MF_CELL_TILE_FLOATS 32768
+#define PS_MF_CELL_TILE_FLOATS 40960
 #endif
 constexpr int kSweepBlock = PS_MF_CELL_THREADS;     // threads per cell workgroup (1024: 16 wavefronts)
-constexpr int kTileFloats = PS_MF_CELL_TILE_FLOATS; // LDS sub-tile of a cell (32768: 128 KiB = ts rows of Kp floats)
+constexpr int kTileFloats = PS_MF_CELL_TILE_FLOATS; // LDS sub-tile of a cell (40960: 160 KiB = ts rows of Kp floats)
 static_assert(kSweepBlock % 256 == 0 && kSweepBlock <= 1024, "cell workgroups hold whole 256-thread quarters");
 static_assert(kTileFloats % 512 == 0 && kTileFloats * 4 <= 160 * 1024, "a cell sub-tile holds whole 512-wide rows in LDS");
 constexpr int kLossSegment = 512;  // ratings per lane group of the loss
@@ -2532,7 +2532,7 @@ int load_ratings(ps_mf_t *h, const int32_t *user, const int32_t *item, const flo
   // with the split; on the 100M-rating K = 128 workload the split saves a quarter.
   const bool split_auto = n / h->B >= kSplitMinRatings;
   if (h->cells) {
-    // cells: one 1024-thread workgroup per cell, a 128 KiB LDS sub-tile of ts rows; a user
+    // cells: one 1024-thread workgroup per cell, a 160 KiB LDS sub-tile of ts rows; a user
     // is dense enough for them when it averages 16 or more ratings per item sub-tile
     lp.cell_rows = kTileFloats / h->Kp;
     lp.cell_groups = kSweepBlock / shape_for(h->Kp).G;
