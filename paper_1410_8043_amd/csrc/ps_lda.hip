@@ -344,13 +344,21 @@ __global__ __launch_bounds__(kWave) void k_lda_sweep(SweepArgs a) {
     int dw[KPL];
 #pragma unroll
     for (int j = 0; j < KPL; ++j) dw[j] = rows[C].dw[j];
-    // the latest of the last F tokens with this word, if any, overrides the fetched row
+    // the latest of the last F tokens with this word, if any, overrides the fetched row (a
+    // branch on the rare repeat, so that the common token runs no selects; the product of
+    // the differences is 0 on a repeat, and on a wrap to 0 the branch only checks for
+    // nothing)
+    uint32_t differ = 1;
 #pragma unroll
-    for (int f = F - 1; f >= 0; --f) {
-      if (fw[f] == w) {
-        valid = fvalid[f];
+    for (int f = 0; f < F; ++f) differ *= static_cast<uint32_t>(fw[f] ^ w);
+    if (__builtin_expect(differ == 0, 0)) {
 #pragma unroll
-        for (int j = 0; j < KPL; ++j) dw[j] = fdw[f][j];
+      for (int f = F - 1; f >= 0; --f) {
+        if (fw[f] == w) {
+          valid = fvalid[f];
+#pragma unroll
+          for (int j = 0; j < KPL; ++j) dw[j] = fdw[f][j];
+        }
       }
     }
     // an own-change row from an older clock reads as zero (an and with a uniform mask keeps
